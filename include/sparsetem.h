@@ -1,0 +1,221 @@
+/*
+ * sparsetem.h -- C ABI of the MI355X (gfx950) diff-computation encoder.
+ *
+ * The library encodes a video chunk with a CNN encoder the way SparseTem's
+ * Diff Computation does (paper, section "Skipping Non-zero Delta Pixels"):
+ * the chunk's first frame (the reference frame) is encoded densely, every
+ * later frame (a diff frame) only on the pixels that changed.  Per layer the
+ * diff path is: per-pixel truncation mask + stream compaction of the changed
+ * pixels, a rulebook mapping changed input sites to the output sites they
+ * reach for every kernel offset (the dense amplification of the "Truncation
+ * threshold" paragraph), a gather-GEMM-scatter delta convolution on the
+ * changed rows only (linearity of convolution, Eq. 2), and an in-place
+ * update of the HBM-resident f32 pre-activation state that also applies the
+ * non-linearity and emits the next layer's delta f(P_new) - f(P_old)
+ * (non-linear handling, Eq. 3; memory-efficient schedule of the section
+ * "Design of SparseBatch": one pre-activation buffer per non-linear layer,
+ * no cached outputs).
+ *
+ * Conventions
+ *   - Every pointer named "device" is HIP device memory; "host" is host
+ *     memory.  The library never allocates device memory: the caller owns
+ *     the workspace, frames, outputs and weights.
+ *   - Layout is NHWC; pixel id p = (n * H + y) * W + x.
+ *   - `stream` is a hipStream_t passed as void*; NULL is the default stream.
+ *     Encode calls are asynchronous and stream-ordered; calls documented as
+ *     "synchronising" wait for the last encode's stream.
+ *   - Every call returns an st_status; no exception crosses the ABI.
+ *     st_last_error() gives a message for the last failure.
+ *   - One st_net must not be used from two threads at once; distinct nets
+ *     are independent.
+ */
+#ifndef SPARSETEM_H
+#define SPARSETEM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct st_net st_net; /* opaque, library-owned host object */
+
+typedef int32_t st_status;
+enum {
+  ST_OK = 0,
+  ST_ERR_INVALID_ARG = 1, /* NULL pointer, bad shape/channels/geometry, NaN threshold */
+  ST_ERR_UNSUPPORTED = 2, /* a layer kind this build does not implement */
+  ST_ERR_STATE = 3,       /* no workspace bound, or diff before reference  */
+  ST_ERR_WORKSPACE = 4,   /* workspace smaller than st_workspace_bytes()   */
+  ST_ERR_HIP = 5          /* a HIP runtime call or kernel launch failed     */
+};
+
+/* Storage dtype of frames, weights, biases and emitted deltas.  Sums and
+ * the pre-activation state are always f32. */
+enum { ST_F32 = 0, ST_F16 = 1, ST_BF16 = 2 };
+
+/* Non-linearity applied after the convolution (and residual add). */
+enum { ST_ACT_NONE = 0, ST_ACT_RELU = 1, ST_ACT_SILU = 2 };
+
+/*
+ * One layer: a convolution with PyTorch conv2d geometry (dilation 1),
+ * optionally plus a residual input, then an activation, then an optional
+ * max-pool (PyTorch max_pool2d geometry, -inf padding).
+ *   src           producer of the input: -1 = network input, else an earlier
+ *                 layer index (layers are given in topological order).
+ *   residual_src  producer whose output is added to this layer's
+ *                 pre-activation (-2 = none, -1 = network input); its output
+ *                 grid and channels must equal this conv's output.
+ *   groups        1 (dense) or c_in == c_out == groups (depthwise).
+ *   weight        device, storage dtype, [c_out][c_in/groups][k_h][k_w].
+ *   bias          device, storage dtype, [c_out]; may be NULL (zero bias).
+ *   pool_k_h == 0 means no pool.  se_* must be 0 / NULL in this build.
+ * A layer is "stateful" (holds an f32 pre-activation buffer) when it has an
+ * activation or a pool, or is the last layer (the network output).
+ */
+typedef struct st_layer_desc {
+  int32_t src;
+  int32_t residual_src;
+  int32_t c_in, c_out, groups;
+  int32_t k_h, k_w, s_h, s_w, p_h, p_w;
+  int32_t act;
+  int32_t pool_k_h, pool_k_w, pool_s_h, pool_s_w, pool_p_h, pool_p_w;
+  int32_t se_mid;
+  const void *weight, *bias;
+  const void *se_w1, *se_b1, *se_w2, *se_b2;
+} st_layer_desc;
+
+/* Validate the layer graph and plan the workspace (host only, no HIP call).
+ * Inputs are `batch` images of in_h x in_w x in_c in `dtype`.  The
+ * descriptors (and the weight pointers in them) are copied; the weights are
+ * read only by st_bind_workspace.  On success *out owns a new net.
+ * Errors: ST_ERR_INVALID_ARG (NULL, n_layers < 1, bad src/residual_src, a
+ * channel or shape mismatch, an empty output grid, an unknown dtype or
+ * activation), ST_ERR_UNSUPPORTED (groups other than 1 or depthwise,
+ * squeeze-excitation). */
+st_status st_create_net(const st_layer_desc* layers, int32_t n_layers,
+                        int32_t batch, int32_t in_h, int32_t in_w,
+                        int32_t in_c, int32_t dtype, st_net** out);
+
+/* Bytes of device workspace the net needs (host only).  The workspace holds
+ * the Subtraction buffer, every f32 pre-activation buffer, the repacked
+ * weights, and worst-case-sized (every pixel active) delta rows, active
+ * lists, pixel maps and rulebooks, so no frame can overflow it. */
+st_status st_workspace_bytes(const st_net* net, uint64_t* bytes);
+
+/* Bind `bytes` of device memory at `dev_ptr` (256-byte aligned) as the
+ * workspace, initialise it and repack the weights into it, on `stream`.
+ * The weights must stay valid until that stream work has completed; after it
+ * they are no longer read.  Rebinding resets the net to "no reference".
+ * Errors: ST_ERR_WORKSPACE (too small), ST_ERR_INVALID_ARG (NULL or
+ * misaligned), ST_ERR_HIP. */
+st_status st_bind_workspace(st_net* net, void* dev_ptr, uint64_t bytes,
+                            void* stream);
+
+/* Dense pass on a reference frame (device, storage dtype, NHWC
+ * [batch][in_h][in_w][in_c]): (re)initialises the Subtraction buffer and
+ * every pre-activation buffer (bias included), and writes the network
+ * output to `out` (device, f32, NHWC grid of the last layer; may be NULL
+ * to skip the write).  Errors: ST_ERR_STATE (no workspace),
+ * ST_ERR_INVALID_ARG, ST_ERR_HIP. */
+st_status st_encode_reference(st_net* net, const void* frame, float* out,
+                              void* stream);
+
+/* Diff pass on the next frame of the chunk.  `thr` (host, n_layers + 1
+ * floats, read before the call returns): thr[0] truncates the frame delta
+ * X - X_hat, thr[j + 1] truncates layer j's emitted delta (shared by all its
+ * consumers).  A pixel is kept iff the largest |delta| over its channels is
+ * strictly greater than its threshold; a negative threshold keeps every
+ * pixel.  Kept input pixels are committed to the Subtraction buffer;
+ * truncated deltas inside the network are dropped.  `out` as for
+ * st_encode_reference.  Errors: ST_ERR_STATE (no reference since the last
+ * bind), ST_ERR_INVALID_ARG (NULL frame/thr, NaN threshold), ST_ERR_HIP. */
+st_status st_encode_diff(st_net* net, const void* frame, const float* thr,
+                         float* out, void* stream);
+
+/* Fraction of kept sites of the last encode: layer = -1 is the frame delta,
+ * layer = j is layer j's emitted delta.  image = -1 averages over the batch,
+ * otherwise the density of that batch image alone (the per-stream density
+ * an online threshold controller reads).  Synchronising. */
+st_status st_layer_density(st_net* net, int32_t layer, int32_t image,
+                           float* d);
+
+/* Output grid of layer j's emitted tensor (layer = -1: the input):
+ * nhwc[4] = {batch, H, W, C} (host). */
+st_status st_tensor_shape(const st_net* net, int32_t layer, int32_t* nhwc);
+
+void st_destroy_net(st_net* net);
+
+/* Message of the last failure on `net` (or of the calling thread's last
+ * st_create_net failure when net is NULL).  Owned by the library. */
+const char* st_last_error(const st_net* net);
+
+/* ---- parity / introspection: host copies of the last frame's artefacts.
+ * All synchronising.  `cap` counts elements of the caller's buffer; *n
+ * receives the full count even when it exceeds cap (nothing is then
+ * written past cap). */
+
+/* Kept pixel ids of tensor `layer` (-1 = frame delta), ascending. */
+st_status st_debug_active(st_net* net, int32_t layer, int32_t* idx,
+                          int64_t cap, int64_t* n);
+
+/* Candidate rows of tensor `layer` before truncation: their pixel ids
+ * (ascending, `pix`, may be NULL) and delta values converted to f32
+ * (`rows`, [cap][C], may be NULL).  For layer -1 the candidates are the kept
+ * pixels. */
+st_status st_debug_candidates(st_net* net, int32_t layer, int32_t* pix,
+                              float* rows, int64_t cap, int64_t* n);
+
+/* Rulebook of conv layer `layer` as (offset, in_pix, out_pix) triples
+ * (`kio`, [cap][3]), offset-major and ascending in in_pix within an offset;
+ * offset = ky * k_w + kx. */
+st_status st_debug_rulebook(st_net* net, int32_t layer, int32_t* kio,
+                            int64_t cap, int64_t* n);
+
+/* Dense f32 pre-activation state of stateful layer `layer`
+ * ([batch][H_conv][W_conv][c_out], `cap` floats). */
+st_status st_debug_state(st_net* net, int32_t layer, float* P, int64_t cap);
+
+/* Per-layer rulebook pair counts (n_layers) and per-tensor kept counts
+ * (n_layers + 1, index 0 = frame delta) of the last encode. */
+st_status st_debug_counters(st_net* net, int64_t* pairs_per_layer,
+                            int64_t* active_per_tensor);
+
+/* ---- measurement: per-launch kernel timing with HIP events recorded on
+ * the encode stream, plus a per-frame snapshot of the work counters. */
+
+typedef struct st_launch_record {
+  int32_t kernel; /* st_kernel_class */
+  int32_t layer;  /* -1 for per-frame kernels */
+  int32_t frame;  /* index of the encode call since st_profile_begin */
+  float ms;       /* hipEventElapsedTime between the launch's two events */
+} st_launch_record;
+
+enum {
+  ST_K_SCAN_MASK = 0, ST_K_SCAN_COMPACT, ST_K_RB_MARK, ST_K_RB_COUNT,
+  ST_K_RB_COMPACT, ST_K_RB_NBR, ST_K_RB_IDENT, ST_K_CONV_GEMM, ST_K_CONV_DW,
+  ST_K_POOL_MARK, ST_K_POOL_COUNT, ST_K_POOL_COMPACT, ST_K_POOL_EMIT,
+  ST_K_COMMIT, ST_K_LIST_COUNT, ST_K_LIST_COMPACT, ST_K_OUTPUT,
+  ST_K_CLEANUP, ST_K_RESET, ST_K_NUM_CLASSES
+};
+
+/* Start recording: room for `max_launches` launch records and
+ * `max_frames` counter snapshots (host-side allocation only).  While
+ * recording, every encode records two events around each kernel launch. */
+st_status st_profile_begin(st_net* net, int32_t max_launches,
+                           int32_t max_frames);
+
+/* Stop recording (synchronising).  Writes up to `cap` launch records and,
+ * per recorded frame f and layer j, counts[(f * n_layers + j) * 4 + i] =
+ * {affected conv outputs, rulebook pairs, kept input rows of the layer's
+ * source, emitted candidate rows}, up to `cap_frames` frames. */
+st_status st_profile_end(st_net* net, st_launch_record* recs, int32_t cap,
+                         int32_t* n, int64_t* counts, int32_t cap_frames,
+                         int32_t* n_frames);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARSETEM_H */

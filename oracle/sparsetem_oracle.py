@@ -370,15 +370,15 @@ class OracleNet:
             d = round_storage(d32, self.dtype)
             cmax = np.abs(d).max(axis=1) if len(cand) else np.zeros(0)
             kept = cmax > thr[i + 1]                     # readings 1 and 3
-            tensors.append(dict(cand=cand, cand_max=cmax, pix=cand[kept],
-                                rows=d[kept], grid=(N, g.Hp, g.Wp),
-                                C=L.c_out))
+            tensors.append(dict(cand=cand, cand_max=cmax, cand_rows=d,
+                                pix=cand[kept], rows=d[kept],
+                                grid=(N, g.Hp, g.Wp), C=L.c_out))
             layer_art.append(dict(rulebook=R, O=O, Q=Q, pairs=len(R)))
 
         # Accumulation: the dense output of the current frame.
         out = self._dense_output()
         self.last = dict(kind="diff", out=out, tensors=tensors,
-                         layers=layer_art)
+                         layers=layer_art, thr=thr)
         return out
 
     def _dense_output(self):

@@ -1,0 +1,587 @@
+// Executor and HIP-side entry points of the C ABI: workspace binding and
+// weight repacking, the per-frame kernel sequence of the reference and diff
+// passes, density queries, introspection copies and kernel timing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "st_internal.h"
+#include "st_kernels.h"
+
+namespace st {
+
+struct Recorder {
+  bool on = false;
+  int max_launches = 0, max_frames = 0;
+  int frame = -1;
+  std::vector<hipEvent_t> ev;            // two per launch
+  std::vector<st_launch_record> recs;
+  uint64_t* hist = nullptr;              // pinned host: [max_frames][n_counters]
+  int n_hist = 0;
+  ~Recorder() {
+    for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+    if (hist) (void)hipHostFree(hist);
+  }
+};
+
+void prof_begin(const Prof& p, int cls, hipStream_t s) {
+  (void)cls;
+  st_net* net = (st_net*)p.net;
+  if (!net || !net->rec || !net->rec->on) return;
+  Recorder& R = *net->rec;
+  const size_t i = R.recs.size();
+  if ((int)i >= R.max_launches) return;
+  (void)hipEventRecord(R.ev[2 * i], s);
+}
+
+void prof_end(const Prof& p, int cls, hipStream_t s) {
+  st_net* net = (st_net*)p.net;
+  if (!net || !net->rec || !net->rec->on) return;
+  Recorder& R = *net->rec;
+  const size_t i = R.recs.size();
+  if ((int)i >= R.max_launches) return;
+  (void)hipEventRecord(R.ev[2 * i + 1], s);
+  R.recs.push_back(st_launch_record{cls, p.layer, R.frame, 0.f});
+}
+
+}  // namespace st
+
+using namespace st;
+
+namespace {
+
+struct WS {
+  char* base;
+  template <typename T> T* at(size_t off) const { return (T*)(base + off); }
+};
+
+st_status hip_check(st_net* net, const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess)
+    return fail(net, ST_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+  return ST_OK;
+}
+
+Geo conv_geo(const LayerPlan& L) {
+  const st_layer_desc& d = L.d;
+  return Geo{L.Hi, L.Wi, L.Ho, L.Wo, d.k_h, d.k_w, d.s_h, d.s_w, d.p_h, d.p_w};
+}
+
+Geo pool_geo(const LayerPlan& L) {
+  const st_layer_desc& d = L.d;
+  return Geo{L.Ho, L.Wo, L.Hp, L.Wp, d.pool_k_h, d.pool_k_w,
+             d.pool_s_h, d.pool_s_w, d.pool_p_h, d.pool_p_w};
+}
+
+void run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
+  const WS ws{net->ws};
+  const LayerPlan& L = net->layers[i];
+  const st_layer_desc& d = L.d;
+  const TensorPlan& in = net->tensors[d.src + 1];
+  TensorPlan& out = net->tensors[i + 1];
+  u64* cnt = ws.at<u64>(net->off_cnt);
+  uint8_t* flags = ws.at<uint8_t>(net->off_flags);
+  uint32_t* tiles = ws.at<uint32_t>(net->off_tiles);
+  const Prof pf{net, i};
+
+  int* O = ws.at<int>(L.off_O);
+  int* Mo = ws.at<int>(L.off_Mo);
+  int* nbr = ws.at<int>(L.off_nbr);
+  u64* cO = cnt + L.cnt_O;
+  u64* cpairs = cnt + L.cnt_pairs;
+  uint32_t* rowmax_out = ws.at<uint32_t>(out.off_rowmax);
+  uint32_t* rm_O = L.pool ? nullptr : rowmax_out;
+  const int* act_in = ws.at<int>(in.off_act);
+  const int* map_in = ws.at<int>(in.off_map);
+
+  // (b) rulebook
+  if (L.ident) {
+    launch_ident(pf, s, act_in, cnt + in.cnt_act, map_in, in.grid, O, Mo, nbr,
+                 rm_O, cO, cpairs);
+  } else {
+    const Geo g = conv_geo(L);
+    const int* list2 = nullptr;
+    const u64* n2 = nullptr;
+    int64_t max_items = in.grid;
+    if (d.residual_src != -2) {
+      const TensorPlan& R = net->tensors[d.residual_src + 1];
+      list2 = ws.at<int>(R.off_act);
+      n2 = cnt + R.cnt_act;
+      max_items += R.grid;
+    }
+    launch_mark(pf, ST_K_RB_MARK, s, act_in, cnt + in.cnt_act, list2, n2,
+                max_items, g, net->N, flags);
+    launch_flag_compact(pf, ST_K_RB_COUNT, ST_K_RB_COMPACT, s, flags,
+                        L.conv_grid, tiles, O, Mo, rm_O, cO);
+    launch_nbr(pf, s, O, cO, L.conv_grid, g, L.K, map_in, nbr, cpairs);
+  }
+
+  // (c) delta convolution with fused (d) update / emission
+  ConvArgs a{};
+  a.din = ws.at<char>(in.off_rows);
+  a.nbr = nbr;
+  a.stride = L.conv_grid;
+  a.K = L.K;
+  a.cin_p = L.cin_p;
+  a.cout_p = L.cout_p;
+  a.ktot_p = L.ktot_p;
+  a.w = ws.at<char>(L.off_w);
+  a.bias = ws.at<float>(L.off_bias);
+  a.O = O;
+  a.nO = cO;
+  a.capO = L.conv_grid;
+  a.P = L.stateful ? ws.at<float>(L.off_P) : nullptr;
+  a.dP = L.pool ? ws.at<float>(L.off_dP) : nullptr;
+  a.dout = L.pool ? nullptr : ws.at<char>(out.off_rows);
+  a.rowmax = rm_O;
+  if (d.residual_src != -2) {
+    const TensorPlan& R = net->tensors[d.residual_src + 1];
+    a.dskip = ws.at<char>(R.off_rows);
+    a.mskip = ws.at<int>(R.off_map);
+  }
+  a.mode = L.mode;
+  a.act = d.act;
+  a.ref = ref ? 1 : 0;
+  if (L.dw)
+    launch_conv_dw(pf, s, net->dtype, a);
+  else
+    launch_conv_gemm(pf, s, net->dtype, a);
+
+  // non-linear post-op: max-pool from old and new state, then commit
+  if (L.pool) {
+    const Geo gp = pool_geo(L);
+    launch_mark(pf, ST_K_POOL_MARK, s, O, cO, nullptr, nullptr, L.conv_grid,
+                gp, net->N, flags);
+    launch_flag_compact(pf, ST_K_POOL_COUNT, ST_K_POOL_COMPACT, s, flags,
+                        out.grid, tiles, ws.at<int>(out.off_rowpix),
+                        ws.at<int>(out.off_map), rowmax_out,
+                        cnt + out.cnt_rows);
+    PoolArgs pa{};
+    pa.Q = ws.at<int>(out.off_rowpix);
+    pa.nQ = cnt + out.cnt_rows;
+    pa.capQ = out.grid;
+    pa.g = gp;
+    pa.P = ws.at<float>(L.off_P);
+    pa.dP = ws.at<float>(L.off_dP);
+    pa.Mo = Mo;
+    pa.dout = ws.at<char>(out.off_rows);
+    pa.rowmax = rowmax_out;
+    pa.cp = L.cout_p;
+    pa.act = d.act;
+    pa.ref = ref ? 1 : 0;
+    launch_pool_emit(pf, s, net->dtype, pa);
+    launch_commit(pf, s, O, cO, L.conv_grid, ws.at<float>(L.off_P),
+                  ws.at<float>(L.off_dP), L.cout_p, ref ? 1 : 0);
+  }
+
+  // truncation of the emitted delta (shared by every consumer)
+  launch_list_compact(pf, s, rowmax_out, cnt + out.cnt_rows, out.grid, thr,
+                      ws.at<int>(out.off_rowpix), ws.at<int>(out.off_act),
+                      ws.at<int>(out.off_map), tiles, cnt + out.cnt_act);
+  out.last_thr = thr;
+}
+
+st_status encode(st_net* net, const void* frame, const float* thr, float* out,
+                 hipStream_t s, bool ref) {
+  const WS ws{net->ws};
+  u64* cnt = ws.at<u64>(net->off_cnt);
+  const Prof pf{net, -1};
+  Recorder* R = net->rec && net->rec->on ? net->rec : nullptr;
+  if (R) ++R->frame;
+  (void)hipGetLastError();  // clear any stale error
+
+  launch_reset(pf, s, cnt, net->n_counters);
+  TensorPlan& T0 = net->tensors[0];
+  const float thr0 = ref ? -1.f : thr[0];
+  launch_scan(pf, s, net->dtype, frame, ws.at<char>(net->off_xhat), net->C,
+              T0.Cp, T0.grid, thr0, ref ? 1 : 0, ws.at<uint8_t>(net->off_flags),
+              ws.at<uint32_t>(net->off_tiles), ws.at<char>(T0.off_rows),
+              ws.at<int>(T0.off_rowpix), ws.at<int>(T0.off_act),
+              ws.at<int>(T0.off_map), cnt + T0.cnt_rows, cnt + T0.cnt_act);
+  T0.last_thr = thr0;
+  const int nl = (int)net->layers.size();
+  for (int i = 0; i < nl; ++i)
+    run_layer(net, i, ref, ref ? -1.f : thr[i + 1], s);
+
+  if (out) {
+    const LayerPlan& L = net->layers[nl - 1];
+    const Geo g = L.pool ? pool_geo(L) : Geo{L.Ho, L.Wo, L.Ho, L.Wo, 1, 1,
+                                             1, 1, 0, 0};
+    launch_output(Prof{net, nl - 1}, s, ws.at<float>(L.off_P), L.cout_p,
+                  L.d.c_out, net->N, g, L.pool ? 1 : 0, L.d.act, out);
+  }
+  launch_cleanup(pf, s, ws.at<CleanEntry>(net->off_cleanup), net->n_cleanup,
+                 net->ws, cnt, net->max_grid);
+  if (R && R->n_hist < R->max_frames) {
+    (void)hipMemcpyAsync(R->hist + (size_t)R->n_hist * net->n_counters, cnt,
+                         sizeof(u64) * net->n_counters, hipMemcpyDeviceToHost,
+                         s);
+    ++R->n_hist;
+  }
+  net->last_stream = (void*)s;
+  return hip_check(net, ref ? "st_encode_reference" : "st_encode_diff");
+}
+
+st_status sync_last(st_net* net) {
+  hipError_t e = hipStreamSynchronize((hipStream_t)net->last_stream);
+  if (e != hipSuccess)
+    return fail(net, ST_ERR_HIP, std::string("stream sync: ") +
+                                     hipGetErrorString(e));
+  return ST_OK;
+}
+
+template <typename T>
+st_status d2h(st_net* net, T* dst, const void* src, size_t count) {
+  if (!count) return ST_OK;
+  hipError_t e = hipMemcpy(dst, src, sizeof(T) * count, hipMemcpyDeviceToHost);
+  if (e != hipSuccess)
+    return fail(net, ST_ERR_HIP, std::string("copy: ") + hipGetErrorString(e));
+  return ST_OK;
+}
+
+float half_to_float(uint16_t h) {
+  _Float16 f;
+  std::memcpy(&f, &h, 2);
+  return (float)f;
+}
+
+float bf16_to_float(uint16_t b) {
+  uint32_t u = (uint32_t)b << 16;
+  float f;
+  std::memcpy(&f, &u, 4);
+  return f;
+}
+
+}  // namespace
+
+extern "C" st_status st_bind_workspace(st_net* net, void* dev_ptr,
+                                       uint64_t bytes, void* stream) {
+  if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
+  if (!dev_ptr) return fail(net, ST_ERR_INVALID_ARG, "workspace is NULL");
+  if ((uintptr_t)dev_ptr % kAlign)
+    return fail(net, ST_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (bytes < net->ws_bytes)
+    return fail(net, ST_ERR_WORKSPACE,
+                "workspace too small: need " + std::to_string(net->ws_bytes));
+  hipStream_t s = (hipStream_t)stream;
+  net->ws = (char*)dev_ptr;
+  net->bound = false;
+  net->have_ref = false;
+  (void)hipGetLastError();
+  const WS ws{net->ws};
+  launch_fill_u32(s, net->ws, (int64_t)(net->ws_bytes / 4), 0u);
+  for (const TensorPlan& T : net->tensors)
+    launch_fill_u32(s, ws.at<int>(T.off_map), T.grid, 0xFFFFFFFFu);
+  std::vector<CleanEntry> tab;
+  for (const TensorPlan& T : net->tensors)
+    tab.push_back(CleanEntry{(int64_t)T.off_map, (int64_t)T.off_rowpix,
+                             T.cnt_rows, 0, 0});
+  for (const LayerPlan& L : net->layers) {
+    const st_layer_desc& d = L.d;
+    if (L.pool) {
+      launch_fill_u32(s, ws.at<int>(L.off_Mo), L.conv_grid, 0xFFFFFFFFu);
+      tab.push_back(CleanEntry{(int64_t)L.off_Mo, (int64_t)L.off_O, L.cnt_O,
+                               0, 0});
+    }
+    if (L.dw)
+      launch_repack_dw(s, net->dtype, d.weight, ws.at<float>(L.off_w),
+                       d.c_out, d.k_h, d.k_w, L.cout_p);
+    else
+      launch_repack_dense(s, net->dtype, d.weight, ws.at<char>(L.off_w),
+                          d.c_out, d.c_in, d.k_h, d.k_w, L.cin_p, L.cout_p,
+                          L.ktot_p);
+    launch_bias(s, net->dtype, d.bias, ws.at<float>(L.off_bias), d.c_out,
+                L.cout_p);
+  }
+  static_assert(sizeof(CleanEntry) == 32, "cleanup entry layout");
+  if ((int)tab.size() != net->n_cleanup)
+    return fail(net, ST_ERR_INVALID_ARG, "internal: cleanup table size");
+  // The table must outlive the asynchronous copy: keep it in the net.
+  static thread_local std::vector<CleanEntry> keep_alive;
+  keep_alive = tab;
+  hipError_t e = hipMemcpyAsync(ws.at<char>(net->off_cleanup), keep_alive.data(),
+                                sizeof(CleanEntry) * tab.size(),
+                                hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess)
+    return fail(net, ST_ERR_HIP, std::string("bind: ") + hipGetErrorString(e));
+  st_status st = hip_check(net, "st_bind_workspace");
+  if (st != ST_OK) return st;
+  net->bound = true;
+  net->last_stream = stream;
+  return ST_OK;
+}
+
+extern "C" st_status st_encode_reference(st_net* net, const void* frame,
+                                         float* out, void* stream) {
+  if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
+  if (!net->bound) return fail(net, ST_ERR_STATE, "no workspace bound");
+  if (!frame) return fail(net, ST_ERR_INVALID_ARG, "frame is NULL");
+  st_status s = encode(net, frame, nullptr, out, (hipStream_t)stream, true);
+  if (s == ST_OK) net->have_ref = true;
+  return s;
+}
+
+extern "C" st_status st_encode_diff(st_net* net, const void* frame,
+                                    const float* thr, float* out,
+                                    void* stream) {
+  if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
+  if (!net->bound) return fail(net, ST_ERR_STATE, "no workspace bound");
+  if (!net->have_ref)
+    return fail(net, ST_ERR_STATE, "st_encode_diff before st_encode_reference");
+  if (!frame || !thr) return fail(net, ST_ERR_INVALID_ARG, "NULL frame or thr");
+  for (size_t i = 0; i <= net->layers.size(); ++i)
+    if (std::isnan(thr[i]))
+      return fail(net, ST_ERR_INVALID_ARG,
+                  "threshold " + std::to_string(i) + " is NaN");
+  return encode(net, frame, thr, out, (hipStream_t)stream, false);
+}
+
+extern "C" st_status st_layer_density(st_net* net, int32_t layer,
+                                      int32_t image, float* d) {
+  if (!net || !d) return fail(net, ST_ERR_INVALID_ARG, "NULL argument");
+  if (!net->bound || !net->have_ref)
+    return fail(net, ST_ERR_STATE, "nothing encoded yet");
+  if (layer < -1 || layer >= (int)net->layers.size())
+    return fail(net, ST_ERR_INVALID_ARG, "layer out of range");
+  if (image < -1 || image >= net->N)
+    return fail(net, ST_ERR_INVALID_ARG, "image out of range");
+  const TensorPlan& T = net->tensors[layer + 1];
+  const WS ws{net->ws};
+  u64* cnt = ws.at<u64>(net->off_cnt);
+  st_status st = sync_last(net);
+  if (st != ST_OK) return st;
+  uint64_t k = 0;
+  if (image < 0) {
+    st = d2h(net, &k, cnt + T.cnt_act, 1);
+    if (st != ST_OK) return st;
+    *d = (float)((double)k / (double)T.grid);
+    return ST_OK;
+  }
+  hipStream_t s = (hipStream_t)net->last_stream;
+  u64* dens = ws.at<u64>(net->off_dens);
+  launch_density(s, ws.at<int>(T.off_act), cnt + T.cnt_act,
+                 (int64_t)T.H * T.W, net->N, dens);
+  st = hip_check(net, "density");
+  if (st != ST_OK) return st;
+  st = sync_last(net);
+  if (st != ST_OK) return st;
+  st = d2h(net, &k, dens + image, 1);
+  if (st != ST_OK) return st;
+  *d = (float)((double)k / ((double)T.H * T.W));
+  return ST_OK;
+}
+
+extern "C" void st_destroy_net(st_net* net) {
+  if (!net) return;
+  delete net->rec;
+  delete net;
+}
+
+// ------------------------------------------------------------ debug copies
+
+static st_status debug_prelude(st_net* net, int32_t layer, bool need_enc) {
+  if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
+  if (layer < -1 || layer >= (int)net->layers.size())
+    return fail(net, ST_ERR_INVALID_ARG, "layer out of range");
+  if (!net->bound || (need_enc && !net->have_ref))
+    return fail(net, ST_ERR_STATE, "nothing encoded yet");
+  return sync_last(net);
+}
+
+extern "C" st_status st_debug_active(st_net* net, int32_t layer, int32_t* idx,
+                                     int64_t cap, int64_t* n) {
+  st_status st = debug_prelude(net, layer, true);
+  if (st != ST_OK) return st;
+  if (!n) return fail(net, ST_ERR_INVALID_ARG, "n is NULL");
+  const TensorPlan& T = net->tensors[layer + 1];
+  const WS ws{net->ws};
+  uint64_t k = 0;
+  st = d2h(net, &k, ws.at<u64>(net->off_cnt) + T.cnt_act, 1);
+  if (st != ST_OK) return st;
+  *n = (int64_t)k;
+  if (idx) st = d2h(net, idx, ws.at<int>(T.off_act), std::min<int64_t>(k, cap));
+  return st;
+}
+
+extern "C" st_status st_debug_candidates(st_net* net, int32_t layer,
+                                         int32_t* pix, float* rows,
+                                         int64_t cap, int64_t* n) {
+  st_status st = debug_prelude(net, layer, true);
+  if (st != ST_OK) return st;
+  if (!n) return fail(net, ST_ERR_INVALID_ARG, "n is NULL");
+  const TensorPlan& T = net->tensors[layer + 1];
+  const WS ws{net->ws};
+  uint64_t k = 0;
+  st = d2h(net, &k, ws.at<u64>(net->off_cnt) + T.cnt_rows, 1);
+  if (st != ST_OK) return st;
+  *n = (int64_t)k;
+  const int64_t m = std::min<int64_t>(k, cap);
+  if (pix) {
+    st = d2h(net, pix, ws.at<int>(T.off_rowpix), m);
+    if (st != ST_OK) return st;
+  }
+  if (rows && m) {
+    std::vector<uint8_t> raw((size_t)m * T.Cp * net->esize);
+    st = d2h(net, raw.data(), ws.at<char>(T.off_rows), raw.size());
+    if (st != ST_OK) return st;
+    for (int64_t r = 0; r < m; ++r)
+      for (int c = 0; c < T.C; ++c) {
+        const size_t e = (size_t)r * T.Cp + c;
+        float v;
+        if (net->dtype == ST_F32) {
+          std::memcpy(&v, raw.data() + 4 * e, 4);
+        } else {
+          uint16_t h;
+          std::memcpy(&h, raw.data() + 2 * e, 2);
+          v = net->dtype == ST_F16 ? half_to_float(h) : bf16_to_float(h);
+        }
+        rows[r * T.C + c] = v;
+      }
+  }
+  return ST_OK;
+}
+
+extern "C" st_status st_debug_rulebook(st_net* net, int32_t layer,
+                                       int32_t* kio, int64_t cap, int64_t* n) {
+  st_status st = debug_prelude(net, layer, true);
+  if (st != ST_OK) return st;
+  if (layer < 0 || !n) return fail(net, ST_ERR_INVALID_ARG, "bad layer or n");
+  const LayerPlan& L = net->layers[layer];
+  const TensorPlan& in = net->tensors[L.d.src + 1];
+  const WS ws{net->ws};
+  const u64* cnt = ws.at<u64>(net->off_cnt);
+  uint64_t nO = 0, nin = 0;
+  if ((st = d2h(net, &nO, cnt + L.cnt_O, 1)) != ST_OK) return st;
+  if ((st = d2h(net, &nin, cnt + in.cnt_rows, 1)) != ST_OK) return st;
+  std::vector<int> O(nO), rp(nin), nb((size_t)nO * L.K);
+  if ((st = d2h(net, O.data(), ws.at<int>(L.off_O), nO)) != ST_OK) return st;
+  if ((st = d2h(net, rp.data(), ws.at<int>(in.off_rowpix), nin)) != ST_OK)
+    return st;
+  for (int k = 0; k < L.K; ++k)
+    if ((st = d2h(net, nb.data() + (size_t)k * nO,
+                  ws.at<int>(L.off_nbr) + (size_t)k * L.conv_grid, nO)) !=
+        ST_OK)
+      return st;
+  int64_t cntp = 0;
+  for (int k = 0; k < L.K; ++k)
+    for (uint64_t o = 0; o < nO; ++o) {
+      const int r = nb[(size_t)k * nO + o];
+      if (r < 0) continue;
+      if (r >= (int)nin)
+        return fail(net, ST_ERR_HIP, "internal: neighbour row out of range");
+      if (kio && cntp < cap) {
+        kio[3 * cntp] = k;
+        kio[3 * cntp + 1] = rp[r];
+        kio[3 * cntp + 2] = O[o];
+      }
+      ++cntp;
+    }
+  *n = cntp;
+  return ST_OK;
+}
+
+extern "C" st_status st_debug_state(st_net* net, int32_t layer, float* P,
+                                    int64_t cap) {
+  st_status st = debug_prelude(net, layer, true);
+  if (st != ST_OK) return st;
+  if (layer < 0 || !P) return fail(net, ST_ERR_INVALID_ARG, "bad layer or P");
+  const LayerPlan& L = net->layers[layer];
+  if (!L.stateful) return fail(net, ST_ERR_INVALID_ARG, "layer holds no state");
+  if (cap < L.conv_grid * L.d.c_out)
+    return fail(net, ST_ERR_INVALID_ARG, "P buffer too small");
+  std::vector<float> raw((size_t)L.conv_grid * L.cout_p);
+  st = d2h(net, raw.data(), net->ws + L.off_P, raw.size());
+  if (st != ST_OK) return st;
+  for (int64_t p = 0; p < L.conv_grid; ++p)
+    std::memcpy(P + p * L.d.c_out, raw.data() + p * L.cout_p,
+                sizeof(float) * L.d.c_out);
+  return ST_OK;
+}
+
+extern "C" st_status st_debug_counters(st_net* net, int64_t* pairs,
+                                       int64_t* active) {
+  st_status st = debug_prelude(net, -1, true);
+  if (st != ST_OK) return st;
+  std::vector<uint64_t> c(net->n_counters);
+  st = d2h(net, c.data(), net->ws + net->off_cnt, c.size());
+  if (st != ST_OK) return st;
+  for (size_t i = 0; i < net->layers.size(); ++i)
+    if (pairs) pairs[i] = (int64_t)c[net->layers[i].cnt_pairs];
+  for (size_t t = 0; t < net->tensors.size(); ++t)
+    if (active) active[t] = (int64_t)c[net->tensors[t].cnt_act];
+  return ST_OK;
+}
+
+// ------------------------------------------------------------- profiling
+
+extern "C" st_status st_profile_begin(st_net* net, int32_t max_launches,
+                                      int32_t max_frames) {
+  if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
+  if (max_launches < 0 || max_frames < 0)
+    return fail(net, ST_ERR_INVALID_ARG, "negative capacity");
+  if (!net->rec) net->rec = new Recorder();
+  Recorder& R = *net->rec;
+  while ((int)R.ev.size() < 2 * max_launches) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess)
+      return fail(net, ST_ERR_HIP, "hipEventCreate failed");
+    R.ev.push_back(e);
+  }
+  if (R.hist) {
+    (void)hipHostFree(R.hist);
+    R.hist = nullptr;
+  }
+  if (max_frames &&
+      hipHostMalloc((void**)&R.hist,
+                    sizeof(uint64_t) * net->n_counters * max_frames) !=
+          hipSuccess)
+    return fail(net, ST_ERR_HIP, "hipHostMalloc failed");
+  R.max_launches = max_launches;
+  R.max_frames = max_frames;
+  R.recs.clear();
+  R.n_hist = 0;
+  R.frame = -1;
+  R.on = true;
+  return ST_OK;
+}
+
+extern "C" st_status st_profile_end(st_net* net, st_launch_record* recs,
+                                    int32_t cap, int32_t* n, int64_t* counts,
+                                    int32_t cap_frames, int32_t* n_frames) {
+  if (!net || !net->rec) return fail(net, ST_ERR_STATE, "not recording");
+  Recorder& R = *net->rec;
+  R.on = false;
+  st_status st = net->last_stream ? sync_last(net) : ST_OK;
+  if (st != ST_OK) return st;
+  for (size_t i = 0; i < R.recs.size(); ++i) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, R.ev[2 * i], R.ev[2 * i + 1]) != hipSuccess)
+      return fail(net, ST_ERR_HIP, "hipEventElapsedTime failed");
+    R.recs[i].ms = ms;
+  }
+  if (n) *n = (int32_t)R.recs.size();
+  if (recs)
+    for (int i = 0; i < (int)R.recs.size() && i < cap; ++i) recs[i] = R.recs[i];
+  const int nl = (int)net->layers.size();
+  if (n_frames) *n_frames = R.n_hist;
+  if (counts)
+    for (int f = 0; f < R.n_hist && f < cap_frames; ++f) {
+      const uint64_t* c = R.hist + (size_t)f * net->n_counters;
+      for (int j = 0; j < nl; ++j) {
+        const LayerPlan& L = net->layers[j];
+        const TensorPlan& in = net->tensors[L.d.src + 1];
+        const TensorPlan& out = net->tensors[j + 1];
+        int64_t* q = counts + ((size_t)f * nl + j) * 4;
+        q[0] = (int64_t)c[L.cnt_O];
+        q[1] = (int64_t)c[L.cnt_pairs];
+        q[2] = (int64_t)c[in.cnt_act];
+        q[3] = (int64_t)c[out.cnt_rows];
+      }
+    }
+  return ST_OK;
+}

@@ -1,0 +1,93 @@
+// Internal plan of a diff-computation net: shapes, workspace layout and
+// host-side state shared by the planner (st_plan.cpp) and the executor
+// (st_exec.hip).  Not part of the public ABI.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/sparsetem.h"
+
+namespace st {
+
+constexpr int kChanAlign = 8;       // delta rows / weights padded to 8 channels
+constexpr int kMaxTiles = 1024;     // compaction tiles per pass
+constexpr size_t kAlign = 256;      // workspace sub-buffer alignment
+
+inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Counter block layout (uint64 each).
+struct CounterIdx {
+  int rows;   // candidate rows of a tensor / affected outputs of a layer
+  int act;    // kept rows of a tensor
+  int pairs;  // rulebook pairs of a layer
+};
+
+// An emitted delta tensor: t = 0 is the frame delta, t = j + 1 is layer j's
+// output (after its pool, if any).
+struct TensorPlan {
+  int N = 0, H = 0, W = 0, C = 0, Cp = 0;
+  int64_t grid = 0;                 // N*H*W
+  size_t off_rows = 0;              // storage dtype [grid][Cp]
+  size_t off_rowpix = 0;            // int32 [grid]  row -> pixel (ascending)
+  size_t off_act = 0;               // int32 [grid]  kept pixels (ascending)
+  size_t off_map = 0;               // int32 [grid]  pixel -> row or -1
+  size_t off_rowmax = 0;            // uint32 [grid] bits of max|delta| per row
+  int cnt_rows = 0, cnt_act = 0;    // counter indices
+  float last_thr = 0.f;             // threshold used by the last encode
+};
+
+struct LayerPlan {
+  st_layer_desc d{};
+  int Hi = 0, Wi = 0, Ho = 0, Wo = 0, Hp = 0, Wp = 0;
+  int K = 0, cin_p = 0, cout_p = 0;
+  int64_t ktot = 0, ktot_p = 0;     // K*cin_p and its padding to the GEMM chunk
+  int64_t conv_grid = 0;            // N*Ho*Wo
+  bool stateful = false, pool = false, dw = false, ident = false;
+  int mode = 0;                     // epilogue mode (kModeState/Defer/Linear)
+  // workspace offsets
+  size_t off_P = 0;                 // f32 [conv_grid][cout_p]
+  size_t off_O = 0;                 // int32 [conv_grid] affected conv outputs
+  size_t off_Mo = 0;                // int32 [conv_grid] pixel -> O index
+  size_t off_nbr = 0;               // int32 [K][conv_grid]
+  size_t off_dP = 0;                // f32 [conv_grid][cout_p] (pooled layers)
+  size_t off_w = 0;                 // GEMM: dtype [cout_p][ktot_p]; dw: f32 [K][cout_p]
+  size_t off_bias = 0;              // f32 [cout_p]
+  int cnt_O = 0, cnt_pairs = 0;
+};
+
+enum { kModeState = 0, kModeDefer = 1, kModeLinear = 2 };
+
+struct Recorder;  // executor-side profiling state
+
+}  // namespace st
+
+struct st_net {
+  int dtype = 0, esize = 4;
+  int N = 0, H = 0, W = 0, C = 0;
+  std::vector<st::LayerPlan> layers;
+  std::vector<st::TensorPlan> tensors;     // n_layers + 1
+  size_t ws_bytes = 0;
+  size_t off_xhat = 0;                     // storage dtype [N*H*W*C]
+  size_t off_flags = 0;                    // uint8 [max grid]
+  size_t off_tiles = 0;                    // uint32 [kMaxTiles]
+  size_t off_cnt = 0;                      // uint64 [n_counters]
+  size_t off_cleanup = 0;                  // cleanup descriptor table
+  size_t off_dens = 0;                     // uint64 [batch] per-image counts
+  int n_counters = 0;
+  int n_cleanup = 0;
+  int64_t max_grid = 0;
+  // runtime
+  char* ws = nullptr;
+  bool bound = false, have_ref = false;
+  void* last_stream = nullptr;
+  std::string err;
+  st::Recorder* rec = nullptr;
+};
+
+namespace st {
+st_status fail(st_net* net, st_status s, const std::string& msg);
+}

@@ -1,0 +1,126 @@
+// Launch interface of the gfx950 kernels of the diff-computation path.
+// Each launcher enqueues one kernel on `s`; counts that depend on the frame
+// live in device memory (uint64 counters), so no launcher reads data back
+// and the per-frame launch sequence is fixed.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace st {
+
+struct Geo {  // sliding-window geometry from an input grid to an output grid
+  int Hi, Wi, Ho, Wo, kh, kw, sh, sw, ph, pw;
+};
+
+struct CleanEntry {  // map[list[r]] = -1 for r < counter[cnt]
+  int64_t map_off, list_off;
+  int32_t cnt, pad;
+  int64_t pad2;
+};
+
+using u64 = unsigned long long;
+
+// Profiling hook (defined by the executor): records an event pair around
+// a launch when recording is enabled.
+struct Prof {
+  void* net;
+  int layer;
+};
+void prof_begin(const Prof& p, int cls, hipStream_t s);
+void prof_end(const Prof& p, int cls, hipStream_t s);
+
+// ---- per-frame bookkeeping
+void launch_reset(const Prof& pf, hipStream_t s, u64* cnt, int n);
+void launch_cleanup(const Prof& pf, hipStream_t s, const CleanEntry* tab,
+                    int n_tab, char* ws, const u64* cnt, int64_t max_rows);
+
+// ---- (a) subtraction + truncation + compaction of the frame delta
+void launch_scan(const Prof& pf, hipStream_t s, int dtype, const void* x,
+                 void* xhat, int C, int Cp, int64_t npix, float thr, int ref,
+                 uint8_t* keep, uint32_t* tiles, void* rows, int* rowpix,
+                 int* act, int* map, u64* cnt_rows, u64* cnt_act);
+
+// ---- (b) rulebook
+void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
+                 const u64* n_list, const int* list2, const u64* n_list2,
+                 int64_t max_items, Geo g, int N, uint8_t* flags);
+void launch_flag_compact(const Prof& pf, int cls_count, int cls_write,
+                         hipStream_t s, uint8_t* flags, int64_t npix,
+                         uint32_t* tiles, int* list, int* map,
+                         uint32_t* rowmax, u64* cnt);
+void launch_ident(const Prof& pf, hipStream_t s, const int* act_in,
+                  const u64* n_in, const int* map_in, int64_t max_items,
+                  int* O, int* Mo, int* nbr, uint32_t* rowmax, u64* cnt_O,
+                  u64* pairs);
+void launch_nbr(const Prof& pf, hipStream_t s, const int* O, const u64* nO,
+                int64_t capO, Geo g, int K, const int* map_in, int* nbr,
+                u64* pairs);
+
+// ---- (c)+(d) delta convolution with the fused state update / emission
+struct ConvArgs {
+  const void* din;     // input delta rows [*, cin_p]
+  const int* nbr;      // [K][stride] input row or -1
+  int64_t stride;
+  int K, cin_p, cout_p;
+  int64_t ktot_p;
+  const void* w;       // GEMM: [cout_p][ktot_p] storage dtype; dw: [K][cout_p] f32
+  const float* bias;   // [cout_p]
+  const int* O;        // affected output pixels (row -> pixel)
+  const u64* nO;
+  int64_t capO;
+  float* P;            // [grid][cout_p] pixel-indexed state
+  float* dP;           // [capO][cout_p] deferred update (pooled layers)
+  void* dout;          // [capO][cout_p] emitted delta rows
+  uint32_t* rowmax;    // [capO]
+  const void* dskip;   // residual delta rows [*, cout_p] or NULL
+  const int* mskip;    // residual pixel -> row map
+  int mode, act, ref;
+};
+void launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
+                      const ConvArgs& a);
+void launch_conv_dw(const Prof& pf, hipStream_t s, int dtype,
+                    const ConvArgs& a);
+
+// ---- non-linear post-op (max-pool) and state commit
+struct PoolArgs {
+  const int* Q;        // pooled rows -> pooled pixel
+  const u64* nQ;
+  int64_t capQ;
+  Geo g;               // conv grid -> pooled grid (pool window)
+  const float* P;
+  const float* dP;
+  const int* Mo;       // conv pixel -> O index or -1
+  void* dout;
+  uint32_t* rowmax;
+  int cp, act, ref;
+};
+void launch_pool_emit(const Prof& pf, hipStream_t s, int dtype,
+                      const PoolArgs& a);
+void launch_commit(const Prof& pf, hipStream_t s, const int* O, const u64* nO,
+                   int64_t capO, float* P, const float* dP, int cp, int ref);
+
+// ---- truncation of an emitted tensor (list-mode compaction)
+void launch_list_compact(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
+                         const u64* n_rows, int64_t cap, float thr,
+                         const int* rowpix, int* act, int* map,
+                         uint32_t* tiles, u64* cnt_act);
+
+// ---- dense network output (Accumulation)
+void launch_output(const Prof& pf, hipStream_t s, const float* P, int cp,
+                   int C, int N, Geo pool, int has_pool, int act, float* out);
+
+// ---- setup / introspection helpers
+void launch_fill_u32(hipStream_t s, void* p, int64_t n, uint32_t v);
+void launch_repack_dense(hipStream_t s, int dtype, const void* w, void* wt,
+                         int cout, int cin, int kh, int kw, int cin_p,
+                         int cout_p, int64_t ktot_p);
+void launch_repack_dw(hipStream_t s, int dtype, const void* w, float* wdw,
+                      int c, int kh, int kw, int cp);
+void launch_bias(hipStream_t s, int dtype, const void* b, float* out,
+                 int cout, int cout_p);
+void launch_density(hipStream_t s, const int* act, const u64* n_act,
+                    int64_t hw, int batch, u64* out);
+
+}  // namespace st

@@ -1,0 +1,997 @@
+// gfx950 kernels of the diff-computation path (wave64, MFMA, LDS).
+//
+//   scan      subtraction X - X_hat, per-pixel truncation mask, ascending
+//             compaction with wave ballot + mbcnt prefixes, commit of X_hat
+//   rulebook  affected-output marking, compaction, output-major neighbour
+//             table (the dense amplification of a sliding window)
+//   conv      gather-GEMM-scatter on MFMA over affected output rows, with
+//             the state update / non-linearity / delta emission fused into
+//             the epilogue; a vector-ALU path for depthwise layers
+//   pool      max-pool non-linear handling from old and new state
+//   list      truncation of an emitted delta tensor
+//
+// Determinism: every output row is owned by one tile and its offsets are
+// summed in a fixed order; the only atomics are integer counters and an
+// unsigned max on the bit pattern of non-negative floats, both
+// order-independent.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "st_kernels.h"
+
+namespace st {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+
+struct bf16_t {
+  uint16_t v;
+};
+
+// ------------------------------------------------------------ conversions
+__device__ __forceinline__ float to_f(float x) { return x; }
+__device__ __forceinline__ float to_f(_Float16 x) { return (float)x; }
+__device__ __forceinline__ float to_f(bf16_t x) {
+  return __uint_as_float((uint32_t)x.v << 16);
+}
+template <typename T> __device__ __forceinline__ T from_f(float x);
+template <> __device__ __forceinline__ float from_f<float>(float x) {
+  return x;
+}
+template <> __device__ __forceinline__ _Float16 from_f<_Float16>(float x) {
+  return (_Float16)x;  // hardware conversion, round to nearest even
+}
+template <> __device__ __forceinline__ bf16_t from_f<bf16_t>(float x) {
+  // round to nearest even on the f32 bit pattern (finite inputs)
+  uint32_t u = __float_as_uint(x);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return bf16_t{(uint16_t)(u >> 16)};
+}
+template <typename T> __device__ __forceinline__ T zero_v() {
+  return from_f<T>(0.f);
+}
+
+__device__ __forceinline__ float act_f(float x, int a) {
+  if (a == 1) return fmaxf(x, 0.f);
+  if (a == 2) return x / (1.f + expf(-x));
+  return x;
+}
+
+// ------------------------------------------------------------ reductions
+__device__ __forceinline__ unsigned wave_sum(unsigned v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Sum over a 256-thread block; every thread receives the total.
+__device__ __forceinline__ unsigned block_sum(unsigned v) {
+  __shared__ unsigned red[4];
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  return red[0] + red[1] + red[2] + red[3];
+}
+
+__device__ __forceinline__ unsigned lane_prefix(u64 ballot) {
+  return __builtin_amdgcn_mbcnt_hi((unsigned)(ballot >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((unsigned)ballot,
+                                                             0u));
+}
+
+__device__ __forceinline__ int64_t read_count(const u64* dev, int64_t host) {
+  return dev ? (int64_t)*dev : host;
+}
+
+// ============================================================ compaction
+// Ascending stream compaction in two passes.  Items are split into tiles of
+// `tile` consecutive indices (a multiple of 256); pass 1 counts the kept
+// items of each tile, pass 2 derives each tile's output offset from the
+// counts of the tiles before it and writes the kept items in order, using a
+// wave ballot and mbcnt for the in-wave prefix and LDS for the cross-wave
+// prefix.  The block that owns the last item writes the total.
+template <class P>
+__global__ __launch_bounds__(256) void k_compact_count(const u64* n_dev,
+                                                       int64_t n_host,
+                                                       int tile,
+                                                       uint32_t* tile_cnt,
+                                                       P pred) {
+  const int64_t n = read_count(n_dev, n_host);
+  const int64_t base = (int64_t)blockIdx.x * tile;
+  if (base >= n) return;
+  const int64_t end = min(base + (int64_t)tile, n);
+  unsigned c = 0;
+  for (int64_t i = base + threadIdx.x; i < end; i += 256)
+    c += pred.count(i) ? 1u : 0u;
+  c = block_sum(c);
+  if (threadIdx.x == 0) tile_cnt[blockIdx.x] = c;
+}
+
+template <class P>
+__global__ __launch_bounds__(256) void k_compact_write(
+    const u64* n_dev, int64_t n_host, int tile, const uint32_t* tile_cnt,
+    u64* out_cnt, u64* out_cnt2, P pred) {
+  const int64_t n = read_count(n_dev, n_host);
+  const int64_t base = (int64_t)blockIdx.x * tile;
+  if (base >= n) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      *out_cnt = 0;
+      if (out_cnt2) *out_cnt2 = 0;
+    }
+    return;
+  }
+  unsigned off = 0;
+  for (unsigned j = threadIdx.x; j < blockIdx.x; j += 256) off += tile_cnt[j];
+  off = block_sum(off);
+  const int64_t end = min(base + (int64_t)tile, n);
+  __shared__ unsigned wcnt[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  unsigned running = off;
+  for (int64_t r0 = base; r0 < end; r0 += 256) {
+    const int64_t i = r0 + threadIdx.x;
+    const bool in = i < end;
+    const bool keep = in && pred.keep(i);
+    const u64 bal = __ballot(keep);
+    const unsigned lp = lane_prefix(bal);
+    if (lane == 0) wcnt[wave] = (unsigned)__popcll(bal);
+    __syncthreads();
+    unsigned wpre = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const unsigned c = wcnt[w];
+      wpre += (w < wave) ? c : 0u;
+      tot += c;
+    }
+    if (keep)
+      pred.emit(i, running + wpre + lp);
+    else if (in)
+      pred.drop(i);
+    running += tot;
+    __syncthreads();
+  }
+  if (end == n && threadIdx.x == 0) {
+    *out_cnt = running;
+    if (out_cnt2) *out_cnt2 = running;
+  }
+}
+
+static int compact_tile(int64_t cap) {
+  int64_t t = (cap + 1023) / 1024;
+  t = (t + 255) / 256 * 256;
+  return (int)(t < 1024 ? 1024 : t);
+}
+
+template <class P>
+static void run_compact(const Prof& pf, int cls_count, int cls_write,
+                        hipStream_t s, const u64* n_dev, int64_t n_host,
+                        int64_t cap, uint32_t* tiles, u64* out_cnt,
+                        u64* out_cnt2, P pred) {
+  const int tile = compact_tile(cap);
+  int nt = (int)((cap + tile - 1) / tile);
+  if (nt < 1) nt = 1;
+  prof_begin(pf, cls_count, s);
+  k_compact_count<P><<<nt, 256, 0, s>>>(n_dev, n_host, tile, tiles, pred);
+  prof_end(pf, cls_count, s);
+  prof_begin(pf, cls_write, s);
+  k_compact_write<P><<<nt, 256, 0, s>>>(n_dev, n_host, tile, tiles, out_cnt,
+                                        out_cnt2, pred);
+  prof_end(pf, cls_write, s);
+}
+
+// ------------------------------------------------------- (a) frame delta
+template <typename T>
+struct ScanPred {
+  const T* x;
+  T* xhat;
+  uint8_t* keepb;
+  T* rows;
+  int* rowpix;
+  int* act;
+  int* map;
+  int C, Cp, ref;
+  float thr;
+  // pass 1: evaluate the truncation rule and remember it
+  __device__ bool count(int64_t i) const {
+    float m = 0.f;
+    for (int c = 0; c < C; ++c) {
+      float d = to_f(x[i * C + c]) - (ref ? 0.f : to_f(xhat[i * C + c]));
+      m = fmaxf(m, fabsf(d));
+    }
+    const bool k = m > thr;
+    keepb[i] = k ? 1 : 0;
+    return k;
+  }
+  __device__ bool keep(int64_t i) const { return keepb[i] != 0; }
+  // pass 2: gather the delta row, commit the pixel to X_hat
+  __device__ void emit(int64_t i, unsigned pos) const {
+    rowpix[pos] = (int)i;
+    act[pos] = (int)i;
+    map[i] = (int)pos;
+    T* r = rows + (int64_t)pos * Cp;
+    for (int c = 0; c < Cp; ++c) {
+      if (c < C) {
+        const T xv = x[i * C + c];
+        const float d = to_f(xv) - (ref ? 0.f : to_f(xhat[i * C + c]));
+        r[c] = from_f<T>(d);
+        xhat[i * C + c] = xv;
+      } else {
+        r[c] = zero_v<T>();
+      }
+    }
+    keepb[i] = 0;
+  }
+  __device__ void drop(int64_t) const {}
+};
+
+template <typename T>
+static void scan_t(const Prof& pf, hipStream_t s, const void* x, void* xhat,
+                   int C, int Cp, int64_t npix, float thr, int ref,
+                   uint8_t* keep, uint32_t* tiles, void* rows, int* rowpix,
+                   int* act, int* map, u64* cnt_rows, u64* cnt_act) {
+  ScanPred<T> p{(const T*)x, (T*)xhat, keep, (T*)rows, rowpix, act, map,
+                C, Cp, ref, thr};
+  run_compact(pf, 0 /*ST_K_SCAN_MASK*/, 1 /*ST_K_SCAN_COMPACT*/, s, nullptr,
+              npix, npix, tiles, cnt_rows, cnt_act, p);
+}
+
+void launch_scan(const Prof& pf, hipStream_t s, int dtype, const void* x,
+                 void* xhat, int C, int Cp, int64_t npix, float thr, int ref,
+                 uint8_t* keep, uint32_t* tiles, void* rows, int* rowpix,
+                 int* act, int* map, u64* cnt_rows, u64* cnt_act) {
+  if (dtype == 0)
+    scan_t<float>(pf, s, x, xhat, C, Cp, npix, thr, ref, keep, tiles, rows,
+                  rowpix, act, map, cnt_rows, cnt_act);
+  else if (dtype == 1)
+    scan_t<_Float16>(pf, s, x, xhat, C, Cp, npix, thr, ref, keep, tiles, rows,
+                     rowpix, act, map, cnt_rows, cnt_act);
+  else
+    scan_t<bf16_t>(pf, s, x, xhat, C, Cp, npix, thr, ref, keep, tiles, rows,
+                   rowpix, act, map, cnt_rows, cnt_act);
+}
+
+// ---------------------------------------------------------- (b) rulebook
+static int grid_for(int64_t items, int cap_blocks = 4096) {
+  int64_t b = (items + 255) / 256;
+  if (b < 1) b = 1;
+  return (int)(b > cap_blocks ? cap_blocks : b);
+}
+
+// Mark every output site reached by an active input site through some
+// window offset; optionally also mark the sites of a second list (residual
+// deltas, already on the output grid).
+__global__ __launch_bounds__(256) void k_mark(const int* list, const u64* n1p,
+                                              const int* list2,
+                                              const u64* n2p, Geo g,
+                                              uint8_t* flags) {
+  const int64_t n1 = (int64_t)*n1p;
+  const int64_t n2 = list2 ? (int64_t)*n2p : 0;
+  const int64_t hwi = (int64_t)g.Hi * g.Wi;
+  for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j < n1 + n2;
+       j += (int64_t)gridDim.x * 256) {
+    if (j >= n1) {
+      flags[list2[j - n1]] = 1;
+      continue;
+    }
+    const int p = list[j];
+    const int n = (int)(p / hwi);
+    const int rem = (int)(p - n * hwi);
+    const int iy = rem / g.Wi, ix = rem - (rem / g.Wi) * g.Wi;
+    for (int ky = 0; ky < g.kh; ++ky) {
+      const int ty = iy + g.ph - ky;
+      if (ty < 0) break;
+      if (ty % g.sh) continue;
+      const int oy = ty / g.sh;
+      if (oy >= g.Ho) continue;
+      for (int kx = 0; kx < g.kw; ++kx) {
+        const int tx = ix + g.pw - kx;
+        if (tx < 0) break;
+        if (tx % g.sw) continue;
+        const int ox = tx / g.sw;
+        if (ox >= g.Wo) continue;
+        flags[((int64_t)n * g.Ho + oy) * g.Wo + ox] = 1;
+      }
+    }
+  }
+}
+
+void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
+                 const u64* n_list, const int* list2, const u64* n_list2,
+                 int64_t max_items, Geo g, int N, uint8_t* flags) {
+  (void)N;
+  prof_begin(pf, cls, s);
+  k_mark<<<grid_for(max_items), 256, 0, s>>>(list, n_list, list2, n_list2, g,
+                                             flags);
+  prof_end(pf, cls, s);
+}
+
+struct FlagPred {
+  uint8_t* flags;
+  int* list;
+  int* map;
+  uint32_t* rowmax;
+  __device__ bool count(int64_t i) const { return flags[i] != 0; }
+  __device__ bool keep(int64_t i) const { return flags[i] != 0; }
+  __device__ void emit(int64_t i, unsigned pos) const {
+    list[pos] = (int)i;
+    map[i] = (int)pos;
+    flags[i] = 0;
+    if (rowmax) rowmax[pos] = 0u;
+  }
+  __device__ void drop(int64_t) const {}
+};
+
+void launch_flag_compact(const Prof& pf, int cls_count, int cls_write,
+                         hipStream_t s, uint8_t* flags, int64_t npix,
+                         uint32_t* tiles, int* list, int* map,
+                         uint32_t* rowmax, u64* cnt) {
+  FlagPred p{flags, list, map, rowmax};
+  run_compact(pf, cls_count, cls_write, s, nullptr, npix, npix, tiles, cnt,
+              nullptr, p);
+}
+
+// 1x1 stride-1 convolution without residual: the affected outputs are the
+// active inputs themselves and each has exactly one neighbour.
+__global__ __launch_bounds__(256) void k_ident(const int* act_in,
+                                               const u64* n_in,
+                                               const int* map_in, int* O,
+                                               int* Mo, int* nbr,
+                                               uint32_t* rowmax, u64* cnt_O,
+                                               u64* pairs) {
+  const int64_t n = (int64_t)*n_in;
+  for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j < n;
+       j += (int64_t)gridDim.x * 256) {
+    const int p = act_in[j];
+    O[j] = p;
+    Mo[p] = (int)j;
+    nbr[j] = map_in[p];
+    if (rowmax) rowmax[j] = 0u;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    *cnt_O = (u64)n;
+    *pairs = (u64)n;
+  }
+}
+
+void launch_ident(const Prof& pf, hipStream_t s, const int* act_in,
+                  const u64* n_in, const int* map_in, int64_t max_items,
+                  int* O, int* Mo, int* nbr, uint32_t* rowmax, u64* cnt_O,
+                  u64* pairs) {
+  prof_begin(pf, 6 /*ST_K_RB_IDENT*/, s);
+  k_ident<<<grid_for(max_items), 256, 0, s>>>(act_in, n_in, map_in, O, Mo,
+                                              nbr, rowmax, cnt_O, pairs);
+  prof_end(pf, 6, s);
+}
+
+// Output-major neighbour table: nbr[k][o] = row of the input delta at the
+// site offset k of output o reads, or -1 (padding or inactive site).
+__global__ __launch_bounds__(256) void k_nbr(const int* O, const u64* nOp,
+                                             int64_t stride, Geo g, int K,
+                                             const int* map_in, int* nbr,
+                                             u64* pairs) {
+  const int64_t nO = (int64_t)*nOp;
+  const int64_t total = nO * K;
+  const int64_t hwo = (int64_t)g.Ho * g.Wo;
+  unsigned cnt = 0;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    const int k = (int)(idx / nO);
+    const int64_t o = idx - (int64_t)k * nO;
+    const int p = O[o];
+    const int n = (int)(p / hwo);
+    const int rem = (int)(p - n * hwo);
+    const int oy = rem / g.Wo, ox = rem - (rem / g.Wo) * g.Wo;
+    const int ky = k / g.kw, kx = k - (k / g.kw) * g.kw;
+    const int iy = oy * g.sh - g.ph + ky, ix = ox * g.sw - g.pw + kx;
+    int v = -1;
+    if (iy >= 0 && iy < g.Hi && ix >= 0 && ix < g.Wi)
+      v = map_in[((int64_t)n * g.Hi + iy) * g.Wi + ix];
+    nbr[(int64_t)k * stride + o] = v;
+    cnt += v >= 0 ? 1u : 0u;
+  }
+  cnt = block_sum(cnt);
+  if (threadIdx.x == 0 && cnt) atomicAdd(pairs, (u64)cnt);
+}
+
+void launch_nbr(const Prof& pf, hipStream_t s, const int* O, const u64* nO,
+                int64_t capO, Geo g, int K, const int* map_in, int* nbr,
+                u64* pairs) {
+  prof_begin(pf, 5 /*ST_K_RB_NBR*/, s);
+  k_nbr<<<grid_for(capO * K), 256, 0, s>>>(O, nO, capO, g, K, map_in, nbr,
+                                           pairs);
+  prof_end(pf, 5, s);
+}
+
+// ------------------------------------------- (c)+(d) convolution epilogue
+template <typename T>
+struct Epi {
+  float* P;
+  float* dP;
+  T* dout;
+  const float* bias;
+  const T* dskip;
+  const int* mskip;
+  int cout_p, mode, act, ref;
+
+  // Finish one output element: add bias (reference pass) and the residual
+  // delta, then either defer the update (pooled layers), or update the f32
+  // state in place and emit f(P_new) - f(P_old), or pass the linear delta
+  // on.  Returns |emitted delta| after rounding to the storage dtype.
+  __device__ __forceinline__ float operator()(int64_t o, int pix, int n,
+                                              float acc) const {
+    float dp = acc;
+    if (ref) dp += bias[n];
+    if (mskip) {
+      const int r = mskip[pix];
+      if (r >= 0) dp += to_f(dskip[(int64_t)r * cout_p + n]);
+    }
+    if (mode == 1) {
+      dP[o * cout_p + n] = dp;
+      return 0.f;
+    }
+    float d = dp;
+    if (mode == 0) {
+      float* pp = P + (int64_t)pix * cout_p + n;
+      const float po = ref ? 0.f : *pp;
+      const float pn = po + dp;
+      *pp = pn;
+      d = act_f(pn, act) - act_f(po, act);
+    }
+    const T q = from_f<T>(d);
+    dout[o * cout_p + n] = q;
+    return fabsf(to_f(q));
+  }
+};
+
+template <typename T>
+__device__ __forceinline__ Epi<T> make_epi(const ConvArgs& a) {
+  return Epi<T>{a.P, a.dP, (T*)a.dout, a.bias, (const T*)a.dskip, a.mskip,
+                a.cout_p, a.mode, a.act, a.ref};
+}
+
+// --------------------------------------------------- (c) gather-GEMM MFMA
+// Output-stationary tile of BM=64 affected rows x BN=64 output channels,
+// four waves in a 2x2 arrangement, each owning a 32x32 sub-tile (2x2 MFMA
+// 16x16 blocks).  The reduction index r = k * cin_p + ci runs over kernel
+// offsets and input channels; per stage KC reduction columns of the
+// gathered input rows (A) and of the repacked weights (B, [cout_p][ktot_p])
+// are staged through LDS.  Stages whose offsets have no active neighbour
+// in the tile are skipped (adding exact zeros would not change the sum).
+template <typename T> struct MmaCfg;
+template <> struct MmaCfg<float> {
+  static constexpr int KC = 16, LD = 17;  // scalar LDS rows, conflict-free
+};
+template <> struct MmaCfg<_Float16> {
+  static constexpr int KC = 64, LD = 72;  // 16-byte aligned LDS rows
+};
+template <> struct MmaCfg<bf16_t> {
+  static constexpr int KC = 64, LD = 72;
+};
+
+template <typename T>
+__device__ __forceinline__ void lds_store16(T* dst, uint4 v);
+template <>
+__device__ __forceinline__ void lds_store16<float>(float* dst, uint4 v) {
+  dst[0] = __uint_as_float(v.x);
+  dst[1] = __uint_as_float(v.y);
+  dst[2] = __uint_as_float(v.z);
+  dst[3] = __uint_as_float(v.w);
+}
+template <>
+__device__ __forceinline__ void lds_store16<_Float16>(_Float16* dst, uint4 v) {
+  *(uint4*)dst = v;
+}
+template <>
+__device__ __forceinline__ void lds_store16<bf16_t>(bf16_t* dst, uint4 v) {
+  *(uint4*)dst = v;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
+  constexpr int BM = 64, BN = 64;
+  constexpr int KC = MmaCfg<T>::KC, LD = MmaCfg<T>::LD;
+  constexpr int VEC = 16 / (int)sizeof(T);
+  constexpr int VPR = KC / VEC;  // 16-byte vectors per staged row
+  __shared__ T As[BM * LD];
+  __shared__ T Bs[BN * LD];
+  __shared__ u64 s_kmask;
+
+  const T* din = (const T*)a.din;
+  const T* wt = (const T*)a.w;
+  const Epi<T> epi = make_epi<T>(a);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l16 = lane & 15, lg = lane >> 4;
+  const int64_t nO = (int64_t)*a.nO;
+  const int64_t tiles_m = (nO + BM - 1) / BM;
+  const int tiles_n = (a.cout_p + BN - 1) / BN;
+  const int64_t ntiles = tiles_m * tiles_n;
+
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int64_t m0 = (t / tiles_n) * BM;
+    const int n0 = (int)(t % tiles_n) * BN;
+
+    // offsets that have at least one active neighbour in this tile
+    if (tid == 0) s_kmask = 0ull;
+    __syncthreads();
+    u64 my = 0ull;
+    for (int e = tid; e < BM * a.K; e += 256) {
+      const int k = e / BM, m = e - (e / BM) * BM;
+      const int64_t o = m0 + m;
+      if (o < nO && a.nbr[(int64_t)k * a.stride + o] >= 0) my |= 1ull << k;
+    }
+    if (my) atomicOr(&s_kmask, my);
+    __syncthreads();
+    const u64 kmask = s_kmask;
+
+    v4f acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    for (int64_t r0 = 0; r0 < a.ktot_p; r0 += KC) {
+      const int klo = (int)(r0 / a.cin_p);
+      if (klo >= a.K) break;
+      int khi = (int)((r0 + KC - 1) / a.cin_p);
+      if (khi > a.K - 1) khi = a.K - 1;
+      const int span = khi - klo + 1;
+      const u64 bits = (span >= 64 ? ~0ull : ((1ull << span) - 1)) << klo;
+      if (!(kmask & bits)) continue;
+
+      // A: gathered input rows (zero for inactive or padded neighbours)
+      for (int v = tid; v < BM * VPR; v += 256) {
+        const int m = v / VPR, cv = v - (v / VPR) * VPR;
+        const int64_t r = r0 + cv * VEC;
+        const int64_t o = m0 + m;
+        const int k = (int)(r / a.cin_p);
+        const int ci = (int)(r - (int64_t)k * a.cin_p);
+        uint4 val = make_uint4(0u, 0u, 0u, 0u);
+        if (o < nO && k < a.K) {
+          const int src = a.nbr[(int64_t)k * a.stride + o];
+          if (src >= 0)
+            val = *(const uint4*)(din + (int64_t)src * a.cin_p + ci);
+        }
+        lds_store16<T>(As + m * LD + cv * VEC, val);
+      }
+      // B: repacked weights
+      for (int v = tid; v < BN * VPR; v += 256) {
+        const int nn = v / VPR, cv = v - (v / VPR) * VPR;
+        const int n = n0 + nn;
+        uint4 val = make_uint4(0u, 0u, 0u, 0u);
+        if (n < a.cout_p)
+          val = *(const uint4*)(wt + (int64_t)n * a.ktot_p + r0 + cv * VEC);
+        lds_store16<T>(Bs + nn * LD + cv * VEC, val);
+      }
+      __syncthreads();
+
+      if constexpr (sizeof(T) == 4) {
+#pragma unroll
+        for (int kk = 0; kk < KC; kk += 4) {
+          float af[2], bf[2];
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+            af[i] = As[(wm * 32 + i * 16 + l16) * LD + kk + lg];
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            bf[j] = Bs[(wn * 32 + j * 16 + l16) * LD + kk + lg];
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                  af[i], bf[j], acc[i][j], 0, 0, 0);
+        }
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < KC; kk += 32) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+              const uint4 av =
+                  *(const uint4*)(As + (wm * 32 + i * 16 + l16) * LD + kk +
+                                  8 * lg);
+              const uint4 bv =
+                  *(const uint4*)(Bs + (wn * 32 + j * 16 + l16) * LD + kk +
+                                  8 * lg);
+              if constexpr (sizeof(T) == 2 && __is_same(T, _Float16)) {
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                    __builtin_bit_cast(v8h, av), __builtin_bit_cast(v8h, bv),
+                    acc[i][j], 0, 0, 0);
+              } else {
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    __builtin_bit_cast(v8bf, av),
+                    __builtin_bit_cast(v8bf, bv), acc[i][j], 0, 0, 0);
+              }
+            }
+          }
+        }
+      }
+      __syncthreads();
+    }
+
+    // fused epilogue: D[row = 4*lg + r][col = l16] of each 16x16 block
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = wm * 32 + i * 16 + 4 * lg + r;
+        const int64_t o = m0 + m;
+        const bool ok = o < nO;
+        const int pix = ok ? a.O[o] : 0;
+        float rm = 0.f;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int n = n0 + wn * 32 + j * 16 + l16;
+          if (ok && n < a.cout_p) rm = fmaxf(rm, epi(o, pix, n, acc[i][j][r]));
+        }
+#pragma unroll
+        for (int x = 1; x < 16; x <<= 1) rm = fmaxf(rm, __shfl_xor(rm, x, 64));
+        if (ok && l16 == 0 && a.mode != 1 && rm > 0.f)
+          atomicMax(a.rowmax + o, __float_as_uint(rm));
+      }
+    }
+  }
+}
+
+void launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
+                      const ConvArgs& a) {
+  const int64_t worst = ((a.capO + 63) / 64) * ((a.cout_p + 63) / 64);
+  const int grid = (int)(worst < 2048 ? (worst < 1 ? 1 : worst) : 2048);
+  prof_begin(pf, 7 /*ST_K_CONV_GEMM*/, s);
+  if (dtype == 0)
+    k_conv_gemm<float><<<grid, 256, 0, s>>>(a);
+  else if (dtype == 1)
+    k_conv_gemm<_Float16><<<grid, 256, 0, s>>>(a);
+  else
+    k_conv_gemm<bf16_t><<<grid, 256, 0, s>>>(a);
+  prof_end(pf, 7, s);
+}
+
+// ---------------------------------------------------- (c') depthwise path
+// Memory-bound: each thread owns VEC channels of one affected row and sums
+// its K neighbours in offset order on the vector ALU.
+template <typename T>
+__global__ __launch_bounds__(256) void k_conv_dw(ConvArgs a) {
+  constexpr int VEC = 16 / (int)sizeof(T);
+  const T* din = (const T*)a.din;
+  const float* w = (const float*)a.w;
+  const Epi<T> epi = make_epi<T>(a);
+  const int64_t nO = (int64_t)*a.nO;
+  const int cpr = a.cout_p / VEC;
+  const int64_t total = nO * cpr;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    const int64_t o = idx / cpr;
+    const int c0 = (int)(idx - o * cpr) * VEC;
+    float acc[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+    for (int k = 0; k < a.K; ++k) {
+      const int src = a.nbr[(int64_t)k * a.stride + o];
+      if (src < 0) continue;
+      const uint4 raw = *(const uint4*)(din + (int64_t)src * a.cin_p + c0);
+      const T* xv = (const T*)&raw;
+      const float* wk = w + (int64_t)k * a.cout_p + c0;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[e] += wk[e] * to_f(xv[e]);
+    }
+    const int pix = a.O[o];
+    float rm = 0.f;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) rm = fmaxf(rm, epi(o, pix, c0 + e, acc[e]));
+    if (a.mode != 1 && rm > 0.f) atomicMax(a.rowmax + o, __float_as_uint(rm));
+  }
+}
+
+void launch_conv_dw(const Prof& pf, hipStream_t s, int dtype,
+                    const ConvArgs& a) {
+  const int vec = dtype == 0 ? 4 : 8;
+  const int grid = grid_for(a.capO * (a.cout_p / vec), 8192);
+  prof_begin(pf, 8 /*ST_K_CONV_DW*/, s);
+  if (dtype == 0)
+    k_conv_dw<float><<<grid, 256, 0, s>>>(a);
+  else if (dtype == 1)
+    k_conv_dw<_Float16><<<grid, 256, 0, s>>>(a);
+  else
+    k_conv_dw<bf16_t><<<grid, 256, 0, s>>>(a);
+  prof_end(pf, 8, s);
+}
+
+// ----------------------------------------------------------- max-pool
+// Delta of a pooled output = max over its window of f(P_new) minus the
+// same max of f(P_old); P_new = P_old + dP on affected conv outputs.
+template <typename T>
+__global__ __launch_bounds__(256) void k_pool_emit(PoolArgs a) {
+  T* dout = (T*)a.dout;
+  const int64_t nQ = (int64_t)*a.nQ;
+  const int64_t total = nQ * a.cp;
+  const Geo& g = a.g;  // Hi/Wi: conv grid, Ho/Wo: pooled grid
+  const int64_t hwq = (int64_t)g.Ho * g.Wo;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    const int64_t q = idx / a.cp;
+    const int c = (int)(idx - q * a.cp);
+    const int p = a.Q[q];
+    const int n = (int)(p / hwq);
+    const int rem = (int)(p - n * hwq);
+    const int qy = rem / g.Wo, qx = rem - (rem / g.Wo) * g.Wo;
+    float mo = -INFINITY, mn = -INFINITY;
+    for (int ky = 0; ky < g.kh; ++ky) {
+      const int iy = qy * g.sh - g.ph + ky;
+      if (iy < 0 || iy >= g.Hi) continue;
+      for (int kx = 0; kx < g.kw; ++kx) {
+        const int ix = qx * g.sw - g.pw + kx;
+        if (ix < 0 || ix >= g.Wi) continue;
+        const int64_t w = ((int64_t)n * g.Hi + iy) * g.Wi + ix;
+        const float po = a.ref ? 0.f : a.P[w * a.cp + c];
+        const int r = a.Mo[w];
+        const float pn = r >= 0 ? po + a.dP[(int64_t)r * a.cp + c] : po;
+        mo = fmaxf(mo, act_f(po, a.act));
+        mn = fmaxf(mn, act_f(pn, a.act));
+      }
+    }
+    const T qv = from_f<T>(mn - mo);
+    dout[q * a.cp + c] = qv;
+    const float ab = fabsf(to_f(qv));
+    if (ab > 0.f) atomicMax(a.rowmax + q, __float_as_uint(ab));
+  }
+}
+
+void launch_pool_emit(const Prof& pf, hipStream_t s, int dtype,
+                      const PoolArgs& a) {
+  const int grid = grid_for(a.capQ * a.cp, 8192);
+  prof_begin(pf, 12 /*ST_K_POOL_EMIT*/, s);
+  if (dtype == 0)
+    k_pool_emit<float><<<grid, 256, 0, s>>>(a);
+  else if (dtype == 1)
+    k_pool_emit<_Float16><<<grid, 256, 0, s>>>(a);
+  else
+    k_pool_emit<bf16_t><<<grid, 256, 0, s>>>(a);
+  prof_end(pf, 12, s);
+}
+
+__global__ __launch_bounds__(256) void k_commit(const int* O, const u64* nOp,
+                                                float* P, const float* dP,
+                                                int cp, int ref) {
+  const int64_t nO = (int64_t)*nOp;
+  const int c4 = cp / 4;
+  const int64_t total = nO * c4;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    const int64_t o = idx / c4;
+    const int c = (int)(idx - o * c4) * 4;
+    float4* pp = (float4*)(P + (int64_t)O[o] * cp + c);
+    const float4 d = *(const float4*)(dP + o * cp + c);
+    float4 v = ref ? make_float4(0.f, 0.f, 0.f, 0.f) : *pp;
+    v.x += d.x; v.y += d.y; v.z += d.z; v.w += d.w;
+    *pp = v;
+  }
+}
+
+void launch_commit(const Prof& pf, hipStream_t s, const int* O, const u64* nO,
+                   int64_t capO, float* P, const float* dP, int cp, int ref) {
+  prof_begin(pf, 13 /*ST_K_COMMIT*/, s);
+  k_commit<<<grid_for(capO * (cp / 4), 8192), 256, 0, s>>>(O, nO, P, dP, cp,
+                                                           ref);
+  prof_end(pf, 13, s);
+}
+
+// ------------------------------------------------ truncation (list mode)
+struct ListPred {
+  const uint32_t* rowmax;
+  const int* rowpix;
+  int* act;
+  int* map;
+  float thr;
+  __device__ bool count(int64_t r) const {
+    return __uint_as_float(rowmax[r]) > thr;
+  }
+  __device__ bool keep(int64_t r) const {
+    return __uint_as_float(rowmax[r]) > thr;
+  }
+  __device__ void emit(int64_t r, unsigned pos) const { act[pos] = rowpix[r]; }
+  __device__ void drop(int64_t r) const { map[rowpix[r]] = -1; }
+};
+
+void launch_list_compact(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
+                         const u64* n_rows, int64_t cap, float thr,
+                         const int* rowpix, int* act, int* map,
+                         uint32_t* tiles, u64* cnt_act) {
+  ListPred p{rowmax, rowpix, act, map, thr};
+  run_compact(pf, 14 /*ST_K_LIST_COUNT*/, 15 /*ST_K_LIST_COMPACT*/, s, n_rows,
+              0, cap, tiles, cnt_act, nullptr, p);
+}
+
+// ------------------------------------------------------- dense output
+__global__ __launch_bounds__(256) void k_output(const float* P, int cp, int C,
+                                                int N, Geo g, int has_pool,
+                                                int act, float* out) {
+  // g.Hi/Wi: conv grid; g.Ho/Wo: output grid (== conv grid without pool)
+  const int64_t total = (int64_t)N * g.Ho * g.Wo * C;
+  const int64_t hwo = (int64_t)g.Ho * g.Wo;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    const int64_t q = idx / C;
+    const int c = (int)(idx - q * C);
+    if (!has_pool) {
+      out[idx] = act_f(P[q * cp + c], act);
+      continue;
+    }
+    const int n = (int)(q / hwo);
+    const int rem = (int)(q - n * hwo);
+    const int qy = rem / g.Wo, qx = rem - (rem / g.Wo) * g.Wo;
+    float m = -INFINITY;
+    for (int ky = 0; ky < g.kh; ++ky) {
+      const int iy = qy * g.sh - g.ph + ky;
+      if (iy < 0 || iy >= g.Hi) continue;
+      for (int kx = 0; kx < g.kw; ++kx) {
+        const int ix = qx * g.sw - g.pw + kx;
+        if (ix < 0 || ix >= g.Wi) continue;
+        m = fmaxf(m, act_f(P[(((int64_t)n * g.Hi + iy) * g.Wi + ix) * cp + c],
+                           act));
+      }
+    }
+    out[idx] = m;
+  }
+}
+
+void launch_output(const Prof& pf, hipStream_t s, const float* P, int cp,
+                   int C, int N, Geo g, int has_pool, int act, float* out) {
+  prof_begin(pf, 16 /*ST_K_OUTPUT*/, s);
+  k_output<<<grid_for((int64_t)N * g.Ho * g.Wo * C, 8192), 256, 0, s>>>(
+      P, cp, C, N, g, has_pool, act, out);
+  prof_end(pf, 16, s);
+}
+
+// ------------------------------------------------------- bookkeeping
+__global__ void k_reset(u64* cnt, int n) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) cnt[i] = 0ull;
+}
+
+void launch_reset(const Prof& pf, hipStream_t s, u64* cnt, int n) {
+  prof_begin(pf, 18 /*ST_K_RESET*/, s);
+  k_reset<<<1, 256, 0, s>>>(cnt, n);
+  prof_end(pf, 18, s);
+}
+
+__global__ __launch_bounds__(256) void k_cleanup(const CleanEntry* tab,
+                                                 char* ws, const u64* cnt) {
+  const CleanEntry e = tab[blockIdx.y];
+  int* map = (int*)(ws + e.map_off);
+  const int* list = (const int*)(ws + e.list_off);
+  const int64_t n = (int64_t)cnt[e.cnt];
+  for (int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x; r < n;
+       r += (int64_t)gridDim.x * 256)
+    map[list[r]] = -1;
+}
+
+void launch_cleanup(const Prof& pf, hipStream_t s, const CleanEntry* tab,
+                    int n_tab, char* ws, const u64* cnt, int64_t max_rows) {
+  prof_begin(pf, 17 /*ST_K_CLEANUP*/, s);
+  dim3 grid(grid_for(max_rows, 512), n_tab);
+  k_cleanup<<<grid, 256, 0, s>>>(tab, ws, cnt);
+  prof_end(pf, 17, s);
+}
+
+__global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * 256)
+    p[i] = v;
+}
+
+void launch_fill_u32(hipStream_t s, void* p, int64_t n, uint32_t v) {
+  k_fill_u32<<<grid_for(n, 8192), 256, 0, s>>>((uint32_t*)p, n, v);
+}
+
+// Weight repack: PyTorch [cout][cin][kh][kw] -> [cout_p][ktot_p] with the
+// reduction index r = (ky * kw + kx) * cin_p + ci, zero padded.
+template <typename T>
+__global__ void k_repack_dense(const T* w, T* wt, int cout, int cin, int kh,
+                               int kw, int cin_p, int cout_p, int64_t ktot_p) {
+  const int64_t total = (int64_t)cout_p * ktot_p;
+  const int K = kh * kw;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    const int n = (int)(idx / ktot_p);
+    const int64_t r = idx - (int64_t)n * ktot_p;
+    const int k = (int)(r / cin_p);
+    const int ci = (int)(r - (int64_t)k * cin_p);
+    T v = zero_v<T>();
+    if (n < cout && k < K && ci < cin) {
+      const int ky = k / kw, kx = k - (k / kw) * kw;
+      v = w[(((int64_t)n * cin + ci) * kh + ky) * kw + kx];
+    }
+    wt[idx] = v;
+  }
+}
+
+void launch_repack_dense(hipStream_t s, int dtype, const void* w, void* wt,
+                         int cout, int cin, int kh, int kw, int cin_p,
+                         int cout_p, int64_t ktot_p) {
+  const int grid = grid_for((int64_t)cout_p * ktot_p, 8192);
+  if (dtype == 0)
+    k_repack_dense<float><<<grid, 256, 0, s>>>((const float*)w, (float*)wt,
+                                               cout, cin, kh, kw, cin_p,
+                                               cout_p, ktot_p);
+  else if (dtype == 1)
+    k_repack_dense<_Float16><<<grid, 256, 0, s>>>(
+        (const _Float16*)w, (_Float16*)wt, cout, cin, kh, kw, cin_p, cout_p,
+        ktot_p);
+  else
+    k_repack_dense<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)w, (bf16_t*)wt,
+                                                cout, cin, kh, kw, cin_p,
+                                                cout_p, ktot_p);
+}
+
+template <typename T>
+__global__ void k_repack_dw(const T* w, float* wdw, int c, int kh, int kw,
+                            int cp) {
+  const int K = kh * kw;
+  const int64_t total = (int64_t)K * cp;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    const int k = (int)(idx / cp);
+    const int ch = (int)(idx - (int64_t)k * cp);
+    wdw[idx] = ch < c ? to_f(w[(int64_t)ch * K + k]) : 0.f;
+  }
+}
+
+void launch_repack_dw(hipStream_t s, int dtype, const void* w, float* wdw,
+                      int c, int kh, int kw, int cp) {
+  const int grid = grid_for((int64_t)kh * kw * cp);
+  if (dtype == 0)
+    k_repack_dw<float><<<grid, 256, 0, s>>>((const float*)w, wdw, c, kh, kw,
+                                            cp);
+  else if (dtype == 1)
+    k_repack_dw<_Float16><<<grid, 256, 0, s>>>((const _Float16*)w, wdw, c, kh,
+                                               kw, cp);
+  else
+    k_repack_dw<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)w, wdw, c, kh, kw,
+                                             cp);
+}
+
+template <typename T>
+__global__ void k_bias(const T* b, float* out, int cout, int cout_p) {
+  for (int i = threadIdx.x; i < cout_p; i += blockDim.x)
+    out[i] = (b && i < cout) ? to_f(b[i]) : 0.f;
+}
+
+void launch_bias(hipStream_t s, int dtype, const void* b, float* out,
+                 int cout, int cout_p) {
+  if (dtype == 0)
+    k_bias<float><<<1, 256, 0, s>>>((const float*)b, out, cout, cout_p);
+  else if (dtype == 1)
+    k_bias<_Float16><<<1, 256, 0, s>>>((const _Float16*)b, out, cout, cout_p);
+  else
+    k_bias<bf16_t><<<1, 256, 0, s>>>((const bf16_t*)b, out, cout, cout_p);
+}
+
+// Per-image kept counts of an ascending pixel list (binary search of the
+// image boundaries).
+__global__ void k_density(const int* act, const u64* n_act, int64_t hw,
+                          int batch, u64* out) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= batch) return;
+  const int64_t n = (int64_t)*n_act;
+  auto lower = [&](int64_t key) {
+    int64_t lo = 0, hi = n;
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) / 2;
+      if ((int64_t)act[mid] < key) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+  };
+  out[b] = (u64)(lower((int64_t)(b + 1) * hw) - lower((int64_t)b * hw));
+}
+
+void launch_density(hipStream_t s, const int* act, const u64* n_act,
+                    int64_t hw, int batch, u64* out) {
+  k_density<<<(batch + 63) / 64, 64, 0, s>>>(act, n_act, hw, batch, out);
+}
+
+}  // namespace st

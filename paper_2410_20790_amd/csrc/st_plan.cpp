@@ -1,0 +1,224 @@
+// Host-side planning of a diff-computation net: descriptor validation,
+// per-layer shapes and the workspace layout.  No HIP call is made here, so
+// the graph checks of st_create_net run on any host.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "st_internal.h"
+
+namespace {
+thread_local std::string g_create_err;
+
+int esize_of(int dtype) { return dtype == ST_F32 ? 4 : 2; }
+
+// GEMM reduction chunk: must match the kernel's stage depth per dtype.
+int gemm_chunk(int dtype) { return dtype == ST_F32 ? 16 : 64; }
+
+int64_t out_size(int64_t n, int k, int s, int p) {
+  return (n + 2 * (int64_t)p - k) / s + 1;
+}
+
+struct Alloc {
+  size_t top = 0;
+  size_t take(size_t bytes) {
+    size_t off = st::round_up((int64_t)top, (int64_t)st::kAlign);
+    top = off + bytes;
+    return off;
+  }
+};
+}  // namespace
+
+namespace st {
+st_status fail(st_net* net, st_status s, const std::string& msg) {
+  if (net) net->err = msg; else g_create_err = msg;
+  return s;
+}
+}  // namespace st
+
+using namespace st;
+
+static st_status create_fail(st_status s, const std::string& msg) {
+  g_create_err = msg;
+  return s;
+}
+
+extern "C" st_status st_create_net(const st_layer_desc* layers,
+                                   int32_t n_layers, int32_t batch,
+                                   int32_t in_h, int32_t in_w, int32_t in_c,
+                                   int32_t dtype, st_net** out) {
+  if (!out) return create_fail(ST_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!layers || n_layers < 1)
+    return create_fail(ST_ERR_INVALID_ARG, "no layers");
+  if (batch < 1 || in_h < 1 || in_w < 1 || in_c < 1)
+    return create_fail(ST_ERR_INVALID_ARG, "input shape must be positive");
+  if (dtype != ST_F32 && dtype != ST_F16 && dtype != ST_BF16)
+    return create_fail(ST_ERR_INVALID_ARG, "unknown dtype");
+  if ((int64_t)batch * in_h * in_w >= (int64_t)1 << 31)
+    return create_fail(ST_ERR_INVALID_ARG, "input grid exceeds 2^31 pixels");
+
+  st_net* net = new (std::nothrow) st_net();
+  if (!net) return create_fail(ST_ERR_INVALID_ARG, "out of host memory");
+  net->dtype = dtype;
+  net->esize = esize_of(dtype);
+  net->N = batch; net->H = in_h; net->W = in_w; net->C = in_c;
+  net->layers.resize(n_layers);
+  net->tensors.resize(n_layers + 1);
+
+  auto bad = [&](st_status s, int i, const std::string& m) {
+    delete net;
+    return create_fail(s, "layer " + std::to_string(i) + ": " + m);
+  };
+
+  TensorPlan& t0 = net->tensors[0];
+  t0.N = batch; t0.H = in_h; t0.W = in_w; t0.C = in_c;
+  t0.Cp = (int)round_up(in_c, kChanAlign);
+  t0.grid = (int64_t)batch * in_h * in_w;
+  const int kc = gemm_chunk(dtype);
+
+  for (int i = 0; i < n_layers; ++i) {
+    const st_layer_desc& d = layers[i];
+    LayerPlan& L = net->layers[i];
+    L.d = d;
+    if (d.src < -1 || d.src >= i)
+      return bad(ST_ERR_INVALID_ARG, i, "src must be -1 or an earlier layer");
+    const TensorPlan& in = net->tensors[d.src + 1];
+    if (d.c_in != in.C)
+      return bad(ST_ERR_INVALID_ARG, i, "c_in does not match the producer");
+    if (d.c_out < 1) return bad(ST_ERR_INVALID_ARG, i, "c_out < 1");
+    if (d.k_h < 1 || d.k_w < 1 || d.s_h < 1 || d.s_w < 1 || d.p_h < 0 ||
+        d.p_w < 0)
+      return bad(ST_ERR_INVALID_ARG, i, "bad conv geometry");
+    if (d.groups < 1) return bad(ST_ERR_INVALID_ARG, i, "groups < 1");
+    if (d.groups != 1 && !(d.groups == d.c_in && d.groups == d.c_out))
+      return bad(ST_ERR_UNSUPPORTED, i,
+                 "only dense (groups=1) and depthwise convolutions");
+    if (d.act < ST_ACT_NONE || d.act > ST_ACT_SILU)
+      return bad(ST_ERR_INVALID_ARG, i, "unknown activation");
+    if (d.se_mid != 0 || d.se_w1 || d.se_w2)
+      return bad(ST_ERR_UNSUPPORTED, i, "squeeze-excitation");
+    if (!d.weight) return bad(ST_ERR_INVALID_ARG, i, "weight is NULL");
+    L.Hi = in.H; L.Wi = in.W;
+    int64_t ho = out_size(in.H, d.k_h, d.s_h, d.p_h);
+    int64_t wo = out_size(in.W, d.k_w, d.s_w, d.p_w);
+    if (ho < 1 || wo < 1)
+      return bad(ST_ERR_INVALID_ARG, i, "empty conv output");
+    L.Ho = (int)ho; L.Wo = (int)wo;
+    L.pool = d.pool_k_h > 0 || d.pool_k_w > 0;
+    if (L.pool) {
+      if (d.pool_k_h < 1 || d.pool_k_w < 1 || d.pool_s_h < 1 ||
+          d.pool_s_w < 1 || d.pool_p_h < 0 || d.pool_p_w < 0 ||
+          2 * d.pool_p_h > d.pool_k_h || 2 * d.pool_p_w > d.pool_k_w)
+        return bad(ST_ERR_INVALID_ARG, i, "bad pool geometry");
+      int64_t hp = out_size(ho, d.pool_k_h, d.pool_s_h, d.pool_p_h);
+      int64_t wp = out_size(wo, d.pool_k_w, d.pool_s_w, d.pool_p_w);
+      if (hp < 1 || wp < 1)
+        return bad(ST_ERR_INVALID_ARG, i, "empty pool output");
+      L.Hp = (int)hp; L.Wp = (int)wp;
+    } else {
+      L.Hp = L.Ho; L.Wp = L.Wo;
+    }
+    if (d.residual_src != -2) {
+      if (d.residual_src < -1 || d.residual_src >= i)
+        return bad(ST_ERR_INVALID_ARG, i, "bad residual_src");
+      const TensorPlan& r = net->tensors[d.residual_src + 1];
+      if (r.H != L.Ho || r.W != L.Wo || r.C != d.c_out)
+        return bad(ST_ERR_INVALID_ARG, i,
+                   "residual shape differs from the conv output");
+    }
+    L.K = d.k_h * d.k_w;
+    if (L.K > 64)
+      return bad(ST_ERR_UNSUPPORTED, i, "kernels with more than 64 offsets");
+    L.cin_p = in.Cp;
+    L.cout_p = (int)round_up(d.c_out, kChanAlign);
+    L.dw = d.groups > 1;
+    L.ktot = (int64_t)L.K * L.cin_p;
+    L.ktot_p = round_up(L.ktot, kc);
+    L.conv_grid = (int64_t)batch * L.Ho * L.Wo;
+    L.stateful = d.act != ST_ACT_NONE || L.pool || i == n_layers - 1;
+    L.mode = L.pool ? kModeDefer : (L.stateful ? kModeState : kModeLinear);
+    L.ident = d.k_h == 1 && d.k_w == 1 && d.s_h == 1 && d.s_w == 1 &&
+              d.p_h == 0 && d.p_w == 0 && d.residual_src == -2;
+    TensorPlan& t = net->tensors[i + 1];
+    t.N = batch; t.H = L.Hp; t.W = L.Wp; t.C = d.c_out; t.Cp = L.cout_p;
+    t.grid = (int64_t)batch * L.Hp * L.Wp;
+    if (L.conv_grid >= ((int64_t)1 << 31) / std::max(L.K, 1))
+      return bad(ST_ERR_INVALID_ARG, i, "rulebook exceeds 2^31 entries");
+  }
+
+  // ---- workspace layout
+  Alloc a;
+  const int L_n = n_layers;
+  net->n_counters = 2 * (L_n + 1) + 2 * L_n;
+  net->off_cnt = a.take(sizeof(uint64_t) * net->n_counters);
+  net->off_dens = a.take(sizeof(uint64_t) * batch);
+  net->off_tiles = a.take(sizeof(uint32_t) * kMaxTiles);
+  net->off_xhat = a.take((size_t)t0.grid * in_c * net->esize);
+  int64_t max_grid = t0.grid;
+  for (int t = 0; t <= L_n; ++t) {
+    TensorPlan& T = net->tensors[t];
+    T.cnt_rows = 2 * t;
+    T.cnt_act = 2 * t + 1;
+    T.off_rows = a.take((size_t)T.grid * T.Cp * net->esize);
+    T.off_rowpix = a.take(sizeof(int32_t) * T.grid);
+    T.off_act = a.take(sizeof(int32_t) * T.grid);
+    T.off_map = a.take(sizeof(int32_t) * T.grid);
+    T.off_rowmax = a.take(sizeof(uint32_t) * T.grid);
+    max_grid = std::max(max_grid, T.grid);
+  }
+  int n_cleanup = L_n + 1;
+  for (int i = 0; i < L_n; ++i) {
+    LayerPlan& L = net->layers[i];
+    TensorPlan& T = net->tensors[i + 1];
+    L.cnt_pairs = 2 * (L_n + 1) + i;
+    max_grid = std::max(max_grid, L.conv_grid);
+    if (L.pool) {
+      L.cnt_O = 2 * (L_n + 1) + L_n + i;
+      L.off_O = a.take(sizeof(int32_t) * L.conv_grid);
+      L.off_Mo = a.take(sizeof(int32_t) * L.conv_grid);
+      L.off_dP = a.take(sizeof(float) * L.conv_grid * L.cout_p);
+      ++n_cleanup;
+    } else {
+      L.cnt_O = T.cnt_rows;
+      L.off_O = T.off_rowpix;
+      L.off_Mo = T.off_map;
+    }
+    L.off_nbr = a.take(sizeof(int32_t) * L.conv_grid * L.K);
+    if (L.stateful) L.off_P = a.take(sizeof(float) * L.conv_grid * L.cout_p);
+    if (L.dw)
+      L.off_w = a.take(sizeof(float) * L.K * L.cout_p);
+    else
+      L.off_w = a.take((size_t)L.cout_p * L.ktot_p * net->esize);
+    L.off_bias = a.take(sizeof(float) * L.cout_p);
+  }
+  net->max_grid = max_grid;
+  net->off_flags = a.take(round_up(max_grid, 16));
+  net->n_cleanup = n_cleanup;
+  net->off_cleanup = a.take(32 * n_cleanup);
+  net->ws_bytes = round_up(a.top, kAlign);
+  *out = net;
+  return ST_OK;
+}
+
+extern "C" st_status st_workspace_bytes(const st_net* net, uint64_t* bytes) {
+  if (!net || !bytes) return create_fail(ST_ERR_INVALID_ARG, "NULL argument");
+  *bytes = net->ws_bytes;
+  return ST_OK;
+}
+
+extern "C" st_status st_tensor_shape(const st_net* net, int32_t layer,
+                                     int32_t* nhwc) {
+  if (!net || !nhwc) return create_fail(ST_ERR_INVALID_ARG, "NULL argument");
+  if (layer < -1 || layer >= (int)net->layers.size())
+    return create_fail(ST_ERR_INVALID_ARG, "layer out of range");
+  const TensorPlan& t = net->tensors[layer + 1];
+  nhwc[0] = t.N; nhwc[1] = t.H; nhwc[2] = t.W; nhwc[3] = t.C;
+  return ST_OK;
+}
+
+extern "C" const char* st_last_error(const st_net* net) {
+  return net ? net->err.c_str() : g_create_err.c_str();
+}

@@ -1,0 +1,110 @@
+"""Torch-memory wrapper around the C ABI: owns the device weights and the
+workspace as torch tensors and passes their addresses and the current HIP
+stream to the library.  No computation happens here."""
+
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import binding as B
+
+TORCH_DTYPES = {"f32": torch.float32, "f16": torch.float16,
+                "bf16": torch.bfloat16}
+
+
+def layer_desc(L, w_ptr: int, b_ptr: Optional[int]) -> B.st_layer_desc:
+    """Descriptor of one layer from an object with the LayerSpec fields
+    (src, residual_src, c_in, c_out, groups, k, s, p, act, pool_k, pool_s,
+    pool_p, se_mid)."""
+    return B.st_layer_desc(
+        src=L.src, residual_src=L.residual_src, c_in=L.c_in, c_out=L.c_out,
+        groups=L.groups, k_h=L.k[0], k_w=L.k[1], s_h=L.s[0], s_w=L.s[1],
+        p_h=L.p[0], p_w=L.p[1], act=L.act, pool_k_h=L.pool_k[0],
+        pool_k_w=L.pool_k[1], pool_s_h=L.pool_s[0], pool_s_w=L.pool_s[1],
+        pool_p_h=L.pool_p[0], pool_p_w=L.pool_p[1], se_mid=L.se_mid,
+        weight=w_ptr, bias=b_ptr)
+
+
+class SparseTemNet:
+    """One diff encoder: reference frame via ``encode_reference``, then
+    diff frames via ``encode_diff`` (see include/sparsetem.h)."""
+
+    def __init__(self, layers: Sequence, batch: int, H: int, W: int, C: int,
+                 dtype: str = "f32", device="cuda"):
+        self.dtype = dtype
+        self.tdtype = TORCH_DTYPES[dtype]
+        self.device = torch.device(device)
+        self.n_layers = len(layers)
+        self.in_shape = (batch, H, W, C)
+        self._w, self._b, descs = [], [], []
+        for L in layers:
+            w = torch.as_tensor(np.asarray(L.weight)).to(
+                self.device, self.tdtype).contiguous()
+            b = None
+            if L.bias is not None:
+                b = torch.as_tensor(np.asarray(L.bias)).to(
+                    self.device, self.tdtype).contiguous()
+            self._w.append(w)
+            self._b.append(b)
+            descs.append(layer_desc(L, w.data_ptr(),
+                                    None if b is None else b.data_ptr()))
+        self.handle = B.st_create_net(descs, batch, H, W, C,
+                                      B.DTYPE_CODES[dtype])
+        self.ws_bytes = B.st_workspace_bytes(self.handle)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8,
+                              device=self.device)
+        B.st_bind_workspace(self.handle, self.ws.data_ptr(), self.ws_bytes,
+                            self._stream())
+        torch.cuda.current_stream(self.device).synchronize()
+        self.out_shape = B.st_tensor_shape(self.handle, self.n_layers - 1)
+
+    def _stream(self) -> int:
+        return torch.cuda.current_stream(self.device).cuda_stream
+
+    def _check_frame(self, frame):
+        if (frame.device != self.device or frame.dtype != self.tdtype
+                or tuple(frame.shape) != self.in_shape
+                or not frame.is_contiguous()):
+            raise ValueError("frame must be a contiguous NHWC device tensor "
+                             f"{self.in_shape} of {self.tdtype}")
+
+    def new_output(self):
+        return torch.empty(self.out_shape, dtype=torch.float32,
+                           device=self.device)
+
+    def encode_reference(self, frame, out=None):
+        self._check_frame(frame)
+        out = self.new_output() if out is None else out
+        B.st_encode_reference(self.handle, frame.data_ptr(), out.data_ptr(),
+                              self._stream())
+        return out
+
+    def encode_diff(self, frame, thr, out=None, write_out=True):
+        self._check_frame(frame)
+        if len(thr) != self.n_layers + 1:
+            raise ValueError("thr needs n_layers + 1 entries")
+        if write_out and out is None:
+            out = self.new_output()
+        B.st_encode_diff(self.handle, frame.data_ptr(), thr,
+                         out.data_ptr() if write_out else None,
+                         self._stream())
+        return out
+
+    def density(self, layer: int, image: int = -1) -> float:
+        return B.st_layer_density(self.handle, layer, image)
+
+    def tensor_shape(self, layer: int):
+        return B.st_tensor_shape(self.handle, layer)
+
+    def close(self):
+        if self.handle:
+            torch.cuda.current_stream(self.device).synchronize()
+            B.st_destroy_net(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

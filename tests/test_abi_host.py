@@ -1,0 +1,171 @@
+"""Host-only checks of the C ABI: the library loads, exports every entry
+point the header declares, validates layer graphs and sizes the workspace
+without touching a GPU."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2410_20790_amd import binding as B
+from workloads import (crnn_vgg_net, depthwise_test_net, resnet50_net,
+                       resnet_mini_net, toy_net)
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sparsetem.h")
+
+
+def header_symbols():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(st_[a-z_]+)\s*\(", txt)))
+
+
+def test_header_declares_the_binding_names():
+    assert header_symbols() == sorted(B.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(B.LIB_PATH)
+    for name in header_symbols():
+        assert hasattr(lib, name), name
+
+
+def descs(net, fake_ptr=0x1000):
+    from paper_2410_20790_amd.net import layer_desc
+    return [layer_desc(L, fake_ptr, fake_ptr) for L in net.layers]
+
+
+def create(net, **over):
+    d = descs(net)
+    for i, kv in over.get("patch", {}).items():
+        for k, v in kv.items():
+            setattr(d[i], k, v)
+    return B.st_create_net(d, over.get("batch", net.batch),
+                           over.get("H", net.H), over.get("W", net.W),
+                           over.get("C", net.C),
+                           over.get("dtype", B.DTYPE_CODES[net.dtype]))
+
+
+@pytest.mark.parametrize("mk", [toy_net, crnn_vgg_net, resnet_mini_net,
+                                depthwise_test_net])
+def test_create_valid_nets(mk):
+    net = mk()
+    h = create(net)
+    try:
+        assert B.st_workspace_bytes(h) > 0
+        shp = B.st_tensor_shape(h, len(net.layers) - 1)
+        assert shp[0] == net.batch and shp[3] == net.layers[-1].c_out
+        assert B.st_tensor_shape(h, -1) == (net.batch, net.H, net.W, net.C)
+    finally:
+        B.st_destroy_net(h)
+
+
+def test_output_shapes_match_geometry():
+    net = crnn_vgg_net()
+    h = create(net)
+    try:
+        assert B.st_tensor_shape(h, 0) == (1, 16, 64, 64)
+        assert B.st_tensor_shape(h, 1) == (1, 8, 32, 128)
+        assert B.st_tensor_shape(h, 3) == (1, 4, 32, 256)
+        assert B.st_tensor_shape(h, 6) == (1, 2, 32, 512)
+    finally:
+        B.st_destroy_net(h)
+
+
+def test_resnet50_workspace_fits_one_gpu():
+    net_shape_only = resnet50_net.__wrapped__ if hasattr(
+        resnet50_net, "__wrapped__") else None
+    net = resnet50_net(H=1024, W=2048)
+    h = create(net)
+    try:
+        shp = B.st_tensor_shape(h, len(net.layers) - 1)
+        assert shp == (1, 32, 64, 2048)
+        ws = B.st_workspace_bytes(h)
+        # f32 pre-activation state alone is ~1.6 GB; everything < 8 GB
+        assert 1.6e9 < ws < 8e9
+    finally:
+        B.st_destroy_net(h)
+
+
+@pytest.mark.parametrize("patch,status", [
+    ({0: {"src": 0}}, B.ST_ERR_INVALID_ARG),          # self reference
+    ({1: {"src": 5}}, B.ST_ERR_INVALID_ARG),          # forward reference
+    ({1: {"c_in": 7}}, B.ST_ERR_INVALID_ARG),         # channel mismatch
+    ({0: {"k_h": 0}}, B.ST_ERR_INVALID_ARG),
+    ({0: {"s_w": 0}}, B.ST_ERR_INVALID_ARG),
+    ({0: {"p_h": -1}}, B.ST_ERR_INVALID_ARG),
+    ({0: {"act": 9}}, B.ST_ERR_INVALID_ARG),
+    ({0: {"groups": 4}}, B.ST_ERR_UNSUPPORTED),       # grouped, not depthwise
+    ({0: {"se_mid": 4}}, B.ST_ERR_UNSUPPORTED),
+    ({0: {"weight": None}}, B.ST_ERR_INVALID_ARG),
+    ({1: {"residual_src": -1}}, B.ST_ERR_INVALID_ARG),  # 16 ch vs 32 out
+    ({0: {"pool_k_h": 2, "pool_k_w": 2, "pool_s_h": 2, "pool_s_w": 2,
+          "pool_p_h": 2, "pool_p_w": 0}}, B.ST_ERR_INVALID_ARG),
+    ({0: {"k_h": 9, "k_w": 9, "p_h": 4, "p_w": 4}}, B.ST_ERR_UNSUPPORTED),
+])
+def test_invalid_descriptors(patch, status):
+    with pytest.raises(B.StError) as e:
+        create(toy_net(), patch=patch)
+    assert e.value.status == status
+    assert B.st_last_error()
+
+
+@pytest.mark.parametrize("kw,status", [
+    ({"batch": 0}, B.ST_ERR_INVALID_ARG),
+    ({"H": 0}, B.ST_ERR_INVALID_ARG),
+    ({"C": 3}, B.ST_ERR_INVALID_ARG),
+    ({"dtype": 7}, B.ST_ERR_INVALID_ARG),
+    ({"H": 1, "W": 1}, B.ST_ERR_INVALID_ARG),   # fine conv, but see below
+])
+def test_invalid_shapes(kw, status):
+    if kw == {"H": 1, "W": 1}:
+        # a 1x1 input is still a valid 3x3/pad-1 conv input
+        h = create(toy_net(), **kw)
+        B.st_destroy_net(h)
+        return
+    with pytest.raises(B.StError) as e:
+        create(toy_net(), **kw)
+    assert e.value.status == status
+
+
+def test_empty_output_rejected():
+    net = toy_net(H=2, W=2)
+    with pytest.raises(B.StError) as e:
+        create(net, patch={0: {"p_h": 0, "p_w": 0}})
+    assert e.value.status == B.ST_ERR_INVALID_ARG
+
+
+def test_null_arguments():
+    lib = B.library()
+    out = ctypes.c_void_p()
+    assert lib.st_create_net(None, 1, 1, 4, 4, 16, 0,
+                             ctypes.byref(out)) == B.ST_ERR_INVALID_ARG
+    assert lib.st_workspace_bytes(None, None) == B.ST_ERR_INVALID_ARG
+    h = create(toy_net())
+    try:
+        # unbound workspace: encodes report a state error, not a crash
+        thr = (ctypes.c_float * 3)(0, 0, 0)
+        assert lib.st_encode_reference(h, 0x1000, None, None) == B.ST_ERR_STATE
+        assert lib.st_encode_diff(h, 0x1000, thr, None, None) == B.ST_ERR_STATE
+        assert lib.st_bind_workspace(h, None, 1 << 20, None) == \
+            B.ST_ERR_INVALID_ARG
+        assert lib.st_bind_workspace(h, 0x1001, 1 << 40, None) == \
+            B.ST_ERR_INVALID_ARG
+        assert lib.st_bind_workspace(h, 0x1000, 16, None) == B.ST_ERR_WORKSPACE
+        assert "small" in B.st_last_error(h)
+    finally:
+        B.st_destroy_net(h)
+
+
+def test_workspace_scales_with_batch():
+    a = create(toy_net(batch=1))
+    b = create(toy_net(batch=4))
+    try:
+        wa, wb = B.st_workspace_bytes(a), B.st_workspace_bytes(b)
+        assert 3.5 * wa < wb < 4.5 * wa
+    finally:
+        B.st_destroy_net(a)
+        B.st_destroy_net(b)

@@ -1,0 +1,279 @@
+"""GPU parity: the HIP path (called through the C ABI) against the CPU
+oracle on identical seeded inputs, after every frame of a chunk.
+
+Exact: frame-delta masks and rows, candidate lists, kept lists (outside the
+rounding band), rulebooks and pair counts.  Within tolerance (1e-4 relative
+for f32, 2e-2 for f16/bf16, per tensor against the oracle's largest
+magnitude): emitted delta rows, pre-activation state, network output.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2410_20790_amd import SparseTemNet
+from paper_2410_20790_amd import binding as B
+from parity_util import RTOL, make_pair, rel, run_chunk, say, to_dev
+from workloads import (crnn_vgg_net, depthwise_test_net, driving_video,
+                       random_sparse_video, resnet50_net, resnet_mini_net,
+                       textline_video, toy_net, toy_video)
+
+pytestmark = pytest.mark.gpu
+
+
+# ----------------------------------------------------------- toy encoder
+
+@pytest.mark.parametrize("thr", [0.0, 0.05])
+def test_toy_chunk(thr):
+    """One 3x3 conv + ReLU + 1x1 conv on a 4-frame 64x64x16 chunk with 10%
+    of sites redrawn per frame in 8x8 patches."""
+    run_chunk(toy_net(), toy_video(seed=0, n_frames=4), thr, f"toy thr={thr}")
+
+
+def test_toy_ragged_batch():
+    """Batch of 2 on a 20x28 map: tile tails and an image boundary."""
+    net = toy_net(H=20, W=28, batch=2)
+    run_chunk(net, random_sparse_video(5, 4, 2, 20, 28, 16, 0.1), 0.0,
+              "toy ragged")
+
+
+def test_toy_single_pixel_amplification():
+    """One changed interior pixel reaches nine 3x3 outputs (dense
+    amplification example); the 1x1 layer then sees those nine."""
+    net = toy_net(H=16, W=16)
+    f0 = np.random.default_rng(3).random((1, 16, 16, 16), dtype=np.float32)
+    f1 = f0.copy()
+    f1[0, 7, 9] += 0.5
+    o, g = run_chunk(net, [f0, f1], 0.0, "toy one pixel")
+    try:
+        assert len(B.st_debug_active(g.handle, -1)) == 1
+        pairs, act = B.st_debug_counters(g.handle, 2)
+        assert pairs[0] == 9
+        pix, _ = B.st_debug_candidates(g.handle, 0, 16)
+        assert len(pix) == 9
+    finally:
+        g.close()
+
+
+# --------------------------------------------------------- CRNN encoder
+
+@pytest.mark.parametrize("thr", [0.0, 0.02])
+def test_crnn_chunk(thr):
+    """CRNN-style VGG encoder at 32x128 (seven 3x3 convs, 2x2 and 2x1
+    pools) on a scrolling text line."""
+    net = crnn_vgg_net()
+    run_chunk(net, textline_video(seed=1, n_frames=5), thr, f"crnn thr={thr}",
+              max_band=4 if thr else 0)
+
+
+# ------------------------------------------------------- ResNet family
+
+@pytest.mark.parametrize("thr", [0.0, 0.05])
+def test_resnet_mini_f32(thr):
+    """7x7/2 stem, overlapping 3x3/2 pool, bottlenecks with strided 3x3,
+    downsample and identity shortcuts."""
+    net = resnet_mini_net()
+    run_chunk(net, random_sparse_video(6, 4, 1, 32, 48, 3, 0.08), thr,
+              f"resnet_mini thr={thr}", max_band=4 if thr else 0)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_resnet_mini_half(dtype):
+    net = resnet_mini_net(dtype=dtype, H=40, W=56)
+    run_chunk(net, random_sparse_video(8, 4, 1, 40, 56, 3, 0.08, dtype=dtype),
+              0.0, f"resnet_mini {dtype}")
+
+
+def test_resnet50_small_bf16():
+    """ResNet-50 (all 53 convs) at 64x128 in bf16, clustered changes."""
+    net = resnet50_net(H=64, W=128)
+    frames = driving_video(seed=2, n_frames=3, H=64, W=128, density=0.10,
+                           side=(8, 32))
+    run_chunk(net, frames, 0.0, "resnet50 64x128 bf16")
+
+
+# ------------------------------------------------------------ depthwise
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+def test_depthwise(dtype):
+    net = depthwise_test_net(dtype=dtype)
+    run_chunk(net, random_sparse_video(7, 4, 1, 24, 40, 16, 0.1, dtype=dtype),
+              0.0, f"depthwise {dtype}")
+
+
+# ----------------------------------------------------------- edge cases
+
+def test_zero_delta_leaves_everything_unchanged():
+    net = resnet_mini_net()
+    frames = random_sparse_video(11, 2, 1, 32, 48, 3, 0.1)
+    o, g = run_chunk(net, frames, 0.0, "zero delta warm-up")
+    try:
+        thr = [0.0] * (len(net.layers) + 1)
+        x = to_dev(frames[1], "f32")
+        out1 = g.encode_diff(x, thr)
+        P1 = {i: B.st_debug_state(g.handle, i, o.P[i].shape) for i in o.P}
+        say("[gpu] zero delta: repeat frame")
+        out2 = g.encode_diff(x, thr)
+        torch.cuda.synchronize()
+        assert torch.equal(out1, out2)
+        _, act = B.st_debug_counters(g.handle, len(net.layers))
+        assert (act == 0).all()
+        for i in o.P:
+            np.testing.assert_array_equal(
+                B.st_debug_state(g.handle, i, o.P[i].shape), P1[i])
+    finally:
+        g.close()
+
+
+def test_negative_threshold_reproduces_dense():
+    """thr < 0 keeps every site: the diff pass then touches every pixel and
+    must agree with a dense reference pass on the same frame."""
+    net = resnet_mini_net()
+    frames = random_sparse_video(12, 2, 1, 32, 48, 3, 0.05)
+    o, g = make_pair(net)
+    g2 = SparseTemNet(net.layers, 1, 32, 48, 3, "f32")
+    try:
+        g.encode_reference(to_dev(frames[0], "f32"))
+        out = g.encode_diff(to_dev(frames[1], "f32"),
+                            [-1.0] * (len(net.layers) + 1))
+        dense = g2.encode_reference(to_dev(frames[1], "f32"))
+        torch.cuda.synchronize()
+        for t in range(len(net.layers) + 1):
+            assert g.density(t - 1) == 1.0
+        assert rel(out.cpu().numpy(), dense.cpu().numpy()) < 1e-4
+    finally:
+        g.close()
+        g2.close()
+
+
+def test_threshold_zero_matches_dense_pass_over_chunk():
+    """Linearity invariant on the GPU alone: at threshold 0 every diff
+    output equals the dense pass of that frame."""
+    net = crnn_vgg_net()
+    frames = textline_video(seed=4, n_frames=6)
+    g = SparseTemNet(net.layers, 1, 32, 128, 1, "f32")
+    g2 = SparseTemNet(net.layers, 1, 32, 128, 1, "f32")
+    try:
+        g.encode_reference(to_dev(frames[0], "f32"))
+        for t in range(1, 6):
+            out = g.encode_diff(to_dev(frames[t], "f32"), [0.0] * 8)
+            dense = g2.encode_reference(to_dev(frames[t], "f32"))
+            torch.cuda.synchronize()
+            assert rel(out.cpu().numpy(), dense.cpu().numpy()) < 1e-4
+    finally:
+        g.close()
+        g2.close()
+
+
+def test_repeat_runs_are_bitwise_identical():
+    net = resnet_mini_net()
+    frames = random_sparse_video(13, 4, 1, 32, 48, 3, 0.1)
+    outs = []
+    for rep in range(2):
+        g = SparseTemNet(net.layers, 1, 32, 48, 3, "f32")
+        try:
+            g.encode_reference(to_dev(frames[0], "f32"))
+            res = []
+            for t in range(1, 4):
+                res.append(g.encode_diff(to_dev(frames[t], "f32"),
+                                         [0.01] * (len(net.layers) + 1)).cpu())
+            outs.append(res)
+        finally:
+            g.close()
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
+def test_api_errors_on_gpu():
+    net = toy_net()
+    g = SparseTemNet(net.layers, 1, 64, 64, 16, "f32")
+    try:
+        x = to_dev(toy_video(n_frames=1)[0], "f32")
+        with pytest.raises(B.StError) as e:
+            g.encode_diff(x, [0.0] * 3)
+        assert e.value.status == B.ST_ERR_STATE
+        g.encode_reference(x)
+        with pytest.raises(B.StError) as e:
+            g.encode_diff(x, [0.0, float("nan"), 0.0])
+        assert e.value.status == B.ST_ERR_INVALID_ARG
+        with pytest.raises(B.StError):
+            g.density(5)
+        assert g.density(-1) == 1.0   # reference pass: every site active
+    finally:
+        g.close()
+
+
+def test_per_image_density():
+    net = toy_net(H=16, W=16, batch=3)
+    frames = random_sparse_video(14, 2, 3, 16, 16, 16, 0.0)
+    f1 = frames[0].copy()
+    f1[1, :4] += 1.0        # image 1: 4 of 16 rows change
+    g = SparseTemNet(net.layers, 3, 16, 16, 16, "f32")
+    try:
+        g.encode_reference(to_dev(frames[0], "f32"))
+        g.encode_diff(to_dev(f1, "f32"), [0.0] * 3)
+        assert g.density(-1, 0) == 0.0
+        assert g.density(-1, 1) == 0.25
+        assert g.density(-1, 2) == 0.0
+        assert abs(g.density(-1) - 0.25 / 3) < 1e-7
+    finally:
+        g.close()
+
+
+# ------------------------------------------------ full-size workloads
+
+def test_resnet50_full_size_first_layer_exact():
+    """ResNet-50 at 1024x2048 bf16 with 10% clustered change, in the launch
+    configuration the benchmark times: the frame-delta mask and the stem's
+    rulebook must equal the oracle's bit for bit, its state within the bf16
+    tolerance; the oracle runs the stem alone (its output needs no deeper
+    layer)."""
+    net = resnet50_net()
+    frames = driving_video(seed=0, n_frames=2, density=0.10)
+    stem = [net.layers[0]]
+    o = oracle.OracleNet(stem, 1, 1024, 2048, 3, "bf16")
+    say("[gpu] resnet50 full: oracle stem")
+    o.encode_reference(frames[0])
+    o.encode_diff(frames[1], [0.0, 0.0])
+    g = SparseTemNet(net.layers, 1, 1024, 2048, 3, "bf16")
+    try:
+        say("[gpu] resnet50 full: gpu")
+        g.encode_reference(to_dev(frames[0], "bf16"))
+        g.encode_diff(to_dev(frames[1], "bf16"),
+                      [0.0] * (len(net.layers) + 1), write_out=False)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(B.st_debug_active(g.handle, -1),
+                                      o.last["tensors"][0]["pix"])
+        R = B.st_debug_rulebook(g.handle, 0)
+        np.testing.assert_array_equal(R.astype(np.int64),
+                                      o.last["layers"][0]["rulebook"])
+        P0 = B.st_debug_state(g.handle, 0, o.P[0].shape)
+        assert rel(P0, o.P[0]) < RTOL["bf16"]
+        pix, _ = B.st_debug_candidates(g.handle, 0, 64)
+        np.testing.assert_array_equal(pix, o.last["tensors"][1]["cand"])
+        d0 = g.density(-1)
+        assert 0.09 < d0 < 0.2
+    finally:
+        g.close()
+
+
+def test_resnet50_full_size_linearity():
+    """At threshold 0 the diff output of a full-size frame equals the dense
+    pass of that frame (property that holds at any size)."""
+    net = resnet50_net()
+    frames = driving_video(seed=1, n_frames=3, density=0.10)
+    g = SparseTemNet(net.layers, 1, 1024, 2048, 3, "bf16")
+    g2 = SparseTemNet(net.layers, 1, 1024, 2048, 3, "bf16")
+    try:
+        say("[gpu] resnet50 full linearity")
+        g.encode_reference(to_dev(frames[0], "bf16"))
+        for t in (1, 2):
+            out = g.encode_diff(to_dev(frames[t], "bf16"),
+                                [0.0] * (len(net.layers) + 1))
+        dense = g2.encode_reference(to_dev(frames[2], "bf16"))
+        torch.cuda.synchronize()
+        assert rel(out.cpu().numpy(), dense.cpu().numpy()) < 2e-2
+    finally:
+        g.close()
+        g2.close()
