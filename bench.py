@@ -1,0 +1,385 @@
+#!/usr/bin/env python3
+"""Benchmark of the diff-computation encoder on one MI355X.
+
+One step = one diff frame through the whole hot path (frame-delta mask and
+compaction, and for every layer rulebook, gather-GEMM / depthwise conv with
+the fused state update and delta emission, pool handling, truncation), plus
+the dense network output, on synthetic temporally continuous video resident
+in HBM.  Default workload: ResNet-50 encoder, bf16 storage, 1024x2048x3
+frames, 10% of the sites re-drawn per frame in clustered rectangles,
+threshold 0 (exact).
+
+Prints one JSON line with diff-frames/s (value), algorithmic TFLOP/s,
+speedup over dense convolution of the same net (MIOpen through PyTorch, and
+the library's own dense pass), the roofline of the dominant kernel from HIP
+events recorded around every launch in a second timed pass, and the CPU
+oracle's rate on the host cores.
+"""
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("diff-frames/sec + effective TFLOP/s at 10% change density; "
+          "speedup vs dense")
+HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f16": 2500.0, "f32": 157.3}
+ESIZE = {"f32": 4, "f16": 2, "bf16": 2}
+
+
+def workload(name, density):
+    from workloads import (crnn_vgg_net, driving_video, resnet50_net,
+                           textline_video, toy_net, toy_video)
+    if name == "resnet50":
+        net = resnet50_net(H=1024, W=2048)
+        return dict(
+            net=net, desc=f"resnet50-bf16-1024x2048-density{density:g}",
+            frames=lambda n, H=1024, W=2048: driving_video(
+                seed=0, n_frames=n, H=H, W=W, density=density),
+            crop=(256, 512))
+    if name == "crnn":
+        net = crnn_vgg_net()
+        return dict(net=net, desc="crnn_vgg-f32-32x128-band7",
+                    frames=lambda n, H=32, W=128: textline_video(
+                        seed=0, n_frames=n, H=H, W=W),
+                    crop=None)
+    if name == "toy":
+        net = toy_net()
+        return dict(net=net, desc="toy-f32-64x64x16-density0.1",
+                    frames=lambda n, H=64, W=64: toy_video(
+                        seed=0, n_frames=n, H=H, W=W), crop=None)
+    raise SystemExit(f"unknown workload {name}")
+
+
+def dense_flops(net, shapes):
+    tot = 0
+    for i, L in enumerate(net.layers):
+        N, Ho, Wo = shapes[i]
+        tot += 2 * N * Ho * Wo * L.c_out * (L.c_in // L.groups) * \
+            L.k[0] * L.k[1]
+    return tot
+
+
+def conv_launch_bytes(L, c, es, mode):
+    """Algorithmic HBM bytes of one conv launch (gather-GEMM or depthwise)
+    with fused epilogue, from the frame's counters
+    c = (affected outputs, pairs, kept input rows, candidate rows, kept
+    rows, kept residual rows): every kept input row and the weights read
+    once, the neighbour table and output list read once, the f32 state read
+    and written and the delta written once per affected output row (or the
+    deferred f32 update written, for pooled layers), the residual rows read
+    once."""
+    nO, pairs, n_in, _, _, n_skip = (int(v) for v in c)
+    K = L.k[0] * L.k[1]
+    b = n_in * L.c_in * es + K * (L.c_in // L.groups) * L.c_out * es
+    b += nO * (K + 1) * 4
+    if mode == "state":
+        b += nO * L.c_out * (4 + 4 + es)
+    elif mode == "defer":
+        b += nO * L.c_out * 4
+    else:
+        b += nO * L.c_out * es
+    b += n_skip * L.c_out * es
+    return b
+
+
+def layer_mode(net, i):
+    L = net.layers[i]
+    if L.pool_k[0] > 0:
+        return "defer"
+    if L.act != 0 or i == len(net.layers) - 1:
+        return "state"
+    return "linear"
+
+
+def torch_dense_model(net, dtype):
+    import torch
+    import torch.nn.functional as F
+    tdt = {"f32": torch.float32, "f16": torch.float16,
+           "bf16": torch.bfloat16}[dtype]
+    Ws = [torch.as_tensor(L.weight).to("cuda", tdt).contiguous(
+        memory_format=torch.channels_last) for L in net.layers]
+    Bs = [torch.as_tensor(L.bias).to("cuda", tdt) for L in net.layers]
+
+    def fwd(x_nhwc):
+        acts = {-1: x_nhwc.permute(0, 3, 1, 2)}
+        for i, L in enumerate(net.layers):
+            y = F.conv2d(acts[L.src], Ws[i], Bs[i], L.s, L.p, 1, L.groups)
+            if L.residual_src != -2:
+                y = y + acts[L.residual_src]
+            if L.act == 1:
+                y = F.relu(y)
+            elif L.act == 2:
+                y = F.silu(y)
+            if L.pool_k[0] > 0:
+                y = F.max_pool2d(y, L.pool_k, L.pool_s, L.pool_p)
+            acts[i] = y
+        return acts[len(net.layers) - 1]
+    return fwd
+
+
+def time_gpu(fn, reps, warm=2):
+    import torch
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        torch.cuda.synchronize()
+        ts.append(a.elapsed_time(b))
+    return statistics.median(ts)
+
+
+def cpu_baseline(wl, net, thr_val):
+    """The oracle (numpy, fp64 accumulation) on the host cores, on a bounded
+    sample of the same workload: a spatial crop of the same synthetic video
+    (full frames when the workload is small), one untimed reference frame
+    and two timed diff frames; the rate is scaled to full frames by the
+    pixel ratio."""
+    import oracle
+    from threadpoolctl import threadpool_info
+    crop = wl["crop"]
+    frames = wl["frames"](3)
+    H, W = net.H, net.W
+    if crop:
+        h, w = crop
+        frames = [np.ascontiguousarray(f[:, :h, :w, :]) for f in frames]
+    else:
+        h, w = H, W
+    o = oracle.OracleNet(net.layers, net.batch, h, w, net.C, net.dtype)
+    o.encode_reference(frames[0])
+    thr = [thr_val] * (len(net.layers) + 1)
+    t0 = time.perf_counter()
+    dens = []
+    for t in (1, 2):
+        o.encode_diff(frames[t], thr)
+        dens.append(o.density(0))
+    dt = (time.perf_counter() - t0) / 2
+    scale = (h * w) / float(H * W)
+    threads = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
+    cpu = "unknown"
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                cpu = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": scale / dt, "unit": "diff-frames/s", "cores": threads,
+            "kind": "oracle",
+            "sample": (f"oracle diff pass on a {h}x{w} crop of the same video "
+                       f"(input density {np.mean(dens):.3f}), 2 diff frames "
+                       f"after an untimed reference, {dt:.2f} s/frame, rate "
+                       f"scaled by the pixel ratio {scale:g}"),
+            "cpu_model": cpu}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="resnet50",
+                    choices=["resnet50", "crnn", "toy"])
+    ap.add_argument("--density", type=float, default=0.10)
+    ap.add_argument("--thr", type=float, default=0.0)
+    ap.add_argument("--profile-steps", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(independent streams shard by image; see the design notes). "
+              "Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2410_20790_amd import SparseTemNet
+    from paper_2410_20790_amd import binding as B
+
+    wl = workload(args.workload, args.density)
+    net = wl["net"]
+    dt = net.dtype
+    es = ESIZE[dt]
+    K, W, KP = args.steps, args.warmup, args.profile_steps
+    t_gen = time.perf_counter()
+    frames_np = wl["frames"](1 + W + K + KP)
+    t_gen = time.perf_counter() - t_gen
+    tdt = {"f32": torch.float32, "f16": torch.float16,
+           "bf16": torch.bfloat16}[dt]
+    frames = [torch.from_numpy(f).to("cuda", tdt).contiguous()
+              for f in frames_np]
+    del frames_np
+    g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt)
+    L_n = len(net.layers)
+    thr = [args.thr] * (L_n + 1)
+    out = g.new_output()
+    conv_grid = []
+    for i, L in enumerate(net.layers):
+        Hi, Wi = ((net.H, net.W) if L.src < 0 else
+                  g.tensor_shape(L.src)[1:3])
+        Ho = (Hi + 2 * L.p[0] - L.k[0]) // L.s[0] + 1
+        Wo = (Wi + 2 * L.p[1] - L.k[1]) // L.s[1] + 1
+        conv_grid.append((net.batch, Ho, Wo))
+    dflops = dense_flops(net, conv_grid)
+
+    # reference frame + warm-up
+    g.encode_reference(frames[0], out=out)
+    fi = 1
+    for _ in range(W):
+        g.encode_diff(frames[fi], thr, out=out)
+        fi += 1
+    torch.cuda.synchronize()
+
+    # ---- timed region: K diff frames, nothing else
+    s_ev = torch.cuda.Event(enable_timing=True)
+    e_ev = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    s_ev.record()
+    for _ in range(K):
+        g.encode_diff(frames[fi], thr, out=out)
+        fi += 1
+    e_ev.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1000.0 / K
+    ev_ms = s_ev.elapsed_time(e_ev) / K
+    dens0 = g.density(-1)
+
+    # ---- second timed pass with an event pair around every launch
+    B.st_profile_begin(g.handle, KP * 1024, KP + 1)
+    torch.cuda.synchronize()
+    tp = time.perf_counter()
+    for _ in range(KP):
+        g.encode_diff(frames[fi], thr, out=out)
+        fi += 1
+    torch.cuda.synchronize()
+    prof_ms_step = (time.perf_counter() - tp) * 1000.0 / KP
+    recs, counts = B.st_profile_end(g.handle, L_n)
+    per_frame_flops = [
+        sum(2 * int(counts[f, j, 1]) * (L.c_in // L.groups) * L.c_out
+            for j, L in enumerate(net.layers)) for f in range(len(counts))]
+    alg_flops = float(np.mean(per_frame_flops))
+    classes = {}
+    for r in recs:
+        name = B.KERNEL_CLASSES[r["kernel"]]
+        c = classes.setdefault(name, {"launches": 0, "ms": 0.0, "bytes": 0.0,
+                                      "flops": 0.0})
+        c["launches"] += 1
+        c["ms"] += float(r["ms"])
+        f, j = int(r["frame"]), int(r["layer"])
+        if name in ("conv_gemm", "conv_dw") and f < len(counts):
+            L = net.layers[j]
+            c["bytes"] += conv_launch_bytes(L, counts[f, j], es,
+                                            layer_mode(net, j))
+            c["flops"] += 2.0 * counts[f, j, 1] * (L.c_in // L.groups) * \
+                L.c_out
+        elif name == "scan_mask":
+            c["bytes"] += net.batch * net.H * net.W * (2 * net.C * es + 1)
+        elif name == "scan_compact" and f < len(counts):
+            n0 = counts[f, 0, 2] if net.layers[0].src == -1 else 0
+            c["bytes"] += net.batch * net.H * net.W + n0 * (
+                3 * net.C * es + 12)
+    total_ms = sum(c["ms"] for c in classes.values())
+    kern = {}
+    for name, c in sorted(classes.items(), key=lambda kv: -kv[1]["ms"]):
+        e = {"launches": c["launches"],
+             "avg_us": 1000.0 * c["ms"] / c["launches"],
+             "share": c["ms"] / total_ms}
+        if c["bytes"]:
+            e["alg_GBps"] = c["bytes"] / (c["ms"] * 1e-3) / 1e9
+            e["hbm_frac"] = e["alg_GBps"] / HBM_PEAK_GBS
+        if c["flops"]:
+            e["alg_TFLOPs"] = c["flops"] / (c["ms"] * 1e-3) / 1e12
+            e["mfma_frac"] = e["alg_TFLOPs"] / MFMA_PEAK_TFLOPS[dt]
+        kern[name] = e
+    dom = max(classes, key=lambda k: classes[k]["ms"])
+    dc = classes[dom]
+    avg_s = dc["ms"] * 1e-3 / dc["launches"]
+    roof = None
+    if dc["bytes"] or dc["flops"]:
+        ai = dc["flops"] / max(dc["bytes"], 1.0)
+        ridge = MFMA_PEAK_TFLOPS[dt] * 1e12 / (HBM_PEAK_GBS * 1e9)
+        if dc["flops"] and ai > ridge:
+            ach = dc["flops"] / dc["launches"] / avg_s / 1e12
+            roof = {"bound": "mfma", "achieved": ach,
+                    "peak": MFMA_PEAK_TFLOPS[dt], "unit": "TFLOP/s",
+                    "frac": ach / MFMA_PEAK_TFLOPS[dt], "traffic": None}
+        else:
+            ach = dc["bytes"] / dc["launches"] / avg_s / 1e9
+            roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
+                    "traffic": None}
+        roof.update({"kernel": dom, "launches": dc["launches"],
+                     "avg_launch_us": avg_s * 1e6,
+                     "alg_bytes_per_launch": dc["bytes"] / dc["launches"],
+                     "alg_flops_per_launch": dc["flops"] / dc["launches"],
+                     "arith_intensity": ai})
+
+    # ---- dense comparators on the same GPU, net and dtype
+    dense = {}
+    if not args.no_dense:
+        x = frames[0]
+        dense["own_dense_ms"] = time_gpu(
+            lambda: g.encode_reference(x, out=out), 5)
+        fwd = torch_dense_model(net, dt)
+        with torch.no_grad():
+            dense["miopen_ms"] = time_gpu(lambda: fwd(x), 10, warm=3)
+            ref_t = fwd(x).permute(0, 2, 3, 1).float()
+        g.encode_reference(x, out=out)
+        torch.cuda.synchronize()
+        dense["miopen_vs_own_rel_err"] = float(
+            (ref_t - out).abs().max() / out.abs().max())
+
+    res = {
+        "metric": METRIC,
+        "value": 1000.0 / ms_step,
+        "unit": "diff-frames/s",
+        "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": dt,
+        "data": "synthetic (seeded temporally continuous video, "
+                "random-init weights)",
+        "config": {"workload": wl["desc"], "batch": net.batch, "H": net.H,
+                   "W": net.W, "C": net.C, "layers": L_n,
+                   "target_density": args.density,
+                   "measured_input_density": dens0, "thr": args.thr},
+        "event_ms_per_step": ev_ms,
+        "effective_tflops": alg_flops / (ms_step * 1e-3) / 1e12,
+        "alg_gflop_per_frame": alg_flops / 1e9,
+        "dense_gflop_per_frame": dflops / 1e9,
+        "dense_equiv_tflops": dflops / (ms_step * 1e-3) / 1e12,
+    }
+    if dense:
+        res["speedup_vs_dense"] = {
+            "miopen": dense["miopen_ms"] / ms_step,
+            "own_dense": dense["own_dense_ms"] / ms_step}
+        res["dense_ms"] = dense
+    res["roofline"] = roof
+    res["kernels"] = kern
+    res["profiled_ms_per_step"] = prof_ms_step
+    res["frame_gen_s"] = t_gen
+    g.close()
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wl, net, args.thr)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

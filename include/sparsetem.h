@@ -207,9 +207,10 @@ st_status st_profile_begin(st_net* net, int32_t max_launches,
                            int32_t max_frames);
 
 /* Stop recording (synchronising).  Writes up to `cap` launch records and,
- * per recorded frame f and layer j, counts[(f * n_layers + j) * 4 + i] =
+ * per recorded frame f and layer j, counts[(f * n_layers + j) * 6 + i] =
  * {affected conv outputs, rulebook pairs, kept input rows of the layer's
- * source, emitted candidate rows}, up to `cap_frames` frames. */
+ * source, emitted candidate rows, emitted kept rows, kept rows of the
+ * residual source (0 without residual)}, up to `cap_frames` frames. */
 st_status st_profile_end(st_net* net, st_launch_record* recs, int32_t cap,
                          int32_t* n, int64_t* counts, int32_t cap_frames,
                          int32_t* n_frames);

@@ -576,11 +576,15 @@ extern "C" st_status st_profile_end(st_net* net, st_launch_record* recs,
         const LayerPlan& L = net->layers[j];
         const TensorPlan& in = net->tensors[L.d.src + 1];
         const TensorPlan& out = net->tensors[j + 1];
-        int64_t* q = counts + ((size_t)f * nl + j) * 4;
+        int64_t* q = counts + ((size_t)f * nl + j) * 6;
         q[0] = (int64_t)c[L.cnt_O];
         q[1] = (int64_t)c[L.cnt_pairs];
         q[2] = (int64_t)c[in.cnt_act];
         q[3] = (int64_t)c[out.cnt_rows];
+        q[4] = (int64_t)c[out.cnt_act];
+        q[5] = L.d.residual_src == -2
+                   ? 0
+                   : (int64_t)c[net->tensors[L.d.residual_src + 1].cnt_act];
       }
     }
   return ST_OK;

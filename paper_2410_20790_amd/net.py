@@ -34,7 +34,10 @@ class SparseTemNet:
                  dtype: str = "f32", device="cuda"):
         self.dtype = dtype
         self.tdtype = TORCH_DTYPES[dtype]
-        self.device = torch.device(device)
+        dev = torch.device(device)
+        if dev.type == "cuda" and dev.index is None:
+            dev = torch.device("cuda", torch.cuda.current_device())
+        self.device = dev
         self.n_layers = len(layers)
         self.in_shape = (batch, H, W, C)
         self._w, self._b, descs = [], [], []

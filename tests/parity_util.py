@@ -1,7 +1,9 @@
 """Comparison helpers for the GPU-vs-oracle parity tests.
 
 Tolerances (per tensor, relative to the oracle's largest magnitude):
-1e-4 for f32 nets, 2e-2 for f16/bf16 nets.  Masks, active lists and
+1e-4 for f32 nets, 2e-2 for f16/bf16 nets; half-precision deltas of stateful
+layers are bounded through the state they are differences of (see
+compare_frame).  Masks, active lists and
 rulebooks are compared exactly; where a row's keep decision depends on
 floating point that the two sides round differently (its max |delta| lies
 within a band around the threshold) it is reported and allowed.
@@ -78,8 +80,19 @@ def compare_frame(net, o, g, out_g, tag, check_rulebook=True):
                 pix_g, T["cand"], err_msg=f"{tag}: candidates of tensor {t}")
         # candidate delta values (before truncation)
         if exact_inputs and len(T["cand"]):
-            err = rel(rows_g, T["cand_rows"])
-            assert err <= rtol, f"{tag}: delta rows of tensor {t}: {err}"
+            err = float(np.abs(rows_g - T["cand_rows"]).max())
+            bound = rtol * float(np.abs(T["cand_rows"]).max())
+            if dt != "f32" and (t - 1) in o.P:
+                # A stateful layer emits f(P_new) - f(P_old) with f
+                # 1-Lipschitz, so its error is at most the sum of the errors
+                # of the two states; both meet the state tolerance, hence
+                # |delta error| <= 2 * rtol * max|P|.  (In a deep half
+                # precision chain the deltas are small next to the state and
+                # the two sides' re-rounding of every activation makes the
+                # states drift apart by up to ~1%.)
+                bound = max(bound, 2 * rtol * float(np.abs(o.P[t - 1]).max()))
+            assert err <= bound, (f"{tag}: delta rows of tensor {t}: "
+                                  f"{err} > {bound}")
         # kept sets: exact except band rows
         a, b = set(act_g.tolist()), set(T["pix"].tolist())
         diff = a ^ b

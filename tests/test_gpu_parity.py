@@ -90,7 +90,7 @@ def test_resnet50_small_bf16():
     net = resnet50_net(H=64, W=128)
     frames = driving_video(seed=2, n_frames=3, H=64, W=128, density=0.10,
                            side=(8, 32))
-    run_chunk(net, frames, 0.0, "resnet50 64x128 bf16")
+    run_chunk(net, frames, 0.0, "resnet50 64x128 bf16", max_band=8)
 
 
 # ------------------------------------------------------------ depthwise
