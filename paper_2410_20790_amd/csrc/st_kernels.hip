@@ -406,7 +406,12 @@ void launch_nbr(const Prof& pf, hipStream_t s, const int* O, const u64* nO,
 }
 
 // ------------------------------------------- (c)+(d) convolution epilogue
-template <typename T>
+struct EpiIn {
+  float po;  // old state (state mode, diff pass)
+  float sk;  // residual delta
+};
+
+template <typename T, bool REF>
 struct Epi {
   float* P;
   float* dP;
@@ -414,31 +419,39 @@ struct Epi {
   const float* bias;
   const T* dskip;
   const int* mskip;
-  int cout_p, mode, act, ref;
+  int cout_p, mode, act;
 
-  // Finish one output element: add bias (reference pass) and the residual
-  // delta, then either defer the update (pooled layers), or update the f32
-  // state in place and emit f(P_new) - f(P_old), or pass the linear delta
-  // on.  Returns |emitted delta| after rounding to the storage dtype.
-  __device__ __forceinline__ float operator()(int64_t o, int pix, int n,
-                                              float acc) const {
-    float dp = acc;
-    if (ref) dp += bias[n];
+  // Phase 1: every global load one output element needs.  Callers issue
+  // the loads of all their elements before any store, so the loads overlap
+  // instead of each waiting behind a store that might alias it.
+  __device__ __forceinline__ EpiIn load(int pix, int n) const {
+    EpiIn e{0.f, 0.f};
+    if (mode == 0 && !REF) e.po = P[(int64_t)pix * cout_p + n];
     if (mskip) {
       const int r = mskip[pix];
-      if (r >= 0) dp += to_f(dskip[(int64_t)r * cout_p + n]);
+      if (r >= 0) e.sk = to_f(dskip[(int64_t)r * cout_p + n]);
     }
+    return e;
+  }
+
+  // Phase 2: add bias (reference pass) and the residual delta, then either
+  // defer the update (pooled layers), or update the f32 state in place and
+  // emit f(P_new) - f(P_old), or pass the linear delta on.  Returns
+  // |emitted delta| after rounding to the storage dtype.
+  __device__ __forceinline__ float store(int64_t o, int pix, int n, float acc,
+                                         EpiIn in) const {
+    float dp = acc;
+    if (REF) dp += bias[n];
+    dp += in.sk;
     if (mode == 1) {
       dP[o * cout_p + n] = dp;
       return 0.f;
     }
     float d = dp;
     if (mode == 0) {
-      float* pp = P + (int64_t)pix * cout_p + n;
-      const float po = ref ? 0.f : *pp;
-      const float pn = po + dp;
-      *pp = pn;
-      d = act_f(pn, act) - act_f(po, act);
+      const float pn = in.po + dp;
+      P[(int64_t)pix * cout_p + n] = pn;
+      d = act_f(pn, act) - act_f(in.po, act);
     }
     const T q = from_f<T>(d);
     dout[o * cout_p + n] = q;
@@ -446,10 +459,10 @@ struct Epi {
   }
 };
 
-template <typename T>
-__device__ __forceinline__ Epi<T> make_epi(const ConvArgs& a) {
-  return Epi<T>{a.P, a.dP, (T*)a.dout, a.bias, (const T*)a.dskip, a.mskip,
-                a.cout_p, a.mode, a.act, a.ref};
+template <typename T, bool REF>
+__device__ __forceinline__ Epi<T, REF> make_epi(const ConvArgs& a) {
+  return Epi<T, REF>{a.P, a.dP, (T*)a.dout, a.bias, (const T*)a.dskip,
+                     a.mskip, a.cout_p, a.mode, a.act};
 }
 
 // --------------------------------------------------- (c) gather-GEMM MFMA
@@ -458,8 +471,16 @@ __device__ __forceinline__ Epi<T> make_epi(const ConvArgs& a) {
 // 16x16 blocks).  The reduction index r = k * cin_p + ci runs over kernel
 // offsets and input channels; per stage KC reduction columns of the
 // gathered input rows (A) and of the repacked weights (B, [cout_p][ktot_p])
-// are staged through LDS.  Stages whose offsets have no active neighbour
-// in the tile are skipped (adding exact zeros would not change the sum).
+// are staged through LDS.
+//
+// Latency hiding: the tile's neighbour indices are staged in LDS once, so a
+// stage's gather is a single global round trip; the next active stage's A
+// and B vectors are loaded into registers while the MFMAs of the current
+// stage run, and the LDS tiles are double buffered (one barrier per stage).
+// Stages whose offsets have no active neighbour in the tile are skipped
+// (adding exact zeros would not change the sum).  Tiles are assigned so that
+// the blocks of one XCD (blocks are dealt round-robin over the 8 XCDs) work
+// on consecutive tiles, which share gathered rows in that XCD's L2.
 template <typename T> struct MmaCfg;
 template <> struct MmaCfg<float> {
   static constexpr int KC = 16, LD = 17;  // scalar LDS rows, conflict-free
@@ -489,19 +510,81 @@ __device__ __forceinline__ void lds_store16<bf16_t>(bf16_t* dst, uint4 v) {
   *(uint4*)dst = v;
 }
 
-template <typename T>
+constexpr int kGemmBM = 64, kGemmBN = 64, kXcd = 8;
+
+// 8 consecutive storage elements <-> 8 floats (16- or 32-byte aligned).
+template <typename T> struct Vec8;
+template <> struct Vec8<float> {
+  __device__ __forceinline__ static void load(const float* p, float* f) {
+    const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
+    f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+  }
+  // stores the rounded values, returns their largest magnitude
+  __device__ __forceinline__ static float store(float* p, const float* f) {
+    *(float4*)p = make_float4(f[0], f[1], f[2], f[3]);
+    *(float4*)(p + 4) = make_float4(f[4], f[5], f[6], f[7]);
+    float m = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) m = fmaxf(m, fabsf(f[e]));
+    return m;
+  }
+};
+template <typename T> struct Vec8Half {
+  __device__ __forceinline__ static void load(const T* p, float* f) {
+    const uint4 v = *(const uint4*)p;
+    const T* h = (const T*)&v;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) f[e] = to_f(h[e]);
+  }
+  __device__ __forceinline__ static float store(T* p, const float* f) {
+    uint4 v;
+    T* h = (T*)&v;
+    float m = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      h[e] = from_f<T>(f[e]);
+      m = fmaxf(m, fabsf(to_f(h[e])));
+    }
+    *(uint4*)p = v;
+    return m;
+  }
+};
+template <> struct Vec8<_Float16> : Vec8Half<_Float16> {};
+template <> struct Vec8<bf16_t> : Vec8Half<bf16_t> {};
+
+__device__ __forceinline__ void load8f(const float* p, float* f) {
+  Vec8<float>::load(p, f);
+}
+__device__ __forceinline__ void store8f(float* p, const float* f) {
+  *(float4*)p = make_float4(f[0], f[1], f[2], f[3]);
+  *(float4*)(p + 4) = make_float4(f[4], f[5], f[6], f[7]);
+}
+
+template <typename T, bool REF>
 __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
-  constexpr int BM = 64, BN = 64;
+  constexpr int BM = kGemmBM, BN = kGemmBN;
   constexpr int KC = MmaCfg<T>::KC, LD = MmaCfg<T>::LD;
   constexpr int VEC = 16 / (int)sizeof(T);
-  constexpr int VPR = KC / VEC;  // 16-byte vectors per staged row
-  __shared__ T As[BM * LD];
-  __shared__ T Bs[BN * LD];
+  constexpr int VPR = KC / VEC;           // 16-byte vectors per staged row
+  constexpr int AV = BM * VPR / 256;      // A vectors per thread per stage
+  constexpr int BV = BN * VPR / 256;      // B vectors per thread per stage
+  constexpr int CLD = BN + 4;             // f32 accumulator tile row
+  constexpr size_t AB_BYTES = 2ull * (BM + BN) * LD * sizeof(T);
+  constexpr size_t C_BYTES = (size_t)BM * CLD * sizeof(float);
+  __shared__ __align__(16) char smem[AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES];
   __shared__ u64 s_kmask;
+  extern __shared__ int s_nbr[];          // [K][BM]
+  // LDS carve-up: A[2][BM][LD], B[2][BN][LD]; the f32 accumulator tile of
+  // the epilogue reuses the same bytes
+  T* const sA = (T*)smem;
+  T* const sB = (T*)smem + 2 * BM * LD;
+  float* const Cs = (float*)smem;
 
   const T* din = (const T*)a.din;
   const T* wt = (const T*)a.w;
-  const Epi<T> epi = make_epi<T>(a);
+  T* dout = (T*)a.dout;
+  const T* dskip = (const T*)a.dskip;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int l16 = lane & 15, lg = lane >> 4;
@@ -509,23 +592,116 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   const int64_t tiles_m = (nO + BM - 1) / BM;
   const int tiles_n = (a.cout_p + BN - 1) / BN;
   const int64_t ntiles = tiles_m * tiles_n;
+  const int K = a.K, cin_p = a.cin_p, cout_p = a.cout_p;
+  // reduction stages that hold real (not padding) columns
+  const int64_t kend = min(a.ktot_p, ((int64_t)K * cin_p + KC - 1) / KC * KC);
+  // XCD-aware order: blocks are dealt round-robin over the kXcd XCDs
+  // (gridDim.x is a multiple of kXcd); the tile range is cut into kXcd
+  // contiguous chunks, one per XCD, and the XCD's blocks stride through
+  // their chunk, so neighbouring tiles (which share gathered rows) meet in
+  // one L2 and every XCD gets work however few tiles there are.
+  const int64_t chunk = (ntiles + kXcd - 1) / kXcd;
+  const int xcd = blockIdx.x % kXcd;
+  const int64_t t_end = min(ntiles, (int64_t)(xcd + 1) * chunk);
+  const int per_xcd = gridDim.x / kXcd;
+  // epilogue ownership: thread -> row em, columns [ec, ec + 16) of the tile
+  const int em = tid >> 2, ec = (tid & 3) * 16;
 
-  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+  for (int64_t t = (int64_t)xcd * chunk + blockIdx.x / kXcd; t < t_end;
+       t += per_xcd) {
     const int64_t m0 = (t / tiles_n) * BM;
     const int n0 = (int)(t % tiles_n) * BN;
 
-    // offsets that have at least one active neighbour in this tile
+    __syncthreads();  // previous tile's LDS reads are complete
     if (tid == 0) s_kmask = 0ull;
+    // this thread's epilogue row; its old state and residual are fetched
+    // now so that they arrive while the reduction runs
+    const int64_t eo = m0 + em;
+    const bool eok = eo < nO;
+    const int epix = eok ? a.O[eo] : 0;
     __syncthreads();
     u64 my = 0ull;
-    for (int e = tid; e < BM * a.K; e += 256) {
+    for (int e = tid; e < BM * K; e += 256) {
       const int k = e / BM, m = e - (e / BM) * BM;
       const int64_t o = m0 + m;
-      if (o < nO && a.nbr[(int64_t)k * a.stride + o] >= 0) my |= 1ull << k;
+      const int src = o < nO ? a.nbr[(int64_t)k * a.stride + o] : -1;
+      s_nbr[e] = src;
+      if (src >= 0) my |= 1ull << k;
     }
     if (my) atomicOr(&s_kmask, my);
+    bool hv[2];
+    float po[2][8], sk[2][8];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int n = n0 + ec + 8 * h;
+      hv[h] = eok && n < cout_p;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) po[h][e] = sk[h][e] = 0.f;
+      if (hv[h] && a.mode == 0 && !REF)
+        load8f(a.P + (int64_t)epix * cout_p + n, po[h]);
+    }
+    const int rsk = (a.mskip && eok) ? a.mskip[epix] : -1;
+    if (rsk >= 0) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        if (hv[h])
+          Vec8<T>::load(dskip + (int64_t)rsk * cout_p + n0 + ec + 8 * h,
+                        sk[h]);
+    }
     __syncthreads();
     const u64 kmask = s_kmask;
+
+    auto stage_active = [&](int64_t r0) {
+      const int klo = (int)(r0 / cin_p);
+      int khi = (int)((r0 + KC - 1) / cin_p);
+      if (khi > K - 1) khi = K - 1;
+      const int span = khi - klo + 1;
+      const u64 bits = (span >= 64 ? ~0ull : ((1ull << span) - 1)) << klo;
+      return (kmask & bits) != 0ull;
+    };
+    auto next_stage = [&](int64_t r0) {
+      while (r0 < kend && !stage_active(r0)) r0 += KC;
+      return r0;
+    };
+
+    uint4 ra[AV], rb[BV];
+    auto load_stage = [&](int64_t r0) {
+#pragma unroll
+      for (int q = 0; q < AV; ++q) {
+        const int v = tid + q * 256;
+        const int m = v / VPR, cv = v - (v / VPR) * VPR;
+        const int64_t r = r0 + cv * VEC;
+        const int k = (int)(r / cin_p);
+        const int ci = (int)(r - (int64_t)k * cin_p);
+        const int src = k < K ? s_nbr[k * BM + m] : -1;
+        ra[q] = src >= 0 ? *(const uint4*)(din + (int64_t)src * cin_p + ci)
+                         : make_uint4(0u, 0u, 0u, 0u);
+      }
+#pragma unroll
+      for (int q = 0; q < BV; ++q) {
+        const int v = tid + q * 256;
+        const int nn = v / VPR, cv = v - (v / VPR) * VPR;
+        const int n = n0 + nn;
+        rb[q] = n < cout_p
+                    ? *(const uint4*)(wt + (int64_t)n * a.ktot_p + r0 +
+                                      cv * VEC)
+                    : make_uint4(0u, 0u, 0u, 0u);
+      }
+    };
+    auto store_stage = [&](int buf) {
+#pragma unroll
+      for (int q = 0; q < AV; ++q) {
+        const int v = tid + q * 256;
+        const int m = v / VPR, cv = v - (v / VPR) * VPR;
+        lds_store16<T>(sA + buf * BM * LD + m * LD + cv * VEC, ra[q]);
+      }
+#pragma unroll
+      for (int q = 0; q < BV; ++q) {
+        const int v = tid + q * 256;
+        const int nn = v / VPR, cv = v - (v / VPR) * VPR;
+        lds_store16<T>(sB + buf * BN * LD + nn * LD + cv * VEC, rb[q]);
+      }
+    };
 
     v4f acc[2][2];
 #pragma unroll
@@ -533,51 +709,26 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
 #pragma unroll
       for (int j = 0; j < 2; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-    for (int64_t r0 = 0; r0 < a.ktot_p; r0 += KC) {
-      const int klo = (int)(r0 / a.cin_p);
-      if (klo >= a.K) break;
-      int khi = (int)((r0 + KC - 1) / a.cin_p);
-      if (khi > a.K - 1) khi = a.K - 1;
-      const int span = khi - klo + 1;
-      const u64 bits = (span >= 64 ? ~0ull : ((1ull << span) - 1)) << klo;
-      if (!(kmask & bits)) continue;
-
-      // A: gathered input rows (zero for inactive or padded neighbours)
-      for (int v = tid; v < BM * VPR; v += 256) {
-        const int m = v / VPR, cv = v - (v / VPR) * VPR;
-        const int64_t r = r0 + cv * VEC;
-        const int64_t o = m0 + m;
-        const int k = (int)(r / a.cin_p);
-        const int ci = (int)(r - (int64_t)k * a.cin_p);
-        uint4 val = make_uint4(0u, 0u, 0u, 0u);
-        if (o < nO && k < a.K) {
-          const int src = a.nbr[(int64_t)k * a.stride + o];
-          if (src >= 0)
-            val = *(const uint4*)(din + (int64_t)src * a.cin_p + ci);
-        }
-        lds_store16<T>(As + m * LD + cv * VEC, val);
-      }
-      // B: repacked weights
-      for (int v = tid; v < BN * VPR; v += 256) {
-        const int nn = v / VPR, cv = v - (v / VPR) * VPR;
-        const int n = n0 + nn;
-        uint4 val = make_uint4(0u, 0u, 0u, 0u);
-        if (n < a.cout_p)
-          val = *(const uint4*)(wt + (int64_t)n * a.ktot_p + r0 + cv * VEC);
-        lds_store16<T>(Bs + nn * LD + cv * VEC, val);
-      }
+    int64_t r0 = next_stage(0);
+    if (r0 < kend) load_stage(r0);
+    int buf = 0;
+    while (r0 < kend) {
+      store_stage(buf);
       __syncthreads();
-
+      const int64_t r1 = next_stage(r0 + KC);
+      if (r1 < kend) load_stage(r1);   // in flight during the MFMAs below
+      const T* Ab = sA + buf * BM * LD;
+      const T* Bb = sB + buf * BN * LD;
       if constexpr (sizeof(T) == 4) {
 #pragma unroll
         for (int kk = 0; kk < KC; kk += 4) {
           float af[2], bf[2];
 #pragma unroll
           for (int i = 0; i < 2; ++i)
-            af[i] = As[(wm * 32 + i * 16 + l16) * LD + kk + lg];
+            af[i] = Ab[(wm * 32 + i * 16 + l16) * LD + kk + lg];
 #pragma unroll
           for (int j = 0; j < 2; ++j)
-            bf[j] = Bs[(wn * 32 + j * 16 + l16) * LD + kk + lg];
+            bf[j] = Bb[(wn * 32 + j * 16 + l16) * LD + kk + lg];
 #pragma unroll
           for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -588,79 +739,120 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
       } else {
 #pragma unroll
         for (int kk = 0; kk < KC; kk += 32) {
+          uint4 av[2], bv[2];
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+            av[i] = *(const uint4*)(Ab + (wm * 32 + i * 16 + l16) * LD + kk +
+                                    8 * lg);
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            bv[j] = *(const uint4*)(Bb + (wn * 32 + j * 16 + l16) * LD + kk +
+                                    8 * lg);
 #pragma unroll
           for (int i = 0; i < 2; ++i) {
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
-              const uint4 av =
-                  *(const uint4*)(As + (wm * 32 + i * 16 + l16) * LD + kk +
-                                  8 * lg);
-              const uint4 bv =
-                  *(const uint4*)(Bs + (wn * 32 + j * 16 + l16) * LD + kk +
-                                  8 * lg);
-              if constexpr (sizeof(T) == 2 && __is_same(T, _Float16)) {
+              if constexpr (__is_same(T, _Float16)) {
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                    __builtin_bit_cast(v8h, av), __builtin_bit_cast(v8h, bv),
-                    acc[i][j], 0, 0, 0);
+                    __builtin_bit_cast(v8h, av[i]),
+                    __builtin_bit_cast(v8h, bv[j]), acc[i][j], 0, 0, 0);
               } else {
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    __builtin_bit_cast(v8bf, av),
-                    __builtin_bit_cast(v8bf, bv), acc[i][j], 0, 0, 0);
+                    __builtin_bit_cast(v8bf, av[i]),
+                    __builtin_bit_cast(v8bf, bv[j]), acc[i][j], 0, 0, 0);
               }
             }
           }
         }
       }
-      __syncthreads();
+      buf ^= 1;
+      r0 = r1;
     }
 
-    // fused epilogue: D[row = 4*lg + r][col = l16] of each 16x16 block
+    // ---- fused epilogue.  The accumulator tile goes through LDS so that
+    // each thread finishes 16 contiguous columns of one row: full-width
+    // state loads/stores and 16-byte delta stores.  MFMA 16x16 block
+    // layout: D[row = 4*lg + r][col = l16].
+    __syncthreads();  // every wave is done reading the staged tiles
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = wm * 32 + i * 16 + 4 * lg + r;
-        const int64_t o = m0 + m;
-        const bool ok = o < nO;
-        const int pix = ok ? a.O[o] : 0;
-        float rm = 0.f;
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int n = n0 + wn * 32 + j * 16 + l16;
-          if (ok && n < a.cout_p) rm = fmaxf(rm, epi(o, pix, n, acc[i][j][r]));
-        }
+        for (int r = 0; r < 4; ++r)
+          Cs[(wm * 32 + i * 16 + 4 * lg + r) * CLD + wn * 32 + j * 16 + l16] =
+              acc[i][j][r];
+    __syncthreads();
+    float rm = 0.f;
 #pragma unroll
-        for (int x = 1; x < 16; x <<= 1) rm = fmaxf(rm, __shfl_xor(rm, x, 64));
-        if (ok && l16 == 0 && a.mode != 1 && rm > 0.f)
-          atomicMax(a.rowmax + o, __float_as_uint(rm));
+    for (int h = 0; h < 2; ++h) {
+      if (!hv[h]) continue;
+      const int n = n0 + ec + 8 * h;
+      float v[8];
+      load8f(Cs + em * CLD + ec + 8 * h, v);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (REF) v[e] += a.bias[n + e];
+        v[e] += sk[h][e];
       }
+      if (a.mode == 1) {
+        store8f(a.dP + eo * cout_p + n, v);
+        continue;
+      }
+      if (a.mode == 0) {
+        float pn[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          pn[e] = po[h][e] + v[e];
+          v[e] = act_f(pn[e], a.act) - act_f(po[h][e], a.act);
+        }
+        store8f(a.P + (int64_t)epix * cout_p + n, pn);
+      }
+      rm = fmaxf(rm, Vec8<T>::store(dout + eo * cout_p + n, v));
     }
+    // the four threads of a row are adjacent lanes
+    rm = fmaxf(rm, __shfl_xor(rm, 1, 64));
+    rm = fmaxf(rm, __shfl_xor(rm, 2, 64));
+    if (eok && (tid & 3) == 0 && a.mode != 1 && rm > 0.f)
+      atomicMax(a.rowmax + eo, __float_as_uint(rm));
   }
+}
+
+template <typename T>
+static void gemm_t(hipStream_t s, int grid, size_t lds, const ConvArgs& a) {
+  if (a.ref)
+    k_conv_gemm<T, true><<<grid, 256, lds, s>>>(a);
+  else
+    k_conv_gemm<T, false><<<grid, 256, lds, s>>>(a);
 }
 
 void launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
                       const ConvArgs& a) {
-  const int64_t worst = ((a.capO + 63) / 64) * ((a.cout_p + 63) / 64);
-  const int grid = (int)(worst < 2048 ? (worst < 1 ? 1 : worst) : 2048);
+  const int64_t worst = ((a.capO + kGemmBM - 1) / kGemmBM) *
+                        ((a.cout_p + kGemmBN - 1) / kGemmBN);
+  // persistent blocks: about what the 256 CUs hold at once
+  int64_t grid = worst < 1024 ? worst : 1024;
+  grid = (grid + kXcd - 1) / kXcd * kXcd;
+  const size_t lds = sizeof(int) * (size_t)a.K * kGemmBM;
   prof_begin(pf, 7 /*ST_K_CONV_GEMM*/, s);
   if (dtype == 0)
-    k_conv_gemm<float><<<grid, 256, 0, s>>>(a);
+    gemm_t<float>(s, (int)grid, lds, a);
   else if (dtype == 1)
-    k_conv_gemm<_Float16><<<grid, 256, 0, s>>>(a);
+    gemm_t<_Float16>(s, (int)grid, lds, a);
   else
-    k_conv_gemm<bf16_t><<<grid, 256, 0, s>>>(a);
+    gemm_t<bf16_t>(s, (int)grid, lds, a);
   prof_end(pf, 7, s);
 }
 
 // ---------------------------------------------------- (c') depthwise path
 // Memory-bound: each thread owns VEC channels of one affected row and sums
 // its K neighbours in offset order on the vector ALU.
-template <typename T>
+template <typename T, bool REF>
 __global__ __launch_bounds__(256) void k_conv_dw(ConvArgs a) {
   constexpr int VEC = 16 / (int)sizeof(T);
   const T* din = (const T*)a.din;
   const float* w = (const float*)a.w;
-  const Epi<T> epi = make_epi<T>(a);
+  const Epi<T, REF> epi = make_epi<T, REF>(a);
   const int64_t nO = (int64_t)*a.nO;
   const int cpr = a.cout_p / VEC;
   const int64_t total = nO * cpr;
@@ -681,11 +873,23 @@ __global__ __launch_bounds__(256) void k_conv_dw(ConvArgs a) {
       for (int e = 0; e < VEC; ++e) acc[e] += wk[e] * to_f(xv[e]);
     }
     const int pix = a.O[o];
+    EpiIn pre[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) pre[e] = epi.load(pix, c0 + e);
     float rm = 0.f;
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) rm = fmaxf(rm, epi(o, pix, c0 + e, acc[e]));
+    for (int e = 0; e < VEC; ++e)
+      rm = fmaxf(rm, epi.store(o, pix, c0 + e, acc[e], pre[e]));
     if (a.mode != 1 && rm > 0.f) atomicMax(a.rowmax + o, __float_as_uint(rm));
   }
+}
+
+template <typename T>
+static void dw_t(hipStream_t s, int grid, const ConvArgs& a) {
+  if (a.ref)
+    k_conv_dw<T, true><<<grid, 256, 0, s>>>(a);
+  else
+    k_conv_dw<T, false><<<grid, 256, 0, s>>>(a);
 }
 
 void launch_conv_dw(const Prof& pf, hipStream_t s, int dtype,
@@ -694,11 +898,11 @@ void launch_conv_dw(const Prof& pf, hipStream_t s, int dtype,
   const int grid = grid_for(a.capO * (a.cout_p / vec), 8192);
   prof_begin(pf, 8 /*ST_K_CONV_DW*/, s);
   if (dtype == 0)
-    k_conv_dw<float><<<grid, 256, 0, s>>>(a);
+    dw_t<float>(s, grid, a);
   else if (dtype == 1)
-    k_conv_dw<_Float16><<<grid, 256, 0, s>>>(a);
+    dw_t<_Float16>(s, grid, a);
   else
-    k_conv_dw<bf16_t><<<grid, 256, 0, s>>>(a);
+    dw_t<bf16_t>(s, grid, a);
   prof_end(pf, 8, s);
 }
 
