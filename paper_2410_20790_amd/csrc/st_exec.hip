@@ -77,6 +77,39 @@ Geo pool_geo(const LayerPlan& L) {
              d.pool_s_h, d.pool_s_w, d.pool_p_h, d.pool_p_w};
 }
 
+// Rulebook preparation the kept rows of tensor t do for the layers that
+// read it (see ConsList in st_kernels.h).
+ConsList consumers_of(st_net* net, int t) {
+  const WS ws{net->ws};
+  u64* cnt = ws.at<u64>(net->off_cnt);
+  ConsList cl{};
+  cl.n = 0;
+  for (const auto& cr : net->tensors[t].consumers) {
+    const int j = cr.first;
+    const LayerPlan& L = net->layers[j];
+    Cons c{};
+    if (cr.second == 0 && L.ident) {
+      c.kind = kConsIdent;
+      c.O = ws.at<int>(L.off_O);
+      c.Mo = ws.at<int>(L.off_Mo);
+      c.nbr = ws.at<int>(L.off_nbr);
+      c.rowmax = L.pool ? nullptr
+                        : ws.at<uint32_t>(net->tensors[j + 1].off_rowmax);
+      c.cnt_O = cnt + L.cnt_O;
+      c.pairs = cnt + L.cnt_pairs;
+    } else if (cr.second == 0) {
+      c.kind = kConsMark;
+      c.flags = ws.at<uint8_t>(L.off_flags);
+      c.g = conv_geo(L);
+    } else {
+      c.kind = kConsMarkSame;
+      c.flags = ws.at<uint8_t>(L.off_flags);
+    }
+    cl.c[cl.n++] = c;
+  }
+  return cl;
+}
+
 void run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   const WS ws{net->ws};
   const LayerPlan& L = net->layers[i];
@@ -84,8 +117,8 @@ void run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   const TensorPlan& in = net->tensors[d.src + 1];
   TensorPlan& out = net->tensors[i + 1];
   u64* cnt = ws.at<u64>(net->off_cnt);
-  uint8_t* flags = ws.at<uint8_t>(net->off_flags);
   uint32_t* tiles = ws.at<uint32_t>(net->off_tiles);
+  uint32_t* grp = ws.at<uint32_t>(net->off_grp);
   const Prof pf{net, i};
 
   int* O = ws.at<int>(L.off_O);
@@ -95,29 +128,24 @@ void run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   u64* cpairs = cnt + L.cnt_pairs;
   uint32_t* rowmax_out = ws.at<uint32_t>(out.off_rowmax);
   uint32_t* rm_O = L.pool ? nullptr : rowmax_out;
-  const int* act_in = ws.at<int>(in.off_act);
-  const int* map_in = ws.at<int>(in.off_map);
 
-  // (b) rulebook
-  if (L.ident) {
-    launch_ident(pf, s, act_in, cnt + in.cnt_act, map_in, in.grid, O, Mo, nbr,
-                 rm_O, cO, cpairs);
-  } else {
-    const Geo g = conv_geo(L);
-    const int* list2 = nullptr;
-    const u64* n2 = nullptr;
-    int64_t max_items = in.grid;
-    if (d.residual_src != -2) {
-      const TensorPlan& R = net->tensors[d.residual_src + 1];
-      list2 = ws.at<int>(R.off_act);
-      n2 = cnt + R.cnt_act;
-      max_items += R.grid;
-    }
-    launch_mark(pf, ST_K_RB_MARK, s, act_in, cnt + in.cnt_act, list2, n2,
-                max_items, g, net->N, flags);
-    launch_flag_compact(pf, ST_K_RB_COUNT, ST_K_RB_COMPACT, s, flags,
-                        L.conv_grid, tiles, O, Mo, rm_O, cO);
-    launch_nbr(pf, s, O, cO, L.conv_grid, g, L.K, map_in, nbr, cpairs);
+  // (b) rulebook: the flags were set while the producers emitted their kept
+  // rows; a 1x1 stride-1 layer's rulebook was written there directly.
+  if (!L.ident) {
+    FlagArgs fa{};
+    fa.flags = ws.at<uint8_t>(L.off_flags);
+    fa.npix = L.conv_grid;
+    fa.tiles = tiles;
+    fa.list = O;
+    fa.map = Mo;
+    fa.rowmax = rm_O;
+    fa.nbr = nbr;
+    fa.map_in = ws.at<int>(in.off_map);
+    fa.stride = L.conv_grid;
+    fa.g = conv_geo(L);
+    fa.pairs = cpairs;
+    fa.cnt = cO;
+    launch_flag_compact(pf, ST_K_RB_COUNT, ST_K_RB_COMPACT, s, fa);
   }
 
   // (c) delta convolution with fused (d) update / emission
@@ -146,6 +174,9 @@ void run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   a.mode = L.mode;
   a.act = d.act;
   a.ref = ref ? 1 : 0;
+  a.grp = (L.pool || L.dw) ? nullptr : grp;
+  a.mdone = ws.at<uint32_t>(net->off_mdone);
+  a.keep_thr = thr;
   if (L.dw)
     launch_conv_dw(pf, s, net->dtype, a);
   else
@@ -154,12 +185,17 @@ void run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   // non-linear post-op: max-pool from old and new state, then commit
   if (L.pool) {
     const Geo gp = pool_geo(L);
-    launch_mark(pf, ST_K_POOL_MARK, s, O, cO, nullptr, nullptr, L.conv_grid,
-                gp, net->N, flags);
-    launch_flag_compact(pf, ST_K_POOL_COUNT, ST_K_POOL_COMPACT, s, flags,
-                        out.grid, tiles, ws.at<int>(out.off_rowpix),
-                        ws.at<int>(out.off_map), rowmax_out,
-                        cnt + out.cnt_rows);
+    uint8_t* pflags = ws.at<uint8_t>(L.off_pflags);
+    launch_mark(pf, ST_K_POOL_MARK, s, O, cO, L.conv_grid, gp, pflags);
+    FlagArgs fp{};
+    fp.flags = pflags;
+    fp.npix = out.grid;
+    fp.tiles = tiles;
+    fp.list = ws.at<int>(out.off_rowpix);
+    fp.map = ws.at<int>(out.off_map);
+    fp.rowmax = rowmax_out;
+    fp.cnt = cnt + out.cnt_rows;
+    launch_flag_compact(pf, ST_K_POOL_COUNT, ST_K_POOL_COMPACT, s, fp);
     PoolArgs pa{};
     pa.Q = ws.at<int>(out.off_rowpix);
     pa.nQ = cnt + out.cnt_rows;
@@ -177,11 +213,24 @@ void run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
     launch_commit(pf, s, O, cO, L.conv_grid, ws.at<float>(L.off_P),
                   ws.at<float>(L.off_dP), L.cout_p, ref ? 1 : 0);
   }
+  if (L.pool || L.dw)
+    launch_group_count(pf, s, rowmax_out, cnt + out.cnt_rows, out.grid, thr,
+                       grp);
 
-  // truncation of the emitted delta (shared by every consumer)
-  launch_list_compact(pf, s, rowmax_out, cnt + out.cnt_rows, out.grid, thr,
-                      ws.at<int>(out.off_rowpix), ws.at<int>(out.off_act),
-                      ws.at<int>(out.off_map), tiles, cnt + out.cnt_act);
+  // truncation of the emitted delta (shared by every consumer), which also
+  // prepares the consumers' rulebooks
+  ListArgs la{};
+  la.rowmax = rowmax_out;
+  la.n_rows = cnt + out.cnt_rows;
+  la.cap = out.grid;
+  la.thr = thr;
+  la.rowpix = ws.at<int>(out.off_rowpix);
+  la.act = ws.at<int>(out.off_act);
+  la.map = ws.at<int>(out.off_map);
+  la.grp = grp;
+  la.cnt_act = cnt + out.cnt_act;
+  la.cons = consumers_of(net, i + 1);
+  launch_list_compact(pf, s, la);
   out.last_thr = thr;
 }
 
@@ -197,11 +246,24 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
   launch_reset(pf, s, cnt, net->n_counters);
   TensorPlan& T0 = net->tensors[0];
   const float thr0 = ref ? -1.f : thr[0];
-  launch_scan(pf, s, net->dtype, frame, ws.at<char>(net->off_xhat), net->C,
-              T0.Cp, T0.grid, thr0, ref ? 1 : 0, ws.at<uint8_t>(net->off_flags),
-              ws.at<uint32_t>(net->off_tiles), ws.at<char>(T0.off_rows),
-              ws.at<int>(T0.off_rowpix), ws.at<int>(T0.off_act),
-              ws.at<int>(T0.off_map), cnt + T0.cnt_rows, cnt + T0.cnt_act);
+  ScanArgs sa{};
+  sa.x = frame;
+  sa.xhat = ws.at<char>(net->off_xhat);
+  sa.C = net->C;
+  sa.Cp = T0.Cp;
+  sa.npix = T0.grid;
+  sa.thr = thr0;
+  sa.ref = ref ? 1 : 0;
+  sa.keep = ws.at<uint8_t>(net->off_flags);
+  sa.tiles = ws.at<uint32_t>(net->off_tiles);
+  sa.rows = ws.at<char>(T0.off_rows);
+  sa.rowpix = ws.at<int>(T0.off_rowpix);
+  sa.act = ws.at<int>(T0.off_act);
+  sa.map = ws.at<int>(T0.off_map);
+  sa.cnt_rows = cnt + T0.cnt_rows;
+  sa.cnt_act = cnt + T0.cnt_act;
+  sa.cons = consumers_of(net, 0);
+  launch_scan(pf, s, net->dtype, sa);
   T0.last_thr = thr0;
   const int nl = (int)net->layers.size();
   for (int i = 0; i < nl; ++i)

@@ -6,6 +6,7 @@
 #include <cstddef>
 #include <cstdint>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "../../include/sparsetem.h"
@@ -13,7 +14,8 @@
 namespace st {
 
 constexpr int kChanAlign = 8;       // delta rows / weights padded to 8 channels
-constexpr int kMaxTiles = 1024;     // compaction tiles per pass
+constexpr int kMaxTiles = 4096;     // compaction tiles per pass
+constexpr int64_t kMaxGrid = (int64_t)kMaxTiles * 8192;  // sites per grid
 constexpr size_t kAlign = 256;      // workspace sub-buffer alignment
 
 inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
@@ -38,6 +40,8 @@ struct TensorPlan {
   size_t off_rowmax = 0;            // uint32 [grid] bits of max|delta| per row
   int cnt_rows = 0, cnt_act = 0;    // counter indices
   float last_thr = 0.f;             // threshold used by the last encode
+  // layers reading this tensor: (layer, 0 = as conv input, 1 = as residual)
+  std::vector<std::pair<int, int>> consumers;
 };
 
 struct LayerPlan {
@@ -56,6 +60,8 @@ struct LayerPlan {
   size_t off_dP = 0;                // f32 [conv_grid][cout_p] (pooled layers)
   size_t off_w = 0;                 // GEMM: dtype [cout_p][ktot_p]; dw: f32 [K][cout_p]
   size_t off_bias = 0;              // f32 [cout_p]
+  size_t off_flags = 0;             // uint8 [conv_grid] affected-output flags
+  size_t off_pflags = 0;            // uint8 [pooled grid] (pooled layers)
   int cnt_O = 0, cnt_pairs = 0;
 };
 
@@ -72,8 +78,10 @@ struct st_net {
   std::vector<st::TensorPlan> tensors;     // n_layers + 1
   size_t ws_bytes = 0;
   size_t off_xhat = 0;                     // storage dtype [N*H*W*C]
-  size_t off_flags = 0;                    // uint8 [max grid]
+  size_t off_flags = 0;                    // uint8 [input grid] keep bytes
   size_t off_tiles = 0;                    // uint32 [kMaxTiles]
+  size_t off_grp = 0;                      // uint32 [max grid / 64 + 1]
+  size_t off_mdone = 0;                    // uint32 [max grid / 64 + 1]
   size_t off_cnt = 0;                      // uint64 [n_counters]
   size_t off_cleanup = 0;                  // cleanup descriptor table
   size_t off_dens = 0;                     // uint64 [batch] per-image counts

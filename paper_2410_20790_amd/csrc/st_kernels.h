@@ -36,27 +36,65 @@ void launch_reset(const Prof& pf, hipStream_t s, u64* cnt, int n);
 void launch_cleanup(const Prof& pf, hipStream_t s, const CleanEntry* tab,
                     int n_tab, char* ws, const u64* cnt, int64_t max_rows);
 
-// ---- (a) subtraction + truncation + compaction of the frame delta
-void launch_scan(const Prof& pf, hipStream_t s, int dtype, const void* x,
-                 void* xhat, int C, int Cp, int64_t npix, float thr, int ref,
-                 uint8_t* keep, uint32_t* tiles, void* rows, int* rowpix,
-                 int* act, int* map, u64* cnt_rows, u64* cnt_act);
+// ---- consumer-side rulebook preparation (done while a tensor's kept rows
+// are emitted)
+enum { kConsNone = 0, kConsIdent = 1, kConsMark = 2, kConsMarkSame = 3 };
+constexpr int kMaxCons = 4;
+struct Cons {
+  int kind;
+  int* O;             // ident: affected list, map, one-entry neighbour table
+  int* Mo;
+  int* nbr;
+  uint32_t* rowmax;   // ident: row maxima of the consumer's output to clear
+  u64* cnt_O;
+  u64* pairs;
+  uint8_t* flags;     // mark: the consumer's affected-output flags
+  Geo g;              // mark: the consumer's window geometry
+};
+struct ConsList {
+  Cons c[kMaxCons];
+  int n;
+};
 
-// ---- (b) rulebook
-void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
-                 const u64* n_list, const int* list2, const u64* n_list2,
-                 int64_t max_items, Geo g, int N, uint8_t* flags);
+// ---- (a) subtraction + truncation + compaction of the frame delta
+struct ScanArgs {
+  const void* x;
+  void* xhat;
+  int C, Cp;
+  int64_t npix;
+  float thr;
+  int ref;
+  uint8_t* keep;
+  uint32_t* tiles;
+  void* rows;
+  int* rowpix;
+  int* act;
+  int* map;
+  u64* cnt_rows;
+  u64* cnt_act;
+  ConsList cons;
+};
+void launch_scan(const Prof& pf, hipStream_t s, int dtype, const ScanArgs& a);
+
+// ---- (b) rulebook: affected-output compaction with the neighbour table
+struct FlagArgs {
+  uint8_t* flags;
+  int64_t npix;       // sites of the output grid
+  uint32_t* tiles;
+  int* list;
+  int* map;
+  uint32_t* rowmax;   // or NULL
+  int* nbr;           // or NULL (pool windows)
+  const int* map_in;
+  int64_t stride;
+  Geo g;
+  u64* pairs;
+  u64* cnt;
+};
 void launch_flag_compact(const Prof& pf, int cls_count, int cls_write,
-                         hipStream_t s, uint8_t* flags, int64_t npix,
-                         uint32_t* tiles, int* list, int* map,
-                         uint32_t* rowmax, u64* cnt);
-void launch_ident(const Prof& pf, hipStream_t s, const int* act_in,
-                  const u64* n_in, const int* map_in, int64_t max_items,
-                  int* O, int* Mo, int* nbr, uint32_t* rowmax, u64* cnt_O,
-                  u64* pairs);
-void launch_nbr(const Prof& pf, hipStream_t s, const int* O, const u64* nO,
-                int64_t capO, Geo g, int K, const int* map_in, int* nbr,
-                u64* pairs);
+                         hipStream_t s, const FlagArgs& a);
+void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
+                 const u64* n_list, int64_t max_items, Geo g, uint8_t* flags);
 
 // ---- (c)+(d) delta convolution with the fused state update / emission
 struct ConvArgs {
@@ -77,6 +115,9 @@ struct ConvArgs {
   const void* dskip;   // residual delta rows [*, cout_p] or NULL
   const int* mskip;    // residual pixel -> row map
   int mode, act, ref;
+  uint32_t* grp;       // per-64-row kept counts (or NULL)
+  uint32_t* mdone;     // per-row-tile arrival counters (zero between uses)
+  float keep_thr;      // threshold of the emitted tensor
 };
 void launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
                       const ConvArgs& a);
@@ -102,10 +143,22 @@ void launch_commit(const Prof& pf, hipStream_t s, const int* O, const u64* nO,
                    int64_t capO, float* P, const float* dP, int cp, int ref);
 
 // ---- truncation of an emitted tensor (list-mode compaction)
-void launch_list_compact(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
-                         const u64* n_rows, int64_t cap, float thr,
-                         const int* rowpix, int* act, int* map,
-                         uint32_t* tiles, u64* cnt_act);
+struct ListArgs {
+  const uint32_t* rowmax;
+  const u64* n_rows;
+  int64_t cap;
+  float thr;
+  const int* rowpix;
+  int* act;
+  int* map;
+  const uint32_t* grp;   // per-64-row kept counts
+  u64* cnt_act;
+  ConsList cons;
+};
+void launch_list_compact(const Prof& pf, hipStream_t s, const ListArgs& a);
+void launch_group_count(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
+                        const u64* n_rows, int64_t cap, float thr,
+                        uint32_t* grp);
 
 // ---- dense network output (Accumulation)
 void launch_output(const Prof& pf, hipStream_t s, const float* P, int cp,

@@ -88,12 +88,13 @@ __device__ __forceinline__ int64_t read_count(const u64* dev, int64_t host) {
 }
 
 // ============================================================ compaction
-// Ascending stream compaction in two passes.  Items are split into tiles of
-// `tile` consecutive indices (a multiple of 256); pass 1 counts the kept
-// items of each tile, pass 2 derives each tile's output offset from the
-// counts of the tiles before it and writes the kept items in order, using a
-// wave ballot and mbcnt for the in-wave prefix and LDS for the cross-wave
-// prefix.  The block that owns the last item writes the total.
+// Ascending stream compaction.  Items are split into tiles of `tile`
+// consecutive indices (a multiple of 256).  The write pass derives each
+// tile's output offset from per-tile or per-64-item-group counts of the
+// items before it -- counted by a separate pass, or by the kernel that
+// produced the items -- and writes the kept items in order, using a wave
+// ballot and mbcnt for the in-wave prefix and LDS for the cross-wave prefix.
+// The block that owns the last item writes the total.
 template <class P>
 __global__ __launch_bounds__(256) void k_compact_count(const u64* n_dev,
                                                        int64_t n_host,
@@ -111,75 +112,179 @@ __global__ __launch_bounds__(256) void k_compact_count(const u64* n_dev,
   if (threadIdx.x == 0) tile_cnt[blockIdx.x] = c;
 }
 
+// Exclusive prefix of a per-thread count over a 256-thread block (wave
+// scan with DPP-free shuffles, wave totals through LDS); also returns the
+// block total.
+__device__ __forceinline__ unsigned block_exclusive_scan(unsigned v,
+                                                         unsigned* total) {
+  __shared__ unsigned wsum[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  unsigned incl = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const unsigned t = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += t;
+  }
+  __syncthreads();
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  unsigned wpre = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    wpre += (w < wave) ? wsum[w] : 0u;
+    tot += wsum[w];
+  }
+  *total = tot;
+  return wpre + incl - v;
+}
+
+// cnts: `per_tile` counts per tile (1 = per-tile counts, tile/64 = counts of
+// 64-item groups).  Each thread owns `tile / 256` consecutive items of the
+// tile, evaluates all of them before emitting, and emits in item order, so
+// the whole tile costs one round of dependent loads.  pred.emit returns a
+// work count that is summed over the block and handed to pred.block_done;
+// pred.finish receives the total.
+constexpr int kMaxItemsPerThread = 32;
+
 template <class P>
 __global__ __launch_bounds__(256) void k_compact_write(
-    const u64* n_dev, int64_t n_host, int tile, const uint32_t* tile_cnt,
-    u64* out_cnt, u64* out_cnt2, P pred) {
+    const u64* n_dev, int64_t n_host, int tile, const uint32_t* cnts,
+    int per_tile, u64* out_cnt, u64* out_cnt2, P pred) {
   const int64_t n = read_count(n_dev, n_host);
   const int64_t base = (int64_t)blockIdx.x * tile;
   if (base >= n) {
     if (blockIdx.x == 0 && threadIdx.x == 0) {
       *out_cnt = 0;
       if (out_cnt2) *out_cnt2 = 0;
+      pred.finish(0u);
     }
     return;
   }
   unsigned off = 0;
-  for (unsigned j = threadIdx.x; j < blockIdx.x; j += 256) off += tile_cnt[j];
-  off = block_sum(off);
+  const unsigned nprev = blockIdx.x * (unsigned)per_tile;
+  for (unsigned j = threadIdx.x; j < nprev; j += 256) off += cnts[j];
+  const int ipt = tile / 256;
+  const int64_t first = base + (int64_t)threadIdx.x * ipt;
   const int64_t end = min(base + (int64_t)tile, n);
-  __shared__ unsigned wcnt[4];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  unsigned running = off;
-  for (int64_t r0 = base; r0 < end; r0 += 256) {
-    const int64_t i = r0 + threadIdx.x;
-    const bool in = i < end;
-    const bool keep = in && pred.keep(i);
-    const u64 bal = __ballot(keep);
-    const unsigned lp = lane_prefix(bal);
-    if (lane == 0) wcnt[wave] = (unsigned)__popcll(bal);
-    __syncthreads();
-    unsigned wpre = 0, tot = 0;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const unsigned c = wcnt[w];
-      wpre += (w < wave) ? c : 0u;
-      tot += c;
+  uint32_t keepbits = 0;
+  unsigned mine = 0;
+  for (int j = 0; j < ipt; ++j) {
+    const int64_t i = first + j;
+    if (i < end && pred.keep(i)) {
+      keepbits |= 1u << j;
+      ++mine;
     }
-    if (keep)
-      pred.emit(i, running + wpre + lp);
-    else if (in)
+  }
+  off = block_sum(off);
+  unsigned tile_total = 0;
+  unsigned pos = off + block_exclusive_scan(mine, &tile_total);
+  unsigned work = 0;
+  for (int j = 0; j < ipt; ++j) {
+    const int64_t i = first + j;
+    if (i >= end) break;
+    if (keepbits & (1u << j))
+      work += pred.emit(i, pos++);
+    else
       pred.drop(i);
-    running += tot;
-    __syncthreads();
   }
-  if (end == n && threadIdx.x == 0) {
-    *out_cnt = running;
-    if (out_cnt2) *out_cnt2 = running;
+  work = block_sum(work);
+  if (threadIdx.x == 0) {
+    pred.block_done(work);
+    if (end == n) {
+      const unsigned total = off + tile_total;
+      *out_cnt = total;
+      if (out_cnt2) *out_cnt2 = total;
+      pred.finish(total);
+    }
   }
 }
 
+// Tile of a compaction pass: a multiple of 256 items, at least 512, with at
+// most kMaxTiles tiles (the tile-count buffer) and at most 32 items per
+// thread (the keep bitmask of k_compact_write).
 static int compact_tile(int64_t cap) {
-  int64_t t = (cap + 1023) / 1024;
+  int64_t t = (cap + 4095) / 4096;
   t = (t + 255) / 256 * 256;
-  return (int)(t < 1024 ? 1024 : t);
+  return (int)(t < 512 ? 512 : t);
 }
 
+static int compact_tiles(int64_t cap) {
+  const int tile = compact_tile(cap);
+  const int nt = (int)((cap + tile - 1) / tile);
+  return nt < 1 ? 1 : nt;
+}
+
+// Counting pass + write pass.
 template <class P>
 static void run_compact(const Prof& pf, int cls_count, int cls_write,
                         hipStream_t s, const u64* n_dev, int64_t n_host,
                         int64_t cap, uint32_t* tiles, u64* out_cnt,
                         u64* out_cnt2, P pred) {
   const int tile = compact_tile(cap);
-  int nt = (int)((cap + tile - 1) / tile);
-  if (nt < 1) nt = 1;
+  const int nt = compact_tiles(cap);
   prof_begin(pf, cls_count, s);
   k_compact_count<P><<<nt, 256, 0, s>>>(n_dev, n_host, tile, tiles, pred);
   prof_end(pf, cls_count, s);
   prof_begin(pf, cls_write, s);
-  k_compact_write<P><<<nt, 256, 0, s>>>(n_dev, n_host, tile, tiles, out_cnt,
-                                        out_cnt2, pred);
+  k_compact_write<P><<<nt, 256, 0, s>>>(n_dev, n_host, tile, tiles, 1,
+                                        out_cnt, out_cnt2, pred);
   prof_end(pf, cls_write, s);
+}
+
+// ------------------------------------------- consumer-side rulebook prep
+// When a tensor's kept rows are emitted, the rulebooks of the layers that
+// read it are prepared in the same pass: a 1x1 stride-1 convolution gets its
+// affected list, map and one-entry neighbour table directly (its affected
+// outputs are exactly the kept inputs); any other consumer gets its
+// affected output sites marked through its window geometry (or, for a
+// residual input, at the same site).
+__device__ __forceinline__ void mark_window(uint8_t* flags, int p,
+                                            const Geo& g) {
+  const int64_t hwi = (int64_t)g.Hi * g.Wi;
+  const int n = (int)(p / hwi);
+  const int rem = (int)(p - n * hwi);
+  const int iy = rem / g.Wi, ix = rem - (rem / g.Wi) * g.Wi;
+  for (int ky = 0; ky < g.kh; ++ky) {
+    const int ty = iy + g.ph - ky;
+    if (ty < 0) break;
+    if (ty % g.sh) continue;
+    const int oy = ty / g.sh;
+    if (oy >= g.Ho) continue;
+    for (int kx = 0; kx < g.kw; ++kx) {
+      const int tx = ix + g.pw - kx;
+      if (tx < 0) break;
+      if (tx % g.sw) continue;
+      const int ox = tx / g.sw;
+      if (ox >= g.Wo) continue;
+      flags[((int64_t)n * g.Ho + oy) * g.Wo + ox] = 1;
+    }
+  }
+}
+
+__device__ __forceinline__ void cons_emit(const ConsList& cl, int p,
+                                          unsigned pos, int row) {
+  for (int i = 0; i < cl.n; ++i) {
+    const Cons& c = cl.c[i];
+    if (c.kind == kConsIdent) {
+      c.O[pos] = p;
+      c.Mo[p] = (int)pos;
+      c.nbr[pos] = row;
+      if (c.rowmax) c.rowmax[pos] = 0u;
+    } else if (c.kind == kConsMark) {
+      mark_window(c.flags, p, c.g);
+    } else if (c.kind == kConsMarkSame) {
+      c.flags[p] = 1;
+    }
+  }
+}
+
+__device__ __forceinline__ void cons_finish(const ConsList& cl,
+                                            unsigned total) {
+  for (int i = 0; i < cl.n; ++i)
+    if (cl.c[i].kind == kConsIdent) {
+      *cl.c[i].cnt_O = total;
+      *cl.c[i].pairs = total;
+    }
 }
 
 // ------------------------------------------------------- (a) frame delta
@@ -194,6 +299,7 @@ struct ScanPred {
   int* map;
   int C, Cp, ref;
   float thr;
+  ConsList cons;
   // pass 1: evaluate the truncation rule and remember it
   __device__ bool count(int64_t i) const {
     float m = 0.f;
@@ -207,7 +313,7 @@ struct ScanPred {
   }
   __device__ bool keep(int64_t i) const { return keepb[i] != 0; }
   // pass 2: gather the delta row, commit the pixel to X_hat
-  __device__ void emit(int64_t i, unsigned pos) const {
+  __device__ unsigned emit(int64_t i, unsigned pos) const {
     rowpix[pos] = (int)i;
     act[pos] = (int)i;
     map[i] = (int)pos;
@@ -223,34 +329,30 @@ struct ScanPred {
       }
     }
     keepb[i] = 0;
+    cons_emit(cons, (int)i, pos, (int)pos);
+    return 0u;
   }
   __device__ void drop(int64_t) const {}
+  __device__ void block_done(unsigned) const {}
+  __device__ void finish(unsigned total) const { cons_finish(cons, total); }
 };
 
 template <typename T>
-static void scan_t(const Prof& pf, hipStream_t s, const void* x, void* xhat,
-                   int C, int Cp, int64_t npix, float thr, int ref,
-                   uint8_t* keep, uint32_t* tiles, void* rows, int* rowpix,
-                   int* act, int* map, u64* cnt_rows, u64* cnt_act) {
-  ScanPred<T> p{(const T*)x, (T*)xhat, keep, (T*)rows, rowpix, act, map,
-                C, Cp, ref, thr};
+static void scan_t(const Prof& pf, hipStream_t s, const ScanArgs& a) {
+  ScanPred<T> p{(const T*)a.x, (T*)a.xhat, a.keep, (T*)a.rows, a.rowpix,
+                a.act, a.map, a.C, a.Cp, a.ref, a.thr, a.cons};
   run_compact(pf, 0 /*ST_K_SCAN_MASK*/, 1 /*ST_K_SCAN_COMPACT*/, s, nullptr,
-              npix, npix, tiles, cnt_rows, cnt_act, p);
+              a.npix, a.npix, a.tiles, a.cnt_rows, a.cnt_act, p);
 }
 
-void launch_scan(const Prof& pf, hipStream_t s, int dtype, const void* x,
-                 void* xhat, int C, int Cp, int64_t npix, float thr, int ref,
-                 uint8_t* keep, uint32_t* tiles, void* rows, int* rowpix,
-                 int* act, int* map, u64* cnt_rows, u64* cnt_act) {
+void launch_scan(const Prof& pf, hipStream_t s, int dtype,
+                 const ScanArgs& a) {
   if (dtype == 0)
-    scan_t<float>(pf, s, x, xhat, C, Cp, npix, thr, ref, keep, tiles, rows,
-                  rowpix, act, map, cnt_rows, cnt_act);
+    scan_t<float>(pf, s, a);
   else if (dtype == 1)
-    scan_t<_Float16>(pf, s, x, xhat, C, Cp, npix, thr, ref, keep, tiles, rows,
-                     rowpix, act, map, cnt_rows, cnt_act);
+    scan_t<_Float16>(pf, s, a);
   else
-    scan_t<bf16_t>(pf, s, x, xhat, C, Cp, npix, thr, ref, keep, tiles, rows,
-                   rowpix, act, map, cnt_rows, cnt_act);
+    scan_t<bf16_t>(pf, s, a);
 }
 
 // ---------------------------------------------------------- (b) rulebook
@@ -260,149 +362,105 @@ static int grid_for(int64_t items, int cap_blocks = 4096) {
   return (int)(b > cap_blocks ? cap_blocks : b);
 }
 
-// Mark every output site reached by an active input site through some
-// window offset; optionally also mark the sites of a second list (residual
-// deltas, already on the output grid).
+// Mark every output site reached by an active site through the window
+// (used for the pool windows of pooled layers).
 __global__ __launch_bounds__(256) void k_mark(const int* list, const u64* n1p,
-                                              const int* list2,
-                                              const u64* n2p, Geo g,
-                                              uint8_t* flags) {
+                                              Geo g, uint8_t* flags) {
   const int64_t n1 = (int64_t)*n1p;
-  const int64_t n2 = list2 ? (int64_t)*n2p : 0;
-  const int64_t hwi = (int64_t)g.Hi * g.Wi;
-  for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j < n1 + n2;
-       j += (int64_t)gridDim.x * 256) {
-    if (j >= n1) {
-      flags[list2[j - n1]] = 1;
-      continue;
-    }
-    const int p = list[j];
-    const int n = (int)(p / hwi);
-    const int rem = (int)(p - n * hwi);
-    const int iy = rem / g.Wi, ix = rem - (rem / g.Wi) * g.Wi;
-    for (int ky = 0; ky < g.kh; ++ky) {
-      const int ty = iy + g.ph - ky;
-      if (ty < 0) break;
-      if (ty % g.sh) continue;
-      const int oy = ty / g.sh;
-      if (oy >= g.Ho) continue;
-      for (int kx = 0; kx < g.kw; ++kx) {
-        const int tx = ix + g.pw - kx;
-        if (tx < 0) break;
-        if (tx % g.sw) continue;
-        const int ox = tx / g.sw;
-        if (ox >= g.Wo) continue;
-        flags[((int64_t)n * g.Ho + oy) * g.Wo + ox] = 1;
-      }
-    }
-  }
+  for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j < n1;
+       j += (int64_t)gridDim.x * 256)
+    mark_window(flags, list[j], g);
 }
 
 void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
-                 const u64* n_list, const int* list2, const u64* n_list2,
-                 int64_t max_items, Geo g, int N, uint8_t* flags) {
-  (void)N;
+                 const u64* n_list, int64_t max_items, Geo g,
+                 uint8_t* flags) {
   prof_begin(pf, cls, s);
-  k_mark<<<grid_for(max_items), 256, 0, s>>>(list, n_list, list2, n_list2, g,
-                                             flags);
+  k_mark<<<grid_for(max_items), 256, 0, s>>>(list, n_list, g, flags);
   prof_end(pf, cls, s);
 }
 
+// Affected-output compaction.  With `nbr` set, each emitted output also gets
+// its output-major neighbour entries nbr[k][o] = row of the input delta at
+// the site offset k reads (or -1: padding or inactive site), and the block
+// adds its number of valid entries to `pairs`.
 struct FlagPred {
   uint8_t* flags;
   int* list;
   int* map;
   uint32_t* rowmax;
+  int* nbr;
+  const int* map_in;
+  int64_t stride;
+  Geo g;  // conv geometry: input grid -> this (output) grid
+  u64* pairs;
   __device__ bool count(int64_t i) const { return flags[i] != 0; }
   __device__ bool keep(int64_t i) const { return flags[i] != 0; }
-  __device__ void emit(int64_t i, unsigned pos) const {
+  __device__ unsigned emit(int64_t i, unsigned pos) const {
     list[pos] = (int)i;
     map[i] = (int)pos;
     flags[i] = 0;
     if (rowmax) rowmax[pos] = 0u;
+    if (!nbr) return 0u;
+    const int64_t hwo = (int64_t)g.Ho * g.Wo;
+    const int n = (int)(i / hwo);
+    const int rem = (int)(i - n * hwo);
+    const int oy = rem / g.Wo, ox = rem - (rem / g.Wo) * g.Wo;
+    unsigned valid = 0;
+    for (int ky = 0; ky < g.kh; ++ky) {
+      const int iy = oy * g.sh - g.ph + ky;
+      const bool rok = iy >= 0 && iy < g.Hi;
+      for (int kx = 0; kx < g.kw; ++kx) {
+        const int ix = ox * g.sw - g.pw + kx;
+        int v = -1;
+        if (rok && ix >= 0 && ix < g.Wi)
+          v = map_in[((int64_t)n * g.Hi + iy) * g.Wi + ix];
+        nbr[(int64_t)(ky * g.kw + kx) * stride + pos] = v;
+        valid += v >= 0 ? 1u : 0u;
+      }
+    }
+    return valid;
   }
   __device__ void drop(int64_t) const {}
+  __device__ void block_done(unsigned w) const {
+    if (pairs && w) atomicAdd(pairs, (u64)w);
+  }
+  __device__ void finish(unsigned) const {}
 };
 
 void launch_flag_compact(const Prof& pf, int cls_count, int cls_write,
-                         hipStream_t s, uint8_t* flags, int64_t npix,
-                         uint32_t* tiles, int* list, int* map,
-                         uint32_t* rowmax, u64* cnt) {
-  FlagPred p{flags, list, map, rowmax};
-  run_compact(pf, cls_count, cls_write, s, nullptr, npix, npix, tiles, cnt,
-              nullptr, p);
+                         hipStream_t s, const FlagArgs& a) {
+  FlagPred p{a.flags, a.list, a.map, a.rowmax, a.nbr, a.map_in, a.stride,
+             a.g, a.pairs};
+  run_compact(pf, cls_count, cls_write, s, nullptr, a.npix, a.npix, a.tiles,
+              a.cnt, nullptr, p);
 }
 
-// 1x1 stride-1 convolution without residual: the affected outputs are the
-// active inputs themselves and each has exactly one neighbour.
-__global__ __launch_bounds__(256) void k_ident(const int* act_in,
-                                               const u64* n_in,
-                                               const int* map_in, int* O,
-                                               int* Mo, int* nbr,
-                                               uint32_t* rowmax, u64* cnt_O,
-                                               u64* pairs) {
-  const int64_t n = (int64_t)*n_in;
-  for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j < n;
-       j += (int64_t)gridDim.x * 256) {
-    const int p = act_in[j];
-    O[j] = p;
-    Mo[p] = (int)j;
-    nbr[j] = map_in[p];
-    if (rowmax) rowmax[j] = 0u;
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    *cnt_O = (u64)n;
-    *pairs = (u64)n;
+// Per-64-row kept counts of an emitted tensor (rows whose max |delta|
+// exceeds thr), one wave per group; for the kernels whose epilogue does
+// not count them itself.
+__global__ __launch_bounds__(256) void k_group_count(const uint32_t* rowmax,
+                                                     const u64* n_rows,
+                                                     float thr,
+                                                     uint32_t* grp) {
+  const int64_t n = (int64_t)*n_rows;
+  const int64_t ngrp = (n + 63) / 64;
+  const int lane = threadIdx.x & 63;
+  for (int64_t gi = ((int64_t)blockIdx.x * 256 + threadIdx.x) / 64; gi < ngrp;
+       gi += (int64_t)gridDim.x * 4) {
+    const int64_t r = gi * 64 + lane;
+    const bool k = r < n && __uint_as_float(rowmax[r]) > thr;
+    const u64 b = __ballot(k);
+    if (lane == 0) grp[gi] = (uint32_t)__popcll(b);
   }
 }
 
-void launch_ident(const Prof& pf, hipStream_t s, const int* act_in,
-                  const u64* n_in, const int* map_in, int64_t max_items,
-                  int* O, int* Mo, int* nbr, uint32_t* rowmax, u64* cnt_O,
-                  u64* pairs) {
-  prof_begin(pf, 6 /*ST_K_RB_IDENT*/, s);
-  k_ident<<<grid_for(max_items), 256, 0, s>>>(act_in, n_in, map_in, O, Mo,
-                                              nbr, rowmax, cnt_O, pairs);
-  prof_end(pf, 6, s);
-}
-
-// Output-major neighbour table: nbr[k][o] = row of the input delta at the
-// site offset k of output o reads, or -1 (padding or inactive site).
-__global__ __launch_bounds__(256) void k_nbr(const int* O, const u64* nOp,
-                                             int64_t stride, Geo g, int K,
-                                             const int* map_in, int* nbr,
-                                             u64* pairs) {
-  const int64_t nO = (int64_t)*nOp;
-  const int64_t total = nO * K;
-  const int64_t hwo = (int64_t)g.Ho * g.Wo;
-  unsigned cnt = 0;
-  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
-       idx += (int64_t)gridDim.x * 256) {
-    const int k = (int)(idx / nO);
-    const int64_t o = idx - (int64_t)k * nO;
-    const int p = O[o];
-    const int n = (int)(p / hwo);
-    const int rem = (int)(p - n * hwo);
-    const int oy = rem / g.Wo, ox = rem - (rem / g.Wo) * g.Wo;
-    const int ky = k / g.kw, kx = k - (k / g.kw) * g.kw;
-    const int iy = oy * g.sh - g.ph + ky, ix = ox * g.sw - g.pw + kx;
-    int v = -1;
-    if (iy >= 0 && iy < g.Hi && ix >= 0 && ix < g.Wi)
-      v = map_in[((int64_t)n * g.Hi + iy) * g.Wi + ix];
-    nbr[(int64_t)k * stride + o] = v;
-    cnt += v >= 0 ? 1u : 0u;
-  }
-  cnt = block_sum(cnt);
-  if (threadIdx.x == 0 && cnt) atomicAdd(pairs, (u64)cnt);
-}
-
-void launch_nbr(const Prof& pf, hipStream_t s, const int* O, const u64* nO,
-                int64_t capO, Geo g, int K, const int* map_in, int* nbr,
-                u64* pairs) {
-  prof_begin(pf, 5 /*ST_K_RB_NBR*/, s);
-  k_nbr<<<grid_for(capO * K), 256, 0, s>>>(O, nO, capO, g, K, map_in, nbr,
-                                           pairs);
-  prof_end(pf, 5, s);
+void launch_group_count(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
+                        const u64* n_rows, int64_t cap, float thr,
+                        uint32_t* grp) {
+  prof_begin(pf, 14 /*ST_K_LIST_COUNT*/, s);
+  k_group_count<<<grid_for(cap, 2048), 256, 0, s>>>(rowmax, n_rows, thr, grp);
+  prof_end(pf, 14, s);
 }
 
 // ------------------------------------------- (c)+(d) convolution epilogue
@@ -574,6 +632,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   constexpr size_t C_BYTES = (size_t)BM * CLD * sizeof(float);
   __shared__ __align__(16) char smem[AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES];
   __shared__ u64 s_kmask;
+  __shared__ int s_last;
   extern __shared__ int s_nbr[];          // [K][BM]
   // LDS carve-up: A[2][BM][LD], B[2][BN][LD]; the f32 accumulator tile of
   // the epilogue reuses the same bytes
@@ -813,8 +872,43 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     // the four threads of a row are adjacent lanes
     rm = fmaxf(rm, __shfl_xor(rm, 1, 64));
     rm = fmaxf(rm, __shfl_xor(rm, 2, 64));
+    // row maxima: device-scope atomics whose results are waited for, so
+    // they have completed at the coherence point before the barrier below
+    unsigned seen = 0u;
     if (eok && (tid & 3) == 0 && a.mode != 1 && rm > 0.f)
-      atomicMax(a.rowmax + eo, __float_as_uint(rm));
+      seen = __hip_atomic_fetch_max(a.rowmax + eo, __float_as_uint(rm),
+                                    __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_AGENT);
+
+    // The last block to finish a row tile (over its column tiles) counts
+    // the tile's kept rows for the truncation pass, reading the row maxima
+    // with device-scope atomic loads; the arrival counter is reset by the
+    // block that reads it.  No cache-maintenance fence is needed: only
+    // atomics carry data between the blocks.
+    if (a.grp) {
+      const int64_t tm = m0 / BM;
+      if (seen == 0xFFFFFFFFu) s_last = 0;  // consumes the atomic results
+      __syncthreads();
+      if (tid == 0)
+        s_last = __hip_atomic_fetch_add(a.mdone + tm, 1u, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT) ==
+                 (unsigned)(tiles_n - 1);
+      __syncthreads();
+      if (s_last && tid < 64) {
+        const int64_t o = m0 + tid;
+        bool k = false;
+        if (o < nO)
+          k = __uint_as_float(__hip_atomic_load(a.rowmax + o, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT)) >
+              a.keep_thr;
+        const u64 b = __ballot(k);
+        if (tid == 0) {
+          a.grp[tm] = (uint32_t)__popcll(b);
+          __hip_atomic_store(a.mdone + tm, 0u, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    }
   }
 }
 
@@ -986,29 +1080,43 @@ void launch_commit(const Prof& pf, hipStream_t s, const int* O, const u64* nO,
 }
 
 // ------------------------------------------------ truncation (list mode)
+// Keeps the rows of an emitted tensor whose max |delta| exceeds the
+// threshold (ascending kept list), removes dropped rows from the pixel map
+// and prepares the consumers' rulebooks.  Offsets come from per-64-row
+// kept counts written by the producing kernel (or k_group_count).
 struct ListPred {
   const uint32_t* rowmax;
   const int* rowpix;
   int* act;
   int* map;
   float thr;
+  ConsList cons;
   __device__ bool count(int64_t r) const {
     return __uint_as_float(rowmax[r]) > thr;
   }
   __device__ bool keep(int64_t r) const {
     return __uint_as_float(rowmax[r]) > thr;
   }
-  __device__ void emit(int64_t r, unsigned pos) const { act[pos] = rowpix[r]; }
+  __device__ unsigned emit(int64_t r, unsigned pos) const {
+    const int p = rowpix[r];
+    act[pos] = p;
+    cons_emit(cons, p, pos, (int)r);
+    return 0u;
+  }
   __device__ void drop(int64_t r) const { map[rowpix[r]] = -1; }
+  __device__ void block_done(unsigned) const {}
+  __device__ void finish(unsigned total) const { cons_finish(cons, total); }
 };
 
-void launch_list_compact(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
-                         const u64* n_rows, int64_t cap, float thr,
-                         const int* rowpix, int* act, int* map,
-                         uint32_t* tiles, u64* cnt_act) {
-  ListPred p{rowmax, rowpix, act, map, thr};
-  run_compact(pf, 14 /*ST_K_LIST_COUNT*/, 15 /*ST_K_LIST_COMPACT*/, s, n_rows,
-              0, cap, tiles, cnt_act, nullptr, p);
+void launch_list_compact(const Prof& pf, hipStream_t s, const ListArgs& a) {
+  ListPred p{a.rowmax, a.rowpix, a.act, a.map, a.thr, a.cons};
+  const int tile = compact_tile(a.cap);
+  const int nt = compact_tiles(a.cap);
+  prof_begin(pf, 15 /*ST_K_LIST_COMPACT*/, s);
+  k_compact_write<ListPred><<<nt, 256, 0, s>>>(a.n_rows, 0, tile, a.grp,
+                                               tile / 64, a.cnt_act, nullptr,
+                                               p);
+  prof_end(pf, 15, s);
 }
 
 // ------------------------------------------------------- dense output

@@ -59,6 +59,9 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
     return create_fail(ST_ERR_INVALID_ARG, "unknown dtype");
   if ((int64_t)batch * in_h * in_w >= (int64_t)1 << 31)
     return create_fail(ST_ERR_INVALID_ARG, "input grid exceeds 2^31 pixels");
+  if ((int64_t)batch * in_h * in_w > kMaxGrid)
+    return create_fail(ST_ERR_UNSUPPORTED, "input grid above the compaction "
+                                           "limit");
 
   st_net* net = new (std::nothrow) st_net();
   if (!net) return create_fail(ST_ERR_INVALID_ARG, "out of host memory");
@@ -142,12 +145,24 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
     L.mode = L.pool ? kModeDefer : (L.stateful ? kModeState : kModeLinear);
     L.ident = d.k_h == 1 && d.k_w == 1 && d.s_h == 1 && d.s_w == 1 &&
               d.p_h == 0 && d.p_w == 0 && d.residual_src == -2;
+    net->tensors[d.src + 1].consumers.push_back({i, 0});
+    if (d.residual_src != -2)
+      net->tensors[d.residual_src + 1].consumers.push_back({i, 1});
     TensorPlan& t = net->tensors[i + 1];
     t.N = batch; t.H = L.Hp; t.W = L.Wp; t.C = d.c_out; t.Cp = L.cout_p;
     t.grid = (int64_t)batch * L.Hp * L.Wp;
     if (L.conv_grid >= ((int64_t)1 << 31) / std::max(L.K, 1))
       return bad(ST_ERR_INVALID_ARG, i, "rulebook exceeds 2^31 entries");
+    if (L.conv_grid > kMaxGrid || t.grid > kMaxGrid)
+      return bad(ST_ERR_UNSUPPORTED, i, "grid above the compaction limit");
   }
+
+  for (int t = 0; t <= n_layers; ++t)
+    if (net->tensors[t].consumers.size() > 4) {
+      delete net;
+      return create_fail(ST_ERR_UNSUPPORTED,
+                         "a tensor read by more than 4 layers");
+    }
 
   // ---- workspace layout
   Alloc a;
@@ -193,9 +208,13 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
     else
       L.off_w = a.take((size_t)L.cout_p * L.ktot_p * net->esize);
     L.off_bias = a.take(sizeof(float) * L.cout_p);
+    if (!L.ident) L.off_flags = a.take(round_up(L.conv_grid, 16));
+    if (L.pool) L.off_pflags = a.take(round_up(T.grid, 16));
   }
   net->max_grid = max_grid;
-  net->off_flags = a.take(round_up(max_grid, 16));
+  net->off_flags = a.take(round_up(t0.grid, 16));
+  net->off_grp = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
+  net->off_mdone = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
   net->n_cleanup = n_cleanup;
   net->off_cleanup = a.take(32 * n_cleanup);
   net->ws_bytes = round_up(a.top, kAlign);
