@@ -619,7 +619,7 @@ __device__ __forceinline__ void store8f(float* p, const float* f) {
   *(float4*)(p + 4) = make_float4(f[4], f[5], f[6], f[7]);
 }
 
-template <typename T, bool REF>
+template <typename T, bool REF, bool ALIGNED>
 __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   constexpr int BM = kGemmBM, BN = kGemmBN;
   constexpr int KC = MmaCfg<T>::KC, LD = MmaCfg<T>::LD;
@@ -652,24 +652,28 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   const int tiles_n = (a.cout_p + BN - 1) / BN;
   const int64_t ntiles = tiles_m * tiles_n;
   const int K = a.K, cin_p = a.cin_p, cout_p = a.cout_p;
-  // reduction stages that hold real (not padding) columns
-  const int64_t kend = min(a.ktot_p, ((int64_t)K * cin_p + KC - 1) / KC * KC);
+  const int ktot_p = (int)a.ktot_p;
+  // reduction stages that hold real (not padding) columns; with ALIGNED
+  // (cin_p a multiple of KC) every stage lies within one kernel offset and
+  // offset k covers stages [k * spk, (k + 1) * spk)
+  const int nst = min(ktot_p, (K * cin_p + KC - 1) / KC * KC) / KC;
+  const int spk = ALIGNED ? cin_p / KC : 1;
   // XCD-aware order: blocks are dealt round-robin over the kXcd XCDs
   // (gridDim.x is a multiple of kXcd); the tile range is cut into kXcd
   // contiguous chunks, one per XCD, and the XCD's blocks stride through
   // their chunk, so neighbouring tiles (which share gathered rows) meet in
   // one L2 and every XCD gets work however few tiles there are.
-  const int64_t chunk = (ntiles + kXcd - 1) / kXcd;
+  const int chunk = (int)((ntiles + kXcd - 1) / kXcd);
   const int xcd = blockIdx.x % kXcd;
-  const int64_t t_end = min(ntiles, (int64_t)(xcd + 1) * chunk);
+  const int t_end = (int)min(ntiles, (int64_t)(xcd + 1) * chunk);
   const int per_xcd = gridDim.x / kXcd;
   // epilogue ownership: thread -> row em, columns [ec, ec + 16) of the tile
   const int em = tid >> 2, ec = (tid & 3) * 16;
 
-  for (int64_t t = (int64_t)xcd * chunk + blockIdx.x / kXcd; t < t_end;
-       t += per_xcd) {
-    const int64_t m0 = (t / tiles_n) * BM;
-    const int n0 = (int)(t % tiles_n) * BN;
+  for (int t = xcd * chunk + blockIdx.x / kXcd; t < t_end; t += per_xcd) {
+    const int tm_i = (int)((unsigned)t / (unsigned)tiles_n);
+    const int64_t m0 = (int64_t)tm_i * BM;
+    const int n0 = (t - tm_i * tiles_n) * BN;
 
     __syncthreads();  // previous tile's LDS reads are complete
     if (tid == 0) s_kmask = 0ull;
@@ -710,28 +714,41 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     __syncthreads();
     const u64 kmask = s_kmask;
 
-    auto stage_active = [&](int64_t r0) {
-      const int klo = (int)(r0 / cin_p);
-      int khi = (int)((r0 + KC - 1) / cin_p);
+    auto stage_active = [&](int st) {
+      if (ALIGNED) return ((kmask >> (st / spk)) & 1ull) != 0ull;
+      const int klo = (st * KC) / cin_p;
+      int khi = (st * KC + KC - 1) / cin_p;
       if (khi > K - 1) khi = K - 1;
       const int span = khi - klo + 1;
       const u64 bits = (span >= 64 ? ~0ull : ((1ull << span) - 1)) << klo;
       return (kmask & bits) != 0ull;
     };
-    auto next_stage = [&](int64_t r0) {
-      while (r0 < kend && !stage_active(r0)) r0 += KC;
-      return r0;
+    auto next_stage = [&](int st) {
+      while (st < nst && !stage_active(st)) ++st;
+      return st;
     };
 
     uint4 ra[AV], rb[BV];
-    auto load_stage = [&](int64_t r0) {
+    // stage st = (kc, sub) in the aligned case (kc, sub updated before the
+    // call)
+    int kc_l = 0, sub_l = 0;
+    auto load_stage = [&](int st) {
+      const int r0 = st * KC;
+      const int ks = kc_l;
+      const int cs = sub_l * KC;
 #pragma unroll
       for (int q = 0; q < AV; ++q) {
         const int v = tid + q * 256;
         const int m = v / VPR, cv = v - (v / VPR) * VPR;
-        const int64_t r = r0 + cv * VEC;
-        const int k = (int)(r / cin_p);
-        const int ci = (int)(r - (int64_t)k * cin_p);
+        int k, ci;
+        if (ALIGNED) {
+          k = ks;
+          ci = cs + cv * VEC;
+        } else {
+          const int r = r0 + cv * VEC;
+          k = r / cin_p;
+          ci = r - k * cin_p;
+        }
         const int src = k < K ? s_nbr[k * BM + m] : -1;
         ra[q] = src >= 0 ? *(const uint4*)(din + (int64_t)src * cin_p + ci)
                          : make_uint4(0u, 0u, 0u, 0u);
@@ -742,8 +759,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
         const int nn = v / VPR, cv = v - (v / VPR) * VPR;
         const int n = n0 + nn;
         rb[q] = n < cout_p
-                    ? *(const uint4*)(wt + (int64_t)n * a.ktot_p + r0 +
-                                      cv * VEC)
+                    ? *(const uint4*)(wt + (int64_t)n * ktot_p + r0 + cv * VEC)
                     : make_uint4(0u, 0u, 0u, 0u);
       }
     };
@@ -768,14 +784,40 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
 #pragma unroll
       for (int j = 0; j < 2; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-    int64_t r0 = next_stage(0);
-    if (r0 < kend) load_stage(r0);
+    // aligned: walk stages as (offset k, sub-stage), jumping over offsets
+    // without active neighbours by a bit scan of the offset mask
+    auto next_k = [&](int k) {
+      if (k >= K) return K;
+      const u64 mk = kmask >> k;
+      return mk ? k + __builtin_ctzll(mk) : K;
+    };
+    int kc = 0, sub = 0, st = 0;
+    if (ALIGNED) {
+      kc = next_k(0);
+      st = kc < K ? kc * spk : nst;
+    } else {
+      st = next_stage(0);
+    }
+    kc_l = kc;
+    sub_l = sub;
+    if (st < nst) load_stage(st);
     int buf = 0;
-    while (r0 < kend) {
+    while (st < nst) {
       store_stage(buf);
       __syncthreads();
-      const int64_t r1 = next_stage(r0 + KC);
-      if (r1 < kend) load_stage(r1);   // in flight during the MFMAs below
+      int st1;
+      if (ALIGNED) {
+        if (++sub == spk) {
+          kc = next_k(kc + 1);
+          sub = 0;
+        }
+        st1 = kc < K ? kc * spk + sub : nst;
+      } else {
+        st1 = next_stage(st + 1);
+      }
+      kc_l = kc;
+      sub_l = sub;
+      if (st1 < nst) load_stage(st1);   // in flight during the MFMAs below
       const T* Ab = sA + buf * BM * LD;
       const T* Bb = sB + buf * BN * LD;
       if constexpr (sizeof(T) == 4) {
@@ -825,7 +867,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
         }
       }
       buf ^= 1;
-      r0 = r1;
+      st = st1;
     }
 
     // ---- fused epilogue.  The accumulator tile goes through LDS so that
@@ -914,10 +956,18 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
 
 template <typename T>
 static void gemm_t(hipStream_t s, int grid, size_t lds, const ConvArgs& a) {
-  if (a.ref)
-    k_conv_gemm<T, true><<<grid, 256, lds, s>>>(a);
-  else
-    k_conv_gemm<T, false><<<grid, 256, lds, s>>>(a);
+  const bool aligned = a.cin_p % MmaCfg<T>::KC == 0;
+  if (a.ref) {
+    if (aligned)
+      k_conv_gemm<T, true, true><<<grid, 256, lds, s>>>(a);
+    else
+      k_conv_gemm<T, true, false><<<grid, 256, lds, s>>>(a);
+  } else {
+    if (aligned)
+      k_conv_gemm<T, false, true><<<grid, 256, lds, s>>>(a);
+    else
+      k_conv_gemm<T, false, false><<<grid, 256, lds, s>>>(a);
+  }
 }
 
 void launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
