@@ -110,7 +110,7 @@ ConsList consumers_of(st_net* net, int t) {
   return cl;
 }
 
-void run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
+bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   const WS ws{net->ws};
   const LayerPlan& L = net->layers[i];
   const st_layer_desc& d = L.d;
@@ -177,10 +177,11 @@ void run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   a.grp = (L.pool || L.dw) ? nullptr : grp;
   a.mdone = ws.at<uint32_t>(net->off_mdone);
   a.keep_thr = thr;
+  a.zero = ws.at<char>(net->off_zero);
   if (L.dw)
     launch_conv_dw(pf, s, net->dtype, a);
-  else
-    launch_conv_gemm(pf, s, net->dtype, a);
+  else if (!launch_conv_gemm(pf, s, net->dtype, a))
+    return false;
 
   // non-linear post-op: max-pool from old and new state, then commit
   if (L.pool) {
@@ -232,6 +233,7 @@ void run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   la.cons = consumers_of(net, i + 1);
   launch_list_compact(pf, s, la);
   out.last_thr = thr;
+  return true;
 }
 
 st_status encode(st_net* net, const void* frame, const float* thr, float* out,
@@ -267,7 +269,8 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
   T0.last_thr = thr0;
   const int nl = (int)net->layers.size();
   for (int i = 0; i < nl; ++i)
-    run_layer(net, i, ref, ref ? -1.f : thr[i + 1], s);
+    if (!run_layer(net, i, ref, ref ? -1.f : thr[i + 1], s))
+      return fail(net, ST_ERR_HIP, "internal: GEMM launch arguments");
 
   if (out) {
     const LayerPlan& L = net->layers[nl - 1];

@@ -82,6 +82,7 @@ struct st_net {
   size_t off_tiles = 0;                    // uint32 [kMaxTiles]
   size_t off_grp = 0;                      // uint32 [max grid / 64 + 1]
   size_t off_mdone = 0;                    // uint32 [max grid / 64 + 1]
+  size_t off_zero = 0;                     // 256 zero bytes
   size_t off_cnt = 0;                      // uint64 [n_counters]
   size_t off_cleanup = 0;                  // cleanup descriptor table
   size_t off_dens = 0;                     // uint64 [batch] per-image counts

@@ -118,8 +118,10 @@ struct ConvArgs {
   uint32_t* grp;       // per-64-row kept counts (or NULL)
   uint32_t* mdone;     // per-row-tile arrival counters (zero between uses)
   float keep_thr;      // threshold of the emitted tensor
+  const void* zero;    // 16 zero bytes (16-byte aligned)
 };
-void launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
+// Returns false (and launches nothing) when a.zero is missing or misaligned.
+bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
                       const ConvArgs& a);
 void launch_conv_dw(const Prof& pf, hipStream_t s, int dtype,
                     const ConvArgs& a);

@@ -642,6 +642,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
 
   const T* din = (const T*)a.din;
   const T* wt = (const T*)a.w;
+  const T* zvec = (const T*)a.zero;
   T* dout = (T*)a.dout;
   const T* dskip = (const T*)a.dskip;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -715,7 +716,6 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     const u64 kmask = s_kmask;
 
     auto stage_active = [&](int st) {
-      if (ALIGNED) return ((kmask >> (st / spk)) & 1ull) != 0ull;
       const int klo = (st * KC) / cin_p;
       int khi = (st * KC + KC - 1) / cin_p;
       if (khi > K - 1) khi = K - 1;
@@ -723,47 +723,79 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
       const u64 bits = (span >= 64 ? ~0ull : ((1ull << span) - 1)) << klo;
       return (kmask & bits) != 0ull;
     };
-    auto next_stage = [&](int st) {
-      while (st < nst && !stage_active(st)) ++st;
-      return st;
+    auto next_k = [&](int k) {
+      if (k >= K) return K;
+      const u64 mk = kmask >> k;
+      return mk ? k + __builtin_ctzll(mk) : K;
+    };
+    // Stage iterator.  ALIGNED: stages are walked as (offset kc, sub-stage)
+    // pairs, jumping over offsets without active neighbours by a bit scan of
+    // the offset mask; otherwise stage by stage with the span test.
+    struct It {
+      int kc, sub, st;
+    };
+    auto first_stage = [&]() {
+      It it{0, 0, 0};
+      if (ALIGNED) {
+        it.kc = next_k(0);
+        it.st = it.kc < K ? it.kc * spk : nst;
+      } else {
+        while (it.st < nst && !stage_active(it.st)) ++it.st;
+      }
+      return it;
+    };
+    auto advance = [&](It it) {
+      if (it.st >= nst) return it;
+      if (ALIGNED) {
+        if (++it.sub == spk) {
+          it.kc = next_k(it.kc + 1);
+          it.sub = 0;
+        }
+        it.st = it.kc < K ? it.kc * spk + it.sub : nst;
+      } else {
+        ++it.st;
+        while (it.st < nst && !stage_active(it.st)) ++it.st;
+      }
+      return it;
     };
 
-    uint4 ra[AV], rb[BV];
-    // stage st = (kc, sub) in the aligned case (kc, sub updated before the
-    // call)
-    int kc_l = 0, sub_l = 0;
-    auto load_stage = [&](int st) {
-      const int r0 = st * KC;
-      const int ks = kc_l;
-      const int cs = sub_l * KC;
+    // Loads of one stage into a register slot.  Every lane always issues
+    // its loads (inactive neighbours, columns past cout_p and stages past
+    // the end read a zero vector), so the loads of the next two stages can
+    // stay in flight while the current one is staged and multiplied.
+    auto load_stage = [&](const It& it, uint4 (&ra)[AV], uint4 (&rb)[BV]) {
+      const bool live = it.st < nst;
+      const int r0 = it.st * KC;
 #pragma unroll
       for (int q = 0; q < AV; ++q) {
         const int v = tid + q * 256;
         const int m = v / VPR, cv = v - (v / VPR) * VPR;
         int k, ci;
         if (ALIGNED) {
-          k = ks;
-          ci = cs + cv * VEC;
+          k = it.kc;
+          ci = it.sub * KC + cv * VEC;
         } else {
           const int r = r0 + cv * VEC;
           k = r / cin_p;
           ci = r - k * cin_p;
         }
-        const int src = k < K ? s_nbr[k * BM + m] : -1;
-        ra[q] = src >= 0 ? *(const uint4*)(din + (int64_t)src * cin_p + ci)
-                         : make_uint4(0u, 0u, 0u, 0u);
+        const int src = (live && k < K) ? s_nbr[k * BM + m] : -1;
+        const T* pa = src >= 0 ? din + (int64_t)src * cin_p + ci : zvec;
+        ra[q] = *(const uint4*)pa;
       }
 #pragma unroll
       for (int q = 0; q < BV; ++q) {
         const int v = tid + q * 256;
         const int nn = v / VPR, cv = v - (v / VPR) * VPR;
         const int n = n0 + nn;
-        rb[q] = n < cout_p
-                    ? *(const uint4*)(wt + (int64_t)n * ktot_p + r0 + cv * VEC)
-                    : make_uint4(0u, 0u, 0u, 0u);
+        const T* pb = (live && n < cout_p)
+                          ? wt + (int64_t)n * ktot_p + r0 + cv * VEC
+                          : zvec;
+        rb[q] = *(const uint4*)pb;
       }
     };
-    auto store_stage = [&](int buf) {
+    auto store_stage = [&](int buf, const uint4 (&ra)[AV],
+                           const uint4 (&rb)[BV]) {
 #pragma unroll
       for (int q = 0; q < AV; ++q) {
         const int v = tid + q * 256;
@@ -784,40 +816,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
 #pragma unroll
       for (int j = 0; j < 2; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-    // aligned: walk stages as (offset k, sub-stage), jumping over offsets
-    // without active neighbours by a bit scan of the offset mask
-    auto next_k = [&](int k) {
-      if (k >= K) return K;
-      const u64 mk = kmask >> k;
-      return mk ? k + __builtin_ctzll(mk) : K;
-    };
-    int kc = 0, sub = 0, st = 0;
-    if (ALIGNED) {
-      kc = next_k(0);
-      st = kc < K ? kc * spk : nst;
-    } else {
-      st = next_stage(0);
-    }
-    kc_l = kc;
-    sub_l = sub;
-    if (st < nst) load_stage(st);
-    int buf = 0;
-    while (st < nst) {
-      store_stage(buf);
-      __syncthreads();
-      int st1;
-      if (ALIGNED) {
-        if (++sub == spk) {
-          kc = next_k(kc + 1);
-          sub = 0;
-        }
-        st1 = kc < K ? kc * spk + sub : nst;
-      } else {
-        st1 = next_stage(st + 1);
-      }
-      kc_l = kc;
-      sub_l = sub;
-      if (st1 < nst) load_stage(st1);   // in flight during the MFMAs below
+    auto compute = [&](int buf) {
       const T* Ab = sA + buf * BM * LD;
       const T* Bb = sB + buf * BN * LD;
       if constexpr (sizeof(T) == 4) {
@@ -866,8 +865,31 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
           }
         }
       }
+    };
+
+    // two stages in flight: slot 0 / slot 1 alternate
+    uint4 ra0[AV], rb0[BV], ra1[AV], rb1[BV];
+    It ia = first_stage();
+    load_stage(ia, ra0, rb0);
+    It ib = advance(ia);
+    load_stage(ib, ra1, rb1);
+    int buf = 0;
+    while (ia.st < nst) {
+      store_stage(buf, ra0, rb0);
+      __syncthreads();
+      const It ic = advance(ib);
+      load_stage(ic, ra0, rb0);
+      compute(buf);
       buf ^= 1;
-      st = st1;
+      if (ib.st >= nst) break;
+      store_stage(buf, ra1, rb1);
+      __syncthreads();
+      const It id = advance(ic);
+      load_stage(id, ra1, rb1);
+      compute(buf);
+      buf ^= 1;
+      ia = ic;
+      ib = id;
     }
 
     // ---- fused epilogue.  The accumulator tile goes through LDS so that
@@ -970,8 +992,10 @@ static void gemm_t(hipStream_t s, int grid, size_t lds, const ConvArgs& a) {
   }
 }
 
-void launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
+bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
                       const ConvArgs& a) {
+  // inactive lanes read the zero vector: never launch without it
+  if (!a.zero || ((uintptr_t)a.zero & 15)) return false;
   const int64_t worst = ((a.capO + kGemmBM - 1) / kGemmBM) *
                         ((a.cout_p + kGemmBN - 1) / kGemmBN);
   // persistent blocks: about what the 256 CUs hold at once
@@ -986,6 +1010,7 @@ void launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
   else
     gemm_t<bf16_t>(s, (int)grid, lds, a);
   prof_end(pf, 7, s);
+  return true;
 }
 
 // ---------------------------------------------------- (c') depthwise path

@@ -215,6 +215,7 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
   net->off_flags = a.take(round_up(t0.grid, 16));
   net->off_grp = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
   net->off_mdone = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
+  net->off_zero = a.take(256);
   net->n_cleanup = n_cleanup;
   net->off_cleanup = a.take(32 * n_cleanup);
   net->ws_bytes = round_up(a.top, kAlign);
