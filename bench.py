@@ -202,6 +202,135 @@ def cpu_baseline(wl, net, thr_val):
             "cpu_model": cpu}
 
 
+COPY_BYTES = 256 << 20
+
+
+def copy_calibration():
+    """A plain device-to-device copy of COPY_BYTES, launched 10 times: the
+    reference whose FETCH_SIZE / WRITE_SIZE counters convert the conv
+    kernel's counter readings into bytes."""
+    import torch
+    x = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(10):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 10}))
+
+
+def kernel_source_hash():
+    import hashlib
+    src = os.path.join(ROOT, "paper_2410_20790_amd", "csrc",
+                       "st_kernels.hip")
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(workload_desc, kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (profiles/hbm_traffic.json), or None when it is missing, was taken on
+    another workload, or the kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    try:
+        d = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    e = d.get(workload_desc, {}).get(kernel)
+    if not e or e.get("source_hash") != kernel_source_hash():
+        return None
+    return e.get("bytes_per_launch")
+
+
+KCLASS = {"k_conv_gemm": "conv_gemm", "k_conv_dw": "conv_dw",
+          "k_pool_emit": "pool_emit", "k_commit": "commit",
+          "k_output": "output"}
+
+
+def ingest_counters(base, workload_name, density):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the diff-pass kernels,
+    scaled by what the same counters read for a plain copy of COPY_BYTES,
+    averaged per launch; written to profiles/hbm_traffic.json with the
+    kernel source hash."""
+    import csv
+    import collections
+
+    def rows(name):
+        path = os.path.join(base, name, "run_counter_collection.csv")
+        return list(csv.DictReader(open(path)))
+
+    scale = {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        v = [float(r["Counter_Value"]) for r in rows(f"pmc_copy_{c}")
+             if "copyBuffer" in r["Kernel_Name"]]
+        scale[c] = (COPY_BYTES / 1024.0) / (sum(v) / len(v))
+    per = collections.defaultdict(lambda: collections.defaultdict(list))
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        for r in rows(f"pmc_bench_{c}"):
+            head = r["Kernel_Name"].split("(")[0]
+            fn = head.split("<")[0].split("::")[-1]
+            targs = (head.split("<", 1)[1].rstrip(">").split(", ")
+                     if "<" in head else [])
+            if fn not in KCLASS:
+                continue
+            if fn in ("k_conv_gemm", "k_conv_dw") and targs[1:2] == ["true"]:
+                continue  # reference-pass instantiations
+            per[KCLASS[fn]][c].append(float(r["Counter_Value"]))
+    wl = workload(workload_name, density)
+    out_path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    try:
+        d = json.load(open(out_path))
+    except (OSError, ValueError):
+        d = {}
+    entry = {}
+    for k, v in per.items():
+        f = sum(v["FETCH_SIZE"]) / max(len(v["FETCH_SIZE"]), 1)
+        w = sum(v["WRITE_SIZE"]) / max(len(v["WRITE_SIZE"]), 1)
+        entry[k] = {"bytes_per_launch": 1024.0 * (f * scale["FETCH_SIZE"] +
+                                                  w * scale["WRITE_SIZE"]),
+                    "fetch_kib_raw": f, "write_kib_raw": w,
+                    "launches": len(v["FETCH_SIZE"]),
+                    "scale": scale, "source_hash": kernel_source_hash()}
+    d[wl["desc"]] = entry
+    json.dump(d, open(out_path, "w"), indent=1, sort_keys=True)
+    print(json.dumps(entry))
+
+
+def density_sweep(net, thr, densities, steps):
+    """diff-frames/s and algorithmic TFLOP/s at several change densities of
+    the same video recipe (each: reference + 2 warm-up + `steps` timed
+    frames)."""
+    import torch
+    from paper_2410_20790_amd import SparseTemNet
+    from paper_2410_20790_amd import binding as B
+    from workloads import driving_video
+    tdt = torch.bfloat16 if net.dtype == "bf16" else torch.float32
+    out = {}
+    g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, net.dtype)
+    o = g.new_output()
+    L_n = len(net.layers)
+    for d in densities:
+        fr = [torch.from_numpy(f).to("cuda", tdt) for f in driving_video(
+            seed=7, n_frames=3 + steps, H=net.H, W=net.W, density=d)]
+        g.encode_reference(fr[0], out=o)
+        for i in (1, 2):
+            g.encode_diff(fr[i], [thr] * (L_n + 1), out=o)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(3, 3 + steps):
+            g.encode_diff(fr[i], [thr] * (L_n + 1), out=o)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1000.0 / steps
+        pairs, _ = B.st_debug_counters(g.handle, L_n)
+        fl = sum(2 * int(pairs[j]) * (L.c_in // L.groups) * L.c_out
+                 for j, L in enumerate(net.layers))
+        out[f"{d:g}"] = {"ms_per_frame": ms, "diff_frames_per_s": 1000.0 / ms,
+                         "input_density": g.density(-1),
+                         "alg_gflop": fl / 1e9,
+                         "effective_tflops": fl / (ms * 1e-3) / 1e12}
+        del fr
+    g.close()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -214,7 +343,22 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--sweep-steps", type=int, default=10)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of a known size "
+                         "(reference kernel for the HBM byte counters)")
+    ap.add_argument("--ingest-counters", metavar="DIR",
+                    help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs "
+                         "(DIR/pmc_{bench,copy}_{FETCH,WRITE}_SIZE) into "
+                         "profiles/hbm_traffic.json")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    if args.ingest_counters:
+        ingest_counters(args.ingest_counters, args.workload, args.density)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -340,6 +484,9 @@ def main():
             roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
                     "traffic": None}
+        tb = measured_traffic(wl["desc"], dom)
+        if tb is not None:
+            roof["traffic"] = tb
         roof.update({"kernel": dom, "launches": dc["launches"],
                      "avg_launch_us": avg_s * 1e6,
                      "alg_bytes_per_launch": dc["bytes"] / dc["launches"],
@@ -390,7 +537,12 @@ def main():
     res["kernels"] = kern
     res["profiled_ms_per_step"] = prof_ms_step
     res["frame_gen_s"] = t_gen
+    res["kernel_source_hash"] = kernel_source_hash()
     g.close()
+    del frames
+    if args.workload == "resnet50" and not args.no_sweep:
+        res["density_sweep"] = density_sweep(
+            net, args.thr, [0.02, 0.05, 0.10, 0.20, 0.40], args.sweep_steps)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, net, args.thr)
     print(json.dumps(res), flush=True)
