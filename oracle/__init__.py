@@ -10,10 +10,10 @@ it; the two meet only on identical seeded inputs from ``workloads``.
 from .sparsetem_oracle import (ACT_NONE, ACT_RELU, ACT_SILU, OracleNet,
                                activation, conv2d_nhwc, dense_forward,
                                maxpool_nhwc, round_storage, rulebook,
-                               window_targets)
+                               se_apply, se_gates, window_targets)
 
 __all__ = [
     "ACT_NONE", "ACT_RELU", "ACT_SILU", "OracleNet", "activation",
     "conv2d_nhwc", "dense_forward", "maxpool_nhwc", "round_storage",
-    "rulebook", "window_targets",
+    "rulebook", "se_apply", "se_gates", "window_targets",
 ]

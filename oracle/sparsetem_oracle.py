@@ -30,7 +30,10 @@ Readings of points the paper leaves open (all listed in the design notes):
 5. Bias enters only the reference pass; it cancels in deltas (Eq. 2).
 6. Convolution / max-pool follow PyTorch's conv2d / max_pool2d geometry
    (stride, zero padding, groups; -inf pool padding).  The delta of a
-   pooled layer is max_window f(P_new) - max_window f(P_old).
+   pooled layer is max_window f(P_new) - max_window f(P_old).  A
+   squeeze-excitation layer keeps its gates s (per image and channel) as
+   state; its delta is f(P_new) * s_new - f(P_old) * s_old at every site,
+   with s recomputed from the dense activation of the frame.
 7. Sums are accumulated in fp64 and rounded once to f32; the pre-activation
    state is f32; emitted deltas are rounded to the storage dtype with
    round-to-nearest-even; the mask is taken on the rounded values.
@@ -131,6 +134,26 @@ def maxpool_nhwc(x, k, s, p):
     return out
 
 
+def se_gates(a32, L):
+    """Squeeze-excitation gates of activation map a32 [N,H,W,C] (f32):
+    s[n] = sigmoid(W2 @ silu(W1 @ mean_hw(a[n]) + b1) + b2), each stage
+    evaluated in fp64 and rounded to f32."""
+    a = np.asarray(a32, dtype=np.float32).astype(np.float64)
+    m = f32(a.mean(axis=(1, 2)))                           # [N, C]
+    w1 = np.asarray(L.se_w1, np.float64)
+    w2 = np.asarray(L.se_w2, np.float64)
+    z = f32(m.astype(np.float64) @ w1.T + np.asarray(L.se_b1, np.float64))
+    z = activation(z, ACT_SILU)
+    e = z.astype(np.float64) @ w2.T + np.asarray(L.se_b2, np.float64)
+    return f32(1.0 / (1.0 + np.exp(-f32(e).astype(np.float64))))
+
+
+def se_apply(a32, s):
+    """Channel gating a * s (f32 product) of a [N,H,W,C] by s [N,C]."""
+    return f32(np.asarray(a32, np.float64) * np.asarray(s, np.float64)
+               [:, None, None, :])
+
+
 # ------------------------------------------------------- sparse geometry
 
 def window_targets(pix, in_hw, out_hw, k, s, p):
@@ -216,17 +239,17 @@ def _apply_offset(rows, w, ky, kx, groups):
     return out
 
 
-def dense_forward(layers, frame, dtype):
+def dense_forward(layers, frame, dtype, with_se=False):
     """Plain dense forward of one frame (the definition the diff chain must
     reproduce at threshold 0): returns (out, P, acts) where P[i] is the f32
     pre-activation of every stateful layer, acts[i] the emitted activation
-    rounded to the storage dtype, and out the f32 network output."""
+    rounded to the storage dtype, and out the f32 network output; with
+    with_se also the squeeze-excitation gates S[i]."""
     acts = {-1: round_storage(frame, dtype)}
     P = {}
+    S = {}
     out = None
     for i, L in enumerate(layers):
-        if L.se_mid:
-            raise NotImplementedError("squeeze-excitation")
         a = conv2d_nhwc(acts[L.src], L.weight, L.bias, L.s, L.p, L.groups)
         if L.residual_src != -2:
             a = a + acts[L.residual_src]
@@ -237,12 +260,15 @@ def dense_forward(layers, frame, dtype):
             if L.pool_k[0] > 0:
                 e = maxpool_nhwc(e, L.pool_k, L.pool_s, L.pool_p)
             e32 = f32(e)
+            if L.se_mid:
+                S[i] = se_gates(e32, L)
+                e32 = se_apply(e32, S[i])
         else:
             e32 = p32
         acts[i] = round_storage(e32, dtype)
         if i == len(layers) - 1:
             out = e32
-    return out, P, acts
+    return (out, P, acts, S) if with_se else (out, P, acts)
 
 
 class OracleNet:
@@ -271,6 +297,7 @@ class OracleNet:
                          for i in range(len(self.layers))]
         self.xhat = None
         self.P = {}
+        self.S = {}
         self.last = None
 
     # -- reference frame ---------------------------------------------------
@@ -279,9 +306,11 @@ class OracleNet:
         Subtraction buffer and the cached pre-activations (SparseBatch)."""
         frame = np.asarray(frame, dtype=np.float64)
         assert frame.shape == self.in_shape
-        out, P, acts = dense_forward(self.layers, frame, self.dtype)
+        out, P, acts, S = dense_forward(self.layers, frame, self.dtype,
+                                        with_se=True)
         self.xhat = round_storage(frame, self.dtype)
         self.P = {i: p.copy() for i, p in P.items()}
+        self.S = {i: g.copy() for i, g in S.items()}
         self.last = dict(kind="reference", out=out, acts=acts)
         return out
 
@@ -343,7 +372,23 @@ class OracleNet:
                 Pg = self.P[i].reshape(N * g.Ho * g.Wo, L.c_out)
                 P_old = Pg[O].copy()
                 P_new = f32(P_old.astype(np.float64) + dP32)
-                if g.pool:
+                if L.se_mid:
+                    # Squeeze-excitation (reading 6): the gates follow the
+                    # dense activation, so every site's output moves:
+                    # delta = f(P_new) * s_new - f(P_old) * s_old.
+                    a_old = activation(Pg.reshape(N, g.Ho, g.Wo, L.c_out),
+                                       L.act)
+                    Pg[O] = P_new
+                    a_new = activation(Pg.reshape(N, g.Ho, g.Wo, L.c_out),
+                                       L.act)
+                    s_new = se_gates(a_new, L)
+                    e_old = se_apply(a_old, self.S[i]).reshape(-1, L.c_out)
+                    e_new = se_apply(a_new, s_new).reshape(-1, L.c_out)
+                    self.S[i] = s_new
+                    d32 = f32(e_new.astype(np.float64)
+                              - e_old.astype(np.float64))
+                    cand = np.arange(N * g.Ho * g.Wo, dtype=np.int64)
+                elif g.pool:
                     T = window_targets(O, (g.Ho, g.Wo), (g.Hp, g.Wp),
                                        L.pool_k, L.pool_s, L.pool_p)
                     Q = np.unique(T[:, 2]).astype(np.int64)
@@ -387,7 +432,10 @@ class OracleNet:
         e = activation(self.P[i], L.act).astype(np.float64)
         if g.pool:
             e = maxpool_nhwc(e, L.pool_k, L.pool_s, L.pool_p)
-        return f32(e)
+        e = f32(e)
+        if L.se_mid:
+            e = se_apply(e, self.S[i])
+        return e
 
     # -- introspection -----------------------------------------------------
     def density(self, t):

@@ -19,8 +19,9 @@ import torch.nn.functional as F
 import oracle
 from oracle import sparsetem_oracle as so
 from workloads import (ACT_NONE, ACT_RELU, ACT_SILU, LayerSpec, crnn_vgg_net,
-                       depthwise_test_net, random_sparse_video,
-                       resnet_mini_net, textline_video, toy_net, toy_video)
+                       depthwise_test_net, efficientnet_mini_net,
+                       random_sparse_video, resnet_mini_net, textline_video,
+                       toy_net, toy_video)
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -101,6 +102,26 @@ def test_activation_matches_torch():
                                F.silu(xt).numpy().astype(np.float32),
                                rtol=2e-7, atol=1e-30)
     np.testing.assert_array_equal(oracle.activation(x, ACT_NONE), x)
+
+
+def test_se_gates_match_torch():
+    """Squeeze-excitation gates against a torch formulation (adaptive average
+    pool, two 1x1 convolutions, SiLU, sigmoid) in fp64."""
+    net = efficientnet_mini_net()
+    L = [l for l in net.layers if l.se_mid][1]
+    rng = np.random.default_rng(11)
+    a = rng.standard_normal((2, 5, 7, L.c_out)).astype(np.float32)
+    ours = oracle.se_gates(a, L)
+    at = torch.from_numpy(a.astype(np.float64)).permute(0, 3, 1, 2)
+    m = F.adaptive_avg_pool2d(at, 1)
+    z = F.silu(F.conv2d(m, torch.from_numpy(L.se_w1.astype(np.float64))
+                        [:, :, None, None],
+                        torch.from_numpy(L.se_b1.astype(np.float64))))
+    e = F.conv2d(z, torch.from_numpy(L.se_w2.astype(np.float64))
+                 [:, :, None, None], torch.from_numpy(L.se_b2.astype(
+                     np.float64)))
+    ref = torch.sigmoid(e)[:, :, 0, 0].numpy()
+    np.testing.assert_allclose(ours, ref, rtol=2e-6, atol=1e-7)
 
 
 # ------------------------------------------------------- rulebook pins
@@ -196,6 +217,8 @@ def small_cases():
          random_sparse_video(7, 4, 1, 24, 40, 16, 0.1)),
         ("crnn_small", crnn_vgg_net(H=16, W=32),
          textline_video(seed=1, n_frames=4, H=16, W=32, band=3)),
+        ("effnet_mini", efficientnet_mini_net(),
+         random_sparse_video(3, 4, 1, 32, 40, 3, 0.08)),
     ]
 
 
@@ -234,8 +257,11 @@ def test_threshold_zero_equals_dense_bf16():
         assert rel_err(out, dense) < 2e-2
 
 
-@pytest.mark.parametrize("name,net,frames", small_cases()[:3],
-                         ids=[c[0] for c in small_cases()[:3]])
+ZERO_CASES = [small_cases()[i] for i in (0, 1, 2, 5)]
+
+
+@pytest.mark.parametrize("name,net,frames", ZERO_CASES,
+                         ids=[c[0] for c in ZERO_CASES])
 def test_zero_delta_is_identity(name, net, frames):
     """A frame equal to the committed input has no diff pixel at any layer
     and leaves output and state bitwise unchanged."""
@@ -327,8 +353,23 @@ def dense_delta_sim(net, frames, thr):
     is a full map that is zero on truncated pixels; convolutions go through
     torch conv2d.  Written independently of the oracle's sparse code."""
     layers = net.layers
-    stateful = [L.act != ACT_NONE or L.pool_k[0] > 0 or i == len(layers) - 1
-                for i, L in enumerate(layers)]
+    stateful = [L.act != ACT_NONE or L.pool_k[0] > 0 or L.se_mid > 0
+                or i == len(layers) - 1 for i, L in enumerate(layers)]
+
+    def gates(a, L):
+        # squeeze-excitation re-stated with torch ops
+        at = torch.from_numpy(a.astype(np.float64))
+        m = at.mean(dim=(1, 2)).float().double()
+        z = (m @ torch.from_numpy(L.se_w1.astype(np.float64)).T
+             + torch.from_numpy(L.se_b1.astype(np.float64))).float().double()
+        z = (z / (1 + torch.exp(-z))).float().double()
+        e = (z @ torch.from_numpy(L.se_w2.astype(np.float64)).T
+             + torch.from_numpy(L.se_b2.astype(np.float64))).float().double()
+        return torch.sigmoid(e).float().numpy()
+
+    def gate(a, g):
+        return (a.astype(np.float64) * g[:, None, None, :].astype(
+            np.float64)).astype(np.float32)
 
     def act(x, a):
         x64 = x.astype(np.float64)
@@ -353,7 +394,7 @@ def dense_delta_sim(net, frames, thr):
 
     # reference
     acts = {-1: frames[0].astype(np.float64)}
-    P = {}
+    P, S = {}, {}
     for i, L in enumerate(layers):
         a = torch_conv_nhwc(acts[L.src], L.weight, L.bias, L.s, L.p, L.groups)
         if L.residual_src != -2:
@@ -361,7 +402,11 @@ def dense_delta_sim(net, frames, thr):
         p32 = a.astype(np.float32)
         if stateful[i]:
             P[i] = p32
-            acts[i] = pool(act(p32, L.act), L).astype(np.float64)
+            e = pool(act(p32, L.act), L)
+            if L.se_mid:
+                S[i] = gates(e, L)
+                e = gate(e, S[i])
+            acts[i] = e.astype(np.float64)
         else:
             acts[i] = p32.astype(np.float64)
     xhat = frames[0].astype(np.float32).copy()
@@ -379,21 +424,32 @@ def dense_delta_sim(net, frames, thr):
             dp32 = dp.astype(np.float32)
             if stateful[i]:
                 Pn = (P[i].astype(np.float64) + dp32).astype(np.float32)
-                e = (pool(act(Pn, L.act), L).astype(np.float64)
-                     - pool(act(P[i], L.act), L).astype(np.float64))
+                en = pool(act(Pn, L.act), L)
+                eo = pool(act(P[i], L.act), L)
+                if L.se_mid:
+                    sn = gates(en, L)
+                    en, eo = gate(en, sn), gate(eo, S[i])
+                    S[i] = sn
+                e = (en.astype(np.float64) - eo.astype(np.float64))
                 P[i] = Pn
                 e = e.astype(np.float32)
             else:
                 e = dp32
             fm.append(np.abs(e).max(axis=-1) > thr[i + 1])
             d[i] = mask(e, thr[i + 1]).astype(np.float64)
-        outs.append(pool(act(P[len(layers) - 1], layers[-1].act), layers[-1]))
+        last = pool(act(P[len(layers) - 1], layers[-1].act), layers[-1])
+        if layers[-1].se_mid:
+            last = gate(last, S[len(layers) - 1])
+        outs.append(last)
         masks.append(fm)
     return outs, masks
 
 
-@pytest.mark.parametrize("name,net,frames", small_cases()[:4],
-                         ids=[c[0] for c in small_cases()[:4]])
+SIM_CASES = [small_cases()[i] for i in (0, 1, 2, 3, 5)]
+
+
+@pytest.mark.parametrize("name,net,frames", SIM_CASES,
+                         ids=[c[0] for c in SIM_CASES])
 @pytest.mark.parametrize("thr", [0.0, 0.05])
 def test_matches_dense_delta_simulation(name, net, frames, thr):
     thrs = [thr] * (len(net.layers) + 1)

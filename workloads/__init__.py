@@ -13,14 +13,16 @@ representable in the network's storage dtype (``"f32"``, ``"f16"`` or
 """
 
 from .nets import (ACT_NONE, ACT_RELU, ACT_SILU, LayerSpec, NetSpec,
-                   crnn_vgg_net, depthwise_test_net, resnet50_net,
-                   resnet_mini_net, toy_net, to_storage)
-from .video import (driving_video, textline_video, toy_video,
-                    random_sparse_video)
+                   crnn_vgg_net, depthwise_test_net, efficientnet_mini_net,
+                   efficientnet_net, resnet50_net, resnet_mini_net, toy_net,
+                   to_storage)
+from .video import (driving_video, object_video, multistream_video,
+                    random_sparse_video, textline_video, toy_video)
 
 __all__ = [
     "ACT_NONE", "ACT_RELU", "ACT_SILU", "LayerSpec", "NetSpec",
-    "crnn_vgg_net", "depthwise_test_net", "resnet50_net", "resnet_mini_net",
-    "toy_net", "to_storage", "driving_video", "textline_video", "toy_video",
-    "random_sparse_video",
+    "crnn_vgg_net", "depthwise_test_net", "efficientnet_mini_net",
+    "efficientnet_net", "resnet50_net", "resnet_mini_net", "toy_net",
+    "to_storage", "driving_video", "object_video", "multistream_video",
+    "random_sparse_video", "textline_video", "toy_video",
 ]

@@ -54,6 +54,12 @@ class LayerSpec:
     se_mid: int = 0
     weight: Optional[np.ndarray] = None   # [Cout, Cin/groups, kh, kw] f32
     bias: Optional[np.ndarray] = None     # [Cout] f32
+    # squeeze-excitation after the activation (se_mid > 0):
+    # s = sigmoid(se_w2 @ silu(se_w1 @ mean_hw(a) + se_b1) + se_b2)
+    se_w1: Optional[np.ndarray] = None    # [se_mid, Cout]
+    se_b1: Optional[np.ndarray] = None    # [se_mid]
+    se_w2: Optional[np.ndarray] = None    # [Cout, se_mid]
+    se_b2: Optional[np.ndarray] = None    # [Cout]
     name: str = ""
 
 
@@ -73,6 +79,11 @@ def _finish(layers: List[LayerSpec], dtype: str) -> None:
     for L in layers:
         L.weight = to_storage(L.weight, dtype)
         L.bias = to_storage(L.bias, dtype)
+        if L.se_mid:
+            L.se_w1 = to_storage(L.se_w1, dtype)
+            L.se_b1 = to_storage(L.se_b1, dtype)
+            L.se_w2 = to_storage(L.se_w2, dtype)
+            L.se_b2 = to_storage(L.se_b2, dtype)
 
 
 def toy_net(seed: int = 1000, dtype: str = "f32", H: int = 64, W: int = 64,
@@ -223,3 +234,79 @@ def depthwise_test_net(seed: int = 1021, dtype: str = "f32", H: int = 24,
         L.bias = rng.normal(0.0, 0.02, (L.c_out,)).astype(np.float32)
     _finish(layers, dtype)
     return NetSpec("dw_test", layers, batch, H, W, C, dtype)
+
+
+# EfficientNet-B0 stage table: expansion t, kernel k, stride s, channels c,
+# repeats n.
+B0_STAGES = [(1, 3, 1, 16, 1), (6, 3, 2, 24, 2), (6, 5, 2, 40, 2),
+             (6, 3, 2, 80, 3), (6, 5, 1, 112, 3), (6, 5, 2, 192, 4),
+             (6, 3, 1, 320, 1)]
+
+
+def efficientnet_net(seed: int = 1005, dtype: str = "f16", H: int = 512,
+                     W: int = 512, batch: int = 1, stages=None,
+                     stem: int = 32, name: str = "efficientnet_b0") -> NetSpec:
+    """EfficientNet-B0 backbone (no head): 3x3/2 stem conv + SiLU, then
+    inverted-residual blocks (MBConv): 1x1 expand + SiLU (t > 1), depthwise
+    kxk/s + SiLU + squeeze-excitation (reduction to 1/4 of the block's
+    input channels, SiLU, sigmoid gate), linear 1x1 project, identity skip
+    when stride 1 and channels match.  Batch norm folded; He-normal
+    weights (projection scaled by 0.5), biases ~ N(0, 0.02)."""
+    rng = np.random.default_rng(seed)
+    stages = B0_STAGES if stages is None else stages
+    layers: List[LayerSpec] = []
+
+    def add(L):
+        layers.append(L)
+        return len(layers) - 1
+
+    st = LayerSpec(src=-1, c_in=3, c_out=stem, k=(3, 3), s=(2, 2), p=(1, 1),
+                   act=ACT_SILU, name="stem")
+    st.weight = _he(rng, stem, 3, 3, 3)
+    st.bias = rng.normal(0.0, 0.02, (stem,)).astype(np.float32)
+    prev, cin = add(st), stem
+    for si, (t, k, s_, c, n) in enumerate(stages):
+        for b in range(n):
+            stride = s_ if b == 0 else 1
+            block_in, mid = prev, cin * t
+            src = block_in
+            if t != 1:
+                ex = LayerSpec(src=block_in, c_in=cin, c_out=mid, k=(1, 1),
+                               s=(1, 1), p=(0, 0), act=ACT_SILU,
+                               name=f"b{si}{b}_expand")
+                ex.weight = _he(rng, mid, cin, 1, 1)
+                ex.bias = rng.normal(0.0, 0.02, (mid,)).astype(np.float32)
+                src = add(ex)
+            se = max(1, int(cin * 0.25))
+            dw = LayerSpec(src=src, c_in=mid, c_out=mid, k=(k, k),
+                           s=(stride, stride), p=(k // 2, k // 2), groups=mid,
+                           act=ACT_SILU, se_mid=se, name=f"b{si}{b}_dw")
+            dw.weight = _he(rng, mid, 1, k, k)
+            dw.bias = rng.normal(0.0, 0.02, (mid,)).astype(np.float32)
+            dw.se_w1 = rng.normal(0.0, np.sqrt(2.0 / mid),
+                                  (se, mid)).astype(np.float32)
+            dw.se_b1 = rng.normal(0.0, 0.02, (se,)).astype(np.float32)
+            dw.se_w2 = rng.normal(0.0, np.sqrt(1.0 / se),
+                                  (mid, se)).astype(np.float32)
+            dw.se_b2 = rng.normal(1.0, 0.2, (mid,)).astype(np.float32)
+            d_i = add(dw)
+            pr = LayerSpec(src=d_i, c_in=mid, c_out=c, k=(1, 1), s=(1, 1),
+                           p=(0, 0), act=ACT_NONE,
+                           residual_src=(block_in if (stride == 1 and
+                                                      cin == c) else -2),
+                           name=f"b{si}{b}_project")
+            pr.weight = _he(rng, c, mid, 1, 1, scale=0.5)
+            pr.bias = rng.normal(0.0, 0.02, (c,)).astype(np.float32)
+            prev = add(pr)
+            cin = c
+    _finish(layers, dtype)
+    return NetSpec(name, layers, batch, H, W, 3, dtype)
+
+
+def efficientnet_mini_net(seed: int = 1015, dtype: str = "f32", H: int = 32,
+                          W: int = 40, batch: int = 1) -> NetSpec:
+    """Three MBConv blocks of the B0 kinds (no-expand block, expand + 5x5
+    stride-2 block, block with identity skip) at small widths."""
+    return efficientnet_net(seed, dtype, H, W, batch,
+                            stages=[(1, 3, 1, 8, 1), (4, 5, 2, 12, 2)],
+                            stem=8, name="efficientnet_mini")

@@ -146,3 +146,64 @@ def random_sparse_video(seed: int, n_frames: int, N: int, H: int, W: int,
         f[m] = scale * rng.random((int(m.sum()), C), dtype=np.float32)
         frames.append(to_storage(f, dtype))
     return frames
+
+
+def object_video(seed: int = 0, n_frames: int = 8, N: int = 1, H: int = 512,
+                 W: int = 512, C: int = 3, obj_frac: float = 0.03,
+                 obj: int = 32, dtype: str = "f16") -> List[np.ndarray]:
+    """Detection-like frames: a Gaussian-blurred (sigma = 4 px) noise canvas
+    scaled to [0, 1] translated by 1-2 px per frame along a random
+    direction, plus ceil(obj_frac * H * W / obj^2) textured obj x obj objects
+    moving 2-4 px per frame."""
+    rng = np.random.default_rng(seed)
+    pad = 8 * n_frames + 16
+    canvas = torch.from_numpy(rng.random((N * C, 1, H + 2 * pad,
+                                          W + 2 * pad), dtype=np.float32))
+    r = torch.arange(-12, 13, dtype=torch.float32)
+    k1 = torch.exp(-r ** 2 / (2 * 4.0 ** 2))
+    k1 = (k1 / k1.sum())
+    canvas = F.conv2d(canvas, k1.view(1, 1, 1, -1), padding=(0, 12))
+    canvas = F.conv2d(canvas, k1.view(1, 1, -1, 1), padding=(12, 0))
+    canvas = canvas.view(N, C, H + 2 * pad, W + 2 * pad)
+    lo = canvas.amin(dim=(1, 2, 3), keepdim=True)
+    hi = canvas.amax(dim=(1, 2, 3), keepdim=True)
+    canvas = ((canvas - lo) / (hi - lo)).permute(0, 2, 3, 1).numpy()
+    n_obj = int(np.ceil(obj_frac * H * W / obj ** 2))
+    tex = rng.random((N, n_obj, obj, obj, C), dtype=np.float32)
+    pos = rng.uniform(0, [H - obj, W - obj], (N, n_obj, 2))
+    vel = rng.uniform(2, 4, (N, n_obj, 2)) * rng.choice([-1, 1],
+                                                         (N, n_obj, 2))
+    ang = rng.uniform(0, 2 * np.pi, N)
+    step = rng.uniform(1, 2, N)
+    frames = []
+    for t in range(n_frames):
+        f = np.empty((N, H, W, C), np.float32)
+        for n in range(N):
+            dy = int(round(pad + t * step[n] * np.sin(ang[n])))
+            dx = int(round(pad + t * step[n] * np.cos(ang[n])))
+            f[n] = canvas[n, dy:dy + H, dx:dx + W]
+            for j in range(n_obj):
+                y, x = (pos[n, j] + t * vel[n, j]).astype(int)
+                y = int(np.clip(y, 0, H - obj))
+                x = int(np.clip(x, 0, W - obj))
+                f[n, y:y + obj, x:x + obj] = tex[n, j]
+        frames.append(to_storage(f, dtype))
+    return frames
+
+
+def multistream_video(seed: int = 7, n_frames: int = 8, N: int = 32,
+                      H: int = 256, W: int = 256, C: int = 3,
+                      dens=(0.01, 0.30), dtype: str = "bf16"):
+    """N independent streams: stream s has its own seed (2000 + s) and a
+    change density drawn uniformly from `dens` with the master seed; each
+    stream is a driving-like video whose later frames re-draw rectangles
+    (sides 16-64) until that density is covered.  Returns (frames,
+    densities)."""
+    rng = np.random.default_rng(seed)
+    d = rng.uniform(dens[0], dens[1], N)
+    per = [driving_video(seed=2000 + s, n_frames=n_frames, N=1, H=H, W=W,
+                         C=C, density=float(d[s]), side=(16, 64),
+                         dtype=dtype) for s in range(N)]
+    frames = [np.concatenate([per[s][t] for s in range(N)], axis=0)
+              for t in range(n_frames)]
+    return frames, d
