@@ -25,7 +25,7 @@ KERNEL_CLASSES = [
     "scan_mask", "scan_compact", "rb_mark", "rb_count", "rb_compact",
     "rb_nbr", "rb_ident", "conv_gemm", "conv_dw", "pool_mark", "pool_count",
     "pool_compact", "pool_emit", "commit", "list_count", "list_compact",
-    "output", "cleanup", "reset",
+    "output", "cleanup", "reset", "se_squeeze", "se_excite", "se_emit",
 ]
 
 EXPORTED = [
@@ -58,6 +58,12 @@ class st_launch_record(ctypes.Structure):
 
 
 def _load():
+    # The library must use the HIP runtime PyTorch ships (its device
+    # pointers and streams come from there).  Loaded first, the library
+    # would pull in the system runtime and PyTorch a second copy of it: two
+    # HSA runtimes in one process, and the second to open the device finds
+    # none.  Importing torch first makes the library bind to torch's copy.
+    import torch  # noqa: F401
     if not os.path.exists(LIB_PATH):
         raise ImportError(
             f"{LIB_PATH} is missing: build it with "

@@ -99,7 +99,8 @@ def test_resnet50_workspace_fits_one_gpu():
     ({0: {"p_h": -1}}, B.ST_ERR_INVALID_ARG),
     ({0: {"act": 9}}, B.ST_ERR_INVALID_ARG),
     ({0: {"groups": 4}}, B.ST_ERR_UNSUPPORTED),       # grouped, not depthwise
-    ({0: {"se_mid": 4}}, B.ST_ERR_UNSUPPORTED),
+    ({0: {"se_mid": 4}}, B.ST_ERR_INVALID_ARG),       # no SE weights
+    ({0: {"se_mid": -1}}, B.ST_ERR_INVALID_ARG),
     ({0: {"weight": None}}, B.ST_ERR_INVALID_ARG),
     ({1: {"residual_src": -1}}, B.ST_ERR_INVALID_ARG),  # 16 ch vs 32 out
     ({0: {"pool_k_h": 2, "pool_k_w": 2, "pool_s_h": 2, "pool_s_w": 2,
@@ -169,3 +170,20 @@ def test_workspace_scales_with_batch():
     finally:
         B.st_destroy_net(a)
         B.st_destroy_net(b)
+
+
+def test_single_hip_runtime():
+    """Importing the binding first must not load a second HIP runtime next
+    to PyTorch's (two HSA runtimes in one process cannot share the GPU)."""
+    import subprocess
+    import sys
+    code = ("from paper_2410_20790_amd import binding\n"
+            "import torch\n"
+            "libs = {l.split()[-1] for l in open('/proc/self/maps')\n"
+            "        if 'libamdhip64' in l}\n"
+            "print(len(libs))\n")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c", code], cwd=root,
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.strip().splitlines()[-1] == "1"
