@@ -70,9 +70,19 @@ enum { ST_ACT_NONE = 0, ST_ACT_RELU = 1, ST_ACT_SILU = 2 };
  *   groups        1 (dense) or c_in == c_out == groups (depthwise).
  *   weight        device, storage dtype, [c_out][c_in/groups][k_h][k_w].
  *   bias          device, storage dtype, [c_out]; may be NULL (zero bias).
- *   pool_k_h == 0 means no pool.  se_* must be 0 / NULL in this build.
+ *   pool_k_h == 0 means no pool.
+ *   se_mid > 0    squeeze-excitation after the activation: per image,
+ *                 s = sigmoid(se_w2 . silu(se_w1 . mean_hw(a) + se_b1) + se_b2)
+ *                 and the layer emits a * s.  se_w1 [se_mid][c_out],
+ *                 se_b1 [se_mid], se_w2 [c_out][se_mid], se_b2 [c_out]
+ *                 (device, storage dtype; biases may be NULL).  The gates
+ *                 of the previous frame are kept as state: a diff frame
+ *                 emits f(P_new) * s_new - f(P_old) * s_old at every site
+ *                 (the gates follow the dense activation).  Not combined
+ *                 with a pool.
  * A layer is "stateful" (holds an f32 pre-activation buffer) when it has an
- * activation or a pool, or is the last layer (the network output).
+ * activation, a pool or squeeze-excitation, or is the last layer (the
+ * network output).
  */
 typedef struct st_layer_desc {
   int32_t src;
@@ -92,8 +102,8 @@ typedef struct st_layer_desc {
  * read only by st_bind_workspace.  On success *out owns a new net.
  * Errors: ST_ERR_INVALID_ARG (NULL, n_layers < 1, bad src/residual_src, a
  * channel or shape mismatch, an empty output grid, an unknown dtype or
- * activation), ST_ERR_UNSUPPORTED (groups other than 1 or depthwise,
- * squeeze-excitation). */
+ * activation, squeeze-excitation without its weights), ST_ERR_UNSUPPORTED
+ * (groups other than 1 or depthwise, squeeze-excitation with a pool). */
 st_status st_create_net(const st_layer_desc* layers, int32_t n_layers,
                         int32_t batch, int32_t in_h, int32_t in_w,
                         int32_t in_c, int32_t dtype, st_net** out);
@@ -197,7 +207,8 @@ enum {
   ST_K_RB_COMPACT, ST_K_RB_NBR, ST_K_RB_IDENT, ST_K_CONV_GEMM, ST_K_CONV_DW,
   ST_K_POOL_MARK, ST_K_POOL_COUNT, ST_K_POOL_COMPACT, ST_K_POOL_EMIT,
   ST_K_COMMIT, ST_K_LIST_COUNT, ST_K_LIST_COMPACT, ST_K_OUTPUT,
-  ST_K_CLEANUP, ST_K_RESET, ST_K_NUM_CLASSES
+  ST_K_CLEANUP, ST_K_RESET, ST_K_SE_SQUEEZE, ST_K_SE_EXCITE, ST_K_SE_EMIT,
+  ST_K_NUM_CLASSES
 };
 
 /* Start recording: room for `max_launches` launch records and

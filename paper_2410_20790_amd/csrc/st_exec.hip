@@ -93,8 +93,9 @@ ConsList consumers_of(st_net* net, int t) {
       c.O = ws.at<int>(L.off_O);
       c.Mo = ws.at<int>(L.off_Mo);
       c.nbr = ws.at<int>(L.off_nbr);
-      c.rowmax = L.pool ? nullptr
-                        : ws.at<uint32_t>(net->tensors[j + 1].off_rowmax);
+      c.rowmax = (L.pool || L.se)
+                     ? nullptr
+                     : ws.at<uint32_t>(net->tensors[j + 1].off_rowmax);
       c.cnt_O = cnt + L.cnt_O;
       c.pairs = cnt + L.cnt_pairs;
     } else if (cr.second == 0) {
@@ -127,7 +128,10 @@ bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   u64* cO = cnt + L.cnt_O;
   u64* cpairs = cnt + L.cnt_pairs;
   uint32_t* rowmax_out = ws.at<uint32_t>(out.off_rowmax);
-  uint32_t* rm_O = L.pool ? nullptr : rowmax_out;
+  // pooled and squeeze-excitation layers emit rows of their own (pooled
+  // sites / every site), not the affected conv outputs
+  const bool own_rows = L.pool || L.se;
+  uint32_t* rm_O = own_rows ? nullptr : rowmax_out;
 
   // (b) rulebook: the flags were set while the producers emitted their kept
   // rows; a 1x1 stride-1 layer's rulebook was written there directly.
@@ -163,8 +167,8 @@ bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   a.nO = cO;
   a.capO = L.conv_grid;
   a.P = L.stateful ? ws.at<float>(L.off_P) : nullptr;
-  a.dP = L.pool ? ws.at<float>(L.off_dP) : nullptr;
-  a.dout = L.pool ? nullptr : ws.at<char>(out.off_rows);
+  a.dP = own_rows ? ws.at<float>(L.off_dP) : nullptr;
+  a.dout = own_rows ? nullptr : ws.at<char>(out.off_rows);
   a.rowmax = rm_O;
   if (d.residual_src != -2) {
     const TensorPlan& R = net->tensors[d.residual_src + 1];
@@ -174,7 +178,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   a.mode = L.mode;
   a.act = d.act;
   a.ref = ref ? 1 : 0;
-  a.grp = (L.pool || L.dw) ? nullptr : grp;
+  a.grp = (L.pool || L.dw || L.se) ? nullptr : grp;
   a.mdone = ws.at<uint32_t>(net->off_mdone);
   a.keep_thr = thr;
   a.zero = ws.at<char>(net->off_zero);
@@ -214,9 +218,43 @@ bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
     launch_commit(pf, s, O, cO, L.conv_grid, ws.at<float>(L.off_P),
                   ws.at<float>(L.off_dP), L.cout_p, ref ? 1 : 0);
   }
+  if (L.se) {
+    SeArgs sa{};
+    sa.P = ws.at<float>(L.off_P);
+    sa.dP = ws.at<float>(L.off_dP);
+    sa.Mo = Mo;
+    sa.part = ws.at<float>(L.off_separt);
+    sa.w1 = ws.at<float>(L.off_sew1);
+    sa.b1 = ws.at<float>(L.off_seb1);
+    sa.w2 = ws.at<float>(L.off_sew2);
+    sa.b2 = ws.at<float>(L.off_seb2);
+    float* gates = ws.at<float>(L.off_ses);
+    const int64_t gsz = (int64_t)net->N * L.cout_p;
+    sa.s_old = gates + L.se_par * gsz;
+    sa.s_new = gates + (L.se_par ^ 1) * gsz;
+    sa.dout = ws.at<char>(out.off_rows);
+    sa.rowmax = rowmax_out;
+    sa.rowpix = ws.at<int>(out.off_rowpix);
+    sa.map = ws.at<int>(out.off_map);
+    sa.grp = grp;
+    sa.cnt_rows = cnt + out.cnt_rows;
+    sa.npix = L.conv_grid;
+    sa.hw = (int64_t)L.Ho * L.Wo;
+    sa.N = net->N;
+    sa.cp = L.cout_p;
+    sa.c = d.c_out;
+    sa.mid = L.se_mid;
+    sa.act = d.act;
+    sa.ref = ref ? 1 : 0;
+    sa.chunk = L.se_chunk;
+    sa.nchunk = L.se_nchunk;
+    sa.keep_thr = thr;
+    launch_se(pf, s, net->dtype, sa);
+  }
   if (L.pool || L.dw)
-    launch_group_count(pf, s, rowmax_out, cnt + out.cnt_rows, out.grid, thr,
-                       grp);
+    if (!L.se)
+      launch_group_count(pf, s, rowmax_out, cnt + out.cnt_rows, out.grid,
+                         thr, grp);
 
   // truncation of the emitted delta (shared by every consumer), which also
   // prepares the consumers' rulebooks
@@ -276,9 +314,16 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
     const LayerPlan& L = net->layers[nl - 1];
     const Geo g = L.pool ? pool_geo(L) : Geo{L.Ho, L.Wo, L.Ho, L.Wo, 1, 1,
                                              1, 1, 0, 0};
+    const float* se =
+        L.se ? ws.at<float>(L.off_ses) +
+                   (L.se_par ^ 1) * (int64_t)net->N * L.cout_p
+             : nullptr;
     launch_output(Prof{net, nl - 1}, s, ws.at<float>(L.off_P), L.cout_p,
-                  L.d.c_out, net->N, g, L.pool ? 1 : 0, L.d.act, out);
+                  L.d.c_out, net->N, g, L.pool ? 1 : 0, L.d.act, se, out);
   }
+  // the gates just computed become the previous frame's
+  for (LayerPlan& L : net->layers)
+    if (L.se) L.se_par ^= 1;
   launch_cleanup(pf, s, ws.at<CleanEntry>(net->off_cleanup), net->n_cleanup,
                  net->ws, cnt, net->max_grid);
   if (R && R->n_hist < R->max_frames) {
@@ -347,10 +392,20 @@ extern "C" st_status st_bind_workspace(st_net* net, void* dev_ptr,
                              T.cnt_rows, 0, 0});
   for (const LayerPlan& L : net->layers) {
     const st_layer_desc& d = L.d;
-    if (L.pool) {
+    if (L.pool || L.se) {
       launch_fill_u32(s, ws.at<int>(L.off_Mo), L.conv_grid, 0xFFFFFFFFu);
       tab.push_back(CleanEntry{(int64_t)L.off_Mo, (int64_t)L.off_O, L.cnt_O,
                                0, 0});
+    }
+    if (L.se) {
+      launch_to_f32_pad(s, net->dtype, d.se_w1, ws.at<float>(L.off_sew1),
+                        d.se_mid, d.c_out, d.se_mid, L.cout_p);
+      launch_to_f32_pad(s, net->dtype, d.se_b1, ws.at<float>(L.off_seb1), 1,
+                        d.se_mid, 1, d.se_mid);
+      launch_to_f32_pad(s, net->dtype, d.se_w2, ws.at<float>(L.off_sew2),
+                        d.c_out, d.se_mid, L.cout_p, d.se_mid);
+      launch_to_f32_pad(s, net->dtype, d.se_b2, ws.at<float>(L.off_seb2), 1,
+                        d.c_out, 1, L.cout_p);
     }
     if (L.dw)
       launch_repack_dw(s, net->dtype, d.weight, ws.at<float>(L.off_w),

@@ -51,6 +51,9 @@ struct LayerPlan {
   int64_t ktot = 0, ktot_p = 0;     // K*cin_p and its padding to the GEMM chunk
   int64_t conv_grid = 0;            // N*Ho*Wo
   bool stateful = false, pool = false, dw = false, ident = false;
+  bool se = false;                  // squeeze-excitation after the act
+  int se_mid = 0, se_chunk = 0, se_nchunk = 0;
+  int se_par = 0;                   // which gate buffer holds the last gates
   int mode = 0;                     // epilogue mode (kModeState/Defer/Linear)
   // workspace offsets
   size_t off_P = 0;                 // f32 [conv_grid][cout_p]
@@ -60,6 +63,9 @@ struct LayerPlan {
   size_t off_dP = 0;                // f32 [conv_grid][cout_p] (pooled layers)
   size_t off_w = 0;                 // GEMM: dtype [cout_p][ktot_p]; dw: f32 [K][cout_p]
   size_t off_bias = 0;              // f32 [cout_p]
+  size_t off_sew1 = 0, off_seb1 = 0, off_sew2 = 0, off_seb2 = 0;  // f32
+  size_t off_ses = 0;               // f32 [2][N][cout_p] gates (ping-pong)
+  size_t off_separt = 0;            // f32 [N][se_nchunk][cout_p]
   size_t off_flags = 0;             // uint8 [conv_grid] affected-output flags
   size_t off_pflags = 0;            // uint8 [pooled grid] (pooled layers)
   int cnt_O = 0, cnt_pairs = 0;

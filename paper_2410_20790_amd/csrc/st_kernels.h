@@ -162,9 +162,36 @@ void launch_group_count(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
                         const u64* n_rows, int64_t cap, float thr,
                         uint32_t* grp);
 
+// ---- squeeze-excitation on a deferred layer
+struct SeArgs {
+  const float* P;      // state [npix][cp] (updated in place by the emission)
+  const float* dP;     // deferred update rows
+  const int* Mo;       // site -> dP row or -1
+  float* part;         // [N][nchunk][cp] partial sums
+  const float* w1;     // [mid][cp]
+  const float* b1;     // [mid]
+  const float* w2;     // [cp][mid]
+  const float* b2;     // [cp]
+  float* s_new;        // [N][cp]
+  const float* s_old;  // [N][cp]
+  void* dout;          // emitted rows [npix][cp] (row = site)
+  uint32_t* rowmax;
+  int* rowpix;
+  int* map;
+  uint32_t* grp;       // per-64-site kept counts
+  u64* cnt_rows;
+  int64_t npix, hw;
+  int N, cp, c, mid, act, ref, chunk, nchunk;
+  float keep_thr;
+};
+void launch_se(const Prof& pf, hipStream_t s, int dtype, const SeArgs& a);
+void launch_to_f32_pad(hipStream_t s, int dtype, const void* src, float* dst,
+                       int rows, int cols, int rows_p, int cols_p);
+
 // ---- dense network output (Accumulation)
 void launch_output(const Prof& pf, hipStream_t s, const float* P, int cp,
-                   int C, int N, Geo pool, int has_pool, int act, float* out);
+                   int C, int N, Geo pool, int has_pool, int act,
+                   const float* se, float* out);
 
 // ---- setup / introspection helpers
 void launch_fill_u32(hipStream_t s, void* p, int64_t n, uint32_t v);

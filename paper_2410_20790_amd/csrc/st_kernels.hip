@@ -1194,10 +1194,163 @@ void launch_list_compact(const Prof& pf, hipStream_t s, const ListArgs& a) {
   prof_end(pf, 15, s);
 }
 
+// ------------------------------------------------- squeeze-excitation
+// Exact squeeze-excitation on a deferred layer (state P, update dP on the
+// affected sites Mo): partial per-channel sums of f(P_new) over chunks of
+// sites (fixed order, no atomics), gates per image, then the dense emission
+// delta = f(P_new) * s_new - f(P_old) * s_old at every site, with the state
+// commit, row maxima and 64-site kept counts done in the same block.
+__global__ __launch_bounds__(256) void k_se_squeeze(SeArgs a) {
+  const int n = blockIdx.y;
+  const int64_t p0 = (int64_t)n * a.hw + (int64_t)blockIdx.x * a.chunk;
+  const int64_t p1 = min(p0 + a.chunk, (int64_t)(n + 1) * a.hw);
+  for (int c = threadIdx.x; c < a.cp; c += 256) {
+    float sum = 0.f;
+    for (int64_t p = p0; p < p1; ++p) {
+      const float po = a.ref ? 0.f : a.P[p * a.cp + c];
+      const int r = a.Mo[p];
+      const float pn = r >= 0 ? po + a.dP[(int64_t)r * a.cp + c] : po;
+      sum += act_f(pn, a.act);
+    }
+    a.part[((int64_t)n * a.nchunk + blockIdx.x) * a.cp + c] = sum;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_se_excite(SeArgs a) {
+  extern __shared__ float sm[];  // [cp] means, then [mid] hidden
+  float* m = sm;
+  float* z = sm + a.cp;
+  const int n = blockIdx.x;
+  const float inv = 1.f / (float)a.hw;
+  for (int c = threadIdx.x; c < a.cp; c += 256) {
+    float sum = 0.f;
+    for (int k = 0; k < a.nchunk; ++k)
+      sum += a.part[((int64_t)n * a.nchunk + k) * a.cp + c];
+    m[c] = sum * inv;
+  }
+  __syncthreads();
+  // one wave per hidden unit: z = silu(w1 . m + b1)
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int j = wave; j < a.mid; j += 4) {
+    float d = 0.f;
+    for (int c = lane; c < a.cp; c += 64) d += a.w1[(int64_t)j * a.cp + c] * m[c];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) d += __shfl_xor(d, o, 64);
+    if (lane == 0) z[j] = act_f(d + a.b1[j], 2);
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < a.cp; c += 256) {
+    float e = a.b2[c];
+    for (int j = 0; j < a.mid; ++j) e += a.w2[(int64_t)c * a.mid + j] * z[j];
+    a.s_new[(int64_t)n * a.cp + c] = c < a.c ? 1.f / (1.f + expf(-e)) : 0.f;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_se_emit(SeArgs a) {
+  T* dout = (T*)a.dout;
+  const int64_t pix = (int64_t)blockIdx.x * 64 + (threadIdx.x >> 2);
+  const int q = threadIdx.x & 3;
+  const bool in = pix < a.npix;
+  float rm = 0.f;
+  if (in) {
+    const int n = (int)(pix / a.hw);
+    const int r = a.Mo[pix];
+    const float* sn = a.s_new + (int64_t)n * a.cp;
+    const float* so = a.s_old + (int64_t)n * a.cp;
+    for (int c0 = q * 8; c0 < a.cp; c0 += 32) {
+      float po[8], dp[8], pn[8], d[8];
+      if (a.ref) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) po[e] = 0.f;
+      } else {
+        load8f(a.P + pix * a.cp + c0, po);
+      }
+      if (r >= 0) {
+        load8f(a.dP + (int64_t)r * a.cp + c0, dp);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dp[e] = 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        pn[e] = r >= 0 ? po[e] + dp[e] : po[e];
+        const float en = act_f(pn[e], a.act) * sn[c0 + e];
+        const float eo = a.ref ? 0.f : act_f(po[e], a.act) * so[c0 + e];
+        d[e] = en - eo;
+      }
+      rm = fmaxf(rm, Vec8<T>::store(dout + pix * a.cp + c0, d));
+      if (r >= 0) store8f(const_cast<float*>(a.P) + pix * a.cp + c0, pn);
+    }
+  }
+  rm = fmaxf(rm, __shfl_xor(rm, 1, 64));
+  rm = fmaxf(rm, __shfl_xor(rm, 2, 64));
+  if (in && q == 0) {
+    a.rowmax[pix] = __float_as_uint(rm);
+    a.rowpix[pix] = (int)pix;
+    a.map[pix] = (int)pix;
+  }
+  const u64 b = __ballot(in && q == 0 && rm > a.keep_thr);
+  __shared__ unsigned wc[4];
+  if ((threadIdx.x & 63) == 0) wc[threadIdx.x >> 6] = (unsigned)__popcll(b);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    a.grp[blockIdx.x] = wc[0] + wc[1] + wc[2] + wc[3];
+    if (blockIdx.x == 0) *a.cnt_rows = (u64)a.npix;
+  }
+}
+
+void launch_se(const Prof& pf, hipStream_t s, int dtype, const SeArgs& a) {
+  prof_begin(pf, 19 /*ST_K_SE_SQUEEZE*/, s);
+  k_se_squeeze<<<dim3(a.nchunk, a.N), 256, 0, s>>>(a);
+  prof_end(pf, 19, s);
+  prof_begin(pf, 20 /*ST_K_SE_EXCITE*/, s);
+  k_se_excite<<<a.N, 256, sizeof(float) * (a.cp + a.mid), s>>>(a);
+  prof_end(pf, 20, s);
+  const int blocks = (int)((a.npix + 63) / 64);
+  prof_begin(pf, 21 /*ST_K_SE_EMIT*/, s);
+  if (dtype == 0)
+    k_se_emit<float><<<blocks, 256, 0, s>>>(a);
+  else if (dtype == 1)
+    k_se_emit<_Float16><<<blocks, 256, 0, s>>>(a);
+  else
+    k_se_emit<bf16_t><<<blocks, 256, 0, s>>>(a);
+  prof_end(pf, 21, s);
+}
+
+// Storage-dtype matrix [rows][cols] -> f32 [rows_p][cols_p], zero padded
+// (squeeze-excitation weights); src may be NULL (zeros).
+template <typename T>
+__global__ void k_to_f32_pad(const T* src, float* dst, int rows, int cols,
+                             int rows_p, int cols_p) {
+  const int64_t total = (int64_t)rows_p * cols_p;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    const int r = (int)(idx / cols_p), c = (int)(idx - (int64_t)r * cols_p);
+    dst[idx] = (src && r < rows && c < cols)
+                   ? to_f(src[(int64_t)r * cols + c]) : 0.f;
+  }
+}
+
+void launch_to_f32_pad(hipStream_t s, int dtype, const void* src, float* dst,
+                       int rows, int cols, int rows_p, int cols_p) {
+  const int grid = grid_for((int64_t)rows_p * cols_p, 1024);
+  if (dtype == 0)
+    k_to_f32_pad<float><<<grid, 256, 0, s>>>((const float*)src, dst, rows,
+                                             cols, rows_p, cols_p);
+  else if (dtype == 1)
+    k_to_f32_pad<_Float16><<<grid, 256, 0, s>>>((const _Float16*)src, dst,
+                                                rows, cols, rows_p, cols_p);
+  else
+    k_to_f32_pad<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)src, dst, rows,
+                                              cols, rows_p, cols_p);
+}
+
 // ------------------------------------------------------- dense output
 __global__ __launch_bounds__(256) void k_output(const float* P, int cp, int C,
                                                 int N, Geo g, int has_pool,
-                                                int act, float* out) {
+                                                int act, const float* se,
+                                                float* out) {
   // g.Hi/Wi: conv grid; g.Ho/Wo: output grid (== conv grid without pool)
   const int64_t total = (int64_t)N * g.Ho * g.Wo * C;
   const int64_t hwo = (int64_t)g.Ho * g.Wo;
@@ -1206,7 +1359,8 @@ __global__ __launch_bounds__(256) void k_output(const float* P, int cp, int C,
     const int64_t q = idx / C;
     const int c = (int)(idx - q * C);
     if (!has_pool) {
-      out[idx] = act_f(P[q * cp + c], act);
+      const float v = act_f(P[q * cp + c], act);
+      out[idx] = se ? v * se[(q / hwo) * cp + c] : v;
       continue;
     }
     const int n = (int)(q / hwo);
@@ -1228,10 +1382,11 @@ __global__ __launch_bounds__(256) void k_output(const float* P, int cp, int C,
 }
 
 void launch_output(const Prof& pf, hipStream_t s, const float* P, int cp,
-                   int C, int N, Geo g, int has_pool, int act, float* out) {
+                   int C, int N, Geo g, int has_pool, int act,
+                   const float* se, float* out) {
   prof_begin(pf, 16 /*ST_K_OUTPUT*/, s);
   k_output<<<grid_for((int64_t)N * g.Ho * g.Wo * C, 8192), 256, 0, s>>>(
-      P, cp, C, N, g, has_pool, act, out);
+      P, cp, C, N, g, has_pool, act, se, out);
   prof_end(pf, 16, s);
 }
 

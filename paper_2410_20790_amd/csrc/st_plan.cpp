@@ -101,8 +101,11 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
                  "only dense (groups=1) and depthwise convolutions");
     if (d.act < ST_ACT_NONE || d.act > ST_ACT_SILU)
       return bad(ST_ERR_INVALID_ARG, i, "unknown activation");
-    if (d.se_mid != 0 || d.se_w1 || d.se_w2)
-      return bad(ST_ERR_UNSUPPORTED, i, "squeeze-excitation");
+    if (d.se_mid < 0) return bad(ST_ERR_INVALID_ARG, i, "se_mid < 0");
+    if (d.se_mid > 0 && (!d.se_w1 || !d.se_w2))
+      return bad(ST_ERR_INVALID_ARG, i, "squeeze-excitation weights missing");
+    if (d.se_mid > 0 && (d.pool_k_h > 0 || d.pool_k_w > 0))
+      return bad(ST_ERR_UNSUPPORTED, i, "squeeze-excitation with a pool");
     if (!d.weight) return bad(ST_ERR_INVALID_ARG, i, "weight is NULL");
     L.Hi = in.H; L.Wi = in.W;
     int64_t ho = out_size(in.H, d.k_h, d.s_h, d.p_h);
@@ -141,8 +144,11 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
     L.ktot = (int64_t)L.K * L.cin_p;
     L.ktot_p = round_up(L.ktot, kc);
     L.conv_grid = (int64_t)batch * L.Ho * L.Wo;
-    L.stateful = d.act != ST_ACT_NONE || L.pool || i == n_layers - 1;
-    L.mode = L.pool ? kModeDefer : (L.stateful ? kModeState : kModeLinear);
+    L.se = d.se_mid > 0;
+    L.se_mid = d.se_mid;
+    L.stateful = d.act != ST_ACT_NONE || L.pool || L.se || i == n_layers - 1;
+    L.mode = (L.pool || L.se) ? kModeDefer
+                              : (L.stateful ? kModeState : kModeLinear);
     L.ident = d.k_h == 1 && d.k_w == 1 && d.s_h == 1 && d.s_w == 1 &&
               d.p_h == 0 && d.p_w == 0 && d.residual_src == -2;
     net->tensors[d.src + 1].consumers.push_back({i, 0});
@@ -190,7 +196,7 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
     TensorPlan& T = net->tensors[i + 1];
     L.cnt_pairs = 2 * (L_n + 1) + i;
     max_grid = std::max(max_grid, L.conv_grid);
-    if (L.pool) {
+    if (L.pool || L.se) {
       L.cnt_O = 2 * (L_n + 1) + L_n + i;
       L.off_O = a.take(sizeof(int32_t) * L.conv_grid);
       L.off_Mo = a.take(sizeof(int32_t) * L.conv_grid);
@@ -210,6 +216,17 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
     L.off_bias = a.take(sizeof(float) * L.cout_p);
     if (!L.ident) L.off_flags = a.take(round_up(L.conv_grid, 16));
     if (L.pool) L.off_pflags = a.take(round_up(T.grid, 16));
+    if (L.se) {
+      const int64_t hw = (int64_t)L.Ho * L.Wo;
+      L.se_chunk = 128;
+      L.se_nchunk = (int)ceil_div(hw, L.se_chunk);
+      L.off_sew1 = a.take(sizeof(float) * L.se_mid * L.cout_p);
+      L.off_seb1 = a.take(sizeof(float) * L.se_mid);
+      L.off_sew2 = a.take(sizeof(float) * L.cout_p * L.se_mid);
+      L.off_seb2 = a.take(sizeof(float) * L.cout_p);
+      L.off_ses = a.take(sizeof(float) * 2 * batch * L.cout_p);
+      L.off_separt = a.take(sizeof(float) * batch * L.se_nchunk * L.cout_p);
+    }
   }
   net->max_grid = max_grid;
   net->off_flags = a.take(round_up(t0.grid, 16));

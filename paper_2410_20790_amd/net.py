@@ -13,17 +13,20 @@ TORCH_DTYPES = {"f32": torch.float32, "f16": torch.float16,
                 "bf16": torch.bfloat16}
 
 
-def layer_desc(L, w_ptr: int, b_ptr: Optional[int]) -> B.st_layer_desc:
+def layer_desc(L, w_ptr: int, b_ptr: Optional[int],
+               se_ptrs=(None, None, None, None)) -> B.st_layer_desc:
     """Descriptor of one layer from an object with the LayerSpec fields
     (src, residual_src, c_in, c_out, groups, k, s, p, act, pool_k, pool_s,
-    pool_p, se_mid)."""
+    pool_p, se_mid); se_ptrs are the device addresses of the
+    squeeze-excitation weights (w1, b1, w2, b2)."""
     return B.st_layer_desc(
         src=L.src, residual_src=L.residual_src, c_in=L.c_in, c_out=L.c_out,
         groups=L.groups, k_h=L.k[0], k_w=L.k[1], s_h=L.s[0], s_w=L.s[1],
         p_h=L.p[0], p_w=L.p[1], act=L.act, pool_k_h=L.pool_k[0],
         pool_k_w=L.pool_k[1], pool_s_h=L.pool_s[0], pool_s_w=L.pool_s[1],
         pool_p_h=L.pool_p[0], pool_p_w=L.pool_p[1], se_mid=L.se_mid,
-        weight=w_ptr, bias=b_ptr)
+        weight=w_ptr, bias=b_ptr, se_w1=se_ptrs[0], se_b1=se_ptrs[1],
+        se_w2=se_ptrs[2], se_b2=se_ptrs[3])
 
 
 class SparseTemNet:
@@ -50,8 +53,15 @@ class SparseTemNet:
                     self.device, self.tdtype).contiguous()
             self._w.append(w)
             self._b.append(b)
+            se = (None, None, None, None)
+            if getattr(L, "se_mid", 0):
+                t = [torch.as_tensor(np.asarray(x)).to(
+                    self.device, self.tdtype).contiguous()
+                    for x in (L.se_w1, L.se_b1, L.se_w2, L.se_b2)]
+                self._w.extend(t)
+                se = tuple(x.data_ptr() for x in t)
             descs.append(layer_desc(L, w.data_ptr(),
-                                    None if b is None else b.data_ptr()))
+                                    None if b is None else b.data_ptr(), se))
         self.handle = B.st_create_net(descs, batch, H, W, C,
                                       B.DTYPE_CODES[dtype])
         self.ws_bytes = B.st_workspace_bytes(self.handle)

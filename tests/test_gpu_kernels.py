@@ -139,3 +139,65 @@ def test_empty_delta_frame():
     net = one_layer("pool3x3_s2", "f32")
     f = random_sparse_video(24, 1, 2, 23, 37, 8, 0.0)[0]
     check(net, [f, f.copy(), f.copy()], 0.0)
+
+
+def se_net(dtype, last_se):
+    """1x1 expand (SiLU) -> depthwise 3x3 (SiLU) + squeeze-excitation
+    [-> linear 1x1 project]: every path of the squeeze-excitation kernels,
+    with the gated layer last (output gated) or feeding a 1x1 layer."""
+    rng = np.random.default_rng(5)
+    C, E, M = 8, 24, 4
+    l0 = LayerSpec(src=-1, c_in=C, c_out=E, k=(1, 1), s=(1, 1), p=(0, 0),
+                   act=ACT_SILU, name="expand")
+    l1 = LayerSpec(src=0, c_in=E, c_out=E, k=(3, 3), s=(1, 1), p=(1, 1),
+                   groups=E, act=ACT_SILU, se_mid=M, name="dw_se")
+    layers = [l0, l1]
+    if not last_se:
+        layers.append(LayerSpec(src=1, c_in=E, c_out=C, k=(1, 1), s=(1, 1),
+                                p=(0, 0), act=ACT_NONE, residual_src=-1,
+                                name="project"))
+    for L in layers:
+        L.weight = to_storage(rng.normal(0, 0.3, (L.c_out, L.c_in // L.groups,
+                                                  *L.k)), dtype)
+        L.bias = to_storage(rng.normal(0, 0.1, L.c_out), dtype)
+    l1.se_w1 = to_storage(rng.normal(0, 0.3, (M, E)), dtype)
+    l1.se_b1 = to_storage(rng.normal(0, 0.1, M), dtype)
+    l1.se_w2 = to_storage(rng.normal(0, 0.3, (E, M)), dtype)
+    l1.se_b2 = to_storage(rng.normal(1, 0.2, E), dtype)
+    return NetSpec("se", layers, 2, 19, 23, C, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("last_se", [True, False])
+def test_squeeze_excitation(dtype, last_se):
+    net = se_net(dtype, last_se)
+    say(f"[gpu] squeeze-excitation {dtype} last={last_se}")
+    frames = random_sparse_video(25, 4, 2, 19, 23, 8, 0.08, dtype=dtype)
+    o, g = make_pair(net)
+    try:
+        o.encode_reference(frames[0])
+        out = g.encode_reference(to_dev(frames[0], dtype))
+        torch.cuda.synchronize()
+        tol = 1e-5 if dtype == "f32" else 2e-2
+        assert np.abs(out.cpu().numpy() - o.last["out"]).max() <= \
+            tol * np.abs(o.last["out"]).max()
+        thr = [0.0] * (len(net.layers) + 1)
+        for t in range(1, 4):
+            o.encode_diff(frames[t], thr)
+            out = g.encode_diff(to_dev(frames[t], dtype), thr)
+            torch.cuda.synchronize()
+            oo = o.last["out"]
+            assert np.abs(out.cpu().numpy() - oo).max() <= \
+                tol * np.abs(oo).max()
+            for i in o.P:
+                Pg = B.st_debug_state(g.handle, i, o.P[i].shape)
+                assert np.abs(Pg - o.P[i]).max() <= \
+                    tol * np.abs(o.P[i]).max(), f"state {i}"
+            T = o.last["tensors"][2]
+            pix, rows = B.st_debug_candidates(g.handle, 1, T["C"])
+            np.testing.assert_array_equal(pix, T["cand"])  # every site
+            sc = np.abs(T["cand_rows"]).max()
+            assert np.abs(rows - T["cand_rows"]).max() <= tol * sc + \
+                (2.0 ** -7 if dtype != "f32" else 0) * sc
+    finally:
+        g.close()

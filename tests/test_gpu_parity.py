@@ -16,8 +16,9 @@ from paper_2410_20790_amd import SparseTemNet
 from paper_2410_20790_amd import binding as B
 from parity_util import RTOL, make_pair, rel, run_chunk, say, to_dev
 from workloads import (crnn_vgg_net, depthwise_test_net, driving_video,
-                       random_sparse_video, resnet50_net, resnet_mini_net,
-                       textline_video, toy_net, toy_video)
+                       efficientnet_mini_net, efficientnet_net,
+                       object_video, random_sparse_video, resnet50_net,
+                       resnet_mini_net, textline_video, toy_net, toy_video)
 
 pytestmark = pytest.mark.gpu
 
@@ -100,6 +101,27 @@ def test_depthwise(dtype):
     net = depthwise_test_net(dtype=dtype)
     run_chunk(net, random_sparse_video(7, 4, 1, 24, 40, 16, 0.1, dtype=dtype),
               0.0, f"depthwise {dtype}")
+
+
+# ------------------------------------------------- EfficientNet family
+
+@pytest.mark.parametrize("dtype,thr", [("f32", 0.0), ("f32", 0.05),
+                                       ("f16", 0.0), ("bf16", 0.0)])
+def test_efficientnet_mini(dtype, thr):
+    """MBConv blocks: expand, depthwise 3x3 / 5x5 stride 2, exact
+    squeeze-excitation, linear project with identity skip."""
+    net = efficientnet_mini_net(dtype=dtype)
+    run_chunk(net, random_sparse_video(3, 4, 1, 32, 40, 3, 0.08, dtype=dtype),
+              thr, f"effnet_mini {dtype} thr={thr}",
+              max_band=8 if (thr or dtype != "f32") else 0)
+
+
+def test_efficientnet_b0_small_f16():
+    """All 16 MBConv blocks of EfficientNet-B0 at 64x64, fp16, on the
+    detection-like video (global translation plus moving objects)."""
+    net = efficientnet_net(H=64, W=64)
+    frames = object_video(seed=1, n_frames=3, H=64, W=64, obj=8)
+    run_chunk(net, frames, 0.02, "effnet-b0 64x64 f16", max_band=64)
 
 
 # ----------------------------------------------------------- edge cases
