@@ -14,7 +14,8 @@ import torch
 import oracle
 from paper_2410_20790_amd import SparseTemNet
 from paper_2410_20790_amd import binding as B
-from parity_util import RTOL, make_pair, rel, run_chunk, say, to_dev
+from parity_util import (RTOL, compare_frame, make_pair, rel, run_chunk,
+                         say, to_dev)
 from workloads import (crnn_vgg_net, depthwise_test_net, driving_video,
                        efficientnet_mini_net, efficientnet_net,
                        object_video, random_sparse_video, resnet50_net,
@@ -122,6 +123,52 @@ def test_efficientnet_b0_small_f16():
     net = efficientnet_net(H=64, W=64)
     frames = object_video(seed=1, n_frames=3, H=64, W=64, obj=8)
     run_chunk(net, frames, 0.02, "effnet-b0 64x64 f16", max_band=64)
+
+
+# ---------------------------------------- online threshold adjustment
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+def test_ibst_chunk(dtype):
+    """Thresholds chosen per frame by the iterative binary search from the
+    oracle's sparsities; the GPU encodes with the same thresholds, and a
+    second controller fed from the GPU's own densities must choose the same
+    thresholds."""
+    from paper_2410_20790_amd.ibst import (IBST, nonlinear_tensors,
+                                           sparsity_from_counts)
+    net = efficientnet_mini_net(dtype=dtype)
+    frames = object_video(seed=2, n_frames=7, H=32, W=40, obj=8,
+                          obj_frac=0.1, dtype=dtype)
+    L_n = len(net.layers)
+    ctl = nonlinear_tensors(net.layers)
+    c_o = IBST(L_n + 1, ctl, target=0.7, eps=0.05, theta_max=0.5)
+    c_g = IBST(L_n + 1, ctl, target=0.7, eps=0.05, theta_max=0.5)
+    o, g = make_pair(net)
+    tag = f"ibst {dtype}"
+    try:
+        o.encode_reference(frames[0])
+        g.encode_reference(to_dev(frames[0], dtype))
+        grids = [int(np.prod(g.tensor_shape(k - 1)[:3]))
+                 for k in range(L_n + 1)]
+        n_band = 0
+        for t in range(1, len(frames)):
+            if t == 4:  # a new cycle restarts the brackets
+                c_o.start_cycle()
+                c_g.start_cycle()
+            thr = c_o.thresholds()
+            if n_band == 0:  # equal counts so far: equal decisions
+                assert thr == c_g.thresholds(), f"{tag} f{t}"
+            say(f"[gpu] {tag}: frame {t} thr[0:3]={thr[:3]}")
+            o.encode_diff(frames[t], thr)
+            out_g = g.encode_diff(to_dev(frames[t], dtype), thr)
+            torch.cuda.synchronize()
+            n_band += compare_frame(net, o, g, out_g, f"{tag} f{t}")
+            c_o.update([1.0 - o.density(k) for k in range(L_n + 1)])
+            _, act = B.st_debug_counters(g.handle, L_n)
+            c_g.update(sparsity_from_counts(act, grids))
+        assert n_band <= (0 if dtype == "f32" else 4)
+        assert any(v > 0 for v in c_o.thresholds())
+    finally:
+        g.close()
 
 
 # ----------------------------------------------------------- edge cases
