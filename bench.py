@@ -36,7 +36,11 @@ ESIZE = {"f32": 4, "f16": 2, "bf16": 2}
 
 
 def workload(name, density):
-    from workloads import (crnn_vgg_net, driving_video, resnet50_net,
+    """Network, synthetic video and run shape of a named workload.  `chunk`
+    is the number of frames per reference frame (None: one reference, then
+    diff frames only); `ibst` selects online threshold adjustment."""
+    from workloads import (crnn_vgg_net, driving_video, efficientnet_net,
+                           multistream_video, object_video, resnet50_net,
                            textline_video, toy_net, toy_video)
     if name == "resnet50":
         net = resnet50_net(H=1024, W=2048)
@@ -44,18 +48,38 @@ def workload(name, density):
             net=net, desc=f"resnet50-bf16-1024x2048-density{density:g}",
             frames=lambda n, H=1024, W=2048: driving_video(
                 seed=0, n_frames=n, H=H, W=W, density=density),
-            crop=(256, 512))
+            crop=(256, 512), chunk=None, ibst=False)
+    if name == "effnet_b0":
+        net = efficientnet_net(H=512, W=512, dtype="f16")
+        return dict(
+            net=net, desc="efficientnet_b0-f16-512x512-objects-ibst0.9",
+            frames=lambda n: object_video(seed=0, n_frames=n, H=512, W=512,
+                                          dtype="f16"),
+            crop=None, chunk=8, ibst=True)
+    if name == "multistream":
+        net = efficientnet_net(H=256, W=256, dtype="bf16", batch=32)
+        wl = dict(net=net,
+                  desc="efficientnet_b0x32-bf16-256x256-streams-ibst0.9",
+                  crop=None, chunk=8, ibst=True)
+
+        def frames(n):
+            f, d = multistream_video(n_frames=n, N=32, H=256, W=256)
+            wl["stream_density_targets"] = [float(v) for v in d]
+            return f
+        wl["frames"] = frames
+        return wl
     if name == "crnn":
         net = crnn_vgg_net()
         return dict(net=net, desc="crnn_vgg-f32-32x128-band7",
                     frames=lambda n, H=32, W=128: textline_video(
                         seed=0, n_frames=n, H=H, W=W),
-                    crop=None)
+                    crop=None, chunk=16, ibst=False)
     if name == "toy":
         net = toy_net()
         return dict(net=net, desc="toy-f32-64x64x16-density0.1",
                     frames=lambda n, H=64, W=64: toy_video(
-                        seed=0, n_frames=n, H=H, W=W), crop=None)
+                        seed=0, n_frames=n, H=H, W=W), crop=None,
+                    chunk=4, ibst=False)
     raise SystemExit(f"unknown workload {name}")
 
 
@@ -93,7 +117,7 @@ def conv_launch_bytes(L, c, es, mode):
 
 def layer_mode(net, i):
     L = net.layers[i]
-    if L.pool_k[0] > 0:
+    if L.pool_k[0] > 0 or L.se_mid:
         return "defer"
     if L.act != 0 or i == len(net.layers) - 1:
         return "state"
@@ -108,6 +132,9 @@ def torch_dense_model(net, dtype):
     Ws = [torch.as_tensor(L.weight).to("cuda", tdt).contiguous(
         memory_format=torch.channels_last) for L in net.layers]
     Bs = [torch.as_tensor(L.bias).to("cuda", tdt) for L in net.layers]
+    SE = {i: [torch.as_tensor(getattr(L, k)).to("cuda", tdt)
+              for k in ("se_w1", "se_b1", "se_w2", "se_b2")]
+          for i, L in enumerate(net.layers) if L.se_mid}
 
     def fwd(x_nhwc):
         acts = {-1: x_nhwc.permute(0, 3, 1, 2)}
@@ -121,6 +148,10 @@ def torch_dense_model(net, dtype):
                 y = F.silu(y)
             if L.pool_k[0] > 0:
                 y = F.max_pool2d(y, L.pool_k, L.pool_s, L.pool_p)
+            if L.se_mid:
+                w1, b1, w2, b2 = SE[i]
+                z = F.silu(F.linear(y.mean(dim=(2, 3)), w1, b1))
+                y = y * torch.sigmoid(F.linear(z, w2, b2))[:, :, None, None]
             acts[i] = y
         return acts[len(net.layers) - 1]
     return fwd
@@ -331,19 +362,358 @@ def density_sweep(net, thr, densities, steps):
     return out
 
 
+class Feed:
+    """Walks a synthetic video: a reference frame every `chunk` frames (only
+    the first frame when chunk is None), diff frames in between.  With a
+    controller, each diff frame's thresholds come from it and its kept-row
+    counters are fed back after the frame (one host round trip per frame,
+    part of the timed work)."""
+
+    def __init__(self, g, n_layers, frames, chunk, thr, ctl, out):
+        from paper_2410_20790_amd import binding as B
+        self.B = B
+        self.g, self.frames, self.chunk = g, frames, chunk
+        self.thr, self.ctl, self.out = thr, ctl, out
+        self.pos = 0
+        self.L_n = n_layers
+        self.grids = [int(np.prod(g.tensor_shape(t - 1)[:3]))
+                      for t in range(self.L_n + 1)]
+        self.sparsity = []     # per diff frame, every tensor
+
+    def next_is_ref(self):
+        return self.pos == 0 or bool(self.chunk and self.pos % self.chunk == 0)
+
+    def ref(self):
+        if self.ctl:
+            self.ctl.start_cycle()
+        self.g.encode_reference(self.frames[self.pos], out=self.out)
+        self.pos += 1
+
+    def diff(self):
+        from paper_2410_20790_amd.ibst import sparsity_from_counts
+        thr = self.ctl.thresholds() if self.ctl else self.thr
+        self.g.encode_diff(self.frames[self.pos], thr, out=self.out)
+        self.pos += 1
+        if self.ctl:
+            _, act = self.B.st_debug_counters(self.g.handle, self.L_n)
+            sp = sparsity_from_counts(act, self.grids)
+            self.sparsity.append(sp)
+            self.ctl.update(sp)
+
+
+def run_diffs(feed, n):
+    """Encode frames until `n` diff frames are done.  Returns the wall
+    seconds spent in diff frames (reference frames in between are
+    synchronised around and left out) and the reference frames' ms."""
+    import torch
+    total, refs, done = 0.0, [], 0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while done < n:
+        if feed.next_is_ref():
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            total += t1 - t0
+            feed.ref()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            refs.append((t0 - t1) * 1000.0)
+        else:
+            feed.diff()
+            done += 1
+    torch.cuda.synchronize()
+    total += time.perf_counter() - t0
+    return total, refs
+
+
+def frames_needed(chunk, W, K, KP):
+    pos = 0
+
+    def is_ref(p):
+        return p == 0 or bool(chunk and p % chunk == 0)
+    for n in (W, K):
+        d = 0
+        while d < n:
+            d += 0 if is_ref(pos) else 1
+            pos += 1
+    if chunk:  # the profiled frames start with a reference frame
+        while not is_ref(pos):
+            pos += 1
+        return pos + 1 + KP
+    return pos + KP
+
+
+def kernel_table(net, recs, counts, es):
+    """Per kernel class: launches, time, algorithmic bytes / FLOPs from the
+    frame's counters (see conv_launch_bytes)."""
+    from paper_2410_20790_amd import binding as B
+    classes = {}
+    for r in recs:
+        name = B.KERNEL_CLASSES[r["kernel"]]
+        c = classes.setdefault(name, {"launches": 0, "ms": 0.0, "bytes": 0.0,
+                                      "flops": 0.0})
+        c["launches"] += 1
+        c["ms"] += float(r["ms"])
+        f, j = int(r["frame"]), int(r["layer"])
+        if f >= len(counts):
+            continue
+        if name in ("conv_gemm", "conv_dw"):
+            L = net.layers[j]
+            c["bytes"] += conv_launch_bytes(L, counts[f, j], es,
+                                            layer_mode(net, j))
+            c["flops"] += 2.0 * counts[f, j, 1] * (L.c_in // L.groups) * \
+                L.c_out
+        elif name in ("se_squeeze", "se_emit"):
+            # squeeze: the site map, and f32 state and update rows of the
+            # affected sites; emit: the state and map of every site, update
+            # rows, the delta and row bookkeeping of every site written,
+            # and the affected state rows written back
+            L = net.layers[j]
+            npix = int(np.prod(net_conv_grid(net, j)))
+            nO = int(counts[f, j, 0])
+            if name == "se_squeeze":
+                b = npix * 4 + nO * L.c_out * 8
+            else:
+                b = npix * (L.c_out * (4 + es) + 16) + nO * L.c_out * 8
+            c["bytes"] += b
+        elif name == "scan_mask":
+            c["bytes"] += net.batch * net.H * net.W * (2 * net.C * es + 1)
+        elif name == "scan_compact":
+            n0 = counts[f, 0, 2] if net.layers[0].src == -1 else 0
+            c["bytes"] += net.batch * net.H * net.W + n0 * (
+                3 * net.C * es + 12)
+    return classes
+
+
+_GRIDS = {}
+
+
+def net_conv_grid(net, j):
+    """(N, Ho, Wo) of layer j's convolution output."""
+    key = (id(net), j)
+    if key not in _GRIDS:
+        shapes = {-1: (net.H, net.W)}
+        for i, L in enumerate(net.layers):
+            Hi, Wi = shapes[L.src]
+            Ho = (Hi + 2 * L.p[0] - L.k[0]) // L.s[0] + 1
+            Wo = (Wi + 2 * L.p[1] - L.k[1]) // L.s[1] + 1
+            _GRIDS[(id(net), i)] = (net.batch, Ho, Wo)
+            if L.pool_k[0] > 0:
+                Ho = (Ho + 2 * L.pool_p[0] - L.pool_k[0]) // L.pool_s[0] + 1
+                Wo = (Wo + 2 * L.pool_p[1] - L.pool_k[1]) // L.pool_s[1] + 1
+            shapes[i] = (Ho, Wo)
+    return _GRIDS[key]
+
+
+def roofline_of(classes, dt, desc):
+    dom = max(classes, key=lambda k: classes[k]["ms"])
+    dc = classes[dom]
+    avg_s = dc["ms"] * 1e-3 / dc["launches"]
+    if not (dc["bytes"] or dc["flops"]):
+        return {"kernel": dom, "bound": None, "launches": dc["launches"],
+                "avg_launch_us": avg_s * 1e6}
+    ai = dc["flops"] / max(dc["bytes"], 1.0)
+    ridge = MFMA_PEAK_TFLOPS[dt] * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if dc["flops"] and ai > ridge:
+        ach = dc["flops"] / dc["launches"] / avg_s / 1e12
+        roof = {"bound": "mfma", "achieved": ach,
+                "peak": MFMA_PEAK_TFLOPS[dt], "unit": "TFLOP/s",
+                "frac": ach / MFMA_PEAK_TFLOPS[dt], "traffic": None}
+    else:
+        ach = dc["bytes"] / dc["launches"] / avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "traffic": None}
+    tb = measured_traffic(desc, dom)
+    if tb is not None:
+        roof["traffic"] = tb
+    roof.update({"kernel": dom, "launches": dc["launches"],
+                 "avg_launch_us": avg_s * 1e6,
+                 "alg_bytes_per_launch": dc["bytes"] / dc["launches"],
+                 "alg_flops_per_launch": dc["flops"] / dc["launches"],
+                 "arith_intensity": ai})
+    return roof
+
+
+def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025):
+    """Time K diff frames of a workload (after W warm-up diff frames), then
+    KP more with an event pair around every launch; dense comparators on
+    the same net.  Returns the result fields and the live objects."""
+    import torch
+    from paper_2410_20790_amd import SparseTemNet
+    from paper_2410_20790_amd import binding as B
+    from paper_2410_20790_amd.ibst import IBST, nonlinear_tensors
+    net = wl["net"]
+    dt = net.dtype
+    es = ESIZE[dt]
+    chunk = wl["chunk"]
+    if chunk:
+        KP = min(KP, chunk - 1)
+    t_gen = time.perf_counter()
+    frames_np = wl["frames"](frames_needed(chunk, W, K, KP))
+    t_gen = time.perf_counter() - t_gen
+    tdt = {"f32": torch.float32, "f16": torch.float16,
+           "bf16": torch.bfloat16}[dt]
+    frames = [torch.from_numpy(f).to("cuda", tdt).contiguous()
+              for f in frames_np]
+    del frames_np
+    g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt)
+    L_n = len(net.layers)
+    thr = [thr_val] * (L_n + 1)
+    out = g.new_output()
+    ctl = None
+    if wl["ibst"]:
+        ctl = IBST(L_n + 1, nonlinear_tensors(net.layers), target, eps)
+    feed = Feed(g, L_n, frames, chunk, thr, ctl, out)
+    dflops = dense_flops(net, [net_conv_grid(net, i) for i in range(L_n)])
+
+    run_diffs(feed, W)  # reference frame + warm-up
+
+    # ---- timed region: K diff frames (reference frames of later chunks
+    # are synchronised around and excluded)
+    s_ev = torch.cuda.Event(enable_timing=True)
+    e_ev = torch.cuda.Event(enable_timing=True)
+    n_sp = len(feed.sparsity)
+    torch.cuda.synchronize()
+    s_ev.record()
+    wall, refs = run_diffs(feed, K)
+    e_ev.record()
+    torch.cuda.synchronize()
+    ms_step = wall * 1000.0 / K
+    ev_ms = s_ev.elapsed_time(e_ev) / K if not refs else None
+    dens0 = g.density(-1)
+    sp_timed = np.array(feed.sparsity[n_sp:]) if feed.sparsity else None
+
+    # ---- profiled diff frames: an event pair around every launch
+    if chunk:
+        while not feed.next_is_ref():
+            feed.diff()
+        feed.ref()
+    B.st_profile_begin(g.handle, KP * 1024, KP + 1)
+    torch.cuda.synchronize()
+    tp = time.perf_counter()
+    for _ in range(KP):
+        feed.diff()
+    torch.cuda.synchronize()
+    prof_ms_step = (time.perf_counter() - tp) * 1000.0 / KP
+    recs, counts = B.st_profile_end(g.handle, L_n)
+    per_frame_flops = [
+        sum(2 * int(counts[f, j, 1]) * (L.c_in // L.groups) * L.c_out
+            for j, L in enumerate(net.layers)) for f in range(len(counts))]
+    alg_flops = float(np.mean(per_frame_flops))
+    classes = kernel_table(net, recs, counts, es)
+    total_ms = sum(c["ms"] for c in classes.values())
+    kern = {}
+    for name, c in sorted(classes.items(), key=lambda kv: -kv[1]["ms"]):
+        e = {"launches": c["launches"],
+             "avg_us": 1000.0 * c["ms"] / c["launches"],
+             "share": c["ms"] / total_ms}
+        if c["bytes"]:
+            e["alg_GBps"] = c["bytes"] / (c["ms"] * 1e-3) / 1e9
+            e["hbm_frac"] = e["alg_GBps"] / HBM_PEAK_GBS
+        if c["flops"]:
+            e["alg_TFLOPs"] = c["flops"] / (c["ms"] * 1e-3) / 1e12
+            e["mfma_frac"] = e["alg_TFLOPs"] / MFMA_PEAK_TFLOPS[dt]
+        kern[name] = e
+    roof = roofline_of(classes, dt, wl["desc"])
+    stream_dens = ([round(g.density(-1, n), 5) for n in range(net.batch)]
+                   if net.batch > 1 else None)
+
+    # ---- dense comparators on the same GPU, net and dtype
+    dense_ms = {}
+    if dense:
+        x = frames[0]
+        dense_ms["own_dense_ms"] = time_gpu(
+            lambda: g.encode_reference(x, out=out), 5)
+        fwd = torch_dense_model(net, dt)
+        with torch.no_grad():
+            dense_ms["miopen_ms"] = time_gpu(lambda: fwd(x), 10, warm=3)
+            ref_t = fwd(x).permute(0, 2, 3, 1).float()
+        g.encode_reference(x, out=out)
+        torch.cuda.synchronize()
+        dense_ms["miopen_vs_own_rel_err"] = float(
+            (ref_t - out).abs().max() / out.abs().max())
+
+    res = {
+        "value": 1000.0 / ms_step,
+        "ms_per_step": ms_step,
+        "event_ms_per_step": ev_ms,
+        "effective_tflops": alg_flops / (ms_step * 1e-3) / 1e12,
+        "alg_gflop_per_frame": alg_flops / 1e9,
+        "dense_gflop_per_frame": dflops / 1e9,
+        "dense_equiv_tflops": dflops / (ms_step * 1e-3) / 1e12,
+        "measured_input_density": dens0,
+    }
+    if chunk:
+        ref_ms = float(np.median(refs)) if refs else None
+        res["chunk"] = chunk
+        res["ref_ms"] = ref_ms
+        if ref_ms is not None:
+            res["chunk_amortised_frames_per_s"] = 1000.0 * chunk / (
+                ref_ms + (chunk - 1) * ms_step)
+    if dense_ms:
+        res["speedup_vs_dense"] = {
+            "miopen": dense_ms["miopen_ms"] / ms_step,
+            "own_dense": dense_ms["own_dense_ms"] / ms_step}
+        res["dense_ms"] = dense_ms
+    if ctl is not None and sp_timed is not None and len(sp_timed):
+        c_idx = ctl.ctl
+        s_c = sp_timed[:, c_idx]
+        th = np.array(ctl.thresholds())[c_idx]
+        res["ibst"] = {
+            "target": target, "eps": eps, "theta_max": ctl.theta_max,
+            "controlled_tensors": len(c_idx),
+            "mean_sparsity_controlled": float(s_c.mean()),
+            "in_band_frac_last_frame": float(np.mean(
+                np.abs(s_c[-1] - target) <= eps)),
+            "theta_last": {"min": float(th.min()),
+                           "median": float(np.median(th)),
+                           "max": float(th.max())},
+            "mean_input_sparsity": float(sp_timed[:, 0].mean())}
+    if stream_dens:
+        res["per_stream_input_density"] = stream_dens
+        if "stream_density_targets" in wl:
+            res["stream_change_targets"] = [
+                round(v, 5) for v in wl["stream_density_targets"]]
+    res["roofline"] = roof
+    res["kernels"] = kern
+    res["profiled_ms_per_step"] = prof_ms_step
+    res["frame_gen_s"] = t_gen
+    g.close()
+    del frames
+    return res
+
+
+def extra_workload(name, steps, warmup):
+    """A secondary workload measured in the same run, summarised."""
+    import torch
+    wl = workload(name, 0.0)
+    net = wl["net"]
+    r = measure(wl, steps, warmup, 7, 0.0)
+    r["config"] = {"workload": wl["desc"], "batch": net.batch, "H": net.H,
+                   "W": net.W, "C": net.C, "layers": len(net.layers),
+                   "dtype": net.dtype}
+    torch.cuda.empty_cache()
+    return r
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="resnet50",
-                    choices=["resnet50", "crnn", "toy"])
+                    choices=["resnet50", "effnet_b0", "multistream", "crnn",
+                             "toy"])
     ap.add_argument("--density", type=float, default=0.10)
     ap.add_argument("--thr", type=float, default=0.0)
     ap.add_argument("--profile-steps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the EfficientNet-B0 workloads (512x512 f16 "
+                         "and 32 streams of 256x256 bf16, both with online "
+                         "threshold adjustment)")
     ap.add_argument("--sweep-steps", type=int, default=10)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of a known size "
@@ -366,183 +736,34 @@ def main():
               "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
-    import torch
-    from paper_2410_20790_amd import SparseTemNet
-    from paper_2410_20790_amd import binding as B
-
     wl = workload(args.workload, args.density)
     net = wl["net"]
-    dt = net.dtype
-    es = ESIZE[dt]
     K, W, KP = args.steps, args.warmup, args.profile_steps
-    t_gen = time.perf_counter()
-    frames_np = wl["frames"](1 + W + K + KP)
-    t_gen = time.perf_counter() - t_gen
-    tdt = {"f32": torch.float32, "f16": torch.float16,
-           "bf16": torch.bfloat16}[dt]
-    frames = [torch.from_numpy(f).to("cuda", tdt).contiguous()
-              for f in frames_np]
-    del frames_np
-    g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt)
-    L_n = len(net.layers)
-    thr = [args.thr] * (L_n + 1)
-    out = g.new_output()
-    conv_grid = []
-    for i, L in enumerate(net.layers):
-        Hi, Wi = ((net.H, net.W) if L.src < 0 else
-                  g.tensor_shape(L.src)[1:3])
-        Ho = (Hi + 2 * L.p[0] - L.k[0]) // L.s[0] + 1
-        Wo = (Wi + 2 * L.p[1] - L.k[1]) // L.s[1] + 1
-        conv_grid.append((net.batch, Ho, Wo))
-    dflops = dense_flops(net, conv_grid)
-
-    # reference frame + warm-up
-    g.encode_reference(frames[0], out=out)
-    fi = 1
-    for _ in range(W):
-        g.encode_diff(frames[fi], thr, out=out)
-        fi += 1
-    torch.cuda.synchronize()
-
-    # ---- timed region: K diff frames, nothing else
-    s_ev = torch.cuda.Event(enable_timing=True)
-    e_ev = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    s_ev.record()
-    for _ in range(K):
-        g.encode_diff(frames[fi], thr, out=out)
-        fi += 1
-    e_ev.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_step = wall * 1000.0 / K
-    ev_ms = s_ev.elapsed_time(e_ev) / K
-    dens0 = g.density(-1)
-
-    # ---- second timed pass with an event pair around every launch
-    B.st_profile_begin(g.handle, KP * 1024, KP + 1)
-    torch.cuda.synchronize()
-    tp = time.perf_counter()
-    for _ in range(KP):
-        g.encode_diff(frames[fi], thr, out=out)
-        fi += 1
-    torch.cuda.synchronize()
-    prof_ms_step = (time.perf_counter() - tp) * 1000.0 / KP
-    recs, counts = B.st_profile_end(g.handle, L_n)
-    per_frame_flops = [
-        sum(2 * int(counts[f, j, 1]) * (L.c_in // L.groups) * L.c_out
-            for j, L in enumerate(net.layers)) for f in range(len(counts))]
-    alg_flops = float(np.mean(per_frame_flops))
-    classes = {}
-    for r in recs:
-        name = B.KERNEL_CLASSES[r["kernel"]]
-        c = classes.setdefault(name, {"launches": 0, "ms": 0.0, "bytes": 0.0,
-                                      "flops": 0.0})
-        c["launches"] += 1
-        c["ms"] += float(r["ms"])
-        f, j = int(r["frame"]), int(r["layer"])
-        if name in ("conv_gemm", "conv_dw") and f < len(counts):
-            L = net.layers[j]
-            c["bytes"] += conv_launch_bytes(L, counts[f, j], es,
-                                            layer_mode(net, j))
-            c["flops"] += 2.0 * counts[f, j, 1] * (L.c_in // L.groups) * \
-                L.c_out
-        elif name == "scan_mask":
-            c["bytes"] += net.batch * net.H * net.W * (2 * net.C * es + 1)
-        elif name == "scan_compact" and f < len(counts):
-            n0 = counts[f, 0, 2] if net.layers[0].src == -1 else 0
-            c["bytes"] += net.batch * net.H * net.W + n0 * (
-                3 * net.C * es + 12)
-    total_ms = sum(c["ms"] for c in classes.values())
-    kern = {}
-    for name, c in sorted(classes.items(), key=lambda kv: -kv[1]["ms"]):
-        e = {"launches": c["launches"],
-             "avg_us": 1000.0 * c["ms"] / c["launches"],
-             "share": c["ms"] / total_ms}
-        if c["bytes"]:
-            e["alg_GBps"] = c["bytes"] / (c["ms"] * 1e-3) / 1e9
-            e["hbm_frac"] = e["alg_GBps"] / HBM_PEAK_GBS
-        if c["flops"]:
-            e["alg_TFLOPs"] = c["flops"] / (c["ms"] * 1e-3) / 1e12
-            e["mfma_frac"] = e["alg_TFLOPs"] / MFMA_PEAK_TFLOPS[dt]
-        kern[name] = e
-    dom = max(classes, key=lambda k: classes[k]["ms"])
-    dc = classes[dom]
-    avg_s = dc["ms"] * 1e-3 / dc["launches"]
-    roof = None
-    if dc["bytes"] or dc["flops"]:
-        ai = dc["flops"] / max(dc["bytes"], 1.0)
-        ridge = MFMA_PEAK_TFLOPS[dt] * 1e12 / (HBM_PEAK_GBS * 1e9)
-        if dc["flops"] and ai > ridge:
-            ach = dc["flops"] / dc["launches"] / avg_s / 1e12
-            roof = {"bound": "mfma", "achieved": ach,
-                    "peak": MFMA_PEAK_TFLOPS[dt], "unit": "TFLOP/s",
-                    "frac": ach / MFMA_PEAK_TFLOPS[dt], "traffic": None}
-        else:
-            ach = dc["bytes"] / dc["launches"] / avg_s / 1e9
-            roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS,
-                    "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
-                    "traffic": None}
-        tb = measured_traffic(wl["desc"], dom)
-        if tb is not None:
-            roof["traffic"] = tb
-        roof.update({"kernel": dom, "launches": dc["launches"],
-                     "avg_launch_us": avg_s * 1e6,
-                     "alg_bytes_per_launch": dc["bytes"] / dc["launches"],
-                     "alg_flops_per_launch": dc["flops"] / dc["launches"],
-                     "arith_intensity": ai})
-
-    # ---- dense comparators on the same GPU, net and dtype
-    dense = {}
-    if not args.no_dense:
-        x = frames[0]
-        dense["own_dense_ms"] = time_gpu(
-            lambda: g.encode_reference(x, out=out), 5)
-        fwd = torch_dense_model(net, dt)
-        with torch.no_grad():
-            dense["miopen_ms"] = time_gpu(lambda: fwd(x), 10, warm=3)
-            ref_t = fwd(x).permute(0, 2, 3, 1).float()
-        g.encode_reference(x, out=out)
-        torch.cuda.synchronize()
-        dense["miopen_vs_own_rel_err"] = float(
-            (ref_t - out).abs().max() / out.abs().max())
-
+    r = measure(wl, K, W, KP, args.thr, dense=not args.no_dense)
     res = {
         "metric": METRIC,
-        "value": 1000.0 / ms_step,
+        "value": r.pop("value"),
         "unit": "diff-frames/s",
         "n_gpus": 1, "steps": K, "warmup": W,
-        "ms_per_step": ms_step,
+        "ms_per_step": r.pop("ms_per_step"),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": dt,
+        "dtype": net.dtype,
         "data": "synthetic (seeded temporally continuous video, "
                 "random-init weights)",
         "config": {"workload": wl["desc"], "batch": net.batch, "H": net.H,
-                   "W": net.W, "C": net.C, "layers": L_n,
+                   "W": net.W, "C": net.C, "layers": len(net.layers),
                    "target_density": args.density,
-                   "measured_input_density": dens0, "thr": args.thr},
-        "event_ms_per_step": ev_ms,
-        "effective_tflops": alg_flops / (ms_step * 1e-3) / 1e12,
-        "alg_gflop_per_frame": alg_flops / 1e9,
-        "dense_gflop_per_frame": dflops / 1e9,
-        "dense_equiv_tflops": dflops / (ms_step * 1e-3) / 1e12,
+                   "measured_input_density": r.pop("measured_input_density"),
+                   "thr": "ibst" if wl["ibst"] else args.thr},
     }
-    if dense:
-        res["speedup_vs_dense"] = {
-            "miopen": dense["miopen_ms"] / ms_step,
-            "own_dense": dense["own_dense_ms"] / ms_step}
-        res["dense_ms"] = dense
-    res["roofline"] = roof
-    res["kernels"] = kern
-    res["profiled_ms_per_step"] = prof_ms_step
-    res["frame_gen_s"] = t_gen
+    res.update(r)
     res["kernel_source_hash"] = kernel_source_hash()
-    g.close()
-    del frames
     if args.workload == "resnet50" and not args.no_sweep:
         res["density_sweep"] = density_sweep(
             net, args.thr, [0.02, 0.05, 0.10, 0.20, 0.40], args.sweep_steps)
+    if args.workload == "resnet50" and not args.no_extra:
+        res["other_workloads"] = {
+            n: extra_workload(n, 14, 7) for n in ("effnet_b0", "multistream")}
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, net, args.thr)
     print(json.dumps(res), flush=True)

@@ -224,9 +224,10 @@ bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
     sa.dP = ws.at<float>(L.off_dP);
     sa.Mo = Mo;
     sa.part = ws.at<float>(L.off_separt);
+    sa.S = ws.at<double>(L.off_sesum);
     sa.w1 = ws.at<float>(L.off_sew1);
     sa.b1 = ws.at<float>(L.off_seb1);
-    sa.w2 = ws.at<float>(L.off_sew2);
+    sa.w2t = ws.at<float>(L.off_sew2);
     sa.b2 = ws.at<float>(L.off_seb2);
     float* gates = ws.at<float>(L.off_ses);
     const int64_t gsz = (int64_t)net->N * L.cout_p;
@@ -240,6 +241,8 @@ bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
     sa.cnt_rows = cnt + out.cnt_rows;
     sa.npix = L.conv_grid;
     sa.hw = (int64_t)L.Ho * L.Wo;
+    sa.ngrp = L.conv_grid / 64 + 1;
+    sa.tps = L.se_tps;
     sa.N = net->N;
     sa.cp = L.cout_p;
     sa.c = d.c_out;
@@ -403,7 +406,7 @@ extern "C" st_status st_bind_workspace(st_net* net, void* dev_ptr,
       launch_to_f32_pad(s, net->dtype, d.se_b1, ws.at<float>(L.off_seb1), 1,
                         d.se_mid, 1, d.se_mid);
       launch_to_f32_pad(s, net->dtype, d.se_w2, ws.at<float>(L.off_sew2),
-                        d.c_out, d.se_mid, L.cout_p, d.se_mid);
+                        d.se_mid, d.c_out, d.se_mid, L.cout_p, true);
       launch_to_f32_pad(s, net->dtype, d.se_b2, ws.at<float>(L.off_seb2), 1,
                         d.c_out, 1, L.cout_p);
     }

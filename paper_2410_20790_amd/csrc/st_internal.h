@@ -18,6 +18,20 @@ constexpr int kMaxTiles = 4096;     // compaction tiles per pass
 constexpr int64_t kMaxGrid = (int64_t)kMaxTiles * 8192;  // sites per grid
 constexpr size_t kAlign = 256;      // workspace sub-buffer alignment
 
+// Squeeze-excitation row mapping: each site is handled by a power-of-two
+// group of threads (at most one wave), each thread owning 8-channel vectors;
+// a 256-thread block covers 256 / tps sites side by side.  The squeeze
+// splits each image into about kSePartialFloats / cp site ranges (4..256),
+// so that the partial sums one excitation block reduces stay near
+// kSePartialFloats floats.
+constexpr int kSeMaxChannels = 2048;
+constexpr int kSePartialFloats = 16384;
+inline int se_threads_per_site(int cp) {
+  int t = 1;
+  while (t < cp / 8 && t < 64) t <<= 1;
+  return t;
+}
+
 inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -52,7 +66,7 @@ struct LayerPlan {
   int64_t conv_grid = 0;            // N*Ho*Wo
   bool stateful = false, pool = false, dw = false, ident = false;
   bool se = false;                  // squeeze-excitation after the act
-  int se_mid = 0, se_chunk = 0, se_nchunk = 0;
+  int se_mid = 0, se_chunk = 0, se_nchunk = 0, se_tps = 0;
   int se_par = 0;                   // which gate buffer holds the last gates
   int mode = 0;                     // epilogue mode (kModeState/Defer/Linear)
   // workspace offsets
@@ -65,6 +79,7 @@ struct LayerPlan {
   size_t off_bias = 0;              // f32 [cout_p]
   size_t off_sew1 = 0, off_seb1 = 0, off_sew2 = 0, off_seb2 = 0;  // f32
   size_t off_ses = 0;               // f32 [2][N][cout_p] gates (ping-pong)
+  size_t off_sesum = 0;             // f64 [N][cout_p] channel sums of f(P)
   size_t off_separt = 0;            // f32 [N][se_nchunk][cout_p]
   size_t off_flags = 0;             // uint8 [conv_grid] affected-output flags
   size_t off_pflags = 0;            // uint8 [pooled grid] (pooled layers)

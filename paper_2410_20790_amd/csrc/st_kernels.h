@@ -166,11 +166,12 @@ void launch_group_count(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
 struct SeArgs {
   const float* P;      // state [npix][cp] (updated in place by the emission)
   const float* dP;     // deferred update rows
-  const int* Mo;       // site -> dP row or -1
-  float* part;         // [N][nchunk][cp] partial sums
+  const int* Mo;       // site -> dP row or -1 (every site in the reference)
+  float* part;         // [N][nchunk][cp] partial sums of this frame's change
+  double* S;           // [N][cp] channel sums of f(P), kept across frames
   const float* w1;     // [mid][cp]
   const float* b1;     // [mid]
-  const float* w2;     // [cp][mid]
+  const float* w2t;    // [mid][cp] (second excitation layer, transposed)
   const float* b2;     // [cp]
   float* s_new;        // [N][cp]
   const float* s_old;  // [N][cp]
@@ -178,15 +179,18 @@ struct SeArgs {
   uint32_t* rowmax;
   int* rowpix;
   int* map;
-  uint32_t* grp;       // per-64-site kept counts
+  uint32_t* grp;       // per-64-site kept counts (zeroed by the squeeze)
   u64* cnt_rows;
-  int64_t npix, hw;
-  int N, cp, c, mid, act, ref, chunk, nchunk;
+  int64_t npix, hw, ngrp;
+  int N, cp, c, mid, act, ref, chunk, nchunk, tps;
   float keep_thr;
 };
 void launch_se(const Prof& pf, hipStream_t s, int dtype, const SeArgs& a);
+// Storage-dtype matrix src [rows][cols] (or, transposed, src [cols][rows])
+// to f32 dst [rows_p][cols_p], zero padded; src may be NULL (zeros).
 void launch_to_f32_pad(hipStream_t s, int dtype, const void* src, float* dst,
-                       int rows, int cols, int rows_p, int cols_p);
+                       int rows, int cols, int rows_p, int cols_p,
+                       bool transposed = false);
 
 // ---- dense network output (Accumulation)
 void launch_output(const Prof& pf, hipStream_t s, const float* P, int cp,

@@ -1195,155 +1195,300 @@ void launch_list_compact(const Prof& pf, hipStream_t s, const ListArgs& a) {
 }
 
 // ------------------------------------------------- squeeze-excitation
-// Exact squeeze-excitation on a deferred layer (state P, update dP on the
-// affected sites Mo): partial per-channel sums of f(P_new) over chunks of
-// sites (fixed order, no atomics), gates per image, then the dense emission
-// delta = f(P_new) * s_new - f(P_old) * s_old at every site, with the state
-// commit, row maxima and 64-site kept counts done in the same block.
+__host__ __device__ __forceinline__ int round_up8(int x) {
+  return (x + 7) & ~7;
+}
+
+// Exact squeeze-excitation on a deferred layer (state P, update rows dP of
+// the affected sites, Mo: site -> dP row).  The pooled mean of f(P) is kept
+// as per-image f64 channel sums S that each frame moves by
+// sum over affected sites of f(P_new) - f(P_old) (in the reference pass:
+// by f(P) over every site, from S = 0).  Squeeze: partial sums of that
+// change over fixed site ranges; excite: S, mean and gates per image;
+// emit: delta = f(P_new) * s_new - f(P_old) * s_old at every site, the state
+// commit, row maxima and the 64-site kept counts.  Every sum runs in a fixed
+// order, so results do not depend on scheduling.
+//
+// Row mapping: TPS threads per site (a power of two up to one wave), each
+// owning the 8-channel vectors lane, lane + TPS, ... (at most 4 of them for
+// up to 2048 channels); 256 / TPS sites side by side per block.
+template <int TPS>
 __global__ __launch_bounds__(256) void k_se_squeeze(SeArgs a) {
-  const int n = blockIdx.y;
-  const int64_t p0 = (int64_t)n * a.hw + (int64_t)blockIdx.x * a.chunk;
-  const int64_t p1 = min(p0 + a.chunk, (int64_t)(n + 1) * a.hw);
-  for (int c = threadIdx.x; c < a.cp; c += 256) {
-    float sum = 0.f;
-    for (int64_t p = p0; p < p1; ++p) {
-      const float po = a.ref ? 0.f : a.P[p * a.cp + c];
-      const int r = a.Mo[p];
-      const float pn = r >= 0 ? po + a.dP[(int64_t)r * a.cp + c] : po;
-      sum += act_f(pn, a.act);
-    }
-    a.part[((int64_t)n * a.nchunk + blockIdx.x) * a.cp + c] = sum;
-  }
-}
-
-__global__ __launch_bounds__(256) void k_se_excite(SeArgs a) {
-  extern __shared__ float sm[];  // [cp] means, then [mid] hidden
-  float* m = sm;
-  float* z = sm + a.cp;
-  const int n = blockIdx.x;
-  const float inv = 1.f / (float)a.hw;
-  for (int c = threadIdx.x; c < a.cp; c += 256) {
-    float sum = 0.f;
-    for (int k = 0; k < a.nchunk; ++k)
-      sum += a.part[((int64_t)n * a.nchunk + k) * a.cp + c];
-    m[c] = sum * inv;
-  }
-  __syncthreads();
-  // one wave per hidden unit: z = silu(w1 . m + b1)
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int j = wave; j < a.mid; j += 4) {
-    float d = 0.f;
-    for (int c = lane; c < a.cp; c += 64) d += a.w1[(int64_t)j * a.cp + c] * m[c];
+  constexpr int R = 256 / TPS, IT = TPS == 64 ? 4 : 1;
+  __shared__ float sm[256 * IT * 8];  // [R][cp] per-lane partials
+  const int n = blockIdx.y, g = blockIdx.x;
+  const int lane = threadIdx.x % TPS, rl = threadIdx.x / TPS;
+  const int cp = a.cp, V = cp / 8;
+  // the emission adds its kept counts into these
+  const int64_t nthr = (int64_t)gridDim.x * gridDim.y * 256;
+  for (int64_t i = ((int64_t)n * gridDim.x + g) * 256 + threadIdx.x;
+       i < a.ngrp; i += nthr)
+    a.grp[i] = 0u;
+  float acc[IT][8];
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) d += __shfl_xor(d, o, 64);
-    if (lane == 0) z[j] = act_f(d + a.b1[j], 2);
-  }
-  __syncthreads();
-  for (int c = threadIdx.x; c < a.cp; c += 256) {
-    float e = a.b2[c];
-    for (int j = 0; j < a.mid; ++j) e += a.w2[(int64_t)c * a.mid + j] * z[j];
-    a.s_new[(int64_t)n * a.cp + c] = c < a.c ? 1.f / (1.f + expf(-e)) : 0.f;
-  }
-}
-
-template <typename T>
-__global__ __launch_bounds__(256) void k_se_emit(SeArgs a) {
-  T* dout = (T*)a.dout;
-  const int64_t pix = (int64_t)blockIdx.x * 64 + (threadIdx.x >> 2);
-  const int q = threadIdx.x & 3;
-  const bool in = pix < a.npix;
-  float rm = 0.f;
-  if (in) {
-    const int n = (int)(pix / a.hw);
-    const int r = a.Mo[pix];
-    const float* sn = a.s_new + (int64_t)n * a.cp;
-    const float* so = a.s_old + (int64_t)n * a.cp;
-    for (int c0 = q * 8; c0 < a.cp; c0 += 32) {
-      float po[8], dp[8], pn[8], d[8];
+  for (int k = 0; k < IT; ++k)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[k][e] = 0.f;
+  const int64_t base = (int64_t)n * a.hw;
+  const int64_t s0 = (int64_t)g * a.chunk;
+  const int64_t s1 = min(s0 + (int64_t)a.chunk, a.hw);
+  for (int64_t si = s0 + rl; si < s1; si += R) {
+    const int64_t p = base + si;
+    const int r = a.Mo[p];
+    if (r < 0) continue;
+#pragma unroll
+    for (int k = 0; k < IT; ++k) {
+      const int v = lane + k * TPS;
+      if (v >= V) break;
+      float po[8], dp[8];
       if (a.ref) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) po[e] = 0.f;
       } else {
-        load8f(a.P + pix * a.cp + c0, po);
+        load8f(a.P + p * cp + v * 8, po);
+      }
+      load8f(a.dP + (int64_t)r * cp + v * 8, dp);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        acc[k][e] += act_f(po[e] + dp[e], a.act) - act_f(po[e], a.act);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < IT; ++k) {
+    const int v = lane + k * TPS;
+    if (v < V) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sm[rl * cp + v * 8 + e] = acc[k][e];
+    }
+  }
+  __syncthreads();
+  // pairwise tree over the R row lanes (fixed pairing)
+  for (int h = R / 2; h > 0; h >>= 1) {
+    for (int i = threadIdx.x; i < h * cp; i += 256) {
+      const int j = i / cp, c = i - j * cp;
+      sm[j * cp + c] += sm[(j + h) * cp + c];
+    }
+    __syncthreads();
+  }
+  for (int c = threadIdx.x; c < cp; c += 256)
+    a.part[((int64_t)n * a.nchunk + g) * cp + c] = sm[c];
+}
+
+__global__ __launch_bounds__(256) void k_se_excite(SeArgs a) {
+  extern __shared__ __align__(16) float sm[];  // [cp] means, [mid], [1024]
+  float* m = sm;
+  float* z = sm + a.cp;
+  float4* red = (float4*)(sm + a.cp + round_up8(a.mid));
+  const int n = blockIdx.x, cp = a.cp, V4 = cp / 4;
+  // partial sums as 4-channel vectors: Lc chunk lanes per vector take the
+  // partials g = l, l + Lc, ...; lane 0 adds the Lc results in order
+  const int Lc = V4 <= 256 ? 256 / V4 : 1;
+  const float4* part = (const float4*)(a.part + (int64_t)n * a.nchunk * cp);
+  for (int v0 = 0; v0 < V4; v0 += 256) {
+    const int t = threadIdx.x;
+    const int v = v0 + (Lc > 1 ? t % V4 : t), l = Lc > 1 ? t / V4 : 0;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (v < V4 && l < Lc) {
+#pragma unroll 8
+      for (int g = l; g < a.nchunk; g += Lc) {
+        const float4 q = part[(int64_t)g * V4 + v];
+        acc.x += q.x; acc.y += q.y; acc.z += q.z; acc.w += q.w;
+      }
+    }
+    red[t] = acc;
+    __syncthreads();
+    if (v < V4 && l == 0) {
+      float4 tot = red[t];
+      for (int j = 1; j < Lc; ++j) {
+        const float4 q = red[t + j * V4];
+        tot.x += q.x; tot.y += q.y; tot.z += q.z; tot.w += q.w;
+      }
+      const float tv[4] = {tot.x, tot.y, tot.z, tot.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int c = 4 * v + k;
+        double* S = a.S + (int64_t)n * cp + c;
+        const double sv = (a.ref ? 0.0 : *S) + (double)tv[k];
+        *S = sv;
+        m[c] = (float)(sv / (double)a.hw);
+      }
+    }
+    __syncthreads();
+  }
+  // hidden units z = silu(w1 . m + b1): one wave per unit, two units per
+  // pass, 4-channel vectors (up to 8 per lane in flight)
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const float4* m4 = (const float4*)m;
+  for (int j0 = wave; j0 < a.mid; j0 += 8) {
+    const int j1 = j0 + 4;
+    const float4* w0 = (const float4*)(a.w1 + (int64_t)j0 * cp);
+    const float4* w1 = (const float4*)(a.w1 + (int64_t)(j1 < a.mid ? j1 : j0)
+                                       * cp);
+    float d0 = 0.f, d1 = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int v = lane + 64 * i;
+      if (v < cp / 4) {
+        const float4 x = m4[v], p = w0[v], q = w1[v];
+        d0 += p.x * x.x + p.y * x.y + p.z * x.z + p.w * x.w;
+        d1 += q.x * x.x + q.y * x.y + q.z * x.z + q.w * x.w;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      d0 += __shfl_xor(d0, o, 64);
+      d1 += __shfl_xor(d1, o, 64);
+    }
+    if (lane == 0) {
+      z[j0] = act_f(d0 + a.b1[j0], 2);
+      if (j1 < a.mid) z[j1] = act_f(d1 + a.b1[j1], 2);
+    }
+  }
+  __syncthreads();
+  // gates: 4-channel vectors, hidden loop unrolled so loads overlap
+  for (int v = threadIdx.x; v < cp / 4; v += 256) {
+    float4 e = ((const float4*)a.b2)[v];
+    const float4* w = (const float4*)a.w2t + v;
+#pragma unroll 8
+    for (int j = 0; j < a.mid; ++j) {
+      const float4 q = w[(int64_t)j * (cp / 4)];
+      const float zj = z[j];
+      e.x += q.x * zj; e.y += q.y * zj; e.z += q.z * zj; e.w += q.w * zj;
+    }
+    const float ev[4] = {e.x, e.y, e.z, e.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int c = 4 * v + k;
+      a.s_new[(int64_t)n * cp + c] =
+          c < a.c ? 1.f / (1.f + expf(-ev[k])) : 0.f;
+    }
+  }
+}
+
+template <typename T, int TPS>
+__global__ __launch_bounds__(256) void k_se_emit(SeArgs a) {
+  constexpr int R = 256 / TPS, IT = TPS == 64 ? 4 : 1;
+  T* dout = (T*)a.dout;
+  const int lane = threadIdx.x % TPS;
+  const int64_t row = (int64_t)blockIdx.x * R + threadIdx.x / TPS;
+  const int cp = a.cp, V = cp / 8;
+  const bool in = row < a.npix;
+  float rm = 0.f;
+  if (in) {
+    const int n = (int)(row / a.hw);
+    const int r = a.Mo[row];
+    const float* sn = a.s_new + (int64_t)n * cp;
+    const float* so = a.s_old + (int64_t)n * cp;
+#pragma unroll
+    for (int k = 0; k < IT; ++k) {
+      const int v = lane + k * TPS;
+      if (v >= V) break;
+      const int c0 = v * 8;
+      float po[8], dp[8], gn[8], go[8], pn[8], d[8];
+      if (a.ref) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) po[e] = 0.f;
+      } else {
+        load8f(a.P + row * cp + c0, po);
       }
       if (r >= 0) {
-        load8f(a.dP + (int64_t)r * a.cp + c0, dp);
+        load8f(a.dP + (int64_t)r * cp + c0, dp);
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) dp[e] = 0.f;
       }
+      load8f(sn + c0, gn);
+      load8f(so + c0, go);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        pn[e] = r >= 0 ? po[e] + dp[e] : po[e];
-        const float en = act_f(pn[e], a.act) * sn[c0 + e];
-        const float eo = a.ref ? 0.f : act_f(po[e], a.act) * so[c0 + e];
+        pn[e] = po[e] + dp[e];
+        const float en = act_f(pn[e], a.act) * gn[e];
+        const float eo = a.ref ? 0.f : act_f(po[e], a.act) * go[e];
         d[e] = en - eo;
       }
-      rm = fmaxf(rm, Vec8<T>::store(dout + pix * a.cp + c0, d));
-      if (r >= 0) store8f(const_cast<float*>(a.P) + pix * a.cp + c0, pn);
+      rm = fmaxf(rm, Vec8<T>::store(dout + row * cp + c0, d));
+      if (r >= 0) store8f(const_cast<float*>(a.P) + row * cp + c0, pn);
     }
   }
-  rm = fmaxf(rm, __shfl_xor(rm, 1, 64));
-  rm = fmaxf(rm, __shfl_xor(rm, 2, 64));
-  if (in && q == 0) {
-    a.rowmax[pix] = __float_as_uint(rm);
-    a.rowpix[pix] = (int)pix;
-    a.map[pix] = (int)pix;
+#pragma unroll
+  for (int o = 1; o < TPS; o <<= 1) rm = fmaxf(rm, __shfl_xor(rm, o, 64));
+  if (in && lane == 0) {
+    a.rowmax[row] = __float_as_uint(rm);
+    a.rowpix[row] = (int)row;
+    a.map[row] = (int)row;
   }
-  const u64 b = __ballot(in && q == 0 && rm > a.keep_thr);
-  __shared__ unsigned wc[4];
-  if ((threadIdx.x & 63) == 0) wc[threadIdx.x >> 6] = (unsigned)__popcll(b);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    a.grp[blockIdx.x] = wc[0] + wc[1] + wc[2] + wc[3];
-    if (blockIdx.x == 0) *a.cnt_rows = (u64)a.npix;
+  // the sites of one wave lie in one 64-site group
+  const u64 b = __ballot(in && lane == 0 && rm > a.keep_thr);
+  if ((threadIdx.x & 63) == 0 && b) {
+    const int64_t first = (int64_t)blockIdx.x * R + (threadIdx.x / TPS);
+    atomicAdd(a.grp + first / 64, (unsigned)__popcll(b));
   }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *a.cnt_rows = (u64)a.npix;
 }
 
-void launch_se(const Prof& pf, hipStream_t s, int dtype, const SeArgs& a) {
+template <int TPS>
+static void se_t(const Prof& pf, hipStream_t s, int dtype, const SeArgs& a) {
   prof_begin(pf, 19 /*ST_K_SE_SQUEEZE*/, s);
-  k_se_squeeze<<<dim3(a.nchunk, a.N), 256, 0, s>>>(a);
+  k_se_squeeze<TPS><<<dim3(a.nchunk, a.N), 256, 0, s>>>(a);
   prof_end(pf, 19, s);
   prof_begin(pf, 20 /*ST_K_SE_EXCITE*/, s);
-  k_se_excite<<<a.N, 256, sizeof(float) * (a.cp + a.mid), s>>>(a);
+  k_se_excite<<<a.N, 256,
+                sizeof(float) * (a.cp + round_up8(a.mid) + 1024), s>>>(a);
   prof_end(pf, 20, s);
-  const int blocks = (int)((a.npix + 63) / 64);
+  constexpr int R = 256 / TPS;
+  const int blocks = (int)((a.npix + R - 1) / R);
   prof_begin(pf, 21 /*ST_K_SE_EMIT*/, s);
   if (dtype == 0)
-    k_se_emit<float><<<blocks, 256, 0, s>>>(a);
+    k_se_emit<float, TPS><<<blocks, 256, 0, s>>>(a);
   else if (dtype == 1)
-    k_se_emit<_Float16><<<blocks, 256, 0, s>>>(a);
+    k_se_emit<_Float16, TPS><<<blocks, 256, 0, s>>>(a);
   else
-    k_se_emit<bf16_t><<<blocks, 256, 0, s>>>(a);
+    k_se_emit<bf16_t, TPS><<<blocks, 256, 0, s>>>(a);
   prof_end(pf, 21, s);
 }
 
-// Storage-dtype matrix [rows][cols] -> f32 [rows_p][cols_p], zero padded
-// (squeeze-excitation weights); src may be NULL (zeros).
+void launch_se(const Prof& pf, hipStream_t s, int dtype, const SeArgs& a) {
+  switch (a.tps) {
+    case 1: se_t<1>(pf, s, dtype, a); break;
+    case 2: se_t<2>(pf, s, dtype, a); break;
+    case 4: se_t<4>(pf, s, dtype, a); break;
+    case 8: se_t<8>(pf, s, dtype, a); break;
+    case 16: se_t<16>(pf, s, dtype, a); break;
+    case 32: se_t<32>(pf, s, dtype, a); break;
+    default: se_t<64>(pf, s, dtype, a); break;
+  }
+}
+
 template <typename T>
 __global__ void k_to_f32_pad(const T* src, float* dst, int rows, int cols,
-                             int rows_p, int cols_p) {
+                             int rows_p, int cols_p, int transposed) {
   const int64_t total = (int64_t)rows_p * cols_p;
   for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
        idx += (int64_t)gridDim.x * 256) {
     const int r = (int)(idx / cols_p), c = (int)(idx - (int64_t)r * cols_p);
-    dst[idx] = (src && r < rows && c < cols)
-                   ? to_f(src[(int64_t)r * cols + c]) : 0.f;
+    float v = 0.f;
+    if (src && r < rows && c < cols)
+      v = to_f(transposed ? src[(int64_t)c * rows + r]
+                          : src[(int64_t)r * cols + c]);
+    dst[idx] = v;
   }
 }
 
 void launch_to_f32_pad(hipStream_t s, int dtype, const void* src, float* dst,
-                       int rows, int cols, int rows_p, int cols_p) {
+                       int rows, int cols, int rows_p, int cols_p,
+                       bool transposed) {
   const int grid = grid_for((int64_t)rows_p * cols_p, 1024);
+  const int tr = transposed ? 1 : 0;
   if (dtype == 0)
     k_to_f32_pad<float><<<grid, 256, 0, s>>>((const float*)src, dst, rows,
-                                             cols, rows_p, cols_p);
+                                             cols, rows_p, cols_p, tr);
   else if (dtype == 1)
     k_to_f32_pad<_Float16><<<grid, 256, 0, s>>>((const _Float16*)src, dst,
-                                                rows, cols, rows_p, cols_p);
+                                                rows, cols, rows_p, cols_p,
+                                                tr);
   else
     k_to_f32_pad<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)src, dst, rows,
-                                              cols, rows_p, cols_p);
+                                              cols, rows_p, cols_p, tr);
 }
 
 // ------------------------------------------------------- dense output

@@ -146,6 +146,9 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
     L.conv_grid = (int64_t)batch * L.Ho * L.Wo;
     L.se = d.se_mid > 0;
     L.se_mid = d.se_mid;
+    if (L.se && L.cout_p > kSeMaxChannels)
+      return bad(ST_ERR_UNSUPPORTED, i,
+                 "squeeze-excitation on more than 2048 channels");
     L.stateful = d.act != ST_ACT_NONE || L.pool || L.se || i == n_layers - 1;
     L.mode = (L.pool || L.se) ? kModeDefer
                               : (L.stateful ? kModeState : kModeLinear);
@@ -218,13 +221,19 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
     if (L.pool) L.off_pflags = a.take(round_up(T.grid, 16));
     if (L.se) {
       const int64_t hw = (int64_t)L.Ho * L.Wo;
-      L.se_chunk = 128;
+      L.se_tps = se_threads_per_site(L.cout_p);
+      const int64_t lanes = 256 / L.se_tps;
+      const int64_t parts =
+          std::min<int64_t>(256, std::max<int64_t>(4, kSePartialFloats /
+                                                          L.cout_p));
+      L.se_chunk = (int)round_up(ceil_div(hw, parts), lanes);
       L.se_nchunk = (int)ceil_div(hw, L.se_chunk);
       L.off_sew1 = a.take(sizeof(float) * L.se_mid * L.cout_p);
       L.off_seb1 = a.take(sizeof(float) * L.se_mid);
       L.off_sew2 = a.take(sizeof(float) * L.cout_p * L.se_mid);
       L.off_seb2 = a.take(sizeof(float) * L.cout_p);
       L.off_ses = a.take(sizeof(float) * 2 * batch * L.cout_p);
+      L.off_sesum = a.take(sizeof(double) * batch * L.cout_p);
       L.off_separt = a.take(sizeof(float) * batch * L.se_nchunk * L.cout_p);
     }
   }
