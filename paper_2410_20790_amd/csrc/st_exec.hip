@@ -182,6 +182,8 @@ bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   a.mdone = ws.at<uint32_t>(net->off_mdone);
   a.keep_thr = thr;
   a.zero = ws.at<char>(net->off_zero);
+  a.part = ws.at<float>(net->off_part);
+  a.split_max = L.split_max;
   if (L.dw)
     launch_conv_dw(pf, s, net->dtype, a);
   else if (!launch_conv_gemm(pf, s, net->dtype, a))

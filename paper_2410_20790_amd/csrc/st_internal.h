@@ -24,6 +24,12 @@ constexpr size_t kAlign = 256;      // workspace sub-buffer alignment
 // splits each image into about kSePartialFloats / cp site ranges (4..256),
 // so that the partial sums one excitation block reduces stay near
 // kSePartialFloats floats.
+// Reduction splits of the gather-GEMM: a layer with at least
+// kSplitMinLayerStages reduction stages may split each output tile into up
+// to stages / 8 (at most kSplitMax) parts when a frame has few tiles.
+constexpr int kSplitMinLayerStages = 32;
+constexpr int kSplitMax = 8;
+
 constexpr int kSeMaxChannels = 2048;
 constexpr int kSePartialFloats = 16384;
 inline int se_threads_per_site(int cp) {
@@ -69,6 +75,7 @@ struct LayerPlan {
   int se_mid = 0, se_chunk = 0, se_nchunk = 0, se_tps = 0;
   int se_par = 0;                   // which gate buffer holds the last gates
   int mode = 0;                     // epilogue mode (kModeState/Defer/Linear)
+  int split_max = 1;                // most reduction splits per output tile
   // workspace offsets
   size_t off_P = 0;                 // f32 [conv_grid][cout_p]
   size_t off_O = 0;                 // int32 [conv_grid] affected conv outputs
@@ -104,6 +111,7 @@ struct st_net {
   size_t off_grp = 0;                      // uint32 [max grid / 64 + 1]
   size_t off_mdone = 0;                    // uint32 [max grid / 64 + 1]
   size_t off_zero = 0;                     // 256 zero bytes
+  size_t off_part = 0;                     // f32 split partials (shared)
   size_t off_cnt = 0;                      // uint64 [n_counters]
   size_t off_cleanup = 0;                  // cleanup descriptor table
   size_t off_dens = 0;                     // uint64 [batch] per-image counts

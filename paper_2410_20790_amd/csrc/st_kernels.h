@@ -119,6 +119,11 @@ struct ConvArgs {
   uint32_t* mdone;     // per-row-tile arrival counters (zero between uses)
   float keep_thr;      // threshold of the emitted tensor
   const void* zero;    // 16 zero bytes (16-byte aligned)
+  // split reduction: up to split_max splits of the reduction stages per
+  // output tile (chosen per frame from the tile count), their f32 partial
+  // tiles in part [split][capO][cout_p]; split_max = 1: no split
+  float* part;
+  int split_max;
 };
 // Returns false (and launches nothing) when a.zero is missing or misaligned.
 bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,

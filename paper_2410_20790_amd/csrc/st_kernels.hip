@@ -619,7 +619,119 @@ __device__ __forceinline__ void store8f(float* p, const float* f) {
   *(float4*)(p + 4) = make_float4(f[4], f[5], f[6], f[7]);
 }
 
-template <typename T, bool REF, bool ALIGNED>
+// Reduction stages of a layer that hold real (not padding) columns.
+template <typename T>
+__device__ __forceinline__ int gemm_stages(const ConvArgs& a) {
+  constexpr int KC = MmaCfg<T>::KC;
+  return min((int)a.ktot_p, (a.K * a.cin_p + KC - 1) / KC * KC) / KC;
+}
+
+// Splits of the reduction per output tile for this frame: enough work units
+// (tiles x splits) to give every CU several, at most split_max, and at
+// least kSplitMinStages stages per split.  The GEMM and its split epilogue
+// both derive it from the same device count.
+constexpr int kSplitTarget = 1024, kSplitMinStages = 4;
+__device__ __forceinline__ int split_count(int64_t ntiles, int nst, int smax) {
+  if (smax <= 1 || ntiles <= 0) return 1;
+  int64_t sp = (kSplitTarget + ntiles - 1) / ntiles;
+  sp = min(sp, (int64_t)smax);
+  sp = min(sp, (int64_t)max(1, nst / kSplitMinStages));
+  return (int)max(sp, (int64_t)1);
+}
+
+// Finishes one thread's share of an output tile -- row eo of the tile,
+// columns n0 + ec + [0, 16) -- from the reduced values v: adds the bias
+// (reference pass) and the residual delta, then either defers the update
+// (mode 1), or updates the f32 state in place and emits f(P_new) - f(P_old)
+// (mode 0), or passes the linear delta on (mode 2).  Row maxima are merged
+// with device-scope atomics; the last block to finish a row tile (over its
+// column tiles) counts the tile's kept rows for the truncation pass.  Every
+// thread of the block must call it (it synchronises).
+template <typename T, bool REF, class LoadV>
+__device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
+                                            const float (&po)[2][8],
+                                            const float (&sk)[2][8],
+                                            const bool (&hv)[2], int64_t eo,
+                                            bool eok, int epix, int64_t m0,
+                                            int n0, int ec, int tiles_n,
+                                            int64_t nO, int* s_last) {
+  constexpr int BM = kGemmBM;
+  const int tid = threadIdx.x;
+  const int cout_p = a.cout_p;
+  T* dout = (T*)a.dout;
+  float rm = 0.f;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (!hv[h]) continue;
+    const int n = n0 + ec + 8 * h;
+    float v[8];
+    load_v(h, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (REF) v[e] += a.bias[n + e];
+      v[e] += sk[h][e];
+    }
+    if (a.mode == 1) {
+      store8f(a.dP + eo * cout_p + n, v);
+      continue;
+    }
+    if (a.mode == 0) {
+      float pn[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        pn[e] = po[h][e] + v[e];
+        v[e] = act_f(pn[e], a.act) - act_f(po[h][e], a.act);
+      }
+      store8f(a.P + (int64_t)epix * cout_p + n, pn);
+    }
+    rm = fmaxf(rm, Vec8<T>::store(dout + eo * cout_p + n, v));
+  }
+  // the four threads of a row are adjacent lanes
+  rm = fmaxf(rm, __shfl_xor(rm, 1, 64));
+  rm = fmaxf(rm, __shfl_xor(rm, 2, 64));
+  // row maxima: device-scope atomics whose results are waited for, so
+  // they have completed at the coherence point before the barrier below
+  unsigned seen = 0u;
+  if (eok && (tid & 3) == 0 && a.mode != 1 && rm > 0.f)
+    seen = __hip_atomic_fetch_max(a.rowmax + eo, __float_as_uint(rm),
+                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+  // The last block to finish a row tile (over its column tiles) counts
+  // the tile's kept rows for the truncation pass, reading the row maxima
+  // with device-scope atomic loads; the arrival counter is reset by the
+  // block that reads it.  No cache-maintenance fence is needed: only
+  // atomics carry data between the blocks.
+  if (a.grp) {
+    const int64_t tm = m0 / BM;
+    if (seen == 0xFFFFFFFFu) *s_last = 0;  // consumes the atomic results
+    __syncthreads();
+    if (tid == 0)
+      *s_last = __hip_atomic_fetch_add(a.mdone + tm, 1u, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT) ==
+                (unsigned)(tiles_n - 1);
+    __syncthreads();
+    if (*s_last && tid < 64) {
+      const int64_t o = m0 + tid;
+      bool k = false;
+      if (o < nO)
+        k = __uint_as_float(__hip_atomic_load(a.rowmax + o, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT)) >
+            a.keep_thr;
+      const u64 b = __ballot(k);
+      if (tid == 0) {
+        a.grp[tm] = (uint32_t)__popcll(b);
+        __hip_atomic_store(a.mdone + tm, 0u, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
+}
+
+// SPLIT: the layer's reduction may be split (split_max > 1); every unit
+// then writes its partial tile (even when this frame needs one split) and
+// the split epilogue finishes the tiles, so no epilogue state is held
+// through the reduction.
+template <typename T, bool REF, bool ALIGNED, bool SPLIT>
 __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   constexpr int BM = kGemmBM, BN = kGemmBN;
   constexpr int KC = MmaCfg<T>::KC, LD = MmaCfg<T>::LD;
@@ -643,7 +755,6 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   const T* din = (const T*)a.din;
   const T* wt = (const T*)a.w;
   const T* zvec = (const T*)a.zero;
-  T* dout = (T*)a.dout;
   const T* dskip = (const T*)a.dskip;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -657,21 +768,30 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   // reduction stages that hold real (not padding) columns; with ALIGNED
   // (cin_p a multiple of KC) every stage lies within one kernel offset and
   // offset k covers stages [k * spk, (k + 1) * spk)
-  const int nst = min(ktot_p, (K * cin_p + KC - 1) / KC * KC) / KC;
+  const int nst = gemm_stages<T>(a);
   const int spk = ALIGNED ? cin_p / KC : 1;
+  // work units: (split, tile) pairs, split-major, so that neighbouring
+  // tiles of one split (which gather the same input rows) stay together
+  const int S = SPLIT ? split_count(ntiles, nst, a.split_max) : 1;
+  const int64_t nunits = ntiles * S;
   // XCD-aware order: blocks are dealt round-robin over the kXcd XCDs
-  // (gridDim.x is a multiple of kXcd); the tile range is cut into kXcd
+  // (gridDim.x is a multiple of kXcd); the unit range is cut into kXcd
   // contiguous chunks, one per XCD, and the XCD's blocks stride through
   // their chunk, so neighbouring tiles (which share gathered rows) meet in
-  // one L2 and every XCD gets work however few tiles there are.
-  const int chunk = (int)((ntiles + kXcd - 1) / kXcd);
+  // one L2 and every XCD gets work however few units there are.
+  const int chunk = (int)((nunits + kXcd - 1) / kXcd);
   const int xcd = blockIdx.x % kXcd;
-  const int t_end = (int)min(ntiles, (int64_t)(xcd + 1) * chunk);
+  const int u_end = (int)min(nunits, (int64_t)(xcd + 1) * chunk);
   const int per_xcd = gridDim.x / kXcd;
   // epilogue ownership: thread -> row em, columns [ec, ec + 16) of the tile
   const int em = tid >> 2, ec = (tid & 3) * 16;
 
-  for (int t = xcd * chunk + blockIdx.x / kXcd; t < t_end; t += per_xcd) {
+  for (int u = xcd * chunk + blockIdx.x / kXcd; u < u_end; u += per_xcd) {
+    // this unit's split and tile, and its reduction stages [st_lo, st_hi)
+    const int sp = SPLIT ? (int)((unsigned)u / (unsigned)ntiles) : 0;
+    const int t = SPLIT ? u - sp * (int)ntiles : u;
+    const int st_lo = SPLIT ? (int)((int64_t)sp * nst / S) : 0;
+    const int st_hi = SPLIT ? (int)((int64_t)(sp + 1) * nst / S) : nst;
     const int tm_i = (int)((unsigned)t / (unsigned)tiles_n);
     const int64_t m0 = (int64_t)tm_i * BM;
     const int n0 = (t - tm_i * tiles_n) * BN;
@@ -701,10 +821,10 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
       hv[h] = eok && n < cout_p;
 #pragma unroll
       for (int e = 0; e < 8; ++e) po[h][e] = sk[h][e] = 0.f;
-      if (hv[h] && a.mode == 0 && !REF)
+      if (!SPLIT && hv[h] && a.mode == 0 && !REF)
         load8f(a.P + (int64_t)epix * cout_p + n, po[h]);
     }
-    const int rsk = (a.mskip && eok) ? a.mskip[epix] : -1;
+    const int rsk = (!SPLIT && a.mskip && eok) ? a.mskip[epix] : -1;
     if (rsk >= 0) {
 #pragma unroll
       for (int h = 0; h < 2; ++h)
@@ -735,26 +855,37 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
       int kc, sub, st;
     };
     auto first_stage = [&]() {
-      It it{0, 0, 0};
-      if (ALIGNED) {
+      It it{0, 0, st_lo};
+      if (ALIGNED && !SPLIT) {
         it.kc = next_k(0);
-        it.st = it.kc < K ? it.kc * spk : nst;
+        it.st = it.kc < K ? it.kc * spk : st_hi;
+      } else if (ALIGNED) {
+        it.kc = st_lo / spk;
+        it.sub = st_lo - it.kc * spk;
+        if (!((kmask >> it.kc) & 1ull)) {
+          it.kc = next_k(it.kc + 1);
+          it.sub = 0;
+        }
+        it.st = it.kc < K ? min(it.kc * spk + it.sub, st_hi) : st_hi;
       } else {
-        while (it.st < nst && !stage_active(it.st)) ++it.st;
+        while (it.st < st_hi && !stage_active(it.st)) ++it.st;
       }
       return it;
     };
     auto advance = [&](It it) {
-      if (it.st >= nst) return it;
+      if (it.st >= st_hi) return it;
       if (ALIGNED) {
         if (++it.sub == spk) {
           it.kc = next_k(it.kc + 1);
           it.sub = 0;
         }
-        it.st = it.kc < K ? it.kc * spk + it.sub : nst;
+        if (SPLIT)
+          it.st = it.kc < K ? min(it.kc * spk + it.sub, st_hi) : st_hi;
+        else
+          it.st = it.kc < K ? it.kc * spk + it.sub : st_hi;
       } else {
         ++it.st;
-        while (it.st < nst && !stage_active(it.st)) ++it.st;
+        while (it.st < st_hi && !stage_active(it.st)) ++it.st;
       }
       return it;
     };
@@ -764,7 +895,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     // the end read a zero vector), so the loads of the next two stages can
     // stay in flight while the current one is staged and multiplied.
     auto load_stage = [&](const It& it, uint4 (&ra)[AV], uint4 (&rb)[BV]) {
-      const bool live = it.st < nst;
+      const bool live = it.st < st_hi;
       const int r0 = it.st * KC;
 #pragma unroll
       for (int q = 0; q < AV; ++q) {
@@ -874,14 +1005,14 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     It ib = advance(ia);
     load_stage(ib, ra1, rb1);
     int buf = 0;
-    while (ia.st < nst) {
+    while (ia.st < st_hi) {
       store_stage(buf, ra0, rb0);
       __syncthreads();
       const It ic = advance(ib);
       load_stage(ic, ra0, rb0);
       compute(buf);
       buf ^= 1;
-      if (ib.st >= nst) break;
+      if (ib.st >= st_hi) break;
       store_stage(buf, ra1, rb1);
       __syncthreads();
       const It id = advance(ic);
@@ -906,100 +1037,124 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
           Cs[(wm * 32 + i * 16 + 4 * lg + r) * CLD + wn * 32 + j * 16 + l16] =
               acc[i][j][r];
     __syncthreads();
-    float rm = 0.f;
+    const float* crow = Cs + em * CLD + ec;
+    if constexpr (SPLIT) {
+      // partial tile of split sp, reduced by the split epilogue
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        if (!hv[h]) continue;
+        float v[8];
+        load8f(crow + 8 * h, v);
+        store8f(a.part + ((int64_t)sp * a.capO + eo) * cout_p + n0 + ec +
+                    8 * h,
+                v);
+      }
+    } else {
+      finish_tile<T, REF>(
+          a, [&](int h, float* v) { load8f(crow + 8 * h, v); }, po, sk, hv,
+          eo, eok, epix, m0, n0, ec, tiles_n, nO, &s_last);
+    }
+  }
+}
+
+// Split epilogue: sums the partial tiles of this frame's splits in split
+// order and finishes each output tile as the unsplit GEMM does.
+template <typename T, bool REF>
+__global__ __launch_bounds__(256) void k_split_epi(ConvArgs a) {
+  constexpr int BM = kGemmBM, BN = kGemmBN;
+  __shared__ int s_last;
+  const int64_t nO = (int64_t)*a.nO;
+  const int64_t tiles_m = (nO + BM - 1) / BM;
+  const int tiles_n = (a.cout_p + BN - 1) / BN;
+  const int64_t ntiles = tiles_m * tiles_n;
+  const int S = split_count(ntiles, gemm_stages<T>(a), a.split_max);
+  const int tid = threadIdx.x, cout_p = a.cout_p;
+  const int em = tid >> 2, ec = (tid & 3) * 16;
+  const T* dskip = (const T*)a.dskip;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    __syncthreads();  // the previous tile's reads of s_last are done
+    const int64_t tm_i = t / tiles_n;
+    const int64_t m0 = tm_i * BM;
+    const int n0 = (int)(t - tm_i * tiles_n) * BN;
+    const int64_t eo = m0 + em;
+    const bool eok = eo < nO;
+    const int epix = eok ? a.O[eo] : 0;
+    bool hv[2];
+    float po[2][8], sk[2][8];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      if (!hv[h]) continue;
       const int n = n0 + ec + 8 * h;
-      float v[8];
-      load8f(Cs + em * CLD + ec + 8 * h, v);
+      hv[h] = eok && n < cout_p;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        if (REF) v[e] += a.bias[n + e];
-        v[e] += sk[h][e];
-      }
-      if (a.mode == 1) {
-        store8f(a.dP + eo * cout_p + n, v);
-        continue;
-      }
-      if (a.mode == 0) {
-        float pn[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          pn[e] = po[h][e] + v[e];
-          v[e] = act_f(pn[e], a.act) - act_f(po[h][e], a.act);
-        }
-        store8f(a.P + (int64_t)epix * cout_p + n, pn);
-      }
-      rm = fmaxf(rm, Vec8<T>::store(dout + eo * cout_p + n, v));
+      for (int e = 0; e < 8; ++e) po[h][e] = sk[h][e] = 0.f;
+      if (hv[h] && a.mode == 0 && !REF)
+        load8f(a.P + (int64_t)epix * cout_p + n, po[h]);
     }
-    // the four threads of a row are adjacent lanes
-    rm = fmaxf(rm, __shfl_xor(rm, 1, 64));
-    rm = fmaxf(rm, __shfl_xor(rm, 2, 64));
-    // row maxima: device-scope atomics whose results are waited for, so
-    // they have completed at the coherence point before the barrier below
-    unsigned seen = 0u;
-    if (eok && (tid & 3) == 0 && a.mode != 1 && rm > 0.f)
-      seen = __hip_atomic_fetch_max(a.rowmax + eo, __float_as_uint(rm),
-                                    __ATOMIC_RELAXED,
-                                    __HIP_MEMORY_SCOPE_AGENT);
+    const int rsk = (a.mskip && eok) ? a.mskip[epix] : -1;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      if (hv[h] && rsk >= 0)
+        Vec8<T>::load(dskip + (int64_t)rsk * cout_p + n0 + ec + 8 * h, sk[h]);
+    const float* prow = a.part + eo * cout_p + n0 + ec;
+    const int64_t pstride = a.capO * cout_p;
+    finish_tile<T, REF>(
+        a,
+        [&](int h, float* v) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = 0.f;
+          for (int sp = 0; sp < S; ++sp) {
+            float q[8];
+            load8f(prow + sp * pstride + 8 * h, q);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] += q[e];
+          }
+        },
+        po, sk, hv, eo, eok, epix, m0, n0, ec, tiles_n, nO, &s_last);
+  }
+}
 
-    // The last block to finish a row tile (over its column tiles) counts
-    // the tile's kept rows for the truncation pass, reading the row maxima
-    // with device-scope atomic loads; the arrival counter is reset by the
-    // block that reads it.  No cache-maintenance fence is needed: only
-    // atomics carry data between the blocks.
-    if (a.grp) {
-      const int64_t tm = m0 / BM;
-      if (seen == 0xFFFFFFFFu) s_last = 0;  // consumes the atomic results
-      __syncthreads();
-      if (tid == 0)
-        s_last = __hip_atomic_fetch_add(a.mdone + tm, 1u, __ATOMIC_RELAXED,
-                                        __HIP_MEMORY_SCOPE_AGENT) ==
-                 (unsigned)(tiles_n - 1);
-      __syncthreads();
-      if (s_last && tid < 64) {
-        const int64_t o = m0 + tid;
-        bool k = false;
-        if (o < nO)
-          k = __uint_as_float(__hip_atomic_load(a.rowmax + o, __ATOMIC_RELAXED,
-                                                __HIP_MEMORY_SCOPE_AGENT)) >
-              a.keep_thr;
-        const u64 b = __ballot(k);
-        if (tid == 0) {
-          a.grp[tm] = (uint32_t)__popcll(b);
-          __hip_atomic_store(a.mdone + tm, 0u, __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
-        }
-      }
-    }
+template <typename T>
+static void split_epi_t(hipStream_t s, int grid, const ConvArgs& a) {
+  if (a.ref)
+    k_split_epi<T, true><<<grid, 256, 0, s>>>(a);
+  else
+    k_split_epi<T, false><<<grid, 256, 0, s>>>(a);
+}
+
+template <typename T, bool SPLIT>
+static void gemm_t(hipStream_t s, int grid, size_t lds, const ConvArgs& a) {
+  const bool aligned = a.cin_p % MmaCfg<T>::KC == 0;
+  if (a.ref) {
+    if (aligned)
+      k_conv_gemm<T, true, true, SPLIT><<<grid, 256, lds, s>>>(a);
+    else
+      k_conv_gemm<T, true, false, SPLIT><<<grid, 256, lds, s>>>(a);
+  } else {
+    if (aligned)
+      k_conv_gemm<T, false, true, SPLIT><<<grid, 256, lds, s>>>(a);
+    else
+      k_conv_gemm<T, false, false, SPLIT><<<grid, 256, lds, s>>>(a);
   }
 }
 
 template <typename T>
 static void gemm_t(hipStream_t s, int grid, size_t lds, const ConvArgs& a) {
-  const bool aligned = a.cin_p % MmaCfg<T>::KC == 0;
-  if (a.ref) {
-    if (aligned)
-      k_conv_gemm<T, true, true><<<grid, 256, lds, s>>>(a);
-    else
-      k_conv_gemm<T, true, false><<<grid, 256, lds, s>>>(a);
-  } else {
-    if (aligned)
-      k_conv_gemm<T, false, true><<<grid, 256, lds, s>>>(a);
-    else
-      k_conv_gemm<T, false, false><<<grid, 256, lds, s>>>(a);
-  }
+  if (a.split_max > 1)
+    gemm_t<T, true>(s, grid, lds, a);
+  else
+    gemm_t<T, false>(s, grid, lds, a);
 }
 
 bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
                       const ConvArgs& a) {
   // inactive lanes read the zero vector: never launch without it
   if (!a.zero || ((uintptr_t)a.zero & 15)) return false;
+  if (a.split_max > 1 && !a.part) return false;
   const int64_t worst = ((a.capO + kGemmBM - 1) / kGemmBM) *
                         ((a.cout_p + kGemmBN - 1) / kGemmBN);
   // persistent blocks: about what the 256 CUs hold at once
-  int64_t grid = worst < 1024 ? worst : 1024;
+  const int64_t units = worst * (a.split_max > 1 ? a.split_max : 1);
+  int64_t grid = units < 1024 ? units : 1024;
   grid = (grid + kXcd - 1) / kXcd * kXcd;
   const size_t lds = sizeof(int) * (size_t)a.K * kGemmBM;
   prof_begin(pf, 7 /*ST_K_CONV_GEMM*/, s);
@@ -1010,6 +1165,17 @@ bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
   else
     gemm_t<bf16_t>(s, (int)grid, lds, a);
   prof_end(pf, 7, s);
+  if (a.split_max > 1) {
+    const int egrid = (int)(worst < 1024 ? worst : 1024);
+    prof_begin(pf, 22 /*ST_K_CONV_SPLIT_EPI*/, s);
+    if (dtype == 0)
+      split_epi_t<float>(s, egrid, a);
+    else if (dtype == 1)
+      split_epi_t<_Float16>(s, egrid, a);
+    else
+      split_epi_t<bf16_t>(s, egrid, a);
+    prof_end(pf, 22, s);
+  }
   return true;
 }
 

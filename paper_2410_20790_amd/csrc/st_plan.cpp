@@ -194,6 +194,7 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
     max_grid = std::max(max_grid, T.grid);
   }
   int n_cleanup = L_n + 1;
+  size_t part_bytes = 0;
   for (int i = 0; i < L_n; ++i) {
     LayerPlan& L = net->layers[i];
     TensorPlan& T = net->tensors[i + 1];
@@ -217,6 +218,15 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
     else
       L.off_w = a.take((size_t)L.cout_p * L.ktot_p * net->esize);
     L.off_bias = a.take(sizeof(float) * L.cout_p);
+    if (!L.dw) {
+      const int64_t stages = L.ktot_p / kc;
+      if (stages >= kSplitMinLayerStages)
+        L.split_max = (int)std::min<int64_t>(kSplitMax, stages / 8);
+      part_bytes = std::max<size_t>(
+          part_bytes, L.split_max > 1 ? sizeof(float) * L.split_max *
+                                            L.conv_grid * L.cout_p
+                                      : 0);
+    }
     if (!L.ident) L.off_flags = a.take(round_up(L.conv_grid, 16));
     if (L.pool) L.off_pflags = a.take(round_up(T.grid, 16));
     if (L.se) {
@@ -242,6 +252,7 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
   net->off_grp = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
   net->off_mdone = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
   net->off_zero = a.take(256);
+  net->off_part = a.take(std::max<size_t>(part_bytes, 256));
   net->n_cleanup = n_cleanup;
   net->off_cleanup = a.take(32 * n_cleanup);
   net->ws_bytes = round_up(a.top, kAlign);

@@ -5,7 +5,8 @@ emitted deltas within one storage ulp (plus the state's rounding), masks and
 rulebooks exact.  Geometries cover every path of the kernels: ragged row and
 channel tiles, several reduction stages, small input channels packed across
 kernel offsets, strides, 5x5 and 7x7 windows, 1x1 identity rulebooks,
-depthwise, max-pool (disjoint and overlapping) and linear layers."""
+depthwise, max-pool (disjoint and overlapping), linear layers, and deep
+reductions split across work units."""
 
 import numpy as np
 import pytest
@@ -39,6 +40,12 @@ GEOMS = {
                    ((3, 3), (2, 2), (1, 1))),
     "pool2x1": (16, 32, (3, 3), (1, 1), (1, 1), 1, ACT_RELU,
                 ((2, 1), (2, 1), (0, 0))),
+    # deep reductions on few output tiles: the reduction is split across
+    # work units and finished by the split epilogue (state, pooled-defer)
+    "3x3_deep": (512, 512, (3, 3), (1, 1), (1, 1), 1, ACT_RELU, None),
+    "1x1_deep": (1024, 256, (1, 1), (1, 1), (0, 0), 1, ACT_RELU, None),
+    "pool_deep": (256, 64, (3, 3), (1, 1), (1, 1), 1, ACT_RELU,
+                  ((2, 2), (2, 2), (0, 0))),
 }
 
 
