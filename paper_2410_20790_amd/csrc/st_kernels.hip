@@ -647,10 +647,9 @@ __device__ __forceinline__ int split_count(int64_t ntiles, int nst, int smax) {
 // with device-scope atomics; the last block to finish a row tile (over its
 // column tiles) counts the tile's kept rows for the truncation pass.  Every
 // thread of the block must call it (it synchronises).
-template <typename T, bool REF, class LoadV>
+template <typename T, bool REF, class LoadV, class LoadPo, class LoadSk>
 __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
-                                            const float (&po)[2][8],
-                                            const float (&sk)[2][8],
+                                            LoadPo load_po, LoadSk load_sk,
                                             const bool (&hv)[2], int64_t eo,
                                             bool eok, int epix, int64_t m0,
                                             int n0, int ec, int tiles_n,
@@ -664,23 +663,25 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
   for (int h = 0; h < 2; ++h) {
     if (!hv[h]) continue;
     const int n = n0 + ec + 8 * h;
-    float v[8];
+    float v[8], sk[8];
     load_v(h, v);
+    load_sk(h, sk);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       if (REF) v[e] += a.bias[n + e];
-      v[e] += sk[h][e];
+      v[e] += sk[e];
     }
     if (a.mode == 1) {
       store8f(a.dP + eo * cout_p + n, v);
       continue;
     }
     if (a.mode == 0) {
-      float pn[8];
+      float po[8], pn[8];
+      load_po(h, po);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        pn[e] = po[h][e] + v[e];
-        v[e] = act_f(pn[e], a.act) - act_f(po[h][e], a.act);
+        pn[e] = po[e] + v[e];
+        v[e] = act_f(pn[e], a.act) - act_f(po[e], a.act);
       }
       store8f(a.P + (int64_t)epix * cout_p + n, pn);
     }
@@ -814,24 +815,8 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     }
     if (my) atomicOr(&s_kmask, my);
     bool hv[2];
-    float po[2][8], sk[2][8];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int n = n0 + ec + 8 * h;
-      hv[h] = eok && n < cout_p;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) po[h][e] = sk[h][e] = 0.f;
-      if (!SPLIT && hv[h] && a.mode == 0 && !REF)
-        load8f(a.P + (int64_t)epix * cout_p + n, po[h]);
-    }
-    const int rsk = (!SPLIT && a.mskip && eok) ? a.mskip[epix] : -1;
-    if (rsk >= 0) {
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-        if (hv[h])
-          Vec8<T>::load(dskip + (int64_t)rsk * cout_p + n0 + ec + 8 * h,
-                        sk[h]);
-    }
+    for (int h = 0; h < 2; ++h) hv[h] = eok && n0 + ec + 8 * h < cout_p;
     __syncthreads();
     const u64 kmask = s_kmask;
 
@@ -1050,9 +1035,27 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
                 v);
       }
     } else {
+      const int rsk = (a.mskip && eok) ? a.mskip[epix] : -1;
       finish_tile<T, REF>(
-          a, [&](int h, float* v) { load8f(crow + 8 * h, v); }, po, sk, hv,
-          eo, eok, epix, m0, n0, ec, tiles_n, nO, &s_last);
+          a, [&](int h, float* v) { load8f(crow + 8 * h, v); },
+          [&](int h, float* po) {
+            if (REF) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) po[e] = 0.f;
+            } else {
+              load8f(a.P + (int64_t)epix * cout_p + n0 + ec + 8 * h, po);
+            }
+          },
+          [&](int h, float* sk) {
+            if (rsk >= 0) {
+              Vec8<T>::load(dskip + (int64_t)rsk * cout_p + n0 + ec + 8 * h,
+                            sk);
+            } else {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) sk[e] = 0.f;
+            }
+          },
+          hv, eo, eok, epix, m0, n0, ec, tiles_n, nO, &s_last);
     }
   }
 }
@@ -1109,7 +1112,15 @@ __global__ __launch_bounds__(256) void k_split_epi(ConvArgs a) {
             for (int e = 0; e < 8; ++e) v[e] += q[e];
           }
         },
-        po, sk, hv, eo, eok, epix, m0, n0, ec, tiles_n, nO, &s_last);
+        [&](int h, float* o) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = po[h][e];
+        },
+        [&](int h, float* o) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = sk[h][e];
+        },
+        hv, eo, eok, epix, m0, n0, ec, tiles_n, nO, &s_last);
   }
 }
 
