@@ -516,3 +516,20 @@ def test_planted_mistake_flipped_offset_is_caught(monkeypatch):
     R = so.rulebook(active, (6, 7), (6, 7), (3, 3), (1, 1), (1, 1))
     assert [tuple(map(int, r)) for r in R] != brute_rulebook(
         active, 1, 6, 7, 6, 7, (3, 3), (1, 1), (1, 1))
+
+
+def test_planted_mistake_frozen_se_gates_is_caught(monkeypatch):
+    """Keeping the reference frame's squeeze-excitation gates in diff
+    frames (instead of recomputing them from the dense activation) breaks
+    Eq. 2 for a net with squeeze-excitation; the threshold-0 pin must catch
+    it."""
+    net = efficientnet_mini_net()
+    frames = random_sparse_video(3, 2, 1, 32, 40, 3, 0.08)
+    dense, _, _ = oracle.dense_forward(net.layers, frames[1], "f32")
+    o = make_oracle(net)
+    o.encode_reference(frames[0])
+    frozen = {i: s.copy() for i, s in o.S.items()}
+    monkeypatch.setattr(so, "se_gates",
+                        lambda a, L: frozen[net.layers.index(L)])
+    out = o.encode_diff(frames[1], [0.0] * (len(net.layers) + 1))
+    assert rel_err(out, dense) > 1e-4
