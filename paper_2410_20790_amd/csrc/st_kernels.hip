@@ -140,18 +140,37 @@ __device__ __forceinline__ unsigned block_exclusive_scan(unsigned v,
 
 // cnts: `per_tile` counts per tile (1 = per-tile counts, tile/64 = counts of
 // 64-item groups).  Each thread owns `tile / 256` consecutive items of the
-// tile, evaluates all of them before emitting, and emits in item order, so
-// the whole tile costs one round of dependent loads.  pred.emit returns a
-// work count that is summed over the block and handed to pred.block_done;
-// pred.finish receives the total.
+// tile, evaluates all of them before emitting, and emits in item order.
+// The predicate's item data (P::Item, from P::load) is requested together
+// with the item count and the counts before the tile -- all loads stay
+// within the capacity `cap`, and which items are real is decided once the
+// count has arrived -- so a block waits for one round of loads, not three.
+// With IPT > 0 (items per thread known at compile time) the items are kept
+// in registers from load to emit.  pred.emit returns a work count that is
+// summed over the block and handed to pred.block_done; pred.finish
+// receives the total.
 constexpr int kMaxItemsPerThread = 32;
 
-template <class P>
+template <class P, int IPT>
 __global__ __launch_bounds__(256) void k_compact_write(
-    const u64* n_dev, int64_t n_host, int tile, const uint32_t* cnts,
-    int per_tile, u64* out_cnt, u64* out_cnt2, P pred) {
-  const int64_t n = read_count(n_dev, n_host);
+    const u64* n_dev, int64_t n_host, int64_t cap, int tile,
+    const uint32_t* cnts, int per_tile, u64* out_cnt, u64* out_cnt2,
+    P pred) {
+  using Item = typename P::Item;
   const int64_t base = (int64_t)blockIdx.x * tile;
+  const int64_t n_req = read_count(n_dev, n_host);
+  unsigned off = 0;
+  const unsigned nprev = blockIdx.x * (unsigned)per_tile;
+  for (unsigned j = threadIdx.x; j < nprev; j += 256) off += cnts[j];
+  const int ipt = IPT > 0 ? IPT : tile / 256;
+  const int64_t first = base + (int64_t)threadIdx.x * ipt;
+  Item it[IPT > 0 ? IPT : 1];
+  if constexpr (IPT > 0) {
+#pragma unroll
+    for (int j = 0; j < IPT; ++j)
+      if (first + j < cap) it[j] = pred.load(first + j);
+  }
+  const int64_t n = n_req;
   if (base >= n) {
     if (blockIdx.x == 0 && threadIdx.x == 0) {
       *out_cnt = 0;
@@ -160,17 +179,19 @@ __global__ __launch_bounds__(256) void k_compact_write(
     }
     return;
   }
-  unsigned off = 0;
-  const unsigned nprev = blockIdx.x * (unsigned)per_tile;
-  for (unsigned j = threadIdx.x; j < nprev; j += 256) off += cnts[j];
-  const int ipt = tile / 256;
-  const int64_t first = base + (int64_t)threadIdx.x * ipt;
   const int64_t end = min(base + (int64_t)tile, n);
   uint32_t keepbits = 0;
   unsigned mine = 0;
   for (int j = 0; j < ipt; ++j) {
     const int64_t i = first + j;
-    if (i < end && pred.keep(i)) {
+    bool k = false;
+    if (i < end) {
+      if constexpr (IPT > 0)
+        k = pred.keep(it[j < IPT ? j : 0]);
+      else
+        k = pred.keep(pred.load(i));
+    }
+    if (k) {
       keepbits |= 1u << j;
       ++mine;
     }
@@ -182,10 +203,15 @@ __global__ __launch_bounds__(256) void k_compact_write(
   for (int j = 0; j < ipt; ++j) {
     const int64_t i = first + j;
     if (i >= end) break;
-    if (keepbits & (1u << j))
-      work += pred.emit(i, pos++);
+    Item x;
+    if constexpr (IPT > 0)
+      x = it[j < IPT ? j : 0];
     else
-      pred.drop(i);
+      x = pred.load(i);
+    if (keepbits & (1u << j))
+      work += pred.emit(i, pos++, x);
+    else
+      pred.drop(i, x);
   }
   work = block_sum(work);
   if (threadIdx.x == 0) {
@@ -197,6 +223,21 @@ __global__ __launch_bounds__(256) void k_compact_write(
       pred.finish(total);
     }
   }
+}
+
+template <class P>
+static void launch_compact_write(hipStream_t s, int nt, const u64* n_dev,
+                                 int64_t n_host, int64_t cap, int tile,
+                                 const uint32_t* cnts, int per_tile,
+                                 u64* out_cnt, u64* out_cnt2, const P& pred) {
+  if (tile == 512)
+    k_compact_write<P, 2><<<nt, 256, 0, s>>>(n_dev, n_host, cap, tile, cnts,
+                                             per_tile, out_cnt, out_cnt2,
+                                             pred);
+  else
+    k_compact_write<P, 0><<<nt, 256, 0, s>>>(n_dev, n_host, cap, tile, cnts,
+                                             per_tile, out_cnt, out_cnt2,
+                                             pred);
 }
 
 // Tile of a compaction pass: a multiple of 256 items, at least 512, with at
@@ -226,8 +267,8 @@ static void run_compact(const Prof& pf, int cls_count, int cls_write,
   k_compact_count<P><<<nt, 256, 0, s>>>(n_dev, n_host, tile, tiles, pred);
   prof_end(pf, cls_count, s);
   prof_begin(pf, cls_write, s);
-  k_compact_write<P><<<nt, 256, 0, s>>>(n_dev, n_host, tile, tiles, 1,
-                                        out_cnt, out_cnt2, pred);
+  launch_compact_write(s, nt, n_dev, n_host, cap, tile, tiles, 1, out_cnt,
+                       out_cnt2, pred);
   prof_end(pf, cls_write, s);
 }
 
@@ -311,9 +352,13 @@ struct ScanPred {
     keepb[i] = k ? 1 : 0;
     return k;
   }
-  __device__ bool keep(int64_t i) const { return keepb[i] != 0; }
+  struct Item {
+    uint8_t k;
+  };
+  __device__ Item load(int64_t i) const { return Item{keepb[i]}; }
+  __device__ bool keep(const Item& it) const { return it.k != 0; }
   // pass 2: gather the delta row, commit the pixel to X_hat
-  __device__ unsigned emit(int64_t i, unsigned pos) const {
+  __device__ unsigned emit(int64_t i, unsigned pos, const Item&) const {
     rowpix[pos] = (int)i;
     act[pos] = (int)i;
     map[i] = (int)pos;
@@ -332,7 +377,7 @@ struct ScanPred {
     cons_emit(cons, (int)i, pos, (int)pos);
     return 0u;
   }
-  __device__ void drop(int64_t) const {}
+  __device__ void drop(int64_t, const Item&) const {}
   __device__ void block_done(unsigned) const {}
   __device__ void finish(unsigned total) const { cons_finish(cons, total); }
 };
@@ -394,9 +439,13 @@ struct FlagPred {
   int64_t stride;
   Geo g;  // conv geometry: input grid -> this (output) grid
   u64* pairs;
+  struct Item {
+    uint8_t f;
+  };
   __device__ bool count(int64_t i) const { return flags[i] != 0; }
-  __device__ bool keep(int64_t i) const { return flags[i] != 0; }
-  __device__ unsigned emit(int64_t i, unsigned pos) const {
+  __device__ Item load(int64_t i) const { return Item{flags[i]}; }
+  __device__ bool keep(const Item& it) const { return it.f != 0; }
+  __device__ unsigned emit(int64_t i, unsigned pos, const Item&) const {
     list[pos] = (int)i;
     map[i] = (int)pos;
     flags[i] = 0;
@@ -406,22 +455,32 @@ struct FlagPred {
     const int n = (int)(i / hwo);
     const int rem = (int)(i - n * hwo);
     const int oy = rem / g.Wo, ox = rem - (rem / g.Wo) * g.Wo;
+    const int K = g.kh * g.kw;
     unsigned valid = 0;
-    for (int ky = 0; ky < g.kh; ++ky) {
-      const int iy = oy * g.sh - g.ph + ky;
-      const bool rok = iy >= 0 && iy < g.Hi;
-      for (int kx = 0; kx < g.kw; ++kx) {
-        const int ix = ox * g.sw - g.pw + kx;
-        int v = -1;
-        if (rok && ix >= 0 && ix < g.Wi)
-          v = map_in[((int64_t)n * g.Hi + iy) * g.Wi + ix];
-        nbr[(int64_t)(ky * g.kw + kx) * stride + pos] = v;
-        valid += v >= 0 ? 1u : 0u;
+    // up to 16 window entries at a time: all their loads are issued before
+    // any neighbour-table store (the two may alias for the compiler)
+    for (int k0 = 0; k0 < K; k0 += 16) {
+      int v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int k = k0 + u;
+        const int ky = k / g.kw, kx = k - (k / g.kw) * g.kw;
+        const int iy = oy * g.sh - g.ph + ky, ix = ox * g.sw - g.pw + kx;
+        v[u] = -1;
+        if (k < K && iy >= 0 && iy < g.Hi && ix >= 0 && ix < g.Wi)
+          v[u] = map_in[((int64_t)n * g.Hi + iy) * g.Wi + ix];
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        if (k0 + u < K) {
+          nbr[(int64_t)(k0 + u) * stride + pos] = v[u];
+          valid += v[u] >= 0 ? 1u : 0u;
+        }
       }
     }
     return valid;
   }
-  __device__ void drop(int64_t) const {}
+  __device__ void drop(int64_t, const Item&) const {}
   __device__ void block_done(unsigned w) const {
     if (pairs && w) atomicAdd(pairs, (u64)w);
   }
@@ -1343,19 +1402,23 @@ struct ListPred {
   int* map;
   float thr;
   ConsList cons;
+  struct Item {
+    uint32_t rm;
+    int pix;
+  };
   __device__ bool count(int64_t r) const {
     return __uint_as_float(rowmax[r]) > thr;
   }
-  __device__ bool keep(int64_t r) const {
-    return __uint_as_float(rowmax[r]) > thr;
+  __device__ Item load(int64_t r) const { return Item{rowmax[r], rowpix[r]}; }
+  __device__ bool keep(const Item& it) const {
+    return __uint_as_float(it.rm) > thr;
   }
-  __device__ unsigned emit(int64_t r, unsigned pos) const {
-    const int p = rowpix[r];
-    act[pos] = p;
-    cons_emit(cons, p, pos, (int)r);
+  __device__ unsigned emit(int64_t r, unsigned pos, const Item& it) const {
+    act[pos] = it.pix;
+    cons_emit(cons, it.pix, pos, (int)r);
     return 0u;
   }
-  __device__ void drop(int64_t r) const { map[rowpix[r]] = -1; }
+  __device__ void drop(int64_t, const Item& it) const { map[it.pix] = -1; }
   __device__ void block_done(unsigned) const {}
   __device__ void finish(unsigned total) const { cons_finish(cons, total); }
 };
@@ -1365,9 +1428,8 @@ void launch_list_compact(const Prof& pf, hipStream_t s, const ListArgs& a) {
   const int tile = compact_tile(a.cap);
   const int nt = compact_tiles(a.cap);
   prof_begin(pf, 15 /*ST_K_LIST_COMPACT*/, s);
-  k_compact_write<ListPred><<<nt, 256, 0, s>>>(a.n_rows, 0, tile, a.grp,
-                                               tile / 64, a.cnt_act, nullptr,
-                                               p);
+  launch_compact_write(s, nt, a.n_rows, 0, a.cap, tile, a.grp, tile / 64,
+                       a.cnt_act, nullptr, p);
   prof_end(pf, 15, s);
 }
 

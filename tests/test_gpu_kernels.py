@@ -208,3 +208,24 @@ def test_squeeze_excitation(dtype, last_se):
                 (2.0 ** -7 if dtype != "f32" else 0) * sc
     finally:
         g.close()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("kind", ["conv", "dw"])
+def test_large_grid(kind, dtype):
+    """A large grid (one layer at 416x416, 173056 sites): hundreds of
+    compaction tiles, per-64-row kept counts from the GEMM's last block per
+    row tile or from the group-count kernel after a depthwise layer."""
+    rng = np.random.default_rng(11)
+    H = W = 416
+    C = 8 if kind == "conv" else 16
+    L = LayerSpec(src=-1, c_in=C, c_out=16, k=(3, 3), s=(1, 1), p=(1, 1),
+                  groups=1 if kind == "conv" else 16, act=ACT_RELU, name=kind)
+    L.weight = to_storage(rng.normal(0, 0.3, (L.c_out, L.c_in // L.groups,
+                                              *L.k)), dtype)
+    L.bias = to_storage(rng.normal(0, 0.1, L.c_out), dtype)
+    net = NetSpec("large", [L], 1, H, W, C, dtype)
+    say(f"[gpu] large tensor {kind} {dtype}")
+    frames = random_sparse_video(31, 3, 1, H, W, C, 0.05, dtype=dtype)
+    for thr in (0.0, 0.05):
+        check(net, frames, thr)
