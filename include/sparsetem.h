@@ -108,6 +108,19 @@ st_status st_create_net(const st_layer_desc* layers, int32_t n_layers,
                         int32_t batch, int32_t in_h, int32_t in_w,
                         int32_t in_c, int32_t dtype, st_net** out);
 
+/* As st_create_net, with room to encode up to `max_frames` (1..32) diff
+ * frames in one st_encode_chunk call (the layer-major schedule of section
+ * "Design of SparseBatch"): delta rows, active lists, pixel maps and
+ * rulebooks are sized for max_frames frames, the pre-activation state and
+ * the Subtraction buffer are not.  A net created here also accepts every
+ * other call.  Errors as st_create_net, plus ST_ERR_INVALID_ARG for
+ * max_frames outside [1, 32]. */
+st_status st_create_net_chunked(const st_layer_desc* layers,
+                                int32_t n_layers, int32_t batch,
+                                int32_t max_frames, int32_t in_h,
+                                int32_t in_w, int32_t in_c, int32_t dtype,
+                                st_net** out);
+
 /* Bytes of device workspace the net needs (host only).  The workspace holds
  * the Subtraction buffer, every f32 pre-activation buffer, the repacked
  * weights, and worst-case-sized (every pixel active) delta rows, active
@@ -143,6 +156,25 @@ st_status st_encode_reference(st_net* net, const void* frame, float* out,
  * bind), ST_ERR_INVALID_ARG (NULL frame/thr, NaN threshold), ST_ERR_HIP. */
 st_status st_encode_diff(st_net* net, const void* frame, const float* thr,
                          float* out, void* stream);
+
+/* The next n_frames diff frames at once, layer by layer (section "Design of
+ * SparseBatch": one rulebook, GEMM and truncation launch per layer for all
+ * frames, the frames taken in order per site wherever one frame's result
+ * depends on the previous one's -- the Subtraction buffer, the
+ * pre-activation state, max-pool windows).  Result and final state equal
+ * n_frames successive st_encode_diff calls with the same `thr` (host,
+ * n_layers + 1 floats, shared by the frames).  `frames`: device, storage
+ * dtype, [n_frames][batch][in_h][in_w][in_c] contiguous; `out`: device f32
+ * [n_frames][last layer's NHWC grid], or NULL.  Afterwards the introspection
+ * calls see the frames as n_frames * batch images (frame t's images after
+ * frame t-1's), and st_layer_density takes image = t * batch + n.
+ * Errors: ST_ERR_STATE (no workspace or no reference), ST_ERR_INVALID_ARG
+ * (NULL, NaN threshold, n_frames outside [1, max_frames]),
+ * ST_ERR_UNSUPPORTED (a net created without chunk capacity, more than 16
+ * input channels, squeeze-excitation layers, a pooled last layer),
+ * ST_ERR_HIP. */
+st_status st_encode_chunk(st_net* net, const void* frames, int32_t n_frames,
+                          const float* thr, float* out, void* stream);
 
 /* Fraction of kept sites of the last encode: layer = -1 is the frame delta,
  * layer = j is layer j's emitted delta.  image = -1 averages over the batch,
@@ -208,7 +240,7 @@ enum {
   ST_K_POOL_MARK, ST_K_POOL_COUNT, ST_K_POOL_COMPACT, ST_K_POOL_EMIT,
   ST_K_COMMIT, ST_K_LIST_COUNT, ST_K_LIST_COMPACT, ST_K_OUTPUT,
   ST_K_CLEANUP, ST_K_RESET, ST_K_SE_SQUEEZE, ST_K_SE_EXCITE, ST_K_SE_EMIT,
-  ST_K_CONV_SPLIT_EPI, ST_K_NUM_CLASSES
+  ST_K_CONV_SPLIT_EPI, ST_K_CHUNK_UPDATE, ST_K_NUM_CLASSES
 };
 
 /* Start recording: room for `max_launches` launch records and

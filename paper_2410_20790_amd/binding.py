@@ -26,12 +26,13 @@ KERNEL_CLASSES = [
     "rb_nbr", "rb_ident", "conv_gemm", "conv_dw", "pool_mark", "pool_count",
     "pool_compact", "pool_emit", "commit", "list_count", "list_compact",
     "output", "cleanup", "reset", "se_squeeze", "se_excite", "se_emit",
-    "conv_split_epi",
+    "conv_split_epi", "chunk_update",
 ]
 
 EXPORTED = [
-    "st_create_net", "st_workspace_bytes", "st_bind_workspace",
-    "st_encode_reference", "st_encode_diff", "st_layer_density",
+    "st_create_net", "st_create_net_chunked", "st_workspace_bytes",
+    "st_bind_workspace", "st_encode_reference", "st_encode_diff",
+    "st_encode_chunk", "st_layer_density",
     "st_tensor_shape", "st_destroy_net", "st_last_error", "st_debug_active",
     "st_debug_candidates", "st_debug_rulebook", "st_debug_state",
     "st_debug_counters", "st_profile_begin", "st_profile_end",
@@ -75,6 +76,10 @@ def _load():
     sig = {
         "st_create_net": [ctypes.POINTER(st_layer_desc), I32, I32, I32, I32,
                           I32, I32, ctypes.POINTER(P)],
+        "st_create_net_chunked": [ctypes.POINTER(st_layer_desc), I32, I32,
+                                  I32, I32, I32, I32, I32,
+                                  ctypes.POINTER(P)],
+        "st_encode_chunk": [P, P, I32, ctypes.POINTER(ctypes.c_float), P, P],
         "st_workspace_bytes": [P, ctypes.POINTER(U64)],
         "st_bind_workspace": [P, P, U64, P],
         "st_encode_reference": [P, P, P, P],
@@ -129,6 +134,16 @@ def st_create_net(layers: Sequence[st_layer_desc], batch, in_h, in_w, in_c,
     return out.value
 
 
+def st_create_net_chunked(layers: Sequence[st_layer_desc], batch,
+                          max_frames, in_h, in_w, in_c, dtype) -> int:
+    arr = (st_layer_desc * len(layers))(*layers)
+    out = ctypes.c_void_p()
+    _check(_lib.st_create_net_chunked(arr, len(layers), batch, max_frames,
+                                      in_h, in_w, in_c, dtype,
+                                      ctypes.byref(out)))
+    return out.value
+
+
 def st_workspace_bytes(net) -> int:
     b = ctypes.c_uint64()
     _check(_lib.st_workspace_bytes(net, ctypes.byref(b)), net)
@@ -149,6 +164,12 @@ def st_encode_diff(net, frame_ptr, thr, out_ptr=None, stream=0):
     t = (ctypes.c_float * len(thr))(*[float(v) for v in thr])
     _check(_lib.st_encode_diff(net, _ptr(frame_ptr), t, _ptr(out_ptr),
                                _ptr(stream)), net)
+
+
+def st_encode_chunk(net, frames_ptr, n_frames, thr, out_ptr=None, stream=0):
+    t = (ctypes.c_float * len(thr))(*[float(v) for v in thr])
+    _check(_lib.st_encode_chunk(net, _ptr(frames_ptr), n_frames, t,
+                                _ptr(out_ptr), _ptr(stream)), net)
 
 
 def st_layer_density(net, layer, image=-1) -> float:

@@ -145,7 +145,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
     fa.rowmax = rm_O;
     fa.nbr = nbr;
     fa.map_in = ws.at<int>(in.off_map);
-    fa.stride = L.conv_grid;
+    fa.stride = L.conv_grid * net->F;  // the table holds F frames' rows
     fa.g = conv_geo(L);
     fa.pairs = cpairs;
     fa.cnt = cO;
@@ -156,7 +156,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   ConvArgs a{};
   a.din = ws.at<char>(in.off_rows);
   a.nbr = nbr;
-  a.stride = L.conv_grid;
+  a.stride = L.conv_grid * net->F;
   a.K = L.K;
   a.cin_p = L.cin_p;
   a.cout_p = L.cout_p;
@@ -283,6 +283,7 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
                  hipStream_t s, bool ref) {
   const WS ws{net->ws};
   u64* cnt = ws.at<u64>(net->off_cnt);
+  net->last_nf = 1;
   const Prof pf{net, -1};
   Recorder* R = net->rec && net->rec->on ? net->rec : nullptr;
   if (R) ++R->frame;
@@ -341,6 +342,211 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
   return hip_check(net, ref ? "st_encode_reference" : "st_encode_diff");
 }
 
+// ---- chunk mode: the frames of a chunk as items (frame t's sites after
+// frame t-1's) for the rulebooks, GEMMs and truncations; per-site frame
+// loops for the frame delta, the state update and the pools.
+bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
+                     hipStream_t s) {
+  const WS ws{net->ws};
+  const LayerPlan& L = net->layers[i];
+  const st_layer_desc& d = L.d;
+  const TensorPlan& in = net->tensors[d.src + 1];
+  TensorPlan& outT = net->tensors[i + 1];
+  u64* cnt = ws.at<u64>(net->off_cnt);
+  uint32_t* tiles = ws.at<uint32_t>(net->off_tiles);
+  uint32_t* grp = ws.at<uint32_t>(net->off_grp);
+  const Prof pf{net, i};
+  const int64_t citems = L.conv_grid * nf;
+  const int64_t stride = L.conv_grid * net->F;
+  float* cdp = ws.at<float>(net->off_chunk_dp);
+
+  int* O = ws.at<int>(L.off_O);
+  int* Mo = ws.at<int>(L.off_Mo);
+  int* nbr = ws.at<int>(L.off_nbr);
+  u64* cO = cnt + L.cnt_O;
+  u64* cpairs = cnt + L.cnt_pairs;
+  uint32_t* rowmax_out = ws.at<uint32_t>(outT.off_rowmax);
+  uint32_t* rm_O = L.pool ? nullptr : rowmax_out;
+
+  if (!L.ident) {
+    FlagArgs fa{};
+    fa.flags = ws.at<uint8_t>(L.off_flags);
+    fa.npix = citems;
+    fa.tiles = tiles;
+    fa.list = O;
+    fa.map = Mo;
+    fa.rowmax = rm_O;
+    fa.nbr = nbr;
+    fa.map_in = ws.at<int>(in.off_map);
+    fa.stride = stride;
+    fa.g = conv_geo(L);
+    fa.pairs = cpairs;
+    fa.cnt = cO;
+    launch_flag_compact(pf, ST_K_RB_COUNT, ST_K_RB_COMPACT, s, fa);
+  }
+
+  ConvArgs a{};
+  a.din = ws.at<char>(in.off_rows);
+  a.nbr = nbr;
+  a.stride = stride;
+  a.K = L.K;
+  a.cin_p = L.cin_p;
+  a.cout_p = L.cout_p;
+  a.ktot_p = L.ktot_p;
+  a.w = ws.at<char>(L.off_w);
+  a.bias = ws.at<float>(L.off_bias);
+  a.O = O;
+  a.nO = cO;
+  a.capO = citems;
+  if (L.stateful) {
+    // every frame's update is deferred; the frame loop applies them
+    a.mode = kModeDefer;
+    a.dP = cdp;
+  } else {
+    a.mode = kModeLinear;
+    a.dout = ws.at<char>(outT.off_rows);
+    a.rowmax = rowmax_out;
+    a.grp = grp;
+  }
+  if (d.residual_src != -2) {
+    const TensorPlan& R = net->tensors[d.residual_src + 1];
+    a.dskip = ws.at<char>(R.off_rows);
+    a.mskip = ws.at<int>(R.off_map);
+  }
+  a.act = d.act;
+  a.ref = 0;
+  a.mdone = ws.at<uint32_t>(net->off_mdone);
+  a.keep_thr = thr;
+  a.zero = ws.at<char>(net->off_zero);
+  a.part = ws.at<float>(net->off_part);
+  a.split_max = L.split_max;
+  if (L.dw)
+    launch_conv_dw(pf, s, net->dtype, a);
+  else if (!launch_conv_gemm(pf, s, net->dtype, a))
+    return false;
+
+  if (L.stateful) {
+    ChunkUpdArgs u{};
+    u.P = ws.at<float>(L.off_P);
+    u.dP = cdp;
+    u.Mo = Mo;
+    u.dout = ws.at<char>(outT.off_rows);
+    u.rowmax = rowmax_out;
+    u.aff = ws.at<uint32_t>(net->off_chunk_aff);
+    u.out = out;
+    u.npix = L.conv_grid;
+    u.nf = nf;
+    u.cp = L.cout_p;
+    u.c = d.c_out;
+    u.act = d.act;
+    u.pool_mode = L.pool ? 1 : 0;
+    u.tps = se_threads_per_site(L.cout_p);
+    launch_chunk_update(pf, s, net->dtype, u);
+  }
+  if (L.pool) {
+    const Geo gp = pool_geo(L);
+    uint8_t* pflags = ws.at<uint8_t>(L.off_pflags);
+    launch_mark(pf, ST_K_POOL_MARK, s, O, cO, citems, gp, pflags);
+    FlagArgs fp{};
+    fp.flags = pflags;
+    fp.npix = outT.grid * nf;
+    fp.tiles = tiles;
+    fp.list = ws.at<int>(outT.off_rowpix);
+    fp.map = ws.at<int>(outT.off_map);
+    fp.rowmax = rowmax_out;
+    fp.cnt = cnt + outT.cnt_rows;
+    launch_flag_compact(pf, ST_K_POOL_COUNT, ST_K_POOL_COMPACT, s, fp);
+    ChunkPoolArgs pa{};
+    pa.Q = ws.at<int>(outT.off_rowpix);
+    pa.nQ = cnt + outT.cnt_rows;
+    pa.capQ = outT.grid * nf;
+    pa.g = gp;
+    pa.P = ws.at<float>(L.off_P);
+    pa.Pt = cdp;
+    pa.Mo = Mo;
+    pa.aff = ws.at<uint32_t>(net->off_chunk_aff);
+    pa.dout = ws.at<char>(outT.off_rows);
+    pa.rowmax = rowmax_out;
+    pa.nconv = L.conv_grid;
+    pa.npool = outT.grid;
+    pa.cp = L.cout_p;
+    pa.act = d.act;
+    pa.tps = se_threads_per_site(L.cout_p);
+    launch_chunk_pool_emit(pf, s, net->dtype, pa);
+    launch_chunk_commit(pf, s, ws.at<float>(L.off_P), cdp, Mo,
+                        ws.at<uint32_t>(net->off_chunk_aff), L.conv_grid,
+                        L.cout_p);
+  }
+  if (L.stateful)
+    launch_group_count(pf, s, rowmax_out, cnt + outT.cnt_rows,
+                       outT.grid * nf, thr, grp);
+
+  ListArgs la{};
+  la.rowmax = rowmax_out;
+  la.n_rows = cnt + outT.cnt_rows;
+  la.cap = outT.grid * nf;
+  la.thr = thr;
+  la.rowpix = ws.at<int>(outT.off_rowpix);
+  la.act = ws.at<int>(outT.off_act);
+  la.map = ws.at<int>(outT.off_map);
+  la.grp = grp;
+  la.cnt_act = cnt + outT.cnt_act;
+  la.cons = consumers_of(net, i + 1);
+  launch_list_compact(pf, s, la);
+  outT.last_thr = thr;
+  return true;
+}
+
+st_status encode_chunk(st_net* net, const void* frames, int nf,
+                       const float* thr, float* out, hipStream_t s) {
+  const WS ws{net->ws};
+  u64* cnt = ws.at<u64>(net->off_cnt);
+  const Prof pf{net, -1};
+  Recorder* R = net->rec && net->rec->on ? net->rec : nullptr;
+  if (R) ++R->frame;
+  (void)hipGetLastError();
+  net->last_nf = nf;
+
+  launch_reset(pf, s, cnt, net->n_counters);
+  TensorPlan& T0 = net->tensors[0];
+  ChunkScanArgs sa{};
+  sa.x = frames;
+  sa.xhat = ws.at<char>(net->off_xhat);
+  sa.C = net->C;
+  sa.Cp = T0.Cp;
+  sa.nf = nf;
+  sa.npix = T0.grid;
+  sa.thr = thr[0];
+  sa.keep = ws.at<uint8_t>(net->off_flags);
+  sa.base = ws.at<uint8_t>(net->off_chunk_base);
+  sa.last = ws.at<uint8_t>(net->off_chunk_last);
+  sa.tiles = ws.at<uint32_t>(net->off_tiles);
+  sa.rows = ws.at<char>(T0.off_rows);
+  sa.rowpix = ws.at<int>(T0.off_rowpix);
+  sa.act = ws.at<int>(T0.off_act);
+  sa.map = ws.at<int>(T0.off_map);
+  sa.cnt_rows = cnt + T0.cnt_rows;
+  sa.cnt_act = cnt + T0.cnt_act;
+  sa.cons = consumers_of(net, 0);
+  launch_chunk_scan(pf, s, net->dtype, sa);
+  T0.last_thr = thr[0];
+  const int nl = (int)net->layers.size();
+  for (int i = 0; i < nl; ++i)
+    if (!run_layer_chunk(net, i, nf, thr[i + 1], i == nl - 1 ? out : nullptr,
+                         s))
+      return fail(net, ST_ERR_HIP, "internal: GEMM launch arguments");
+  launch_cleanup(pf, s, ws.at<CleanEntry>(net->off_cleanup), net->n_cleanup,
+                 net->ws, cnt, net->max_grid);
+  if (R && R->n_hist < R->max_frames) {
+    (void)hipMemcpyAsync(R->hist + (size_t)R->n_hist * net->n_counters, cnt,
+                         sizeof(u64) * net->n_counters, hipMemcpyDeviceToHost,
+                         s);
+    ++R->n_hist;
+  }
+  net->last_stream = (void*)s;
+  return hip_check(net, "st_encode_chunk");
+}
+
 st_status sync_last(st_net* net) {
   hipError_t e = hipStreamSynchronize((hipStream_t)net->last_stream);
   if (e != hipSuccess)
@@ -389,8 +595,9 @@ extern "C" st_status st_bind_workspace(st_net* net, void* dev_ptr,
   (void)hipGetLastError();
   const WS ws{net->ws};
   launch_fill_u32(s, net->ws, (int64_t)(net->ws_bytes / 4), 0u);
+  // pixel maps start empty for every frame slot of a chunk
   for (const TensorPlan& T : net->tensors)
-    launch_fill_u32(s, ws.at<int>(T.off_map), T.grid, 0xFFFFFFFFu);
+    launch_fill_u32(s, ws.at<int>(T.off_map), T.grid * net->F, 0xFFFFFFFFu);
   std::vector<CleanEntry> tab;
   for (const TensorPlan& T : net->tensors)
     tab.push_back(CleanEntry{(int64_t)T.off_map, (int64_t)T.off_rowpix,
@@ -398,7 +605,8 @@ extern "C" st_status st_bind_workspace(st_net* net, void* dev_ptr,
   for (const LayerPlan& L : net->layers) {
     const st_layer_desc& d = L.d;
     if (L.pool || L.se) {
-      launch_fill_u32(s, ws.at<int>(L.off_Mo), L.conv_grid, 0xFFFFFFFFu);
+      launch_fill_u32(s, ws.at<int>(L.off_Mo), L.conv_grid * net->F,
+                      0xFFFFFFFFu);
       tab.push_back(CleanEntry{(int64_t)L.off_Mo, (int64_t)L.off_O, L.cnt_O,
                                0, 0});
     }
@@ -451,6 +659,37 @@ extern "C" st_status st_encode_reference(st_net* net, const void* frame,
   return s;
 }
 
+extern "C" st_status st_encode_chunk(st_net* net, const void* frames,
+                                     int32_t n_frames, const float* thr,
+                                     float* out, void* stream) {
+  if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
+  if (!net->bound) return fail(net, ST_ERR_STATE, "no workspace bound");
+  if (!net->have_ref)
+    return fail(net, ST_ERR_STATE, "no reference frame encoded yet");
+  if (!frames || !thr)
+    return fail(net, ST_ERR_INVALID_ARG, "frames or thr is NULL");
+  if (n_frames < 1 || n_frames > net->F)
+    return fail(net, ST_ERR_INVALID_ARG,
+                "n_frames must be in [1, max_frames of the net]");
+  const int nl = (int)net->layers.size();
+  for (int i = 0; i <= nl; ++i)
+    if (std::isnan(thr[i]))
+      return fail(net, ST_ERR_INVALID_ARG, "threshold is NaN");
+  if (net->F < 2)
+    return fail(net, ST_ERR_UNSUPPORTED,
+                "net created without chunk capacity (st_create_net_chunked)");
+  if (net->C > kChunkMaxInC)
+    return fail(net, ST_ERR_UNSUPPORTED,
+                "chunks need at most 16 input channels");
+  for (const LayerPlan& L : net->layers)
+    if (L.se)
+      return fail(net, ST_ERR_UNSUPPORTED,
+                  "squeeze-excitation layers are encoded frame by frame");
+  if (net->layers[nl - 1].pool)
+    return fail(net, ST_ERR_UNSUPPORTED, "a pooled last layer in a chunk");
+  return encode_chunk(net, frames, n_frames, thr, out, (hipStream_t)stream);
+}
+
 extern "C" st_status st_encode_diff(st_net* net, const void* frame,
                                     const float* thr, float* out,
                                     void* stream) {
@@ -473,7 +712,8 @@ extern "C" st_status st_layer_density(st_net* net, int32_t layer,
     return fail(net, ST_ERR_STATE, "nothing encoded yet");
   if (layer < -1 || layer >= (int)net->layers.size())
     return fail(net, ST_ERR_INVALID_ARG, "layer out of range");
-  if (image < -1 || image >= net->N)
+  const int images = net->N * net->last_nf;
+  if (image < -1 || image >= images)
     return fail(net, ST_ERR_INVALID_ARG, "image out of range");
   const TensorPlan& T = net->tensors[layer + 1];
   const WS ws{net->ws};
@@ -484,13 +724,13 @@ extern "C" st_status st_layer_density(st_net* net, int32_t layer,
   if (image < 0) {
     st = d2h(net, &k, cnt + T.cnt_act, 1);
     if (st != ST_OK) return st;
-    *d = (float)((double)k / (double)T.grid);
+    *d = (float)((double)k / ((double)T.grid * net->last_nf));
     return ST_OK;
   }
   hipStream_t s = (hipStream_t)net->last_stream;
   u64* dens = ws.at<u64>(net->off_dens);
   launch_density(s, ws.at<int>(T.off_act), cnt + T.cnt_act,
-                 (int64_t)T.H * T.W, net->N, dens);
+                 (int64_t)T.H * T.W, images, dens);
   st = hip_check(net, "density");
   if (st != ST_OK) return st;
   st = sync_last(net);
@@ -589,7 +829,7 @@ extern "C" st_status st_debug_rulebook(st_net* net, int32_t layer,
     return st;
   for (int k = 0; k < L.K; ++k)
     if ((st = d2h(net, nb.data() + (size_t)k * nO,
-                  ws.at<int>(L.off_nbr) + (size_t)k * L.conv_grid, nO)) !=
+                  ws.at<int>(L.off_nbr) + (size_t)k * L.conv_grid * net->F, nO)) !=
         ST_OK)
       return st;
   int64_t cntp = 0;

@@ -14,6 +14,8 @@
 namespace st {
 
 constexpr int kChanAlign = 8;       // delta rows / weights padded to 8 channels
+constexpr int kMaxChunkFrames = 32; // diff frames per chunk (frame bit masks)
+constexpr int kChunkMaxInC = 16;    // input channels of a chunk's frame scan
 constexpr int kMaxTiles = 4096;     // compaction tiles per pass
 constexpr int64_t kMaxGrid = (int64_t)kMaxTiles * 8192;  // sites per grid
 constexpr size_t kAlign = 256;      // workspace sub-buffer alignment
@@ -102,6 +104,8 @@ struct Recorder;  // executor-side profiling state
 struct st_net {
   int dtype = 0, esize = 4;
   int N = 0, H = 0, W = 0, C = 0;
+  int F = 1;                               // diff frames per chunk (capacity)
+  int last_nf = 1;                         // frames of the last encode
   std::vector<st::LayerPlan> layers;
   std::vector<st::TensorPlan> tensors;     // n_layers + 1
   size_t ws_bytes = 0;
@@ -112,6 +116,12 @@ struct st_net {
   size_t off_mdone = 0;                    // uint32 [max grid / 64 + 1]
   size_t off_zero = 0;                     // 256 zero bytes
   size_t off_part = 0;                     // f32 split partials (shared)
+  // chunk mode (F > 1): f32 deferred updates of the current layer (shared),
+  // per input item the frame whose value X_hat held (0xFF: the X_hat of
+  // the chunk's start), per input site the last kept frame, per conv site
+  // the frames that updated it (bit mask)
+  size_t off_chunk_dp = 0, off_chunk_base = 0, off_chunk_last = 0;
+  size_t off_chunk_aff = 0;
   size_t off_cnt = 0;                      // uint64 [n_counters]
   size_t off_cleanup = 0;                  // cleanup descriptor table
   size_t off_dens = 0;                     // uint64 [batch] per-image counts

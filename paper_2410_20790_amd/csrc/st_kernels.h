@@ -197,6 +197,64 @@ void launch_to_f32_pad(hipStream_t s, int dtype, const void* src, float* dst,
                        int rows, int cols, int rows_p, int cols_p,
                        bool transposed = false);
 
+// ---- chunk mode: the diff frames of a chunk encoded layer-major
+// Items: frame t's sites follow frame t-1's (item = t * sites + site).
+struct ChunkScanArgs {
+  const void* x;       // frames [nf][npix][C] (storage dtype)
+  void* xhat;          // [npix][C]
+  int C, Cp, nf;
+  int64_t npix;        // input sites per frame
+  float thr;
+  uint8_t* keep;       // [nf * npix] keep bytes
+  uint8_t* base;       // [nf * npix] frame X_hat held (0xFF: chunk start)
+  uint8_t* last;       // [npix] last kept frame (0xFF: none)
+  uint32_t* tiles;
+  void* rows;
+  int* rowpix;
+  int* act;
+  int* map;
+  u64* cnt_rows;
+  u64* cnt_act;
+  ConsList cons;
+};
+void launch_chunk_scan(const Prof& pf, hipStream_t s, int dtype,
+                       const ChunkScanArgs& a);
+
+struct ChunkUpdArgs {
+  float* P;            // state [npix][cp] (physical sites)
+  float* dP;           // deferred update rows [*][cp] (pool mode: P_t)
+  const int* Mo;       // conv item -> dP row or -1
+  void* dout;          // emitted rows [*][cp] (not in pool mode)
+  uint32_t* rowmax;    // [rows]
+  uint32_t* aff;       // [npix] frames that updated each site (pool mode)
+  float* out;          // dense output [nf][npix][c] or NULL
+  int64_t npix;        // conv sites per frame
+  int nf, cp, c, act, pool_mode, tps;
+};
+void launch_chunk_update(const Prof& pf, hipStream_t s, int dtype,
+                         const ChunkUpdArgs& a);
+
+struct ChunkPoolArgs {
+  const int* Q;        // pooled rows -> pooled item
+  const u64* nQ;
+  int64_t capQ;
+  Geo g;               // conv grid -> pooled grid (one frame)
+  const float* P;      // state at the chunk's start [conv sites][cp]
+  const float* Pt;     // P after frame t, per conv row
+  const int* Mo;       // conv item -> row or -1
+  const uint32_t* aff; // [conv sites] frames that updated each site
+  void* dout;          // pooled rows [*][cp]
+  uint32_t* rowmax;
+  int64_t nconv, npool;  // conv / pooled sites per frame
+  int cp, act, tps;
+};
+void launch_chunk_pool_emit(const Prof& pf, hipStream_t s, int dtype,
+                            const ChunkPoolArgs& a);
+// P[w] = P after the last frame that updated w (pooled layers)
+void launch_chunk_commit(const Prof& pf, hipStream_t s, float* P,
+                         const float* Pt, const int* Mo, const uint32_t* aff,
+                         int64_t nconv, int cp);
+
 // ---- dense network output (Accumulation)
 void launch_output(const Prof& pf, hipStream_t s, const float* P, int cp,
                    int C, int N, Geo pool, int has_pool, int act,

@@ -1730,6 +1730,363 @@ void launch_to_f32_pad(hipStream_t s, int dtype, const void* src, float* dst,
                                               cols, rows_p, cols_p, tr);
 }
 
+// ------------------------------------------------------------ chunk mode
+// The diff frames of a chunk encoded layer-major (the SparseBatch schedule):
+// rulebooks, gather-GEMMs and truncations treat the frames as extra images
+// ("items", frame t's sites after frame t-1's); the steps that couple
+// frames -- the frame delta against the evolving X_hat, the state update,
+// the max-pool over states -- loop over the frames per site in order, so
+// every frame sees exactly the state the previous one left.
+
+// Frame-delta decisions: per input site, in frame order, the keep bit and
+// the frame whose value X_hat holds at that point; X_hat itself is only
+// committed after the deltas are gathered.
+template <typename T>
+__global__ __launch_bounds__(256) void k_chunk_scan_prep(ChunkScanArgs a) {
+  const T* x = (const T*)a.x;
+  const T* xhat = (const T*)a.xhat;
+  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < a.npix;
+       p += (int64_t)gridDim.x * 256) {
+    float xh[16];
+    for (int c = 0; c < a.C; ++c) xh[c] = to_f(xhat[p * a.C + c]);
+    uint8_t cur = 0xFF;
+    for (int t = 0; t < a.nf; ++t) {
+      const int64_t i = (int64_t)t * a.npix + p;
+      const T* xt = x + i * a.C;
+      float m = 0.f;
+      for (int c = 0; c < a.C; ++c) m = fmaxf(m, fabsf(to_f(xt[c]) - xh[c]));
+      const bool k = m > a.thr;
+      a.keep[i] = k ? 1 : 0;
+      a.base[i] = cur;
+      if (k) {
+        for (int c = 0; c < a.C; ++c) xh[c] = to_f(xt[c]);
+        cur = (uint8_t)t;
+      }
+    }
+    a.last[p] = cur;
+  }
+}
+
+template <typename T>
+struct ChunkScanPred {
+  const T* x;
+  const T* xhat;
+  uint8_t* keepb;
+  const uint8_t* base;
+  T* rows;
+  int* rowpix;
+  int* act;
+  int* map;
+  int C, Cp;
+  int64_t npix;
+  ConsList cons;
+  struct Item {
+    uint8_t k;
+  };
+  __device__ bool count(int64_t i) const { return keepb[i] != 0; }
+  __device__ Item load(int64_t i) const { return Item{keepb[i]}; }
+  __device__ bool keep(const Item& it) const { return it.k != 0; }
+  // delta against the value X_hat held when frame t arrived
+  __device__ unsigned emit(int64_t i, unsigned pos, const Item&) const {
+    const int64_t p = i % npix;
+    const uint8_t b = base[i];
+    const T* xt = x + i * C;
+    const T* xb = b == 0xFF ? xhat + p * C : x + ((int64_t)b * npix + p) * C;
+    T* r = rows + (int64_t)pos * Cp;
+    for (int c = 0; c < Cp; ++c)
+      r[c] = c < C ? from_f<T>(to_f(xt[c]) - to_f(xb[c])) : zero_v<T>();
+    rowpix[pos] = (int)i;
+    act[pos] = (int)i;
+    map[i] = (int)pos;
+    keepb[i] = 0;
+    cons_emit(cons, (int)i, pos, (int)pos);
+    return 0u;
+  }
+  __device__ void drop(int64_t, const Item&) const {}
+  __device__ void block_done(unsigned) const {}
+  __device__ void finish(unsigned total) const { cons_finish(cons, total); }
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_chunk_xhat_commit(ChunkScanArgs a) {
+  const T* x = (const T*)a.x;
+  T* xhat = (T*)a.xhat;
+  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < a.npix;
+       p += (int64_t)gridDim.x * 256) {
+    const uint8_t b = a.last[p];
+    if (b == 0xFF) continue;
+    for (int c = 0; c < a.C; ++c)
+      xhat[p * a.C + c] = x[((int64_t)b * a.npix + p) * a.C + c];
+  }
+}
+
+template <typename T>
+static void chunk_scan_t(const Prof& pf, hipStream_t s,
+                         const ChunkScanArgs& a) {
+  prof_begin(pf, 0 /*ST_K_SCAN_MASK*/, s);
+  k_chunk_scan_prep<T><<<grid_for(a.npix, 4096), 256, 0, s>>>(a);
+  prof_end(pf, 0, s);
+  ChunkScanPred<T> p{(const T*)a.x, (const T*)a.xhat, a.keep, a.base,
+                     (T*)a.rows, a.rowpix, a.act, a.map, a.C, a.Cp, a.npix,
+                     a.cons};
+  const int64_t items = (int64_t)a.nf * a.npix;
+  run_compact(pf, 0 /*ST_K_SCAN_MASK*/, 1 /*ST_K_SCAN_COMPACT*/, s, nullptr,
+              items, items, a.tiles, a.cnt_rows, a.cnt_act, p);
+  prof_begin(pf, 1 /*ST_K_SCAN_COMPACT*/, s);
+  k_chunk_xhat_commit<T><<<grid_for(a.npix, 4096), 256, 0, s>>>(a);
+  prof_end(pf, 1, s);
+}
+
+void launch_chunk_scan(const Prof& pf, hipStream_t s, int dtype,
+                       const ChunkScanArgs& a) {
+  if (dtype == 0)
+    chunk_scan_t<float>(pf, s, a);
+  else if (dtype == 1)
+    chunk_scan_t<_Float16>(pf, s, a);
+  else
+    chunk_scan_t<bf16_t>(pf, s, a);
+}
+
+// State update of a stateful layer over the chunk's frames: per conv site
+// (a group of TPS threads, 8 channels each, as in the squeeze-excitation
+// kernels), the state stays in registers while the frames that updated the
+// site are applied in order; each frame's row gets
+// f(P_t) - f(P_{t-1}) and its max |delta|.  Pool mode: the rows get P_t
+// instead (the pool compares window states per frame) and the frames that
+// updated each site are recorded; the state is committed afterwards.
+// With `out` the dense output f(P) after every frame is written too.
+template <typename T, int TPS>
+__global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
+  constexpr int R = 256 / TPS, IT = TPS == 64 ? 4 : 1;
+  T* dout = (T*)a.dout;
+  const int lane = threadIdx.x % TPS;
+  const int64_t p = (int64_t)blockIdx.x * R + threadIdx.x / TPS;
+  if (p >= a.npix) return;
+  const int cp = a.cp, V = cp / 8;
+  float pv[IT][8];
+#pragma unroll
+  for (int k = 0; k < IT; ++k) {
+    const int v = lane + k * TPS;
+    if (v < V) load8f(a.P + p * cp + v * 8, pv[k]);
+  }
+  uint32_t bits = 0;
+  for (int t = 0; t < a.nf; ++t) {
+    const int r = a.Mo[(int64_t)t * a.npix + p];
+    if (r >= 0) {
+      bits |= 1u << t;
+      float rm = 0.f;
+#pragma unroll
+      for (int k = 0; k < IT; ++k) {
+        const int v = lane + k * TPS;
+        if (v < V) {
+          float dp[8], pn[8];
+          float* row = a.dP + (int64_t)r * cp + v * 8;
+          load8f(row, dp);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) pn[e] = pv[k][e] + dp[e];
+          if (a.pool_mode) {
+            store8f(row, pn);
+          } else {
+            float d[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              d[e] = act_f(pn[e], a.act) - act_f(pv[k][e], a.act);
+            rm = fmaxf(rm, Vec8<T>::store(dout + (int64_t)r * cp + v * 8, d));
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) pv[k][e] = pn[e];
+        }
+      }
+      if (!a.pool_mode) {
+#pragma unroll
+        for (int o = 1; o < TPS; o <<= 1)
+          rm = fmaxf(rm, __shfl_xor(rm, o, 64));
+        if (lane == 0) a.rowmax[r] = __float_as_uint(rm);
+      }
+    }
+    if (a.out) {
+      float* o = a.out + ((int64_t)t * a.npix + p) * a.c;
+#pragma unroll
+      for (int k = 0; k < IT; ++k) {
+        const int v = lane + k * TPS;
+        if (v < V) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (v * 8 + e < a.c) o[v * 8 + e] = act_f(pv[k][e], a.act);
+        }
+      }
+    }
+  }
+  if (a.pool_mode) {
+    if (lane == 0) a.aff[p] = bits;
+  } else if (bits) {
+#pragma unroll
+    for (int k = 0; k < IT; ++k) {
+      const int v = lane + k * TPS;
+      if (v < V) store8f(a.P + p * cp + v * 8, pv[k]);
+    }
+  }
+}
+
+// P of conv site w after frame t (the latest frame <= t that updated it,
+// else the chunk's starting state); t < 0: the starting state.
+__device__ __forceinline__ const float* state_at(const ChunkPoolArgs& a,
+                                                 int64_t w, int t) {
+  if (t >= 0) {
+    const uint32_t b = a.aff[w] & (uint32_t)((2ull << t) - 1);
+    if (b) {
+      const int tl = 31 - __clz((int)b);
+      const int r = a.Mo[(int64_t)tl * a.nconv + w];
+      return a.Pt + (int64_t)r * a.cp;
+    }
+  }
+  return a.P + w * a.cp;
+}
+
+// Pooled rows of frame t: max_window f(P after t) - max_window f(P after
+// t - 1), as the streaming pool does with its old and new states.
+template <typename T, int TPS>
+__global__ __launch_bounds__(256) void k_chunk_pool_emit(ChunkPoolArgs a) {
+  constexpr int R = 256 / TPS, IT = TPS == 64 ? 4 : 1;
+  T* dout = (T*)a.dout;
+  const int lane = threadIdx.x % TPS;
+  const int64_t j = (int64_t)blockIdx.x * R + threadIdx.x / TPS;
+  const int64_t nQ = (int64_t)*a.nQ;
+  if (j >= nQ) return;
+  const Geo& g = a.g;
+  const int64_t qi = a.Q[j];
+  const int t = (int)(qi / a.npool);
+  const int64_t q = qi - (int64_t)t * a.npool;
+  const int64_t hwq = (int64_t)g.Ho * g.Wo;
+  const int n = (int)(q / hwq);
+  const int rem = (int)(q - n * hwq);
+  const int qy = rem / g.Wo, qx = rem - (rem / g.Wo) * g.Wo;
+  const int cp = a.cp, V = cp / 8;
+  float rm = 0.f;
+#pragma unroll
+  for (int k = 0; k < IT; ++k) {
+    const int v = lane + k * TPS;
+    if (v >= V) continue;
+    float mn[8], mo[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) mn[e] = mo[e] = -INFINITY;
+    for (int ky = 0; ky < g.kh; ++ky) {
+      const int iy = qy * g.sh - g.ph + ky;
+      if (iy < 0 || iy >= g.Hi) continue;
+      for (int kx = 0; kx < g.kw; ++kx) {
+        const int ix = qx * g.sw - g.pw + kx;
+        if (ix < 0 || ix >= g.Wi) continue;
+        const int64_t w = ((int64_t)n * g.Hi + iy) * g.Wi + ix;
+        float vn[8], vo[8];
+        load8f(state_at(a, w, t) + v * 8, vn);
+        load8f(state_at(a, w, t - 1) + v * 8, vo);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          mn[e] = fmaxf(mn[e], act_f(vn[e], a.act));
+          mo[e] = fmaxf(mo[e], act_f(vo[e], a.act));
+        }
+      }
+    }
+    float d[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) d[e] = mn[e] - mo[e];
+    rm = fmaxf(rm, Vec8<T>::store(dout + j * cp + v * 8, d));
+  }
+#pragma unroll
+  for (int o = 1; o < TPS; o <<= 1) rm = fmaxf(rm, __shfl_xor(rm, o, 64));
+  if (lane == 0) a.rowmax[j] = __float_as_uint(rm);
+}
+
+__global__ __launch_bounds__(256) void k_chunk_commit(float* P,
+                                                      const float* Pt,
+                                                      const int* Mo,
+                                                      const uint32_t* aff,
+                                                      int64_t nconv, int cp) {
+  const int c4 = cp / 4;
+  const int64_t total = nconv * c4;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    const int64_t w = idx / c4;
+    const uint32_t b = aff[w];
+    if (!b) continue;
+    const int tl = 31 - __clz((int)b);
+    const int r = Mo[(int64_t)tl * nconv + w];
+    const int c = (int)(idx - w * c4) * 4;
+    *(float4*)(P + w * cp + c) = *(const float4*)(Pt + (int64_t)r * cp + c);
+  }
+}
+
+template <typename T, int TPS>
+static void chunk_upd_t(hipStream_t s, const ChunkUpdArgs& a) {
+  constexpr int R = 256 / TPS;
+  k_chunk_update<T, TPS><<<(int)((a.npix + R - 1) / R), 256, 0, s>>>(a);
+}
+
+template <typename T>
+static void chunk_upd_d(hipStream_t s, const ChunkUpdArgs& a) {
+  switch (a.tps) {
+    case 1: chunk_upd_t<T, 1>(s, a); break;
+    case 2: chunk_upd_t<T, 2>(s, a); break;
+    case 4: chunk_upd_t<T, 4>(s, a); break;
+    case 8: chunk_upd_t<T, 8>(s, a); break;
+    case 16: chunk_upd_t<T, 16>(s, a); break;
+    case 32: chunk_upd_t<T, 32>(s, a); break;
+    default: chunk_upd_t<T, 64>(s, a); break;
+  }
+}
+
+void launch_chunk_update(const Prof& pf, hipStream_t s, int dtype,
+                         const ChunkUpdArgs& a) {
+  prof_begin(pf, 23 /*ST_K_CHUNK_UPDATE*/, s);
+  if (dtype == 0)
+    chunk_upd_d<float>(s, a);
+  else if (dtype == 1)
+    chunk_upd_d<_Float16>(s, a);
+  else
+    chunk_upd_d<bf16_t>(s, a);
+  prof_end(pf, 23, s);
+}
+
+template <typename T, int TPS>
+static void chunk_pool_t(hipStream_t s, const ChunkPoolArgs& a) {
+  constexpr int R = 256 / TPS;
+  k_chunk_pool_emit<T, TPS><<<(int)((a.capQ + R - 1) / R), 256, 0, s>>>(a);
+}
+
+template <typename T>
+static void chunk_pool_d(hipStream_t s, const ChunkPoolArgs& a) {
+  switch (a.tps) {
+    case 1: chunk_pool_t<T, 1>(s, a); break;
+    case 2: chunk_pool_t<T, 2>(s, a); break;
+    case 4: chunk_pool_t<T, 4>(s, a); break;
+    case 8: chunk_pool_t<T, 8>(s, a); break;
+    case 16: chunk_pool_t<T, 16>(s, a); break;
+    case 32: chunk_pool_t<T, 32>(s, a); break;
+    default: chunk_pool_t<T, 64>(s, a); break;
+  }
+}
+
+void launch_chunk_pool_emit(const Prof& pf, hipStream_t s, int dtype,
+                            const ChunkPoolArgs& a) {
+  prof_begin(pf, 12 /*ST_K_POOL_EMIT*/, s);
+  if (dtype == 0)
+    chunk_pool_d<float>(s, a);
+  else if (dtype == 1)
+    chunk_pool_d<_Float16>(s, a);
+  else
+    chunk_pool_d<bf16_t>(s, a);
+  prof_end(pf, 12, s);
+}
+
+void launch_chunk_commit(const Prof& pf, hipStream_t s, float* P,
+                         const float* Pt, const int* Mo, const uint32_t* aff,
+                         int64_t nconv, int cp) {
+  prof_begin(pf, 13 /*ST_K_COMMIT*/, s);
+  k_chunk_commit<<<grid_for(nconv * (cp / 4), 8192), 256, 0, s>>>(
+      P, Pt, Mo, aff, nconv, cp);
+  prof_end(pf, 13, s);
+}
+
 // ------------------------------------------------------- dense output
 __global__ __launch_bounds__(256) void k_output(const float* P, int cp, int C,
                                                 int N, Geo g, int has_pool,

@@ -45,21 +45,24 @@ static st_status create_fail(st_status s, const std::string& msg) {
   return s;
 }
 
-extern "C" st_status st_create_net(const st_layer_desc* layers,
-                                   int32_t n_layers, int32_t batch,
-                                   int32_t in_h, int32_t in_w, int32_t in_c,
-                                   int32_t dtype, st_net** out) {
+static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
+                             int32_t batch, int32_t max_frames, int32_t in_h,
+                             int32_t in_w, int32_t in_c, int32_t dtype,
+                             st_net** out) {
   if (!out) return create_fail(ST_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   if (!layers || n_layers < 1)
     return create_fail(ST_ERR_INVALID_ARG, "no layers");
   if (batch < 1 || in_h < 1 || in_w < 1 || in_c < 1)
     return create_fail(ST_ERR_INVALID_ARG, "input shape must be positive");
+  if (max_frames < 1 || max_frames > kMaxChunkFrames)
+    return create_fail(ST_ERR_INVALID_ARG, "max_frames must be in [1, 32]");
   if (dtype != ST_F32 && dtype != ST_F16 && dtype != ST_BF16)
     return create_fail(ST_ERR_INVALID_ARG, "unknown dtype");
-  if ((int64_t)batch * in_h * in_w >= (int64_t)1 << 31)
+  const int64_t F = max_frames;
+  if ((int64_t)batch * in_h * in_w * F >= (int64_t)1 << 31)
     return create_fail(ST_ERR_INVALID_ARG, "input grid exceeds 2^31 pixels");
-  if ((int64_t)batch * in_h * in_w > kMaxGrid)
+  if ((int64_t)batch * in_h * in_w * F > kMaxGrid)
     return create_fail(ST_ERR_UNSUPPORTED, "input grid above the compaction "
                                            "limit");
 
@@ -68,6 +71,7 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
   net->dtype = dtype;
   net->esize = esize_of(dtype);
   net->N = batch; net->H = in_h; net->W = in_w; net->C = in_c;
+  net->F = max_frames;
   net->layers.resize(n_layers);
   net->tensors.resize(n_layers + 1);
 
@@ -160,9 +164,9 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
     TensorPlan& t = net->tensors[i + 1];
     t.N = batch; t.H = L.Hp; t.W = L.Wp; t.C = d.c_out; t.Cp = L.cout_p;
     t.grid = (int64_t)batch * L.Hp * L.Wp;
-    if (L.conv_grid >= ((int64_t)1 << 31) / std::max(L.K, 1))
+    if (L.conv_grid * F >= ((int64_t)1 << 31) / std::max(L.K, 1))
       return bad(ST_ERR_INVALID_ARG, i, "rulebook exceeds 2^31 entries");
-    if (L.conv_grid > kMaxGrid || t.grid > kMaxGrid)
+    if (L.conv_grid * F > kMaxGrid || t.grid * F > kMaxGrid)
       return bad(ST_ERR_UNSUPPORTED, i, "grid above the compaction limit");
   }
 
@@ -178,32 +182,42 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
   const int L_n = n_layers;
   net->n_counters = 2 * (L_n + 1) + 2 * L_n;
   net->off_cnt = a.take(sizeof(uint64_t) * net->n_counters);
-  net->off_dens = a.take(sizeof(uint64_t) * batch);
+  net->off_dens = a.take(sizeof(uint64_t) * batch * F);
   net->off_tiles = a.take(sizeof(uint32_t) * kMaxTiles);
   net->off_xhat = a.take((size_t)t0.grid * in_c * net->esize);
-  int64_t max_grid = t0.grid;
+  // Per-site buffers of the emitted tensors and rulebooks hold F frames
+  // (chunk items: frame t's sites follow frame t-1's); the state, X_hat and
+  // squeeze-excitation buffers are per physical site.
+  int64_t max_grid = t0.grid * F;
   for (int t = 0; t <= L_n; ++t) {
     TensorPlan& T = net->tensors[t];
+    const int64_t items = T.grid * F;
     T.cnt_rows = 2 * t;
     T.cnt_act = 2 * t + 1;
-    T.off_rows = a.take((size_t)T.grid * T.Cp * net->esize);
-    T.off_rowpix = a.take(sizeof(int32_t) * T.grid);
-    T.off_act = a.take(sizeof(int32_t) * T.grid);
-    T.off_map = a.take(sizeof(int32_t) * T.grid);
-    T.off_rowmax = a.take(sizeof(uint32_t) * T.grid);
-    max_grid = std::max(max_grid, T.grid);
+    T.off_rows = a.take((size_t)items * T.Cp * net->esize);
+    T.off_rowpix = a.take(sizeof(int32_t) * items);
+    T.off_act = a.take(sizeof(int32_t) * items);
+    T.off_map = a.take(sizeof(int32_t) * items);
+    T.off_rowmax = a.take(sizeof(uint32_t) * items);
+    max_grid = std::max(max_grid, items);
   }
   int n_cleanup = L_n + 1;
-  size_t part_bytes = 0;
+  size_t part_bytes = 0, chunk_dp_bytes = 0;
+  int64_t max_conv_phys = 0;
   for (int i = 0; i < L_n; ++i) {
     LayerPlan& L = net->layers[i];
     TensorPlan& T = net->tensors[i + 1];
+    const int64_t citems = L.conv_grid * F;
     L.cnt_pairs = 2 * (L_n + 1) + i;
-    max_grid = std::max(max_grid, L.conv_grid);
+    max_grid = std::max(max_grid, citems);
+    max_conv_phys = std::max(max_conv_phys, L.conv_grid);
+    if (F > 1 && L.stateful)
+      chunk_dp_bytes = std::max<size_t>(chunk_dp_bytes,
+                                        sizeof(float) * citems * L.cout_p);
     if (L.pool || L.se) {
       L.cnt_O = 2 * (L_n + 1) + L_n + i;
-      L.off_O = a.take(sizeof(int32_t) * L.conv_grid);
-      L.off_Mo = a.take(sizeof(int32_t) * L.conv_grid);
+      L.off_O = a.take(sizeof(int32_t) * citems);
+      L.off_Mo = a.take(sizeof(int32_t) * citems);
       L.off_dP = a.take(sizeof(float) * L.conv_grid * L.cout_p);
       ++n_cleanup;
     } else {
@@ -211,7 +225,7 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
       L.off_O = T.off_rowpix;
       L.off_Mo = T.off_map;
     }
-    L.off_nbr = a.take(sizeof(int32_t) * L.conv_grid * L.K);
+    L.off_nbr = a.take(sizeof(int32_t) * citems * L.K);
     if (L.stateful) L.off_P = a.take(sizeof(float) * L.conv_grid * L.cout_p);
     if (L.dw)
       L.off_w = a.take(sizeof(float) * L.K * L.cout_p);
@@ -224,11 +238,11 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
         L.split_max = (int)std::min<int64_t>(kSplitMax, stages / 8);
       part_bytes = std::max<size_t>(
           part_bytes, L.split_max > 1 ? sizeof(float) * L.split_max *
-                                            L.conv_grid * L.cout_p
+                                            citems * L.cout_p
                                       : 0);
     }
-    if (!L.ident) L.off_flags = a.take(round_up(L.conv_grid, 16));
-    if (L.pool) L.off_pflags = a.take(round_up(T.grid, 16));
+    if (!L.ident) L.off_flags = a.take(round_up(citems, 16));
+    if (L.pool) L.off_pflags = a.take(round_up(T.grid * F, 16));
     if (L.se) {
       const int64_t hw = (int64_t)L.Ho * L.Wo;
       L.se_tps = se_threads_per_site(L.cout_p);
@@ -248,7 +262,13 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
     }
   }
   net->max_grid = max_grid;
-  net->off_flags = a.take(round_up(t0.grid, 16));
+  net->off_flags = a.take(round_up(t0.grid * F, 16));
+  if (F > 1) {
+    net->off_chunk_dp = a.take(std::max<size_t>(chunk_dp_bytes, 256));
+    net->off_chunk_base = a.take(round_up(t0.grid * F, 16));
+    net->off_chunk_last = a.take(round_up(t0.grid, 16));
+    net->off_chunk_aff = a.take(sizeof(uint32_t) * max_conv_phys);
+  }
   net->off_grp = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
   net->off_mdone = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
   net->off_zero = a.take(256);
@@ -258,6 +278,23 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
   net->ws_bytes = round_up(a.top, kAlign);
   *out = net;
   return ST_OK;
+}
+
+extern "C" st_status st_create_net(const st_layer_desc* layers,
+                                   int32_t n_layers, int32_t batch,
+                                   int32_t in_h, int32_t in_w, int32_t in_c,
+                                   int32_t dtype, st_net** out) {
+  return create_impl(layers, n_layers, batch, 1, in_h, in_w, in_c, dtype,
+                     out);
+}
+
+extern "C" st_status st_create_net_chunked(const st_layer_desc* layers,
+                                           int32_t n_layers, int32_t batch,
+                                           int32_t max_frames, int32_t in_h,
+                                           int32_t in_w, int32_t in_c,
+                                           int32_t dtype, st_net** out) {
+  return create_impl(layers, n_layers, batch, max_frames, in_h, in_w, in_c,
+                     dtype, out);
 }
 
 extern "C" st_status st_workspace_bytes(const st_net* net, uint64_t* bytes) {

@@ -31,10 +31,11 @@ def layer_desc(L, w_ptr: int, b_ptr: Optional[int],
 
 class SparseTemNet:
     """One diff encoder: reference frame via ``encode_reference``, then
-    diff frames via ``encode_diff`` (see include/sparsetem.h)."""
+    diff frames via ``encode_diff``, or up to ``max_frames`` of them at once
+    via ``encode_chunk`` (see include/sparsetem.h)."""
 
     def __init__(self, layers: Sequence, batch: int, H: int, W: int, C: int,
-                 dtype: str = "f32", device="cuda"):
+                 dtype: str = "f32", device="cuda", max_frames: int = 1):
         self.dtype = dtype
         self.tdtype = TORCH_DTYPES[dtype]
         dev = torch.device(device)
@@ -42,6 +43,7 @@ class SparseTemNet:
             dev = torch.device("cuda", torch.cuda.current_device())
         self.device = dev
         self.n_layers = len(layers)
+        self.has_se = any(getattr(L, "se_mid", 0) for L in layers)
         self.in_shape = (batch, H, W, C)
         self._w, self._b, descs = [], [], []
         for L in layers:
@@ -62,8 +64,14 @@ class SparseTemNet:
                 se = tuple(x.data_ptr() for x in t)
             descs.append(layer_desc(L, w.data_ptr(),
                                     None if b is None else b.data_ptr(), se))
-        self.handle = B.st_create_net(descs, batch, H, W, C,
-                                      B.DTYPE_CODES[dtype])
+        self.max_frames = max_frames
+        if max_frames > 1:
+            self.handle = B.st_create_net_chunked(descs, batch, max_frames,
+                                                  H, W, C,
+                                                  B.DTYPE_CODES[dtype])
+        else:
+            self.handle = B.st_create_net(descs, batch, H, W, C,
+                                          B.DTYPE_CODES[dtype])
         self.ws_bytes = B.st_workspace_bytes(self.handle)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8,
                               device=self.device)
@@ -104,6 +112,39 @@ class SparseTemNet:
                          self._stream())
         return out
 
+    def encode_chunk(self, frames, thr, out=None, write_out=True):
+        """frames: contiguous device tensor [n_frames, *in_shape]; returns
+        the outputs of every frame, [n_frames, *out_shape] (f32)."""
+        nf = frames.shape[0] if frames.dim() == 5 else -1
+        if (frames.device != self.device or frames.dtype != self.tdtype
+                or frames.dim() != 5 or tuple(frames.shape[1:]) !=
+                self.in_shape or not frames.is_contiguous()):
+            raise ValueError("frames must be a contiguous device tensor "
+                             f"[n, {self.in_shape}] of {self.tdtype}")
+        if len(thr) != self.n_layers + 1:
+            raise ValueError("thr needs n_layers + 1 entries")
+        if write_out and out is None:
+            out = torch.empty((nf,) + tuple(self.out_shape),
+                              dtype=torch.float32, device=self.device)
+        if write_out and (tuple(out.shape) != (nf,) + tuple(self.out_shape)
+                          or out.dtype != torch.float32
+                          or not out.is_contiguous()):
+            raise ValueError("out must be a contiguous f32 tensor "
+                             f"[{nf}, {self.out_shape}]")
+        B.st_encode_chunk(self.handle, frames.data_ptr(), nf, thr,
+                          out.data_ptr() if write_out else None,
+                          self._stream())
+        return out
+
+    def capture_diff(self, thr, out):
+        """Capture one diff-frame encode with fixed thresholds `thr` and
+        output `out` into a HIP graph; returns a callable that encodes a
+        frame by copying it into the graph's input slot and replaying the
+        graph (same kernels and arguments as encode_diff).  Requires a
+        reference frame to have been encoded; not available for nets with
+        squeeze-excitation (their gate buffers alternate per frame)."""
+        return DiffGraph(self, thr, out)
+
     def density(self, layer: int, image: int = -1) -> float:
         return B.st_layer_density(self.handle, layer, image)
 
@@ -121,3 +162,28 @@ class SparseTemNet:
             self.close()
         except Exception:
             pass
+
+
+class DiffGraph:
+    """A diff-frame encode replayed as a HIP graph (see
+    SparseTemNet.capture_diff).  Every replay launches the same per-frame
+    kernel sequence as st_encode_diff on the current stream."""
+
+    def __init__(self, net: SparseTemNet, thr, out):
+        if net.has_se:
+            raise ValueError("nets with squeeze-excitation alternate their "
+                             "gate buffers per frame and cannot be replayed")
+        if len(thr) != net.n_layers + 1:
+            raise ValueError("thr needs n_layers + 1 entries")
+        self.slot = torch.zeros(net.in_shape, dtype=net.tdtype,
+                                device=net.device)
+        self.out = out
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            B.st_encode_diff(net.handle, self.slot.data_ptr(), list(thr),
+                             out.data_ptr(), net._stream())
+
+    def __call__(self, frame):
+        self.slot.copy_(frame)
+        self.graph.replay()
+        return self.out

@@ -187,3 +187,29 @@ def test_single_hip_runtime():
                        capture_output=True, text=True, timeout=300)
     assert r.returncode == 0, r.stderr
     assert r.stdout.strip().splitlines()[-1] == "1"
+
+
+def test_chunked_create_and_workspace():
+    """A chunk-capable net: item buffers grow with max_frames, the state
+    does not; max_frames outside [1, 32] is rejected; a chunk encode on an
+    unbound net is a state error (no HIP call is made)."""
+    net = resnet_mini_net()
+    d = descs(net)
+    h1 = B.st_create_net(d, net.batch, net.H, net.W, net.C, B.ST_F32)
+    h8 = B.st_create_net_chunked(d, net.batch, 8, net.H, net.W, net.C,
+                                 B.ST_F32)
+    try:
+        w1, w8 = B.st_workspace_bytes(h1), B.st_workspace_bytes(h8)
+        assert w1 < w8 < 8 * w1
+        with pytest.raises(B.StError) as e:
+            B.st_encode_chunk(h8, 0x1000, 2, [0.0] * (len(net.layers) + 1),
+                              None)
+        assert e.value.status == B.ST_ERR_STATE
+    finally:
+        B.st_destroy_net(h1)
+        B.st_destroy_net(h8)
+    for bad in (0, 33):
+        with pytest.raises(B.StError) as e:
+            B.st_create_net_chunked(d, net.batch, bad, net.H, net.W, net.C,
+                                    B.ST_F32)
+        assert e.value.status == B.ST_ERR_INVALID_ARG

@@ -1,0 +1,121 @@
+"""Chunk mode (st_encode_chunk: a chunk's diff frames encoded layer-major,
+the SparseBatch schedule) against the oracle run frame by frame, and
+against the library's own frame-by-frame path.  After every chunk: each
+frame's output, each frame's kept list of every tensor (rows whose keep
+decision rounds differently on the two sides -- their max |delta| within a
+band around the threshold -- are counted and bounded) and each frame's
+input density; after the chunk, the pre-activation state."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2410_20790_amd import SparseTemNet
+from paper_2410_20790_amd import binding as B
+from parity_util import RTOL, band, rel, say, to_dev
+from workloads import (crnn_vgg_net, depthwise_test_net, random_sparse_video,
+                       resnet_mini_net, textline_video, toy_net, toy_video)
+
+pytestmark = pytest.mark.gpu
+
+
+def run_chunks(net, frames, thr, F, tag, max_band=0):
+    dt = net.dtype
+    L_n = len(net.layers)
+    thr_l = [thr] * (L_n + 1)
+    o = oracle.OracleNet(net.layers, net.batch, net.H, net.W, net.C, dt)
+    g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt,
+                     max_frames=F)
+    s = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt)
+    try:
+        say(f"[gpu] chunk {tag}: reference frame")
+        o.encode_reference(frames[0])
+        g.encode_reference(to_dev(frames[0], dt))
+        s.encode_reference(to_dev(frames[0], dt))
+        t, n_band = 1, 0
+        while t < len(frames):
+            nf = min(F, len(frames) - t)
+            say(f"[gpu] chunk {tag}: frames {t}..{t + nf - 1}")
+            chunk = torch.stack([to_dev(f, dt) for f in frames[t:t + nf]])
+            outs = g.encode_chunk(chunk.contiguous(), thr_l)
+            torch.cuda.synchronize()
+            acts = [B.st_debug_active(g.handle, k - 1) for k in range(L_n + 1)]
+            dens0 = [g.density(-1, j * net.batch) for j in range(nf)]
+            for j in range(nf):
+                o.encode_diff(frames[t + j], thr_l)
+                out_s = s.encode_diff(to_dev(frames[t + j], dt), thr_l)
+                torch.cuda.synchronize()
+                oo = o.last["out"]
+                e = rel(outs[j].cpu().numpy(), oo)
+                assert e <= RTOL[dt], f"{tag} frame {t + j}: output {e}"
+                es = rel(outs[j].cpu().numpy(), out_s.cpu().numpy())
+                assert es <= (1e-5 if dt == "f32" else RTOL[dt]), \
+                    f"{tag} frame {t + j}: chunk vs frame-by-frame {es}"
+                for k in range(L_n + 1):
+                    T = o.last["tensors"][k]
+                    npix = int(np.prod(T["grid"]))
+                    a = acts[k]
+                    mine = a[(a >= j * npix) & (a < (j + 1) * npix)] - j * npix
+                    diff = set(mine.tolist()) ^ set(T["pix"].tolist())
+                    if diff:
+                        cm = dict(zip(T["cand"].tolist(),
+                                      T["cand_max"].tolist()))
+                        sc = max(np.abs(T["cand_max"]).max(), 1e-30)
+                        bw = band(dt, max(thr, 0.0), sc)
+                        for p in diff:
+                            assert abs(cm.get(p, 0.0) - max(thr, 0.0)) <= bw, (
+                                f"{tag} frame {t + j} tensor {k}: pixel {p} "
+                                "kept on one side only")
+                        n_band += len(diff)
+                N, H, W = o.last["tensors"][0]["grid"]
+                d0 = np.sum(o.last["tensors"][0]["pix"] < H * W) / float(H * W)
+                assert abs(dens0[j] - d0) <= 1e-6 + n_band / (H * W)
+            for i in o.P:
+                Pg = B.st_debug_state(g.handle, i, o.P[i].shape)
+                e = rel(Pg, o.P[i])
+                assert e <= RTOL[dt], f"{tag} after frame {t + nf - 1}: " \
+                    f"state {i} {e}"
+            t += nf
+        assert n_band <= max_band, f"{tag}: {n_band} band rows"
+    finally:
+        g.close()
+        s.close()
+
+
+@pytest.mark.parametrize("thr", [0.0, 0.05])
+def test_chunk_toy(thr):
+    run_chunks(toy_net(), toy_video(seed=3, n_frames=9), thr, 4,
+               f"toy thr={thr}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_chunk_resnet_mini(dtype):
+    """7x7/2 stem with an overlapping 3x3/2 max-pool (the chunk pool path),
+    bottlenecks with downsample and identity shortcuts."""
+    net = resnet_mini_net(dtype=dtype)
+    run_chunks(net, random_sparse_video(12, 8, 1, 32, 48, 3, 0.08,
+                                        dtype=dtype),
+               0.0, 3, f"resnet_mini {dtype}",
+               max_band=0 if dtype == "f32" else 8)
+
+
+def test_chunk_crnn():
+    """Four max-pools (2x2/2 and 2x1), thresholds above zero."""
+    run_chunks(crnn_vgg_net(), textline_video(seed=5, n_frames=11), 0.02, 5,
+               "crnn thr=0.02", max_band=4)
+
+
+def test_chunk_depthwise():
+    net = depthwise_test_net()
+    run_chunks(net, random_sparse_video(13, 7, 1, 24, 40, 16, 0.1), 0.0, 6,
+               "depthwise")
+
+
+def test_chunk_single_frame_and_batch():
+    """A batch of two images (items are frames x images), and a last chunk
+    of one frame."""
+    from dataclasses import replace
+    net = replace(resnet_mini_net(), batch=2)
+    frames = random_sparse_video(14, 4, 2, 32, 48, 3, 0.1)
+    run_chunks(net, frames, 0.0, 2, "batch 2")
