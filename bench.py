@@ -48,7 +48,7 @@ def workload(name, density):
             net=net, desc=f"resnet50-bf16-1024x2048-density{density:g}",
             frames=lambda n, H=1024, W=2048: driving_video(
                 seed=0, n_frames=n, H=H, W=W, density=density),
-            crop=(256, 512), chunk=None, ibst=False)
+            crop=(256, 512), chunk=10, ibst=False)
     if name == "effnet_b0":
         net = efficientnet_net(H=512, W=512, dtype="f16")
         return dict(
@@ -274,10 +274,12 @@ def measured_traffic(workload_desc, kernel):
 KCLASS = {"k_conv_gemm": "conv_gemm", "k_conv_dw": "conv_dw",
           "k_split_epi": "conv_split_epi", "k_pool_emit": "pool_emit",
           "k_commit": "commit", "k_output": "output",
-          "k_se_squeeze": "se_squeeze", "k_se_emit": "se_emit"}
+          "k_se_squeeze": "se_squeeze", "k_se_emit": "se_emit",
+          "k_chunk_update": "chunk_update", "k_chunk_pool_emit": "pool_emit",
+          "k_chunk_commit": "commit"}
 
 
-def ingest_counters(base, workload_name, density):
+def ingest_counters(base, workload_name, density, schedule=None):
     """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the diff-pass kernels,
     scaled by what the same counters read for a plain copy of COPY_BYTES,
     averaged per launch; written to profiles/hbm_traffic.json with the
@@ -322,39 +324,46 @@ def ingest_counters(base, workload_name, density):
                     "fetch_kib_raw": f, "write_kib_raw": w,
                     "launches": len(v["FETCH_SIZE"]),
                     "scale": scale, "source_hash": kernel_source_hash()}
-    d[wl["desc"]] = entry
+    d[f"{wl['desc']}-{default_schedule(wl, schedule)}"] = entry
     json.dump(d, open(out_path, "w"), indent=1, sort_keys=True)
     print(json.dumps(entry))
 
 
-def density_sweep(net, thr, densities, steps):
+def density_sweep(net, thr, densities, steps, chunk, schedule):
     """diff-frames/s and algorithmic TFLOP/s at several change densities of
-    the same video recipe (each: reference + 2 warm-up + `steps` timed
-    frames)."""
+    the same video recipe, in the given schedule (each: a reference frame
+    and one warm-up chunk, then `steps` timed diff frames in chunks of
+    `chunk` frames, reference frames synchronised around and left out)."""
     import torch
     from paper_2410_20790_amd import SparseTemNet
     from paper_2410_20790_amd import binding as B
     from workloads import driving_video
     tdt = torch.bfloat16 if net.dtype == "bf16" else torch.float32
+    batch = chunk - 1 if schedule == "chunk" else 1
     out = {}
-    g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, net.dtype)
-    o = g.new_output()
+    g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, net.dtype,
+                     max_frames=batch)
+    o = torch.empty((batch,) + tuple(g.out_shape), dtype=torch.float32,
+                    device="cuda")
+    if batch == 1:
+        o = o[0]
     L_n = len(net.layers)
+    thr_l = [thr] * (L_n + 1)
     for d in densities:
-        fr = [torch.from_numpy(f).to("cuda", tdt) for f in driving_video(
-            seed=7, n_frames=3 + steps, H=net.H, W=net.W, density=d)]
-        g.encode_reference(fr[0], out=o)
-        for i in (1, 2):
-            g.encode_diff(fr[i], [thr] * (L_n + 1), out=o)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for i in range(3, 3 + steps):
-            g.encode_diff(fr[i], [thr] * (L_n + 1), out=o)
-        torch.cuda.synchronize()
-        ms = (time.perf_counter() - t0) * 1000.0 / steps
+        fr_np = driving_video(seed=7, n_frames=frames_needed(
+            chunk, chunk - 1, steps, 0), H=net.H, W=net.W, density=d)
+        fr = torch.empty((len(fr_np), net.batch, net.H, net.W, net.C),
+                         dtype=tdt, device="cuda")
+        for i, f in enumerate(fr_np):
+            fr[i].copy_(torch.from_numpy(f))
+        del fr_np
+        feed = Feed(g, L_n, fr, chunk, thr_l, None, o, batch)
+        run_diffs(feed, chunk - 1)
+        wall, _ = run_diffs(feed, steps)
+        ms = wall * 1000.0 / steps
         pairs, _ = B.st_debug_counters(g.handle, L_n)
         fl = sum(2 * int(pairs[j]) * (L.c_in // L.groups) * L.c_out
-                 for j, L in enumerate(net.layers))
+                 for j, L in enumerate(net.layers)) / feed.last_m
         out[f"{d:g}"] = {"ms_per_frame": ms, "diff_frames_per_s": 1000.0 / ms,
                          "input_density": g.density(-1),
                          "alg_gflop": fl / 1e9,
@@ -366,17 +375,23 @@ def density_sweep(net, thr, densities, steps):
 
 class Feed:
     """Walks a synthetic video: a reference frame every `chunk` frames (only
-    the first frame when chunk is None), diff frames in between.  With a
-    controller, each diff frame's thresholds come from it and its kept-row
+    the first frame when chunk is None), diff frames in between.  With
+    `batch` > 1 (the SparseBatch schedule) the diff frames of a chunk are
+    encoded up to `batch` at a time by one st_encode_chunk call, else one
+    st_encode_diff call per frame.  With a controller (frame schedule
+    only), each diff frame's thresholds come from it and its kept-row
     counters are fed back after the frame (one host round trip per frame,
     part of the timed work)."""
 
-    def __init__(self, g, n_layers, frames, chunk, thr, ctl, out):
+    def __init__(self, g, n_layers, frames, chunk, thr, ctl, out, batch=1):
         from paper_2410_20790_amd import binding as B
         self.B = B
         self.replay = None     # a captured diff-frame graph, when set
         self.g, self.frames, self.chunk = g, frames, chunk
         self.thr, self.ctl, self.out = thr, ctl, out
+        self.batch = batch
+        if batch > 1 and ctl is not None:
+            raise ValueError("the controller adjusts thresholds per frame")
         self.pos = 0
         self.L_n = n_layers
         self.grids = [int(np.prod(g.tensor_shape(t - 1)[:3]))
@@ -389,22 +404,37 @@ class Feed:
     def ref(self):
         if self.ctl:
             self.ctl.start_cycle()
-        self.g.encode_reference(self.frames[self.pos], out=self.out)
+        self.g.encode_reference(self.frames[self.pos],
+                                out=self.out[0] if self.batch > 1
+                                else self.out)
         self.pos += 1
 
-    def diff(self):
+    def diff(self, limit=1):
+        """Encode up to `limit` diff frames (at most to the next reference
+        frame); returns how many."""
         from paper_2410_20790_amd.ibst import sparsity_from_counts
+        if self.batch > 1:
+            m = min(limit, self.batch)
+            if self.chunk:
+                m = min(m, self.chunk - self.pos % self.chunk)
+            self.g.encode_chunk(self.frames[self.pos:self.pos + m], self.thr,
+                                out=self.out[:m])
+            self.pos += m
+            self.last_m = m
+            return m
         thr = self.ctl.thresholds() if self.ctl else self.thr
         if self.replay is not None:
             self.replay(self.frames[self.pos])
         else:
             self.g.encode_diff(self.frames[self.pos], thr, out=self.out)
         self.pos += 1
+        self.last_m = 1
         if self.ctl:
             _, act = self.B.st_debug_counters(self.g.handle, self.L_n)
             sp = sparsity_from_counts(act, self.grids)
             self.sparsity.append(sp)
             self.ctl.update(sp)
+        return 1
 
 
 def run_diffs(feed, n):
@@ -425,8 +455,7 @@ def run_diffs(feed, n):
             t0 = time.perf_counter()
             refs.append((t0 - t1) * 1000.0)
         else:
-            feed.diff()
-            done += 1
+            done += feed.diff(n - done)
     torch.cuda.synchronize()
     total += time.perf_counter() - t0
     return total, refs
@@ -457,9 +486,13 @@ def frames_needed(chunk, W, K, KP, KG=0):
     return pos
 
 
-def kernel_table(net, recs, counts, es):
+def kernel_table(net, recs, counts, es, chunk_mode=False):
     """Per kernel class: launches, time, algorithmic bytes / FLOPs from the
-    frame's counters (see conv_launch_bytes)."""
+    frame's counters (see conv_launch_bytes).  In chunk mode a profiled
+    "frame" is one chunk (counters summed over its frames), every stateful
+    layer's GEMM writes its f32 update rows, and the chunk state update is
+    charged its update-row reads and delta writes (a lower bound: its f32
+    state reads and writes, once per site, are not counted)."""
     from paper_2410_20790_amd import binding as B
     classes = {}
     for r in recs:
@@ -473,8 +506,10 @@ def kernel_table(net, recs, counts, es):
             continue
         if name in ("conv_gemm", "conv_dw"):
             L = net.layers[j]
-            c["bytes"] += conv_launch_bytes(L, counts[f, j], es,
-                                            layer_mode(net, j))
+            mode = layer_mode(net, j)
+            if chunk_mode and mode == "state":
+                mode = "defer"
+            c["bytes"] += conv_launch_bytes(L, counts[f, j], es, mode)
             c["flops"] += 2.0 * counts[f, j, 1] * (L.c_in // L.groups) * \
                 L.c_out
         elif name in ("se_squeeze", "se_emit"):
@@ -490,6 +525,9 @@ def kernel_table(net, recs, counts, es):
             else:
                 b = npix * (L.c_out * (4 + es) + 16) + nO * L.c_out * 8
             c["bytes"] += b
+        elif name == "chunk_update":
+            L = net.layers[j]
+            c["bytes"] += int(counts[f, j, 0]) * L.c_out * (4 + es)
         elif name == "scan_mask":
             c["bytes"] += net.batch * net.H * net.W * (2 * net.C * es + 1)
         elif name == "scan_compact":
@@ -571,10 +609,13 @@ def roofline_of(classes, dt, desc):
     return roof
 
 
-def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025):
+def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
+            schedule="frame"):
     """Time K diff frames of a workload (after W warm-up diff frames), then
     KP more with an event pair around every launch; dense comparators on
-    the same net.  Returns the result fields and the live objects."""
+    the same net.  schedule "chunk" encodes each chunk's diff frames in one
+    st_encode_chunk call (SparseBatch; KP becomes one whole chunk),
+    "frame" one st_encode_diff call per frame."""
     import torch
     from paper_2410_20790_amd import SparseTemNet
     from paper_2410_20790_amd import binding as B
@@ -583,27 +624,41 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025):
     dt = net.dtype
     es = ESIZE[dt]
     chunk = wl["chunk"]
-    if chunk:
+    batch = chunk - 1 if schedule == "chunk" else 1
+    if schedule == "chunk":
+        KP = batch
+    elif chunk:
         KP = min(KP, chunk - 1)
     # graph replay of the per-frame launch sequence: fixed thresholds and
     # no squeeze-excitation (whose gate buffers alternate per frame)
-    KG = K if not wl["ibst"] and not any(L.se_mid for L in net.layers) else 0
+    KG = K if (schedule == "frame" and not wl["ibst"] and
+               not any(L.se_mid for L in net.layers)) else 0
     t_gen = time.perf_counter()
     frames_np = wl["frames"](frames_needed(chunk, W, K, KP, KG))
     t_gen = time.perf_counter() - t_gen
     tdt = {"f32": torch.float32, "f16": torch.float16,
            "bf16": torch.bfloat16}[dt]
-    frames = [torch.from_numpy(f).to("cuda", tdt).contiguous()
-              for f in frames_np]
+    # one resident [n, N, H, W, C] tensor: frame i and chunk slices of it
+    # are contiguous views
+    frames = torch.empty((len(frames_np), net.batch, net.H, net.W, net.C),
+                         dtype=tdt, device="cuda")
+    for i, f in enumerate(frames_np):
+        frames[i].copy_(torch.from_numpy(f))
     del frames_np
-    g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt)
+    g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt,
+                     max_frames=batch)
     L_n = len(net.layers)
     thr = [thr_val] * (L_n + 1)
-    out = g.new_output()
+    if batch > 1:
+        out = torch.empty((batch,) + tuple(g.out_shape),
+                          dtype=torch.float32, device="cuda")
+        out0 = out[0]
+    else:
+        out = out0 = g.new_output()
     ctl = None
     if wl["ibst"]:
         ctl = IBST(L_n + 1, nonlinear_tensors(net.layers), target, eps)
-    feed = Feed(g, L_n, frames, chunk, thr, ctl, out)
+    feed = Feed(g, L_n, frames, chunk, thr, ctl, out, batch)
     dflops = dense_flops(net, [net_conv_grid(net, i) for i in range(L_n)])
 
     run_diffs(feed, W)  # reference frame + warm-up
@@ -626,21 +681,24 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025):
     # ---- profiled diff frames: an event pair around every launch
     if chunk:
         while not feed.next_is_ref():
-            feed.diff()
+            feed.diff(chunk)
         feed.ref()
     B.st_profile_begin(g.handle, KP * 1024, KP + 1)
     torch.cuda.synchronize()
     tp = time.perf_counter()
-    for _ in range(KP):
-        feed.diff()
+    done = 0
+    while done < KP:
+        done += feed.diff(KP - done)
     torch.cuda.synchronize()
     prof_ms_step = (time.perf_counter() - tp) * 1000.0 / KP
     recs, counts = B.st_profile_end(g.handle, L_n)
-    per_frame_flops = [
-        sum(2 * int(counts[f, j, 1]) * (L.c_in // L.groups) * L.c_out
-            for j, L in enumerate(net.layers)) for f in range(len(counts))]
-    alg_flops = float(np.mean(per_frame_flops))
-    classes = kernel_table(net, recs, counts, es)
+    # per diff frame (a profiled record of the chunk schedule is a chunk)
+    alg_flops = sum(
+        2 * int(counts[f, j, 1]) * (L.c_in // L.groups) * L.c_out
+        for f in range(len(counts))
+        for j, L in enumerate(net.layers)) / KP
+    classes = kernel_table(net, recs, counts, es,
+                           chunk_mode=schedule == "chunk")
     total_ms = sum(c["ms"] for c in classes.values())
     kern = {}
     for name, c in sorted(classes.items(), key=lambda kv: -kv[1]["ms"]):
@@ -654,7 +712,8 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025):
             e["alg_TFLOPs"] = c["flops"] / (c["ms"] * 1e-3) / 1e12
             e["mfma_frac"] = e["alg_TFLOPs"] / MFMA_PEAK_TFLOPS[dt]
         kern[name] = e
-    roof = roofline_of(classes, dt, wl["desc"])
+    desc = f"{wl['desc']}-{schedule}"
+    roof = roofline_of(classes, dt, desc)
     roof["event_pair_overhead_us"] = event_overhead_us()
 
     # ---- graph replay: the same diff frames' launch sequence captured once
@@ -678,17 +737,19 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025):
     if dense:
         x = frames[0]
         dense_ms["own_dense_ms"] = time_gpu(
-            lambda: g.encode_reference(x, out=out), 5)
+            lambda: g.encode_reference(x, out=out0), 5)
         fwd = torch_dense_model(net, dt)
         with torch.no_grad():
             dense_ms["miopen_ms"] = time_gpu(lambda: fwd(x), 10, warm=3)
             ref_t = fwd(x).permute(0, 2, 3, 1).float()
-        g.encode_reference(x, out=out)
+        g.encode_reference(x, out=out0)
         torch.cuda.synchronize()
         dense_ms["miopen_vs_own_rel_err"] = float(
-            (ref_t - out).abs().max() / out.abs().max())
+            (ref_t - out0).abs().max() / out0.abs().max())
 
     res = {
+        "schedule": schedule,
+        "workload": desc,
         "value": 1000.0 / ms_step,
         "ms_per_step": ms_step,
         "event_ms_per_step": ev_ms,
@@ -740,15 +801,39 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025):
     return res
 
 
+def default_schedule(wl, requested=None):
+    """SparseBatch (one st_encode_chunk call per chunk) where the library
+    offers it -- nets without squeeze-excitation whose input has at most
+    16 channels, and whose thresholds are fixed over a chunk -- else one
+    st_encode_diff call per frame."""
+    net = wl["net"]
+    ok = (wl["chunk"] and wl["chunk"] > 2 and not wl["ibst"] and
+          not any(L.se_mid for L in net.layers) and net.C <= 16)
+    if requested == "frame" or not ok:
+        return "frame"
+    return "chunk"
+
+
+FRAME_KEYS = ("value", "ms_per_step", "event_ms_per_step", "effective_tflops",
+              "ref_ms", "chunk_amortised_frames_per_s", "roofline",
+              "graph_replay", "profiled_ms_per_step", "workload")
+
+
 def extra_workload(name, steps, warmup, thr=0.0):
-    """A secondary workload measured in the same run, summarised."""
+    """A secondary workload measured in the same run, summarised; in the
+    SparseBatch schedule where it applies, with the frame-by-frame figure
+    beside it."""
     import torch
     wl = workload(name, 0.0)
     net = wl["net"]
-    r = measure(wl, steps, warmup, 7, thr)
+    sched = default_schedule(wl)
+    r = measure(wl, steps, warmup, 7, thr, schedule=sched)
+    if sched == "chunk":
+        f = measure(wl, steps, warmup, 7, thr, dense=False, schedule="frame")
+        r["frame_by_frame"] = {k: f[k] for k in FRAME_KEYS if k in f}
     r["config"] = {"workload": wl["desc"], "batch": net.batch, "H": net.H,
                    "W": net.W, "C": net.C, "layers": len(net.layers),
-                   "dtype": net.dtype,
+                   "dtype": net.dtype, "chunk": wl["chunk"],
                    "thr": "ibst" if wl["ibst"] else thr}
     torch.cuda.empty_cache()
     return r
@@ -757,23 +842,31 @@ def extra_workload(name, steps, warmup, thr=0.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=45,
+                    help="timed diff frames (ResNet-50: five chunks of 9)")
+    ap.add_argument("--warmup", type=int, default=9)
     ap.add_argument("--workload", default="resnet50",
                     choices=["resnet50", "effnet_b0", "multistream", "crnn",
                              "toy"])
+    ap.add_argument("--schedule", choices=["chunk", "frame"], default=None,
+                    help="chunk: the diff frames of a chunk in one "
+                         "st_encode_chunk call (SparseBatch; the default "
+                         "where the net allows it); frame: one "
+                         "st_encode_diff call per frame")
     ap.add_argument("--density", type=float, default=0.10)
     ap.add_argument("--thr", type=float, default=0.0)
-    ap.add_argument("--profile-steps", type=int, default=10)
+    ap.add_argument("--profile-steps", type=int, default=9)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-frame", action="store_true",
+                    help="skip the frame-by-frame comparison pass")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the other workloads (EfficientNet-B0 512x512 "
                          "f16 and 32 streams of 256x256 bf16, both with "
                          "online threshold adjustment; CRNN-VGG text lines; "
                          "the toy net)")
-    ap.add_argument("--sweep-steps", type=int, default=10)
+    ap.add_argument("--sweep-steps", type=int, default=18)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of a known size "
                          "(reference kernel for the HBM byte counters)")
@@ -786,7 +879,8 @@ def main():
         copy_calibration()
         return
     if args.ingest_counters:
-        ingest_counters(args.ingest_counters, args.workload, args.density)
+        ingest_counters(args.ingest_counters, args.workload, args.density,
+                        args.schedule)
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -797,8 +891,10 @@ def main():
 
     wl = workload(args.workload, args.density)
     net = wl["net"]
+    sched = default_schedule(wl, args.schedule)
     K, W, KP = args.steps, args.warmup, args.profile_steps
-    r = measure(wl, K, W, KP, args.thr, dense=not args.no_dense)
+    r = measure(wl, K, W, KP, args.thr, dense=not args.no_dense,
+                schedule=sched)
     res = {
         "metric": METRIC,
         "value": r.pop("value"),
@@ -809,17 +905,23 @@ def main():
         "dtype": net.dtype,
         "data": "synthetic (seeded temporally continuous video, "
                 "random-init weights)",
-        "config": {"workload": wl["desc"], "batch": net.batch, "H": net.H,
-                   "W": net.W, "C": net.C, "layers": len(net.layers),
+        "config": {"workload": r.pop("workload"), "batch": net.batch,
+                   "H": net.H, "W": net.W, "C": net.C,
+                   "layers": len(net.layers), "chunk": wl["chunk"],
+                   "schedule": sched,
                    "target_density": args.density,
                    "measured_input_density": r.pop("measured_input_density"),
                    "thr": "ibst" if wl["ibst"] else args.thr},
     }
     res.update(r)
+    if sched == "chunk" and not args.no_frame:
+        f = measure(wl, K, W, KP, args.thr, dense=False, schedule="frame")
+        res["frame_by_frame"] = {k: f[k] for k in FRAME_KEYS if k in f}
     res["kernel_source_hash"] = kernel_source_hash()
     if args.workload == "resnet50" and not args.no_sweep:
         res["density_sweep"] = density_sweep(
-            net, args.thr, [0.02, 0.05, 0.10, 0.20, 0.40], args.sweep_steps)
+            net, args.thr, [0.02, 0.05, 0.10, 0.20, 0.40], args.sweep_steps,
+            wl["chunk"], sched)
     if args.workload == "resnet50" and not args.no_extra:
         res["other_workloads"] = {
             "effnet_b0": extra_workload("effnet_b0", 14, 7),
