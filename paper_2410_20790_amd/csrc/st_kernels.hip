@@ -140,15 +140,21 @@ __device__ __forceinline__ unsigned block_exclusive_scan(unsigned v,
 
 // cnts: `per_tile` counts per tile (1 = per-tile counts, tile/64 = counts of
 // 64-item groups).  Each thread owns `tile / 256` consecutive items of the
-// tile, evaluates all of them before emitting, and emits in item order.
-// The predicate's item data (P::Item, from P::load) is requested together
-// with the item count and the counts before the tile -- all loads stay
-// within the capacity `cap`, and which items are real is decided once the
-// count has arrived -- so a block waits for one round of loads, not three.
-// With IPT > 0 (items per thread known at compile time) the items are kept
-// in registers from load to emit.  pred.emit returns a work count that is
-// summed over the block and handed to pred.block_done; pred.finish
-// receives the total.
+// tile and evaluates them; one block scan gives every kept item its
+// position.  The predicate's item data (P::Item, from P::load) is requested
+// together with the item count and the counts before the tile -- all loads
+// stay within the capacity `cap`, and which items are real is decided once
+// the count has arrived -- so a block waits for one round of loads, not
+// three.  With IPT > 0 (items per thread known at compile time) the items
+// are kept in registers until the keep decision.  Dropped items are handed
+// to pred.drop by their owner; the kept ones are listed in LDS in position
+// order and emitted by the whole block, consecutive threads taking
+// consecutive positions, so every lane of a wave runs an emit (emits are
+// the expensive part: rows gathered, windows marked, neighbour tables
+// built) and their stores are contiguous.  pred.emit re-loads its item
+// (predicates whose emit ignores the item let the compiler drop that
+// load); it returns a work count that is summed over the block and handed
+// to pred.block_done; pred.finish receives the total.
 constexpr int kMaxItemsPerThread = 32;
 
 template <class P, int IPT>
@@ -157,6 +163,8 @@ __global__ __launch_bounds__(256) void k_compact_write(
     const uint32_t* cnts, int per_tile, u64* out_cnt, u64* out_cnt2,
     P pred) {
   using Item = typename P::Item;
+  // tile offsets of the kept items (tile <= kMaxItemsPerThread * 256)
+  __shared__ uint16_t kept[kMaxItemsPerThread * 256];
   const int64_t base = (int64_t)blockIdx.x * tile;
   const int64_t n_req = read_count(n_dev, n_host);
   unsigned off = 0;
@@ -198,20 +206,24 @@ __global__ __launch_bounds__(256) void k_compact_write(
   }
   off = block_sum(off);
   unsigned tile_total = 0;
-  unsigned pos = off + block_exclusive_scan(mine, &tile_total);
-  unsigned work = 0;
+  unsigned lp = block_exclusive_scan(mine, &tile_total);
   for (int j = 0; j < ipt; ++j) {
     const int64_t i = first + j;
     if (i >= end) break;
-    Item x;
-    if constexpr (IPT > 0)
-      x = it[j < IPT ? j : 0];
-    else
-      x = pred.load(i);
-    if (keepbits & (1u << j))
-      work += pred.emit(i, pos++, x);
-    else
-      pred.drop(i, x);
+    if (keepbits & (1u << j)) {
+      kept[lp++] = (uint16_t)(i - base);
+    } else {
+      if constexpr (IPT > 0)
+        pred.drop(i, it[j < IPT ? j : 0]);
+      else
+        pred.drop(i, pred.load(i));
+    }
+  }
+  __syncthreads();
+  unsigned work = 0;
+  for (unsigned k = threadIdx.x; k < tile_total; k += 256) {
+    const int64_t i = base + kept[k];
+    work += pred.emit(i, off + k, pred.load(i));
   }
   work = block_sum(work);
   if (threadIdx.x == 0) {
