@@ -240,7 +240,7 @@ enum {
   ST_K_POOL_MARK, ST_K_POOL_COUNT, ST_K_POOL_COMPACT, ST_K_POOL_EMIT,
   ST_K_COMMIT, ST_K_LIST_COUNT, ST_K_LIST_COMPACT, ST_K_OUTPUT,
   ST_K_CLEANUP, ST_K_RESET, ST_K_SE_SQUEEZE, ST_K_SE_EXCITE, ST_K_SE_EMIT,
-  ST_K_CONV_SPLIT_EPI, ST_K_CHUNK_UPDATE, ST_K_NUM_CLASSES
+  ST_K_CONV_SPLIT_EPI, ST_K_CHUNK_UPDATE, ST_K_RUN_TILES, ST_K_NUM_CLASSES
 };
 
 /* Start recording: room for `max_launches` launch records and

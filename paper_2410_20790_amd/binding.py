@@ -26,7 +26,7 @@ KERNEL_CLASSES = [
     "rb_nbr", "rb_ident", "conv_gemm", "conv_dw", "pool_mark", "pool_count",
     "pool_compact", "pool_emit", "commit", "list_count", "list_compact",
     "output", "cleanup", "reset", "se_squeeze", "se_excite", "se_emit",
-    "conv_split_epi", "chunk_update",
+    "conv_split_epi", "chunk_update", "run_tiles",
 ]
 
 EXPORTED = [

@@ -367,6 +367,14 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
   u64* cpairs = cnt + L.cnt_pairs;
   uint32_t* rowmax_out = ws.at<uint32_t>(outT.off_rowmax);
   uint32_t* rm_O = L.pool ? nullptr : rowmax_out;
+  // Stateful layers whose every output row is finished by the GEMM tile
+  // that computes it apply the chunk's updates in the GEMM epilogue (rows
+  // come site-major, tiles are aligned to site runs); pooled and
+  // depthwise layers, layers with a split reduction and the output layer
+  // (which also writes every frame's dense output) defer them to the
+  // update kernel.
+  const bool fused = L.stateful && !L.pool && !L.dw && !out &&
+                     L.split_max <= 1;
 
   if (!L.ident) {
     FlagArgs fa{};
@@ -382,8 +390,13 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
     fa.g = conv_geo(L);
     fa.pairs = cpairs;
     fa.cnt = cO;
+    fa.nf = nf;
+    fa.per = L.conv_grid;
     launch_flag_compact(pf, ST_K_RB_COUNT, ST_K_RB_COMPACT, s, fa);
   }
+  uint32_t* tstart = ws.at<uint32_t>(net->off_chunk_tstart);
+  if (fused)
+    launch_run_tiles(pf, s, O, cO, citems, L.conv_grid, nf, tstart);
 
   ConvArgs a{};
   a.din = ws.at<char>(in.off_rows);
@@ -398,7 +411,15 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
   a.O = O;
   a.nO = cO;
   a.capO = citems;
-  if (L.stateful) {
+  if (fused) {
+    a.mode = kModeChunkState;
+    a.P = ws.at<float>(L.off_P);
+    a.dout = ws.at<char>(outT.off_rows);
+    a.rowmax = rowmax_out;
+    a.tstart = tstart;
+    a.nf = nf;
+    a.per = L.conv_grid;
+  } else if (L.stateful) {
     // every frame's update is deferred; the frame loop applies them
     a.mode = kModeDefer;
     a.dP = cdp;
@@ -425,7 +446,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
   else if (!launch_conv_gemm(pf, s, net->dtype, a))
     return false;
 
-  if (L.stateful) {
+  if (L.stateful && !fused) {
     ChunkUpdArgs u{};
     u.P = ws.at<float>(L.off_P);
     u.dP = cdp;
@@ -455,6 +476,8 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
     fp.map = ws.at<int>(outT.off_map);
     fp.rowmax = rowmax_out;
     fp.cnt = cnt + outT.cnt_rows;
+    fp.nf = nf;
+    fp.per = outT.grid;
     launch_flag_compact(pf, ST_K_POOL_COUNT, ST_K_POOL_COMPACT, s, fp);
     ChunkPoolArgs pa{};
     pa.Q = ws.at<int>(outT.off_rowpix);
@@ -730,7 +753,7 @@ extern "C" st_status st_layer_density(st_net* net, int32_t layer,
   hipStream_t s = (hipStream_t)net->last_stream;
   u64* dens = ws.at<u64>(net->off_dens);
   launch_density(s, ws.at<int>(T.off_act), cnt + T.cnt_act,
-                 (int64_t)T.H * T.W, images, dens);
+                 T.grid * net->last_nf, (int64_t)T.H * T.W, images, dens);
   st = hip_check(net, "density");
   if (st != ST_OK) return st;
   st = sync_last(net);

@@ -10,6 +10,7 @@
 #include <vector>
 
 #include "../../include/sparsetem.h"
+#include "st_modes.h"
 
 namespace st {
 
@@ -76,7 +77,7 @@ struct LayerPlan {
   bool se = false;                  // squeeze-excitation after the act
   int se_mid = 0, se_chunk = 0, se_nchunk = 0, se_tps = 0;
   int se_par = 0;                   // which gate buffer holds the last gates
-  int mode = 0;                     // epilogue mode (kModeState/Defer/Linear)
+  int mode = 0;                     // epilogue mode (kMode*, st_kernels.h)
   int split_max = 1;                // most reduction splits per output tile
   // workspace offsets
   size_t off_P = 0;                 // f32 [conv_grid][cout_p]
@@ -94,8 +95,6 @@ struct LayerPlan {
   size_t off_pflags = 0;            // uint8 [pooled grid] (pooled layers)
   int cnt_O = 0, cnt_pairs = 0;
 };
-
-enum { kModeState = 0, kModeDefer = 1, kModeLinear = 2 };
 
 struct Recorder;  // executor-side profiling state
 
@@ -122,6 +121,7 @@ struct st_net {
   // the frames that updated it (bit mask)
   size_t off_chunk_dp = 0, off_chunk_base = 0, off_chunk_last = 0;
   size_t off_chunk_aff = 0;
+  size_t off_chunk_tstart = 0;      // uint32 run-aligned row tiles
   size_t off_cnt = 0;                      // uint64 [n_counters]
   size_t off_cleanup = 0;                  // cleanup descriptor table
   size_t off_dens = 0;                     // uint64 [batch] per-image counts

@@ -8,6 +8,8 @@
 
 #include <cstdint>
 
+#include "st_modes.h"
+
 namespace st {
 
 struct Geo {  // sliding-window geometry from an input grid to an output grid
@@ -90,11 +92,22 @@ struct FlagArgs {
   Geo g;
   u64* pairs;
   u64* cnt;
+  // chunk mode: nf frames of `per` sites each (item = frame * per + site);
+  // items are compacted site-major (a site's frames adjacent, in frame
+  // order).  nf <= 1: item order.
+  int nf;
+  int64_t per;
 };
 void launch_flag_compact(const Prof& pf, int cls_count, int cls_write,
                          hipStream_t s, const FlagArgs& a);
 void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
                  const u64* n_list, int64_t max_items, Geo g, uint8_t* flags);
+// Run-aligned row tiles of a site-major affected list O (chunk mode):
+// tstart[j] = first row of the run (same site) holding row j * step, for
+// j < ceil(nO / step), and tstart[ceil(nO / step)] = nO.
+void launch_run_tiles(const Prof& pf, hipStream_t s, const int* O,
+                      const u64* nO, int64_t capO, int64_t per, int nf,
+                      uint32_t* tstart);
 
 // ---- (c)+(d) delta convolution with the fused state update / emission
 struct ConvArgs {
@@ -124,6 +137,11 @@ struct ConvArgs {
   // tiles in part [split][capO][cout_p]; split_max = 1: no split
   float* part;
   int split_max;
+  // kModeChunkState: row tile j is [tstart[j], tstart[j + 1]) (tiles step
+  // chunk_tile_step(nf) rows); a row's site is its item modulo `per`
+  const uint32_t* tstart;
+  int nf;
+  int64_t per;
 };
 // Returns false (and launches nothing) when a.zero is missing or misaligned.
 bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
@@ -269,7 +287,8 @@ void launch_repack_dw(hipStream_t s, int dtype, const void* w, float* wdw,
                       int c, int kh, int kw, int cp);
 void launch_bias(hipStream_t s, int dtype, const void* b, float* out,
                  int cout, int cout_p);
+// Kept rows per image of a kept list (any order); cap bounds its length.
 void launch_density(hipStream_t s, const int* act, const u64* n_act,
-                    int64_t hw, int batch, u64* out);
+                    int64_t cap, int64_t hw, int images, u64* out);
 
 }  // namespace st

@@ -437,6 +437,57 @@ void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
   prof_end(pf, cls, s);
 }
 
+// Run-aligned row tiles (chunk mode): the run holding row x starts at most
+// nf - 1 rows earlier; the nf - 1 preceding entries are loaded at once and
+// the run is the unbroken stretch of the same site ending at x.
+__global__ __launch_bounds__(256) void k_run_tiles(const int* O,
+                                                   const u64* nOp,
+                                                   int64_t per, int nf,
+                                                   uint32_t* tstart) {
+  const int64_t nO = (int64_t)*nOp;
+  const int step = chunk_tile_step(nf);
+  const int64_t nt = (nO + step - 1) / step;
+  for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j <= nt;
+       j += (int64_t)gridDim.x * 256) {
+    int64_t r = nO;
+    if (j < nt) {
+      const int64_t x = j * step;
+      const unsigned pu = (unsigned)per;
+      const unsigned site = (unsigned)O[x] % pu;
+      int len = 1;
+      bool alive = true;
+      for (int q = 1; q < nf; ++q) {
+        const int64_t y = x - q;
+        const bool same = y >= 0 && (unsigned)O[y < 0 ? 0 : y] % pu == site;
+        alive = alive && same;
+        len += alive ? 1 : 0;
+      }
+      r = x - len + 1;
+    }
+    tstart[j] = (uint32_t)r;
+  }
+}
+
+void launch_run_tiles(const Prof& pf, hipStream_t s, const int* O,
+                      const u64* nO, int64_t capO, int64_t per, int nf,
+                      uint32_t* tstart) {
+  const int64_t cap_t = capO / chunk_tile_step(nf) + 2;
+  prof_begin(pf, 24 /*ST_K_RUN_TILES*/, s);
+  k_run_tiles<<<grid_for(cap_t), 256, 0, s>>>(O, nO, per, nf, tstart);
+  prof_end(pf, 24, s);
+}
+
+// Compaction order of chunk-mode items (item = frame * per + site): the
+// j-th item visited is site j / nf, frame j % nf, so a site's frames come
+// out adjacent and in frame order.  nf <= 1: item order.
+__device__ __forceinline__ int64_t site_major(int64_t j, int nf,
+                                              int64_t per) {
+  if (nf <= 1) return j;
+  // items stay below 2^31 (grids times frames are bounded at plan time)
+  const unsigned jj = (unsigned)j, site = jj / (unsigned)nf;
+  return (int64_t)(jj - site * (unsigned)nf) * per + site;
+}
+
 // Affected-output compaction.  With `nbr` set, each emitted output also gets
 // its output-major neighbour entries nbr[k][o] = row of the input delta at
 // the site offset k reads (or -1: padding or inactive site), and the block
@@ -451,13 +502,20 @@ struct FlagPred {
   int64_t stride;
   Geo g;  // conv geometry: input grid -> this (output) grid
   u64* pairs;
+  int nf;
+  int64_t per;
   struct Item {
     uint8_t f;
   };
-  __device__ bool count(int64_t i) const { return flags[i] != 0; }
-  __device__ Item load(int64_t i) const { return Item{flags[i]}; }
+  __device__ bool count(int64_t j) const {
+    return flags[site_major(j, nf, per)] != 0;
+  }
+  __device__ Item load(int64_t j) const {
+    return Item{flags[site_major(j, nf, per)]};
+  }
   __device__ bool keep(const Item& it) const { return it.f != 0; }
-  __device__ unsigned emit(int64_t i, unsigned pos, const Item&) const {
+  __device__ unsigned emit(int64_t j, unsigned pos, const Item&) const {
+    const int64_t i = site_major(j, nf, per);
     list[pos] = (int)i;
     map[i] = (int)pos;
     flags[i] = 0;
@@ -502,7 +560,7 @@ struct FlagPred {
 void launch_flag_compact(const Prof& pf, int cls_count, int cls_write,
                          hipStream_t s, const FlagArgs& a) {
   FlagPred p{a.flags, a.list, a.map, a.rowmax, a.nbr, a.map_in, a.stride,
-             a.g, a.pairs};
+             a.g, a.pairs, a.nf, a.per};
   run_compact(pf, cls_count, cls_write, s, nullptr, a.npix, a.npix, a.tiles,
               a.cnt, nullptr, p);
 }
@@ -724,7 +782,7 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
                                             const bool (&hv)[2], int64_t eo,
                                             bool eok, int epix, int64_t m0,
                                             int n0, int ec, int tiles_n,
-                                            int64_t nO, int* s_last) {
+                                            int64_t m_end, int* s_last) {
   constexpr int BM = kGemmBM;
   const int tid = threadIdx.x;
   const int cout_p = a.cout_p;
@@ -785,7 +843,7 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
     if (*s_last && tid < 64) {
       const int64_t o = m0 + tid;
       bool k = false;
-      if (o < nO)
+      if (o < m_end)
         k = __uint_as_float(__hip_atomic_load(a.rowmax + o, __ATOMIC_RELAXED,
                                               __HIP_MEMORY_SCOPE_AGENT)) >
             a.keep_thr;
@@ -799,12 +857,171 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
   }
 }
 
+// Four channels of a delta row stored in the storage type; returns the
+// largest magnitude of the rounded values.
+template <typename T>
+__device__ __forceinline__ float store4(T* p, const float* f) {
+  float m = 0.f;
+  if constexpr (sizeof(T) == 4) {
+    *(float4*)p = make_float4(f[0], f[1], f[2], f[3]);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(f[e]));
+  } else {
+    uint2 v;
+    T* h = (T*)&v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      h[e] = from_f<T>(f[e]);
+      m = fmaxf(m, fabsf(to_f(h[e])));
+    }
+    *(uint2*)p = v;
+  }
+  return m;
+}
+
+// Chunk-state epilogue, for CPT columns per thread (64 / CPT threads per
+// run, adjacent lanes).  The runs' states and the rows' residual deltas are
+// requested together; the residual deltas are added into Cs (four threads
+// per row, 16 columns each); then each run's threads apply its frames in
+// order from LDS -- P_t = P_{t-1} + update, emit f(P_t) - f(P_{t-1}) and
+// the row maximum (device atomics, one per row and column tile) -- and
+// store the state once.
+template <typename T, int CPT>
+__device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
+                                                int cld, const int* s_run,
+                                                int nruns, int64_t m0,
+                                                int rows, int n0,
+                                                const int* s_site,
+                                                const int* s_rsk) {
+  constexpr int TPR = 64 / CPT, Q = CPT / 4;
+  const int tid = threadIdx.x;
+  const int cout_p = a.cout_p;
+  T* dout = (T*)a.dout;
+  const T* dskip = (const T*)a.dskip;
+  // this thread's run and columns
+  const int g = tid / TPR, j = tid - (tid / TPR) * TPR;
+  const int c0 = n0 + j * CPT;
+  const bool run = g < nruns;
+  const int64_t site = run ? s_site[s_run[g]] : 0;
+  float P[CPT];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (run && c0 + 4 * q < cout_p)
+      v = *(const float4*)(a.P + site * cout_p + c0 + 4 * q);
+    P[4 * q] = v.x;
+    P[4 * q + 1] = v.y;
+    P[4 * q + 2] = v.z;
+    P[4 * q + 3] = v.w;
+  }
+  // residual rows: four threads per row, 16 columns each, kept in their
+  // storage type until added
+  {
+    constexpr int SKV = (int)sizeof(T) / 2;  // 16-byte vectors / 8 channels
+    const int er = tid >> 2, ec = (tid & 3) * 16;
+    const int rsk = er < rows ? s_rsk[er] : -1;
+    uint4 sk[2][SKV];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int c = n0 + ec + 8 * h;
+#pragma unroll
+      for (int v = 0; v < SKV; ++v)
+        sk[h][v] =
+            (rsk >= 0 && c < cout_p)
+                ? ((const uint4*)(dskip + (int64_t)rsk * cout_p + c))[v]
+                : make_uint4(0u, 0u, 0u, 0u);
+    }
+    if (rsk >= 0) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        float f[8];
+        Vec8<T>::load((const T*)sk[h], f);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) Cs[er * cld + ec + 8 * h + e] += f[e];
+      }
+    }
+  }
+  __syncthreads();
+  if (!run) return;
+  const int r0 = s_run[g], r1 = s_run[g + 1];
+  for (int r = r0; r < r1; ++r) {
+    float rm = 0.f;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      if (c0 + 4 * q >= cout_p) continue;
+      const float4 u = *(const float4*)(Cs + r * cld + (c0 - n0) + 4 * q);
+      const float uv[4] = {u.x, u.y, u.z, u.w};
+      float d[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float po = P[4 * q + e], pn = po + uv[e];
+        d[e] = act_f(pn, a.act) - act_f(po, a.act);
+        P[4 * q + e] = pn;
+      }
+      rm = fmaxf(rm, store4<T>(dout + (m0 + r) * cout_p + c0 + 4 * q, d));
+    }
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) rm = fmaxf(rm, __shfl_xor(rm, o, 64));
+    if (j == 0 && rm > 0.f) atomicMax(a.rowmax + m0 + r, __float_as_uint(rm));
+  }
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+    if (c0 + 4 * q < cout_p)
+      *(float4*)(a.P + site * cout_p + c0 + 4 * q) =
+          make_float4(P[4 * q], P[4 * q + 1], P[4 * q + 2], P[4 * q + 3]);
+}
+
+// Chunk-state epilogue: the tile's rows [m0, m0 + rows) are whole site
+// runs (a site's frames, in frame order), its f32 accumulators in Cs (row
+// stride cld), the rows' sites and residual rows in s_site / s_rsk.  The
+// runs are listed, then each run gets 4, 8 or 16 threads (16, 8 or 4
+// columns each) -- as many as the tile's run count leaves -- so that long
+// runs (sites that changed in most frames) still keep the block busy.
+// Every thread of the block must call it.
+template <typename T>
+__device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
+                                                  float* Cs, int cld,
+                                                  int* s_run, int64_t m0,
+                                                  int rows, int n0,
+                                                  const int* s_site,
+                                                  const int* s_rsk) {
+  constexpr int BM = kGemmBM;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // run starts: s_run[0..nruns) (wave 0 lists them), s_run[nruns] = rows,
+  // s_run[BM + 1] = nruns
+  if (wave == 0) {
+    const bool first =
+        lane < rows && (lane == 0 || s_site[lane] != s_site[lane - 1]);
+    const u64 starts = __ballot(first);
+    const int nr = __popcll(starts);
+    if (first) s_run[lane_prefix(starts)] = lane;
+    if (lane == 0) {
+      s_run[nr] = rows;
+      s_run[BM + 1] = nr;
+    }
+  }
+  __syncthreads();
+  const int nruns = s_run[BM + 1];
+  if (nruns > 32)
+    chunk_tile_runs<T, 16>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
+                           s_rsk);
+  else if (nruns > 16)
+    chunk_tile_runs<T, 8>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
+                          s_rsk);
+  else
+    chunk_tile_runs<T, 4>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
+                          s_rsk);
+}
+
 // SPLIT: the layer's reduction may be split (split_max > 1); every unit
 // then writes its partial tile (even when this frame needs one split) and
 // the split epilogue finishes the tiles, so no epilogue state is held
 // through the reduction.
+// Four waves per SIMD (the persistent grid holds four blocks per CU):
+// the register budget is fixed at that occupancy.
 template <typename T, bool REF, bool ALIGNED, bool SPLIT>
-__global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
+void k_conv_gemm(ConvArgs a) {
   constexpr int BM = kGemmBM, BN = kGemmBN;
   constexpr int KC = MmaCfg<T>::KC, LD = MmaCfg<T>::LD;
   constexpr int VEC = 16 / (int)sizeof(T);
@@ -817,6 +1034,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   __shared__ __align__(16) char smem[AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES];
   __shared__ u64 s_kmask;
   __shared__ int s_last;
+  __shared__ int s_site[BM], s_rsk[BM], s_run[BM + 2];
   extern __shared__ int s_nbr[];          // [K][BM]
   // LDS carve-up: A[2][BM][LD], B[2][BN][LD]; the f32 accumulator tile of
   // the epilogue reuses the same bytes
@@ -832,7 +1050,10 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
   const int wm = wave >> 1, wn = wave & 1;
   const int l16 = lane & 15, lg = lane >> 4;
   const int64_t nO = (int64_t)*a.nO;
-  const int64_t tiles_m = (nO + BM - 1) / BM;
+  // row tiles: 64 rows each, or (chunk-state mode) aligned to site runs
+  const bool runs = a.tstart != nullptr;
+  const int rstep = runs ? chunk_tile_step(a.nf) : BM;
+  const int64_t tiles_m = (nO + rstep - 1) / rstep;
   const int tiles_n = (a.cout_p + BN - 1) / BN;
   const int64_t ntiles = tiles_m * tiles_n;
   const int K = a.K, cin_p = a.cin_p, cout_p = a.cout_p;
@@ -865,7 +1086,8 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     const int st_lo = SPLIT ? (int)((int64_t)sp * nst / S) : 0;
     const int st_hi = SPLIT ? (int)((int64_t)(sp + 1) * nst / S) : nst;
     const int tm_i = (int)((unsigned)t / (unsigned)tiles_n);
-    const int64_t m0 = (int64_t)tm_i * BM;
+    const int64_t m0 = runs ? (int64_t)a.tstart[tm_i] : (int64_t)tm_i * BM;
+    const int64_t m1 = runs ? (int64_t)a.tstart[tm_i + 1] : min(m0 + BM, nO);
     const int n0 = (t - tm_i * tiles_n) * BN;
 
     __syncthreads();  // previous tile's LDS reads are complete
@@ -873,14 +1095,14 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     // this thread's epilogue row; its old state and residual are fetched
     // now so that they arrive while the reduction runs
     const int64_t eo = m0 + em;
-    const bool eok = eo < nO;
+    const bool eok = eo < m1;
     const int epix = eok ? a.O[eo] : 0;
     __syncthreads();
     u64 my = 0ull;
     for (int e = tid; e < BM * K; e += 256) {
       const int k = e / BM, m = e - (e / BM) * BM;
       const int64_t o = m0 + m;
-      const int src = o < nO ? a.nbr[(int64_t)k * a.stride + o] : -1;
+      const int src = o < m1 ? a.nbr[(int64_t)k * a.stride + o] : -1;
       s_nbr[e] = src;
       if (src >= 0) my |= 1ull << k;
     }
@@ -1083,6 +1305,12 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
     // each thread finishes 16 contiguous columns of one row: full-width
     // state loads/stores and 16-byte delta stores.  MFMA 16x16 block
     // layout: D[row = 4*lg + r][col = l16].
+    // this thread's output row's residual row
+    const int rsk = (!SPLIT && a.mskip && eok) ? a.mskip[epix] : -1;
+    if (a.mode == kModeChunkState && (tid & 3) == 0) {
+      s_site[em] = eok ? (int)((unsigned)epix % (unsigned)a.per) : -1;
+      s_rsk[em] = rsk;
+    }
     __syncthreads();  // every wave is done reading the staged tiles
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -1105,8 +1333,10 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
                     8 * h,
                 v);
       }
+    } else if (a.mode == kModeChunkState) {
+      finish_chunk_tile<T>(a, Cs, CLD, s_run, m0, (int)(m1 - m0), n0,
+                           s_site, s_rsk);
     } else {
-      const int rsk = (a.mskip && eok) ? a.mskip[epix] : -1;
       finish_tile<T, REF>(
           a, [&](int h, float* v) { load8f(crow + 8 * h, v); },
           [&](int h, float* po) {
@@ -1126,7 +1356,7 @@ __global__ __launch_bounds__(256) void k_conv_gemm(ConvArgs a) {
               for (int e = 0; e < 8; ++e) sk[e] = 0.f;
             }
           },
-          hv, eo, eok, epix, m0, n0, ec, tiles_n, nO, &s_last);
+          hv, eo, eok, epix, m0, n0, ec, tiles_n, m1, &s_last);
     }
   }
 }
@@ -1232,7 +1462,13 @@ bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
   // inactive lanes read the zero vector: never launch without it
   if (!a.zero || ((uintptr_t)a.zero & 15)) return false;
   if (a.split_max > 1 && !a.part) return false;
-  const int64_t worst = ((a.capO + kGemmBM - 1) / kGemmBM) *
+  // run-aligned tiles belong to the chunk-state epilogue, which finishes
+  // whole tiles itself (no split)
+  if ((a.tstart != nullptr) != (a.mode == kModeChunkState)) return false;
+  if (a.tstart && (a.split_max > 1 || a.nf < 1 || a.nf > 32 || a.per < 1))
+    return false;
+  const int rstep = a.tstart ? chunk_tile_step(a.nf) : kGemmBM;
+  const int64_t worst = ((a.capO + rstep - 1) / rstep) *
                         ((a.cout_p + kGemmBN - 1) / kGemmBN);
   // persistent blocks: about what the 256 CUs hold at once
   const int64_t units = worst * (a.split_max > 1 ? a.split_max : 1);
@@ -1789,17 +2025,23 @@ struct ChunkScanPred {
   int* rowpix;
   int* act;
   int* map;
-  int C, Cp;
+  int C, Cp, nf;
   int64_t npix;
   ConsList cons;
   struct Item {
     uint8_t k;
   };
-  __device__ bool count(int64_t i) const { return keepb[i] != 0; }
-  __device__ Item load(int64_t i) const { return Item{keepb[i]}; }
+  // items are visited site-major (a site's kept frames adjacent)
+  __device__ bool count(int64_t j) const {
+    return keepb[site_major(j, nf, npix)] != 0;
+  }
+  __device__ Item load(int64_t j) const {
+    return Item{keepb[site_major(j, nf, npix)]};
+  }
   __device__ bool keep(const Item& it) const { return it.k != 0; }
   // delta against the value X_hat held when frame t arrived
-  __device__ unsigned emit(int64_t i, unsigned pos, const Item&) const {
+  __device__ unsigned emit(int64_t j, unsigned pos, const Item&) const {
+    const int64_t i = site_major(j, nf, npix);
     const int64_t p = i % npix;
     const uint8_t b = base[i];
     const T* xt = x + i * C;
@@ -1839,8 +2081,8 @@ static void chunk_scan_t(const Prof& pf, hipStream_t s,
   k_chunk_scan_prep<T><<<grid_for(a.npix, 4096), 256, 0, s>>>(a);
   prof_end(pf, 0, s);
   ChunkScanPred<T> p{(const T*)a.x, (const T*)a.xhat, a.keep, a.base,
-                     (T*)a.rows, a.rowpix, a.act, a.map, a.C, a.Cp, a.npix,
-                     a.cons};
+                     (T*)a.rows, a.rowpix, a.act, a.map, a.C, a.Cp, a.nf,
+                     a.npix, a.cons};
   const int64_t items = (int64_t)a.nf * a.npix;
   run_compact(pf, 0 /*ST_K_SCAN_MASK*/, 1 /*ST_K_SCAN_COMPACT*/, s, nullptr,
               items, items, a.tiles, a.cnt_rows, a.cnt_act, p);
@@ -2268,25 +2510,40 @@ void launch_bias(hipStream_t s, int dtype, const void* b, float* out,
 
 // Per-image kept counts of an ascending pixel list (binary search of the
 // image boundaries).
-__global__ void k_density(const int* act, const u64* n_act, int64_t hw,
-                          int batch, u64* out) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= batch) return;
+// Kept rows per image (image = item / hw) of a kept list in any order: a
+// per-block histogram in LDS (up to kDensityLdsImages images; beyond that,
+// device atomics directly), added to `out` (zeroed first).
+constexpr int kDensityLdsImages = 4096;
+
+__global__ __launch_bounds__(256) void k_density(const int* act,
+                                                 const u64* n_act,
+                                                 int64_t hw, int images,
+                                                 u64* out) {
+  __shared__ unsigned h[kDensityLdsImages];
+  const bool lds = images <= kDensityLdsImages;
+  if (lds)
+    for (int b = threadIdx.x; b < images; b += 256) h[b] = 0u;
+  __syncthreads();
   const int64_t n = (int64_t)*n_act;
-  auto lower = [&](int64_t key) {
-    int64_t lo = 0, hi = n;
-    while (lo < hi) {
-      const int64_t mid = (lo + hi) / 2;
-      if ((int64_t)act[mid] < key) lo = mid + 1; else hi = mid;
-    }
-    return lo;
-  };
-  out[b] = (u64)(lower((int64_t)(b + 1) * hw) - lower((int64_t)b * hw));
+  for (int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x; r < n;
+       r += (int64_t)gridDim.x * 256) {
+    const int b = (int)((int64_t)act[r] / hw);
+    if (lds)
+      atomicAdd(&h[b], 1u);
+    else
+      atomicAdd(out + b, (u64)1);
+  }
+  __syncthreads();
+  if (lds)
+    for (int b = threadIdx.x; b < images; b += 256)
+      if (h[b]) atomicAdd(out + b, (u64)h[b]);
 }
 
 void launch_density(hipStream_t s, const int* act, const u64* n_act,
-                    int64_t hw, int batch, u64* out) {
-  k_density<<<(batch + 63) / 64, 64, 0, s>>>(act, n_act, hw, batch, out);
+                    int64_t cap, int64_t hw, int images, u64* out) {
+  launch_fill_u32(s, out, 2 * (int64_t)images, 0u);
+  k_density<<<grid_for(cap, 1024), 256, 0, s>>>(act, n_act, hw, images,
+                                                 out);
 }
 
 }  // namespace st

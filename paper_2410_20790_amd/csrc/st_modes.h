@@ -1,0 +1,19 @@
+// Epilogue modes of the convolution kernels and the chunk-mode row tiling,
+// shared by the planner, the executor and the kernels.
+#pragma once
+
+namespace st {
+
+// State: P += dP in place, emit f(P_new) - f(P_old).  Defer: write the f32
+// update rows (applied later).  Linear: emit dP itself.  ChunkState (chunk
+// mode, rows grouped by site in frame order, tiles aligned to those runs):
+// walk each site's frames in order with the state in registers and emit
+// every frame's f(P_t) - f(P_{t-1}).
+enum { kModeState = 0, kModeDefer = 1, kModeLinear = 2, kModeChunkState = 3 };
+
+// Rows per tile step of the run-aligned tiling: a tile starts at the first
+// row of the site run that holds row j * step, so with runs of at most nf
+// rows (nf <= 32) no tile exceeds 64 rows and none is empty.
+constexpr int chunk_tile_step(int nf) { return 65 - nf; }
+
+}  // namespace st
