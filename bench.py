@@ -96,17 +96,21 @@ def conv_launch_bytes(L, c, es, mode):
     """Algorithmic HBM bytes of one conv launch (gather-GEMM or depthwise)
     with fused epilogue, from the frame's counters
     c = (affected outputs, pairs, kept input rows, candidate rows, kept
-    rows, kept residual rows): every kept input row and the weights read
-    once, the neighbour table and output list read once, the f32 state read
-    and written and the delta written once per affected output row (or the
-    deferred f32 update written, for pooled layers), the residual rows read
-    once."""
-    nO, pairs, n_in, _, _, n_skip = (int(v) for v in c)
+    rows, kept residual rows, updated sites of a chunk): every kept input
+    row and the weights read once, the neighbour table and output list read
+    once, the f32 state read and written and the delta written once per
+    affected output row (or the deferred f32 update written, for pooled
+    layers; in a chunk's fused epilogue the delta written per row and the
+    state read and written once per site), the residual rows read once."""
+    nO, pairs, n_in, _, _, n_skip = (int(v) for v in c[:6])
+    sites = int(c[6]) if len(c) > 6 else 0
     K = L.k[0] * L.k[1]
     b = n_in * L.c_in * es + K * (L.c_in // L.groups) * L.c_out * es
     b += nO * (K + 1) * 4
     if mode == "state":
         b += nO * L.c_out * (4 + 4 + es)
+    elif mode == "fused":
+        b += nO * L.c_out * es + sites * L.c_out * (4 + 4)
     elif mode == "defer":
         b += nO * L.c_out * 4
     else:
@@ -489,10 +493,12 @@ def frames_needed(chunk, W, K, KP, KG=0):
 def kernel_table(net, recs, counts, es, chunk_mode=False):
     """Per kernel class: launches, time, algorithmic bytes / FLOPs from the
     frame's counters (see conv_launch_bytes).  In chunk mode a profiled
-    "frame" is one chunk (counters summed over its frames), every stateful
-    layer's GEMM writes its f32 update rows, and the chunk state update is
-    charged its update-row reads and delta writes (a lower bound: its f32
-    state reads and writes, once per site, are not counted)."""
+    "frame" is one chunk (counters summed over its frames); a stateful
+    layer whose GEMM epilogue applies the chunk's updates is charged its
+    delta rows and one state read and write per updated site, the others
+    write f32 update rows, and the chunk state update kernel is charged its
+    update-row reads and delta writes (a lower bound: its f32 state reads
+    and writes, once per site, are not counted)."""
     from paper_2410_20790_amd import binding as B
     classes = {}
     for r in recs:
@@ -508,7 +514,7 @@ def kernel_table(net, recs, counts, es, chunk_mode=False):
             L = net.layers[j]
             mode = layer_mode(net, j)
             if chunk_mode and mode == "state":
-                mode = "defer"
+                mode = "fused" if counts[f, j, 6] > 0 else "defer"
             c["bytes"] += conv_launch_bytes(L, counts[f, j], es, mode)
             c["flops"] += 2.0 * counts[f, j, 1] * (L.c_in // L.groups) * \
                 L.c_out

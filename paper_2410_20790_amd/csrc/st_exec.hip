@@ -396,7 +396,8 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
   }
   uint32_t* tstart = ws.at<uint32_t>(net->off_chunk_tstart);
   if (fused)
-    launch_run_tiles(pf, s, O, cO, citems, L.conv_grid, nf, tstart);
+    launch_run_tiles(pf, s, O, cO, citems, L.conv_grid, nf, tstart,
+                     cnt + L.cnt_sites);
 
   ConvArgs a{};
   a.din = ws.at<char>(in.off_rows);
@@ -964,7 +965,7 @@ extern "C" st_status st_profile_end(st_net* net, st_launch_record* recs,
         const LayerPlan& L = net->layers[j];
         const TensorPlan& in = net->tensors[L.d.src + 1];
         const TensorPlan& out = net->tensors[j + 1];
-        int64_t* q = counts + ((size_t)f * nl + j) * 6;
+        int64_t* q = counts + ((size_t)f * nl + j) * 7;
         q[0] = (int64_t)c[L.cnt_O];
         q[1] = (int64_t)c[L.cnt_pairs];
         q[2] = (int64_t)c[in.cnt_act];
@@ -973,6 +974,9 @@ extern "C" st_status st_profile_end(st_net* net, st_launch_record* recs,
         q[5] = L.d.residual_src == -2
                    ? 0
                    : (int64_t)c[net->tensors[L.d.residual_src + 1].cnt_act];
+        q[6] = 0;
+        for (int k = 0; k < kSiteSlots; ++k)
+          q[6] += (int64_t)c[L.cnt_sites + k];
       }
     }
   return ST_OK;

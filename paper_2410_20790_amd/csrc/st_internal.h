@@ -94,6 +94,8 @@ struct LayerPlan {
   size_t off_flags = 0;             // uint8 [conv_grid] affected-output flags
   size_t off_pflags = 0;            // uint8 [pooled grid] (pooled layers)
   int cnt_O = 0, cnt_pairs = 0;
+  int cnt_sites = 0;                // chunk mode: sites whose state a fused
+                                    // GEMM updated (site runs)
 };
 
 struct Recorder;  // executor-side profiling state

@@ -104,10 +104,11 @@ void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
                  const u64* n_list, int64_t max_items, Geo g, uint8_t* flags);
 // Run-aligned row tiles of a site-major affected list O (chunk mode):
 // tstart[j] = first row of the run (same site) holding row j * step, for
-// j < ceil(nO / step), and tstart[ceil(nO / step)] = nO.
+// j < ceil(nO / step), and tstart[ceil(nO / step)] = nO; the number of runs
+// (distinct sites) is added to sites[0 .. kSiteSlots) (partial counts).
 void launch_run_tiles(const Prof& pf, hipStream_t s, const int* O,
                       const u64* nO, int64_t capO, int64_t per, int nf,
-                      uint32_t* tstart);
+                      uint32_t* tstart, u64* sites);
 
 // ---- (c)+(d) delta convolution with the fused state update / emission
 struct ConvArgs {

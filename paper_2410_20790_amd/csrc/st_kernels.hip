@@ -439,20 +439,34 @@ void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
 
 // Run-aligned row tiles (chunk mode): the run holding row x starts at most
 // nf - 1 rows earlier; the nf - 1 preceding entries are loaded at once and
-// the run is the unbroken stretch of the same site ending at x.
+// the run is the unbroken stretch of the same site ending at x.  Also
+// counts the runs (distinct sites) into *sites.
 __global__ __launch_bounds__(256) void k_run_tiles(const int* O,
                                                    const u64* nOp,
                                                    int64_t per, int nf,
-                                                   uint32_t* tstart) {
+                                                   uint32_t* tstart,
+                                                   u64* sites) {
   const int64_t nO = (int64_t)*nOp;
   const int step = chunk_tile_step(nf);
   const int64_t nt = (nO + step - 1) / step;
+  const unsigned pu = (unsigned)per;
+  unsigned runs = 0;
+  for (int64_t base = (int64_t)blockIdx.x * 256; base < nO;
+       base += (int64_t)gridDim.x * 256) {
+    const int64_t r = base + threadIdx.x;
+    const bool first =
+        r < nO && (r == 0 || (unsigned)O[r] % pu != (unsigned)O[r - 1] % pu);
+    runs += __popcll(__ballot(first));
+  }
+  // one device atomic per block (every wave's lane 0 holds its count)
+  runs = block_sum((threadIdx.x & 63) == 0 ? runs : 0u);
+  if (threadIdx.x == 0 && runs)
+    atomicAdd(sites + blockIdx.x % kSiteSlots, (u64)runs);
   for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j <= nt;
        j += (int64_t)gridDim.x * 256) {
     int64_t r = nO;
     if (j < nt) {
       const int64_t x = j * step;
-      const unsigned pu = (unsigned)per;
       const unsigned site = (unsigned)O[x] % pu;
       int len = 1;
       bool alive = true;
@@ -470,10 +484,10 @@ __global__ __launch_bounds__(256) void k_run_tiles(const int* O,
 
 void launch_run_tiles(const Prof& pf, hipStream_t s, const int* O,
                       const u64* nO, int64_t capO, int64_t per, int nf,
-                      uint32_t* tstart) {
-  const int64_t cap_t = capO / chunk_tile_step(nf) + 2;
+                      uint32_t* tstart, u64* sites) {
   prof_begin(pf, 24 /*ST_K_RUN_TILES*/, s);
-  k_run_tiles<<<grid_for(cap_t), 256, 0, s>>>(O, nO, per, nf, tstart);
+  k_run_tiles<<<grid_for(capO, 512), 256, 0, s>>>(O, nO, per, nf, tstart,
+                                                   sites);
   prof_end(pf, 24, s);
 }
 

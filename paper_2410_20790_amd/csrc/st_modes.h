@@ -16,4 +16,8 @@ enum { kModeState = 0, kModeDefer = 1, kModeLinear = 2, kModeChunkState = 3 };
 // rows (nf <= 32) no tile exceeds 64 rows and none is empty.
 constexpr int chunk_tile_step(int nf) { return 65 - nf; }
 
+// Partial counters per layer for the sites a chunk's fused epilogue
+// updated (blocks add to slot blockIdx % kSiteSlots; the host sums them).
+constexpr int kSiteSlots = 8;
+
 }  // namespace st

@@ -180,7 +180,10 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
   // ---- workspace layout
   Alloc a;
   const int L_n = n_layers;
-  net->n_counters = 2 * (L_n + 1) + 2 * L_n;
+  // per tensor: candidate and kept rows; per layer: pairs, own affected
+  // list (pooled / SE layers), and kSiteSlots partial counts of the sites
+  // a chunk's fused epilogue updated
+  net->n_counters = 2 * (L_n + 1) + (2 + kSiteSlots) * L_n;
   net->off_cnt = a.take(sizeof(uint64_t) * net->n_counters);
   net->off_dens = a.take(sizeof(uint64_t) * batch * F);
   net->off_tiles = a.take(sizeof(uint32_t) * kMaxTiles);
@@ -209,6 +212,7 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
     TensorPlan& T = net->tensors[i + 1];
     const int64_t citems = L.conv_grid * F;
     L.cnt_pairs = 2 * (L_n + 1) + i;
+    L.cnt_sites = 2 * (L_n + 1) + 2 * L_n + kSiteSlots * i;
     max_grid = std::max(max_grid, citems);
     max_conv_phys = std::max(max_conv_phys, L.conv_grid);
     if (F > 1 && L.stateful)
