@@ -382,10 +382,11 @@ class Feed:
     the first frame when chunk is None), diff frames in between.  With
     `batch` > 1 (the SparseBatch schedule) the diff frames of a chunk are
     encoded up to `batch` at a time by one st_encode_chunk call, else one
-    st_encode_diff call per frame.  With a controller (frame schedule
-    only), each diff frame's thresholds come from it and its kept-row
-    counters are fed back after the frame (one host round trip per frame,
-    part of the timed work)."""
+    st_encode_diff call per frame.  ctl = "device": the thresholds are
+    adjusted on the device (st_encode_diff_adaptive, no host round trip);
+    ctl = a host controller: each diff frame's thresholds come from it and
+    its kept-row counters are fed back after the frame (one host round trip
+    per frame, part of the timed work)."""
 
     def __init__(self, g, n_layers, frames, chunk, thr, ctl, out, batch=1):
         from paper_2410_20790_amd import binding as B
@@ -396,6 +397,9 @@ class Feed:
         self.batch = batch
         if batch > 1 and ctl is not None:
             raise ValueError("the controller adjusts thresholds per frame")
+        self.device_ctl = ctl == "device"
+        if self.device_ctl:
+            self.ctl = None
         self.pos = 0
         self.L_n = n_layers
         self.grids = [int(np.prod(g.tensor_shape(t - 1)[:3]))
@@ -429,6 +433,8 @@ class Feed:
         thr = self.ctl.thresholds() if self.ctl else self.thr
         if self.replay is not None:
             self.replay(self.frames[self.pos])
+        elif self.device_ctl:
+            self.g.encode_diff_adaptive(self.frames[self.pos], out=self.out)
         else:
             self.g.encode_diff(self.frames[self.pos], thr, out=self.out)
         self.pos += 1
@@ -625,7 +631,7 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
     import torch
     from paper_2410_20790_amd import SparseTemNet
     from paper_2410_20790_amd import binding as B
-    from paper_2410_20790_amd.ibst import IBST, nonlinear_tensors
+    from paper_2410_20790_amd.ibst import nonlinear_tensors
     net = wl["net"]
     dt = net.dtype
     es = ESIZE[dt]
@@ -662,8 +668,11 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
     else:
         out = out0 = g.new_output()
     ctl = None
+    ctl_idx = nonlinear_tensors(net.layers)
     if wl["ibst"]:
-        ctl = IBST(L_n + 1, nonlinear_tensors(net.layers), target, eps)
+        # the online threshold adjustment runs on the device
+        g.set_threshold_control(ctl_idx, thr, target, eps, 1.0)
+        ctl = "device"
     feed = Feed(g, L_n, frames, chunk, thr, ctl, out, batch)
     dflops = dense_flops(net, [net_conv_grid(net, i) for i in range(L_n)])
 
@@ -673,7 +682,6 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
     # are synchronised around and excluded)
     s_ev = torch.cuda.Event(enable_timing=True)
     e_ev = torch.cuda.Event(enable_timing=True)
-    n_sp = len(feed.sparsity)
     torch.cuda.synchronize()
     s_ev.record()
     wall, refs = run_diffs(feed, K)
@@ -682,7 +690,6 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
     ms_step = wall * 1000.0 / K
     ev_ms = s_ev.elapsed_time(e_ev) / K if not refs else None
     dens0 = g.density(-1)
-    sp_timed = np.array(feed.sparsity[n_sp:]) if feed.sparsity else None
 
     # ---- profiled diff frames: an event pair around every launch
     if chunk:
@@ -720,6 +727,20 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
         kern[name] = e
     desc = f"{wl['desc']}-{schedule}"
     roof = roofline_of(classes, dt, desc)
+    # online adjustment: sparsity of every tensor in the profiled frames
+    # (their kept-row counters), thresholds after them
+    ibst_sp = ibst_thr = None
+    if ctl == "device":
+        ibst_thr = g.thresholds()
+        rows = []
+        for f in range(len(counts)):
+            kept = np.zeros(L_n + 1)
+            for j, L in enumerate(net.layers):
+                kept[j + 1] = counts[f, j, 4]
+                if L.src == -1:
+                    kept[0] = counts[f, j, 2]
+            rows.append(1.0 - kept / np.array(feed.grids, dtype=np.float64))
+        ibst_sp = np.array(rows)
     roof["event_pair_overhead_us"] = event_overhead_us()
 
     # ---- graph replay: the same diff frames' launch sequence captured once
@@ -777,20 +798,21 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
             "miopen": dense_ms["miopen_ms"] / ms_step,
             "own_dense": dense_ms["own_dense_ms"] / ms_step}
         res["dense_ms"] = dense_ms
-    if ctl is not None and sp_timed is not None and len(sp_timed):
-        c_idx = ctl.ctl
-        s_c = sp_timed[:, c_idx]
-        th = np.array(ctl.thresholds())[c_idx]
+    if ibst_sp is not None and len(ibst_sp):
+        s_c = ibst_sp[:, ctl_idx]
+        th = ibst_thr[ctl_idx]
         res["ibst"] = {
-            "target": target, "eps": eps, "theta_max": ctl.theta_max,
-            "controlled_tensors": len(c_idx),
+            "where": "device (st_encode_diff_adaptive)",
+            "target": target, "eps": eps, "theta_max": 1.0,
+            "controlled_tensors": len(ctl_idx),
+            "sample": f"the {len(ibst_sp)} event-instrumented diff frames",
             "mean_sparsity_controlled": float(s_c.mean()),
             "in_band_frac_last_frame": float(np.mean(
                 np.abs(s_c[-1] - target) <= eps)),
             "theta_last": {"min": float(th.min()),
                            "median": float(np.median(th)),
                            "max": float(th.max())},
-            "mean_input_sparsity": float(sp_timed[:, 0].mean())}
+            "mean_input_sparsity": float(ibst_sp[:, 0].mean())}
     if stream_dens:
         res["per_stream_input_density"] = stream_dens
         if "stream_density_targets" in wl:

@@ -183,6 +183,44 @@ st_status st_encode_chunk(st_net* net, const void* frames, int32_t n_frames,
 st_status st_layer_density(st_net* net, int32_t layer, int32_t image,
                            float* d);
 
+/* ---- online truncation-threshold adjustment on the device (section
+ * "Online Truncation Threshold Adjustment": a binary search per layer
+ * toward a target sparsity band, restarted every cycle).
+ *
+ * st_set_threshold_control keeps, for every produced tensor t (index as in
+ * `thr`), a threshold theta_t in device memory.  Controlled tensors
+ * (controlled[t] != 0) start at theta0 (theta0 < 0: theta_max / 2) with
+ * the bracket [0, theta_max]; the others keep fixed_thr[t].  After each
+ * st_encode_diff_adaptive frame, every controlled tensor's sparsity
+ * s = 1 - kept rows / sites (f64) moves theta one bisection step: s <
+ * target - eps: lo = theta, theta = (theta + hi) / 2; s > target + eps:
+ * hi = theta, theta = (lo + theta) / 2; the kernels read theta rounded to
+ * f32.  Every st_encode_reference starts a new cycle (brackets back to
+ * [0, theta_max], theta kept).  No host round trip per frame: the step is
+ * a kernel on the encode stream.
+ *
+ * controlled, fixed_thr: host arrays of n_layers + 1 entries, read during
+ * the call.  The state is uploaded on `stream` and the call waits for it.
+ * Errors: ST_ERR_STATE (no workspace), ST_ERR_INVALID_ARG (NULL arrays,
+ * target outside [0, 1], eps < 0, theta_max <= 0, theta0 > theta_max, NaN
+ * threshold), ST_ERR_HIP. */
+st_status st_set_threshold_control(st_net* net, const uint8_t* controlled,
+                                   const float* fixed_thr, double target,
+                                   double eps, double theta_max,
+                                   double theta0, void* stream);
+
+/* A diff frame encoded with the device thresholds (as st_encode_diff
+ * otherwise), followed by the controller's step.  Errors: ST_ERR_STATE (no
+ * workspace, no reference frame, threshold control not set),
+ * ST_ERR_INVALID_ARG (NULL frame), ST_ERR_HIP. */
+st_status st_encode_diff_adaptive(st_net* net, const void* frame, float* out,
+                                  void* stream);
+
+/* The current f32 thresholds (n_layers + 1 host floats), i.e. those the
+ * next adaptive frame uses; synchronises with the last encode.  Errors:
+ * ST_ERR_STATE (threshold control not set), ST_ERR_INVALID_ARG, ST_ERR_HIP. */
+st_status st_get_thresholds(st_net* net, float* thr);
+
 /* Output grid of layer j's emitted tensor (layer = -1: the input):
  * nhwc[4] = {batch, H, W, C} (host). */
 st_status st_tensor_shape(const st_net* net, int32_t layer, int32_t* nhwc);

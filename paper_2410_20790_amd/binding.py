@@ -36,6 +36,8 @@ EXPORTED = [
     "st_tensor_shape", "st_destroy_net", "st_last_error", "st_debug_active",
     "st_debug_candidates", "st_debug_rulebook", "st_debug_state",
     "st_debug_counters", "st_profile_begin", "st_profile_end",
+    "st_set_threshold_control", "st_encode_diff_adaptive",
+    "st_get_thresholds",
 ]
 
 
@@ -94,6 +96,12 @@ def _load():
         "st_profile_begin": [P, I32, I32],
         "st_profile_end": [P, P, I32, ctypes.POINTER(I32), P, I32,
                            ctypes.POINTER(I32)],
+        "st_set_threshold_control": [P, ctypes.POINTER(ctypes.c_uint8),
+                                     ctypes.POINTER(ctypes.c_float),
+                                     ctypes.c_double, ctypes.c_double,
+                                     ctypes.c_double, ctypes.c_double, P],
+        "st_encode_diff_adaptive": [P, P, P, P],
+        "st_get_thresholds": [P, ctypes.POINTER(ctypes.c_float)],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -164,6 +172,32 @@ def st_encode_diff(net, frame_ptr, thr, out_ptr=None, stream=0):
     t = (ctypes.c_float * len(thr))(*[float(v) for v in thr])
     _check(_lib.st_encode_diff(net, _ptr(frame_ptr), t, _ptr(out_ptr),
                                _ptr(stream)), net)
+
+
+def st_set_threshold_control(net, controlled, fixed_thr, target=0.9,
+                             eps=0.025, theta_max=1.0, theta0=-1.0,
+                             stream=0):
+    """controlled: n_layers + 1 flags; fixed_thr: n_layers + 1 thresholds
+    (used by the tensors that are not controlled)."""
+    if len(controlled) != len(fixed_thr):
+        raise ValueError("controlled and fixed_thr differ in length")
+    c = (ctypes.c_uint8 * len(controlled))(*[1 if v else 0
+                                             for v in controlled])
+    f = (ctypes.c_float * len(fixed_thr))(*[float(v) for v in fixed_thr])
+    _check(_lib.st_set_threshold_control(net, c, f, float(target), float(eps),
+                                         float(theta_max), float(theta0),
+                                         _ptr(stream)), net)
+
+
+def st_encode_diff_adaptive(net, frame_ptr, out_ptr=None, stream=0):
+    _check(_lib.st_encode_diff_adaptive(net, _ptr(frame_ptr), _ptr(out_ptr),
+                                        _ptr(stream)), net)
+
+
+def st_get_thresholds(net, n_tensors):
+    t = (ctypes.c_float * n_tensors)()
+    _check(_lib.st_get_thresholds(net, t), net)
+    return np.array(t[:], dtype=np.float32)
 
 
 def st_encode_chunk(net, frames_ptr, n_frames, thr, out_ptr=None, stream=0):

@@ -111,7 +111,12 @@ ConsList consumers_of(st_net* net, int t) {
   return cl;
 }
 
-bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
+IbstArgs ibst_args(st_net* net);
+
+// thr_dev: this layer's emitted-tensor threshold in device memory (online
+// adjustment), or NULL to use thr.
+bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
+               hipStream_t s) {
   const WS ws{net->ws};
   const LayerPlan& L = net->layers[i];
   const st_layer_desc& d = L.d;
@@ -181,6 +186,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   a.grp = (L.pool || L.dw || L.se) ? nullptr : grp;
   a.mdone = ws.at<uint32_t>(net->off_mdone);
   a.keep_thr = thr;
+  a.keep_thr_dev = thr_dev;
   a.zero = ws.at<char>(net->off_zero);
   a.part = ws.at<float>(net->off_part);
   a.split_max = L.split_max;
@@ -254,12 +260,13 @@ bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
     sa.chunk = L.se_chunk;
     sa.nchunk = L.se_nchunk;
     sa.keep_thr = thr;
+    sa.keep_thr_dev = thr_dev;
     launch_se(pf, s, net->dtype, sa);
   }
   if (L.pool || L.dw)
     if (!L.se)
       launch_group_count(pf, s, rowmax_out, cnt + out.cnt_rows, out.grid,
-                         thr, grp);
+                         thr, thr_dev, grp);
 
   // truncation of the emitted delta (shared by every consumer), which also
   // prepares the consumers' rulebooks
@@ -268,6 +275,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   la.n_rows = cnt + out.cnt_rows;
   la.cap = out.grid;
   la.thr = thr;
+  la.thr_dev = thr_dev;
   la.rowpix = ws.at<int>(out.off_rowpix);
   la.act = ws.at<int>(out.off_act);
   la.map = ws.at<int>(out.off_map);
@@ -279,8 +287,12 @@ bool run_layer(st_net* net, int i, bool ref, float thr, hipStream_t s) {
   return true;
 }
 
+// thr: host thresholds (ignored for the reference frame), or NULL for the
+// thresholds of the online adjustment in device memory.
 st_status encode(st_net* net, const void* frame, const float* thr, float* out,
                  hipStream_t s, bool ref) {
+  const float* thr_dev =
+      (!ref && !thr) ? WS{net->ws}.at<float>(net->off_ibst_thr) : nullptr;
   const WS ws{net->ws};
   u64* cnt = ws.at<u64>(net->off_cnt);
   net->last_nf = 1;
@@ -291,7 +303,7 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
 
   launch_reset(pf, s, cnt, net->n_counters);
   TensorPlan& T0 = net->tensors[0];
-  const float thr0 = ref ? -1.f : thr[0];
+  const float thr0 = ref ? -1.f : thr_dev ? 0.f : thr[0];
   ScanArgs sa{};
   sa.x = frame;
   sa.xhat = ws.at<char>(net->off_xhat);
@@ -299,6 +311,7 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
   sa.Cp = T0.Cp;
   sa.npix = T0.grid;
   sa.thr = thr0;
+  sa.thr_dev = thr_dev;
   sa.ref = ref ? 1 : 0;
   sa.keep = ws.at<uint8_t>(net->off_flags);
   sa.tiles = ws.at<uint32_t>(net->off_tiles);
@@ -313,7 +326,8 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
   T0.last_thr = thr0;
   const int nl = (int)net->layers.size();
   for (int i = 0; i < nl; ++i)
-    if (!run_layer(net, i, ref, ref ? -1.f : thr[i + 1], s))
+    if (!run_layer(net, i, ref, ref ? -1.f : thr_dev ? 0.f : thr[i + 1],
+                   thr_dev ? thr_dev + i + 1 : nullptr, s))
       return fail(net, ST_ERR_HIP, "internal: GEMM launch arguments");
 
   if (out) {
@@ -332,6 +346,15 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
     if (L.se) L.se_par ^= 1;
   launch_cleanup(pf, s, ws.at<CleanEntry>(net->off_cleanup), net->n_cleanup,
                  net->ws, cnt, net->max_grid);
+  // online adjustment: a reference frame starts a new cycle; after a diff
+  // frame encoded with the device thresholds, one bisection step
+  if (net->ibst_on && (ref || thr_dev)) {
+    const IbstArgs ia = ibst_args(net);
+    if (ref)
+      launch_ibst_restart(s, ia);
+    else
+      launch_ibst_step(s, cnt, ia);
+  }
   if (R && R->n_hist < R->max_frames) {
     (void)hipMemcpyAsync(R->hist + (size_t)R->n_hist * net->n_counters, cnt,
                          sizeof(u64) * net->n_counters, hipMemcpyDeviceToHost,
@@ -345,6 +368,22 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
 // ---- chunk mode: the frames of a chunk as items (frame t's sites after
 // frame t-1's) for the rulebooks, GEMMs and truncations; per-site frame
 // loops for the frame delta, the state update and the pools.
+IbstArgs ibst_args(st_net* net) {
+  const WS ws{net->ws};
+  IbstArgs a{};
+  a.theta = ws.at<double>(net->off_ibst_theta);
+  a.lo = ws.at<double>(net->off_ibst_lo);
+  a.hi = ws.at<double>(net->off_ibst_hi);
+  a.thr = ws.at<float>(net->off_ibst_thr);
+  a.ctl = ws.at<uint8_t>(net->off_ibst_ctl);
+  a.sites = ws.at<int64_t>(net->off_ibst_sites);
+  a.n = (int)net->tensors.size();
+  a.target = net->ibst_target;
+  a.eps = net->ibst_eps;
+  a.theta_max = net->ibst_theta_max;
+  return a;
+}
+
 bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
                      hipStream_t s) {
   const WS ws{net->ws};
@@ -503,7 +542,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
   }
   if (L.stateful)
     launch_group_count(pf, s, rowmax_out, cnt + outT.cnt_rows,
-                       outT.grid * nf, thr, grp);
+                       outT.grid * nf, thr, nullptr, grp);
 
   ListArgs la{};
   la.rowmax = rowmax_out;
@@ -727,6 +766,90 @@ extern "C" st_status st_encode_diff(st_net* net, const void* frame,
       return fail(net, ST_ERR_INVALID_ARG,
                   "threshold " + std::to_string(i) + " is NaN");
   return encode(net, frame, thr, out, (hipStream_t)stream, false);
+}
+
+extern "C" st_status st_set_threshold_control(st_net* net,
+                                              const uint8_t* controlled,
+                                              const float* fixed_thr,
+                                              double target, double eps,
+                                              double theta_max, double theta0,
+                                              void* stream) {
+  if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
+  if (!net->bound) return fail(net, ST_ERR_STATE, "no workspace bound");
+  if (!controlled || !fixed_thr)
+    return fail(net, ST_ERR_INVALID_ARG, "NULL controlled or fixed_thr");
+  if (!(target >= 0.0 && target <= 1.0) || !(eps >= 0.0) ||
+      !(theta_max > 0.0) || std::isnan(theta0) || theta0 > theta_max)
+    return fail(net, ST_ERR_INVALID_ARG,
+                "need 0 <= target <= 1, eps >= 0, theta_max > 0, "
+                "theta0 <= theta_max");
+  const size_t n = net->tensors.size();
+  std::vector<double> theta(n), lo(n, 0.0), hi(n, theta_max);
+  std::vector<float> thr(n);
+  std::vector<uint8_t> ctl(n);
+  std::vector<int64_t> sites(n);
+  for (size_t t = 0; t < n; ++t) {
+    if (std::isnan(fixed_thr[t]))
+      return fail(net, ST_ERR_INVALID_ARG,
+                  "threshold " + std::to_string(t) + " is NaN");
+    ctl[t] = controlled[t] ? 1 : 0;
+    theta[t] = ctl[t] ? (theta0 < 0.0 ? theta_max / 2 : theta0)
+                      : (double)fixed_thr[t];
+    thr[t] = (float)theta[t];
+    sites[t] = net->tensors[t].grid;
+  }
+  const WS ws{net->ws};
+  hipStream_t s = (hipStream_t)stream;
+  const struct {
+    void* dst;
+    const void* src;
+    size_t bytes;
+  } copies[] = {
+      {ws.at<double>(net->off_ibst_theta), theta.data(), sizeof(double) * n},
+      {ws.at<double>(net->off_ibst_lo), lo.data(), sizeof(double) * n},
+      {ws.at<double>(net->off_ibst_hi), hi.data(), sizeof(double) * n},
+      {ws.at<float>(net->off_ibst_thr), thr.data(), sizeof(float) * n},
+      {ws.at<uint8_t>(net->off_ibst_ctl), ctl.data(), n},
+      {ws.at<int64_t>(net->off_ibst_sites), sites.data(),
+       sizeof(int64_t) * n},
+  };
+  for (const auto& c : copies)
+    if (hipMemcpyAsync(c.dst, c.src, c.bytes, hipMemcpyHostToDevice, s) !=
+        hipSuccess)
+      return fail(net, ST_ERR_HIP, "threshold state upload failed");
+  // the host vectors must outlive the copies
+  if (hipStreamSynchronize(s) != hipSuccess)
+    return fail(net, ST_ERR_HIP, "threshold state upload failed");
+  net->ibst_on = true;
+  net->ibst_target = target;
+  net->ibst_eps = eps;
+  net->ibst_theta_max = theta_max;
+  return ST_OK;
+}
+
+extern "C" st_status st_encode_diff_adaptive(st_net* net, const void* frame,
+                                             float* out, void* stream) {
+  if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
+  if (!net->bound) return fail(net, ST_ERR_STATE, "no workspace bound");
+  if (!net->ibst_on)
+    return fail(net, ST_ERR_STATE, "threshold control not set");
+  if (!net->have_ref)
+    return fail(net, ST_ERR_STATE,
+                "st_encode_diff_adaptive before st_encode_reference");
+  if (!frame) return fail(net, ST_ERR_INVALID_ARG, "NULL frame");
+  return encode(net, frame, nullptr, out, (hipStream_t)stream, false);
+}
+
+extern "C" st_status st_get_thresholds(st_net* net, float* thr) {
+  if (!net || !thr) return fail(net, ST_ERR_INVALID_ARG, "NULL argument");
+  if (!net->ibst_on)
+    return fail(net, ST_ERR_STATE, "threshold control not set");
+  if (net->last_stream) {
+    const st_status st = sync_last(net);
+    if (st != ST_OK) return st;
+  }
+  return d2h(net, thr, WS{net->ws}.at<float>(net->off_ibst_thr),
+             net->tensors.size());
 }
 
 extern "C" st_status st_layer_density(st_net* net, int32_t layer,

@@ -117,6 +117,13 @@ struct st_net {
   size_t off_mdone = 0;                    // uint32 [max grid / 64 + 1]
   size_t off_zero = 0;                     // 256 zero bytes
   size_t off_part = 0;                     // f32 split partials (shared)
+  // online threshold adjustment, per produced tensor
+  size_t off_ibst_theta = 0, off_ibst_lo = 0, off_ibst_hi = 0;  // f64
+  size_t off_ibst_thr = 0;                 // f32 thresholds the kernels read
+  size_t off_ibst_ctl = 0;                 // uint8 controlled flags
+  size_t off_ibst_sites = 0;               // int64 sites per tensor
+  bool ibst_on = false;
+  double ibst_target = 0.9, ibst_eps = 0.025, ibst_theta_max = 1.0;
   // chunk mode (F > 1): f32 deferred updates of the current layer (shared),
   // per input item the frame whose value X_hat held (0xFF: the X_hat of
   // the chunk's start), per input site the last kept frame, per conv site

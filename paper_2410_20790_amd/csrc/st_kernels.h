@@ -65,6 +65,7 @@ struct ScanArgs {
   int C, Cp;
   int64_t npix;
   float thr;
+  const float* thr_dev;  // threshold in device memory (or NULL: thr)
   int ref;
   uint8_t* keep;
   uint32_t* tiles;
@@ -132,6 +133,7 @@ struct ConvArgs {
   uint32_t* grp;       // per-64-row kept counts (or NULL)
   uint32_t* mdone;     // per-row-tile arrival counters (zero between uses)
   float keep_thr;      // threshold of the emitted tensor
+  const float* keep_thr_dev;  // in device memory (or NULL: keep_thr)
   const void* zero;    // 16 zero bytes (16-byte aligned)
   // split reduction: up to split_max splits of the reduction stages per
   // output tile (chosen per frame from the tile count), their f32 partial
@@ -174,6 +176,7 @@ struct ListArgs {
   const u64* n_rows;
   int64_t cap;
   float thr;
+  const float* thr_dev;  // threshold in device memory (or NULL: thr)
   const int* rowpix;
   int* act;
   int* map;
@@ -184,7 +187,7 @@ struct ListArgs {
 void launch_list_compact(const Prof& pf, hipStream_t s, const ListArgs& a);
 void launch_group_count(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
                         const u64* n_rows, int64_t cap, float thr,
-                        uint32_t* grp);
+                        const float* thr_dev, uint32_t* grp);
 
 // ---- squeeze-excitation on a deferred layer
 struct SeArgs {
@@ -208,6 +211,7 @@ struct SeArgs {
   int64_t npix, hw, ngrp;
   int N, cp, c, mid, act, ref, chunk, nchunk, tps;
   float keep_thr;
+  const float* keep_thr_dev;  // in device memory (or NULL: keep_thr)
 };
 void launch_se(const Prof& pf, hipStream_t s, int dtype, const SeArgs& a);
 // Storage-dtype matrix src [rows][cols] (or, transposed, src [cols][rows])
@@ -288,6 +292,26 @@ void launch_repack_dw(hipStream_t s, int dtype, const void* w, float* wdw,
                       int c, int kh, int kw, int cp);
 void launch_bias(hipStream_t s, int dtype, const void* b, float* out,
                  int cout, int cout_p);
+// ---- online threshold adjustment on the device
+// Per tensor t: bisection state theta/lo/hi (f64), the f32 threshold the
+// kernels read, a controlled flag, and the tensor's site count.  After a
+// diff frame, each controlled tensor's sparsity 1 - kept / sites (kept =
+// counters[2 t + 1]) moves theta one bisection step toward
+// [target - eps, target + eps].
+struct IbstArgs {
+  double* theta;
+  double* lo;
+  double* hi;
+  float* thr;
+  const uint8_t* ctl;
+  const int64_t* sites;
+  int n;
+  double target, eps, theta_max;
+};
+void launch_ibst_step(hipStream_t s, const u64* counters, const IbstArgs& a);
+// A new cycle: every controlled bracket back to [0, theta_max].
+void launch_ibst_restart(hipStream_t s, const IbstArgs& a);
+
 // Kept rows per image of a kept list (any order); cap bounds its length.
 void launch_density(hipStream_t s, const int* act, const u64* n_act,
                     int64_t cap, int64_t hw, int images, u64* out);

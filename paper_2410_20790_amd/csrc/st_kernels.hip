@@ -352,9 +352,11 @@ struct ScanPred {
   int* map;
   int C, Cp, ref;
   float thr;
+  const float* thr_dev;
   ConsList cons;
   // pass 1: evaluate the truncation rule and remember it
   __device__ bool count(int64_t i) const {
+    const float thr = thr_dev ? *thr_dev : this->thr;
     float m = 0.f;
     for (int c = 0; c < C; ++c) {
       float d = to_f(x[i * C + c]) - (ref ? 0.f : to_f(xhat[i * C + c]));
@@ -397,7 +399,7 @@ struct ScanPred {
 template <typename T>
 static void scan_t(const Prof& pf, hipStream_t s, const ScanArgs& a) {
   ScanPred<T> p{(const T*)a.x, (T*)a.xhat, a.keep, (T*)a.rows, a.rowpix,
-                a.act, a.map, a.C, a.Cp, a.ref, a.thr, a.cons};
+                a.act, a.map, a.C, a.Cp, a.ref, a.thr, a.thr_dev, a.cons};
   run_compact(pf, 0 /*ST_K_SCAN_MASK*/, 1 /*ST_K_SCAN_COMPACT*/, s, nullptr,
               a.npix, a.npix, a.tiles, a.cnt_rows, a.cnt_act, p);
 }
@@ -585,7 +587,9 @@ void launch_flag_compact(const Prof& pf, int cls_count, int cls_write,
 __global__ __launch_bounds__(256) void k_group_count(const uint32_t* rowmax,
                                                      const u64* n_rows,
                                                      float thr,
+                                                     const float* thr_dev,
                                                      uint32_t* grp) {
+  if (thr_dev) thr = *thr_dev;
   const int64_t n = (int64_t)*n_rows;
   const int64_t ngrp = (n + 63) / 64;
   const int lane = threadIdx.x & 63;
@@ -600,9 +604,10 @@ __global__ __launch_bounds__(256) void k_group_count(const uint32_t* rowmax,
 
 void launch_group_count(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
                         const u64* n_rows, int64_t cap, float thr,
-                        uint32_t* grp) {
+                        const float* thr_dev, uint32_t* grp) {
   prof_begin(pf, 14 /*ST_K_LIST_COUNT*/, s);
-  k_group_count<<<grid_for(cap, 2048), 256, 0, s>>>(rowmax, n_rows, thr, grp);
+  k_group_count<<<grid_for(cap, 2048), 256, 0, s>>>(rowmax, n_rows, thr,
+                                                    thr_dev, grp);
   prof_end(pf, 14, s);
 }
 
@@ -860,7 +865,7 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
       if (o < m_end)
         k = __uint_as_float(__hip_atomic_load(a.rowmax + o, __ATOMIC_RELAXED,
                                               __HIP_MEMORY_SCOPE_AGENT)) >
-            a.keep_thr;
+            (a.keep_thr_dev ? *a.keep_thr_dev : a.keep_thr);
       const u64 b = __ballot(k);
       if (tid == 0) {
         a.grp[tm] = (uint32_t)__popcll(b);
@@ -1663,17 +1668,19 @@ struct ListPred {
   int* act;
   int* map;
   float thr;
+  const float* thr_dev;  // or NULL: thr
   ConsList cons;
   struct Item {
     uint32_t rm;
     int pix;
   };
+  __device__ float th() const { return thr_dev ? *thr_dev : thr; }
   __device__ bool count(int64_t r) const {
-    return __uint_as_float(rowmax[r]) > thr;
+    return __uint_as_float(rowmax[r]) > th();
   }
   __device__ Item load(int64_t r) const { return Item{rowmax[r], rowpix[r]}; }
   __device__ bool keep(const Item& it) const {
-    return __uint_as_float(it.rm) > thr;
+    return __uint_as_float(it.rm) > th();
   }
   __device__ unsigned emit(int64_t r, unsigned pos, const Item& it) const {
     act[pos] = it.pix;
@@ -1686,7 +1693,7 @@ struct ListPred {
 };
 
 void launch_list_compact(const Prof& pf, hipStream_t s, const ListArgs& a) {
-  ListPred p{a.rowmax, a.rowpix, a.act, a.map, a.thr, a.cons};
+  ListPred p{a.rowmax, a.rowpix, a.act, a.map, a.thr, a.thr_dev, a.cons};
   const int tile = compact_tile(a.cap);
   const int nt = compact_tiles(a.cap);
   prof_begin(pf, 15 /*ST_K_LIST_COMPACT*/, s);
@@ -1919,7 +1926,8 @@ __global__ __launch_bounds__(256) void k_se_emit(SeArgs a) {
     a.map[row] = (int)row;
   }
   // the sites of one wave lie in one 64-site group
-  const u64 b = __ballot(in && lane == 0 && rm > a.keep_thr);
+  const float kthr = a.keep_thr_dev ? *a.keep_thr_dev : a.keep_thr;
+  const u64 b = __ballot(in && lane == 0 && rm > kthr);
   if ((threadIdx.x & 63) == 0 && b) {
     const int64_t first = (int64_t)blockIdx.x * R + (threadIdx.x / TPS);
     atomicAdd(a.grp + first / 64, (unsigned)__popcll(b));
@@ -2524,6 +2532,43 @@ void launch_bias(hipStream_t s, int dtype, const void* b, float* out,
 
 // Per-image kept counts of an ascending pixel list (binary search of the
 // image boundaries).
+// ------------------------------------------- online threshold adjustment
+// One bisection step per controlled tensor, in f64 as the host controller
+// takes it; the f32 threshold is theta rounded to nearest.
+__global__ void k_ibst_step(const u64* counters, IbstArgs a) {
+  for (int t = threadIdx.x; t < a.n; t += blockDim.x) {
+    if (!a.ctl[t]) continue;
+    const double sp =
+        1.0 - (double)counters[2 * t + 1] / (double)a.sites[t];
+    double th = a.theta[t];
+    if (sp < a.target - a.eps) {
+      a.lo[t] = th;
+      th = 0.5 * (th + a.hi[t]);
+    } else if (sp > a.target + a.eps) {
+      a.hi[t] = th;
+      th = 0.5 * (a.lo[t] + th);
+    }
+    a.theta[t] = th;
+    a.thr[t] = (float)th;
+  }
+}
+
+__global__ void k_ibst_restart(IbstArgs a) {
+  for (int t = threadIdx.x; t < a.n; t += blockDim.x)
+    if (a.ctl[t]) {
+      a.lo[t] = 0.0;
+      a.hi[t] = a.theta_max;
+    }
+}
+
+void launch_ibst_step(hipStream_t s, const u64* counters, const IbstArgs& a) {
+  k_ibst_step<<<1, 256, 0, s>>>(counters, a);
+}
+
+void launch_ibst_restart(hipStream_t s, const IbstArgs& a) {
+  k_ibst_restart<<<1, 256, 0, s>>>(a);
+}
+
 // Kept rows per image (image = item / hw) of a kept list in any order: a
 // per-block histogram in LDS (up to kDensityLdsImages images; beyond that,
 // device atomics directly), added to `out` (zeroed first).

@@ -278,6 +278,13 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
   net->off_grp = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
   net->off_mdone = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
   net->off_zero = a.take(256);
+  const size_t n_t = (size_t)L_n + 1;
+  net->off_ibst_theta = a.take(sizeof(double) * n_t);
+  net->off_ibst_lo = a.take(sizeof(double) * n_t);
+  net->off_ibst_hi = a.take(sizeof(double) * n_t);
+  net->off_ibst_thr = a.take(sizeof(float) * n_t);
+  net->off_ibst_ctl = a.take(n_t);
+  net->off_ibst_sites = a.take(sizeof(int64_t) * n_t);
   net->off_part = a.take(std::max<size_t>(part_bytes, 256));
   net->n_cleanup = n_cleanup;
   net->off_cleanup = a.take(32 * n_cleanup);

@@ -112,6 +112,38 @@ class SparseTemNet:
                          self._stream())
         return out
 
+    def set_threshold_control(self, controlled, fixed_thr, target=0.9,
+                              eps=0.025, theta_max=1.0, theta0=None):
+        """Online threshold adjustment on the device: `controlled` lists the
+        indices (into thr) of the tensors whose threshold is searched;
+        fixed_thr (n_layers + 1) holds the others'."""
+        if len(fixed_thr) != self.n_layers + 1:
+            raise ValueError("fixed_thr needs n_layers + 1 entries")
+        flags = [0] * (self.n_layers + 1)
+        for t in controlled:
+            if not 0 <= t <= self.n_layers:
+                raise ValueError("controlled tensor index out of range")
+            flags[t] = 1
+        B.st_set_threshold_control(self.handle, flags, fixed_thr, target, eps,
+                                   theta_max,
+                                   -1.0 if theta0 is None else theta0,
+                                   self._stream())
+
+    def encode_diff_adaptive(self, frame, out=None, write_out=True):
+        """A diff frame with the device-adjusted thresholds, then one step
+        of the adjustment."""
+        self._check_frame(frame)
+        if write_out and out is None:
+            out = self.new_output()
+        B.st_encode_diff_adaptive(self.handle, frame.data_ptr(),
+                                  out.data_ptr() if write_out else None,
+                                  self._stream())
+        return out
+
+    def thresholds(self):
+        """The thresholds the next adaptive frame uses (synchronising)."""
+        return B.st_get_thresholds(self.handle, self.n_layers + 1)
+
     def encode_chunk(self, frames, thr, out=None, write_out=True):
         """frames: contiguous device tensor [n_frames, *in_shape]; returns
         the outputs of every frame, [n_frames, *out_shape] (f32)."""

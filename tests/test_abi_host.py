@@ -213,3 +213,25 @@ def test_chunked_create_and_workspace():
             B.st_create_net_chunked(d, net.batch, bad, net.H, net.W, net.C,
                                     B.ST_F32)
         assert e.value.status == B.ST_ERR_INVALID_ARG
+
+
+def test_threshold_control_needs_a_bound_net():
+    """The device threshold controller writes the workspace: on a net with
+    none bound every entry point is a state error (no HIP call is made)."""
+    net = toy_net()
+    h = B.st_create_net(descs(net), net.batch, net.H, net.W, net.C, B.ST_F32)
+    try:
+        n = len(net.layers) + 1
+        with pytest.raises(B.StError) as e:
+            B.st_set_threshold_control(h, [1] * n, [0.0] * n)
+        assert e.value.status == B.ST_ERR_STATE
+        with pytest.raises(B.StError) as e:
+            B.st_encode_diff_adaptive(h, 0x1000)
+        assert e.value.status == B.ST_ERR_STATE
+        with pytest.raises(B.StError) as e:
+            B.st_get_thresholds(h, n)
+        assert e.value.status == B.ST_ERR_STATE
+        with pytest.raises(ValueError):
+            B.st_set_threshold_control(h, [1] * n, [0.0] * (n - 1))
+    finally:
+        B.st_destroy_net(h)
