@@ -25,6 +25,13 @@ Readings of points the paper leaves open (all listed in the design notes):
    commit their new value, truncated ones keep accumulating change.
 3. Rows truncated inside the network are dropped (no residual carried);
    the non-linear op reconstructs from the cached pre-activation only.
+   Optional residual carry (``carry=True``, the output-buffer semantics the
+   paper attributes to DeltaCNN): every emitted tensor keeps the sum of
+   the deltas its consumers received (Y_hat); a candidate row emits
+   e_new - Y_hat, where e is the layer's dense emitted value (f(P), pooled
+   or gated; P itself for a layer without non-linearity, which then keeps
+   P too), kept rows add their rounded delta to Y_hat and truncated rows
+   carry their residual until the site is affected again.
 4. One threshold per produced tensor: ``thr[0]`` masks the frame delta,
    ``thr[j+1]`` masks layer j's emitted delta (shared by all consumers).
 5. Bias enters only the reference pass; it cancels in deltas (Eq. 2).
@@ -239,12 +246,13 @@ def _apply_offset(rows, w, ky, kx, groups):
     return out
 
 
-def dense_forward(layers, frame, dtype, with_se=False):
+def dense_forward(layers, frame, dtype, with_se=False, all_pre=False):
     """Plain dense forward of one frame (the definition the diff chain must
     reproduce at threshold 0): returns (out, P, acts) where P[i] is the f32
-    pre-activation of every stateful layer, acts[i] the emitted activation
-    rounded to the storage dtype, and out the f32 network output; with
-    with_se also the squeeze-excitation gates S[i]."""
+    pre-activation of every stateful layer (of every layer with all_pre),
+    acts[i] the emitted activation rounded to the storage dtype, and out
+    the f32 network output; with with_se also the squeeze-excitation gates
+    S[i]."""
     acts = {-1: round_storage(frame, dtype)}
     P = {}
     S = {}
@@ -254,6 +262,8 @@ def dense_forward(layers, frame, dtype, with_se=False):
         if L.residual_src != -2:
             a = a + acts[L.residual_src]
         p32 = f32(a)
+        if all_pre:
+            P[i] = p32
         if _is_stateful(layers, i):
             P[i] = p32
             e = activation(p32, L.act).astype(np.float64)
@@ -274,11 +284,12 @@ def dense_forward(layers, frame, dtype, with_se=False):
 class OracleNet:
     """Stateful diff encoder over one stream of frames (batch N images)."""
 
-    def __init__(self, layers, batch, H, W, C, dtype="f32"):
+    def __init__(self, layers, batch, H, W, C, dtype="f32", carry=False):
         if dtype not in ("f32", "f16", "bf16"):
             raise ValueError(dtype)
         self.layers = list(layers)
         self.dtype = dtype
+        self.carry = carry
         self.in_shape = (batch, H, W, C)
         shapes = {-1: self.in_shape}
         self.geo = []
@@ -298,6 +309,7 @@ class OracleNet:
         self.xhat = None
         self.P = {}
         self.S = {}
+        self.Y = {}        # residual carry: consumers' view of each tensor
         self.last = None
 
     # -- reference frame ---------------------------------------------------
@@ -307,10 +319,14 @@ class OracleNet:
         frame = np.asarray(frame, dtype=np.float64)
         assert frame.shape == self.in_shape
         out, P, acts, S = dense_forward(self.layers, frame, self.dtype,
-                                        with_se=True)
+                                        with_se=True, all_pre=self.carry)
         self.xhat = round_storage(frame, self.dtype)
         self.P = {i: p.copy() for i, p in P.items()}
         self.S = {i: g.copy() for i, g in S.items()}
+        if self.carry:
+            # the reference frame emits every site: consumers hold acts
+            self.Y = {i: f32(acts[i]).reshape(-1, L.c_out).copy()
+                      for i, L in enumerate(self.layers)}
         self.last = dict(kind="reference", out=out, acts=acts)
         return out
 
@@ -366,7 +382,9 @@ class OracleNet:
             dP32 = f32(dP)
 
             Q = None
-            if self.stateful[i]:
+            if self.carry:
+                d32, cand, Q = self._carry_delta(i, O, dP32)
+            elif self.stateful[i]:
                 # Non-linear handling: reconstruct the dense pre-activation
                 # (Accumulation onto the cached P) and re-sparsify after f.
                 Pg = self.P[i].reshape(N * g.Ho * g.Wo, L.c_out)
@@ -415,6 +433,11 @@ class OracleNet:
             d = round_storage(d32, self.dtype)
             cmax = np.abs(d).max(axis=1) if len(cand) else np.zeros(0)
             kept = cmax > thr[i + 1]                     # readings 1 and 3
+            if self.carry:
+                # kept rows reach the consumers; truncated rows carry over
+                Y = self.Y[i]
+                Y[cand[kept]] = f32(Y[cand[kept]].astype(np.float64)
+                                    + d[kept])
             tensors.append(dict(cand=cand, cand_max=cmax, cand_rows=d,
                                 pix=cand[kept], rows=d[kept],
                                 grid=(N, g.Hp, g.Wp), C=L.c_out))
@@ -425,6 +448,54 @@ class OracleNet:
         self.last = dict(kind="diff", out=out, tensors=tensors,
                          layers=layer_art, thr=thr)
         return out
+
+    def _carry_delta(self, i, O, dP32):
+        """Residual carry: apply the update to P (every layer keeps P) and
+        return (delta = e_new - Y_hat at the candidate sites, candidates,
+        pooled candidates or None), e being the layer's dense emitted value
+        (f(P), pooled or gated; P for a layer without non-linearity)."""
+        L, g = self.layers[i], self.geo[i]
+        N = self.in_shape[0]
+        Pg = self.P[i].reshape(N * g.Ho * g.Wo, L.c_out)
+        Pg[O] = f32(Pg[O].astype(np.float64) + dP32)
+        Y = self.Y[i]
+        if L.se_mid:
+            a_new = activation(Pg.reshape(N, g.Ho, g.Wo, L.c_out), L.act)
+            s_new = se_gates(a_new, L)
+            self.S[i] = s_new
+            e = se_apply(a_new, s_new).reshape(-1, L.c_out)
+            cand = np.arange(N * g.Ho * g.Wo, dtype=np.int64)
+            Q = None
+        elif g.pool:
+            T = window_targets(O, (g.Ho, g.Wo), (g.Hp, g.Wp), L.pool_k,
+                               L.pool_s, L.pool_p)
+            Q = np.unique(T[:, 2]).astype(np.int64)
+            e = f32(maxpool_nhwc(activation(
+                Pg.reshape(N, g.Ho, g.Wo, L.c_out), L.act),
+                L.pool_k, L.pool_s, L.pool_p)).reshape(-1, L.c_out)[Q]
+            cand = Q
+        else:
+            e = activation(Pg[O], L.act) if self.stateful[i] else Pg[O]
+            cand = O
+            Q = None
+        d32 = f32(np.asarray(e, np.float64) - Y[cand].astype(np.float64))
+        return d32, cand, Q
+
+    def emitted(self, i):
+        """The dense emitted value of layer i from the current state:
+        f(P), pooled or gated (P for a layer without non-linearity)."""
+        L, g = self.layers[i], self.geo[i]
+        N = self.in_shape[0]
+        P = self.P[i]
+        if not self.stateful[i]:
+            return P.reshape(-1, L.c_out)
+        e = activation(P, L.act).astype(np.float64)
+        if g.pool:
+            e = maxpool_nhwc(e, L.pool_k, L.pool_s, L.pool_p)
+        e = f32(e)
+        if L.se_mid:
+            e = se_apply(e, self.S[i])
+        return np.asarray(e).reshape(-1, L.c_out)
 
     def _dense_output(self):
         i = len(self.layers) - 1
