@@ -829,6 +829,61 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
     return res
 
 
+def carry_comparison(name, thr_val, steps=18):
+    """Drop (the paper's schedule) against residual carry on one workload
+    at a threshold above zero, frame by frame over one chunk: every diff
+    frame's output error against the dense forward of the same frame (the
+    library's own dense pass), the diff-frames/s of both over `steps` timed
+    frames of further chunks, and the workspace of both."""
+    import torch
+    from paper_2410_20790_amd import SparseTemNet
+    wl = workload(name, 0.10)
+    net = wl["net"]
+    dt = net.dtype
+    chunk = wl["chunk"]
+    tdt = {"f32": torch.float32, "f16": torch.float16,
+           "bf16": torch.bfloat16}[dt]
+    n = frames_needed(chunk, 0, chunk - 1 + steps, 0)
+    frames = torch.empty((n, net.batch, net.H, net.W, net.C), dtype=tdt,
+                         device="cuda")
+    for i, f in enumerate(wl["frames"](n)):
+        frames[i].copy_(torch.from_numpy(f))
+    thr = [thr_val] * (len(net.layers) + 1)
+    mk = lambda carry: SparseTemNet(net.layers, net.batch, net.H, net.W,  # noqa: E731
+                                    net.C, dt, carry=carry)
+    nets = {"drop": mk(False), "carry": mk(True)}
+    dense = mk(False)
+    res = {"workload": wl["desc"], "thr": thr_val, "chunk": chunk}
+    try:
+        errs = {k: [] for k in nets}
+        for g in nets.values():
+            g.encode_reference(frames[0])
+        for t in range(1, chunk):
+            ref = dense.encode_reference(frames[t])
+            scale = float(ref.abs().max())
+            for k, g in nets.items():
+                out = g.encode_diff(frames[t], thr)
+                errs[k].append(float((out - ref).abs().max()) / scale)
+        torch.cuda.synchronize()
+        for k, g in nets.items():
+            feed = Feed(g, len(net.layers), frames, chunk, thr, None,
+                        g.new_output())
+            feed.pos = chunk
+            wall, _ = run_diffs(feed, steps)
+            res[k] = {"diff_frames_per_s": steps / wall,
+                      "max_rel_err_vs_dense_per_frame":
+                          [round(e, 6) for e in errs[k]],
+                      "workspace_bytes": g.ws_bytes}
+        res["extra_memory_bytes"] = (nets["carry"].ws_bytes -
+                                     nets["drop"].ws_bytes)
+    finally:
+        for g in list(nets.values()) + [dense]:
+            g.close()
+        del frames
+        torch.cuda.empty_cache()
+    return res
+
+
 def default_schedule(wl, requested=None):
     """SparseBatch (one st_encode_chunk call per chunk) where the library
     offers it -- nets without squeeze-excitation whose input has at most
@@ -956,6 +1011,10 @@ def main():
             "multistream": extra_workload("multistream", 14, 7),
             "crnn": extra_workload("crnn", 30, 15, thr=0.02),
             "toy": extra_workload("toy", 30, 3)}
+    if args.workload == "resnet50" and not args.no_extra:
+        res["residual_carry"] = {
+            "resnet50": carry_comparison("resnet50", 0.02),
+            "toy": carry_comparison("toy", 0.05, steps=30)}
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, net, args.thr)
     print(json.dumps(res), flush=True)

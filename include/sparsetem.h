@@ -121,6 +121,29 @@ st_status st_create_net_chunked(const st_layer_desc* layers,
                                 int32_t in_w, int32_t in_c, int32_t dtype,
                                 st_net** out);
 
+/* Creation flags (st_create_net_ex). */
+enum {
+  /* Residual carry: every emitted tensor keeps its consumers' view (the sum
+   * of the deltas they received, f32, one buffer per layer output -- the
+   * output caches of the DeltaCNN scheme the paper compares SparseBatch
+   * with, in section "Non-linear operations").  A candidate row emits the
+   * layer's dense emitted value (f(P), pooled or gated; P for a layer
+   * without non-linearity, which then keeps P too) minus the view; kept
+   * rows join the view, truncated rows carry their residual until the site
+   * is affected again, so what consumers see never strays from the dense
+   * value by more than the threshold.  Frame by frame only
+   * (max_frames = 1). */
+  ST_NET_RESIDUAL_CARRY = 1
+};
+
+/* As st_create_net_chunked, with creation flags (ST_NET_*).  Errors as
+ * st_create_net_chunked, plus ST_ERR_INVALID_ARG for an unknown flag and
+ * ST_ERR_UNSUPPORTED for ST_NET_RESIDUAL_CARRY with max_frames > 1. */
+st_status st_create_net_ex(const st_layer_desc* layers, int32_t n_layers,
+                           int32_t batch, int32_t max_frames, int32_t in_h,
+                           int32_t in_w, int32_t in_c, int32_t dtype,
+                           uint32_t flags, st_net** out);
+
 /* Bytes of device workspace the net needs (host only).  The workspace holds
  * the Subtraction buffer, every f32 pre-activation buffer, the repacked
  * weights, and worst-case-sized (every pixel active) delta rows, active
@@ -257,6 +280,12 @@ st_status st_debug_rulebook(st_net* net, int32_t layer, int32_t* kio,
  * ([batch][H_conv][W_conv][c_out], `cap` floats). */
 st_status st_debug_state(st_net* net, int32_t layer, float* P, int64_t cap);
 
+/* Consumers' view of layer `layer`'s emitted tensor on a net created with
+ * ST_NET_RESIDUAL_CARRY ([batch][H_out][W_out][c_out] f32, `cap` floats).
+ * Errors: ST_ERR_STATE (not a residual-carry net), as st_debug_state. */
+st_status st_debug_carry(st_net* net, int32_t layer, float* view,
+                         int64_t cap);
+
 /* Per-layer rulebook pair counts (n_layers) and per-tensor kept counts
  * (n_layers + 1, index 0 = frame delta) of the last encode. */
 st_status st_debug_counters(st_net* net, int64_t* pairs_per_layer,
@@ -278,7 +307,8 @@ enum {
   ST_K_POOL_MARK, ST_K_POOL_COUNT, ST_K_POOL_COMPACT, ST_K_POOL_EMIT,
   ST_K_COMMIT, ST_K_LIST_COUNT, ST_K_LIST_COMPACT, ST_K_OUTPUT,
   ST_K_CLEANUP, ST_K_RESET, ST_K_SE_SQUEEZE, ST_K_SE_EXCITE, ST_K_SE_EMIT,
-  ST_K_CONV_SPLIT_EPI, ST_K_CHUNK_UPDATE, ST_K_RUN_TILES, ST_K_NUM_CLASSES
+  ST_K_CONV_SPLIT_EPI, ST_K_CHUNK_UPDATE, ST_K_RUN_TILES,
+  ST_K_CARRY_COMMIT, ST_K_NUM_CLASSES
 };
 
 /* Start recording: room for `max_launches` launch records and

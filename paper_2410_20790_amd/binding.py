@@ -26,7 +26,7 @@ KERNEL_CLASSES = [
     "rb_nbr", "rb_ident", "conv_gemm", "conv_dw", "pool_mark", "pool_count",
     "pool_compact", "pool_emit", "commit", "list_count", "list_compact",
     "output", "cleanup", "reset", "se_squeeze", "se_excite", "se_emit",
-    "conv_split_epi", "chunk_update", "run_tiles",
+    "conv_split_epi", "chunk_update", "run_tiles", "carry_commit",
 ]
 
 EXPORTED = [
@@ -37,7 +37,7 @@ EXPORTED = [
     "st_debug_candidates", "st_debug_rulebook", "st_debug_state",
     "st_debug_counters", "st_profile_begin", "st_profile_end",
     "st_set_threshold_control", "st_encode_diff_adaptive",
-    "st_get_thresholds",
+    "st_get_thresholds", "st_create_net_ex", "st_debug_carry",
 ]
 
 
@@ -81,6 +81,10 @@ def _load():
         "st_create_net_chunked": [ctypes.POINTER(st_layer_desc), I32, I32,
                                   I32, I32, I32, I32, I32,
                                   ctypes.POINTER(P)],
+        "st_create_net_ex": [ctypes.POINTER(st_layer_desc), I32, I32, I32,
+                             I32, I32, I32, I32, ctypes.c_uint32,
+                             ctypes.POINTER(P)],
+        "st_debug_carry": [P, I32, P, I64],
         "st_encode_chunk": [P, P, I32, ctypes.POINTER(ctypes.c_float), P, P],
         "st_workspace_bytes": [P, ctypes.POINTER(U64)],
         "st_bind_workspace": [P, P, U64, P],
@@ -149,6 +153,19 @@ def st_create_net_chunked(layers: Sequence[st_layer_desc], batch,
     _check(_lib.st_create_net_chunked(arr, len(layers), batch, max_frames,
                                       in_h, in_w, in_c, dtype,
                                       ctypes.byref(out)))
+    return out.value
+
+
+NET_RESIDUAL_CARRY = 1
+
+
+def st_create_net_ex(layers: Sequence[st_layer_desc], batch, max_frames,
+                     in_h, in_w, in_c, dtype, flags) -> int:
+    arr = (st_layer_desc * len(layers))(*layers)
+    out = ctypes.c_void_p()
+    _check(_lib.st_create_net_ex(arr, len(layers), batch, max_frames, in_h,
+                                 in_w, in_c, dtype, flags,
+                                 ctypes.byref(out)))
     return out.value
 
 
@@ -263,6 +280,13 @@ def st_debug_state(net, layer, shape) -> np.ndarray:
     P = np.zeros(shape, np.float32)
     _check(_lib.st_debug_state(net, layer, P.ctypes.data, P.size), net)
     return P
+
+
+def st_debug_carry(net, layer, shape) -> np.ndarray:
+    """Consumers' view of layer `layer`'s emitted tensor (residual carry)."""
+    V = np.zeros(shape, np.float32)
+    _check(_lib.st_debug_carry(net, layer, V.ctypes.data, V.size), net)
+    return V
 
 
 def st_debug_counters(net, n_layers):

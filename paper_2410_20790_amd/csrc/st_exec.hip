@@ -187,6 +187,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
   a.mdone = ws.at<uint32_t>(net->off_mdone);
   a.keep_thr = thr;
   a.keep_thr_dev = thr_dev;
+  a.yhat = net->carry && !own_rows ? ws.at<float>(L.off_yhat) : nullptr;
   a.zero = ws.at<char>(net->off_zero);
   a.part = ws.at<float>(net->off_part);
   a.split_max = L.split_max;
@@ -222,6 +223,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
     pa.cp = L.cout_p;
     pa.act = d.act;
     pa.ref = ref ? 1 : 0;
+    pa.yhat = net->carry ? ws.at<float>(L.off_yhat) : nullptr;
     launch_pool_emit(pf, s, net->dtype, pa);
     launch_commit(pf, s, O, cO, L.conv_grid, ws.at<float>(L.off_P),
                   ws.at<float>(L.off_dP), L.cout_p, ref ? 1 : 0);
@@ -261,6 +263,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
     sa.nchunk = L.se_nchunk;
     sa.keep_thr = thr;
     sa.keep_thr_dev = thr_dev;
+    sa.yhat = net->carry ? ws.at<float>(L.off_yhat) : nullptr;
     launch_se(pf, s, net->dtype, sa);
   }
   if (L.pool || L.dw)
@@ -283,6 +286,11 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
   la.cnt_act = cnt + out.cnt_act;
   la.cons = consumers_of(net, i + 1);
   launch_list_compact(pf, s, la);
+  // residual carry: the kept rows join the consumers' view
+  if (net->carry)
+    launch_carry_commit(pf, s, net->dtype, la.act, la.cnt_act, out.grid,
+                        la.map, ws.at<char>(out.off_rows),
+                        ws.at<float>(L.off_yhat), L.cout_p);
   out.last_thr = thr;
   return true;
 }
@@ -302,6 +310,14 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
   (void)hipGetLastError();  // clear any stale error
 
   launch_reset(pf, s, cnt, net->n_counters);
+  // residual carry: the reference frame's rows (every site) become the
+  // consumers' whole view
+  if (ref && net->carry)
+    for (const LayerPlan& L : net->layers)
+      launch_fill_u32(s, ws.at<float>(L.off_yhat),
+                      net->tensors[&L - net->layers.data() + 1].grid *
+                          L.cout_p,
+                      0u);
   TensorPlan& T0 = net->tensors[0];
   const float thr0 = ref ? -1.f : thr_dev ? 0.f : thr[0];
   ScanArgs sa{};
@@ -1011,6 +1027,27 @@ extern "C" st_status st_debug_state(st_net* net, int32_t layer, float* P,
   if (st != ST_OK) return st;
   for (int64_t p = 0; p < L.conv_grid; ++p)
     std::memcpy(P + p * L.d.c_out, raw.data() + p * L.cout_p,
+                sizeof(float) * L.d.c_out);
+  return ST_OK;
+}
+
+extern "C" st_status st_debug_carry(st_net* net, int32_t layer, float* view,
+                                    int64_t cap) {
+  st_status st = debug_prelude(net, layer, true);
+  if (st != ST_OK) return st;
+  if (!net->carry)
+    return fail(net, ST_ERR_STATE, "not a residual-carry net");
+  if (layer < 0 || !view)
+    return fail(net, ST_ERR_INVALID_ARG, "bad layer or view");
+  const LayerPlan& L = net->layers[layer];
+  const int64_t grid = net->tensors[layer + 1].grid;
+  if (cap < grid * L.d.c_out)
+    return fail(net, ST_ERR_INVALID_ARG, "view buffer too small");
+  std::vector<float> raw((size_t)grid * L.cout_p);
+  st = d2h(net, raw.data(), net->ws + L.off_yhat, raw.size());
+  if (st != ST_OK) return st;
+  for (int64_t p = 0; p < grid; ++p)
+    std::memcpy(view + p * L.d.c_out, raw.data() + p * L.cout_p,
                 sizeof(float) * L.d.c_out);
   return ST_OK;
 }

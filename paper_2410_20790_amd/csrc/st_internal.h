@@ -94,6 +94,7 @@ struct LayerPlan {
   size_t off_flags = 0;             // uint8 [conv_grid] affected-output flags
   size_t off_pflags = 0;            // uint8 [pooled grid] (pooled layers)
   int cnt_O = 0, cnt_pairs = 0;
+  size_t off_yhat = 0;              // residual carry: f32 [out grid][cout_p]
   int cnt_sites = 0;                // chunk mode: sites whose state a fused
                                     // GEMM updated (site runs)
 };
@@ -123,6 +124,7 @@ struct st_net {
   size_t off_ibst_ctl = 0;                 // uint8 controlled flags
   size_t off_ibst_sites = 0;               // int64 sites per tensor
   bool ibst_on = false;
+  bool carry = false;                      // residual-carry semantics
   double ibst_target = 0.9, ibst_eps = 0.025, ibst_theta_max = 1.0;
   // chunk mode (F > 1): f32 deferred updates of the current layer (shared),
   // per input item the frame whose value X_hat held (0xFF: the X_hat of

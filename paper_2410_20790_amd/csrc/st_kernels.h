@@ -140,6 +140,10 @@ struct ConvArgs {
   // tiles in part [split][capO][cout_p]; split_max = 1: no split
   float* part;
   int split_max;
+  // residual carry: the consumers' view of the emitted tensor ([grid]
+  // [cout_p] f32, pixel-indexed) or NULL; diff-pass state-mode emissions
+  // are f(P_new) - view instead of f(P_new) - f(P_old)
+  const float* yhat;
   // kModeChunkState: row tile j is [tstart[j], tstart[j + 1]) (tiles step
   // chunk_tile_step(nf) rows); a row's site is its item modulo `per`
   const uint32_t* tstart;
@@ -164,6 +168,7 @@ struct PoolArgs {
   void* dout;
   uint32_t* rowmax;
   int cp, act, ref;
+  const float* yhat;    // residual carry view (pooled grid) or NULL
 };
 void launch_pool_emit(const Prof& pf, hipStream_t s, int dtype,
                       const PoolArgs& a);
@@ -212,6 +217,7 @@ struct SeArgs {
   int N, cp, c, mid, act, ref, chunk, nchunk, tps;
   float keep_thr;
   const float* keep_thr_dev;  // in device memory (or NULL: keep_thr)
+  const float* yhat;          // residual carry view or NULL
 };
 void launch_se(const Prof& pf, hipStream_t s, int dtype, const SeArgs& a);
 // Storage-dtype matrix src [rows][cols] (or, transposed, src [cols][rows])
@@ -292,6 +298,14 @@ void launch_repack_dw(hipStream_t s, int dtype, const void* w, float* wdw,
                       int c, int kh, int kw, int cp);
 void launch_bias(hipStream_t s, int dtype, const void* b, float* out,
                  int cout, int cout_p);
+// ---- residual carry: the kept rows of an emitted tensor reach the
+// consumers, so they join the view: view[pix] += row (f32) for every kept
+// row (act[k] = pix, map[pix] = its row).
+void launch_carry_commit(const Prof& pf, hipStream_t s, int dtype,
+                         const int* act, const u64* n_act, int64_t cap,
+                         const int* map, const void* rows, float* view,
+                         int cp);
+
 // ---- online threshold adjustment on the device
 // Per tensor t: bisection state theta/lo/hi (f64), the f32 threshold the
 // kernels read, a controlled flag, and the tensor's site count.  After a

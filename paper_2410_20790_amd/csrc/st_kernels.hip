@@ -615,6 +615,7 @@ void launch_group_count(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
 struct EpiIn {
   float po;  // old state (state mode, diff pass)
   float sk;  // residual delta
+  float yh;  // consumers' view (residual carry, diff pass)
 };
 
 template <typename T, bool REF>
@@ -625,14 +626,16 @@ struct Epi {
   const float* bias;
   const T* dskip;
   const int* mskip;
+  const float* yhat;
   int cout_p, mode, act;
 
   // Phase 1: every global load one output element needs.  Callers issue
   // the loads of all their elements before any store, so the loads overlap
   // instead of each waiting behind a store that might alias it.
   __device__ __forceinline__ EpiIn load(int pix, int n) const {
-    EpiIn e{0.f, 0.f};
+    EpiIn e{0.f, 0.f, 0.f};
     if (mode == 0 && !REF) e.po = P[(int64_t)pix * cout_p + n];
+    if (mode == 0 && !REF && yhat) e.yh = yhat[(int64_t)pix * cout_p + n];
     if (mskip) {
       const int r = mskip[pix];
       if (r >= 0) e.sk = to_f(dskip[(int64_t)r * cout_p + n]);
@@ -657,7 +660,7 @@ struct Epi {
     if (mode == 0) {
       const float pn = in.po + dp;
       P[(int64_t)pix * cout_p + n] = pn;
-      d = act_f(pn, act) - act_f(in.po, act);
+      d = act_f(pn, act) - (!REF && yhat ? in.yh : act_f(in.po, act));
     }
     const T q = from_f<T>(d);
     dout[o * cout_p + n] = q;
@@ -668,7 +671,7 @@ struct Epi {
 template <typename T, bool REF>
 __device__ __forceinline__ Epi<T, REF> make_epi(const ConvArgs& a) {
   return Epi<T, REF>{a.P, a.dP, (T*)a.dout, a.bias, (const T*)a.dskip,
-                     a.mskip, a.cout_p, a.mode, a.act};
+                     a.mskip, a.yhat, a.cout_p, a.mode, a.act};
 }
 
 // --------------------------------------------------- (c) gather-GEMM MFMA
@@ -826,10 +829,21 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
     if (a.mode == 0) {
       float po[8], pn[8];
       load_po(h, po);
+      if (!REF && a.yhat) {
+        // residual carry: against what the consumers received
+        float yh[8];
+        load8f(a.yhat + (int64_t)epix * cout_p + n, yh);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        pn[e] = po[e] + v[e];
-        v[e] = act_f(pn[e], a.act) - act_f(po[e], a.act);
+        for (int e = 0; e < 8; ++e) {
+          pn[e] = po[e] + v[e];
+          v[e] = act_f(pn[e], a.act) - yh[e];
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          pn[e] = po[e] + v[e];
+          v[e] = act_f(pn[e], a.act) - act_f(po[e], a.act);
+        }
       }
       store8f(a.P + (int64_t)epix * cout_p + n, pn);
     }
@@ -1611,6 +1625,8 @@ __global__ __launch_bounds__(256) void k_pool_emit(PoolArgs a) {
         mn = fmaxf(mn, act_f(pn, a.act));
       }
     }
+    // residual carry: against what the consumers received
+    if (a.yhat && !a.ref) mo = a.yhat[(int64_t)p * a.cp + c];
     const T qv = from_f<T>(mn - mo);
     dout[q * a.cp + c] = qv;
     const float ab = fabsf(to_f(qv));
@@ -1906,12 +1922,16 @@ __global__ __launch_bounds__(256) void k_se_emit(SeArgs a) {
         for (int e = 0; e < 8; ++e) dp[e] = 0.f;
       }
       load8f(sn + c0, gn);
-      load8f(so + c0, go);
+      const bool carry = a.yhat && !a.ref;
+      // residual carry: against what the consumers received
+      load8f(carry ? a.yhat + row * cp + c0 : so + c0, go);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         pn[e] = po[e] + dp[e];
         const float en = act_f(pn[e], a.act) * gn[e];
-        const float eo = a.ref ? 0.f : act_f(po[e], a.act) * go[e];
+        const float eo = a.ref     ? 0.f
+                         : carry   ? go[e]
+                                   : act_f(po[e], a.act) * go[e];
         d[e] = en - eo;
       }
       rm = fmaxf(rm, Vec8<T>::store(dout + row * cp + c0, d));
@@ -2532,6 +2552,50 @@ void launch_bias(hipStream_t s, int dtype, const void* b, float* out,
 
 // Per-image kept counts of an ascending pixel list (binary search of the
 // image boundaries).
+// ------------------------------------------------------- residual carry
+template <typename T>
+__global__ __launch_bounds__(256) void k_carry_commit(const int* act,
+                                                     const u64* n_act,
+                                                     const int* map,
+                                                     const T* rows,
+                                                     float* view, int cp) {
+  const int64_t n = (int64_t)*n_act;
+  const int c4 = cp / 4;
+  const int64_t total = n * c4;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    const int64_t k = idx / c4;
+    const int c = (int)(idx - k * c4) * 4;
+    const int pix = act[k];
+    const T* rv = rows + (int64_t)map[pix] * cp + c;
+    float4* vp = (float4*)(view + (int64_t)pix * cp + c);
+    float4 v = *vp;
+    v.x += to_f(rv[0]);
+    v.y += to_f(rv[1]);
+    v.z += to_f(rv[2]);
+    v.w += to_f(rv[3]);
+    *vp = v;
+  }
+}
+
+void launch_carry_commit(const Prof& pf, hipStream_t s, int dtype,
+                         const int* act, const u64* n_act, int64_t cap,
+                         const int* map, const void* rows, float* view,
+                         int cp) {
+  const int grid = grid_for(cap * (cp / 4), 8192);
+  prof_begin(pf, 25 /*ST_K_CARRY_COMMIT*/, s);
+  if (dtype == 0)
+    k_carry_commit<float><<<grid, 256, 0, s>>>(act, n_act, map,
+                                              (const float*)rows, view, cp);
+  else if (dtype == 1)
+    k_carry_commit<_Float16><<<grid, 256, 0, s>>>(
+        act, n_act, map, (const _Float16*)rows, view, cp);
+  else
+    k_carry_commit<bf16_t><<<grid, 256, 0, s>>>(act, n_act, map,
+                                               (const bf16_t*)rows, view, cp);
+  prof_end(pf, 25, s);
+}
+
 // ------------------------------------------- online threshold adjustment
 // One bisection step per controlled tensor, in f64 as the host controller
 // takes it; the f32 threshold is theta rounded to nearest.

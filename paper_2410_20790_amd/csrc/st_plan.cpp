@@ -48,7 +48,7 @@ static st_status create_fail(st_status s, const std::string& msg) {
 static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
                              int32_t batch, int32_t max_frames, int32_t in_h,
                              int32_t in_w, int32_t in_c, int32_t dtype,
-                             st_net** out) {
+                             uint32_t flags, st_net** out) {
   if (!out) return create_fail(ST_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   if (!layers || n_layers < 1)
@@ -59,6 +59,12 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
     return create_fail(ST_ERR_INVALID_ARG, "max_frames must be in [1, 32]");
   if (dtype != ST_F32 && dtype != ST_F16 && dtype != ST_BF16)
     return create_fail(ST_ERR_INVALID_ARG, "unknown dtype");
+  if (flags & ~(uint32_t)ST_NET_RESIDUAL_CARRY)
+    return create_fail(ST_ERR_INVALID_ARG, "unknown flag");
+  const bool carry = (flags & ST_NET_RESIDUAL_CARRY) != 0;
+  if (carry && max_frames > 1)
+    return create_fail(ST_ERR_UNSUPPORTED,
+                       "residual carry needs frame-by-frame encoding");
   const int64_t F = max_frames;
   if ((int64_t)batch * in_h * in_w * F >= (int64_t)1 << 31)
     return create_fail(ST_ERR_INVALID_ARG, "input grid exceeds 2^31 pixels");
@@ -72,6 +78,7 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
   net->esize = esize_of(dtype);
   net->N = batch; net->H = in_h; net->W = in_w; net->C = in_c;
   net->F = max_frames;
+  net->carry = carry;
   net->layers.resize(n_layers);
   net->tensors.resize(n_layers + 1);
 
@@ -153,7 +160,10 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
     if (L.se && L.cout_p > kSeMaxChannels)
       return bad(ST_ERR_UNSUPPORTED, i,
                  "squeeze-excitation on more than 2048 channels");
-    L.stateful = d.act != ST_ACT_NONE || L.pool || L.se || i == n_layers - 1;
+    // with residual carry every layer keeps its pre-activation (a layer
+    // without non-linearity emits P_new minus the consumers' view)
+    L.stateful = d.act != ST_ACT_NONE || L.pool || L.se ||
+                 i == n_layers - 1 || carry;
     L.mode = (L.pool || L.se) ? kModeDefer
                               : (L.stateful ? kModeState : kModeLinear);
     L.ident = d.k_h == 1 && d.k_w == 1 && d.s_h == 1 && d.s_w == 1 &&
@@ -231,6 +241,7 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
     }
     L.off_nbr = a.take(sizeof(int32_t) * citems * L.K);
     if (L.stateful) L.off_P = a.take(sizeof(float) * L.conv_grid * L.cout_p);
+    if (carry) L.off_yhat = a.take(sizeof(float) * T.grid * L.cout_p);
     if (L.dw)
       L.off_w = a.take(sizeof(float) * L.K * L.cout_p);
     else
@@ -298,7 +309,17 @@ extern "C" st_status st_create_net(const st_layer_desc* layers,
                                    int32_t in_h, int32_t in_w, int32_t in_c,
                                    int32_t dtype, st_net** out) {
   return create_impl(layers, n_layers, batch, 1, in_h, in_w, in_c, dtype,
-                     out);
+                     0u, out);
+}
+
+extern "C" st_status st_create_net_ex(const st_layer_desc* layers,
+                                      int32_t n_layers, int32_t batch,
+                                      int32_t max_frames, int32_t in_h,
+                                      int32_t in_w, int32_t in_c,
+                                      int32_t dtype, uint32_t flags,
+                                      st_net** out) {
+  return create_impl(layers, n_layers, batch, max_frames, in_h, in_w, in_c,
+                     dtype, flags, out);
 }
 
 extern "C" st_status st_create_net_chunked(const st_layer_desc* layers,
@@ -307,7 +328,7 @@ extern "C" st_status st_create_net_chunked(const st_layer_desc* layers,
                                            int32_t in_w, int32_t in_c,
                                            int32_t dtype, st_net** out) {
   return create_impl(layers, n_layers, batch, max_frames, in_h, in_w, in_c,
-                     dtype, out);
+                     dtype, 0u, out);
 }
 
 extern "C" st_status st_workspace_bytes(const st_net* net, uint64_t* bytes) {

@@ -32,10 +32,12 @@ def layer_desc(L, w_ptr: int, b_ptr: Optional[int],
 class SparseTemNet:
     """One diff encoder: reference frame via ``encode_reference``, then
     diff frames via ``encode_diff``, or up to ``max_frames`` of them at once
-    via ``encode_chunk`` (see include/sparsetem.h)."""
+    via ``encode_chunk`` (see include/sparsetem.h).  ``carry``: residual
+    carry (ST_NET_RESIDUAL_CARRY; frame by frame only)."""
 
     def __init__(self, layers: Sequence, batch: int, H: int, W: int, C: int,
-                 dtype: str = "f32", device="cuda", max_frames: int = 1):
+                 dtype: str = "f32", device="cuda", max_frames: int = 1,
+                 carry: bool = False):
         self.dtype = dtype
         self.tdtype = TORCH_DTYPES[dtype]
         dev = torch.device(device)
@@ -65,7 +67,12 @@ class SparseTemNet:
             descs.append(layer_desc(L, w.data_ptr(),
                                     None if b is None else b.data_ptr(), se))
         self.max_frames = max_frames
-        if max_frames > 1:
+        self.carry = carry
+        if carry:
+            self.handle = B.st_create_net_ex(descs, batch, max_frames, H, W,
+                                             C, B.DTYPE_CODES[dtype],
+                                             B.NET_RESIDUAL_CARRY)
+        elif max_frames > 1:
             self.handle = B.st_create_net_chunked(descs, batch, max_frames,
                                                   H, W, C,
                                                   B.DTYPE_CODES[dtype])

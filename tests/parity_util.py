@@ -45,11 +45,21 @@ def to_dev(frame, dtype):
         "cuda", TORCH[dtype]).contiguous()
 
 
-def make_pair(net):
+def make_pair(net, carry=False):
     o = oracle.OracleNet(net.layers, net.batch, net.H, net.W, net.C,
-                         net.dtype)
-    g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, net.dtype)
+                         net.dtype, carry=carry)
+    g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, net.dtype,
+                     carry=carry)
     return o, g
+
+
+def check_views(net, o, g, tag):
+    """Residual carry: every layer's consumers' view on the GPU against the
+    oracle's (valid while no keep decision has differed)."""
+    for i in range(len(net.layers)):
+        V = B.st_debug_carry(g.handle, i, o.Y[i].shape)
+        e = rel(V, o.Y[i])
+        assert e <= RTOL[net.dtype], f"{tag}: view of layer {i}: {e}"
 
 
 def compare_frame(net, o, g, out_g, tag, check_rulebook=True):
@@ -136,9 +146,10 @@ def check_rulebooks(net, o, g, tag):
         assert pairs[i] == o.last["layers"][i]["pairs"]
 
 
-def run_chunk(net, frames, thr, tag, max_band=0):
-    """Encode a chunk on both sides and compare after every frame."""
-    o, g = make_pair(net)
+def run_chunk(net, frames, thr, tag, max_band=0, carry=False):
+    """Encode a chunk on both sides and compare after every frame (with
+    carry, also the consumers' views while no keep decision differed)."""
+    o, g = make_pair(net, carry)
     try:
         thr_l = [thr] * (len(net.layers) + 1) if np.isscalar(thr) else thr
         say(f"[gpu] {tag}: reference frame")
@@ -157,6 +168,8 @@ def run_chunk(net, frames, thr, tag, max_band=0):
             out_g = g.encode_diff(to_dev(frames[t], net.dtype), thr_l)
             torch.cuda.synchronize()
             total_band += compare_frame(net, o, g, out_g, f"{tag} f{t}")
+            if carry and total_band == 0:
+                check_views(net, o, g, f"{tag} f{t}")
             for t2 in range(len(net.layers) + 1):
                 dg = g.density(t2 - 1)
                 do = o.density(t2)

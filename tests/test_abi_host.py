@@ -235,3 +235,35 @@ def test_threshold_control_needs_a_bound_net():
             B.st_set_threshold_control(h, [1] * n, [0.0] * (n - 1))
     finally:
         B.st_destroy_net(h)
+
+
+def test_residual_carry_flag():
+    """ST_NET_RESIDUAL_CARRY adds one f32 view per layer output (and a state
+    for layers without non-linearity); it needs frame-by-frame encoding;
+    unknown flags are rejected."""
+    net = resnet_mini_net()
+    d = descs(net)
+    h0 = B.st_create_net(d, net.batch, net.H, net.W, net.C, B.ST_F32)
+    h1 = B.st_create_net_ex(d, net.batch, 1, net.H, net.W, net.C, B.ST_F32,
+                            B.NET_RESIDUAL_CARRY)
+    try:
+        extra = B.st_workspace_bytes(h1) - B.st_workspace_bytes(h0)
+        views = 0
+        for L in net.layers:
+            views += 4 * 8 * ((L.c_out + 7) // 8)   # lower bound per site
+        assert extra >= views
+        with pytest.raises(B.StError) as e:
+            B.st_debug_carry(h0, 0, (1,))
+        assert e.value.status == B.ST_ERR_STATE
+    finally:
+        B.st_destroy_net(h0)
+        B.st_destroy_net(h1)
+    for flags, status in ((2, B.ST_ERR_INVALID_ARG),):
+        with pytest.raises(B.StError) as e:
+            B.st_create_net_ex(d, net.batch, 1, net.H, net.W, net.C,
+                               B.ST_F32, flags)
+        assert e.value.status == status
+    with pytest.raises(B.StError) as e:
+        B.st_create_net_ex(d, net.batch, 4, net.H, net.W, net.C, B.ST_F32,
+                           B.NET_RESIDUAL_CARRY)
+    assert e.value.status == B.ST_ERR_UNSUPPORTED
