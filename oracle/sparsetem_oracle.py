@@ -32,6 +32,10 @@ Readings of points the paper leaves open (all listed in the design notes):
    or gated; P itself for a layer without non-linearity, which then keeps
    P too), kept rows add their rounded delta to Y_hat and truncated rows
    carry their residual until the site is affected again.
+   Optional frozen squeeze-excitation (``frozen_se=True``, an approximation
+   of reading 6, flagged as inexact): the gates s computed in the reference
+   frame are kept for the diff frames of the chunk, so the layer emits
+   f(P_new) * s - f(P_old) * s at its affected sites only.
 4. One threshold per produced tensor: ``thr[0]`` masks the frame delta,
    ``thr[j+1]`` masks layer j's emitted delta (shared by all consumers).
 5. Bias enters only the reference pass; it cancels in deltas (Eq. 2).
@@ -284,12 +288,16 @@ def dense_forward(layers, frame, dtype, with_se=False, all_pre=False):
 class OracleNet:
     """Stateful diff encoder over one stream of frames (batch N images)."""
 
-    def __init__(self, layers, batch, H, W, C, dtype="f32", carry=False):
+    def __init__(self, layers, batch, H, W, C, dtype="f32", carry=False,
+                 frozen_se=False):
         if dtype not in ("f32", "f16", "bf16"):
             raise ValueError(dtype)
+        if carry and frozen_se:
+            raise ValueError("carry and frozen_se are exclusive")
         self.layers = list(layers)
         self.dtype = dtype
         self.carry = carry
+        self.frozen_se = frozen_se
         self.in_shape = (batch, H, W, C)
         shapes = {-1: self.in_shape}
         self.geo = []
@@ -390,7 +398,16 @@ class OracleNet:
                 Pg = self.P[i].reshape(N * g.Ho * g.Wo, L.c_out)
                 P_old = Pg[O].copy()
                 P_new = f32(P_old.astype(np.float64) + dP32)
-                if L.se_mid:
+                if L.se_mid and self.frozen_se:
+                    # frozen gates: a per-image, per-channel scale
+                    Pg[O] = P_new
+                    s = self.S[i].reshape(N, L.c_out)[O // (g.Ho * g.Wo)]
+                    d32 = f32(f32(activation(P_new, L.act).astype(np.float64)
+                                  * s)
+                              - f32(activation(P_old, L.act).astype(np.float64)
+                                    * s))
+                    cand = O
+                elif L.se_mid:
                     # Squeeze-excitation (reading 6): the gates follow the
                     # dense activation, so every site's output moves:
                     # delta = f(P_new) * s_new - f(P_old) * s_old.
