@@ -133,12 +133,21 @@ enum {
    * is affected again, so what consumers see never strays from the dense
    * value by more than the threshold.  Frame by frame only
    * (max_frames = 1). */
-  ST_NET_RESIDUAL_CARRY = 1
+  ST_NET_RESIDUAL_CARRY = 1,
+  /* Frozen squeeze-excitation (an approximation, not the exact semantics):
+   * the gates computed densely in the reference frame are kept for the
+   * chunk's diff frames, so a squeeze-excitation layer emits
+   * f(P_new) * s - f(P_old) * s at its affected sites only, with no dense
+   * pass per frame.  Exclusive with ST_NET_RESIDUAL_CARRY; with it the
+   * chunk entry also takes squeeze-excitation nets (last layer without
+   * it). */
+  ST_NET_FROZEN_SE = 2
 };
 
 /* As st_create_net_chunked, with creation flags (ST_NET_*).  Errors as
- * st_create_net_chunked, plus ST_ERR_INVALID_ARG for an unknown flag and
- * ST_ERR_UNSUPPORTED for ST_NET_RESIDUAL_CARRY with max_frames > 1. */
+ * st_create_net_chunked, plus ST_ERR_INVALID_ARG for an unknown flag or
+ * both flags, and ST_ERR_UNSUPPORTED for ST_NET_RESIDUAL_CARRY with
+ * max_frames > 1. */
 st_status st_create_net_ex(const st_layer_desc* layers, int32_t n_layers,
                            int32_t batch, int32_t max_frames, int32_t in_h,
                            int32_t in_w, int32_t in_c, int32_t dtype,
@@ -194,7 +203,8 @@ st_status st_encode_diff(st_net* net, const void* frame, const float* thr,
  * Errors: ST_ERR_STATE (no workspace or no reference), ST_ERR_INVALID_ARG
  * (NULL, NaN threshold, n_frames outside [1, max_frames]),
  * ST_ERR_UNSUPPORTED (a net created without chunk capacity, more than 16
- * input channels, squeeze-excitation layers, a pooled last layer),
+ * input channels, squeeze-excitation layers unless the net was created
+ * with ST_NET_FROZEN_SE, a pooled or squeeze-excitation last layer),
  * ST_ERR_HIP. */
 st_status st_encode_chunk(st_net* net, const void* frames, int32_t n_frames,
                           const float* thr, float* out, void* stream);

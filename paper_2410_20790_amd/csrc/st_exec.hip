@@ -133,9 +133,12 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
   u64* cO = cnt + L.cnt_O;
   u64* cpairs = cnt + L.cnt_pairs;
   uint32_t* rowmax_out = ws.at<uint32_t>(out.off_rowmax);
-  // pooled and squeeze-excitation layers emit rows of their own (pooled
-  // sites / every site), not the affected conv outputs
-  const bool own_rows = L.pool || L.se;
+  // frozen squeeze-excitation in a diff frame: a state-mode layer whose
+  // emitted values are scaled by the reference frame's gates
+  const bool frozen = L.se && net->frozen_se && !ref;
+  // pooled and (exact) squeeze-excitation layers emit rows of their own
+  // (pooled sites / every site), not the affected conv outputs
+  const bool own_rows = L.pool || (L.se && !frozen);
   uint32_t* rm_O = own_rows ? nullptr : rowmax_out;
 
   // (b) rulebook: the flags were set while the producers emitted their kept
@@ -180,10 +183,14 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
     a.dskip = ws.at<char>(R.off_rows);
     a.mskip = ws.at<int>(R.off_map);
   }
-  a.mode = L.mode;
+  a.mode = frozen ? kModeState : L.mode;
   a.act = d.act;
   a.ref = ref ? 1 : 0;
-  a.grp = (L.pool || L.dw || L.se) ? nullptr : grp;
+  a.grp = (L.pool || L.dw || own_rows) ? nullptr : grp;
+  if (frozen) {
+    a.gate = ws.at<float>(L.off_ses) + L.se_par * (int64_t)net->N * L.cout_p;
+    a.gate_hw = (int64_t)L.Ho * L.Wo;
+  }
   a.mdone = ws.at<uint32_t>(net->off_mdone);
   a.keep_thr = thr;
   a.keep_thr_dev = thr_dev;
@@ -228,7 +235,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
     launch_commit(pf, s, O, cO, L.conv_grid, ws.at<float>(L.off_P),
                   ws.at<float>(L.off_dP), L.cout_p, ref ? 1 : 0);
   }
-  if (L.se) {
+  if (L.se && !frozen) {
     SeArgs sa{};
     sa.P = ws.at<float>(L.off_P);
     sa.dP = ws.at<float>(L.off_dP);
@@ -266,10 +273,9 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
     sa.yhat = net->carry ? ws.at<float>(L.off_yhat) : nullptr;
     launch_se(pf, s, net->dtype, sa);
   }
-  if (L.pool || L.dw)
-    if (!L.se)
-      launch_group_count(pf, s, rowmax_out, cnt + out.cnt_rows, out.grid,
-                         thr, thr_dev, grp);
+  if ((L.pool || L.dw) && !(L.se && !frozen))
+    launch_group_count(pf, s, rowmax_out, cnt + out.cnt_rows, out.grid,
+                       thr, thr_dev, grp);
 
   // truncation of the emitted delta (shared by every consumer), which also
   // prepares the consumers' rulebooks
@@ -350,16 +356,18 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
     const LayerPlan& L = net->layers[nl - 1];
     const Geo g = L.pool ? pool_geo(L) : Geo{L.Ho, L.Wo, L.Ho, L.Wo, 1, 1,
                                              1, 1, 0, 0};
+    // the gates this frame used: just computed (exact), or kept from the
+    // reference frame (frozen)
+    const int par = (ref || !net->frozen_se) ? (L.se_par ^ 1) : L.se_par;
     const float* se =
-        L.se ? ws.at<float>(L.off_ses) +
-                   (L.se_par ^ 1) * (int64_t)net->N * L.cout_p
+        L.se ? ws.at<float>(L.off_ses) + par * (int64_t)net->N * L.cout_p
              : nullptr;
     launch_output(Prof{net, nl - 1}, s, ws.at<float>(L.off_P), L.cout_p,
                   L.d.c_out, net->N, g, L.pool ? 1 : 0, L.d.act, se, out);
   }
   // the gates just computed become the previous frame's
   for (LayerPlan& L : net->layers)
-    if (L.se) L.se_par ^= 1;
+    if (L.se && (ref || !net->frozen_se)) L.se_par ^= 1;
   launch_cleanup(pf, s, ws.at<CleanEntry>(net->off_cleanup), net->n_cleanup,
                  net->ws, cnt, net->max_grid);
   // online adjustment: a reference frame starts a new cycle; after a diff
@@ -428,7 +436,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
   // depthwise layers, layers with a split reduction and the output layer
   // (which also writes every frame's dense output) defer them to the
   // update kernel.
-  const bool fused = L.stateful && !L.pool && !L.dw && !out &&
+  const bool fused = L.stateful && !L.pool && !L.dw && !L.se && !out &&
                      L.split_max <= 1;
 
   if (!L.ident) {
@@ -517,6 +525,10 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
     u.c = d.c_out;
     u.act = d.act;
     u.pool_mode = L.pool ? 1 : 0;
+    if (L.se) {  // frozen gates (the chunk entry takes no exact SE)
+      u.gate = ws.at<float>(L.off_ses) + L.se_par * (int64_t)net->N * L.cout_p;
+      u.gate_hw = (int64_t)L.Ho * L.Wo;
+    }
     u.tps = se_threads_per_site(L.cout_p);
     launch_chunk_update(pf, s, net->dtype, u);
   }
@@ -683,7 +695,7 @@ extern "C" st_status st_bind_workspace(st_net* net, void* dev_ptr,
                              T.cnt_rows, 0, 0});
   for (const LayerPlan& L : net->layers) {
     const st_layer_desc& d = L.d;
-    if (L.pool || L.se) {
+    if (L.pool || (L.se && !net->frozen_se)) {
       launch_fill_u32(s, ws.at<int>(L.off_Mo), L.conv_grid * net->F,
                       0xFFFFFFFFu);
       tab.push_back(CleanEntry{(int64_t)L.off_Mo, (int64_t)L.off_O, L.cnt_O,
@@ -760,12 +772,16 @@ extern "C" st_status st_encode_chunk(st_net* net, const void* frames,
   if (net->C > kChunkMaxInC)
     return fail(net, ST_ERR_UNSUPPORTED,
                 "chunks need at most 16 input channels");
+  // exact squeeze-excitation couples every site of a frame; with frozen
+  // gates it is a per-channel scale and batches like any layer
   for (const LayerPlan& L : net->layers)
-    if (L.se)
+    if (L.se && !net->frozen_se)
       return fail(net, ST_ERR_UNSUPPORTED,
-                  "squeeze-excitation layers are encoded frame by frame");
-  if (net->layers[nl - 1].pool)
-    return fail(net, ST_ERR_UNSUPPORTED, "a pooled last layer in a chunk");
+                  "squeeze-excitation layers are encoded frame by frame "
+                  "(unless created with ST_NET_FROZEN_SE)");
+  if (net->layers[nl - 1].pool || net->layers[nl - 1].se)
+    return fail(net, ST_ERR_UNSUPPORTED,
+                "a pooled or squeeze-excitation last layer in a chunk");
   return encode_chunk(net, frames, n_frames, thr, out, (hipStream_t)stream);
 }
 

@@ -125,6 +125,7 @@ struct st_net {
   size_t off_ibst_sites = 0;               // int64 sites per tensor
   bool ibst_on = false;
   bool carry = false;                      // residual-carry semantics
+  bool frozen_se = false;                  // frozen squeeze-excitation gates
   double ibst_target = 0.9, ibst_eps = 0.025, ibst_theta_max = 1.0;
   // chunk mode (F > 1): f32 deferred updates of the current layer (shared),
   // per input item the frame whose value X_hat held (0xFF: the X_hat of

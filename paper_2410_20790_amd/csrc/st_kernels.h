@@ -149,6 +149,11 @@ struct ConvArgs {
   const uint32_t* tstart;
   int nf;
   int64_t per;
+  // frozen squeeze-excitation: per-image gates [N][cout_p] scaling both
+  // emitted values of a state-mode emission (image = site / gate_hw), or
+  // NULL
+  const float* gate;
+  int64_t gate_hw;
 };
 // Returns false (and launches nothing) when a.zero is missing or misaligned.
 bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
@@ -259,6 +264,8 @@ struct ChunkUpdArgs {
   float* out;          // dense output [nf][npix][c] or NULL
   int64_t npix;        // conv sites per frame
   int nf, cp, c, act, pool_mode, tps;
+  const float* gate;    // frozen squeeze-excitation gates [N][cp] or NULL
+  int64_t gate_hw;      // sites per image of the conv grid
 };
 void launch_chunk_update(const Prof& pf, hipStream_t s, int dtype,
                          const ChunkUpdArgs& a);

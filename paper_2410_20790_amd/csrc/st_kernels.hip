@@ -616,6 +616,7 @@ struct EpiIn {
   float po;  // old state (state mode, diff pass)
   float sk;  // residual delta
   float yh;  // consumers' view (residual carry, diff pass)
+  float g;   // frozen squeeze-excitation gate
 };
 
 template <typename T, bool REF>
@@ -627,15 +628,18 @@ struct Epi {
   const T* dskip;
   const int* mskip;
   const float* yhat;
+  const float* gate;
+  int64_t gate_hw;
   int cout_p, mode, act;
 
   // Phase 1: every global load one output element needs.  Callers issue
   // the loads of all their elements before any store, so the loads overlap
   // instead of each waiting behind a store that might alias it.
   __device__ __forceinline__ EpiIn load(int pix, int n) const {
-    EpiIn e{0.f, 0.f, 0.f};
+    EpiIn e{0.f, 0.f, 0.f, 1.f};
     if (mode == 0 && !REF) e.po = P[(int64_t)pix * cout_p + n];
     if (mode == 0 && !REF && yhat) e.yh = yhat[(int64_t)pix * cout_p + n];
+    if (mode == 0 && gate) e.g = gate[(pix / gate_hw) * cout_p + n];
     if (mskip) {
       const int r = mskip[pix];
       if (r >= 0) e.sk = to_f(dskip[(int64_t)r * cout_p + n]);
@@ -660,7 +664,10 @@ struct Epi {
     if (mode == 0) {
       const float pn = in.po + dp;
       P[(int64_t)pix * cout_p + n] = pn;
-      d = act_f(pn, act) - (!REF && yhat ? in.yh : act_f(in.po, act));
+      if (gate)
+        d = act_f(pn, act) * in.g - act_f(in.po, act) * in.g;
+      else
+        d = act_f(pn, act) - (!REF && yhat ? in.yh : act_f(in.po, act));
     }
     const T q = from_f<T>(d);
     dout[o * cout_p + n] = q;
@@ -671,7 +678,8 @@ struct Epi {
 template <typename T, bool REF>
 __device__ __forceinline__ Epi<T, REF> make_epi(const ConvArgs& a) {
   return Epi<T, REF>{a.P, a.dP, (T*)a.dout, a.bias, (const T*)a.dskip,
-                     a.mskip, a.yhat, a.cout_p, a.mode, a.act};
+                     a.mskip, a.yhat, a.gate, a.gate_hw, a.cout_p, a.mode,
+                     a.act};
 }
 
 // --------------------------------------------------- (c) gather-GEMM MFMA
@@ -829,7 +837,16 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
     if (a.mode == 0) {
       float po[8], pn[8];
       load_po(h, po);
-      if (!REF && a.yhat) {
+      if (a.gate) {
+        // frozen squeeze-excitation: both values scaled by the gates
+        float g[8];
+        load8f(a.gate + (epix / a.gate_hw) * cout_p + n, g);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          pn[e] = po[e] + v[e];
+          v[e] = act_f(pn[e], a.act) * g[e] - act_f(po[e], a.act) * g[e];
+        }
+      } else if (!REF && a.yhat) {
         // residual carry: against what the consumers received
         float yh[8];
         load8f(a.yhat + (int64_t)epix * cout_p + n, yh);
@@ -2151,7 +2168,7 @@ void launch_chunk_scan(const Prof& pf, hipStream_t s, int dtype,
 // instead (the pool compares window states per frame) and the frames that
 // updated each site are recorded; the state is committed afterwards.
 // With `out` the dense output f(P) after every frame is written too.
-template <typename T, int TPS>
+template <typename T, int TPS, bool GATE>
 __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
   constexpr int R = 256 / TPS, IT = TPS == 64 ? 4 : 1;
   T* dout = (T*)a.dout;
@@ -2184,9 +2201,19 @@ __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
             store8f(row, pn);
           } else {
             float d[8];
+            if constexpr (GATE) {
+              // frozen squeeze-excitation: both values scaled by the gates
+              float g[8];
+              load8f(a.gate + (p / a.gate_hw) * cp + v * 8, g);
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-              d[e] = act_f(pn[e], a.act) - act_f(pv[k][e], a.act);
+              for (int e = 0; e < 8; ++e)
+                d[e] = act_f(pn[e], a.act) * g[e] -
+                       act_f(pv[k][e], a.act) * g[e];
+            } else {
+#pragma unroll
+              for (int e = 0; e < 8; ++e)
+                d[e] = act_f(pn[e], a.act) - act_f(pv[k][e], a.act);
+            }
             rm = fmaxf(rm, Vec8<T>::store(dout + (int64_t)r * cp + v * 8, d));
           }
 #pragma unroll
@@ -2315,7 +2342,11 @@ __global__ __launch_bounds__(256) void k_chunk_commit(float* P,
 template <typename T, int TPS>
 static void chunk_upd_t(hipStream_t s, const ChunkUpdArgs& a) {
   constexpr int R = 256 / TPS;
-  k_chunk_update<T, TPS><<<(int)((a.npix + R - 1) / R), 256, 0, s>>>(a);
+  const int grid = (int)((a.npix + R - 1) / R);
+  if (a.gate)
+    k_chunk_update<T, TPS, true><<<grid, 256, 0, s>>>(a);
+  else
+    k_chunk_update<T, TPS, false><<<grid, 256, 0, s>>>(a);
 }
 
 template <typename T>

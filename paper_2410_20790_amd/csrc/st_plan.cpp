@@ -59,9 +59,14 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
     return create_fail(ST_ERR_INVALID_ARG, "max_frames must be in [1, 32]");
   if (dtype != ST_F32 && dtype != ST_F16 && dtype != ST_BF16)
     return create_fail(ST_ERR_INVALID_ARG, "unknown dtype");
-  if (flags & ~(uint32_t)ST_NET_RESIDUAL_CARRY)
+  if (flags & ~(uint32_t)(ST_NET_RESIDUAL_CARRY | ST_NET_FROZEN_SE))
     return create_fail(ST_ERR_INVALID_ARG, "unknown flag");
   const bool carry = (flags & ST_NET_RESIDUAL_CARRY) != 0;
+  const bool frozen_se = (flags & ST_NET_FROZEN_SE) != 0;
+  if (carry && frozen_se)
+    return create_fail(ST_ERR_INVALID_ARG,
+                       "residual carry and frozen squeeze-excitation are "
+                       "exclusive");
   if (carry && max_frames > 1)
     return create_fail(ST_ERR_UNSUPPORTED,
                        "residual carry needs frame-by-frame encoding");
@@ -79,6 +84,7 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
   net->N = batch; net->H = in_h; net->W = in_w; net->C = in_c;
   net->F = max_frames;
   net->carry = carry;
+  net->frozen_se = frozen_se;
   net->layers.resize(n_layers);
   net->tensors.resize(n_layers + 1);
 
@@ -228,7 +234,11 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
     if (F > 1 && L.stateful)
       chunk_dp_bytes = std::max<size_t>(chunk_dp_bytes,
                                         sizeof(float) * citems * L.cout_p);
-    if (L.pool || L.se) {
+    // pooled and (exact) squeeze-excitation layers keep their affected
+    // list apart from their emitted rows; with frozen gates a
+    // squeeze-excitation layer emits at its affected sites like any other
+    // (its reference pass still defers the update, so it keeps dP)
+    if (L.pool || (L.se && !frozen_se)) {
       L.cnt_O = 2 * (L_n + 1) + L_n + i;
       L.off_O = a.take(sizeof(int32_t) * citems);
       L.off_Mo = a.take(sizeof(int32_t) * citems);
@@ -238,6 +248,7 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
       L.cnt_O = T.cnt_rows;
       L.off_O = T.off_rowpix;
       L.off_Mo = T.off_map;
+      if (L.se) L.off_dP = a.take(sizeof(float) * L.conv_grid * L.cout_p);
     }
     L.off_nbr = a.take(sizeof(int32_t) * citems * L.K);
     if (L.stateful) L.off_P = a.take(sizeof(float) * L.conv_grid * L.cout_p);

@@ -33,11 +33,13 @@ class SparseTemNet:
     """One diff encoder: reference frame via ``encode_reference``, then
     diff frames via ``encode_diff``, or up to ``max_frames`` of them at once
     via ``encode_chunk`` (see include/sparsetem.h).  ``carry``: residual
-    carry (ST_NET_RESIDUAL_CARRY; frame by frame only)."""
+    carry (ST_NET_RESIDUAL_CARRY; frame by frame only); ``frozen_se``:
+    squeeze-excitation gates kept from the reference frame
+    (ST_NET_FROZEN_SE, an approximation)."""
 
     def __init__(self, layers: Sequence, batch: int, H: int, W: int, C: int,
                  dtype: str = "f32", device="cuda", max_frames: int = 1,
-                 carry: bool = False):
+                 carry: bool = False, frozen_se: bool = False):
         self.dtype = dtype
         self.tdtype = TORCH_DTYPES[dtype]
         dev = torch.device(device)
@@ -68,10 +70,12 @@ class SparseTemNet:
                                     None if b is None else b.data_ptr(), se))
         self.max_frames = max_frames
         self.carry = carry
-        if carry:
+        self.frozen_se = frozen_se
+        if carry or frozen_se:
+            flags = ((B.NET_RESIDUAL_CARRY if carry else 0) |
+                     (B.NET_FROZEN_SE if frozen_se else 0))
             self.handle = B.st_create_net_ex(descs, batch, max_frames, H, W,
-                                             C, B.DTYPE_CODES[dtype],
-                                             B.NET_RESIDUAL_CARRY)
+                                             C, B.DTYPE_CODES[dtype], flags)
         elif max_frames > 1:
             self.handle = B.st_create_net_chunked(descs, batch, max_frames,
                                                   H, W, C,

@@ -45,11 +45,11 @@ def to_dev(frame, dtype):
         "cuda", TORCH[dtype]).contiguous()
 
 
-def make_pair(net, carry=False):
+def make_pair(net, carry=False, frozen_se=False):
     o = oracle.OracleNet(net.layers, net.batch, net.H, net.W, net.C,
-                         net.dtype, carry=carry)
+                         net.dtype, carry=carry, frozen_se=frozen_se)
     g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, net.dtype,
-                     carry=carry)
+                     carry=carry, frozen_se=frozen_se)
     return o, g
 
 
@@ -146,10 +146,11 @@ def check_rulebooks(net, o, g, tag):
         assert pairs[i] == o.last["layers"][i]["pairs"]
 
 
-def run_chunk(net, frames, thr, tag, max_band=0, carry=False):
+def run_chunk(net, frames, thr, tag, max_band=0, carry=False,
+              frozen_se=False):
     """Encode a chunk on both sides and compare after every frame (with
     carry, also the consumers' views while no keep decision differed)."""
-    o, g = make_pair(net, carry)
+    o, g = make_pair(net, carry, frozen_se)
     try:
         thr_l = [thr] * (len(net.layers) + 1) if np.isscalar(thr) else thr
         say(f"[gpu] {tag}: reference frame")

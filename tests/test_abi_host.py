@@ -258,7 +258,10 @@ def test_residual_carry_flag():
     finally:
         B.st_destroy_net(h0)
         B.st_destroy_net(h1)
-    for flags, status in ((2, B.ST_ERR_INVALID_ARG),):
+    # an unknown flag, and carry with frozen squeeze-excitation (exclusive)
+    for flags, status in ((4, B.ST_ERR_INVALID_ARG),
+                          (B.NET_RESIDUAL_CARRY | B.NET_FROZEN_SE,
+                           B.ST_ERR_INVALID_ARG)):
         with pytest.raises(B.StError) as e:
             B.st_create_net_ex(d, net.batch, 1, net.H, net.W, net.C,
                                B.ST_F32, flags)

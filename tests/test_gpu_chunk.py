@@ -20,14 +20,16 @@ from workloads import (crnn_vgg_net, depthwise_test_net, random_sparse_video,
 pytestmark = pytest.mark.gpu
 
 
-def run_chunks(net, frames, thr, F, tag, max_band=0):
+def run_chunks(net, frames, thr, F, tag, max_band=0, frozen_se=False):
     dt = net.dtype
     L_n = len(net.layers)
     thr_l = [thr] * (L_n + 1)
-    o = oracle.OracleNet(net.layers, net.batch, net.H, net.W, net.C, dt)
+    o = oracle.OracleNet(net.layers, net.batch, net.H, net.W, net.C, dt,
+                         frozen_se=frozen_se)
     g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt,
-                     max_frames=F)
-    s = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt)
+                     max_frames=F, frozen_se=frozen_se)
+    s = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt,
+                     frozen_se=frozen_se)
     try:
         say(f"[gpu] chunk {tag}: reference frame")
         o.encode_reference(frames[0])
@@ -130,3 +132,13 @@ def test_chunk_single_frame_and_batch():
     net = replace(resnet_mini_net(), batch=2)
     frames = random_sparse_video(14, 4, 2, 32, 48, 3, 0.1)
     run_chunks(net, frames, 0.0, 2, "batch 2")
+
+
+def test_chunk_frozen_se():
+    """Squeeze-excitation with the reference frame's gates (an
+    approximation) batches like any layer: the mini EfficientNet in chunks
+    of 3, against the oracle's frozen mode and the frame-by-frame path."""
+    from workloads import efficientnet_mini_net
+    net = efficientnet_mini_net()
+    run_chunks(net, random_sparse_video(24, 8, 1, 32, 40, 3, 0.08), 0.02, 3,
+               "frozen se", max_band=2, frozen_se=True)
