@@ -622,7 +622,8 @@ def roofline_of(classes, dt, desc):
 
 
 def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
-            schedule="frame"):
+            schedule="frame", frozen_se=False, thr_list=None,
+            ibst=None):
     """Time K diff frames of a workload (after W warm-up diff frames), then
     KP more with an event pair around every launch; dense comparators on
     the same net.  schedule "chunk" encodes each chunk's diff frames in one
@@ -643,8 +644,9 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
         KP = min(KP, chunk - 1)
     # graph replay of the per-frame launch sequence: fixed thresholds and
     # no squeeze-excitation (whose gate buffers alternate per frame)
-    KG = K if (schedule == "frame" and not wl["ibst"] and
-               not any(L.se_mid for L in net.layers)) else 0
+    use_ibst = wl["ibst"] if ibst is None else ibst
+    KG = K if (schedule == "frame" and not use_ibst and
+               (frozen_se or not any(L.se_mid for L in net.layers))) else 0
     t_gen = time.perf_counter()
     frames_np = wl["frames"](frames_needed(chunk, W, K, KP, KG))
     t_gen = time.perf_counter() - t_gen
@@ -658,9 +660,9 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
         frames[i].copy_(torch.from_numpy(f))
     del frames_np
     g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt,
-                     max_frames=batch)
+                     max_frames=batch, frozen_se=frozen_se)
     L_n = len(net.layers)
-    thr = [thr_val] * (L_n + 1)
+    thr = list(thr_list) if thr_list is not None else [thr_val] * (L_n + 1)
     if batch > 1:
         out = torch.empty((batch,) + tuple(g.out_shape),
                           dtype=torch.float32, device="cuda")
@@ -669,7 +671,7 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
         out = out0 = g.new_output()
     ctl = None
     ctl_idx = nonlinear_tensors(net.layers)
-    if wl["ibst"]:
+    if use_ibst:
         # the online threshold adjustment runs on the device
         g.set_threshold_control(ctl_idx, thr, target, eps, 1.0)
         ctl = "device"
@@ -822,6 +824,8 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
         res["graph_replay"] = graph
     res["roofline"] = roof
     res["kernels"] = kern
+    if ibst_thr is not None:
+        res["_thresholds"] = ibst_thr
     res["profiled_ms_per_step"] = prof_ms_step
     res["frame_gen_s"] = t_gen
     g.close()
@@ -884,6 +888,53 @@ def carry_comparison(name, thr_val, steps=18):
     return res
 
 
+def frozen_se_comparison(name, steps=14, warmup=7):
+    """Squeeze-excitation with the reference frame's gates (an
+    approximation) on an EfficientNet workload: frame by frame with the
+    online threshold adjustment (as the exact line), then in SparseBatch
+    chunks at the thresholds the controller ended with; and the
+    approximation alone -- each diff frame's output at threshold 0 against
+    the exact dense forward -- over one chunk."""
+    import torch
+    from paper_2410_20790_amd import SparseTemNet
+    wl = workload(name, 0.0)
+    net = wl["net"]
+    keys = ("value", "ms_per_step", "effective_tflops", "ref_ms",
+            "chunk_amortised_frames_per_s", "speedup_vs_dense", "ibst",
+            "roofline", "graph_replay")
+    fr = measure(wl, steps, warmup, 7, 0.0, frozen_se=True)
+    out = {"frame_ibst": {k: fr[k] for k in keys if k in fr}}
+    thr_end = [float(v) for v in fr.pop("_thresholds")]
+    ch = measure(wl, steps, warmup, 7, 0.0, dense=False, frozen_se=True,
+                 schedule="chunk", thr_list=thr_end, ibst=False)
+    out["chunk_fixed_thr"] = {k: ch[k] for k in keys if k in ch}
+    out["chunk_fixed_thr"]["thresholds"] = "the frame run's final ones"
+    # the approximation alone
+    chunk = wl["chunk"]
+    frames = [torch.from_numpy(f).to("cuda") for f in wl["frames"](chunk)]
+    tdt = {"f32": torch.float32, "f16": torch.float16,
+           "bf16": torch.bfloat16}[net.dtype]
+    frames = [f.to(tdt).contiguous() for f in frames]
+    g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, net.dtype,
+                     frozen_se=True)
+    d = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, net.dtype)
+    try:
+        g.encode_reference(frames[0])
+        errs = []
+        thr0 = [0.0] * (len(net.layers) + 1)
+        for t in range(1, chunk):
+            o = g.encode_diff(frames[t], thr0)
+            ref = d.encode_reference(frames[t])
+            errs.append(float((o - ref).abs().max() / ref.abs().max()))
+        out["max_rel_err_vs_exact_dense_at_thr0"] = [round(e, 5)
+                                                     for e in errs]
+    finally:
+        g.close()
+        d.close()
+        torch.cuda.empty_cache()
+    return out
+
+
 def default_schedule(wl, requested=None):
     """SparseBatch (one st_encode_chunk call per chunk) where the library
     offers it -- nets without squeeze-excitation whose input has at most
@@ -911,6 +962,7 @@ def extra_workload(name, steps, warmup, thr=0.0):
     net = wl["net"]
     sched = default_schedule(wl)
     r = measure(wl, steps, warmup, 7, thr, schedule=sched)
+    r.pop("_thresholds", None)
     if sched == "chunk":
         f = measure(wl, steps, warmup, 7, thr, dense=False, schedule="frame")
         r["frame_by_frame"] = {k: f[k] for k in FRAME_KEYS if k in f}
@@ -978,6 +1030,7 @@ def main():
     K, W, KP = args.steps, args.warmup, args.profile_steps
     r = measure(wl, K, W, KP, args.thr, dense=not args.no_dense,
                 schedule=sched)
+    r.pop("_thresholds", None)
     res = {
         "metric": METRIC,
         "value": r.pop("value"),
@@ -1008,7 +1061,9 @@ def main():
     if args.workload == "resnet50" and not args.no_extra:
         res["other_workloads"] = {
             "effnet_b0": extra_workload("effnet_b0", 14, 7),
+            "effnet_b0_frozen_se": frozen_se_comparison("effnet_b0"),
             "multistream": extra_workload("multistream", 14, 7),
+            "multistream_frozen_se": frozen_se_comparison("multistream"),
             "crnn": extra_workload("crnn", 30, 15, thr=0.02),
             "toy": extra_workload("toy", 30, 3)}
     if args.workload == "resnet50" and not args.no_extra:
