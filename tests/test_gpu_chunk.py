@@ -142,3 +142,46 @@ def test_chunk_frozen_se():
     net = efficientnet_mini_net()
     run_chunks(net, random_sparse_video(24, 8, 1, 32, 40, 3, 0.08), 0.02, 3,
                "frozen se", max_band=2, frozen_se=True)
+
+
+def test_chunk_resnet50_full_size():
+    """ResNet-50 at 1024x2048 bf16 with 10% clustered change in the launch
+    configuration the benchmark times (a reference frame, then the chunk's
+    9 diff frames in one call): every frame's input kept list equals the
+    frame-by-frame path's bit for bit, every frame's output equals it within
+    the bf16 tolerance, and the last frame's output equals the dense pass
+    of that frame (threshold 0; properties that hold at any size)."""
+    from workloads import driving_video, resnet50_net
+    net = resnet50_net()
+    frames = driving_video(seed=2, n_frames=10, density=0.10)
+    thr = [0.0] * (len(net.layers) + 1)
+    g = SparseTemNet(net.layers, 1, 1024, 2048, 3, "bf16", max_frames=9)
+    s = SparseTemNet(net.layers, 1, 1024, 2048, 3, "bf16")
+    d = SparseTemNet(net.layers, 1, 1024, 2048, 3, "bf16")
+    try:
+        say("[gpu] chunk resnet50 full: reference frame")
+        g.encode_reference(to_dev(frames[0], "bf16"))
+        s.encode_reference(to_dev(frames[0], "bf16"))
+        chunk = torch.stack([to_dev(f, "bf16") for f in frames[1:]])
+        say("[gpu] chunk resnet50 full: chunk of 9")
+        outs = g.encode_chunk(chunk.contiguous(), thr)
+        torch.cuda.synchronize()
+        act_c = B.st_debug_active(g.handle, -1)
+        npix = 1024 * 2048
+        for j in range(9):
+            out_s = s.encode_diff(to_dev(frames[1 + j], "bf16"), thr)
+            torch.cuda.synchronize()
+            mine = np.sort(act_c[(act_c >= j * npix) &
+                                 (act_c < (j + 1) * npix)] - j * npix)
+            np.testing.assert_array_equal(mine, B.st_debug_active(s.handle,
+                                                                   -1))
+            e = rel(outs[j].cpu().numpy(), out_s.cpu().numpy())
+            assert e <= RTOL["bf16"], f"frame {j + 1}: chunk vs frames {e}"
+        dense = d.encode_reference(to_dev(frames[9], "bf16"))
+        torch.cuda.synchronize()
+        e = rel(outs[8].cpu().numpy(), dense.cpu().numpy())
+        assert e <= RTOL["bf16"], f"last frame vs dense pass {e}"
+    finally:
+        g.close()
+        s.close()
+        d.close()
