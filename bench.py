@@ -383,7 +383,8 @@ class Feed:
     `batch` > 1 (the SparseBatch schedule) the diff frames of a chunk are
     encoded up to `batch` at a time by one st_encode_chunk call, else one
     st_encode_diff call per frame.  ctl = "device": the thresholds are
-    adjusted on the device (st_encode_diff_adaptive, no host round trip);
+    adjusted on the device (st_encode_diff_adaptive, or
+    st_encode_chunk_adaptive with one step per chunk; no host round trip);
     ctl = a host controller: each diff frame's thresholds come from it and
     its kept-row counters are fed back after the frame (one host round trip
     per frame, part of the timed work)."""
@@ -395,8 +396,9 @@ class Feed:
         self.g, self.frames, self.chunk = g, frames, chunk
         self.thr, self.ctl, self.out = thr, ctl, out
         self.batch = batch
-        if batch > 1 and ctl is not None:
-            raise ValueError("the controller adjusts thresholds per frame")
+        if batch > 1 and ctl not in (None, "device"):
+            raise ValueError("the host controller adjusts thresholds per "
+                             "frame")
         self.device_ctl = ctl == "device"
         if self.device_ctl:
             self.ctl = None
@@ -425,7 +427,8 @@ class Feed:
             m = min(limit, self.batch)
             if self.chunk:
                 m = min(m, self.chunk - self.pos % self.chunk)
-            self.g.encode_chunk(self.frames[self.pos:self.pos + m], self.thr,
+            self.g.encode_chunk(self.frames[self.pos:self.pos + m],
+                                None if self.device_ctl else self.thr,
                                 out=self.out[:m])
             self.pos += m
             self.last_m = m
@@ -672,8 +675,11 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
     ctl = None
     ctl_idx = nonlinear_tensors(net.layers)
     if use_ibst:
-        # the online threshold adjustment runs on the device
-        g.set_threshold_control(ctl_idx, thr, target, eps, 1.0)
+        # the online threshold adjustment runs on the device; a chunk is
+        # one step, so a search spans chunk - 1 reference periods (as many
+        # steps as frame by frame)
+        g.set_threshold_control(ctl_idx, thr, target, eps, 1.0,
+                                cycle_refs=batch)
         ctl = "device"
     feed = Feed(g, L_n, frames, chunk, thr, ctl, out, batch)
     dflops = dense_flops(net, [net_conv_grid(net, i) for i in range(L_n)])
@@ -741,7 +747,9 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
                 kept[j + 1] = counts[f, j, 4]
                 if L.src == -1:
                     kept[0] = counts[f, j, 2]
-            rows.append(1.0 - kept / np.array(feed.grids, dtype=np.float64))
+            # a record of the chunk schedule covers `batch` frames
+            rows.append(1.0 - kept / (batch * np.array(feed.grids,
+                                                       dtype=np.float64)))
         ibst_sp = np.array(rows)
     roof["event_pair_overhead_us"] = event_overhead_us()
 
@@ -804,10 +812,14 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
         s_c = ibst_sp[:, ctl_idx]
         th = ibst_thr[ctl_idx]
         res["ibst"] = {
-            "where": "device (st_encode_diff_adaptive)",
+            "where": "device (st_encode_chunk_adaptive, one step per "
+                     f"chunk, a search over {batch} chunks)"
+                     if schedule == "chunk" else
+                     "device (st_encode_diff_adaptive)",
             "target": target, "eps": eps, "theta_max": 1.0,
             "controlled_tensors": len(ctl_idx),
-            "sample": f"the {len(ibst_sp)} event-instrumented diff frames",
+            "sample": f"the {len(ibst_sp)} event-instrumented "
+                      + ("chunk" if schedule == "chunk" else "diff frames"),
             "mean_sparsity_controlled": float(s_c.mean()),
             "in_band_frac_last_frame": float(np.mean(
                 np.abs(s_c[-1] - target) <= eps)),
@@ -892,9 +904,10 @@ def frozen_se_comparison(name, steps=14, warmup=7):
     """Squeeze-excitation with the reference frame's gates (an
     approximation) on an EfficientNet workload: frame by frame with the
     online threshold adjustment (as the exact line), then in SparseBatch
-    chunks at the thresholds the controller ended with; and the
-    approximation alone -- each diff frame's output at threshold 0 against
-    the exact dense forward -- over one chunk."""
+    chunks with the adjustment stepping once per chunk, and in chunks at
+    the thresholds the frame run ended with; and the approximation alone --
+    each diff frame's output at threshold 0 against the exact dense forward
+    -- over one chunk."""
     import torch
     from paper_2410_20790_amd import SparseTemNet
     wl = workload(name, 0.0)
@@ -905,6 +918,12 @@ def frozen_se_comparison(name, steps=14, warmup=7):
     fr = measure(wl, steps, warmup, 7, 0.0, frozen_se=True)
     out = {"frame_ibst": {k: fr[k] for k in keys if k in fr}}
     thr_end = [float(v) for v in fr.pop("_thresholds")]
+    # warm-up over one whole search (chunk - 1 chunks), timed over two more
+    nb = wl["chunk"] - 1
+    ci = measure(wl, 2 * nb, nb * nb, 7, 0.0, dense=False, frozen_se=True,
+                 schedule="chunk")
+    ci.pop("_thresholds", None)
+    out["chunk_ibst"] = {k: ci[k] for k in keys if k in ci}
     ch = measure(wl, steps, warmup, 7, 0.0, dense=False, frozen_se=True,
                  schedule="chunk", thr_list=thr_end, ibst=False)
     out["chunk_fixed_thr"] = {k: ch[k] for k in keys if k in ch}

@@ -228,19 +228,24 @@ st_status st_layer_density(st_net* net, int32_t layer, int32_t image,
  * s = 1 - kept rows / sites (f64) moves theta one bisection step: s <
  * target - eps: lo = theta, theta = (theta + hi) / 2; s > target + eps:
  * hi = theta, theta = (lo + theta) / 2; the kernels read theta rounded to
- * f32.  Every st_encode_reference starts a new cycle (brackets back to
- * [0, theta_max], theta kept).  No host round trip per frame: the step is
- * a kernel on the encode stream.
+ * f32.  A cycle spans cycle_refs reference frames: the first
+ * st_encode_reference after this call, and every cycle_refs-th one after
+ * it, starts a new cycle (brackets back to [0, theta_max], theta kept).
+ * Frame by frame, cycle_refs = 1 gives one search per reference period;
+ * st_encode_chunk_adaptive takes one step per chunk, so with a chunk per
+ * reference period a search needs cycle_refs > 1 to take several steps.
+ * No host round trip per frame: the step is a kernel on the encode stream.
  *
  * controlled, fixed_thr: host arrays of n_layers + 1 entries, read during
  * the call.  The state is uploaded on `stream` and the call waits for it.
  * Errors: ST_ERR_STATE (no workspace), ST_ERR_INVALID_ARG (NULL arrays,
  * target outside [0, 1], eps < 0, theta_max <= 0, theta0 > theta_max, NaN
- * threshold), ST_ERR_HIP. */
+ * threshold, cycle_refs < 1), ST_ERR_HIP. */
 st_status st_set_threshold_control(st_net* net, const uint8_t* controlled,
                                    const float* fixed_thr, double target,
                                    double eps, double theta_max,
-                                   double theta0, void* stream);
+                                   double theta0, int32_t cycle_refs,
+                                   void* stream);
 
 /* A diff frame encoded with the device thresholds (as st_encode_diff
  * otherwise), followed by the controller's step.  Errors: ST_ERR_STATE (no
@@ -248,6 +253,16 @@ st_status st_set_threshold_control(st_net* net, const uint8_t* controlled,
  * ST_ERR_INVALID_ARG (NULL frame), ST_ERR_HIP. */
 st_status st_encode_diff_adaptive(st_net* net, const void* frame, float* out,
                                   void* stream);
+
+/* A chunk encoded with the device thresholds (as st_encode_chunk
+ * otherwise: every frame of the chunk uses the same thresholds), followed
+ * by one controller step whose sparsity is that of the whole chunk,
+ * s = 1 - kept rows over all its frames / (sites * n_frames).  Errors: as
+ * st_encode_chunk (thr aside), and ST_ERR_STATE when threshold control is
+ * not set. */
+st_status st_encode_chunk_adaptive(st_net* net, const void* frames,
+                                   int32_t n_frames, float* out,
+                                   void* stream);
 
 /* The current f32 thresholds (n_layers + 1 host floats), i.e. those the
  * next adaptive frame uses; synchronises with the last encode.  Errors:

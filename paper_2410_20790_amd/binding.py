@@ -38,6 +38,7 @@ EXPORTED = [
     "st_debug_counters", "st_profile_begin", "st_profile_end",
     "st_set_threshold_control", "st_encode_diff_adaptive",
     "st_get_thresholds", "st_create_net_ex", "st_debug_carry",
+    "st_encode_chunk_adaptive",
 ]
 
 
@@ -103,8 +104,10 @@ def _load():
         "st_set_threshold_control": [P, ctypes.POINTER(ctypes.c_uint8),
                                      ctypes.POINTER(ctypes.c_float),
                                      ctypes.c_double, ctypes.c_double,
-                                     ctypes.c_double, ctypes.c_double, P],
+                                     ctypes.c_double, ctypes.c_double, I32,
+                                     P],
         "st_encode_diff_adaptive": [P, P, P, P],
+        "st_encode_chunk_adaptive": [P, P, I32, P, P],
         "st_get_thresholds": [P, ctypes.POINTER(ctypes.c_float)],
     }
     for name, args in sig.items():
@@ -194,9 +197,10 @@ def st_encode_diff(net, frame_ptr, thr, out_ptr=None, stream=0):
 
 def st_set_threshold_control(net, controlled, fixed_thr, target=0.9,
                              eps=0.025, theta_max=1.0, theta0=-1.0,
-                             stream=0):
+                             stream=0, cycle_refs=1):
     """controlled: n_layers + 1 flags; fixed_thr: n_layers + 1 thresholds
-    (used by the tensors that are not controlled)."""
+    (used by the tensors that are not controlled); a search cycle spans
+    cycle_refs reference frames."""
     if len(controlled) != len(fixed_thr):
         raise ValueError("controlled and fixed_thr differ in length")
     c = (ctypes.c_uint8 * len(controlled))(*[1 if v else 0
@@ -204,12 +208,18 @@ def st_set_threshold_control(net, controlled, fixed_thr, target=0.9,
     f = (ctypes.c_float * len(fixed_thr))(*[float(v) for v in fixed_thr])
     _check(_lib.st_set_threshold_control(net, c, f, float(target), float(eps),
                                          float(theta_max), float(theta0),
-                                         _ptr(stream)), net)
+                                         int(cycle_refs), _ptr(stream)), net)
 
 
 def st_encode_diff_adaptive(net, frame_ptr, out_ptr=None, stream=0):
     _check(_lib.st_encode_diff_adaptive(net, _ptr(frame_ptr), _ptr(out_ptr),
                                         _ptr(stream)), net)
+
+
+def st_encode_chunk_adaptive(net, frames_ptr, n_frames, out_ptr=None,
+                             stream=0):
+    _check(_lib.st_encode_chunk_adaptive(net, _ptr(frames_ptr), n_frames,
+                                         _ptr(out_ptr), _ptr(stream)), net)
 
 
 def st_get_thresholds(net, n_tensors):

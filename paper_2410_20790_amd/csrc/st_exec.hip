@@ -370,15 +370,12 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
     if (L.se && (ref || !net->frozen_se)) L.se_par ^= 1;
   launch_cleanup(pf, s, ws.at<CleanEntry>(net->off_cleanup), net->n_cleanup,
                  net->ws, cnt, net->max_grid);
-  // online adjustment: a reference frame starts a new cycle; after a diff
-  // frame encoded with the device thresholds, one bisection step
-  if (net->ibst_on && (ref || thr_dev)) {
-    const IbstArgs ia = ibst_args(net);
-    if (ref)
-      launch_ibst_restart(s, ia);
-    else
-      launch_ibst_step(s, cnt, ia);
-  }
+  // online adjustment: every cycle_refs-th reference frame starts a new
+  // cycle; after a diff frame encoded with the device thresholds, one
+  // bisection step
+  if (net->ibst_on && ref && net->ibst_refs++ % net->ibst_cycle_refs == 0)
+    launch_ibst_restart(s, ibst_args(net));
+  if (thr_dev) launch_ibst_step(s, cnt, 1, ibst_args(net));
   if (R && R->n_hist < R->max_frames) {
     (void)hipMemcpyAsync(R->hist + (size_t)R->n_hist * net->n_counters, cnt,
                          sizeof(u64) * net->n_counters, hipMemcpyDeviceToHost,
@@ -408,8 +405,9 @@ IbstArgs ibst_args(st_net* net) {
   return a;
 }
 
-bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
-                     hipStream_t s) {
+// thr_dev: as for run_layer.
+bool run_layer_chunk(st_net* net, int i, int nf, float thr,
+                     const float* thr_dev, float* out, hipStream_t s) {
   const WS ws{net->ws};
   const LayerPlan& L = net->layers[i];
   const st_layer_desc& d = L.d;
@@ -502,6 +500,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
   a.ref = 0;
   a.mdone = ws.at<uint32_t>(net->off_mdone);
   a.keep_thr = thr;
+  a.keep_thr_dev = thr_dev;
   a.zero = ws.at<char>(net->off_zero);
   a.part = ws.at<float>(net->off_part);
   a.split_max = L.split_max;
@@ -570,13 +569,14 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
   }
   if (L.stateful)
     launch_group_count(pf, s, rowmax_out, cnt + outT.cnt_rows,
-                       outT.grid * nf, thr, nullptr, grp);
+                       outT.grid * nf, thr, thr_dev, grp);
 
   ListArgs la{};
   la.rowmax = rowmax_out;
   la.n_rows = cnt + outT.cnt_rows;
   la.cap = outT.grid * nf;
   la.thr = thr;
+  la.thr_dev = thr_dev;
   la.rowpix = ws.at<int>(outT.off_rowpix);
   la.act = ws.at<int>(outT.off_act);
   la.map = ws.at<int>(outT.off_map);
@@ -588,9 +588,12 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr, float* out,
   return true;
 }
 
+// thr: host thresholds, or NULL for the online adjustment's, which then
+// takes one bisection step from the whole chunk's counts.
 st_status encode_chunk(st_net* net, const void* frames, int nf,
                        const float* thr, float* out, hipStream_t s) {
   const WS ws{net->ws};
+  const float* thr_dev = thr ? nullptr : ws.at<float>(net->off_ibst_thr);
   u64* cnt = ws.at<u64>(net->off_cnt);
   const Prof pf{net, -1};
   Recorder* R = net->rec && net->rec->on ? net->rec : nullptr;
@@ -607,7 +610,8 @@ st_status encode_chunk(st_net* net, const void* frames, int nf,
   sa.Cp = T0.Cp;
   sa.nf = nf;
   sa.npix = T0.grid;
-  sa.thr = thr[0];
+  sa.thr = thr ? thr[0] : 0.f;
+  sa.thr_dev = thr_dev;
   sa.keep = ws.at<uint8_t>(net->off_flags);
   sa.base = ws.at<uint8_t>(net->off_chunk_base);
   sa.last = ws.at<uint8_t>(net->off_chunk_last);
@@ -620,14 +624,16 @@ st_status encode_chunk(st_net* net, const void* frames, int nf,
   sa.cnt_act = cnt + T0.cnt_act;
   sa.cons = consumers_of(net, 0);
   launch_chunk_scan(pf, s, net->dtype, sa);
-  T0.last_thr = thr[0];
+  T0.last_thr = sa.thr;
   const int nl = (int)net->layers.size();
   for (int i = 0; i < nl; ++i)
-    if (!run_layer_chunk(net, i, nf, thr[i + 1], i == nl - 1 ? out : nullptr,
-                         s))
+    if (!run_layer_chunk(net, i, nf, thr ? thr[i + 1] : 0.f,
+                         thr_dev ? thr_dev + i + 1 : nullptr,
+                         i == nl - 1 ? out : nullptr, s))
       return fail(net, ST_ERR_HIP, "internal: GEMM launch arguments");
   launch_cleanup(pf, s, ws.at<CleanEntry>(net->off_cleanup), net->n_cleanup,
                  net->ws, cnt, net->max_grid);
+  if (thr_dev) launch_ibst_step(s, cnt, nf, ibst_args(net));
   if (R && R->n_hist < R->max_frames) {
     (void)hipMemcpyAsync(R->hist + (size_t)R->n_hist * net->n_counters, cnt,
                          sizeof(u64) * net->n_counters, hipMemcpyDeviceToHost,
@@ -750,22 +756,18 @@ extern "C" st_status st_encode_reference(st_net* net, const void* frame,
   return s;
 }
 
-extern "C" st_status st_encode_chunk(st_net* net, const void* frames,
-                                     int32_t n_frames, const float* thr,
-                                     float* out, void* stream) {
+// Checks shared by both chunk entry points (thresholds aside).
+static st_status check_chunk(st_net* net, const void* frames,
+                             int32_t n_frames) {
   if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
   if (!net->bound) return fail(net, ST_ERR_STATE, "no workspace bound");
   if (!net->have_ref)
     return fail(net, ST_ERR_STATE, "no reference frame encoded yet");
-  if (!frames || !thr)
-    return fail(net, ST_ERR_INVALID_ARG, "frames or thr is NULL");
+  if (!frames) return fail(net, ST_ERR_INVALID_ARG, "frames is NULL");
   if (n_frames < 1 || n_frames > net->F)
     return fail(net, ST_ERR_INVALID_ARG,
                 "n_frames must be in [1, max_frames of the net]");
   const int nl = (int)net->layers.size();
-  for (int i = 0; i <= nl; ++i)
-    if (std::isnan(thr[i]))
-      return fail(net, ST_ERR_INVALID_ARG, "threshold is NaN");
   if (net->F < 2)
     return fail(net, ST_ERR_UNSUPPORTED,
                 "net created without chunk capacity (st_create_net_chunked)");
@@ -782,7 +784,30 @@ extern "C" st_status st_encode_chunk(st_net* net, const void* frames,
   if (net->layers[nl - 1].pool || net->layers[nl - 1].se)
     return fail(net, ST_ERR_UNSUPPORTED,
                 "a pooled or squeeze-excitation last layer in a chunk");
+  return ST_OK;
+}
+
+extern "C" st_status st_encode_chunk(st_net* net, const void* frames,
+                                     int32_t n_frames, const float* thr,
+                                     float* out, void* stream) {
+  const st_status st = check_chunk(net, frames, n_frames);
+  if (st != ST_OK) return st;
+  if (!thr) return fail(net, ST_ERR_INVALID_ARG, "thr is NULL");
+  for (size_t i = 0; i <= net->layers.size(); ++i)
+    if (std::isnan(thr[i]))
+      return fail(net, ST_ERR_INVALID_ARG, "threshold is NaN");
   return encode_chunk(net, frames, n_frames, thr, out, (hipStream_t)stream);
+}
+
+extern "C" st_status st_encode_chunk_adaptive(st_net* net, const void* frames,
+                                              int32_t n_frames, float* out,
+                                              void* stream) {
+  const st_status st = check_chunk(net, frames, n_frames);
+  if (st != ST_OK) return st;
+  if (!net->ibst_on)
+    return fail(net, ST_ERR_STATE, "threshold control not set");
+  return encode_chunk(net, frames, n_frames, nullptr, out,
+                      (hipStream_t)stream);
 }
 
 extern "C" st_status st_encode_diff(st_net* net, const void* frame,
@@ -805,16 +830,18 @@ extern "C" st_status st_set_threshold_control(st_net* net,
                                               const float* fixed_thr,
                                               double target, double eps,
                                               double theta_max, double theta0,
+                                              int32_t cycle_refs,
                                               void* stream) {
   if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
   if (!net->bound) return fail(net, ST_ERR_STATE, "no workspace bound");
   if (!controlled || !fixed_thr)
     return fail(net, ST_ERR_INVALID_ARG, "NULL controlled or fixed_thr");
   if (!(target >= 0.0 && target <= 1.0) || !(eps >= 0.0) ||
-      !(theta_max > 0.0) || std::isnan(theta0) || theta0 > theta_max)
+      !(theta_max > 0.0) || std::isnan(theta0) || theta0 > theta_max ||
+      cycle_refs < 1)
     return fail(net, ST_ERR_INVALID_ARG,
                 "need 0 <= target <= 1, eps >= 0, theta_max > 0, "
-                "theta0 <= theta_max");
+                "theta0 <= theta_max, cycle_refs >= 1");
   const size_t n = net->tensors.size();
   std::vector<double> theta(n), lo(n, 0.0), hi(n, theta_max);
   std::vector<float> thr(n);
@@ -856,6 +883,8 @@ extern "C" st_status st_set_threshold_control(st_net* net,
   net->ibst_target = target;
   net->ibst_eps = eps;
   net->ibst_theta_max = theta_max;
+  net->ibst_cycle_refs = cycle_refs;
+  net->ibst_refs = 0;
   return ST_OK;
 }
 

@@ -127,6 +127,10 @@ struct st_net {
   bool carry = false;                      // residual-carry semantics
   bool frozen_se = false;                  // frozen squeeze-excitation gates
   double ibst_target = 0.9, ibst_eps = 0.025, ibst_theta_max = 1.0;
+  // a cycle spans this many reference frames; reference frames seen since
+  // the control was set
+  int ibst_cycle_refs = 1;
+  int64_t ibst_refs = 0;
   // chunk mode (F > 1): f32 deferred updates of the current layer (shared),
   // per input item the frame whose value X_hat held (0xFF: the X_hat of
   // the chunk's start), per input site the last kept frame, per conv site

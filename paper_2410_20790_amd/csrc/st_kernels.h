@@ -239,6 +239,7 @@ struct ChunkScanArgs {
   int C, Cp, nf;
   int64_t npix;        // input sites per frame
   float thr;
+  const float* thr_dev;  // threshold in device memory (or NULL: thr)
   uint8_t* keep;       // [nf * npix] keep bytes
   uint8_t* base;       // [nf * npix] frame X_hat held (0xFF: chunk start)
   uint8_t* last;       // [npix] last kept frame (0xFF: none)
@@ -329,7 +330,9 @@ struct IbstArgs {
   int n;
   double target, eps, theta_max;
 };
-void launch_ibst_step(hipStream_t s, const u64* counters, const IbstArgs& a);
+// nf: frames the counters cover (a chunk's kept rows over sites * nf).
+void launch_ibst_step(hipStream_t s, const u64* counters, int nf,
+                      const IbstArgs& a);
 // A new cycle: every controlled bracket back to [0, theta_max].
 void launch_ibst_restart(hipStream_t s, const IbstArgs& a);
 

@@ -2052,6 +2052,7 @@ template <typename T>
 __global__ __launch_bounds__(256) void k_chunk_scan_prep(ChunkScanArgs a) {
   const T* x = (const T*)a.x;
   const T* xhat = (const T*)a.xhat;
+  const float thr = a.thr_dev ? *a.thr_dev : a.thr;
   for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < a.npix;
        p += (int64_t)gridDim.x * 256) {
     float xh[16];
@@ -2062,7 +2063,7 @@ __global__ __launch_bounds__(256) void k_chunk_scan_prep(ChunkScanArgs a) {
       const T* xt = x + i * a.C;
       float m = 0.f;
       for (int c = 0; c < a.C; ++c) m = fmaxf(m, fabsf(to_f(xt[c]) - xh[c]));
-      const bool k = m > a.thr;
+      const bool k = m > thr;
       a.keep[i] = k ? 1 : 0;
       a.base[i] = cur;
       if (k) {
@@ -2630,11 +2631,11 @@ void launch_carry_commit(const Prof& pf, hipStream_t s, int dtype,
 // ------------------------------------------- online threshold adjustment
 // One bisection step per controlled tensor, in f64 as the host controller
 // takes it; the f32 threshold is theta rounded to nearest.
-__global__ void k_ibst_step(const u64* counters, IbstArgs a) {
+__global__ void k_ibst_step(const u64* counters, int nf, IbstArgs a) {
   for (int t = threadIdx.x; t < a.n; t += blockDim.x) {
     if (!a.ctl[t]) continue;
-    const double sp =
-        1.0 - (double)counters[2 * t + 1] / (double)a.sites[t];
+    const double sp = 1.0 - (double)counters[2 * t + 1] /
+                                ((double)a.sites[t] * (double)nf);
     double th = a.theta[t];
     if (sp < a.target - a.eps) {
       a.lo[t] = th;
@@ -2656,8 +2657,9 @@ __global__ void k_ibst_restart(IbstArgs a) {
     }
 }
 
-void launch_ibst_step(hipStream_t s, const u64* counters, const IbstArgs& a) {
-  k_ibst_step<<<1, 256, 0, s>>>(counters, a);
+void launch_ibst_step(hipStream_t s, const u64* counters, int nf,
+                      const IbstArgs& a) {
+  k_ibst_step<<<1, 256, 0, s>>>(counters, nf, a);
 }
 
 void launch_ibst_restart(hipStream_t s, const IbstArgs& a) {

@@ -124,10 +124,12 @@ class SparseTemNet:
         return out
 
     def set_threshold_control(self, controlled, fixed_thr, target=0.9,
-                              eps=0.025, theta_max=1.0, theta0=None):
+                              eps=0.025, theta_max=1.0, theta0=None,
+                              cycle_refs=1):
         """Online threshold adjustment on the device: `controlled` lists the
         indices (into thr) of the tensors whose threshold is searched;
-        fixed_thr (n_layers + 1) holds the others'."""
+        fixed_thr (n_layers + 1) holds the others'; a search cycle spans
+        cycle_refs reference frames."""
         if len(fixed_thr) != self.n_layers + 1:
             raise ValueError("fixed_thr needs n_layers + 1 entries")
         flags = [0] * (self.n_layers + 1)
@@ -138,7 +140,7 @@ class SparseTemNet:
         B.st_set_threshold_control(self.handle, flags, fixed_thr, target, eps,
                                    theta_max,
                                    -1.0 if theta0 is None else theta0,
-                                   self._stream())
+                                   self._stream(), cycle_refs)
 
     def encode_diff_adaptive(self, frame, out=None, write_out=True):
         """A diff frame with the device-adjusted thresholds, then one step
@@ -157,14 +159,16 @@ class SparseTemNet:
 
     def encode_chunk(self, frames, thr, out=None, write_out=True):
         """frames: contiguous device tensor [n_frames, *in_shape]; returns
-        the outputs of every frame, [n_frames, *out_shape] (f32)."""
+        the outputs of every frame, [n_frames, *out_shape] (f32).  thr None:
+        the device-adjusted thresholds, then one step of the adjustment
+        from the whole chunk."""
         nf = frames.shape[0] if frames.dim() == 5 else -1
         if (frames.device != self.device or frames.dtype != self.tdtype
                 or frames.dim() != 5 or tuple(frames.shape[1:]) !=
                 self.in_shape or not frames.is_contiguous()):
             raise ValueError("frames must be a contiguous device tensor "
                              f"[n, {self.in_shape}] of {self.tdtype}")
-        if len(thr) != self.n_layers + 1:
+        if thr is not None and len(thr) != self.n_layers + 1:
             raise ValueError("thr needs n_layers + 1 entries")
         if write_out and out is None:
             out = torch.empty((nf,) + tuple(self.out_shape),
@@ -174,9 +178,14 @@ class SparseTemNet:
                           or not out.is_contiguous()):
             raise ValueError("out must be a contiguous f32 tensor "
                              f"[{nf}, {self.out_shape}]")
-        B.st_encode_chunk(self.handle, frames.data_ptr(), nf, thr,
-                          out.data_ptr() if write_out else None,
-                          self._stream())
+        if thr is None:
+            B.st_encode_chunk_adaptive(self.handle, frames.data_ptr(), nf,
+                                       out.data_ptr() if write_out else None,
+                                       self._stream())
+        else:
+            B.st_encode_chunk(self.handle, frames.data_ptr(), nf, thr,
+                              out.data_ptr() if write_out else None,
+                              self._stream())
         return out
 
     def capture_diff(self, thr, out):

@@ -231,6 +231,9 @@ def test_threshold_control_needs_a_bound_net():
         with pytest.raises(B.StError) as e:
             B.st_get_thresholds(h, n)
         assert e.value.status == B.ST_ERR_STATE
+        with pytest.raises(B.StError) as e:
+            B.st_encode_chunk_adaptive(h, 0x1000, 2)
+        assert e.value.status == B.ST_ERR_STATE
         with pytest.raises(ValueError):
             B.st_set_threshold_control(h, [1] * n, [0.0] * (n - 1))
     finally:
