@@ -16,6 +16,8 @@
 // order-independent.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include <cstdint>
 
 #include "st_kernels.h"
@@ -44,18 +46,26 @@ template <> __device__ __forceinline__ _Float16 from_f<_Float16>(float x) {
   return (_Float16)x;  // hardware conversion, round to nearest even
 }
 template <> __device__ __forceinline__ bf16_t from_f<bf16_t>(float x) {
-  // round to nearest even on the f32 bit pattern (finite inputs)
-  uint32_t u = __float_as_uint(x);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return bf16_t{(uint16_t)(u >> 16)};
+  // hardware conversion (gfx950), round to nearest even
+  return bf16_t{__builtin_bit_cast(uint16_t, (__bf16)x)};
 }
 template <typename T> __device__ __forceinline__ T zero_v() {
   return from_f<T>(0.f);
 }
 
+// Activation f: 0 identity, 1 ReLU, 2 SiLU (x / (1 + e^-x)).
+template <int ACT>
+__device__ __forceinline__ float act_c(float x) {
+  if constexpr (ACT == 1)
+    return __builtin_amdgcn_fmed3f(x, 0.f, __builtin_inff());  // max(x, 0)
+  else if constexpr (ACT == 2)
+    return x / (1.f + expf(-x));
+  else
+    return x;
+}
 __device__ __forceinline__ float act_f(float x, int a) {
-  if (a == 1) return fmaxf(x, 0.f);
-  if (a == 2) return x / (1.f + expf(-x));
+  if (a == 1) return act_c<1>(x);
+  if (a == 2) return act_c<2>(x);
   return x;
 }
 
@@ -142,10 +152,9 @@ __device__ __forceinline__ unsigned block_exclusive_scan(unsigned v,
 // 64-item groups).  Each thread owns `tile / 256` consecutive items of the
 // tile and evaluates them; one block scan gives every kept item its
 // position.  The predicate's item data (P::Item, from P::load) is requested
-// together with the item count and the counts before the tile -- all loads
-// stay within the capacity `cap`, and which items are real is decided once
-// the count has arrived -- so a block waits for one round of loads, not
-// three.  With IPT > 0 (items per thread known at compile time) the items
+// together with the item count -- all loads stay within the capacity
+// `cap`, and which items are real is decided once the count has arrived --
+// and a live block then sums the counts before its tile.  With IPT > 0 (items per thread known at compile time) the items
 // are kept in registers until the keep decision.  Dropped items are handed
 // to pred.drop by their owner; the kept ones are listed in LDS in position
 // order and emitted by the whole block, consecutive threads taking
@@ -167,9 +176,6 @@ __global__ __launch_bounds__(256) void k_compact_write(
   __shared__ uint16_t kept[kMaxItemsPerThread * 256];
   const int64_t base = (int64_t)blockIdx.x * tile;
   const int64_t n_req = read_count(n_dev, n_host);
-  unsigned off = 0;
-  const unsigned nprev = blockIdx.x * (unsigned)per_tile;
-  for (unsigned j = threadIdx.x; j < nprev; j += 256) off += cnts[j];
   const int ipt = IPT > 0 ? IPT : tile / 256;
   const int64_t first = base + (int64_t)threadIdx.x * ipt;
   Item it[IPT > 0 ? IPT : 1];
@@ -187,6 +193,12 @@ __global__ __launch_bounds__(256) void k_compact_write(
     }
     return;
   }
+  // the counts before the tile, read once the tile is known to be live
+  // (a capacity-sized grid has many blocks past the count, and summing a
+  // prefix in each of them would cost a quadratic number of reads)
+  unsigned off = 0;
+  const unsigned nprev = blockIdx.x * (unsigned)per_tile;
+  for (unsigned j = threadIdx.x; j < nprev; j += 256) off += cnts[j];
   const int64_t end = min(base + (int64_t)tile, n);
   uint32_t keepbits = 0;
   unsigned mine = 0;
@@ -754,6 +766,9 @@ template <typename T> struct Vec8Half {
 #pragma unroll
     for (int e = 0; e < 8; ++e) f[e] = to_f(h[e]);
   }
+  // stores the rounded values, returns their largest magnitude: rounding
+  // to nearest is monotone and odd, so that is the rounded largest
+  // magnitude of the unrounded values (one conversion instead of eight)
   __device__ __forceinline__ static float store(T* p, const float* f) {
     uint4 v;
     T* h = (T*)&v;
@@ -761,10 +776,10 @@ template <typename T> struct Vec8Half {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       h[e] = from_f<T>(f[e]);
-      m = fmaxf(m, fabsf(to_f(h[e])));
+      m = fmaxf(m, fabsf(f[e]));
     }
     *(uint4*)p = v;
-    return m;
+    return to_f(from_f<T>(m));
   }
 };
 template <> struct Vec8<_Float16> : Vec8Half<_Float16> {};
@@ -908,41 +923,42 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
 }
 
 // Four channels of a delta row stored in the storage type; returns the
-// largest magnitude of the rounded values.
+// largest magnitude of the rounded values (the rounded largest magnitude,
+// as rounding to nearest is monotone and odd).
 template <typename T>
 __device__ __forceinline__ float store4(T* p, const float* f) {
   float m = 0.f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(f[e]));
   if constexpr (sizeof(T) == 4) {
     *(float4*)p = make_float4(f[0], f[1], f[2], f[3]);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(f[e]));
+    return m;
   } else {
     uint2 v;
     T* h = (T*)&v;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      h[e] = from_f<T>(f[e]);
-      m = fmaxf(m, fabsf(to_f(h[e])));
-    }
+    for (int e = 0; e < 4; ++e) h[e] = from_f<T>(f[e]);
     *(uint2*)p = v;
+    return to_f(from_f<T>(m));
   }
-  return m;
 }
 
 // Chunk-state epilogue, for CPT columns per thread (64 / CPT threads per
 // run, adjacent lanes).  The runs' states and the rows' residual deltas are
 // requested together; the residual deltas are added into Cs (four threads
 // per row, 16 columns each); then each run's threads apply its frames in
-// order from LDS -- P_t = P_{t-1} + update, emit f(P_t) - f(P_{t-1}) and
-// the row maximum (device atomics, one per row and column tile) -- and
-// store the state once.
+// order from LDS -- P_t = P_{t-1} + update, emit f(P_t) - f(P_{t-1}) -- and
+// store the state once.  Row maxima are merged in LDS (s_rmax, one LDS
+// atomic per thread and row, no cross-lane reduction in the frame loop)
+// and then with one device atomic per row and column tile.
 template <typename T, int CPT>
 __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
                                                 int cld, const int* s_run,
                                                 int nruns, int64_t m0,
                                                 int rows, int n0,
                                                 const int* s_site,
-                                                const int* s_rsk) {
+                                                const int* s_rsk,
+                                                unsigned* s_rmax) {
   constexpr int TPR = 64 / CPT, Q = CPT / 4;
   const int tid = threadIdx.x;
   const int cout_p = a.cout_p;
@@ -991,34 +1007,47 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
       }
     }
   }
+  if (tid < kGemmBM) s_rmax[tid] = 0u;
   __syncthreads();
-  if (!run) return;
-  const int r0 = s_run[g], r1 = s_run[g + 1];
-  for (int r = r0; r < r1; ++r) {
-    float rm = 0.f;
+  const int r0 = run ? s_run[g] : 0, r1 = run ? s_run[g + 1] : 0;
+  // the frames of the run, with the activation fixed at compile time
+  auto frames = [&](auto act_tag) {
+    constexpr int ACT = decltype(act_tag)::value;
+    for (int r = r0; r < r1; ++r) {
+      float rm = 0.f;
 #pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      if (c0 + 4 * q >= cout_p) continue;
-      const float4 u = *(const float4*)(Cs + r * cld + (c0 - n0) + 4 * q);
-      const float uv[4] = {u.x, u.y, u.z, u.w};
-      float d[4];
+      for (int q = 0; q < Q; ++q) {
+        if (c0 + 4 * q >= cout_p) continue;
+        const float4 u = *(const float4*)(Cs + r * cld + (c0 - n0) + 4 * q);
+        const float uv[4] = {u.x, u.y, u.z, u.w};
+        float d[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float po = P[4 * q + e], pn = po + uv[e];
-        d[e] = act_f(pn, a.act) - act_f(po, a.act);
-        P[4 * q + e] = pn;
+        for (int e = 0; e < 4; ++e) {
+          const float po = P[4 * q + e], pn = po + uv[e];
+          d[e] = act_c<ACT>(pn) - act_c<ACT>(po);
+          P[4 * q + e] = pn;
+        }
+        rm = fmaxf(rm, store4<T>(dout + (m0 + r) * cout_p + c0 + 4 * q, d));
       }
-      rm = fmaxf(rm, store4<T>(dout + (m0 + r) * cout_p + c0 + 4 * q, d));
+      if (rm > 0.f) atomicMax(s_rmax + r, __float_as_uint(rm));
     }
+  };
+  if (a.act == 1)
+    frames(std::integral_constant<int, 1>{});
+  else if (a.act == 2)
+    frames(std::integral_constant<int, 2>{});
+  else
+    frames(std::integral_constant<int, 0>{});
+  if (run) {
 #pragma unroll
-    for (int o = 1; o < TPR; o <<= 1) rm = fmaxf(rm, __shfl_xor(rm, o, 64));
-    if (j == 0 && rm > 0.f) atomicMax(a.rowmax + m0 + r, __float_as_uint(rm));
+    for (int q = 0; q < Q; ++q)
+      if (c0 + 4 * q < cout_p)
+        *(float4*)(a.P + site * cout_p + c0 + 4 * q) =
+            make_float4(P[4 * q], P[4 * q + 1], P[4 * q + 2], P[4 * q + 3]);
   }
-#pragma unroll
-  for (int q = 0; q < Q; ++q)
-    if (c0 + 4 * q < cout_p)
-      *(float4*)(a.P + site * cout_p + c0 + 4 * q) =
-          make_float4(P[4 * q], P[4 * q + 1], P[4 * q + 2], P[4 * q + 3]);
+  __syncthreads();
+  if (tid < rows && s_rmax[tid])
+    atomicMax(a.rowmax + m0 + tid, s_rmax[tid]);
 }
 
 // Chunk-state epilogue: the tile's rows [m0, m0 + rows) are whole site
@@ -1034,7 +1063,8 @@ __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
                                                   int* s_run, int64_t m0,
                                                   int rows, int n0,
                                                   const int* s_site,
-                                                  const int* s_rsk) {
+                                                  const int* s_rsk,
+                                                  unsigned* s_rmax) {
   constexpr int BM = kGemmBM;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   // run starts: s_run[0..nruns) (wave 0 lists them), s_run[nruns] = rows,
@@ -1054,13 +1084,13 @@ __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
   const int nruns = s_run[BM + 1];
   if (nruns > 32)
     chunk_tile_runs<T, 16>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
-                           s_rsk);
+                           s_rsk, s_rmax);
   else if (nruns > 16)
     chunk_tile_runs<T, 8>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
-                          s_rsk);
+                          s_rsk, s_rmax);
   else
     chunk_tile_runs<T, 4>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
-                          s_rsk);
+                          s_rsk, s_rmax);
 }
 
 // SPLIT: the layer's reduction may be split (split_max > 1); every unit
@@ -1069,7 +1099,7 @@ __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
 // through the reduction.
 // Four waves per SIMD (the persistent grid holds four blocks per CU):
 // the register budget is fixed at that occupancy.
-template <typename T, bool REF, bool ALIGNED, bool SPLIT>
+template <typename T, bool REF, bool ALIGNED, bool SPLIT, bool CHUNK>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
 void k_conv_gemm(ConvArgs a) {
   constexpr int BM = kGemmBM, BN = kGemmBN;
@@ -1085,6 +1115,7 @@ void k_conv_gemm(ConvArgs a) {
   __shared__ u64 s_kmask;
   __shared__ int s_last;
   __shared__ int s_site[BM], s_rsk[BM], s_run[BM + 2];
+  __shared__ unsigned s_rmax[BM];
   extern __shared__ int s_nbr[];          // [K][BM]
   // LDS carve-up: A[2][BM][LD], B[2][BN][LD]; the f32 accumulator tile of
   // the epilogue reuses the same bytes
@@ -1101,7 +1132,7 @@ void k_conv_gemm(ConvArgs a) {
   const int l16 = lane & 15, lg = lane >> 4;
   const int64_t nO = (int64_t)*a.nO;
   // row tiles: 64 rows each, or (chunk-state mode) aligned to site runs
-  const bool runs = a.tstart != nullptr;
+  const bool runs = CHUNK;  // the launcher pairs tstart with this mode
   const int rstep = runs ? chunk_tile_step(a.nf) : BM;
   const int64_t tiles_m = (nO + rstep - 1) / rstep;
   const int tiles_n = (a.cout_p + BN - 1) / BN;
@@ -1129,15 +1160,28 @@ void k_conv_gemm(ConvArgs a) {
   // epilogue ownership: thread -> row em, columns [ec, ec + 16) of the tile
   const int em = tid >> 2, ec = (tid & 3) * 16;
 
-  for (int u = xcd * chunk + blockIdx.x / kXcd; u < u_end; u += per_xcd) {
+  // run-aligned row tiles (chunk-state mode): a unit's bounds are fetched
+  // during the previous unit, so they have arrived when it starts
+  const int u_first = xcd * chunk + blockIdx.x / kXcd;
+  unsigned nb_lo = 0u, nb_hi = 0u;
+  if (CHUNK && u_first < u_end) {
+    const int tm = (int)((unsigned)u_first / (unsigned)tiles_n);
+    nb_lo = a.tstart[tm];
+    nb_hi = a.tstart[tm + 1];
+  }
+  for (int u = u_first; u < u_end; u += per_xcd) {
     // this unit's split and tile, and its reduction stages [st_lo, st_hi)
     const int sp = SPLIT ? (int)((unsigned)u / (unsigned)ntiles) : 0;
     const int t = SPLIT ? u - sp * (int)ntiles : u;
     const int st_lo = SPLIT ? (int)((int64_t)sp * nst / S) : 0;
     const int st_hi = SPLIT ? (int)((int64_t)(sp + 1) * nst / S) : nst;
     const int tm_i = (int)((unsigned)t / (unsigned)tiles_n);
-    const int64_t m0 = runs ? (int64_t)a.tstart[tm_i] : (int64_t)tm_i * BM;
-    const int64_t m1 = runs ? (int64_t)a.tstart[tm_i + 1] : min(m0 + BM, nO);
+    const int64_t m0 =
+        runs ? (int64_t)(unsigned)__builtin_amdgcn_readfirstlane((int)nb_lo)
+             : (int64_t)tm_i * BM;
+    const int64_t m1 =
+        runs ? (int64_t)(unsigned)__builtin_amdgcn_readfirstlane((int)nb_hi)
+             : min(m0 + BM, nO);
     const int n0 = (t - tm_i * tiles_n) * BN;
 
     __syncthreads();  // previous tile's LDS reads are complete
@@ -1162,6 +1206,11 @@ void k_conv_gemm(ConvArgs a) {
     for (int h = 0; h < 2; ++h) hv[h] = eok && n0 + ec + 8 * h < cout_p;
     __syncthreads();
     const u64 kmask = s_kmask;
+    if (CHUNK && u + per_xcd < u_end) {
+      const int tm = (int)((unsigned)(u + per_xcd) / (unsigned)tiles_n);
+      nb_lo = a.tstart[tm];
+      nb_hi = a.tstart[tm + 1];
+    }
 
     auto stage_active = [&](int st) {
       const int klo = (st * KC) / cin_p;
@@ -1326,6 +1375,12 @@ void k_conv_gemm(ConvArgs a) {
       }
     };
 
+    // this thread's output row's residual row, requested now so that it
+    // arrives during the reduction; (chunk-state mode) the row's site
+    const int rsk = (!SPLIT && a.mskip && eok) ? a.mskip[epix] : -1;
+    if (CHUNK && (tid & 3) == 0)
+      s_site[em] = eok ? (int)((unsigned)epix % (unsigned)a.per) : -1;
+
     // two stages in flight: slot 0 / slot 1 alternate
     uint4 ra0[AV], rb0[BV], ra1[AV], rb1[BV];
     It ia = first_stage();
@@ -1355,12 +1410,7 @@ void k_conv_gemm(ConvArgs a) {
     // each thread finishes 16 contiguous columns of one row: full-width
     // state loads/stores and 16-byte delta stores.  MFMA 16x16 block
     // layout: D[row = 4*lg + r][col = l16].
-    // this thread's output row's residual row
-    const int rsk = (!SPLIT && a.mskip && eok) ? a.mskip[epix] : -1;
-    if (a.mode == kModeChunkState && (tid & 3) == 0) {
-      s_site[em] = eok ? (int)((unsigned)epix % (unsigned)a.per) : -1;
-      s_rsk[em] = rsk;
-    }
+    if (CHUNK && (tid & 3) == 0) s_rsk[em] = rsk;
     __syncthreads();  // every wave is done reading the staged tiles
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -1383,9 +1433,9 @@ void k_conv_gemm(ConvArgs a) {
                     8 * h,
                 v);
       }
-    } else if (a.mode == kModeChunkState) {
+    } else if constexpr (CHUNK) {
       finish_chunk_tile<T>(a, Cs, CLD, s_run, m0, (int)(m1 - m0), n0,
-                           s_site, s_rsk);
+                           s_site, s_rsk, s_rmax);
     } else {
       finish_tile<T, REF>(
           a, [&](int h, float* v) { load8f(crow + 8 * h, v); },
@@ -1488,14 +1538,20 @@ static void gemm_t(hipStream_t s, int grid, size_t lds, const ConvArgs& a) {
   const bool aligned = a.cin_p % MmaCfg<T>::KC == 0;
   if (a.ref) {
     if (aligned)
-      k_conv_gemm<T, true, true, SPLIT><<<grid, 256, lds, s>>>(a);
+      k_conv_gemm<T, true, true, SPLIT, false><<<grid, 256, lds, s>>>(a);
     else
-      k_conv_gemm<T, true, false, SPLIT><<<grid, 256, lds, s>>>(a);
+      k_conv_gemm<T, true, false, SPLIT, false><<<grid, 256, lds, s>>>(a);
+  } else if (!SPLIT && a.mode == kModeChunkState) {
+    // the chunk-state epilogue has a build of its own
+    if (aligned)
+      k_conv_gemm<T, false, true, false, true><<<grid, 256, lds, s>>>(a);
+    else
+      k_conv_gemm<T, false, false, false, true><<<grid, 256, lds, s>>>(a);
   } else {
     if (aligned)
-      k_conv_gemm<T, false, true, SPLIT><<<grid, 256, lds, s>>>(a);
+      k_conv_gemm<T, false, true, SPLIT, false><<<grid, 256, lds, s>>>(a);
     else
-      k_conv_gemm<T, false, false, SPLIT><<<grid, 256, lds, s>>>(a);
+      k_conv_gemm<T, false, false, SPLIT, false><<<grid, 256, lds, s>>>(a);
   }
 }
 
