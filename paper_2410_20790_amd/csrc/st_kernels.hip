@@ -68,6 +68,17 @@ __device__ __forceinline__ float act_f(float x, int a) {
   if (a == 2) return act_c<2>(x);
   return x;
 }
+// Calls f(std::integral_constant<int, ACT>{}) for the activation act, so
+// that f's body is built once per activation.
+template <class F>
+__device__ __forceinline__ void with_act(int act, F&& f) {
+  if (act == 1)
+    f(std::integral_constant<int, 1>{});
+  else if (act == 2)
+    f(std::integral_constant<int, 2>{});
+  else
+    f(std::integral_constant<int, 0>{});
+}
 
 // ------------------------------------------------------------ reductions
 __device__ __forceinline__ unsigned wave_sum(unsigned v) {
@@ -821,7 +832,8 @@ __device__ __forceinline__ int split_count(int64_t ntiles, int nst, int smax) {
 // with device-scope atomics; the last block to finish a row tile (over its
 // column tiles) counts the tile's kept rows for the truncation pass.  Every
 // thread of the block must call it (it synchronises).
-template <typename T, bool REF, class LoadV, class LoadPo, class LoadSk>
+template <typename T, bool REF, int ACT, class LoadV, class LoadPo,
+          class LoadSk>
 __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
                                             LoadPo load_po, LoadSk load_sk,
                                             const bool (&hv)[2], int64_t eo,
@@ -859,7 +871,7 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           pn[e] = po[e] + v[e];
-          v[e] = act_f(pn[e], a.act) * g[e] - act_f(po[e], a.act) * g[e];
+          v[e] = act_c<ACT>(pn[e]) * g[e] - act_c<ACT>(po[e]) * g[e];
         }
       } else if (!REF && a.yhat) {
         // residual carry: against what the consumers received
@@ -868,13 +880,13 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           pn[e] = po[e] + v[e];
-          v[e] = act_f(pn[e], a.act) - yh[e];
+          v[e] = act_c<ACT>(pn[e]) - yh[e];
         }
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           pn[e] = po[e] + v[e];
-          v[e] = act_f(pn[e], a.act) - act_f(po[e], a.act);
+          v[e] = act_c<ACT>(pn[e]) - act_c<ACT>(po[e]);
         }
       }
       store8f(a.P + (int64_t)epix * cout_p + n, pn);
@@ -1032,12 +1044,7 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
       if (rm > 0.f) atomicMax(s_rmax + r, __float_as_uint(rm));
     }
   };
-  if (a.act == 1)
-    frames(std::integral_constant<int, 1>{});
-  else if (a.act == 2)
-    frames(std::integral_constant<int, 2>{});
-  else
-    frames(std::integral_constant<int, 0>{});
+  with_act(a.act, frames);
   if (run) {
 #pragma unroll
     for (int q = 0; q < Q; ++q)
@@ -1437,26 +1444,28 @@ void k_conv_gemm(ConvArgs a) {
       finish_chunk_tile<T>(a, Cs, CLD, s_run, m0, (int)(m1 - m0), n0,
                            s_site, s_rsk, s_rmax);
     } else {
-      finish_tile<T, REF>(
-          a, [&](int h, float* v) { load8f(crow + 8 * h, v); },
-          [&](int h, float* po) {
-            if (REF) {
+      auto load_v = [&](int h, float* v) { load8f(crow + 8 * h, v); };
+      auto load_po = [&](int h, float* po) {
+        if (REF) {
 #pragma unroll
-              for (int e = 0; e < 8; ++e) po[e] = 0.f;
-            } else {
-              load8f(a.P + (int64_t)epix * cout_p + n0 + ec + 8 * h, po);
-            }
-          },
-          [&](int h, float* sk) {
-            if (rsk >= 0) {
-              Vec8<T>::load(dskip + (int64_t)rsk * cout_p + n0 + ec + 8 * h,
-                            sk);
-            } else {
+          for (int e = 0; e < 8; ++e) po[e] = 0.f;
+        } else {
+          load8f(a.P + (int64_t)epix * cout_p + n0 + ec + 8 * h, po);
+        }
+      };
+      auto load_sk = [&](int h, float* sk) {
+        if (rsk >= 0) {
+          Vec8<T>::load(dskip + (int64_t)rsk * cout_p + n0 + ec + 8 * h, sk);
+        } else {
 #pragma unroll
-              for (int e = 0; e < 8; ++e) sk[e] = 0.f;
-            }
-          },
-          hv, eo, eok, epix, m0, n0, ec, tiles_n, m1, &s_last);
+          for (int e = 0; e < 8; ++e) sk[e] = 0.f;
+        }
+      };
+      with_act(a.act, [&](auto act_tag) {
+        finish_tile<T, REF, decltype(act_tag)::value>(
+            a, load_v, load_po, load_sk, hv, eo, eok, epix, m0, n0, ec,
+            tiles_n, m1, &s_last);
+      });
     }
   }
 }
@@ -1501,27 +1510,29 @@ __global__ __launch_bounds__(256) void k_split_epi(ConvArgs a) {
         Vec8<T>::load(dskip + (int64_t)rsk * cout_p + n0 + ec + 8 * h, sk[h]);
     const float* prow = a.part + eo * cout_p + n0 + ec;
     const int64_t pstride = a.capO * cout_p;
-    finish_tile<T, REF>(
-        a,
-        [&](int h, float* v) {
+    auto load_v = [&](int h, float* v) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] = 0.f;
-          for (int sp = 0; sp < S; ++sp) {
-            float q[8];
-            load8f(prow + sp * pstride + 8 * h, q);
+      for (int e = 0; e < 8; ++e) v[e] = 0.f;
+      for (int sp = 0; sp < S; ++sp) {
+        float q[8];
+        load8f(prow + sp * pstride + 8 * h, q);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) v[e] += q[e];
-          }
-        },
-        [&](int h, float* o) {
+        for (int e = 0; e < 8; ++e) v[e] += q[e];
+      }
+    };
+    auto load_po = [&](int h, float* o) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) o[e] = po[h][e];
-        },
-        [&](int h, float* o) {
+      for (int e = 0; e < 8; ++e) o[e] = po[h][e];
+    };
+    auto load_sk = [&](int h, float* o) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) o[e] = sk[h][e];
-        },
-        hv, eo, eok, epix, m0, n0, ec, tiles_n, nO, &s_last);
+      for (int e = 0; e < 8; ++e) o[e] = sk[h][e];
+    };
+    with_act(a.act, [&](auto act_tag) {
+      finish_tile<T, REF, decltype(act_tag)::value>(
+          a, load_v, load_po, load_sk, hv, eo, eok, epix, m0, n0, ec, tiles_n,
+          nO, &s_last);
+    });
   }
 }
 
@@ -1604,43 +1615,106 @@ bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
 }
 
 // ---------------------------------------------------- (c') depthwise path
-// Memory-bound: each thread owns VEC channels of one affected row and sums
-// its K neighbours in offset order on the vector ALU.
-template <typename T, bool REF>
-__global__ __launch_bounds__(256) void k_conv_dw(ConvArgs a) {
-  constexpr int VEC = 16 / (int)sizeof(T);
+// Memory-bound: each thread owns 8 channels of one affected row.  The
+// row's neighbour indices are read up to eight offsets at a time and their
+// input rows requested together, then summed in offset order on the vector
+// ALU (the same order as one offset at a time); the epilogue reads and
+// writes whole 8-channel vectors.
+template <typename T, bool REF, int ACT>
+__device__ __forceinline__ void conv_dw_rows(const ConvArgs& a) {
+  constexpr int KB = 8;                       // offsets per batch of loads
+  constexpr int RV = (int)sizeof(T) / 2;      // 16-byte vectors per 8 channels
   const T* din = (const T*)a.din;
   const float* w = (const float*)a.w;
-  const Epi<T, REF> epi = make_epi<T, REF>(a);
+  const T* dskip = (const T*)a.dskip;
+  T* dout = (T*)a.dout;
+  const int cout_p = a.cout_p, cin_p = a.cin_p;
   const int64_t nO = (int64_t)*a.nO;
-  const int cpr = a.cout_p / VEC;
+  const int cpr = cout_p / 8;
   const int64_t total = nO * cpr;
   for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
        idx += (int64_t)gridDim.x * 256) {
     const int64_t o = idx / cpr;
-    const int c0 = (int)(idx - o * cpr) * VEC;
-    float acc[VEC];
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
-    for (int k = 0; k < a.K; ++k) {
-      const int src = a.nbr[(int64_t)k * a.stride + o];
-      if (src < 0) continue;
-      const uint4 raw = *(const uint4*)(din + (int64_t)src * a.cin_p + c0);
-      const T* xv = (const T*)&raw;
-      const float* wk = w + (int64_t)k * a.cout_p + c0;
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) acc[e] += wk[e] * to_f(xv[e]);
-    }
+    const int c0 = (int)(idx - o * cpr) * 8;
     const int pix = a.O[o];
-    EpiIn pre[VEC];
+    float acc[8];
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) pre[e] = epi.load(pix, c0 + e);
-    float rm = 0.f;
+    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+    for (int k0 = 0; k0 < a.K; k0 += KB) {
+      int src[KB];
 #pragma unroll
-    for (int e = 0; e < VEC; ++e)
-      rm = fmaxf(rm, epi.store(o, pix, c0 + e, acc[e], pre[e]));
-    if (a.mode != 1 && rm > 0.f) atomicMax(a.rowmax + o, __float_as_uint(rm));
+      for (int j = 0; j < KB; ++j)
+        src[j] = k0 + j < a.K ? a.nbr[(int64_t)(k0 + j) * a.stride + o] : -1;
+      uint4 raw[KB][RV];
+#pragma unroll
+      for (int j = 0; j < KB; ++j)
+#pragma unroll
+        for (int v = 0; v < RV; ++v)
+          raw[j][v] = src[j] >= 0
+                          ? ((const uint4*)(din + (int64_t)src[j] * cin_p +
+                                            c0))[v]
+                          : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+      for (int j = 0; j < KB; ++j) {
+        if (src[j] < 0) continue;
+        float x[8], wk[8];
+        Vec8<T>::load((const T*)raw[j], x);
+        load8f(w + (int64_t)(k0 + j) * cout_p + c0, wk);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += wk[e] * x[e];
+      }
+    }
+    // every load of the epilogue before its stores
+    const int rsk = a.mskip ? a.mskip[pix] : -1;
+    float sk[8], po[8], ex[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sk[e] = po[e] = 0.f;
+    if (rsk >= 0) Vec8<T>::load(dskip + (int64_t)rsk * cout_p + c0, sk);
+    const bool state = a.mode == kModeState;
+    if (state && !REF) load8f(a.P + (int64_t)pix * cout_p + c0, po);
+    if (state && a.gate)
+      load8f(a.gate + (pix / a.gate_hw) * cout_p + c0, ex);
+    else if (state && !REF && a.yhat)
+      load8f(a.yhat + (int64_t)pix * cout_p + c0, ex);
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      v[e] = acc[e];
+      if (REF) v[e] += a.bias[c0 + e];
+      v[e] += sk[e];
+    }
+    if (a.mode == kModeDefer) {
+      store8f(a.dP + o * cout_p + c0, v);
+      continue;
+    }
+    if (state) {
+      float pn[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pn[e] = po[e] + v[e];
+      store8f(a.P + (int64_t)pix * cout_p + c0, pn);
+      if (a.gate) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          v[e] = act_c<ACT>(pn[e]) * ex[e] - act_c<ACT>(po[e]) * ex[e];
+      } else if (!REF && a.yhat) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = act_c<ACT>(pn[e]) - ex[e];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          v[e] = act_c<ACT>(pn[e]) - act_c<ACT>(po[e]);
+      }
+    }
+    const float rm = Vec8<T>::store(dout + o * cout_p + c0, v);
+    if (rm > 0.f) atomicMax(a.rowmax + o, __float_as_uint(rm));
   }
+}
+
+template <typename T, bool REF>
+__global__ __launch_bounds__(256) void k_conv_dw(ConvArgs a) {
+  with_act(a.act, [&](auto act_tag) {
+    conv_dw_rows<T, REF, decltype(act_tag)::value>(a);
+  });
 }
 
 template <typename T>
@@ -1653,8 +1727,7 @@ static void dw_t(hipStream_t s, int grid, const ConvArgs& a) {
 
 void launch_conv_dw(const Prof& pf, hipStream_t s, int dtype,
                     const ConvArgs& a) {
-  const int vec = dtype == 0 ? 4 : 8;
-  const int grid = grid_for(a.capO * (a.cout_p / vec), 8192);
+  const int grid = grid_for(a.capO * (a.cout_p / 8), 8192);
   prof_begin(pf, 8 /*ST_K_CONV_DW*/, s);
   if (dtype == 0)
     dw_t<float>(s, grid, a);
