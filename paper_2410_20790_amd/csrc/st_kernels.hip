@@ -162,10 +162,11 @@ __device__ __forceinline__ unsigned block_exclusive_scan(unsigned v,
 // cnts: `per_tile` counts per tile (1 = per-tile counts, tile/64 = counts of
 // 64-item groups).  Each thread owns `tile / 256` consecutive items of the
 // tile and evaluates them; one block scan gives every kept item its
-// position.  The predicate's item data (P::Item, from P::load) is requested
-// together with the item count -- all loads stay within the capacity
-// `cap`, and which items are real is decided once the count has arrived --
-// and a live block then sums the counts before its tile.  With IPT > 0 (items per thread known at compile time) the items
+// position.  The predicate's item data (P::Item, from P::load) and the
+// first 256 counts before the tile are requested together with the item
+// count -- all loads stay within the capacity `cap` and the count buffer,
+// and which items are real is decided once the count has arrived -- and a
+// live block then sums the rest of the counts before its tile.  With IPT > 0 (items per thread known at compile time) the items
 // are kept in registers until the keep decision.  Dropped items are handed
 // to pred.drop by their owner; the kept ones are listed in LDS in position
 // order and emitted by the whole block, consecutive threads taking
@@ -187,6 +188,9 @@ __global__ __launch_bounds__(256) void k_compact_write(
   __shared__ uint16_t kept[kMaxItemsPerThread * 256];
   const int64_t base = (int64_t)blockIdx.x * tile;
   const int64_t n_req = read_count(n_dev, n_host);
+  // the first 256 counts before the tile are requested with the count
+  const unsigned nprev = blockIdx.x * (unsigned)per_tile;
+  unsigned off = threadIdx.x < nprev ? cnts[threadIdx.x] : 0u;
   const int ipt = IPT > 0 ? IPT : tile / 256;
   const int64_t first = base + (int64_t)threadIdx.x * ipt;
   Item it[IPT > 0 ? IPT : 1];
@@ -204,12 +208,11 @@ __global__ __launch_bounds__(256) void k_compact_write(
     }
     return;
   }
-  // the counts before the tile, read once the tile is known to be live
-  // (a capacity-sized grid has many blocks past the count, and summing a
-  // prefix in each of them would cost a quadratic number of reads)
-  unsigned off = 0;
-  const unsigned nprev = blockIdx.x * (unsigned)per_tile;
-  for (unsigned j = threadIdx.x; j < nprev; j += 256) off += cnts[j];
+  // the rest of the counts before the tile, read once the tile is known
+  // to be live (a capacity-sized grid has many blocks past the count, and
+  // summing a whole prefix in each of them would cost a quadratic number
+  // of reads)
+  for (unsigned j = threadIdx.x + 256; j < nprev; j += 256) off += cnts[j];
   const int64_t end = min(base + (int64_t)tile, n);
   uint32_t keepbits = 0;
   unsigned mine = 0;
