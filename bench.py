@@ -626,7 +626,7 @@ def roofline_of(classes, dt, desc):
 
 def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
             schedule="frame", frozen_se=False, thr_list=None,
-            ibst=None):
+            ibst=None, bf16_state=False):
     """Time K diff frames of a workload (after W warm-up diff frames), then
     KP more with an event pair around every launch; dense comparators on
     the same net.  schedule "chunk" encodes each chunk's diff frames in one
@@ -663,7 +663,8 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
         frames[i].copy_(torch.from_numpy(f))
     del frames_np
     g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt,
-                     max_frames=batch, frozen_se=frozen_se)
+                     max_frames=batch, frozen_se=frozen_se,
+                     bf16_state=bf16_state)
     L_n = len(net.layers)
     thr = list(thr_list) if thr_list is not None else [thr_val] * (L_n + 1)
     if batch > 1:
@@ -795,6 +796,7 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
         "dense_gflop_per_frame": dflops / 1e9,
         "dense_equiv_tflops": dflops / (ms_step * 1e-3) / 1e12,
         "measured_input_density": dens0,
+        "workspace_bytes": g.ws_bytes,
     }
     if chunk:
         ref_ms = float(np.median(refs)) if refs else None
@@ -954,6 +956,61 @@ def frozen_se_comparison(name, steps=14, warmup=7):
     return out
 
 
+def bf16_state_comparison(name, steps=14, warmup=7):
+    """bf16 pre-activation state (an approximation that halves the state)
+    against the f32 state on an EfficientNet workload: diff-frames/s frame
+    by frame with the device IBST (exact squeeze-excitation) and in
+    SparseBatch chunks with frozen gates and one IBST step per chunk, the
+    workspace of both, and the approximation alone -- each diff frame's
+    output at threshold 0 (exact squeeze-excitation) against the exact
+    dense forward -- over one chunk, for both states."""
+    import torch
+    from paper_2410_20790_amd import SparseTemNet
+    wl = workload(name, 0.0)
+    net = wl["net"]
+    nb = wl["chunk"] - 1
+    keys = ("value", "ms_per_step", "workspace_bytes")
+    out = {}
+    for label, b16 in (("f32_state", False), ("bf16_state", True)):
+        fr = measure(wl, steps, warmup, 7, 0.0, dense=False,
+                     bf16_state=b16)
+        ch = measure(wl, 2 * nb, nb * nb, 7, 0.0, dense=False,
+                     frozen_se=True, schedule="chunk", bf16_state=b16)
+        out[label] = {"frame_ibst": {k: fr[k] for k in keys},
+                      "chunk_frozen_se_ibst": {k: ch[k] for k in keys}}
+    out["state_bytes_saved"] = (out["f32_state"]["frame_ibst"]
+                                ["workspace_bytes"] -
+                                out["bf16_state"]["frame_ibst"]
+                                ["workspace_bytes"])
+    tdt = {"f32": torch.float32, "f16": torch.float16,
+           "bf16": torch.bfloat16}[net.dtype]
+    frames = [torch.from_numpy(f).to("cuda").to(tdt).contiguous()
+              for f in wl["frames"](wl["chunk"])]
+    mk = lambda b16: SparseTemNet(net.layers, net.batch, net.H, net.W,  # noqa: E731
+                                  net.C, net.dtype, bf16_state=b16)
+    nets = {"f32_state": mk(False), "bf16_state": mk(True)}
+    d = mk(False)
+    try:
+        errs = {k: [] for k in nets}
+        thr0 = [0.0] * (len(net.layers) + 1)
+        for g in nets.values():
+            g.encode_reference(frames[0])
+        for t in range(1, len(frames)):
+            ref = d.encode_reference(frames[t])
+            scale = float(ref.abs().max())
+            for k, g in nets.items():
+                o = g.encode_diff(frames[t], thr0)
+                errs[k].append(round(float((o - ref).abs().max()) / scale,
+                                     6))
+        for k in nets:
+            out[k]["max_rel_err_vs_exact_dense_at_thr0"] = errs[k]
+    finally:
+        for g in list(nets.values()) + [d]:
+            g.close()
+        torch.cuda.empty_cache()
+    return out
+
+
 def default_schedule(wl, requested=None):
     """SparseBatch (one st_encode_chunk call per chunk) where the library
     offers it -- nets without squeeze-excitation whose input has at most
@@ -1083,6 +1140,8 @@ def main():
             "effnet_b0_frozen_se": frozen_se_comparison("effnet_b0"),
             "multistream": extra_workload("multistream", 14, 7),
             "multistream_frozen_se": frozen_se_comparison("multistream"),
+            "effnet_b0_bf16_state": bf16_state_comparison("effnet_b0"),
+            "multistream_bf16_state": bf16_state_comparison("multistream"),
             "crnn": extra_workload("crnn", 30, 15, thr=0.02),
             "toy": extra_workload("toy", 30, 3)}
     if args.workload == "resnet50" and not args.no_extra:

@@ -141,13 +141,24 @@ enum {
    * pass per frame.  Exclusive with ST_NET_RESIDUAL_CARRY; with it the
    * chunk entry also takes squeeze-excitation nets (last layer without
    * it). */
-  ST_NET_FROZEN_SE = 2
+  ST_NET_FROZEN_SE = 2,
+  /* Pre-activation state stored in bf16 (half the state memory and its
+   * traffic; an approximation): every update rounds the new state to the
+   * nearest bf16 value (ties to even) before it is stored and before the
+   * emitted delta f(P_new) - f(P_old) is formed from it, the reference
+   * pass rounds the dense pre-activation the same way; so the consumers'
+   * sum of deltas follows the stored state exactly, and the state drifts
+   * from the exact one by at most one bf16 rounding per update.  Not with
+   * max-pooled layers or ST_NET_RESIDUAL_CARRY (ST_ERR_UNSUPPORTED);
+   * combines with ST_NET_FROZEN_SE and both entries. */
+  ST_NET_BF16_STATE = 4
 };
 
 /* As st_create_net_chunked, with creation flags (ST_NET_*).  Errors as
  * st_create_net_chunked, plus ST_ERR_INVALID_ARG for an unknown flag or
- * both flags, and ST_ERR_UNSUPPORTED for ST_NET_RESIDUAL_CARRY with
- * max_frames > 1. */
+ * ST_NET_RESIDUAL_CARRY with ST_NET_FROZEN_SE, and ST_ERR_UNSUPPORTED for
+ * ST_NET_RESIDUAL_CARRY with max_frames > 1 or with ST_NET_BF16_STATE, and
+ * for ST_NET_BF16_STATE on a net with a max-pooled layer. */
 st_status st_create_net_ex(const st_layer_desc* layers, int32_t n_layers,
                            int32_t batch, int32_t max_frames, int32_t in_h,
                            int32_t in_w, int32_t in_c, int32_t dtype,

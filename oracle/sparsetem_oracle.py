@@ -48,6 +48,12 @@ Readings of points the paper leaves open (all listed in the design notes):
 7. Sums are accumulated in fp64 and rounded once to f32; the pre-activation
    state is f32; emitted deltas are rounded to the storage dtype with
    round-to-nearest-even; the mask is taken on the rounded values.
+   Optional bf16 state (``state_bf16=True``, an approximation that halves
+   the state's memory): every stored pre-activation -- the reference
+   pass's and each update's f32 result -- is rounded to bf16 (nearest,
+   ties to even) before the activation sees it, so the emitted delta is
+   f(P_new) - f(P_old) of the stored values.  Not with max-pooled layers
+   or residual carry.
 
 Layout: NHWC; pixel id p = (n * H + y) * W + x.
 """
@@ -250,13 +256,15 @@ def _apply_offset(rows, w, ky, kx, groups):
     return out
 
 
-def dense_forward(layers, frame, dtype, with_se=False, all_pre=False):
+def dense_forward(layers, frame, dtype, with_se=False, all_pre=False,
+                  state_dtype="f32"):
     """Plain dense forward of one frame (the definition the diff chain must
     reproduce at threshold 0): returns (out, P, acts) where P[i] is the f32
     pre-activation of every stateful layer (of every layer with all_pre),
     acts[i] the emitted activation rounded to the storage dtype, and out
     the f32 network output; with with_se also the squeeze-excitation gates
-    S[i]."""
+    S[i].  state_dtype "bf16": a stateful layer's pre-activation is rounded
+    to bf16 before its activation (the bf16-state reading of item 7)."""
     acts = {-1: round_storage(frame, dtype)}
     P = {}
     S = {}
@@ -269,6 +277,8 @@ def dense_forward(layers, frame, dtype, with_se=False, all_pre=False):
         if all_pre:
             P[i] = p32
         if _is_stateful(layers, i):
+            if state_dtype == "bf16":
+                p32 = f32(round_storage(p32, "bf16"))
             P[i] = p32
             e = activation(p32, L.act).astype(np.float64)
             if L.pool_k[0] > 0:
@@ -289,15 +299,18 @@ class OracleNet:
     """Stateful diff encoder over one stream of frames (batch N images)."""
 
     def __init__(self, layers, batch, H, W, C, dtype="f32", carry=False,
-                 frozen_se=False):
+                 frozen_se=False, state_bf16=False):
         if dtype not in ("f32", "f16", "bf16"):
             raise ValueError(dtype)
         if carry and frozen_se:
             raise ValueError("carry and frozen_se are exclusive")
+        if state_bf16 and (carry or any(L.pool_k[0] > 0 for L in layers)):
+            raise ValueError("a bf16 state excludes carry and max-pools")
         self.layers = list(layers)
         self.dtype = dtype
         self.carry = carry
         self.frozen_se = frozen_se
+        self.state_dtype = "bf16" if state_bf16 else "f32"
         self.in_shape = (batch, H, W, C)
         shapes = {-1: self.in_shape}
         self.geo = []
@@ -327,7 +340,8 @@ class OracleNet:
         frame = np.asarray(frame, dtype=np.float64)
         assert frame.shape == self.in_shape
         out, P, acts, S = dense_forward(self.layers, frame, self.dtype,
-                                        with_se=True, all_pre=self.carry)
+                                        with_se=True, all_pre=self.carry,
+                                        state_dtype=self.state_dtype)
         self.xhat = round_storage(frame, self.dtype)
         self.P = {i: p.copy() for i, p in P.items()}
         self.S = {i: g.copy() for i, g in S.items()}
@@ -398,6 +412,8 @@ class OracleNet:
                 Pg = self.P[i].reshape(N * g.Ho * g.Wo, L.c_out)
                 P_old = Pg[O].copy()
                 P_new = f32(P_old.astype(np.float64) + dP32)
+                if self.state_dtype == "bf16":
+                    P_new = f32(round_storage(P_new, "bf16"))
                 if L.se_mid and self.frozen_se:
                     # frozen gates: a per-image, per-channel scale
                     Pg[O] = P_new

@@ -161,6 +161,7 @@ def st_create_net_chunked(layers: Sequence[st_layer_desc], batch,
 
 NET_RESIDUAL_CARRY = 1
 NET_FROZEN_SE = 2
+NET_BF16_STATE = 4
 
 
 def st_create_net_ex(layers: Sequence[st_layer_desc], batch, max_frames,

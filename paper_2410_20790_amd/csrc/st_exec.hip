@@ -162,6 +162,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
 
   // (c) delta convolution with fused (d) update / emission
   ConvArgs a{};
+  a.p16 = net->bf16_state ? 1 : 0;
   a.din = ws.at<char>(in.off_rows);
   a.nbr = nbr;
   a.stride = L.conv_grid * net->F;
@@ -237,6 +238,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
   }
   if (L.se && !frozen) {
     SeArgs sa{};
+    sa.p16 = net->bf16_state ? 1 : 0;
     sa.P = ws.at<float>(L.off_P);
     sa.dP = ws.at<float>(L.off_dP);
     sa.Mo = Mo;
@@ -362,7 +364,8 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
     const float* se =
         L.se ? ws.at<float>(L.off_ses) + par * (int64_t)net->N * L.cout_p
              : nullptr;
-    launch_output(Prof{net, nl - 1}, s, ws.at<float>(L.off_P), L.cout_p,
+    launch_output(Prof{net, nl - 1}, s, ws.at<float>(L.off_P),
+                  net->bf16_state ? 1 : 0, L.cout_p,
                   L.d.c_out, net->N, g, L.pool ? 1 : 0, L.d.act, se, out);
   }
   // the gates just computed become the previous frame's
@@ -461,6 +464,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
                      cnt + L.cnt_sites);
 
   ConvArgs a{};
+  a.p16 = net->bf16_state ? 1 : 0;
   a.din = ws.at<char>(in.off_rows);
   a.nbr = nbr;
   a.stride = stride;
@@ -511,6 +515,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
 
   if (L.stateful && !fused) {
     ChunkUpdArgs u{};
+    u.p16 = net->bf16_state ? 1 : 0;
     u.P = ws.at<float>(L.off_P);
     u.dP = cdp;
     u.Mo = Mo;
@@ -1068,8 +1073,18 @@ extern "C" st_status st_debug_state(st_net* net, int32_t layer, float* P,
   if (cap < L.conv_grid * L.d.c_out)
     return fail(net, ST_ERR_INVALID_ARG, "P buffer too small");
   std::vector<float> raw((size_t)L.conv_grid * L.cout_p);
-  st = d2h(net, raw.data(), net->ws + L.off_P, raw.size());
-  if (st != ST_OK) return st;
+  if (net->bf16_state) {
+    std::vector<uint16_t> h(raw.size());
+    st = d2h(net, h.data(), net->ws + L.off_P, h.size());
+    if (st != ST_OK) return st;
+    for (size_t i = 0; i < h.size(); ++i) {
+      const uint32_t u = (uint32_t)h[i] << 16;
+      std::memcpy(&raw[i], &u, 4);
+    }
+  } else {
+    st = d2h(net, raw.data(), net->ws + L.off_P, raw.size());
+    if (st != ST_OK) return st;
+  }
   for (int64_t p = 0; p < L.conv_grid; ++p)
     std::memcpy(P + p * L.d.c_out, raw.data() + p * L.cout_p,
                 sizeof(float) * L.d.c_out);

@@ -126,6 +126,7 @@ struct st_net {
   bool ibst_on = false;
   bool carry = false;                      // residual-carry semantics
   bool frozen_se = false;                  // frozen squeeze-excitation gates
+  bool bf16_state = false;                 // pre-activation state in bf16
   double ibst_target = 0.9, ibst_eps = 0.025, ibst_theta_max = 1.0;
   // a cycle spans this many reference frames; reference frames seen since
   // the control was set

@@ -113,6 +113,7 @@ void launch_run_tiles(const Prof& pf, hipStream_t s, const int* O,
 
 // ---- (c)+(d) delta convolution with the fused state update / emission
 struct ConvArgs {
+  int p16;             // state stored as bf16 (P points to bf16 values)
   const void* din;     // input delta rows [*, cin_p]
   const int* nbr;      // [K][stride] input row or -1
   int64_t stride;
@@ -201,6 +202,7 @@ void launch_group_count(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
 
 // ---- squeeze-excitation on a deferred layer
 struct SeArgs {
+  int p16;             // state stored as bf16
   const float* P;      // state [npix][cp] (updated in place by the emission)
   const float* dP;     // deferred update rows
   const int* Mo;       // site -> dP row or -1 (every site in the reference)
@@ -256,6 +258,7 @@ void launch_chunk_scan(const Prof& pf, hipStream_t s, int dtype,
                        const ChunkScanArgs& a);
 
 struct ChunkUpdArgs {
+  int p16;             // state stored as bf16
   float* P;            // state [npix][cp] (physical sites)
   float* dP;           // deferred update rows [*][cp] (pool mode: P_t)
   const int* Mo;       // conv item -> dP row or -1
@@ -293,8 +296,9 @@ void launch_chunk_commit(const Prof& pf, hipStream_t s, float* P,
                          int64_t nconv, int cp);
 
 // ---- dense network output (Accumulation)
-void launch_output(const Prof& pf, hipStream_t s, const float* P, int cp,
-                   int C, int N, Geo pool, int has_pool, int act,
+// p16: the state is stored as bf16.
+void launch_output(const Prof& pf, hipStream_t s, const float* P, int p16,
+                   int cp, int C, int N, Geo pool, int has_pool, int act,
                    const float* se, float* out);
 
 // ---- setup / introspection helpers

@@ -638,76 +638,6 @@ void launch_group_count(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
 }
 
 // ------------------------------------------- (c)+(d) convolution epilogue
-struct EpiIn {
-  float po;  // old state (state mode, diff pass)
-  float sk;  // residual delta
-  float yh;  // consumers' view (residual carry, diff pass)
-  float g;   // frozen squeeze-excitation gate
-};
-
-template <typename T, bool REF>
-struct Epi {
-  float* P;
-  float* dP;
-  T* dout;
-  const float* bias;
-  const T* dskip;
-  const int* mskip;
-  const float* yhat;
-  const float* gate;
-  int64_t gate_hw;
-  int cout_p, mode, act;
-
-  // Phase 1: every global load one output element needs.  Callers issue
-  // the loads of all their elements before any store, so the loads overlap
-  // instead of each waiting behind a store that might alias it.
-  __device__ __forceinline__ EpiIn load(int pix, int n) const {
-    EpiIn e{0.f, 0.f, 0.f, 1.f};
-    if (mode == 0 && !REF) e.po = P[(int64_t)pix * cout_p + n];
-    if (mode == 0 && !REF && yhat) e.yh = yhat[(int64_t)pix * cout_p + n];
-    if (mode == 0 && gate) e.g = gate[(pix / gate_hw) * cout_p + n];
-    if (mskip) {
-      const int r = mskip[pix];
-      if (r >= 0) e.sk = to_f(dskip[(int64_t)r * cout_p + n]);
-    }
-    return e;
-  }
-
-  // Phase 2: add bias (reference pass) and the residual delta, then either
-  // defer the update (pooled layers), or update the f32 state in place and
-  // emit f(P_new) - f(P_old), or pass the linear delta on.  Returns
-  // |emitted delta| after rounding to the storage dtype.
-  __device__ __forceinline__ float store(int64_t o, int pix, int n, float acc,
-                                         EpiIn in) const {
-    float dp = acc;
-    if (REF) dp += bias[n];
-    dp += in.sk;
-    if (mode == 1) {
-      dP[o * cout_p + n] = dp;
-      return 0.f;
-    }
-    float d = dp;
-    if (mode == 0) {
-      const float pn = in.po + dp;
-      P[(int64_t)pix * cout_p + n] = pn;
-      if (gate)
-        d = act_f(pn, act) * in.g - act_f(in.po, act) * in.g;
-      else
-        d = act_f(pn, act) - (!REF && yhat ? in.yh : act_f(in.po, act));
-    }
-    const T q = from_f<T>(d);
-    dout[o * cout_p + n] = q;
-    return fabsf(to_f(q));
-  }
-};
-
-template <typename T, bool REF>
-__device__ __forceinline__ Epi<T, REF> make_epi(const ConvArgs& a) {
-  return Epi<T, REF>{a.P, a.dP, (T*)a.dout, a.bias, (const T*)a.dskip,
-                     a.mskip, a.yhat, a.gate, a.gate_hw, a.cout_p, a.mode,
-                     a.act};
-}
-
 // --------------------------------------------------- (c) gather-GEMM MFMA
 // Output-stationary tile of BM=64 affected rows x BN=64 output channels,
 // four waves in a 2x2 arrangement, each owning a 32x32 sub-tile (2x2 MFMA
@@ -799,12 +729,59 @@ template <typename T> struct Vec8Half {
 template <> struct Vec8<_Float16> : Vec8Half<_Float16> {};
 template <> struct Vec8<bf16_t> : Vec8Half<bf16_t> {};
 
+
 __device__ __forceinline__ void load8f(const float* p, float* f) {
   Vec8<float>::load(p, f);
 }
 __device__ __forceinline__ void store8f(float* p, const float* f) {
   *(float4*)p = make_float4(f[0], f[1], f[2], f[3]);
   *(float4*)(p + 4) = make_float4(f[4], f[5], f[6], f[7]);
+}
+
+// Pre-activation state storage: f32, or bf16 (nets created with a bf16
+// state), which holds every value rounded to nearest even.  `half` is the
+// net's choice (uniform); indices count values, not bytes.
+__device__ __forceinline__ float state_round(bool half, float x) {
+  return half ? to_f(from_f<bf16_t>(x)) : x;
+}
+__device__ __forceinline__ void state_load8(const float* P, bool half,
+                                            int64_t i, float* f) {
+  if (half)
+    Vec8<bf16_t>::load((const bf16_t*)P + i, f);
+  else
+    load8f(P + i, f);
+}
+__device__ __forceinline__ void state_store8(float* P, bool half, int64_t i,
+                                             const float* f) {
+  if (half)
+    (void)Vec8<bf16_t>::store((bf16_t*)P + i, f);
+  else
+    store8f(P + i, f);
+}
+__device__ __forceinline__ float4 state_load4(const float* P, bool half,
+                                              int64_t i) {
+  if (!half) return *(const float4*)(P + i);
+  const uint2 v = *(const uint2*)((const bf16_t*)P + i);
+  const bf16_t* h = (const bf16_t*)&v;
+  return make_float4(to_f(h[0]), to_f(h[1]), to_f(h[2]), to_f(h[3]));
+}
+__device__ __forceinline__ void state_store4(float* P, bool half, int64_t i,
+                                             float4 f) {
+  if (!half) {
+    *(float4*)(P + i) = f;
+    return;
+  }
+  uint2 v;
+  bf16_t* h = (bf16_t*)&v;
+  h[0] = from_f<bf16_t>(f.x);
+  h[1] = from_f<bf16_t>(f.y);
+  h[2] = from_f<bf16_t>(f.z);
+  h[3] = from_f<bf16_t>(f.w);
+  *(uint2*)((bf16_t*)P + i) = v;
+}
+__device__ __forceinline__ float state_load1(const float* P, bool half,
+                                             int64_t i) {
+  return half ? to_f(((const bf16_t*)P)[i]) : P[i];
 }
 
 // Reduction stages of a layer that hold real (not padding) columns.
@@ -873,7 +850,7 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
         load8f(a.gate + (epix / a.gate_hw) * cout_p + n, g);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          pn[e] = po[e] + v[e];
+          pn[e] = state_round(a.p16, po[e] + v[e]);
           v[e] = act_c<ACT>(pn[e]) * g[e] - act_c<ACT>(po[e]) * g[e];
         }
       } else if (!REF && a.yhat) {
@@ -882,17 +859,17 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
         load8f(a.yhat + (int64_t)epix * cout_p + n, yh);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          pn[e] = po[e] + v[e];
+          pn[e] = state_round(a.p16, po[e] + v[e]);
           v[e] = act_c<ACT>(pn[e]) - yh[e];
         }
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          pn[e] = po[e] + v[e];
+          pn[e] = state_round(a.p16, po[e] + v[e]);
           v[e] = act_c<ACT>(pn[e]) - act_c<ACT>(po[e]);
         }
       }
-      store8f(a.P + (int64_t)epix * cout_p + n, pn);
+      state_store8(a.P, a.p16, (int64_t)epix * cout_p + n, pn);
     }
     rm = fmaxf(rm, Vec8<T>::store(dout + eo * cout_p + n, v));
   }
@@ -989,7 +966,7 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
   for (int q = 0; q < Q; ++q) {
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
     if (run && c0 + 4 * q < cout_p)
-      v = *(const float4*)(a.P + site * cout_p + c0 + 4 * q);
+      v = state_load4(a.P, a.p16, site * cout_p + c0 + 4 * q);
     P[4 * q] = v.x;
     P[4 * q + 1] = v.y;
     P[4 * q + 2] = v.z;
@@ -1038,7 +1015,8 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
         float d[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float po = P[4 * q + e], pn = po + uv[e];
+          const float po = P[4 * q + e];
+          const float pn = state_round(a.p16, po + uv[e]);
           d[e] = act_c<ACT>(pn) - act_c<ACT>(po);
           P[4 * q + e] = pn;
         }
@@ -1052,8 +1030,9 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
 #pragma unroll
     for (int q = 0; q < Q; ++q)
       if (c0 + 4 * q < cout_p)
-        *(float4*)(a.P + site * cout_p + c0 + 4 * q) =
-            make_float4(P[4 * q], P[4 * q + 1], P[4 * q + 2], P[4 * q + 3]);
+        state_store4(a.P, a.p16, site * cout_p + c0 + 4 * q,
+                     make_float4(P[4 * q], P[4 * q + 1], P[4 * q + 2],
+                                 P[4 * q + 3]));
   }
   __syncthreads();
   if (tid < rows && s_rmax[tid])
@@ -1453,7 +1432,8 @@ void k_conv_gemm(ConvArgs a) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) po[e] = 0.f;
         } else {
-          load8f(a.P + (int64_t)epix * cout_p + n0 + ec + 8 * h, po);
+          state_load8(a.P, a.p16, (int64_t)epix * cout_p + n0 + ec + 8 * h,
+                      po);
         }
       };
       auto load_sk = [&](int h, float* sk) {
@@ -1504,7 +1484,7 @@ __global__ __launch_bounds__(256) void k_split_epi(ConvArgs a) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) po[h][e] = sk[h][e] = 0.f;
       if (hv[h] && a.mode == 0 && !REF)
-        load8f(a.P + (int64_t)epix * cout_p + n, po[h]);
+        state_load8(a.P, a.p16, (int64_t)epix * cout_p + n, po[h]);
     }
     const int rsk = (a.mskip && eok) ? a.mskip[epix] : -1;
 #pragma unroll
@@ -1674,7 +1654,7 @@ __device__ __forceinline__ void conv_dw_rows(const ConvArgs& a) {
     for (int e = 0; e < 8; ++e) sk[e] = po[e] = 0.f;
     if (rsk >= 0) Vec8<T>::load(dskip + (int64_t)rsk * cout_p + c0, sk);
     const bool state = a.mode == kModeState;
-    if (state && !REF) load8f(a.P + (int64_t)pix * cout_p + c0, po);
+    if (state && !REF) state_load8(a.P, a.p16, (int64_t)pix * cout_p + c0, po);
     if (state && a.gate)
       load8f(a.gate + (pix / a.gate_hw) * cout_p + c0, ex);
     else if (state && !REF && a.yhat)
@@ -1693,8 +1673,8 @@ __device__ __forceinline__ void conv_dw_rows(const ConvArgs& a) {
     if (state) {
       float pn[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pn[e] = po[e] + v[e];
-      store8f(a.P + (int64_t)pix * cout_p + c0, pn);
+      for (int e = 0; e < 8; ++e) pn[e] = state_round(a.p16, po[e] + v[e]);
+      state_store8(a.P, a.p16, (int64_t)pix * cout_p + c0, pn);
       if (a.gate) {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
@@ -1918,12 +1898,13 @@ __global__ __launch_bounds__(256) void k_se_squeeze(SeArgs a) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) po[e] = 0.f;
       } else {
-        load8f(a.P + p * cp + v * 8, po);
+        state_load8(a.P, a.p16, p * cp + v * 8, po);
       }
       load8f(a.dP + (int64_t)r * cp + v * 8, dp);
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        acc[k][e] += act_f(po[e] + dp[e], a.act) - act_f(po[e], a.act);
+        acc[k][e] += act_f(state_round(a.p16, po[e] + dp[e]), a.act) -
+                     act_f(po[e], a.act);
     }
   }
 #pragma unroll
@@ -2062,7 +2043,7 @@ __global__ __launch_bounds__(256) void k_se_emit(SeArgs a) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) po[e] = 0.f;
       } else {
-        load8f(a.P + row * cp + c0, po);
+        state_load8(a.P, a.p16, row * cp + c0, po);
       }
       if (r >= 0) {
         load8f(a.dP + (int64_t)r * cp + c0, dp);
@@ -2076,7 +2057,7 @@ __global__ __launch_bounds__(256) void k_se_emit(SeArgs a) {
       load8f(carry ? a.yhat + row * cp + c0 : so + c0, go);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        pn[e] = po[e] + dp[e];
+        pn[e] = state_round(a.p16, po[e] + dp[e]);
         const float en = act_f(pn[e], a.act) * gn[e];
         const float eo = a.ref     ? 0.f
                          : carry   ? go[e]
@@ -2084,7 +2065,7 @@ __global__ __launch_bounds__(256) void k_se_emit(SeArgs a) {
         d[e] = en - eo;
       }
       rm = fmaxf(rm, Vec8<T>::store(dout + row * cp + c0, d));
-      if (r >= 0) store8f(const_cast<float*>(a.P) + row * cp + c0, pn);
+      if (r >= 0) state_store8(const_cast<float*>(a.P), a.p16, row * cp + c0, pn);
     }
   }
 #pragma unroll
@@ -2313,7 +2294,7 @@ __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
 #pragma unroll
   for (int k = 0; k < IT; ++k) {
     const int v = lane + k * TPS;
-    if (v < V) load8f(a.P + p * cp + v * 8, pv[k]);
+    if (v < V) state_load8(a.P, a.p16, p * cp + v * 8, pv[k]);
   }
   uint32_t bits = 0;
   for (int t = 0; t < a.nf; ++t) {
@@ -2329,7 +2310,8 @@ __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
           float* row = a.dP + (int64_t)r * cp + v * 8;
           load8f(row, dp);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) pn[e] = pv[k][e] + dp[e];
+          for (int e = 0; e < 8; ++e)
+            pn[e] = state_round(a.p16, pv[k][e] + dp[e]);
           if (a.pool_mode) {
             store8f(row, pn);
           } else {
@@ -2379,7 +2361,7 @@ __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
 #pragma unroll
     for (int k = 0; k < IT; ++k) {
       const int v = lane + k * TPS;
-      if (v < V) store8f(a.P + p * cp + v * 8, pv[k]);
+      if (v < V) state_store8(a.P, a.p16, p * cp + v * 8, pv[k]);
     }
   }
 }
@@ -2548,10 +2530,10 @@ void launch_chunk_commit(const Prof& pf, hipStream_t s, float* P,
 }
 
 // ------------------------------------------------------- dense output
-__global__ __launch_bounds__(256) void k_output(const float* P, int cp, int C,
-                                                int N, Geo g, int has_pool,
-                                                int act, const float* se,
-                                                float* out) {
+__global__ __launch_bounds__(256) void k_output(const float* P, int p16,
+                                                int cp, int C, int N, Geo g,
+                                                int has_pool, int act,
+                                                const float* se, float* out) {
   // g.Hi/Wi: conv grid; g.Ho/Wo: output grid (== conv grid without pool)
   const int64_t total = (int64_t)N * g.Ho * g.Wo * C;
   const int64_t hwo = (int64_t)g.Ho * g.Wo;
@@ -2560,7 +2542,7 @@ __global__ __launch_bounds__(256) void k_output(const float* P, int cp, int C,
     const int64_t q = idx / C;
     const int c = (int)(idx - q * C);
     if (!has_pool) {
-      const float v = act_f(P[q * cp + c], act);
+      const float v = act_f(state_load1(P, p16, q * cp + c), act);
       out[idx] = se ? v * se[(q / hwo) * cp + c] : v;
       continue;
     }
@@ -2574,7 +2556,9 @@ __global__ __launch_bounds__(256) void k_output(const float* P, int cp, int C,
       for (int kx = 0; kx < g.kw; ++kx) {
         const int ix = qx * g.sw - g.pw + kx;
         if (ix < 0 || ix >= g.Wi) continue;
-        m = fmaxf(m, act_f(P[(((int64_t)n * g.Hi + iy) * g.Wi + ix) * cp + c],
+        m = fmaxf(m, act_f(state_load1(
+                               P, p16,
+                               (((int64_t)n * g.Hi + iy) * g.Wi + ix) * cp + c),
                            act));
       }
     }
@@ -2582,12 +2566,12 @@ __global__ __launch_bounds__(256) void k_output(const float* P, int cp, int C,
   }
 }
 
-void launch_output(const Prof& pf, hipStream_t s, const float* P, int cp,
-                   int C, int N, Geo g, int has_pool, int act,
+void launch_output(const Prof& pf, hipStream_t s, const float* P, int p16,
+                   int cp, int C, int N, Geo g, int has_pool, int act,
                    const float* se, float* out) {
   prof_begin(pf, 16 /*ST_K_OUTPUT*/, s);
   k_output<<<grid_for((int64_t)N * g.Ho * g.Wo * C, 8192), 256, 0, s>>>(
-      P, cp, C, N, g, has_pool, act, se, out);
+      P, p16, cp, C, N, g, has_pool, act, se, out);
   prof_end(pf, 16, s);
 }
 

@@ -59,10 +59,15 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
     return create_fail(ST_ERR_INVALID_ARG, "max_frames must be in [1, 32]");
   if (dtype != ST_F32 && dtype != ST_F16 && dtype != ST_BF16)
     return create_fail(ST_ERR_INVALID_ARG, "unknown dtype");
-  if (flags & ~(uint32_t)(ST_NET_RESIDUAL_CARRY | ST_NET_FROZEN_SE))
+  if (flags & ~(uint32_t)(ST_NET_RESIDUAL_CARRY | ST_NET_FROZEN_SE |
+                          ST_NET_BF16_STATE))
     return create_fail(ST_ERR_INVALID_ARG, "unknown flag");
   const bool carry = (flags & ST_NET_RESIDUAL_CARRY) != 0;
   const bool frozen_se = (flags & ST_NET_FROZEN_SE) != 0;
+  const bool bf16_state = (flags & ST_NET_BF16_STATE) != 0;
+  if (carry && bf16_state)
+    return create_fail(ST_ERR_UNSUPPORTED,
+                       "a bf16 state with residual carry is not supported");
   if (carry && frozen_se)
     return create_fail(ST_ERR_INVALID_ARG,
                        "residual carry and frozen squeeze-excitation are "
@@ -85,6 +90,7 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
   net->F = max_frames;
   net->carry = carry;
   net->frozen_se = frozen_se;
+  net->bf16_state = bf16_state;
   net->layers.resize(n_layers);
   net->tensors.resize(n_layers + 1);
 
@@ -131,6 +137,9 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
       return bad(ST_ERR_INVALID_ARG, i, "empty conv output");
     L.Ho = (int)ho; L.Wo = (int)wo;
     L.pool = d.pool_k_h > 0 || d.pool_k_w > 0;
+    if (L.pool && bf16_state)
+      return bad(ST_ERR_UNSUPPORTED, i,
+                 "a bf16 state is not supported for max-pooled layers");
     if (L.pool) {
       if (d.pool_k_h < 1 || d.pool_k_w < 1 || d.pool_s_h < 1 ||
           d.pool_s_w < 1 || d.pool_p_h < 0 || d.pool_p_w < 0 ||
@@ -251,7 +260,9 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
       if (L.se) L.off_dP = a.take(sizeof(float) * L.conv_grid * L.cout_p);
     }
     L.off_nbr = a.take(sizeof(int32_t) * citems * L.K);
-    if (L.stateful) L.off_P = a.take(sizeof(float) * L.conv_grid * L.cout_p);
+    if (L.stateful)
+      L.off_P = a.take((bf16_state ? 2 : sizeof(float)) * L.conv_grid *
+                       L.cout_p);
     if (carry) L.off_yhat = a.take(sizeof(float) * T.grid * L.cout_p);
     if (L.dw)
       L.off_w = a.take(sizeof(float) * L.K * L.cout_p);

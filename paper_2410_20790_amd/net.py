@@ -35,11 +35,13 @@ class SparseTemNet:
     via ``encode_chunk`` (see include/sparsetem.h).  ``carry``: residual
     carry (ST_NET_RESIDUAL_CARRY; frame by frame only); ``frozen_se``:
     squeeze-excitation gates kept from the reference frame
-    (ST_NET_FROZEN_SE, an approximation)."""
+    (ST_NET_FROZEN_SE, an approximation); ``bf16_state``: pre-activation
+    state stored in bf16 (ST_NET_BF16_STATE, an approximation)."""
 
     def __init__(self, layers: Sequence, batch: int, H: int, W: int, C: int,
                  dtype: str = "f32", device="cuda", max_frames: int = 1,
-                 carry: bool = False, frozen_se: bool = False):
+                 carry: bool = False, frozen_se: bool = False,
+                 bf16_state: bool = False):
         self.dtype = dtype
         self.tdtype = TORCH_DTYPES[dtype]
         dev = torch.device(device)
@@ -71,9 +73,11 @@ class SparseTemNet:
         self.max_frames = max_frames
         self.carry = carry
         self.frozen_se = frozen_se
-        if carry or frozen_se:
+        self.bf16_state = bf16_state
+        if carry or frozen_se or bf16_state:
             flags = ((B.NET_RESIDUAL_CARRY if carry else 0) |
-                     (B.NET_FROZEN_SE if frozen_se else 0))
+                     (B.NET_FROZEN_SE if frozen_se else 0) |
+                     (B.NET_BF16_STATE if bf16_state else 0))
             self.handle = B.st_create_net_ex(descs, batch, max_frames, H, W,
                                              C, B.DTYPE_CODES[dtype], flags)
         elif max_frames > 1:

@@ -45,11 +45,12 @@ def to_dev(frame, dtype):
         "cuda", TORCH[dtype]).contiguous()
 
 
-def make_pair(net, carry=False, frozen_se=False):
+def make_pair(net, carry=False, frozen_se=False, state_bf16=False):
     o = oracle.OracleNet(net.layers, net.batch, net.H, net.W, net.C,
-                         net.dtype, carry=carry, frozen_se=frozen_se)
+                         net.dtype, carry=carry, frozen_se=frozen_se,
+                         state_bf16=state_bf16)
     g = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, net.dtype,
-                     carry=carry, frozen_se=frozen_se)
+                     carry=carry, frozen_se=frozen_se, bf16_state=state_bf16)
     return o, g
 
 
@@ -62,10 +63,14 @@ def check_views(net, o, g, tag):
         assert e <= RTOL[net.dtype], f"{tag}: view of layer {i}: {e}"
 
 
-def compare_frame(net, o, g, out_g, tag, check_rulebook=True):
+def compare_frame(net, o, g, out_g, tag, check_rulebook=True, tol_dtype=None):
     """Compare every artefact of the last diff frame.  Returns the number
-    of band rows (keep decisions that legitimately differ)."""
-    dt = net.dtype
+    of band rows (keep decisions that legitimately differ).  tol_dtype:
+    the precision the tolerances and bands are taken at (default: the
+    net's storage dtype; "bf16" for a bf16 state, whose values the two
+    sides may round to neighbouring bf16 values when their f32 sums differ
+    in the last bit)."""
+    dt = tol_dtype or net.dtype
     rtol = RTOL[dt]
     out_o = o.last["out"]
     e = rel(out_g.cpu().numpy(), out_o)
@@ -147,10 +152,11 @@ def check_rulebooks(net, o, g, tag):
 
 
 def run_chunk(net, frames, thr, tag, max_band=0, carry=False,
-              frozen_se=False):
+              frozen_se=False, state_bf16=False):
     """Encode a chunk on both sides and compare after every frame (with
     carry, also the consumers' views while no keep decision differed)."""
-    o, g = make_pair(net, carry, frozen_se)
+    o, g = make_pair(net, carry, frozen_se, state_bf16)
+    tdt = "bf16" if state_bf16 else net.dtype
     try:
         thr_l = [thr] * (len(net.layers) + 1) if np.isscalar(thr) else thr
         say(f"[gpu] {tag}: reference frame")
@@ -158,17 +164,18 @@ def run_chunk(net, frames, thr, tag, max_band=0, carry=False,
         out_g = g.encode_reference(to_dev(frames[0], net.dtype))
         torch.cuda.synchronize()
         e = rel(out_g.cpu().numpy(), out_o)
-        assert e <= RTOL[net.dtype], f"{tag}: reference output {e}"
+        assert e <= RTOL[tdt], f"{tag}: reference output {e}"
         for i in o.P:
             Pg = B.st_debug_state(g.handle, i, o.P[i].shape)
-            assert rel(Pg, o.P[i]) <= RTOL[net.dtype], f"{tag}: ref state {i}"
+            assert rel(Pg, o.P[i]) <= RTOL[tdt], f"{tag}: ref state {i}"
         total_band = 0
         for t in range(1, len(frames)):
             say(f"[gpu] {tag}: diff frame {t}")
             o.encode_diff(frames[t], thr_l)
             out_g = g.encode_diff(to_dev(frames[t], net.dtype), thr_l)
             torch.cuda.synchronize()
-            total_band += compare_frame(net, o, g, out_g, f"{tag} f{t}")
+            total_band += compare_frame(net, o, g, out_g, f"{tag} f{t}",
+                                        tol_dtype=tdt)
             if carry and total_band == 0:
                 check_views(net, o, g, f"{tag} f{t}")
             for t2 in range(len(net.layers) + 1):

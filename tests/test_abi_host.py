@@ -262,7 +262,7 @@ def test_residual_carry_flag():
         B.st_destroy_net(h0)
         B.st_destroy_net(h1)
     # an unknown flag, and carry with frozen squeeze-excitation (exclusive)
-    for flags, status in ((4, B.ST_ERR_INVALID_ARG),
+    for flags, status in ((8, B.ST_ERR_INVALID_ARG),
                           (B.NET_RESIDUAL_CARRY | B.NET_FROZEN_SE,
                            B.ST_ERR_INVALID_ARG)):
         with pytest.raises(B.StError) as e:
@@ -273,3 +273,35 @@ def test_residual_carry_flag():
         B.st_create_net_ex(d, net.batch, 4, net.H, net.W, net.C, B.ST_F32,
                            B.NET_RESIDUAL_CARRY)
     assert e.value.status == B.ST_ERR_UNSUPPORTED
+
+
+def test_bf16_state_flag():
+    """ST_NET_BF16_STATE halves every stateful layer's state (2 bytes per
+    value instead of 4); it is refused for max-pooled nets and with
+    residual carry."""
+    from oracle import sparsetem_oracle as so
+    net = toy_net()
+    d = descs(net)
+    h0 = B.st_create_net(d, net.batch, net.H, net.W, net.C, B.ST_F32)
+    h1 = B.st_create_net_ex(d, net.batch, 1, net.H, net.W, net.C, B.ST_F32,
+                            B.NET_BF16_STATE)
+    try:
+        saved = B.st_workspace_bytes(h0) - B.st_workspace_bytes(h1)
+        want = 0
+        for i, L in enumerate(net.layers):
+            if so._is_stateful(net.layers, i):
+                n, h, w, _ = B.st_tensor_shape(h0, i)
+                want += 2 * n * h * w * ((L.c_out + 7) // 8 * 8)
+        # each allocation is rounded up to the workspace alignment
+        assert want <= saved + 256 * len(net.layers)
+        assert saved <= want + 256 * len(net.layers)
+    finally:
+        B.st_destroy_net(h0)
+        B.st_destroy_net(h1)
+    pooled = resnet_mini_net()
+    for n, flags in ((pooled, B.NET_BF16_STATE),
+                     (net, B.NET_BF16_STATE | B.NET_RESIDUAL_CARRY)):
+        with pytest.raises(B.StError) as e:
+            B.st_create_net_ex(descs(n), n.batch, 1, n.H, n.W, n.C, B.ST_F32,
+                               flags)
+        assert e.value.status == B.ST_ERR_UNSUPPORTED
