@@ -253,6 +253,45 @@ def copy_calibration():
     print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 10}))
 
 
+def measured_peaks():
+    """The box's own ceilings beside the published ones: a STREAM-like
+    device copy of 1 GiB (read + write bytes over the time of one copy,
+    best of 10 HIP-event-timed copies) and a large bf16 matrix product
+    (8192^3 on the library GEMM, the MFMA-bound ceiling a practical kernel
+    reaches; best of 5)."""
+    import torch
+    n = (1 << 30) // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    y.copy_(x)
+
+    def best(fn, reps):
+        t = []
+        for _ in range(reps):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            t.append(a.elapsed_time(b) * 1e-3)
+        return min(t)
+
+    copy_s = best(lambda: y.copy_(x), 10)
+    del x, y
+    m = 8192
+    a = torch.randn(m, m, dtype=torch.bfloat16, device="cuda")
+    b = torch.randn(m, m, dtype=torch.bfloat16, device="cuda")
+    c = a @ b
+    gemm_s = best(lambda: torch.matmul(a, b, out=c), 5)
+    del a, b, c
+    torch.cuda.empty_cache()
+    return {"copy_GBps": 2.0 * (1 << 30) / copy_s / 1e9,
+            "bf16_gemm_TFLOPs": 2.0 * m ** 3 / gemm_s / 1e12,
+            "published": {"hbm_GBps": HBM_PEAK_GBS,
+                          "bf16_mfma_TFLOPs": MFMA_PEAK_TFLOPS["bf16"]}}
+
+
 def kernel_source_hash():
     import hashlib
     src = os.path.join(ROOT, "paper_2410_20790_amd", "csrc",
@@ -1095,8 +1134,8 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
-              "(independent streams shard by image; see the design notes). "
+        print("bench.py measures one GPU: there is no multi-GPU path "
+              "(independent streams would shard by image, one net per GPU). "
               "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
@@ -1107,6 +1146,8 @@ def main():
     r = measure(wl, K, W, KP, args.thr, dense=not args.no_dense,
                 schedule=sched)
     r.pop("_thresholds", None)
+    if not args.no_dense:
+        r["roofline"]["measured_peaks"] = measured_peaks()
     res = {
         "metric": METRIC,
         "value": r.pop("value"),
