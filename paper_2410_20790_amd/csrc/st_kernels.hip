@@ -1928,22 +1928,26 @@ __global__ __launch_bounds__(256) void k_se_squeeze(SeArgs a) {
     a.part[((int64_t)n * a.nchunk + g) * cp + c] = sm[c];
 }
 
-__global__ __launch_bounds__(256) void k_se_excite(SeArgs a) {
-  extern __shared__ __align__(16) float sm[];  // [cp] means, [mid], [1024]
+// Excitation of one image per block (1024 threads): the frame's partial
+// sums over the site chunks (Lc lanes per 4-channel column, then the Lc
+// results in lane order) move the f64 channel sums S; the means feed the
+// hidden units (one wave per unit, two units per pass) and the gates
+// (each 4-channel output split over Lg thread groups of the hidden units,
+// then summed in group order).
+constexpr int kSeExciteThreads = 1024;
+__global__ __launch_bounds__(kSeExciteThreads) void k_se_excite(SeArgs a) {
+  constexpr int NT = kSeExciteThreads;
+  extern __shared__ __align__(16) float sm[];  // [cp] means, [mid], [NT] x4
   float* m = sm;
   float* z = sm + a.cp;
   float4* red = (float4*)(sm + a.cp + round_up8(a.mid));
-  const int n = blockIdx.x, cp = a.cp, V4 = cp / 4;
-  // partial sums as 4-channel vectors: Lc chunk lanes per vector take the
-  // partials g = l, l + Lc, ...; lane 0 adds the Lc results in order
-  const int Lc = V4 <= 256 ? 256 / V4 : 1;
+  const int n = blockIdx.x, cp = a.cp, V4 = cp / 4, t = threadIdx.x;
+  const int Lc = V4 <= NT ? NT / V4 : 1;
   const float4* part = (const float4*)(a.part + (int64_t)n * a.nchunk * cp);
-  for (int v0 = 0; v0 < V4; v0 += 256) {
-    const int t = threadIdx.x;
+  for (int v0 = 0; v0 < V4; v0 += NT) {
     const int v = v0 + (Lc > 1 ? t % V4 : t), l = Lc > 1 ? t / V4 : 0;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     if (v < V4 && l < Lc) {
-#pragma unroll 8
       for (int g = l; g < a.nchunk; g += Lc) {
         const float4 q = part[(int64_t)g * V4 + v];
         acc.x += q.x; acc.y += q.y; acc.z += q.z; acc.w += q.w;
@@ -1969,12 +1973,11 @@ __global__ __launch_bounds__(256) void k_se_excite(SeArgs a) {
     }
     __syncthreads();
   }
-  // hidden units z = silu(w1 . m + b1): one wave per unit, two units per
-  // pass, 4-channel vectors (up to 8 per lane in flight)
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // hidden units z = silu(w1 . m + b1)
+  const int lane = t & 63, wave = t >> 6, nw = NT / 64;
   const float4* m4 = (const float4*)m;
-  for (int j0 = wave; j0 < a.mid; j0 += 8) {
-    const int j1 = j0 + 4;
+  for (int j0 = wave; j0 < a.mid; j0 += 2 * nw) {
+    const int j1 = j0 + nw;
     const float4* w0 = (const float4*)(a.w1 + (int64_t)j0 * cp);
     const float4* w1 = (const float4*)(a.w1 + (int64_t)(j1 < a.mid ? j1 : j0)
                                        * cp);
@@ -1982,7 +1985,7 @@ __global__ __launch_bounds__(256) void k_se_excite(SeArgs a) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int v = lane + 64 * i;
-      if (v < cp / 4) {
+      if (v < V4) {
         const float4 x = m4[v], p = w0[v], q = w1[v];
         d0 += p.x * x.x + p.y * x.y + p.z * x.z + p.w * x.w;
         d1 += q.x * x.x + q.y * x.y + q.z * x.z + q.w * x.w;
@@ -1999,25 +2002,40 @@ __global__ __launch_bounds__(256) void k_se_excite(SeArgs a) {
     }
   }
   __syncthreads();
-  // gates: 4-channel vectors, hidden loop unrolled so loads overlap
-  for (int v = threadIdx.x; v < cp / 4; v += 256) {
-    float4 e = ((const float4*)a.b2)[v];
-    const float4* w = (const float4*)a.w2t + v;
-#pragma unroll 8
-    for (int j = 0; j < a.mid; ++j) {
-      const float4 q = w[(int64_t)j * (cp / 4)];
-      const float zj = z[j];
-      e.x += q.x * zj; e.y += q.y * zj; e.z += q.z * zj; e.w += q.w * zj;
+  // gates: output vector v, hidden units split over Lg groups
+  const int Lg = V4 <= NT ? NT / V4 : 1;
+  for (int v0 = 0; v0 < V4; v0 += NT) {
+    const int v = v0 + (Lg > 1 ? t % V4 : t), l = Lg > 1 ? t / V4 : 0;
+    float4 e = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (v < V4 && l < Lg) {
+      const float4* w = (const float4*)a.w2t + v;
+#pragma unroll 4
+      for (int j = l; j < a.mid; j += Lg) {
+        const float4 q = w[(int64_t)j * V4];
+        const float zj = z[j];
+        e.x += q.x * zj; e.y += q.y * zj; e.z += q.z * zj; e.w += q.w * zj;
+      }
     }
-    const float ev[4] = {e.x, e.y, e.z, e.w};
+    red[t] = e;
+    __syncthreads();
+    if (v < V4 && l == 0) {
+      float4 tot = ((const float4*)a.b2)[v];
+      for (int j = 0; j < Lg; ++j) {
+        const float4 q = red[t + j * V4];
+        tot.x += q.x; tot.y += q.y; tot.z += q.z; tot.w += q.w;
+      }
+      const float ev[4] = {tot.x, tot.y, tot.z, tot.w};
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int c = 4 * v + k;
-      a.s_new[(int64_t)n * cp + c] =
-          c < a.c ? 1.f / (1.f + expf(-ev[k])) : 0.f;
+      for (int k = 0; k < 4; ++k) {
+        const int c = 4 * v + k;
+        a.s_new[(int64_t)n * cp + c] =
+            c < a.c ? 1.f / (1.f + expf(-ev[k])) : 0.f;
+      }
     }
+    __syncthreads();
   }
 }
+
 
 template <typename T, int TPS>
 __global__ __launch_bounds__(256) void k_se_emit(SeArgs a) {
@@ -2091,8 +2109,10 @@ static void se_t(const Prof& pf, hipStream_t s, int dtype, const SeArgs& a) {
   k_se_squeeze<TPS><<<dim3(a.nchunk, a.N), 256, 0, s>>>(a);
   prof_end(pf, 19, s);
   prof_begin(pf, 20 /*ST_K_SE_EXCITE*/, s);
-  k_se_excite<<<a.N, 256,
-                sizeof(float) * (a.cp + round_up8(a.mid) + 1024), s>>>(a);
+  k_se_excite<<<a.N, kSeExciteThreads,
+                sizeof(float) * (a.cp + round_up8(a.mid) +
+                                 4 * kSeExciteThreads),
+                s>>>(a);
   prof_end(pf, 20, s);
   constexpr int R = 256 / TPS;
   const int blocks = (int)((a.npix + R - 1) / R);
