@@ -684,11 +684,10 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
         KP = batch
     elif chunk:
         KP = min(KP, chunk - 1)
-    # graph replay of the per-frame launch sequence: fixed thresholds and
-    # no squeeze-excitation (whose gate buffers alternate per frame)
+    # graph replay of the per-frame launch sequence (fixed or device-adjusted
+    # thresholds, any layer kind)
     use_ibst = wl["ibst"] if ibst is None else ibst
-    KG = K if (schedule == "frame" and not use_ibst and
-               (frozen_se or not any(L.se_mid for L in net.layers))) else 0
+    KG = K if schedule == "frame" else 0
     t_gen = time.perf_counter()
     frames_np = wl["frames"](frames_needed(chunk, W, K, KP, KG))
     t_gen = time.perf_counter() - t_gen
@@ -800,7 +799,7 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
     if KG:
         if chunk and feed.next_is_ref():
             feed.ref()
-        feed.replay = g.capture_diff(thr, out)
+        feed.replay = g.capture_diff(None if ctl == "device" else thr, out)
         gwall, grefs = run_diffs(feed, KG)
         feed.replay = None
         graph = {"diff_frames_per_s": KG / gwall,

@@ -189,7 +189,9 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
   a.ref = ref ? 1 : 0;
   a.grp = (L.pool || L.dw || own_rows) ? nullptr : grp;
   if (frozen) {
-    a.gate = ws.at<float>(L.off_ses) + L.se_par * (int64_t)net->N * L.cout_p;
+    a.gate = ws.at<float>(L.off_ses);
+    a.gpar = ws.at<int>(net->off_se_par);
+    a.gsz = (int64_t)net->N * L.cout_p;
     a.gate_hw = (int64_t)L.Ho * L.Wo;
   }
   a.mdone = ws.at<uint32_t>(net->off_mdone);
@@ -248,10 +250,9 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
     sa.b1 = ws.at<float>(L.off_seb1);
     sa.w2t = ws.at<float>(L.off_sew2);
     sa.b2 = ws.at<float>(L.off_seb2);
-    float* gates = ws.at<float>(L.off_ses);
-    const int64_t gsz = (int64_t)net->N * L.cout_p;
-    sa.s_old = gates + L.se_par * gsz;
-    sa.s_new = gates + (L.se_par ^ 1) * gsz;
+    sa.gates = ws.at<float>(L.off_ses);
+    sa.gpar = ws.at<int>(net->off_se_par);
+    sa.gsz = (int64_t)net->N * L.cout_p;
     sa.dout = ws.at<char>(out.off_rows);
     sa.rowmax = rowmax_out;
     sa.rowpix = ws.at<int>(out.off_rowpix);
@@ -360,17 +361,17 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
                                              1, 1, 0, 0};
     // the gates this frame used: just computed (exact), or kept from the
     // reference frame (frozen)
-    const int par = (ref || !net->frozen_se) ? (L.se_par ^ 1) : L.se_par;
-    const float* se =
-        L.se ? ws.at<float>(L.off_ses) + par * (int64_t)net->N * L.cout_p
-             : nullptr;
     launch_output(Prof{net, nl - 1}, s, ws.at<float>(L.off_P),
-                  net->bf16_state ? 1 : 0, L.cout_p,
-                  L.d.c_out, net->N, g, L.pool ? 1 : 0, L.d.act, se, out);
+                  net->bf16_state ? 1 : 0, L.cout_p, L.d.c_out, net->N, g,
+                  L.pool ? 1 : 0, L.d.act,
+                  L.se ? ws.at<float>(L.off_ses) : nullptr,
+                  ws.at<int>(net->off_se_par),
+                  (ref || !net->frozen_se) ? 1 : 0, out);
   }
-  // the gates just computed become the previous frame's
-  for (LayerPlan& L : net->layers)
-    if (L.se && (ref || !net->frozen_se)) L.se_par ^= 1;
+  // the gates just computed become the previous frame's (a parity word in
+  // device memory, so that a captured frame replays correctly)
+  if (net->has_se && (ref || !net->frozen_se))
+    launch_flip_parity(s, ws.at<int>(net->off_se_par));
   launch_cleanup(pf, s, ws.at<CleanEntry>(net->off_cleanup), net->n_cleanup,
                  net->ws, cnt, net->max_grid);
   // online adjustment: every cycle_refs-th reference frame starts a new
@@ -530,7 +531,9 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
     u.act = d.act;
     u.pool_mode = L.pool ? 1 : 0;
     if (L.se) {  // frozen gates (the chunk entry takes no exact SE)
-      u.gate = ws.at<float>(L.off_ses) + L.se_par * (int64_t)net->N * L.cout_p;
+      u.gate = ws.at<float>(L.off_ses);
+      u.gpar = ws.at<int>(net->off_se_par);
+      u.gsz = (int64_t)net->N * L.cout_p;
       u.gate_hw = (int64_t)L.Ho * L.Wo;
     }
     u.tps = se_threads_per_site(L.cout_p);

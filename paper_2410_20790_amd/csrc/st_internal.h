@@ -76,7 +76,6 @@ struct LayerPlan {
   bool stateful = false, pool = false, dw = false, ident = false;
   bool se = false;                  // squeeze-excitation after the act
   int se_mid = 0, se_chunk = 0, se_nchunk = 0, se_tps = 0;
-  int se_par = 0;                   // which gate buffer holds the last gates
   int mode = 0;                     // epilogue mode (kMode*, st_kernels.h)
   int split_max = 1;                // most reduction splits per output tile
   // workspace offsets
@@ -127,6 +126,8 @@ struct st_net {
   bool carry = false;                      // residual-carry semantics
   bool frozen_se = false;                  // frozen squeeze-excitation gates
   bool bf16_state = false;                 // pre-activation state in bf16
+  bool has_se = false;                     // any squeeze-excitation layer
+  size_t off_se_par = 0;                   // int: gate slot of the last gates
   double ibst_target = 0.9, ibst_eps = 0.025, ibst_theta_max = 1.0;
   // a cycle spans this many reference frames; reference frames seen since
   // the control was set

@@ -153,7 +153,9 @@ struct ConvArgs {
   // frozen squeeze-excitation: per-image gates [N][cout_p] scaling both
   // emitted values of a state-mode emission (image = site / gate_hw), or
   // NULL
-  const float* gate;
+  const float* gate;   // frozen gates: two slots [2][N][cout_p] (or NULL)
+  const int* gpar;     // the slot in use (device parity word)
+  int64_t gsz;         // floats per slot
   int64_t gate_hw;
 };
 // Returns false (and launches nothing) when a.zero is missing or misaligned.
@@ -212,8 +214,10 @@ struct SeArgs {
   const float* b1;     // [mid]
   const float* w2t;    // [mid][cp] (second excitation layer, transposed)
   const float* b2;     // [cp]
-  float* s_new;        // [N][cp]
-  const float* s_old;  // [N][cp]
+  float* gates;        // two gate slots [2][N][cp]: the previous frame's
+                       // gates in slot *gpar, this frame's in the other
+  const int* gpar;     // device parity word
+  int64_t gsz;         // floats per slot
   void* dout;          // emitted rows [npix][cp] (row = site)
   uint32_t* rowmax;
   int* rowpix;
@@ -268,7 +272,10 @@ struct ChunkUpdArgs {
   float* out;          // dense output [nf][npix][c] or NULL
   int64_t npix;        // conv sites per frame
   int nf, cp, c, act, pool_mode, tps;
-  const float* gate;    // frozen squeeze-excitation gates [N][cp] or NULL
+  const float* gate;    // frozen squeeze-excitation gates, two slots
+                        // [2][N][cp] (slot *gpar in use), or NULL
+  const int* gpar;
+  int64_t gsz;
   int64_t gate_hw;      // sites per image of the conv grid
 };
 void launch_chunk_update(const Prof& pf, hipStream_t s, int dtype,
@@ -296,10 +303,15 @@ void launch_chunk_commit(const Prof& pf, hipStream_t s, float* P,
                          int64_t nconv, int cp);
 
 // ---- dense network output (Accumulation)
-// p16: the state is stored as bf16.
+// p16: the state is stored as bf16.  se: the last layer's two gate slots
+// [2][N][cp] (or NULL), of which slot (*se_par ^ se_flip) applies.
 void launch_output(const Prof& pf, hipStream_t s, const float* P, int p16,
                    int cp, int C, int N, Geo pool, int has_pool, int act,
-                   const float* se, float* out);
+                   const float* se, const int* se_par, int se_flip,
+                   float* out);
+// Flips the net's gate-slot parity word (end of a frame whose
+// squeeze-excitation layers computed new gates).
+void launch_flip_parity(hipStream_t s, int* par);
 
 // ---- setup / introspection helpers
 void launch_fill_u32(hipStream_t s, void* p, int64_t n, uint32_t v);

@@ -779,6 +779,14 @@ __device__ __forceinline__ void state_store4(float* P, bool half, int64_t i,
   h[3] = from_f<bf16_t>(f.w);
   *(uint2*)((bf16_t*)P + i) = v;
 }
+// The gate slot in use: base + (*par ^ flip) * sz (two slots of one
+// squeeze-excitation layer's per-image gates, chosen by a parity word in
+// device memory so that a captured frame replays with either).
+__device__ __forceinline__ const float* gate_slot(const float* base,
+                                                  const int* par, int64_t sz,
+                                                  int flip) {
+  return base + (int64_t)((*par) ^ flip) * sz;
+}
 __device__ __forceinline__ float state_load1(const float* P, bool half,
                                              int64_t i) {
   return half ? to_f(((const bf16_t*)P)[i]) : P[i];
@@ -847,7 +855,9 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
       if (a.gate) {
         // frozen squeeze-excitation: both values scaled by the gates
         float g[8];
-        load8f(a.gate + (epix / a.gate_hw) * cout_p + n, g);
+        load8f(gate_slot(a.gate, a.gpar, a.gsz, 0) + (epix / a.gate_hw) *
+                   cout_p + n,
+               g);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           pn[e] = state_round(a.p16, po[e] + v[e]);
@@ -1656,7 +1666,9 @@ __device__ __forceinline__ void conv_dw_rows(const ConvArgs& a) {
     const bool state = a.mode == kModeState;
     if (state && !REF) state_load8(a.P, a.p16, (int64_t)pix * cout_p + c0, po);
     if (state && a.gate)
-      load8f(a.gate + (pix / a.gate_hw) * cout_p + c0, ex);
+      load8f(gate_slot(a.gate, a.gpar, a.gsz, 0) + (pix / a.gate_hw) *
+                 cout_p + c0,
+             ex);
     else if (state && !REF && a.yhat)
       load8f(a.yhat + (int64_t)pix * cout_p + c0, ex);
     float v[8];
@@ -1942,6 +1954,7 @@ __global__ __launch_bounds__(kSeExciteThreads) void k_se_excite(SeArgs a) {
   float* z = sm + a.cp;
   float4* red = (float4*)(sm + a.cp + round_up8(a.mid));
   const int n = blockIdx.x, cp = a.cp, V4 = cp / 4, t = threadIdx.x;
+  float* s_new = const_cast<float*>(gate_slot(a.gates, a.gpar, a.gsz, 1));
   const int Lc = V4 <= NT ? NT / V4 : 1;
   const float4* part = (const float4*)(a.part + (int64_t)n * a.nchunk * cp);
   for (int v0 = 0; v0 < V4; v0 += NT) {
@@ -2028,7 +2041,7 @@ __global__ __launch_bounds__(kSeExciteThreads) void k_se_excite(SeArgs a) {
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         const int c = 4 * v + k;
-        a.s_new[(int64_t)n * cp + c] =
+        s_new[(int64_t)n * cp + c] =
             c < a.c ? 1.f / (1.f + expf(-ev[k])) : 0.f;
       }
     }
@@ -2049,8 +2062,8 @@ __global__ __launch_bounds__(256) void k_se_emit(SeArgs a) {
   if (in) {
     const int n = (int)(row / a.hw);
     const int r = a.Mo[row];
-    const float* sn = a.s_new + (int64_t)n * cp;
-    const float* so = a.s_old + (int64_t)n * cp;
+    const float* sn = gate_slot(a.gates, a.gpar, a.gsz, 1) + (int64_t)n * cp;
+    const float* so = gate_slot(a.gates, a.gpar, a.gsz, 0) + (int64_t)n * cp;
 #pragma unroll
     for (int k = 0; k < IT; ++k) {
       const int v = lane + k * TPS;
@@ -2339,7 +2352,9 @@ __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
             if constexpr (GATE) {
               // frozen squeeze-excitation: both values scaled by the gates
               float g[8];
-              load8f(a.gate + (p / a.gate_hw) * cp + v * 8, g);
+              load8f(gate_slot(a.gate, a.gpar, a.gsz, 0) +
+                         (p / a.gate_hw) * cp + v * 8,
+                     g);
 #pragma unroll
               for (int e = 0; e < 8; ++e)
                 d[e] = act_f(pn[e], a.act) * g[e] -
@@ -2367,7 +2382,16 @@ __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
 #pragma unroll
       for (int k = 0; k < IT; ++k) {
         const int v = lane + k * TPS;
-        if (v < V) {
+        if (v < V && (a.c & 7) == 0 && ((uintptr_t)a.out & 15) == 0) {
+          // whole 8-channel vectors (rows of c floats, c a multiple of 8,
+          // on a 16-byte aligned output)
+          if (v * 8 < a.c) {
+            float f[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) f[e] = act_f(pv[k][e], a.act);
+            store8f(o + v * 8, f);
+          }
+        } else if (v < V) {
 #pragma unroll
           for (int e = 0; e < 8; ++e)
             if (v * 8 + e < a.c) o[v * 8 + e] = act_f(pv[k][e], a.act);
@@ -2553,7 +2577,12 @@ void launch_chunk_commit(const Prof& pf, hipStream_t s, float* P,
 __global__ __launch_bounds__(256) void k_output(const float* P, int p16,
                                                 int cp, int C, int N, Geo g,
                                                 int has_pool, int act,
-                                                const float* se, float* out) {
+                                                const float* se_base,
+                                                const int* se_par,
+                                                int se_flip, float* out) {
+  const float* se =
+      se_base ? gate_slot(se_base, se_par, (int64_t)N * cp, se_flip)
+              : nullptr;
   // g.Hi/Wi: conv grid; g.Ho/Wo: output grid (== conv grid without pool)
   const int64_t total = (int64_t)N * g.Ho * g.Wo * C;
   const int64_t hwo = (int64_t)g.Ho * g.Wo;
@@ -2588,11 +2617,20 @@ __global__ __launch_bounds__(256) void k_output(const float* P, int p16,
 
 void launch_output(const Prof& pf, hipStream_t s, const float* P, int p16,
                    int cp, int C, int N, Geo g, int has_pool, int act,
-                   const float* se, float* out) {
+                   const float* se, const int* se_par, int se_flip,
+                   float* out) {
   prof_begin(pf, 16 /*ST_K_OUTPUT*/, s);
   k_output<<<grid_for((int64_t)N * g.Ho * g.Wo * C, 8192), 256, 0, s>>>(
-      P, p16, cp, C, N, g, has_pool, act, se, out);
+      P, p16, cp, C, N, g, has_pool, act, se, se_par, se_flip, out);
   prof_end(pf, 16, s);
+}
+
+__global__ void k_flip_parity(int* par) {
+  if (threadIdx.x == 0) *par ^= 1;
+}
+
+void launch_flip_parity(hipStream_t s, int* par) {
+  k_flip_parity<<<1, 64, 0, s>>>(par);
 }
 
 // ------------------------------------------------------- bookkeeping

@@ -212,6 +212,7 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
   net->off_cnt = a.take(sizeof(uint64_t) * net->n_counters);
   net->off_dens = a.take(sizeof(uint64_t) * batch * F);
   net->off_tiles = a.take(sizeof(uint32_t) * kMaxTiles);
+  net->off_se_par = a.take(sizeof(int));
   net->off_xhat = a.take((size_t)t0.grid * in_c * net->esize);
   // Per-site buffers of the emitted tensors and rulebooks hold F frames
   // (chunk items: frame t's sites follow frame t-1's); the state, X_hat and
@@ -294,6 +295,7 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
       L.off_sew2 = a.take(sizeof(float) * L.cout_p * L.se_mid);
       L.off_seb2 = a.take(sizeof(float) * L.cout_p);
       L.off_ses = a.take(sizeof(float) * 2 * batch * L.cout_p);
+      net->has_se = true;
       L.off_sesum = a.take(sizeof(double) * batch * L.cout_p);
       L.off_separt = a.take(sizeof(float) * batch * L.se_nchunk * L.cout_p);
     }

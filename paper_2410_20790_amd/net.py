@@ -193,12 +193,15 @@ class SparseTemNet:
         return out
 
     def capture_diff(self, thr, out):
-        """Capture one diff-frame encode with fixed thresholds `thr` and
-        output `out` into a HIP graph; returns a callable that encodes a
-        frame by copying it into the graph's input slot and replaying the
-        graph (same kernels and arguments as encode_diff).  Requires a
-        reference frame to have been encoded; not available for nets with
-        squeeze-excitation (their gate buffers alternate per frame)."""
+        """Capture one diff-frame encode with output `out` into a HIP graph:
+        with fixed thresholds `thr` (encode_diff), or with thr None the
+        device-adjusted ones and the adjustment's step
+        (encode_diff_adaptive).  Returns a callable that encodes a frame by
+        copying it into the graph's input slot and replaying the graph
+        (the same kernels and arguments as the direct call; the
+        squeeze-excitation gate slots are chosen on the device, so replays
+        and direct calls interleave freely).  Requires a reference frame to
+        have been encoded."""
         return DiffGraph(self, thr, out)
 
     def density(self, layer: int, image: int = -1) -> float:
@@ -226,18 +229,19 @@ class DiffGraph:
     kernel sequence as st_encode_diff on the current stream."""
 
     def __init__(self, net: SparseTemNet, thr, out):
-        if net.has_se:
-            raise ValueError("nets with squeeze-excitation alternate their "
-                             "gate buffers per frame and cannot be replayed")
-        if len(thr) != net.n_layers + 1:
+        if thr is not None and len(thr) != net.n_layers + 1:
             raise ValueError("thr needs n_layers + 1 entries")
         self.slot = torch.zeros(net.in_shape, dtype=net.tdtype,
                                 device=net.device)
         self.out = out
         self.graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(self.graph):
-            B.st_encode_diff(net.handle, self.slot.data_ptr(), list(thr),
-                             out.data_ptr(), net._stream())
+            if thr is None:
+                B.st_encode_diff_adaptive(net.handle, self.slot.data_ptr(),
+                                          out.data_ptr(), net._stream())
+            else:
+                B.st_encode_diff(net.handle, self.slot.data_ptr(), list(thr),
+                                 out.data_ptr(), net._stream())
 
     def __call__(self, frame):
         self.slot.copy_(frame)

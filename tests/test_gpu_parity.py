@@ -395,3 +395,62 @@ def test_graph_replay_matches_eager(which):
     finally:
         ge.close()
         gg.close()
+
+
+@pytest.mark.parametrize("frozen", [False, True])
+def test_graph_replay_squeeze_excitation_adaptive(frozen):
+    """Graph replay of the adaptive entry on the mini EfficientNet (exact or
+    frozen squeeze-excitation, device-adjusted thresholds): the gate slots
+    are chosen by a parity word in device memory, so replays and a
+    reference frame encoded directly between them follow the eager net bit
+    for bit -- outputs, kept lists, states and thresholds after every
+    frame, each replay separated by eager work and a synchronisation."""
+    from paper_2410_20790_amd.ibst import nonlinear_tensors
+    from workloads import efficientnet_mini_net, object_video
+    net = efficientnet_mini_net()
+    frames = object_video(seed=12, n_frames=9, H=32, W=40, obj=8,
+                          obj_frac=0.1)
+    L_n = len(net.layers)
+    ctl = nonlinear_tensors(net.layers)
+    kw = dict(frozen_se=frozen)
+    ge = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, "f32", **kw)
+    gg = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, "f32", **kw)
+    try:
+        say(f"[gpu] graph replay squeeze-excitation frozen={frozen}")
+        for g in (ge, gg):
+            g.set_threshold_control(ctl, [0.01] * (L_n + 1), 0.7, 0.05, 0.5)
+        dev = [to_dev(f, "f32") for f in frames]
+        out_g = gg.new_output()
+        ge.encode_reference(dev[0])
+        gg.encode_reference(dev[0], out=out_g)
+        torch.cuda.synchronize()
+        replay = gg.capture_diff(None, out_g)
+        for t in range(1, len(frames)):
+            if t == 5:  # a reference frame in the middle, encoded directly
+                ge.encode_reference(dev[t])
+                gg.encode_reference(dev[t], out=out_g)
+                torch.cuda.synchronize()
+                continue
+            out_e = ge.encode_diff_adaptive(dev[t])
+            torch.cuda.synchronize()
+            replay(dev[t])
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(out_g.cpu().numpy(),
+                                          out_e.cpu().numpy(),
+                                          err_msg=f"frame {t}")
+            np.testing.assert_array_equal(gg.thresholds(), ge.thresholds())
+            for t2 in range(L_n + 1):
+                np.testing.assert_array_equal(
+                    B.st_debug_active(gg.handle, t2 - 1),
+                    B.st_debug_active(ge.handle, t2 - 1))
+            for i, L in enumerate(net.layers):
+                shape = tuple(ge.tensor_shape(i)[:3]) + (L.c_out,)
+                try:
+                    Pe = B.st_debug_state(ge.handle, i, shape)
+                except B.StError:
+                    continue  # no state in this layer
+                np.testing.assert_array_equal(
+                    B.st_debug_state(gg.handle, i, shape), Pe)
+    finally:
+        ge.close()
+        gg.close()
