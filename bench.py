@@ -890,7 +890,9 @@ def carry_comparison(name, thr_val, steps=18):
     at a threshold above zero, frame by frame over one chunk: every diff
     frame's output error against the dense forward of the same frame (the
     library's own dense pass), the diff-frames/s of both over `steps` timed
-    frames of further chunks, and the workspace of both."""
+    frames of further chunks, frame by frame and in SparseBatch chunks (the
+    chunk entry gives the frame-by-frame results), and the workspace of
+    both."""
     import torch
     from paper_2410_20790_amd import SparseTemNet
     wl = workload(name, 0.10)
@@ -930,6 +932,20 @@ def carry_comparison(name, thr_val, steps=18):
                       "max_rel_err_vs_dense_per_frame":
                           [round(e, 6) for e in errs[k]],
                       "workspace_bytes": g.ws_bytes}
+        # SparseBatch chunks (one st_encode_chunk call per chunk)
+        for k, carry in (("drop", False), ("carry", True)):
+            gc = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt,
+                              max_frames=chunk - 1, carry=carry)
+            try:
+                oc = torch.empty((chunk - 1,) + tuple(gc.out_shape),
+                                 dtype=torch.float32, device="cuda")
+                feed = Feed(gc, len(net.layers), frames, chunk, thr, None,
+                            oc, chunk - 1)
+                run_diffs(feed, chunk - 1)
+                wall, _ = run_diffs(feed, steps)
+                res[k]["chunk_diff_frames_per_s"] = steps / wall
+            finally:
+                gc.close()
         res["extra_memory_bytes"] = (nets["carry"].ws_bytes -
                                      nets["drop"].ws_bytes)
     finally:

@@ -131,8 +131,10 @@ enum {
    * without non-linearity, which then keeps P too) minus the view; kept
    * rows join the view, truncated rows carry their residual until the site
    * is affected again, so what consumers see never strays from the dense
-   * value by more than the threshold.  Frame by frame only
-   * (max_frames = 1). */
+   * value by more than the threshold.  Both entries: in a chunk, every
+   * layer applies its updates site by site in frame order, taking each
+   * frame's keep decision before the site's next frame is formed, so the
+   * result equals frame-by-frame encoding. */
   ST_NET_RESIDUAL_CARRY = 1,
   /* Frozen squeeze-excitation (an approximation, not the exact semantics):
    * the gates computed densely in the reference frame are kept for the
@@ -157,8 +159,8 @@ enum {
 /* As st_create_net_chunked, with creation flags (ST_NET_*).  Errors as
  * st_create_net_chunked, plus ST_ERR_INVALID_ARG for an unknown flag or
  * ST_NET_RESIDUAL_CARRY with ST_NET_FROZEN_SE, and ST_ERR_UNSUPPORTED for
- * ST_NET_RESIDUAL_CARRY with max_frames > 1 or with ST_NET_BF16_STATE, and
- * for ST_NET_BF16_STATE on a net with a max-pooled layer. */
+ * ST_NET_RESIDUAL_CARRY with ST_NET_BF16_STATE and for ST_NET_BF16_STATE on
+ * a net with a max-pooled layer. */
 st_status st_create_net_ex(const st_layer_desc* layers, int32_t n_layers,
                            int32_t batch, int32_t max_frames, int32_t in_h,
                            int32_t in_w, int32_t in_c, int32_t dtype,

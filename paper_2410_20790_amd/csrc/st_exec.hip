@@ -437,9 +437,12 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   // come site-major, tiles are aligned to site runs); pooled and
   // depthwise layers, layers with a split reduction and the output layer
   // (which also writes every frame's dense output) defer them to the
-  // update kernel.
+  // update kernel.  With residual carry every layer defers: a frame's keep
+  // decision (the row's largest magnitude over all its channels) must be
+  // known before the next frame's delta of the same site is formed, and
+  // the update kernel holds a site's channels in one group of lanes.
   const bool fused = L.stateful && !L.pool && !L.dw && !L.se && !out &&
-                     L.split_max <= 1;
+                     L.split_max <= 1 && !net->carry;
 
   if (!L.ident) {
     FlagArgs fa{};
@@ -537,6 +540,11 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
       u.gate_hw = (int64_t)L.Ho * L.Wo;
     }
     u.tps = se_threads_per_site(L.cout_p);
+    if (net->carry && !L.pool) {
+      u.yhat = ws.at<float>(L.off_yhat);
+      u.keep_thr = thr;
+      u.keep_thr_dev = thr_dev;
+    }
     launch_chunk_update(pf, s, net->dtype, u);
   }
   if (L.pool) {
@@ -570,6 +578,11 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
     pa.cp = L.cout_p;
     pa.act = d.act;
     pa.tps = se_threads_per_site(L.cout_p);
+    if (net->carry) {
+      pa.yhat = ws.at<float>(L.off_yhat);
+      pa.keep_thr = thr;
+      pa.keep_thr_dev = thr_dev;
+    }
     launch_chunk_pool_emit(pf, s, net->dtype, pa);
     launch_chunk_commit(pf, s, ws.at<float>(L.off_P), cdp, Mo,
                         ws.at<uint32_t>(net->off_chunk_aff), L.conv_grid,

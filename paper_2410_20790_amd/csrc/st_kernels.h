@@ -277,6 +277,11 @@ struct ChunkUpdArgs {
   const int* gpar;
   int64_t gsz;
   int64_t gate_hw;      // sites per image of the conv grid
+  // residual carry (not in pool mode): the consumers' view [npix][cp] and
+  // the emitted tensor's threshold, or yhat NULL
+  float* yhat;
+  float keep_thr;
+  const float* keep_thr_dev;  // in device memory (or NULL: keep_thr)
 };
 void launch_chunk_update(const Prof& pf, hipStream_t s, int dtype,
                          const ChunkUpdArgs& a);
@@ -294,6 +299,11 @@ struct ChunkPoolArgs {
   uint32_t* rowmax;
   int64_t nconv, npool;  // conv / pooled sites per frame
   int cp, act, tps;
+  // residual carry: the consumers' view of the pooled tensor [npool][cp]
+  // and its threshold, or yhat NULL
+  float* yhat;
+  float keep_thr;
+  const float* keep_thr_dev;
 };
 void launch_chunk_pool_emit(const Prof& pf, hipStream_t s, int dtype,
                             const ChunkPoolArgs& a);

@@ -2315,7 +2315,12 @@ void launch_chunk_scan(const Prof& pf, hipStream_t s, int dtype,
 // instead (the pool compares window states per frame) and the frames that
 // updated each site are recorded; the state is committed afterwards.
 // With `out` the dense output f(P) after every frame is written too.
-template <typename T, int TPS, bool GATE>
+// CARRY (residual carry, not in pool mode): the site's consumers' view
+// stays in registers across the frames; frame t emits f(P_t) - view, and
+// if the row is kept (its largest rounded magnitude, over all the site's
+// channels -- one group of TPS lanes holds them all -- above the
+// threshold) the rounded delta joins the view.
+template <typename T, int TPS, bool GATE, bool CARRY>
 __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
   constexpr int R = 256 / TPS, IT = TPS == 64 ? 4 : 1;
   T* dout = (T*)a.dout;
@@ -2323,18 +2328,22 @@ __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
   const int64_t p = (int64_t)blockIdx.x * R + threadIdx.x / TPS;
   if (p >= a.npix) return;
   const int cp = a.cp, V = cp / 8;
-  float pv[IT][8];
+  float pv[IT][8], yh[IT][8];
 #pragma unroll
   for (int k = 0; k < IT; ++k) {
     const int v = lane + k * TPS;
     if (v < V) state_load8(a.P, a.p16, p * cp + v * 8, pv[k]);
+    if (CARRY && v < V) load8f(a.yhat + p * cp + v * 8, yh[k]);
   }
+  const float kthr =
+      CARRY ? (a.keep_thr_dev ? *a.keep_thr_dev : a.keep_thr) : 0.f;
   uint32_t bits = 0;
   for (int t = 0; t < a.nf; ++t) {
     const int r = a.Mo[(int64_t)t * a.npix + p];
     if (r >= 0) {
       bits |= 1u << t;
       float rm = 0.f;
+      float dr[IT][8];  // the rounded deltas (residual carry)
 #pragma unroll
       for (int k = 0; k < IT; ++k) {
         const int v = lane + k * TPS;
@@ -2359,6 +2368,12 @@ __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
               for (int e = 0; e < 8; ++e)
                 d[e] = act_f(pn[e], a.act) * g[e] -
                        act_f(pv[k][e], a.act) * g[e];
+            } else if constexpr (CARRY) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                d[e] = act_f(pn[e], a.act) - yh[k][e];
+                dr[k][e] = to_f(from_f<T>(d[e]));
+              }
             } else {
 #pragma unroll
               for (int e = 0; e < 8; ++e)
@@ -2375,6 +2390,13 @@ __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
         for (int o = 1; o < TPS; o <<= 1)
           rm = fmaxf(rm, __shfl_xor(rm, o, 64));
         if (lane == 0) a.rowmax[r] = __float_as_uint(rm);
+        if (CARRY && rm > kthr) {
+          // kept: the consumers receive the rounded delta
+#pragma unroll
+          for (int k = 0; k < IT; ++k)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) yh[k][e] += dr[k][e];
+        }
       }
     }
     if (a.out) {
@@ -2406,6 +2428,7 @@ __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
     for (int k = 0; k < IT; ++k) {
       const int v = lane + k * TPS;
       if (v < V) state_store8(a.P, a.p16, p * cp + v * 8, pv[k]);
+      if (CARRY && v < V) store8f(a.yhat + p * cp + v * 8, yh[k]);
     }
   }
 }
@@ -2427,7 +2450,13 @@ __device__ __forceinline__ const float* state_at(const ChunkPoolArgs& a,
 
 // Pooled rows of frame t: max_window f(P after t) - max_window f(P after
 // t - 1), as the streaming pool does with its old and new states.
-template <typename T, int TPS>
+// CARRY (residual carry): the entry that opens a pooled site's run (the
+// kept lists are site-major, so a site's frames are adjacent entries)
+// walks the run in frame order with the site's consumers' view in
+// registers: each frame emits max_win f(P_t) - view, and a kept row (its
+// largest rounded magnitude above the threshold) adds its rounded delta to
+// the view.
+template <typename T, int TPS, bool CARRY>
 __global__ __launch_bounds__(256) void k_chunk_pool_emit(ChunkPoolArgs a) {
   constexpr int R = 256 / TPS, IT = TPS == 64 ? 4 : 1;
   T* dout = (T*)a.dout;
@@ -2437,21 +2466,17 @@ __global__ __launch_bounds__(256) void k_chunk_pool_emit(ChunkPoolArgs a) {
   if (j >= nQ) return;
   const Geo& g = a.g;
   const int64_t qi = a.Q[j];
-  const int t = (int)(qi / a.npool);
-  const int64_t q = qi - (int64_t)t * a.npool;
+  const int64_t q = qi % a.npool;
+  if (CARRY && j > 0 && (int64_t)a.Q[j - 1] % a.npool == q) return;
   const int64_t hwq = (int64_t)g.Ho * g.Wo;
   const int n = (int)(q / hwq);
   const int rem = (int)(q - n * hwq);
   const int qy = rem / g.Wo, qx = rem - (rem / g.Wo) * g.Wo;
   const int cp = a.cp, V = cp / 8;
-  float rm = 0.f;
+  // max over the window of f(P after frame t), 8 channels from v * 8
+  auto pooled = [&](int t, int v, float* mx) {
 #pragma unroll
-  for (int k = 0; k < IT; ++k) {
-    const int v = lane + k * TPS;
-    if (v >= V) continue;
-    float mn[8], mo[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) mn[e] = mo[e] = -INFINITY;
+    for (int e = 0; e < 8; ++e) mx[e] = -INFINITY;
     for (int ky = 0; ky < g.kh; ++ky) {
       const int iy = qy * g.sh - g.ph + ky;
       if (iy < 0 || iy >= g.Hi) continue;
@@ -2459,24 +2484,72 @@ __global__ __launch_bounds__(256) void k_chunk_pool_emit(ChunkPoolArgs a) {
         const int ix = qx * g.sw - g.pw + kx;
         if (ix < 0 || ix >= g.Wi) continue;
         const int64_t w = ((int64_t)n * g.Hi + iy) * g.Wi + ix;
-        float vn[8], vo[8];
-        load8f(state_at(a, w, t) + v * 8, vn);
-        load8f(state_at(a, w, t - 1) + v * 8, vo);
+        float vv[8];
+        load8f(state_at(a, w, t) + v * 8, vv);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          mn[e] = fmaxf(mn[e], act_f(vn[e], a.act));
-          mo[e] = fmaxf(mo[e], act_f(vo[e], a.act));
-        }
+        for (int e = 0; e < 8; ++e) mx[e] = fmaxf(mx[e], act_f(vv[e], a.act));
       }
     }
-    float d[8];
+  };
+  if constexpr (!CARRY) {
+    const int t = (int)(qi / a.npool);
+    float rm = 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) d[e] = mn[e] - mo[e];
-    rm = fmaxf(rm, Vec8<T>::store(dout + j * cp + v * 8, d));
+    for (int k = 0; k < IT; ++k) {
+      const int v = lane + k * TPS;
+      if (v >= V) continue;
+      float mn[8], mo[8], d[8];
+      pooled(t, v, mn);
+      pooled(t - 1, v, mo);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d[e] = mn[e] - mo[e];
+      rm = fmaxf(rm, Vec8<T>::store(dout + j * cp + v * 8, d));
+    }
+#pragma unroll
+    for (int o = 1; o < TPS; o <<= 1) rm = fmaxf(rm, __shfl_xor(rm, o, 64));
+    if (lane == 0) a.rowmax[j] = __float_as_uint(rm);
+  } else {
+    const float kthr = a.keep_thr_dev ? *a.keep_thr_dev : a.keep_thr;
+    float yh[IT][8];
+#pragma unroll
+    for (int k = 0; k < IT; ++k) {
+      const int v = lane + k * TPS;
+      if (v < V) load8f(a.yhat + q * cp + v * 8, yh[k]);
+    }
+    for (int64_t jj = j; jj < nQ; ++jj) {
+      const int64_t qj = a.Q[jj];
+      if (qj % a.npool != q) break;
+      const int t = (int)(qj / a.npool);
+      float rm = 0.f, dr[IT][8];
+#pragma unroll
+      for (int k = 0; k < IT; ++k) {
+        const int v = lane + k * TPS;
+        if (v >= V) continue;
+        float mn[8], d[8];
+        pooled(t, v, mn);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          d[e] = mn[e] - yh[k][e];
+          dr[k][e] = to_f(from_f<T>(d[e]));
+        }
+        rm = fmaxf(rm, Vec8<T>::store(dout + jj * cp + v * 8, d));
+      }
+#pragma unroll
+      for (int o = 1; o < TPS; o <<= 1) rm = fmaxf(rm, __shfl_xor(rm, o, 64));
+      if (lane == 0) a.rowmax[jj] = __float_as_uint(rm);
+      if (rm > kthr) {
+#pragma unroll
+        for (int k = 0; k < IT; ++k)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) yh[k][e] += dr[k][e];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < IT; ++k) {
+      const int v = lane + k * TPS;
+      if (v < V) store8f(a.yhat + q * cp + v * 8, yh[k]);
+    }
   }
-#pragma unroll
-  for (int o = 1; o < TPS; o <<= 1) rm = fmaxf(rm, __shfl_xor(rm, o, 64));
-  if (lane == 0) a.rowmax[j] = __float_as_uint(rm);
 }
 
 __global__ __launch_bounds__(256) void k_chunk_commit(float* P,
@@ -2503,9 +2576,11 @@ static void chunk_upd_t(hipStream_t s, const ChunkUpdArgs& a) {
   constexpr int R = 256 / TPS;
   const int grid = (int)((a.npix + R - 1) / R);
   if (a.gate)
-    k_chunk_update<T, TPS, true><<<grid, 256, 0, s>>>(a);
+    k_chunk_update<T, TPS, true, false><<<grid, 256, 0, s>>>(a);
+  else if (a.yhat && !a.pool_mode)
+    k_chunk_update<T, TPS, false, true><<<grid, 256, 0, s>>>(a);
   else
-    k_chunk_update<T, TPS, false><<<grid, 256, 0, s>>>(a);
+    k_chunk_update<T, TPS, false, false><<<grid, 256, 0, s>>>(a);
 }
 
 template <typename T>
@@ -2536,7 +2611,11 @@ void launch_chunk_update(const Prof& pf, hipStream_t s, int dtype,
 template <typename T, int TPS>
 static void chunk_pool_t(hipStream_t s, const ChunkPoolArgs& a) {
   constexpr int R = 256 / TPS;
-  k_chunk_pool_emit<T, TPS><<<(int)((a.capQ + R - 1) / R), 256, 0, s>>>(a);
+  const int grid = (int)((a.capQ + R - 1) / R);
+  if (a.yhat)
+    k_chunk_pool_emit<T, TPS, true><<<grid, 256, 0, s>>>(a);
+  else
+    k_chunk_pool_emit<T, TPS, false><<<grid, 256, 0, s>>>(a);
 }
 
 template <typename T>

@@ -72,9 +72,6 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
     return create_fail(ST_ERR_INVALID_ARG,
                        "residual carry and frozen squeeze-excitation are "
                        "exclusive");
-  if (carry && max_frames > 1)
-    return create_fail(ST_ERR_UNSUPPORTED,
-                       "residual carry needs frame-by-frame encoding");
   const int64_t F = max_frames;
   if ((int64_t)batch * in_h * in_w * F >= (int64_t)1 << 31)
     return create_fail(ST_ERR_INVALID_ARG, "input grid exceeds 2^31 pixels");

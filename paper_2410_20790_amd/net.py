@@ -33,7 +33,7 @@ class SparseTemNet:
     """One diff encoder: reference frame via ``encode_reference``, then
     diff frames via ``encode_diff``, or up to ``max_frames`` of them at once
     via ``encode_chunk`` (see include/sparsetem.h).  ``carry``: residual
-    carry (ST_NET_RESIDUAL_CARRY; frame by frame only); ``frozen_se``:
+    carry (ST_NET_RESIDUAL_CARRY); ``frozen_se``:
     squeeze-excitation gates kept from the reference frame
     (ST_NET_FROZEN_SE, an approximation); ``bf16_state``: pre-activation
     state stored in bf16 (ST_NET_BF16_STATE, an approximation)."""
