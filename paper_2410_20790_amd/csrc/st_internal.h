@@ -87,7 +87,7 @@ struct LayerPlan {
   size_t off_w = 0;                 // GEMM: dtype [cout_p][ktot_p]; dw: f32 [K][cout_p]
   size_t off_bias = 0;              // f32 [cout_p]
   size_t off_sew1 = 0, off_seb1 = 0, off_sew2 = 0, off_seb2 = 0;  // f32
-  size_t off_ses = 0;               // f32 [2][N][cout_p] gates (ping-pong)
+  size_t off_ses = 0;               // f32 [2][N][cout_p] gates, two slots
   size_t off_sesum = 0;             // f64 [N][cout_p] channel sums of f(P)
   size_t off_separt = 0;            // f32 [N][se_nchunk][cout_p]
   size_t off_flags = 0;             // uint8 [conv_grid] affected-output flags
