@@ -102,9 +102,13 @@ ConsList consumers_of(st_net* net, int t) {
       c.kind = kConsMark;
       c.flags = ws.at<uint8_t>(L.off_flags);
       c.g = conv_geo(L);
+      c.nf = net->last_nf;
+      c.nimg = net->N;
     } else {
       c.kind = kConsMarkSame;
       c.flags = ws.at<uint8_t>(L.off_flags);
+      c.nf = net->last_nf;
+      c.per = net->tensors[t].grid;
     }
     cl.c[cl.n++] = c;
   }
@@ -210,7 +214,8 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
   if (L.pool) {
     const Geo gp = pool_geo(L);
     uint8_t* pflags = ws.at<uint8_t>(L.off_pflags);
-    launch_mark(pf, ST_K_POOL_MARK, s, O, cO, L.conv_grid, gp, pflags);
+    launch_mark(pf, ST_K_POOL_MARK, s, O, cO, L.conv_grid, gp, pflags,
+                net->N, 1);
     FlagArgs fp{};
     fp.flags = pflags;
     fp.npix = out.grid;
@@ -550,7 +555,8 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   if (L.pool) {
     const Geo gp = pool_geo(L);
     uint8_t* pflags = ws.at<uint8_t>(L.off_pflags);
-    launch_mark(pf, ST_K_POOL_MARK, s, O, cO, citems, gp, pflags);
+    launch_mark(pf, ST_K_POOL_MARK, s, O, cO, citems, gp, pflags, net->N,
+                nf);
     FlagArgs fp{};
     fp.flags = pflags;
     fp.npix = outT.grid * nf;

@@ -50,8 +50,11 @@ struct Cons {
   uint32_t* rowmax;   // ident: row maxima of the consumer's output to clear
   u64* cnt_O;
   u64* pairs;
-  uint8_t* flags;     // mark: the consumer's affected-output flags
+  uint8_t* flags;     // mark: the consumer's affected-output flags,
+                      // site-major (site * nf + frame)
   Geo g;              // mark: the consumer's window geometry
+  int nf, nimg;       // mark: frames of the pass, images per frame
+  int64_t per;        // mark-same: sites per frame
 };
 struct ConsList {
   Cons c[kMaxCons];
@@ -101,8 +104,10 @@ struct FlagArgs {
 };
 void launch_flag_compact(const Prof& pf, int cls_count, int cls_write,
                          hipStream_t s, const FlagArgs& a);
+// flags: site-major (site * nf + frame) over nf frames of nimg images.
 void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
-                 const u64* n_list, int64_t max_items, Geo g, uint8_t* flags);
+                 const u64* n_list, int64_t max_items, Geo g, uint8_t* flags,
+                 int nimg, int nf);
 // Run-aligned row tiles of a site-major affected list O (chunk mode):
 // tstart[j] = first row of the run (same site) holding row j * step, for
 // j < ceil(nO / step), and tstart[ceil(nO / step)] = nO; the number of runs
@@ -246,7 +251,7 @@ struct ChunkScanArgs {
   int64_t npix;        // input sites per frame
   float thr;
   const float* thr_dev;  // threshold in device memory (or NULL: thr)
-  uint8_t* keep;       // [nf * npix] keep bytes
+  uint8_t* keep;       // [npix * nf] keep bytes, site-major
   uint8_t* base;       // [nf * npix] frame X_hat held (0xFF: chunk start)
   uint8_t* last;       // [npix] last kept frame (0xFF: none)
   uint32_t* tiles;

@@ -317,11 +317,16 @@ static void run_compact(const Prof& pf, int cls_count, int cls_write,
 // outputs are exactly the kept inputs); any other consumer gets its
 // affected output sites marked through its window geometry (or, for a
 // residual input, at the same site).
+// Marks the outputs whose window holds input item p (n = frame * nimg +
+// image); the output flags are site-major over nf frames (site * nf +
+// frame), so the compactions that visit items site-major read them in
+// order.
 __device__ __forceinline__ void mark_window(uint8_t* flags, int p,
-                                            const Geo& g) {
+                                            const Geo& g, int nimg, int nf) {
   const int64_t hwi = (int64_t)g.Hi * g.Wi;
-  const int n = (int)(p / hwi);
-  const int rem = (int)(p - n * hwi);
+  const int nn = (int)(p / hwi);
+  const int t = nn / nimg, n = nn - t * nimg;
+  const int rem = (int)(p - nn * hwi);
   const int iy = rem / g.Wi, ix = rem - (rem / g.Wi) * g.Wi;
   for (int ky = 0; ky < g.kh; ++ky) {
     const int ty = iy + g.ph - ky;
@@ -335,7 +340,7 @@ __device__ __forceinline__ void mark_window(uint8_t* flags, int p,
       if (tx % g.sw) continue;
       const int ox = tx / g.sw;
       if (ox >= g.Wo) continue;
-      flags[((int64_t)n * g.Ho + oy) * g.Wo + ox] = 1;
+      flags[(((int64_t)n * g.Ho + oy) * g.Wo + ox) * nf + t] = 1;
     }
   }
 }
@@ -350,9 +355,9 @@ __device__ __forceinline__ void cons_emit(const ConsList& cl, int p,
       c.nbr[pos] = row;
       if (c.rowmax) c.rowmax[pos] = 0u;
     } else if (c.kind == kConsMark) {
-      mark_window(c.flags, p, c.g);
+      mark_window(c.flags, p, c.g, c.nimg, c.nf);
     } else if (c.kind == kConsMarkSame) {
-      c.flags[p] = 1;
+      c.flags[(p % c.per) * c.nf + p / c.per] = 1;
     }
   }
 }
@@ -450,18 +455,20 @@ static int grid_for(int64_t items, int cap_blocks = 4096) {
 // Mark every output site reached by an active site through the window
 // (used for the pool windows of pooled layers).
 __global__ __launch_bounds__(256) void k_mark(const int* list, const u64* n1p,
-                                              Geo g, uint8_t* flags) {
+                                              Geo g, uint8_t* flags, int nimg,
+                                              int nf) {
   const int64_t n1 = (int64_t)*n1p;
   for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j < n1;
        j += (int64_t)gridDim.x * 256)
-    mark_window(flags, list[j], g);
+    mark_window(flags, list[j], g, nimg, nf);
 }
 
 void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
-                 const u64* n_list, int64_t max_items, Geo g,
-                 uint8_t* flags) {
+                 const u64* n_list, int64_t max_items, Geo g, uint8_t* flags,
+                 int nimg, int nf) {
   prof_begin(pf, cls, s);
-  k_mark<<<grid_for(max_items), 256, 0, s>>>(list, n_list, g, flags);
+  k_mark<<<grid_for(max_items), 256, 0, s>>>(list, n_list, g, flags, nimg,
+                                              nf);
   prof_end(pf, cls, s);
 }
 
@@ -549,18 +556,15 @@ struct FlagPred {
   struct Item {
     uint8_t f;
   };
-  __device__ bool count(int64_t j) const {
-    return flags[site_major(j, nf, per)] != 0;
-  }
-  __device__ Item load(int64_t j) const {
-    return Item{flags[site_major(j, nf, per)]};
-  }
+  // the flags are site-major: item j's flag is flags[j]
+  __device__ bool count(int64_t j) const { return flags[j] != 0; }
+  __device__ Item load(int64_t j) const { return Item{flags[j]}; }
   __device__ bool keep(const Item& it) const { return it.f != 0; }
   __device__ unsigned emit(int64_t j, unsigned pos, const Item&) const {
     const int64_t i = site_major(j, nf, per);
     list[pos] = (int)i;
     map[i] = (int)pos;
-    flags[i] = 0;
+    flags[j] = 0;
     if (rowmax) rowmax[pos] = 0u;
     if (!nbr) return 0u;
     const int64_t hwo = (int64_t)g.Ho * g.Wo;
@@ -2210,7 +2214,7 @@ __global__ __launch_bounds__(256) void k_chunk_scan_prep(ChunkScanArgs a) {
       float m = 0.f;
       for (int c = 0; c < a.C; ++c) m = fmaxf(m, fabsf(to_f(xt[c]) - xh[c]));
       const bool k = m > thr;
-      a.keep[i] = k ? 1 : 0;
+      a.keep[p * a.nf + t] = k ? 1 : 0;
       a.base[i] = cur;
       if (k) {
         for (int c = 0; c < a.C; ++c) xh[c] = to_f(xt[c]);
@@ -2237,13 +2241,10 @@ struct ChunkScanPred {
   struct Item {
     uint8_t k;
   };
-  // items are visited site-major (a site's kept frames adjacent)
-  __device__ bool count(int64_t j) const {
-    return keepb[site_major(j, nf, npix)] != 0;
-  }
-  __device__ Item load(int64_t j) const {
-    return Item{keepb[site_major(j, nf, npix)]};
-  }
+  // items are visited site-major (a site's kept frames adjacent); the
+  // keep bytes are stored in that order
+  __device__ bool count(int64_t j) const { return keepb[j] != 0; }
+  __device__ Item load(int64_t j) const { return Item{keepb[j]}; }
   __device__ bool keep(const Item& it) const { return it.k != 0; }
   // delta against the value X_hat held when frame t arrived
   __device__ unsigned emit(int64_t j, unsigned pos, const Item&) const {
@@ -2258,7 +2259,7 @@ struct ChunkScanPred {
     rowpix[pos] = (int)i;
     act[pos] = (int)i;
     map[i] = (int)pos;
-    keepb[i] = 0;
+    keepb[j] = 0;
     cons_emit(cons, (int)i, pos, (int)pos);
     return 0u;
   }
