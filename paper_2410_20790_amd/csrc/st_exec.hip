@@ -439,15 +439,17 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   uint32_t* rm_O = L.pool ? nullptr : rowmax_out;
   // Stateful layers whose every output row is finished by the GEMM tile
   // that computes it apply the chunk's updates in the GEMM epilogue (rows
-  // come site-major, tiles are aligned to site runs); pooled and
-  // depthwise layers, layers with a split reduction and the output layer
-  // (which also writes every frame's dense output) defer them to the
-  // update kernel.  With residual carry every layer defers: a frame's keep
-  // decision (the row's largest magnitude over all its channels) must be
-  // known before the next frame's delta of the same site is formed, and
-  // the update kernel holds a site's channels in one group of lanes.
+  // come site-major, tiles are aligned to site runs).  Such a layer runs
+  // unsplit: a chunk holds several frames' rows, enough tiles to fill the
+  // chip without splitting the reduction.  Pooled and depthwise layers and
+  // the output layer (which also writes every frame's dense output) defer
+  // the updates to the update kernel.  With residual carry every layer
+  // defers: a frame's keep decision (the row's largest magnitude over all
+  // its channels) must be known before the next frame's delta of the same
+  // site is formed, and the update kernel holds a site's channels in one
+  // group of lanes.
   const bool fused = L.stateful && !L.pool && !L.dw && !L.se && !out &&
-                     L.split_max <= 1 && !net->carry;
+                     !net->carry;
 
   if (!L.ident) {
     FlagArgs fa{};
@@ -516,7 +518,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   a.keep_thr_dev = thr_dev;
   a.zero = ws.at<char>(net->off_zero);
   a.part = ws.at<float>(net->off_part);
-  a.split_max = L.split_max;
+  a.split_max = fused ? 1 : L.split_max;
   if (L.dw)
     launch_conv_dw(pf, s, net->dtype, a);
   else if (!launch_conv_gemm(pf, s, net->dtype, a))
