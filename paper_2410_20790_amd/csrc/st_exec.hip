@@ -79,7 +79,26 @@ Geo pool_geo(const LayerPlan& L) {
 
 // Rulebook preparation the kept rows of tensor t do for the layers that
 // read it (see ConsList in st_kernels.h).
-ConsList consumers_of(st_net* net, int t) {
+// In a chunk, stateful layers whose every output row is finished by the
+// GEMM tile that computes it apply the chunk's updates in the GEMM epilogue
+// (rows come site-major, tiles are aligned to site runs).  Such a layer
+// runs unsplit: a chunk holds several frames' rows, enough tiles to fill
+// the chip without splitting the reduction.  Pooled and depthwise layers
+// and the output layer (which also writes every frame's dense output)
+// defer the updates to the update kernel.  With residual carry every layer
+// defers: a frame's keep decision (the row's largest magnitude over all its
+// channels) must be known before the next frame's delta of the same site is
+// formed, and the update kernel holds a site's channels in one group of
+// lanes.
+bool chunk_fused(const st_net* net, int i) {
+  const LayerPlan& L = net->layers[i];
+  return L.stateful && !L.pool && !L.dw && !L.se && !net->carry &&
+         i != (int)net->layers.size() - 1;
+}
+
+// list_pass: the consumers of a list compaction in a chunk (the pass that
+// cuts the run-aligned tiles of fused identity consumers).
+ConsList consumers_of(st_net* net, int t, bool list_pass = false) {
   const WS ws{net->ws};
   u64* cnt = ws.at<u64>(net->off_cnt);
   ConsList cl{};
@@ -98,6 +117,11 @@ ConsList consumers_of(st_net* net, int t) {
                      : ws.at<uint32_t>(net->tensors[j + 1].off_rowmax);
       c.cnt_O = cnt + L.cnt_O;
       c.pairs = cnt + L.cnt_pairs;
+      if (list_pass && net->last_nf > 1 && chunk_fused(net, j)) {
+        c.tstart = ws.at<uint32_t>(L.off_tstart);
+        c.nf = net->last_nf;
+        c.per = net->tensors[t].grid;
+      }
     } else if (cr.second == 0) {
       c.kind = kConsMark;
       c.flags = ws.at<uint8_t>(L.off_flags);
@@ -437,19 +461,12 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   u64* cpairs = cnt + L.cnt_pairs;
   uint32_t* rowmax_out = ws.at<uint32_t>(outT.off_rowmax);
   uint32_t* rm_O = L.pool ? nullptr : rowmax_out;
-  // Stateful layers whose every output row is finished by the GEMM tile
-  // that computes it apply the chunk's updates in the GEMM epilogue (rows
-  // come site-major, tiles are aligned to site runs).  Such a layer runs
-  // unsplit: a chunk holds several frames' rows, enough tiles to fill the
-  // chip without splitting the reduction.  Pooled and depthwise layers and
-  // the output layer (which also writes every frame's dense output) defer
-  // the updates to the update kernel.  With residual carry every layer
-  // defers: a frame's keep decision (the row's largest magnitude over all
-  // its channels) must be known before the next frame's delta of the same
-  // site is formed, and the update kernel holds a site's channels in one
-  // group of lanes.
-  const bool fused = L.stateful && !L.pool && !L.dw && !L.se && !out &&
-                     !net->carry;
+  const bool fused = chunk_fused(net, i);
+  // the fused GEMM's run-aligned row tiles: cut by the rulebook
+  // compaction, or (identity layers) by the list compaction of the layer
+  // that emitted the input, else by a pass of their own
+  uint32_t* tstart = fused ? ws.at<uint32_t>(L.off_tstart) : nullptr;
+  bool tiles_cut = fused && nf > 1 && L.ident && d.src >= 0;
 
   if (!L.ident) {
     FlagArgs fa{};
@@ -467,12 +484,14 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
     fa.cnt = cO;
     fa.nf = nf;
     fa.per = L.conv_grid;
+    if (fused && compact_runs_fit(citems, nf)) {
+      fa.tstart = tstart;
+      tiles_cut = true;
+    }
     launch_flag_compact(pf, ST_K_RB_COUNT, ST_K_RB_COMPACT, s, fa);
   }
-  uint32_t* tstart = ws.at<uint32_t>(net->off_chunk_tstart);
-  if (fused)
-    launch_run_tiles(pf, s, O, cO, citems, L.conv_grid, nf, tstart,
-                     cnt + L.cnt_sites);
+  if (fused && !tiles_cut)
+    launch_run_tiles(pf, s, O, cO, citems, L.conv_grid, nf, tstart);
 
   ConvArgs a{};
   a.p16 = net->bf16_state ? 1 : 0;
@@ -494,6 +513,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
     a.dout = ws.at<char>(outT.off_rows);
     a.rowmax = rowmax_out;
     a.tstart = tstart;
+    a.sites = cnt + L.cnt_sites;
     a.nf = nf;
     a.per = L.conv_grid;
   } else if (L.stateful) {
@@ -611,7 +631,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   la.map = ws.at<int>(outT.off_map);
   la.grp = grp;
   la.cnt_act = cnt + outT.cnt_act;
-  la.cons = consumers_of(net, i + 1);
+  la.cons = consumers_of(net, i + 1, true);
   launch_list_compact(pf, s, la);
   outT.last_thr = thr;
   return true;

@@ -96,6 +96,8 @@ struct LayerPlan {
   size_t off_yhat = 0;              // residual carry: f32 [out grid][cout_p]
   int cnt_sites = 0;                // chunk mode: sites whose state a fused
                                     // GEMM updated (site runs)
+  size_t off_tstart = 0;            // chunk mode: uint32 run-aligned GEMM
+                                    // row tiles (fused-state layers)
 };
 
 struct Recorder;  // executor-side profiling state
@@ -139,7 +141,6 @@ struct st_net {
   // the frames that updated it (bit mask)
   size_t off_chunk_dp = 0, off_chunk_base = 0, off_chunk_last = 0;
   size_t off_chunk_aff = 0;
-  size_t off_chunk_tstart = 0;      // uint32 run-aligned row tiles
   size_t off_cnt = 0;                      // uint64 [n_counters]
   size_t off_cleanup = 0;                  // cleanup descriptor table
   size_t off_dens = 0;                     // uint64 [batch] per-image counts

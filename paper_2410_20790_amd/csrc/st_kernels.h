@@ -53,8 +53,11 @@ struct Cons {
   uint8_t* flags;     // mark: the consumer's affected-output flags,
                       // site-major (site * nf + frame)
   Geo g;              // mark: the consumer's window geometry
-  int nf, nimg;       // mark: frames of the pass, images per frame
-  int64_t per;        // mark-same: sites per frame
+  int nf, nimg;       // mark / ident: frames of the pass, images per frame
+  int64_t per;        // mark-same / ident: sites per frame
+  // ident, chunk mode: the consumer's run-aligned GEMM row tiles (as
+  // launch_run_tiles writes them), cut by the list compaction, or NULL
+  uint32_t* tstart;
 };
 struct ConsList {
   Cons c[kMaxCons];
@@ -101,7 +104,12 @@ struct FlagArgs {
   // order).  nf <= 1: item order.
   int nf;
   int64_t per;
+  // chunk mode, or NULL: the emitted list's run-aligned GEMM row tiles (as
+  // launch_run_tiles writes them); the pass's tiles then hold whole sites,
+  // which needs compact_runs_fit(npix, nf)
+  uint32_t* tstart;
 };
+bool compact_runs_fit(int64_t cap, int run);
 void launch_flag_compact(const Prof& pf, int cls_count, int cls_write,
                          hipStream_t s, const FlagArgs& a);
 // flags: site-major (site * nf + frame) over nf frames of nimg images.
@@ -110,11 +118,10 @@ void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
                  int nimg, int nf);
 // Run-aligned row tiles of a site-major affected list O (chunk mode):
 // tstart[j] = first row of the run (same site) holding row j * step, for
-// j < ceil(nO / step), and tstart[ceil(nO / step)] = nO; the number of runs
-// (distinct sites) is added to sites[0 .. kSiteSlots) (partial counts).
+// j < ceil(nO / step), and tstart[ceil(nO / step)] = nO.
 void launch_run_tiles(const Prof& pf, hipStream_t s, const int* O,
                       const u64* nO, int64_t capO, int64_t per, int nf,
-                      uint32_t* tstart, u64* sites);
+                      uint32_t* tstart);
 
 // ---- (c)+(d) delta convolution with the fused state update / emission
 struct ConvArgs {
@@ -151,8 +158,11 @@ struct ConvArgs {
   // are f(P_new) - view instead of f(P_new) - f(P_old)
   const float* yhat;
   // kModeChunkState: row tile j is [tstart[j], tstart[j + 1]) (tiles step
-  // chunk_tile_step(nf) rows); a row's site is its item modulo `per`
+  // chunk_tile_step(nf) rows); a row's site is its item modulo `per`; the
+  // number of runs (distinct sites) is added to sites[0 .. kSiteSlots)
+  // (partial counts)
   const uint32_t* tstart;
+  u64* sites;
   int nf;
   int64_t per;
   // frozen squeeze-excitation: per-image gates [N][cout_p] scaling both

@@ -110,9 +110,9 @@ __device__ __forceinline__ int64_t read_count(const u64* dev, int64_t host) {
 
 // ============================================================ compaction
 // Ascending stream compaction.  Items are split into tiles of `tile`
-// consecutive indices (a multiple of 256).  The write pass derives each
-// tile's output offset from per-tile or per-64-item-group counts of the
-// items before it -- counted by a separate pass, or by the kernel that
+// consecutive indices (at most 256 * kMaxItemsPerThread).  The write pass
+// derives each tile's output offset from per-tile or per-64-item-group
+// counts of the items before it -- counted by a separate pass, or by the kernel that
 // produced the items -- and writes the kept items in order, using a wave
 // ballot and mbcnt for the in-wave prefix and LDS for the cross-wave prefix.
 // The block that owns the last item writes the total.
@@ -160,8 +160,8 @@ __device__ __forceinline__ unsigned block_exclusive_scan(unsigned v,
 }
 
 // cnts: `per_tile` counts per tile (1 = per-tile counts, tile/64 = counts of
-// 64-item groups).  Each thread owns `tile / 256` consecutive items of the
-// tile and evaluates them; one block scan gives every kept item its
+// 64-item groups).  Each thread owns ceil(tile / 256) consecutive items of
+// the tile and evaluates them; one block scan gives every kept item its
 // position.  The predicate's item data (P::Item, from P::load) and the
 // first 256 counts before the tile are requested together with the item
 // count -- all loads stay within the capacity `cap` and the count buffer,
@@ -178,6 +178,16 @@ __device__ __forceinline__ unsigned block_exclusive_scan(unsigned v,
 // to pred.block_done; pred.finish receives the total.
 constexpr int kMaxItemsPerThread = 32;
 
+// Predicates with P::kRanked cut run-aligned row tiles while they emit: the
+// items form runs of pred.run_len() consecutive indices (a chunk's frames of
+// one site), the pass's tiles hold whole runs, and where pred.rank_needed
+// asks for it the write pass hands pred.emit_ranked the number of kept
+// items of the same run before the item.
+template <class P, class = void>
+struct IsRanked : std::false_type {};
+template <class P>
+struct IsRanked<P, std::void_t<decltype(P::kRanked)>> : std::true_type {};
+
 template <class P, int IPT>
 __global__ __launch_bounds__(256) void k_compact_write(
     const u64* n_dev, int64_t n_host, int64_t cap, int tile,
@@ -191,7 +201,7 @@ __global__ __launch_bounds__(256) void k_compact_write(
   // the first 256 counts before the tile are requested with the count
   const unsigned nprev = blockIdx.x * (unsigned)per_tile;
   unsigned off = threadIdx.x < nprev ? cnts[threadIdx.x] : 0u;
-  const int ipt = IPT > 0 ? IPT : tile / 256;
+  const int ipt = IPT > 0 ? IPT : (tile + 255) / 256;
   const int64_t first = base + (int64_t)threadIdx.x * ipt;
   Item it[IPT > 0 ? IPT : 1];
   if constexpr (IPT > 0) {
@@ -249,7 +259,18 @@ __global__ __launch_bounds__(256) void k_compact_write(
   unsigned work = 0;
   for (unsigned k = threadIdx.x; k < tile_total; k += 256) {
     const int64_t i = base + kept[k];
-    work += pred.emit(i, off + k, pred.load(i));
+    if constexpr (IsRanked<P>::value) {
+      const unsigned pos = off + k;
+      unsigned rank = 0;
+      if (pred.rank_needed(pos)) {
+        // tiles start on run boundaries, so tile offsets group like items
+        const unsigned R = pred.run_len(), g = kept[k] / R;
+        while (rank < k && kept[k - 1 - rank] / R == g) ++rank;
+      }
+      work += pred.emit_ranked(i, pos, pred.load(i), rank);
+    } else {
+      work += pred.emit(i, off + k, pred.load(i));
+    }
   }
   work = block_sum(work);
   if (threadIdx.x == 0) {
@@ -268,7 +289,7 @@ static void launch_compact_write(hipStream_t s, int nt, const u64* n_dev,
                                  int64_t n_host, int64_t cap, int tile,
                                  const uint32_t* cnts, int per_tile,
                                  u64* out_cnt, u64* out_cnt2, const P& pred) {
-  if (tile == 512)
+  if ((tile + 255) / 256 == 2)
     k_compact_write<P, 2><<<nt, 256, 0, s>>>(n_dev, n_host, cap, tile, cnts,
                                              per_tile, out_cnt, out_cnt2,
                                              pred);
@@ -280,17 +301,30 @@ static void launch_compact_write(hipStream_t s, int nt, const u64* n_dev,
 
 // Tile of a compaction pass: a multiple of 256 items, at least 512, with at
 // most kMaxTiles tiles (the tile-count buffer) and at most 32 items per
-// thread (the keep bitmask of k_compact_write).
-static int compact_tile(int64_t cap) {
+// thread (the keep bitmask of k_compact_write).  run > 1: a multiple of run
+// instead (whole runs per tile), which may take one item per thread more
+// than k_compact_write holds (compact_runs_fit).
+static int64_t compact_tile(int64_t cap, int run = 0) {
   int64_t t = (cap + 4095) / 4096;
   t = (t + 255) / 256 * 256;
-  return (int)(t < 512 ? 512 : t);
+  if (t < 512) t = 512;
+  if (run > 1) {
+    // the largest multiple of run not above t, unless that takes more
+    // than 4096 tiles
+    const int64_t d = t - t % run;
+    t = (cap + d - 1) / d <= 4096 ? d : d + run;
+  }
+  return t;
 }
 
-static int compact_tiles(int64_t cap) {
-  const int tile = compact_tile(cap);
+static int compact_tiles(int64_t cap, int run = 0) {
+  const int64_t tile = compact_tile(cap, run);
   const int nt = (int)((cap + tile - 1) / tile);
   return nt < 1 ? 1 : nt;
+}
+
+bool compact_runs_fit(int64_t cap, int run) {
+  return compact_tile(cap, run) <= 256 * kMaxItemsPerThread;
 }
 
 // Counting pass + write pass.
@@ -298,9 +332,9 @@ template <class P>
 static void run_compact(const Prof& pf, int cls_count, int cls_write,
                         hipStream_t s, const u64* n_dev, int64_t n_host,
                         int64_t cap, uint32_t* tiles, u64* out_cnt,
-                        u64* out_cnt2, P pred) {
-  const int tile = compact_tile(cap);
-  const int nt = compact_tiles(cap);
+                        u64* out_cnt2, P pred, int run = 0) {
+  const int tile = (int)compact_tile(cap, run);
+  const int nt = compact_tiles(cap, run);
   prof_begin(pf, cls_count, s);
   k_compact_count<P><<<nt, 256, 0, s>>>(n_dev, n_host, tile, tiles, pred);
   prof_end(pf, cls_count, s);
@@ -368,6 +402,10 @@ __device__ __forceinline__ void cons_finish(const ConsList& cl,
     if (cl.c[i].kind == kConsIdent) {
       *cl.c[i].cnt_O = total;
       *cl.c[i].pairs = total;
+      if (cl.c[i].tstart) {
+        const unsigned step = (unsigned)chunk_tile_step(cl.c[i].nf);
+        cl.c[i].tstart[(total + step - 1) / step] = total;
+      }
     }
 }
 
@@ -473,42 +511,35 @@ void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
 }
 
 // Run-aligned row tiles (chunk mode): the run holding row x starts at most
-// nf - 1 rows earlier; the nf - 1 preceding entries are loaded at once and
-// the run is the unbroken stretch of the same site ending at x.  Also
-// counts the runs (distinct sites) into *sites.
+// nf - 1 rows earlier; the nf - 1 preceding entries are requested together
+// (one round trip) and the run is the unbroken stretch of the same site
+// ending at x.
 __global__ __launch_bounds__(256) void k_run_tiles(const int* O,
                                                    const u64* nOp,
                                                    int64_t per, int nf,
-                                                   uint32_t* tstart,
-                                                   u64* sites) {
+                                                   uint32_t* tstart) {
+  constexpr int kMaxBack = 31;  // nf <= 32
   const int64_t nO = (int64_t)*nOp;
   const int step = chunk_tile_step(nf);
   const int64_t nt = (nO + step - 1) / step;
   const unsigned pu = (unsigned)per;
-  unsigned runs = 0;
-  for (int64_t base = (int64_t)blockIdx.x * 256; base < nO;
-       base += (int64_t)gridDim.x * 256) {
-    const int64_t r = base + threadIdx.x;
-    const bool first =
-        r < nO && (r == 0 || (unsigned)O[r] % pu != (unsigned)O[r - 1] % pu);
-    runs += __popcll(__ballot(first));
-  }
-  // one device atomic per block (every wave's lane 0 holds its count)
-  runs = block_sum((threadIdx.x & 63) == 0 ? runs : 0u);
-  if (threadIdx.x == 0 && runs)
-    atomicAdd(sites + blockIdx.x % kSiteSlots, (u64)runs);
   for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j <= nt;
        j += (int64_t)gridDim.x * 256) {
     int64_t r = nO;
     if (j < nt) {
       const int64_t x = j * step;
-      const unsigned site = (unsigned)O[x] % pu;
+      // rows x - q for q < nb; past that the address is clamped (the loads
+      // stay unconditional) and the value ignored
+      const int nb = (int)min((int64_t)nf, x + 1);
+      int v[kMaxBack + 1];
+#pragma unroll
+      for (int q = 0; q <= kMaxBack; ++q) v[q] = O[x - min(q, nb - 1)];
+      const unsigned site = (unsigned)v[0] % pu;
       int len = 1;
       bool alive = true;
-      for (int q = 1; q < nf; ++q) {
-        const int64_t y = x - q;
-        const bool same = y >= 0 && (unsigned)O[y < 0 ? 0 : y] % pu == site;
-        alive = alive && same;
+#pragma unroll
+      for (int q = 1; q <= kMaxBack; ++q) {
+        alive = alive && q < nb && (unsigned)v[q] % pu == site;
         len += alive ? 1 : 0;
       }
       r = x - len + 1;
@@ -519,10 +550,10 @@ __global__ __launch_bounds__(256) void k_run_tiles(const int* O,
 
 void launch_run_tiles(const Prof& pf, hipStream_t s, const int* O,
                       const u64* nO, int64_t capO, int64_t per, int nf,
-                      uint32_t* tstart, u64* sites) {
+                      uint32_t* tstart) {
   prof_begin(pf, 24 /*ST_K_RUN_TILES*/, s);
-  k_run_tiles<<<grid_for(capO, 512), 256, 0, s>>>(O, nO, per, nf, tstart,
-                                                   sites);
+  k_run_tiles<<<grid_for(capO / chunk_tile_step(nf) + 1, 512), 256, 0, s>>>(
+      O, nO, per, nf, tstart);
   prof_end(pf, 24, s);
 }
 
@@ -553,9 +584,23 @@ struct FlagPred {
   u64* pairs;
   int nf;
   int64_t per;
+  uint32_t* tstart;  // run-aligned row tiles of the emitted list, or NULL
+  static constexpr bool kRanked = true;
   struct Item {
     uint8_t f;
   };
+  // a run: one site's nf frames (items site * nf + frame)
+  __device__ unsigned run_len() const { return (unsigned)nf; }
+  __device__ bool rank_needed(unsigned pos) const {
+    return tstart && pos % (unsigned)chunk_tile_step(nf) == 0u;
+  }
+  // tile pos / step starts where the run holding row pos starts
+  __device__ unsigned emit_ranked(int64_t j, unsigned pos, const Item& it,
+                                  unsigned rank) const {
+    if (rank_needed(pos))
+      tstart[pos / (unsigned)chunk_tile_step(nf)] = pos - rank;
+    return emit(j, pos, it);
+  }
   // the flags are site-major: item j's flag is flags[j]
   __device__ bool count(int64_t j) const { return flags[j] != 0; }
   __device__ Item load(int64_t j) const { return Item{flags[j]}; }
@@ -600,15 +645,19 @@ struct FlagPred {
   __device__ void block_done(unsigned w) const {
     if (pairs && w) atomicAdd(pairs, (u64)w);
   }
-  __device__ void finish(unsigned) const {}
+  __device__ void finish(unsigned total) const {
+    if (!tstart) return;
+    const unsigned step = (unsigned)chunk_tile_step(nf);
+    tstart[(total + step - 1) / step] = total;
+  }
 };
 
 void launch_flag_compact(const Prof& pf, int cls_count, int cls_write,
                          hipStream_t s, const FlagArgs& a) {
   FlagPred p{a.flags, a.list, a.map, a.rowmax, a.nbr, a.map_in, a.stride,
-             a.g, a.pairs, a.nf, a.per};
+             a.g, a.pairs, a.nf, a.per, a.tstart};
   run_compact(pf, cls_count, cls_write, s, nullptr, a.npix, a.npix, a.tiles,
-              a.cnt, nullptr, p);
+              a.cnt, nullptr, p, a.tstart ? a.nf : 0);
 }
 
 // Per-64-row kept counts of an emitted tensor (rows whose max |delta|
@@ -1081,6 +1130,9 @@ __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
     if (lane == 0) {
       s_run[nr] = rows;
       s_run[BM + 1] = nr;
+      // every run lies in one row tile: its first column tile counts it
+      if (n0 == 0 && nr)
+        atomicAdd(a.sites + blockIdx.x % kSiteSlots, (u64)nr);
     }
   }
   __syncthreads();
@@ -1579,7 +1631,8 @@ bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
   // run-aligned tiles belong to the chunk-state epilogue, which finishes
   // whole tiles itself (no split)
   if ((a.tstart != nullptr) != (a.mode == kModeChunkState)) return false;
-  if (a.tstart && (a.split_max > 1 || a.nf < 1 || a.nf > 32 || a.per < 1))
+  if (a.tstart && (a.split_max > 1 || a.nf < 1 || a.nf > 32 || a.per < 1 ||
+                   !a.sites))
     return false;
   const int rstep = a.tstart ? chunk_tile_step(a.nf) : kGemmBM;
   const int64_t worst = ((a.capO + rstep - 1) / rstep) *
@@ -1846,6 +1899,24 @@ struct ListPred {
   __device__ unsigned emit(int64_t r, unsigned pos, const Item& it) const {
     act[pos] = it.pix;
     cons_emit(cons, it.pix, pos, (int)r);
+    // an identity consumer's affected list is this list: where its GEMM
+    // tile starts (pos a multiple of the tile step), the tile is moved back
+    // to the start of the site's run.  The rows of a site are adjacent
+    // (the list is site-major); the kept ones among the rows before r give
+    // the rank.  rowmax and rowpix are not written by this pass.
+    for (int i = 0; i < cons.n; ++i) {
+      const Cons& c = cons.c[i];
+      if (c.kind != kConsIdent || !c.tstart) continue;
+      const unsigned step = (unsigned)chunk_tile_step(c.nf);
+      if (pos % step) continue;
+      const unsigned pu = (unsigned)c.per, site = (unsigned)it.pix % pu;
+      unsigned rank = 0;
+      for (int q = 1; q < c.nf && r - q >= 0; ++q) {
+        if ((unsigned)rowpix[r - q] % pu != site) break;
+        rank += __uint_as_float(rowmax[r - q]) > th() ? 1u : 0u;
+      }
+      c.tstart[pos / step] = pos - rank;
+    }
     return 0u;
   }
   __device__ void drop(int64_t, const Item& it) const { map[it.pix] = -1; }
@@ -1855,7 +1926,7 @@ struct ListPred {
 
 void launch_list_compact(const Prof& pf, hipStream_t s, const ListArgs& a) {
   ListPred p{a.rowmax, a.rowpix, a.act, a.map, a.thr, a.thr_dev, a.cons};
-  const int tile = compact_tile(a.cap);
+  const int tile = (int)compact_tile(a.cap);
   const int nt = compact_tiles(a.cap);
   prof_begin(pf, 15 /*ST_K_LIST_COMPACT*/, s);
   launch_compact_write(s, nt, a.n_rows, 0, a.cap, tile, a.grp, tile / 64,

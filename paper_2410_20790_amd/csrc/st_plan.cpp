@@ -277,6 +277,9 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
                                       : 0);
     }
     if (!L.ident) L.off_flags = a.take(round_up(citems, 16));
+    if (F > 1 && L.stateful && !L.pool && !L.dw && !L.se)
+      L.off_tstart = a.take(sizeof(uint32_t) *
+                            (citems / chunk_tile_step(F) + 2));
     if (L.pool) L.off_pflags = a.take(round_up(T.grid * F, 16));
     if (L.se) {
       const int64_t hw = (int64_t)L.Ho * L.Wo;
@@ -304,8 +307,6 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
     net->off_chunk_base = a.take(round_up(t0.grid * F, 16));
     net->off_chunk_last = a.take(round_up(t0.grid, 16));
     net->off_chunk_aff = a.take(sizeof(uint32_t) * max_conv_phys);
-    net->off_chunk_tstart = a.take(
-        sizeof(uint32_t) * (max_conv_phys * F / chunk_tile_step(F) + 2));
   }
   net->off_grp = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
   net->off_mdone = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
