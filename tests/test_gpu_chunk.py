@@ -125,6 +125,33 @@ def test_chunk_depthwise():
                "depthwise")
 
 
+def pointwise_first_net(seed=1031):
+    """1x1 stride-1 layers first: one fed by the frame delta, one fed by a
+    layer's kept rows (the two ways a 1x1 layer's list is formed in a
+    chunk), then a 3x3 layer and a 1x1 output layer."""
+    from workloads.nets import ACT_NONE, ACT_RELU, LayerSpec, NetSpec
+    rng = np.random.default_rng(seed)
+
+    def conv(src, cin, cout, k, act):
+        L = LayerSpec(src=src, c_in=cin, c_out=cout, k=(k, k), s=(1, 1),
+                      p=(k // 2, k // 2), act=act)
+        L.weight = rng.normal(0.0, 0.15, (cout, cin, k, k)).astype(np.float32)
+        L.bias = rng.normal(0.0, 0.1, (cout,)).astype(np.float32)
+        return L
+    layers = [conv(-1, 16, 32, 1, ACT_RELU), conv(0, 32, 32, 1, ACT_RELU),
+              conv(1, 32, 16, 3, ACT_RELU), conv(2, 16, 8, 1, ACT_NONE)]
+    return NetSpec("pointwise_first", layers, 1, 64, 64, 16, "f32")
+
+
+@pytest.mark.parametrize("thr", [0.0, 0.05])
+def test_chunk_pointwise_layers(thr):
+    """Row tiles of the fused 1x1 layers: cut by a pass of their own (fed
+    by the frame delta) and by the producer's list compaction; chunks of
+    4, 4 and 1 frames."""
+    run_chunks(pointwise_first_net(), toy_video(seed=21, n_frames=10), thr,
+               4, f"pointwise thr={thr}")
+
+
 def test_chunk_single_frame_and_batch():
     """A batch of two images (items are frames x images), and a last chunk
     of one frame."""
