@@ -1068,22 +1068,34 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
   // the frames of the run, with the activation fixed at compile time
   auto frames = [&](auto act_tag) {
     constexpr int ACT = decltype(act_tag)::value;
+    // four columns at a time; the delta stores take eight (16 bytes) where
+    // the thread owns at least eight (the padded width is a multiple of 8)
+    constexpr int SV = Q % 2 == 0 ? 8 : 4;
     for (int r = r0; r < r1; ++r) {
       float rm = 0.f;
 #pragma unroll
-      for (int q = 0; q < Q; ++q) {
-        if (c0 + 4 * q >= cout_p) continue;
-        const float4 u = *(const float4*)(Cs + r * cld + (c0 - n0) + 4 * q);
-        const float uv[4] = {u.x, u.y, u.z, u.w};
-        float d[4];
+      for (int q2 = 0; q2 < CPT / SV; ++q2) {
+        if (c0 + SV * q2 >= cout_p) continue;
+        float d[SV];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float po = P[4 * q + e];
-          const float pn = state_round(a.p16, po + uv[e]);
-          d[e] = act_c<ACT>(pn) - act_c<ACT>(po);
-          P[4 * q + e] = pn;
+        for (int h = 0; h < SV / 4; ++h) {
+          const int q = (SV / 4) * q2 + h;
+          const float4 u =
+              *(const float4*)(Cs + r * cld + (c0 - n0) + 4 * q);
+          const float uv[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float po = P[4 * q + e];
+            const float pn = state_round(a.p16, po + uv[e]);
+            d[4 * h + e] = act_c<ACT>(pn) - act_c<ACT>(po);
+            P[4 * q + e] = pn;
+          }
         }
-        rm = fmaxf(rm, store4<T>(dout + (m0 + r) * cout_p + c0 + 4 * q, d));
+        T* dst = dout + (m0 + r) * cout_p + c0 + SV * q2;
+        if constexpr (SV == 8)
+          rm = fmaxf(rm, Vec8<T>::store(dst, d));
+        else
+          rm = fmaxf(rm, store4<T>(dst, d));
       }
       if (rm > 0.f) atomicMax(s_rmax + r, __float_as_uint(rm));
     }
