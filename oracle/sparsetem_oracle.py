@@ -379,91 +379,24 @@ class OracleNet:
         for i, L in enumerate(self.layers):
             g = self.geo[i]
             src = tensors[L.src + 1]
-            R = rulebook(src["pix"], (g.Hi, g.Wi), (g.Ho, g.Wo), L.k, L.s,
-                         L.p)
-            affected = [R[:, 2]]
-            skip = None
-            if L.residual_src != -2:
-                skip = tensors[L.residual_src + 1]
-                affected.append(skip["pix"])
-            O = np.unique(np.concatenate(affected)).astype(np.int64)
-            # Linear part: dP[o] = sum over rulebook pairs of W_k . delta[i]
-            # (Eq. 2, no bias), accumulated in fp64.
-            dP = np.zeros((len(O), L.c_out))
-            w = np.asarray(L.weight, dtype=np.float64)
-            for k in range(L.k[0] * L.k[1]):
-                sel = R[:, 0] == k
-                if not sel.any():
-                    continue
-                ri = np.searchsorted(src["pix"], R[sel, 1])
-                ro = np.searchsorted(O, R[sel, 2])
-                dP[ro] += _apply_offset(src["rows"][ri], w, k // L.k[1],
-                                        k % L.k[1], L.groups)
-            if skip is not None and len(skip["pix"]):
-                dP[np.searchsorted(O, skip["pix"])] += skip["rows"]
-            dP32 = f32(dP)
-
-            Q = None
+            skip = (tensors[L.residual_src + 1] if L.residual_src != -2
+                    else None)
             if self.carry:
+                R, O, dP32 = self._linear(
+                    i, src["pix"], src["rows"],
+                    None if skip is None else skip["pix"],
+                    None if skip is None else skip["rows"])
                 d32, cand, Q = self._carry_delta(i, O, dP32)
-            elif self.stateful[i]:
-                # Non-linear handling: reconstruct the dense pre-activation
-                # (Accumulation onto the cached P) and re-sparsify after f.
-                Pg = self.P[i].reshape(N * g.Ho * g.Wo, L.c_out)
-                P_old = Pg[O].copy()
-                P_new = f32(P_old.astype(np.float64) + dP32)
-                if self.state_dtype == "bf16":
-                    P_new = f32(round_storage(P_new, "bf16"))
-                if L.se_mid and self.frozen_se:
-                    # frozen gates: a per-image, per-channel scale
-                    Pg[O] = P_new
-                    s = self.S[i].reshape(N, L.c_out)[O // (g.Ho * g.Wo)]
-                    d32 = f32(f32(activation(P_new, L.act).astype(np.float64)
-                                  * s)
-                              - f32(activation(P_old, L.act).astype(np.float64)
-                                    * s))
-                    cand = O
-                elif L.se_mid:
-                    # Squeeze-excitation (reading 6): the gates follow the
-                    # dense activation, so every site's output moves:
-                    # delta = f(P_new) * s_new - f(P_old) * s_old.
-                    a_old = activation(Pg.reshape(N, g.Ho, g.Wo, L.c_out),
-                                       L.act)
-                    Pg[O] = P_new
-                    a_new = activation(Pg.reshape(N, g.Ho, g.Wo, L.c_out),
-                                       L.act)
-                    s_new = se_gates(a_new, L)
-                    e_old = se_apply(a_old, self.S[i]).reshape(-1, L.c_out)
-                    e_new = se_apply(a_new, s_new).reshape(-1, L.c_out)
-                    self.S[i] = s_new
-                    d32 = f32(e_new.astype(np.float64)
-                              - e_old.astype(np.float64))
-                    cand = np.arange(N * g.Ho * g.Wo, dtype=np.int64)
-                elif g.pool:
-                    T = window_targets(O, (g.Ho, g.Wo), (g.Hp, g.Wp),
-                                       L.pool_k, L.pool_s, L.pool_p)
-                    Q = np.unique(T[:, 2]).astype(np.int64)
-                    e_old = maxpool_nhwc(activation(
-                        Pg.reshape(N, g.Ho, g.Wo, L.c_out), L.act),
-                        L.pool_k, L.pool_s, L.pool_p)
-                    Pg[O] = P_new
-                    e_new = maxpool_nhwc(activation(
-                        Pg.reshape(N, g.Ho, g.Wo, L.c_out), L.act),
-                        L.pool_k, L.pool_s, L.pool_p)
-                    e_old = e_old.reshape(-1, L.c_out)[Q]
-                    e_new = e_new.reshape(-1, L.c_out)[Q]
-                    d32 = f32(f32(e_new).astype(np.float64)
-                              - f32(e_old).astype(np.float64))
-                    cand = Q
-                else:
-                    Pg[O] = P_new
-                    d32 = f32(activation(P_new, L.act).astype(np.float64)
-                              - activation(P_old, L.act).astype(np.float64))
-                    cand = O
+                d = round_storage(d32, self.dtype)
             else:
-                d32 = dP32
-                cand = O
-            d = round_storage(d32, self.dtype)
+                st = self._step(i, src["pix"], src["rows"],
+                                None if skip is None else skip["pix"],
+                                None if skip is None else skip["rows"],
+                                self.P.get(i), self.S.get(i))
+                R, O, Q, cand, d = (st["rulebook"], st["O"], st["Q"],
+                                    st["cand"], st["cand_rows"])
+                if L.se_mid and not self.frozen_se:
+                    self.S[i] = st["S"]
             cmax = np.abs(d).max(axis=1) if len(cand) else np.zeros(0)
             kept = cmax > thr[i + 1]                     # readings 1 and 3
             if self.carry:
@@ -481,6 +414,126 @@ class OracleNet:
         self.last = dict(kind="diff", out=out, tensors=tensors,
                          layers=layer_art, thr=thr)
         return out
+
+    def _linear(self, i, pix, rows, skip_pix=None, skip_rows=None):
+        """Linear part of layer i on its input's kept rows (pixel ids `pix`,
+        ascending, values `rows`) and its residual input's (or None):
+        the rulebook, the affected output sites O (the rulebook's outputs
+        and the residual's kept sites, ascending) and
+        dP[o] = sum over rulebook pairs of W_k . delta[i] (+ the residual
+        delta), Eq. 2 without bias, accumulated in fp64 and rounded once to
+        f32.  Returns (rulebook, O, dP32)."""
+        L, g = self.layers[i], self.geo[i]
+        R = rulebook(pix, (g.Hi, g.Wi), (g.Ho, g.Wo), L.k, L.s, L.p)
+        affected = [R[:, 2]]
+        if skip_pix is not None:
+            affected.append(np.asarray(skip_pix, np.int64))
+        O = np.unique(np.concatenate(affected)).astype(np.int64)
+        dP = np.zeros((len(O), L.c_out))
+        w = np.asarray(L.weight, dtype=np.float64)
+        for k in range(L.k[0] * L.k[1]):
+            sel = R[:, 0] == k
+            if not sel.any():
+                continue
+            ri = np.searchsorted(pix, R[sel, 1])
+            ro = np.searchsorted(O, R[sel, 2])
+            dP[ro] += _apply_offset(np.asarray(rows)[ri], w, k // L.k[1],
+                                    k % L.k[1], L.groups)
+        if skip_pix is not None and len(skip_pix):
+            dP[np.searchsorted(O, skip_pix)] += skip_rows
+        return R, O, f32(dP)
+
+    def _step(self, i, pix, rows, skip_pix, skip_rows, P, S):
+        """Layer i of Diff Computation (no residual carry) on the given
+        inputs: the linear part (_linear), then, for a layer that holds a
+        cached pre-activation, Accumulation onto P (the dense f32 state
+        [N, Ho, Wo, C], updated in place) and the non-linear handling of
+        Eq. 3 -- reconstruct the dense value before f, re-sparsify after it
+        (pooled: max_window f(P_new) - max_window f(P_old); squeeze-
+        excitation: f(P_new) * s_new - f(P_old) * s_old with the gates S of
+        the previous frame, or the frozen gates) -- else the linear delta
+        passes on.  Returns the rulebook, O, the pooled candidates Q (or
+        None), the candidate sites and their deltas rounded to the storage
+        dtype (before truncation), and the new gates S."""
+        L, g = self.layers[i], self.geo[i]
+        N = self.in_shape[0]
+        R, O, dP32 = self._linear(i, pix, rows, skip_pix, skip_rows)
+        Q = None
+        S_new = S
+        if self.stateful[i]:
+            Pg = P.reshape(N * g.Ho * g.Wo, L.c_out)
+            P_old = Pg[O].copy()
+            P_new = f32(P_old.astype(np.float64) + dP32)
+            if self.state_dtype == "bf16":
+                P_new = f32(round_storage(P_new, "bf16"))
+            if L.se_mid and self.frozen_se:
+                # frozen gates: a per-image, per-channel scale
+                Pg[O] = P_new
+                s = S.reshape(N, L.c_out)[O // (g.Ho * g.Wo)]
+                d32 = f32(f32(activation(P_new, L.act).astype(np.float64)
+                              * s)
+                          - f32(activation(P_old, L.act).astype(np.float64)
+                                * s))
+                cand = O
+            elif L.se_mid:
+                # Squeeze-excitation (reading 6): the gates follow the
+                # dense activation, so every site's output moves:
+                # delta = f(P_new) * s_new - f(P_old) * s_old.
+                a_old = activation(Pg.reshape(N, g.Ho, g.Wo, L.c_out), L.act)
+                Pg[O] = P_new
+                a_new = activation(Pg.reshape(N, g.Ho, g.Wo, L.c_out), L.act)
+                S_new = se_gates(a_new, L)
+                e_old = se_apply(a_old, S).reshape(-1, L.c_out)
+                e_new = se_apply(a_new, S_new).reshape(-1, L.c_out)
+                d32 = f32(e_new.astype(np.float64)
+                          - e_old.astype(np.float64))
+                cand = np.arange(N * g.Ho * g.Wo, dtype=np.int64)
+            elif g.pool:
+                T = window_targets(O, (g.Ho, g.Wo), (g.Hp, g.Wp),
+                                   L.pool_k, L.pool_s, L.pool_p)
+                Q = np.unique(T[:, 2]).astype(np.int64)
+                e_old = maxpool_nhwc(activation(
+                    Pg.reshape(N, g.Ho, g.Wo, L.c_out), L.act),
+                    L.pool_k, L.pool_s, L.pool_p)
+                Pg[O] = P_new
+                e_new = maxpool_nhwc(activation(
+                    Pg.reshape(N, g.Ho, g.Wo, L.c_out), L.act),
+                    L.pool_k, L.pool_s, L.pool_p)
+                e_old = e_old.reshape(-1, L.c_out)[Q]
+                e_new = e_new.reshape(-1, L.c_out)[Q]
+                d32 = f32(f32(e_new).astype(np.float64)
+                          - f32(e_old).astype(np.float64))
+                cand = Q
+            else:
+                Pg[O] = P_new
+                d32 = f32(activation(P_new, L.act).astype(np.float64)
+                          - activation(P_old, L.act).astype(np.float64))
+                cand = O
+        else:
+            d32 = dP32
+            cand = O
+        return dict(rulebook=R, O=O, Q=Q, cand=cand,
+                    cand_rows=round_storage(d32, self.dtype), S=S_new)
+
+    def layer_step(self, i, pix, rows, skip_pix=None, skip_rows=None,
+                   P_old=None, S_old=None):
+        """One layer of Diff Computation on inputs supplied by the caller,
+        leaving the net untouched (a teacher-forced step): the kept rows of
+        the layer's input and residual input, the cached pre-activation
+        before the frame (dense f32 [N, Ho, Wo, C]; None for a layer
+        without one) and the previous frame's squeeze-excitation gates.
+        Returns _step's artefacts plus the updated dense state "P"."""
+        if self.carry:
+            raise ValueError("layer_step follows the drop semantics")
+        P = None if P_old is None else f32(P_old).copy()
+        st = self._step(i, np.asarray(pix, np.int64),
+                        np.asarray(rows, np.float64),
+                        None if skip_pix is None else
+                        np.asarray(skip_pix, np.int64),
+                        None if skip_rows is None else
+                        np.asarray(skip_rows, np.float64), P, S_old)
+        st["P"] = P
+        return st
 
     def _carry_delta(self, i, O, dP32):
         """Residual carry: apply the update to P (every layer keeps P) and

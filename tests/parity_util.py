@@ -2,8 +2,8 @@
 
 Tolerances (per tensor, relative to the oracle's largest magnitude):
 1e-4 for f32 nets, 2e-2 for f16/bf16 nets; half-precision deltas of stateful
-layers are bounded through the state they are differences of (see
-compare_frame).  Masks, active lists and
+layers are compared layer by layer on identical inputs instead (see
+compare_frame and test_gpu_teacher.py).  Masks, active lists and
 rulebooks are compared exactly; where a row's keep decision depends on
 floating point that the two sides round differently (its max |delta| lies
 within a band around the threshold) it is reported and allowed.
@@ -93,19 +93,20 @@ def compare_frame(net, o, g, out_g, tag, check_rulebook=True, tol_dtype=None):
         if exact_inputs:
             np.testing.assert_array_equal(
                 pix_g, T["cand"], err_msg=f"{tag}: candidates of tensor {t}")
-        # candidate delta values (before truncation)
-        if exact_inputs and len(T["cand"]):
+        # candidate delta values (before truncation), at the feature-map
+        # tolerance relative to the tensor's largest delta.  Half-precision
+        # deltas of stateful layers are the exception: a delta
+        # f(P_new) - f(P_old) is small next to the state, and in a deep
+        # half-precision chain the two sides' re-rounding of every emitted
+        # activation moves their states apart by up to ~1% of the state's
+        # scale, far more than the delta's own 2e-2.  Those deltas are
+        # compared layer by layer on identical inputs instead
+        # (test_gpu_teacher.py, at one storage ulp); here the state they are
+        # differences of is compared at 2e-2.
+        half_state = dt != "f32" and (t - 1) in o.P
+        if exact_inputs and len(T["cand"]) and not half_state:
             err = float(np.abs(rows_g - T["cand_rows"]).max())
             bound = rtol * float(np.abs(T["cand_rows"]).max())
-            if dt != "f32" and (t - 1) in o.P:
-                # A stateful layer emits f(P_new) - f(P_old) with f
-                # 1-Lipschitz, so its error is at most the sum of the errors
-                # of the two states; both meet the state tolerance, hence
-                # |delta error| <= 2 * rtol * max|P|.  (In a deep half
-                # precision chain the deltas are small next to the state and
-                # the two sides' re-rounding of every activation makes the
-                # states drift apart by up to ~1%.)
-                bound = max(bound, 2 * rtol * float(np.abs(o.P[t - 1]).max()))
             assert err <= bound, (f"{tag}: delta rows of tensor {t}: "
                                   f"{err} > {bound}")
         # kept sets: exact except band rows

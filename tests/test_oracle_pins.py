@@ -533,3 +533,53 @@ def test_planted_mistake_frozen_se_gates_is_caught(monkeypatch):
                         lambda a, L: frozen[net.layers.index(L)])
     out = o.encode_diff(frames[1], [0.0] * (len(net.layers) + 1))
     assert rel_err(out, dense) > 1e-4
+
+
+# ------------------------------------------------ algorithmic FLOP count
+
+def _single_conv(cin, cout, groups, H, W, k=(3, 3), p=(1, 1)):
+    rng = np.random.default_rng(11)
+    L = LayerSpec(src=-1, c_in=cin, c_out=cout, k=k, s=(1, 1), p=p,
+                  groups=groups, act=ACT_RELU)
+    L.weight = rng.standard_normal((cout, cin // groups, *k)).astype(
+        np.float32)
+    L.bias = np.zeros(cout, np.float32)
+    return L
+
+
+@pytest.mark.parametrize("cin,cout,groups", [(4, 6, 1), (8, 8, 8)])
+@pytest.mark.parametrize("y,x,taps", [(3, 4, 9),    # interior: 3x3 outputs
+                                      (0, 0, 4),    # corner: 2x2
+                                      (0, 4, 6)])   # edge: 2x3
+def test_flops_single_pixel(cin, cout, groups, y, x, taps):
+    """One changed pixel under a 3x3 / pad-1 convolution reaches `taps`
+    outputs (the dense amplification example, clipped at borders), and each
+    reached output costs one multiply-add per input channel of its group
+    and output channel: 2 * taps * (Cin / groups) * Cout."""
+    H, W = 8, 9
+    L = _single_conv(cin, cout, groups, H, W)
+    o = so.OracleNet([L], 1, H, W, cin, "f32")
+    f0 = np.zeros((1, H, W, cin), np.float32)
+    f1 = f0.copy()
+    f1[0, y, x, :] = 1.0
+    o.encode_reference(f0)
+    o.encode_diff(f1, [0.0, 0.0])
+    assert o.flops() == 2 * taps * (cin // groups) * cout
+
+
+@pytest.mark.parametrize("cin,cout,groups", [(3, 5, 1), (6, 6, 6)])
+def test_flops_everything_active(cin, cout, groups):
+    """Negative threshold: every input pixel is active, so the pairs are all
+    in-bounds (input, output) window pairs.  For a 3x3 / stride-1 / pad-1
+    window on an H x W map offset (dy, dx) has (H - |dy|)(W - |dx|) of
+    them, which sums to (3H - 2)(3W - 2)."""
+    H, W = 6, 7
+    L = _single_conv(cin, cout, groups, H, W)
+    o = so.OracleNet([L], 1, H, W, cin, "f32")
+    rng = np.random.default_rng(2)
+    f0 = rng.random((1, H, W, cin), dtype=np.float32)
+    o.encode_reference(f0)
+    o.encode_diff(f0 + 1.0, [-1.0, -1.0])
+    pairs = (3 * H - 2) * (3 * W - 2)
+    assert o.last["layers"][0]["pairs"] == pairs
+    assert o.flops() == 2 * pairs * (cin // groups) * cout
