@@ -35,6 +35,12 @@ MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f16": 2500.0, "f32": 157.3}
 ESIZE = {"f32": 4, "f16": 2, "bf16": 2}
 
 
+def log(msg):
+    """Progress of the run, on stderr (stdout ends with the one result
+    line)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def workload(name, density):
     """Network, synthetic video and run shape of a named workload.  `chunk`
     is the number of frames per reference frame (None: one reference, then
@@ -178,23 +184,28 @@ def time_gpu(fn, reps, warm=2):
     return statistics.median(ts)
 
 
-def cpu_baseline(wl, net, thr_val):
+def cpu_baseline(wl, net, thr_val, n_diff=2, single_thread=True):
     """The oracle (numpy, fp64 accumulation) on the host cores, on a bounded
     sample of the same workload: a spatial crop of the same synthetic video
     (full frames when the workload is small), one untimed reference frame
-    and two timed diff frames; the rate is scaled to full frames by the
-    pixel ratio."""
+    and `n_diff` timed diff frames; the rate is scaled to full frames by
+    the pixel ratio.  Timed with the BLAS thread pool as it comes (every
+    core the process may use) and, with single_thread, again with one
+    thread.  `cores` is the number of threads the timed run used: the BLAS
+    pool's (the oracle's products); its element-wise numpy steps run on
+    one thread."""
     import oracle
-    from threadpoolctl import threadpool_info
+    from threadpoolctl import threadpool_info, threadpool_limits
     crop = wl["crop"]
-    frames = wl["frames"](3)
+    frames = wl["frames"](n_diff + 1)
     H, W = net.H, net.W
     if crop:
-        # the crop position whose change density over the two diff frames
-        # is closest to the full frame's (changes are clustered, so an
+        # the crop position whose change density over the diff frames is
+        # closest to the full frame's (changes are clustered, so an
         # arbitrary corner can be far from representative)
         h, w = crop
-        ch = [np.any(frames[t] != frames[t - 1], axis=-1) for t in (1, 2)]
+        ch = [np.any(frames[t] != frames[t - 1], axis=-1)
+              for t in range(1, n_diff + 1)]
         full = np.mean([c.mean() for c in ch])
         best = None
         for y in range(0, H - h + 1, h // 2):
@@ -207,34 +218,42 @@ def cpu_baseline(wl, net, thr_val):
                   for f in frames]
     else:
         h, w = H, W
-    o = oracle.OracleNet(net.layers, net.batch, h, w, net.C, net.dtype)
-    o.encode_reference(frames[0])
     thr = [thr_val] * (len(net.layers) + 1)
-    t0 = time.perf_counter()
-    dens = []
-    for t in (1, 2):
-        o.encode_diff(frames[t], thr)
-        dens.append(o.density(0))
-    dt = (time.perf_counter() - t0) / 2
+
+    def timed():
+        o = oracle.OracleNet(net.layers, net.batch, h, w, net.C, net.dtype)
+        o.encode_reference(frames[0])
+        dens = []
+        t0 = time.perf_counter()
+        for t in range(1, n_diff + 1):
+            o.encode_diff(frames[t], thr)
+            dens.append(o.density(0))
+        return (time.perf_counter() - t0) / n_diff, float(np.mean(dens))
+
+    dt, dens = timed()
     scale = (h * w) / float(H * W)
     threads = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
-    cpu = "unknown"
+    res = {"value": scale / dt, "unit": "diff-frames/s", "cores": threads,
+           "kind": "oracle",
+           "sample": (f"{n_diff} diff frames of a {h}x{w} "
+                      + ("crop" if crop else "frame")
+                      + f" (density {dens:.3f}) after an untimed reference, "
+                      f"{dt:.2f} s/frame, scaled by {scale:g}"),
+           "affinity_cores": len(os.sched_getaffinity(0)),
+           "s_per_sample_frame": dt}
+    if single_thread:
+        with threadpool_limits(limits=1):
+            dt1, _ = timed()
+        res["single_thread"] = {"value": scale / dt1,
+                                "s_per_sample_frame": dt1}
     try:
         for ln in open("/proc/cpuinfo"):
             if ln.startswith("model name"):
-                cpu = ln.split(":", 1)[1].strip()
+                res["cpu_model"] = ln.split(":", 1)[1].strip()
                 break
     except OSError:
         pass
-    return {"value": scale / dt, "unit": "diff-frames/s", "cores": threads,
-            "kind": "oracle",
-            "sample": (f"oracle diff pass on a {h}x{w} crop of the same video "
-                       f"(position chosen to match the full-frame change "
-                       f"density) "
-                       f"(input density {np.mean(dens):.3f}), 2 diff frames "
-                       f"after an untimed reference, {dt:.2f} s/frame, rate "
-                       f"scaled by the pixel ratio {scale:g}"),
-            "cpu_model": cpu}
+    return res
 
 
 COPY_BYTES = 256 << 20
@@ -808,20 +827,38 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
     stream_dens = ([round(g.density(-1, n), 5) for n in range(net.batch)]
                    if net.batch > 1 else None)
 
-    # ---- dense comparators on the same GPU, net and dtype
+    # ---- dense comparators on the same GPU, net and dtype: the library's
+    # own dense pass, and MIOpen through PyTorch both with its default
+    # algorithm choice and with its benchmarking search (each convolution
+    # shape timed over MIOpen's candidate solvers on first use, the fastest
+    # kept)
     dense_ms = {}
     if dense:
         x = frames[0]
         dense_ms["own_dense_ms"] = time_gpu(
             lambda: g.encode_reference(x, out=out0), 5)
         fwd = torch_dense_model(net, dt)
+        prev = torch.backends.cudnn.benchmark
         with torch.no_grad():
+            torch.backends.cudnn.benchmark = False
+            dense_ms["miopen_default_ms"] = time_gpu(lambda: fwd(x), 10,
+                                                     warm=3)
+            torch.backends.cudnn.benchmark = True
+            t_find = time.perf_counter()
+            fwd(x)
+            torch.cuda.synchronize()
+            dense_ms["miopen_find_s"] = time.perf_counter() - t_find
             dense_ms["miopen_ms"] = time_gpu(lambda: fwd(x), 10, warm=3)
             ref_t = fwd(x).permute(0, 2, 3, 1).float()
+            torch.backends.cudnn.benchmark = prev
         g.encode_reference(x, out=out0)
         torch.cuda.synchronize()
         dense_ms["miopen_vs_own_rel_err"] = float(
             (ref_t - out0).abs().max() / out0.abs().max())
+        dense_ms["miopen_tflops"] = dflops / (dense_ms["miopen_ms"] * 1e-3) \
+            / 1e12
+        dense_ms["own_dense_tflops"] = dflops / (
+            dense_ms["own_dense_ms"] * 1e-3) / 1e12
 
     res = {
         "schedule": schedule,
@@ -846,6 +883,7 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
     if dense_ms:
         res["speedup_vs_dense"] = {
             "miopen": dense_ms["miopen_ms"] / ms_step,
+            "miopen_default": dense_ms["miopen_default_ms"] / ms_step,
             "own_dense": dense_ms["own_dense_ms"] / ms_step}
         res["dense_ms"] = dense_ms
     if ibst_sp is not None and len(ibst_sp):
@@ -1083,19 +1121,24 @@ FRAME_KEYS = ("value", "ms_per_step", "event_ms_per_step", "effective_tflops",
               "graph_replay", "profiled_ms_per_step", "workload")
 
 
-def extra_workload(name, steps, warmup, thr=0.0):
+def extra_workload(name, steps, warmup, thr=0.0, cpu_chunk=False):
     """A secondary workload measured in the same run, summarised; in the
     SparseBatch schedule where it applies, with the frame-by-frame figure
-    beside it."""
+    beside it.  cpu_chunk: the oracle's rate over one whole chunk of diff
+    frames beside it (small workloads)."""
     import torch
     wl = workload(name, 0.0)
     net = wl["net"]
     sched = default_schedule(wl)
+    log(f"workload {name}: {sched} schedule")
     r = measure(wl, steps, warmup, 7, thr, schedule=sched)
     r.pop("_thresholds", None)
     if sched == "chunk":
         f = measure(wl, steps, warmup, 7, thr, dense=False, schedule="frame")
         r["frame_by_frame"] = {k: f[k] for k in FRAME_KEYS if k in f}
+    if cpu_chunk:
+        r["cpu_baseline"] = cpu_baseline(wl, net, thr,
+                                         n_diff=wl["chunk"] - 1)
     r["config"] = {"workload": wl["desc"], "batch": net.batch, "H": net.H,
                    "W": net.W, "C": net.C, "layers": len(net.layers),
                    "dtype": net.dtype, "chunk": wl["chunk"],
@@ -1132,6 +1175,10 @@ def main():
                          "online threshold adjustment; CRNN-VGG text lines; "
                          "the toy net)")
     ap.add_argument("--sweep-steps", type=int, default=18)
+    ap.add_argument("--full-out", default="gpurun_out/bench_full.json",
+                    help="where the full result (every sub-measurement) is "
+                         "written as JSON; stdout ends with one compact "
+                         "headline line ('' to skip the file)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of a known size "
                          "(reference kernel for the HBM byte counters)")
@@ -1158,6 +1205,7 @@ def main():
     net = wl["net"]
     sched = default_schedule(wl, args.schedule)
     K, W, KP = args.steps, args.warmup, args.profile_steps
+    log(f"headline: {wl['desc']}, {sched} schedule, {K} timed diff frames")
     r = measure(wl, K, W, KP, args.thr, dense=not args.no_dense,
                 schedule=sched)
     r.pop("_thresholds", None)
@@ -1183,10 +1231,12 @@ def main():
     }
     res.update(r)
     if sched == "chunk" and not args.no_frame:
+        log("frame-by-frame schedule on the same video")
         f = measure(wl, K, W, KP, args.thr, dense=False, schedule="frame")
         res["frame_by_frame"] = {k: f[k] for k in FRAME_KEYS if k in f}
     res["kernel_source_hash"] = kernel_source_hash()
     if args.workload == "resnet50" and not args.no_sweep:
+        log("density sweep")
         res["density_sweep"] = density_sweep(
             net, args.thr, [0.02, 0.05, 0.10, 0.20, 0.40], args.sweep_steps,
             wl["chunk"], sched)
@@ -1198,15 +1248,87 @@ def main():
             "multistream_frozen_se": frozen_se_comparison("multistream"),
             "effnet_b0_bf16_state": bf16_state_comparison("effnet_b0"),
             "multistream_bf16_state": bf16_state_comparison("multistream"),
-            "crnn": extra_workload("crnn", 30, 15, thr=0.02),
-            "toy": extra_workload("toy", 30, 3)}
+            "crnn": extra_workload("crnn", 30, 15, thr=0.02,
+                                   cpu_chunk=not args.no_cpu_baseline),
+            "toy": extra_workload("toy", 30, 3,
+                                  cpu_chunk=not args.no_cpu_baseline)}
     if args.workload == "resnet50" and not args.no_extra:
+        log("residual carry against drop")
         res["residual_carry"] = {
             "resnet50": carry_comparison("resnet50", 0.02),
             "toy": carry_comparison("toy", 0.05, steps=30)}
     if not args.no_cpu_baseline:
+        log("cpu baseline (the oracle on the host cores)")
         res["cpu_baseline"] = cpu_baseline(wl, net, args.thr)
-    print(json.dumps(res), flush=True)
+    if "dense_ms" in res and "measured_peaks" in res["roofline"]:
+        # the dense network at the box's measured library-GEMM ceiling: a
+        # bound no dense implementation beats, not a measured comparator
+        ceil = res["roofline"]["measured_peaks"]["bf16_gemm_TFLOPs"]
+        res["dense_ms"]["at_gemm_ceiling_ms"] = (
+            res["dense_gflop_per_frame"] / ceil)
+        res["speedup_vs_dense"]["dense_at_gemm_ceiling"] = (
+            res["dense_ms"]["at_gemm_ceiling_ms"] / res["ms_per_step"])
+    full = args.full_out
+    if full:
+        d = os.path.dirname(full)
+        if d:
+            os.makedirs(d, exist_ok=True)
+        with open(full, "w") as fh:
+            json.dump(res, fh, indent=1)
+        log(f"full result: {full}")
+    print(json.dumps(headline(res, full)), flush=True)
+
+
+def _r(x, nd=4):
+    """x to nd significant digits (None passes)."""
+    if x is None or isinstance(x, (bool, str)):
+        return x
+    if isinstance(x, int):
+        return x
+    return float(f"{x:.{nd}g}")
+
+
+def headline(res, full_path):
+    """The one result line: the contract's keys, the dominant kernel's
+    roofline, the CPU baseline and the dense speedups, rounded; everything
+    else stays in the full result file."""
+    keys = ("metric", "value", "unit", "n_gpus", "steps", "warmup",
+            "ms_per_step", "higher_is_better", "scaling", "vs_baseline",
+            "dtype", "data")
+    h = {k: _r(res[k]) for k in keys if k in res}
+    c = res["config"]
+    h["config"] = {"workload": c["workload"], "schedule": c["schedule"],
+                   "chunk": c["chunk"], "thr": c["thr"],
+                   "input_density": _r(c["measured_input_density"], 3)}
+    for k in ("effective_tflops", "dense_equiv_tflops", "ref_ms",
+              "chunk_amortised_frames_per_s"):
+        if res.get(k) is not None:
+            h[k] = _r(res[k])
+    if "speedup_vs_dense" in res:
+        h["speedup_vs_dense"] = {k: _r(v, 3) for k, v in
+                                 res["speedup_vs_dense"].items()}
+        h["dense_ms"] = {k: _r(res["dense_ms"][k]) for k in
+                         ("miopen_ms", "miopen_default_ms", "own_dense_ms",
+                          "at_gemm_ceiling_ms") if k in res["dense_ms"]}
+    rf = res["roofline"]
+    h["roofline"] = {k: _r(rf.get(k)) for k in
+                     ("kernel", "bound", "achieved", "peak", "unit", "frac",
+                      "traffic", "avg_launch_us", "launches")}
+    mp = rf.get("measured_peaks")
+    if mp:
+        h["roofline"]["box_copy_GBps"] = _r(mp["copy_GBps"])
+        h["roofline"]["box_bf16_gemm_TFLOPs"] = _r(mp["bf16_gemm_TFLOPs"])
+    cb = res.get("cpu_baseline")
+    if cb:
+        h["cpu_baseline"] = {"value": _r(cb["value"]), "unit": cb["unit"],
+                             "cores": cb["cores"], "kind": cb["kind"],
+                             "sample": cb["sample"]}
+        if "single_thread" in cb:
+            h["cpu_baseline"]["single_thread_value"] = _r(
+                cb["single_thread"]["value"])
+    if full_path:
+        h["full_result"] = full_path
+    return h
 
 
 if __name__ == "__main__":

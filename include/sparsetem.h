@@ -97,9 +97,14 @@ typedef struct st_layer_desc {
 } st_layer_desc;
 
 /* Validate the layer graph and plan the workspace (host only, no HIP call).
- * Inputs are `batch` images of in_h x in_w x in_c in `dtype`.  The
- * descriptors (and the weight pointers in them) are copied; the weights are
- * read only by st_bind_workspace.  On success *out owns a new net.
+ * Defines the encoder whose frames are encoded by Diff Computation (paper,
+ * section "Skipping Non-zero Delta Pixels": the CNN encoder whose
+ * convolutions, Eq. 1, are evaluated on diff pixels only; one cached
+ * pre-activation per layer followed by a non-linear operation, as the
+ * schedule of section "Design of SparseBatch" keeps).  Inputs are `batch`
+ * images of in_h x in_w x in_c in `dtype`.  The descriptors (and the weight
+ * pointers in them) are copied; the weights are read only by
+ * st_bind_workspace.  On success *out owns a new net.
  * Errors: ST_ERR_INVALID_ARG (NULL, n_layers < 1, bad src/residual_src, a
  * channel or shape mismatch, an empty output grid, an unknown dtype or
  * activation, squeeze-excitation without its weights), ST_ERR_UNSUPPORTED
@@ -181,8 +186,12 @@ st_status st_workspace_bytes(const st_net* net, uint64_t* bytes);
 st_status st_bind_workspace(st_net* net, void* dev_ptr, uint64_t bytes,
                             void* stream);
 
-/* Dense pass on a reference frame (device, storage dtype, NHWC
- * [batch][in_h][in_w][in_c]): (re)initialises the Subtraction buffer and
+/* Dense pass on a reference frame (paper, section "Skipping Non-zero
+ * Delta Pixels": the first frame of a chunk is computed densely and sets
+ * the values later frames are differenced against; section "Design of
+ * SparseBatch": the reference frame is encoded on its own before the diff
+ * frames).  `frame`: device, storage dtype, NHWC
+ * [batch][in_h][in_w][in_c].  (Re)initialises the Subtraction buffer and
  * every pre-activation buffer (bias included), and writes the network
  * output to `out` (device, f32, NHWC grid of the last layer; may be NULL
  * to skip the write).  Errors: ST_ERR_STATE (no workspace),
@@ -190,10 +199,14 @@ st_status st_bind_workspace(st_net* net, void* dev_ptr, uint64_t bytes,
 st_status st_encode_reference(st_net* net, const void* frame, float* out,
                               void* stream);
 
-/* Diff pass on the next frame of the chunk.  `thr` (host, n_layers + 1
- * floats, read before the call returns): thr[0] truncates the frame delta
- * X - X_hat, thr[j + 1] truncates layer j's emitted delta (shared by all its
- * consumers).  A pixel is kept iff the largest |delta| over its channels is
+/* Diff pass on the next frame of the chunk (paper, section "Skipping
+ * Non-zero Delta Pixels": Subtraction against the committed input, the
+ * truncation threshold on each pixel's channels, the convolution of the
+ * remaining diff pixels by linearity (Eq. 2), Accumulation onto the cached
+ * pre-activation and the non-linear handling of Eq. 3).  `thr` (host,
+ * n_layers + 1 floats, read before the call returns): thr[0] truncates the
+ * frame delta X - X_hat, thr[j + 1] truncates layer j's emitted delta
+ * (shared by all its consumers).  A pixel is kept iff the largest |delta| over its channels is
  * strictly greater than its threshold; a negative threshold keeps every
  * pixel.  Kept input pixels are committed to the Subtraction buffer;
  * truncated deltas inside the network are dropped.  `out` as for
@@ -222,7 +235,9 @@ st_status st_encode_diff(st_net* net, const void* frame, const float* thr,
 st_status st_encode_chunk(st_net* net, const void* frames, int32_t n_frames,
                           const float* thr, float* out, void* stream);
 
-/* Fraction of kept sites of the last encode: layer = -1 is the frame delta,
+/* Density (1 - sparsity) of the last encode (paper, section "Online
+ * Truncation Threshold Adjustment": the per-layer sparsity the threshold
+ * search reads).  Fraction of kept sites: layer = -1 is the frame delta,
  * layer = j is layer j's emitted delta.  image = -1 averages over the batch,
  * otherwise the density of that batch image alone (the per-stream density
  * an online threshold controller reads).  Synchronising. */
@@ -292,7 +307,11 @@ void st_destroy_net(st_net* net);
  * st_create_net failure when net is NULL).  Owned by the library. */
 const char* st_last_error(const st_net* net);
 
-/* ---- parity / introspection: host copies of the last frame's artefacts.
+/* ---- parity / introspection: host copies of the last frame's artefacts
+ * (the intermediate products of section "Skipping Non-zero Delta Pixels":
+ * the kept-pixel lists after truncation, the sites each diff pixel reaches
+ * through a window -- the dense amplification of the "Truncation
+ * threshold" paragraph -- and the cached pre-activations of Eq. 3).
  * All synchronising.  `cap` counts elements of the caller's buffer; *n
  * receives the full count even when it exceeds cap (nothing is then
  * written past cap). */
