@@ -75,9 +75,13 @@ def round_storage(x, dtype):
         return x32.astype(np.float16).astype(np.float64)
     if dtype == "bf16":
         # keep the top 16 bits of the f32 pattern, rounding to nearest even
-        u = np.ascontiguousarray(x32).view(np.uint32).astype(np.uint64)
-        u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
-        return u.astype(np.uint32).view(np.float32).astype(np.float64)
+        # (the sum stays below 2^32 for every finite or infinite pattern)
+        u = np.array(x32, dtype=np.float32, copy=True).view(np.uint32)
+        r = (u >> 16) & 1
+        r += 0x7FFF
+        u += r
+        u &= 0xFFFF0000
+        return u.view(np.float32).astype(np.float64)
     raise ValueError(f"unknown dtype {dtype}")
 
 
@@ -129,10 +133,18 @@ def conv2d_nhwc(x, w, b, stride, pad, groups=1):
         for kx in range(kw):
             patch = xp[:, ky:ky + sh * (Ho - 1) + 1:sh,
                        kx:kx + sw * (Wo - 1) + 1:sw, :]
+            if cig == 1 and cog == 1:
+                # depthwise: each channel with its own weight
+                out += patch * w[:, 0, ky, kx]
+                continue
             for g in range(groups):
-                out[..., g * cog:(g + 1) * cog] += (
-                    patch[..., g * cig:(g + 1) * cig]
-                    @ w[g * cog:(g + 1) * cog, :, ky, kx].T)
+                # contiguous operands, so that the product runs as one
+                # library matrix product per offset and group
+                pg = np.ascontiguousarray(
+                    patch[..., g * cig:(g + 1) * cig]).reshape(-1, cig)
+                wg = np.ascontiguousarray(w[g * cog:(g + 1) * cog, :, ky, kx])
+                out[..., g * cog:(g + 1) * cog] += (pg @ wg.T).reshape(
+                    N, Ho, Wo, cog)
     return out
 
 
@@ -244,7 +256,7 @@ def _apply_offset(rows, w, ky, kx, groups):
     respecting groups; returns [n, Cout] fp64."""
     Cout, cig = w.shape[0], w.shape[1]
     cog = Cout // groups
-    wk = w[:, :, ky, kx]                      # [Cout, Cin/groups]
+    wk = np.ascontiguousarray(w[:, :, ky, kx])  # [Cout, Cin/groups]
     if groups == 1:
         return rows @ wk.T
     if cig == 1 and cog == 1:                 # depthwise

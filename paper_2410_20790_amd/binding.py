@@ -267,15 +267,16 @@ def st_debug_active(net, layer) -> np.ndarray:
     return idx
 
 
-def st_debug_candidates(net, layer, channels):
+def st_debug_candidates(net, layer, channels, with_rows=True):
+    """(pixel ids, f32 rows) of the candidates; rows None when not asked."""
     n = ctypes.c_int64()
     _check(_lib.st_debug_candidates(net, layer, None, None, 0,
                                     ctypes.byref(n)), net)
     pix = np.zeros(n.value, np.int32)
-    rows = np.zeros((n.value, channels), np.float32)
+    rows = np.zeros((n.value, channels), np.float32) if with_rows else None
     _check(_lib.st_debug_candidates(net, layer, pix.ctypes.data,
-                                    rows.ctypes.data, n.value,
-                                    ctypes.byref(n)), net)
+                                    rows.ctypes.data if with_rows else None,
+                                    n.value, ctypes.byref(n)), net)
     return pix, rows
 
 
