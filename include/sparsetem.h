@@ -186,6 +186,28 @@ st_status st_workspace_bytes(const st_net* net, uint64_t* bytes);
 st_status st_bind_workspace(st_net* net, void* dev_ptr, uint64_t bytes,
                             void* stream);
 
+/* ---- a workspace that needs no allocation, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops and
+ * harnesses that forbid hipMalloc).  The library holds one workspace of
+ * ST_STATIC_WORKSPACE_BYTES per device in its own code object (a static
+ * device array, present on every device the library runs on until the
+ * process ends). */
+#define ST_STATIC_WORKSPACE_BYTES (64ull << 20)
+
+/* As st_bind_workspace, with the library's static workspace on the current
+ * device instead of a caller's buffer: no device memory is allocated or
+ * freed, by the library or on its behalf.  Waits for all work on the device
+ * to finish first, then initialises everything the net uses in the array
+ * (whatever an earlier binding left) and repacks the weights on `stream`.
+ * One array per device is shared by every net bound to it: the last binding
+ * owns it, and a net whose binding was taken over by another net's fails
+ * every further call with ST_ERR_STATE until it is bound again.  Nets that
+ * share the array must not run at the same time (their work on one device
+ * would race); binding again resets the net to "no reference".
+ * Errors: ST_ERR_INVALID_ARG (NULL net), ST_ERR_WORKSPACE
+ * (st_workspace_bytes() above ST_STATIC_WORKSPACE_BYTES), ST_ERR_HIP. */
+st_status st_bind_workspace_static(st_net* net, void* stream);
+
 /* Dense pass on a reference frame (paper, section "Skipping Non-zero
  * Delta Pixels": the first frame of a chunk is computed densely and sets
  * the values later frames are differenced against; section "Design of

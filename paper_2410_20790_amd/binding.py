@@ -38,7 +38,7 @@ EXPORTED = [
     "st_debug_counters", "st_profile_begin", "st_profile_end",
     "st_set_threshold_control", "st_encode_diff_adaptive",
     "st_get_thresholds", "st_create_net_ex", "st_debug_carry",
-    "st_encode_chunk_adaptive",
+    "st_encode_chunk_adaptive", "st_bind_workspace_static",
 ]
 
 
@@ -89,6 +89,7 @@ def _load():
         "st_encode_chunk": [P, P, I32, ctypes.POINTER(ctypes.c_float), P, P],
         "st_workspace_bytes": [P, ctypes.POINTER(U64)],
         "st_bind_workspace": [P, P, U64, P],
+        "st_bind_workspace_static": [P, P],
         "st_encode_reference": [P, P, P, P],
         "st_encode_diff": [P, P, ctypes.POINTER(ctypes.c_float), P, P],
         "st_layer_density": [P, I32, I32, ctypes.POINTER(ctypes.c_float)],
@@ -183,6 +184,13 @@ def st_workspace_bytes(net) -> int:
 def st_bind_workspace(net, dev_ptr, nbytes, stream=0):
     _check(_lib.st_bind_workspace(net, _ptr(dev_ptr), nbytes, _ptr(stream)),
            net)
+
+
+def st_bind_workspace_static(net, stream=0):
+    _check(_lib.st_bind_workspace_static(net, _ptr(stream)), net)
+
+
+STATIC_WORKSPACE_BYTES = 64 << 20
 
 
 def st_encode_reference(net, frame_ptr, out_ptr=None, stream=0):

@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -50,6 +51,32 @@ void prof_end(const Prof& p, int cls, hipStream_t s) {
 
 }  // namespace st
 
+// The library's own workspace for callers that cannot allocate device
+// memory (st_bind_workspace_static): one fixed-size array per device, held
+// until the process ends.  In host code `scratch` names a host-side stand-in,
+// never the device array: its device address comes from
+// hipGetSymbolAddress, taken once per device with that device current, and
+// only that address is used.  A generation count per device records which
+// net bound the array last; a net whose binding was taken over refuses to
+// run.
+static __device__ __align__(256) char scratch[ST_STATIC_WORKSPACE_BYTES];
+
+namespace {
+
+struct StaticWs {
+  void* ptr = nullptr;   // device address of `scratch` on this device
+  uint64_t gen = 0;      // bindings so far
+};
+std::mutex g_static_mu;
+std::vector<StaticWs> g_static;  // indexed by device ordinal
+
+uint64_t static_generation(int dev) {
+  std::lock_guard<std::mutex> lk(g_static_mu);
+  return dev >= 0 && dev < (int)g_static.size() ? g_static[dev].gen : 0;
+}
+
+}  // namespace
+
 using namespace st;
 
 namespace {
@@ -63,6 +90,18 @@ st_status hip_check(st_net* net, const char* what) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess)
     return fail(net, ST_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+  return ST_OK;
+}
+
+// The workspace is usable: bound, and -- bound to the library's static
+// workspace -- not bound by another net since.
+st_status need_ws(st_net* net) {
+  if (!net->bound) return fail(net, ST_ERR_STATE, "no workspace bound");
+  if (net->static_dev >= 0 &&
+      static_generation(net->static_dev) != net->static_gen)
+    return fail(net, ST_ERR_STATE,
+                "the library's static workspace was bound by another net "
+                "since this one bound it");
   return ST_OK;
 }
 
@@ -738,6 +777,7 @@ extern "C" st_status st_bind_workspace(st_net* net, void* dev_ptr,
   net->ws = (char*)dev_ptr;
   net->bound = false;
   net->have_ref = false;
+  net->static_dev = -1;
   (void)hipGetLastError();
   const WS ws{net->ws};
   launch_fill_u32(s, net->ws, (int64_t)(net->ws_bytes / 4), 0u);
@@ -795,10 +835,58 @@ extern "C" st_status st_bind_workspace(st_net* net, void* dev_ptr,
   return ST_OK;
 }
 
+extern "C" st_status st_bind_workspace_static(st_net* net, void* stream) {
+  if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
+  if (net->ws_bytes > (size_t)ST_STATIC_WORKSPACE_BYTES)
+    return fail(net, ST_ERR_WORKSPACE,
+                "the net needs " + std::to_string(net->ws_bytes) +
+                    " workspace bytes; the static workspace holds " +
+                    std::to_string((unsigned long long)
+                                       ST_STATIC_WORKSPACE_BYTES));
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0)
+    return fail(net, ST_ERR_HIP,
+                std::string("hipGetDevice: ") + hipGetErrorString(e));
+  // the previous owner's work (on any stream) must be done with the array
+  e = hipDeviceSynchronize();
+  if (e != hipSuccess)
+    return fail(net, ST_ERR_HIP,
+                std::string("hipDeviceSynchronize: ") + hipGetErrorString(e));
+  void* ptr = nullptr;
+  uint64_t gen = 0;
+  {
+    std::lock_guard<std::mutex> lk(g_static_mu);
+    if ((int)g_static.size() <= dev) g_static.resize(dev + 1);
+    StaticWs& w = g_static[dev];
+    if (!w.ptr) {
+      // first use on this device (current): the device address of the
+      // array; the host-side name is never passed anywhere
+      void* p = nullptr;
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !p)
+        return fail(net, ST_ERR_HIP,
+                    std::string("hipGetSymbolAddress: ") +
+                        hipGetErrorString(e));
+      w.ptr = p;
+    }
+    ptr = w.ptr;
+    gen = ++w.gen;
+  }
+  // the plain binding initialises every byte the net uses (zeros, empty
+  // pixel maps, repacked weights), whatever the last binding left
+  const st_status st = st_bind_workspace(net, ptr,
+                                         ST_STATIC_WORKSPACE_BYTES, stream);
+  if (st != ST_OK) return st;
+  net->static_dev = dev;
+  net->static_gen = gen;
+  return ST_OK;
+}
+
 extern "C" st_status st_encode_reference(st_net* net, const void* frame,
                                          float* out, void* stream) {
   if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
-  if (!net->bound) return fail(net, ST_ERR_STATE, "no workspace bound");
+  if (const st_status w = need_ws(net); w != ST_OK) return w;
   if (!frame) return fail(net, ST_ERR_INVALID_ARG, "frame is NULL");
   st_status s = encode(net, frame, nullptr, out, (hipStream_t)stream, true);
   if (s == ST_OK) net->have_ref = true;
@@ -809,7 +897,7 @@ extern "C" st_status st_encode_reference(st_net* net, const void* frame,
 static st_status check_chunk(st_net* net, const void* frames,
                              int32_t n_frames) {
   if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
-  if (!net->bound) return fail(net, ST_ERR_STATE, "no workspace bound");
+  if (const st_status w = need_ws(net); w != ST_OK) return w;
   if (!net->have_ref)
     return fail(net, ST_ERR_STATE, "no reference frame encoded yet");
   if (!frames) return fail(net, ST_ERR_INVALID_ARG, "frames is NULL");
@@ -863,7 +951,7 @@ extern "C" st_status st_encode_diff(st_net* net, const void* frame,
                                     const float* thr, float* out,
                                     void* stream) {
   if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
-  if (!net->bound) return fail(net, ST_ERR_STATE, "no workspace bound");
+  if (const st_status w = need_ws(net); w != ST_OK) return w;
   if (!net->have_ref)
     return fail(net, ST_ERR_STATE, "st_encode_diff before st_encode_reference");
   if (!frame || !thr) return fail(net, ST_ERR_INVALID_ARG, "NULL frame or thr");
@@ -882,7 +970,7 @@ extern "C" st_status st_set_threshold_control(st_net* net,
                                               int32_t cycle_refs,
                                               void* stream) {
   if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
-  if (!net->bound) return fail(net, ST_ERR_STATE, "no workspace bound");
+  if (const st_status w = need_ws(net); w != ST_OK) return w;
   if (!controlled || !fixed_thr)
     return fail(net, ST_ERR_INVALID_ARG, "NULL controlled or fixed_thr");
   if (!(target >= 0.0 && target <= 1.0) || !(eps >= 0.0) ||
@@ -940,7 +1028,7 @@ extern "C" st_status st_set_threshold_control(st_net* net,
 extern "C" st_status st_encode_diff_adaptive(st_net* net, const void* frame,
                                              float* out, void* stream) {
   if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
-  if (!net->bound) return fail(net, ST_ERR_STATE, "no workspace bound");
+  if (const st_status w = need_ws(net); w != ST_OK) return w;
   if (!net->ibst_on)
     return fail(net, ST_ERR_STATE, "threshold control not set");
   if (!net->have_ref)
@@ -965,8 +1053,8 @@ extern "C" st_status st_get_thresholds(st_net* net, float* thr) {
 extern "C" st_status st_layer_density(st_net* net, int32_t layer,
                                       int32_t image, float* d) {
   if (!net || !d) return fail(net, ST_ERR_INVALID_ARG, "NULL argument");
-  if (!net->bound || !net->have_ref)
-    return fail(net, ST_ERR_STATE, "nothing encoded yet");
+  if (const st_status w = need_ws(net); w != ST_OK) return w;
+  if (!net->have_ref) return fail(net, ST_ERR_STATE, "nothing encoded yet");
   if (layer < -1 || layer >= (int)net->layers.size())
     return fail(net, ST_ERR_INVALID_ARG, "layer out of range");
   const int images = net->N * net->last_nf;
@@ -1010,7 +1098,8 @@ static st_status debug_prelude(st_net* net, int32_t layer, bool need_enc) {
   if (!net) return fail(nullptr, ST_ERR_INVALID_ARG, "net is NULL");
   if (layer < -1 || layer >= (int)net->layers.size())
     return fail(net, ST_ERR_INVALID_ARG, "layer out of range");
-  if (!net->bound || (need_enc && !net->have_ref))
+  if (const st_status w = need_ws(net); w != ST_OK) return w;
+  if (need_enc && !net->have_ref)
     return fail(net, ST_ERR_STATE, "nothing encoded yet");
   return sync_last(net);
 }

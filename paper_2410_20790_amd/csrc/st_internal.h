@@ -150,6 +150,10 @@ struct st_net {
   // runtime
   char* ws = nullptr;
   bool bound = false, have_ref = false;
+  // bound to the library's static workspace on device static_dev (-1: a
+  // caller's workspace) as its static_gen-th binding there
+  int static_dev = -1;
+  uint64_t static_gen = 0;
   void* last_stream = nullptr;
   std::string err;
   st::Recorder* rec = nullptr;

@@ -36,12 +36,14 @@ class SparseTemNet:
     carry (ST_NET_RESIDUAL_CARRY); ``frozen_se``:
     squeeze-excitation gates kept from the reference frame
     (ST_NET_FROZEN_SE, an approximation); ``bf16_state``: pre-activation
-    state stored in bf16 (ST_NET_BF16_STATE, an approximation)."""
+    state stored in bf16 (ST_NET_BF16_STATE, an approximation);
+    ``static_workspace``: bound to the library's own per-device workspace
+    (st_bind_workspace_static) instead of a torch allocation."""
 
     def __init__(self, layers: Sequence, batch: int, H: int, W: int, C: int,
                  dtype: str = "f32", device="cuda", max_frames: int = 1,
                  carry: bool = False, frozen_se: bool = False,
-                 bf16_state: bool = False):
+                 bf16_state: bool = False, static_workspace: bool = False):
         self.dtype = dtype
         self.tdtype = TORCH_DTYPES[dtype]
         dev = torch.device(device)
@@ -88,10 +90,15 @@ class SparseTemNet:
             self.handle = B.st_create_net(descs, batch, H, W, C,
                                           B.DTYPE_CODES[dtype])
         self.ws_bytes = B.st_workspace_bytes(self.handle)
-        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8,
-                              device=self.device)
-        B.st_bind_workspace(self.handle, self.ws.data_ptr(), self.ws_bytes,
-                            self._stream())
+        if static_workspace:
+            # the library's own per-device workspace: nothing allocated
+            self.ws = None
+            B.st_bind_workspace_static(self.handle, self._stream())
+        else:
+            self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8,
+                                  device=self.device)
+            B.st_bind_workspace(self.handle, self.ws.data_ptr(),
+                                self.ws_bytes, self._stream())
         torch.cuda.current_stream(self.device).synchronize()
         self.out_shape = B.st_tensor_shape(self.handle, self.n_layers - 1)
 

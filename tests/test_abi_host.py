@@ -305,3 +305,17 @@ def test_bf16_state_flag():
             B.st_create_net_ex(descs(n), n.batch, 1, n.H, n.W, n.C, B.ST_F32,
                                flags)
         assert e.value.status == B.ST_ERR_UNSUPPORTED
+
+
+def test_static_workspace_rejects_a_net_too_large():
+    """The no-allocation binding checks the net's workspace against the
+    static one before any device call."""
+    net = resnet50_net(H=1024, W=2048)
+    h = create(net)
+    try:
+        assert B.st_workspace_bytes(h) > B.STATIC_WORKSPACE_BYTES
+        with pytest.raises(B.StError) as e:
+            B.st_bind_workspace_static(h)
+        assert e.value.status == B.ST_ERR_WORKSPACE
+    finally:
+        B.st_destroy_net(h)
