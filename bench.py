@@ -532,9 +532,10 @@ def run_diffs(feed, n):
     return total, refs
 
 
-def frames_needed(chunk, W, K, KP, KG=0):
-    """Frames consumed by the warm-up (W), timed (K), profiled (KP) and
-    graph-replay (KG) passes, reference frames included."""
+def frames_needed(chunk, W, K, KP, KG=0, align=False):
+    """Frames consumed by the warm-up (W; with align, continued to the end
+    of its chunk), timed (K), profiled (KP) and graph-replay (KG) passes,
+    reference frames included."""
     pos = 0
 
     def is_ref(p):
@@ -547,6 +548,9 @@ def frames_needed(chunk, W, K, KP, KG=0):
             d += 0 if is_ref(pos) else 1
             pos += 1
     diffs(W)
+    if align and chunk:
+        while not is_ref(pos):
+            pos += 1
     diffs(K)
     if chunk:  # the profiled frames start with a reference frame
         while not is_ref(pos):
@@ -557,17 +561,29 @@ def frames_needed(chunk, W, K, KP, KG=0):
     return pos
 
 
-def kernel_table(net, recs, counts, es, chunk_mode=False):
+def kernel_table(net, recs, counts, es, chunk_mode=False, nf=1):
     """Per kernel class: launches, time, algorithmic bytes / FLOPs from the
     frame's counters (see conv_launch_bytes).  In chunk mode a profiled
-    "frame" is one chunk (counters summed over its frames); a stateful
-    layer whose GEMM epilogue applies the chunk's updates is charged its
-    delta rows and one state read and write per updated site, the others
-    write f32 update rows, and the chunk state update kernel is charged its
-    update-row reads and delta writes (a lower bound: its f32 state reads
-    and writes, once per site, are not counted)."""
+    "frame" is one chunk of nf frames (counters summed over its frames); a
+    stateful layer whose GEMM epilogue applies the chunk's updates is
+    charged its delta rows and one state read and write per updated site,
+    the others write f32 update rows.
+
+    The other kernels' bytes are their minimal traffic from the same
+    counters: every item a compaction pass visits read once (a keep byte or
+    a row maximum), every kept item's list, map and neighbour entries
+    written once; the chunk update reads each updated site's state once and
+    each update row once, writes each delta row (or, before a pool, each
+    per-frame state) once and each updated site's state once, the output
+    layer's update also every site's state and dense output per frame; the
+    pool emission writes each pooled row once and reads the states of the
+    conv sites its window adds over the previous pooled site (stride area)
+    for both frame states; the commit reads each updated site's last state
+    and writes it once."""
     from paper_2410_20790_amd import binding as B
     classes = {}
+    n_in = net.batch * net.H * net.W
+    seen = set()
     for r in recs:
         name = B.KERNEL_CLASSES[r["kernel"]]
         c = classes.setdefault(name, {"launches": 0, "ms": 0.0, "bytes": 0.0,
@@ -577,37 +593,108 @@ def kernel_table(net, recs, counts, es, chunk_mode=False):
         f, j = int(r["frame"]), int(r["layer"])
         if f >= len(counts):
             continue
+        L = net.layers[j] if j >= 0 else None
+        cnt = counts[f, j] if j >= 0 else None
         if name in ("conv_gemm", "conv_dw"):
-            L = net.layers[j]
             mode = layer_mode(net, j)
             if chunk_mode and mode == "state":
                 mode = "fused" if counts[f, j, 6] > 0 else "defer"
-            c["bytes"] += conv_launch_bytes(L, counts[f, j], es, mode)
-            c["flops"] += 2.0 * counts[f, j, 1] * (L.c_in // L.groups) * \
-                L.c_out
+            c["bytes"] += conv_launch_bytes(L, cnt, es, mode)
+            c["flops"] += 2.0 * cnt[1] * (L.c_in // L.groups) * L.c_out
         elif name in ("se_squeeze", "se_emit"):
             # squeeze: the site map, and f32 state and update rows of the
             # affected sites; emit: the state and map of every site, update
             # rows, the delta and row bookkeeping of every site written,
             # and the affected state rows written back
-            L = net.layers[j]
             npix = int(np.prod(net_conv_grid(net, j)))
-            nO = int(counts[f, j, 0])
+            nO = int(cnt[0])
             if name == "se_squeeze":
                 b = npix * 4 + nO * L.c_out * 8
             else:
                 b = npix * (L.c_out * (4 + es) + 16) + nO * L.c_out * 8
             c["bytes"] += b
         elif name == "chunk_update":
-            L = net.layers[j]
-            c["bytes"] += int(counts[f, j, 0]) * L.c_out * (4 + es)
+            nO, sites = int(cnt[0]), int(cnt[7])
+            npix = int(np.prod(net_conv_grid(net, j)))
+            pool = L.pool_k[0] > 0
+            b = nO * (4 + 4 * L.c_out)             # list + update rows read
+            if sites:                              # walks the affected list
+                b += sites * L.c_out * 4           # state read
+                if pool:
+                    b += nO * L.c_out * 4 + sites * 4   # P_t rows, frame bits
+                else:
+                    b += nO * (L.c_out * es + 4) + sites * L.c_out * 4
+            else:                                  # every site (output)
+                b += nf * npix * 4 + npix * L.c_out * 4      # maps, state
+                b += nf * npix * L.c_out * 4                 # dense output
+                b += nO * (L.c_out * es + 4) + min(nO, npix) * L.c_out * 4
+            c["bytes"] += b
+        elif name == "commit":
+            if chunk_mode:
+                sites = int(cnt[7])
+                c["bytes"] += int(cnt[0]) * 4 + sites * (L.c_out * 8 + 4)
+            else:
+                c["bytes"] += int(cnt[0]) * (4 + L.c_out * 12)
+        elif name == "pool_emit":
+            nQ = int(cnt[3])
+            area = L.pool_s[0] * L.pool_s[1]
+            c["bytes"] += nQ * (4 + L.c_out * es + 4) + \
+                nQ * area * 2 * L.c_out * 4
+        elif name in ("rb_count", "pool_count"):
+            npix = int(np.prod(net_conv_grid(net, j)))
+            if name == "pool_count":
+                g = net_out_grid(net, j)
+                npix = int(np.prod(g))
+            c["bytes"] += npix * nf                       # flag bytes
+        elif name in ("rb_compact", "pool_compact"):
+            npix = int(np.prod(net_conv_grid(net, j)))
+            K = L.k[0] * L.k[1]
+            if name == "pool_compact":
+                npix = int(np.prod(net_out_grid(net, j)))
+                kept, K = int(cnt[3]), 0
+            else:
+                kept = int(cnt[0])
+            # flags read; per kept item list, map, row maximum written and
+            # the flag cleared; neighbour entries written and input map read
+            c["bytes"] += npix * nf + kept * (13 + 8 * K)
+        elif name == "list_count":
+            n = int(cnt[3])
+            c["bytes"] += n * 4 + (n // 64 + 1) * 4
+        elif name == "list_compact":
+            n, kept = int(cnt[3]), int(cnt[4])
+            # row maximum and row site read per candidate; kept list written
+            # per kept row, the map cleared per dropped row; consumers'
+            # affected-output marks or identity lists (12 bytes) per kept row
+            c["bytes"] += n * 8 + kept * 16 + (n - kept) * 4
+        elif name in ("scan_mask", "scan_compact") and (name, f) in seen:
+            continue  # a chunk's second kernel of the class: charged once
         elif name == "scan_mask":
-            c["bytes"] += net.batch * net.H * net.W * (2 * net.C * es + 1)
+            # frames and X_hat read; keep bytes written (a chunk: also the
+            # base-frame and last-frame bytes)
+            C = net.C
+            seen.add((name, f))
+            c["bytes"] += n_in * ((2 * C * es + 1) if not chunk_mode else
+                                  (nf * C * es + C * es + 2 * nf + 1))
         elif name == "scan_compact":
-            n0 = counts[f, 0, 2] if net.layers[0].src == -1 else 0
-            c["bytes"] += net.batch * net.H * net.W + n0 * (
-                3 * net.C * es + 12)
+            seen.add((name, f))
+            n0 = int(counts[f, 0, 2]) if net.layers[0].src == -1 else 0
+            C, Cp = net.C, (net.C + 7) // 8 * 8
+            # keep bytes read; per kept item its frame and reference value
+            # read, the delta row and list, map entries written; X_hat
+            # committed at the changed sites (bounded by the kept items)
+            c["bytes"] += n_in * nf + n0 * (2 * C * es + Cp * es + 12) + \
+                min(n0, n_in) * 2 * C * es
     return classes
+
+
+def net_out_grid(net, j):
+    """(N, Hp, Wp) of layer j's emitted tensor (after its pool)."""
+    N, Ho, Wo = net_conv_grid(net, j)
+    L = net.layers[j]
+    if L.pool_k[0] > 0:
+        Ho = (Ho + 2 * L.pool_p[0] - L.pool_k[0]) // L.pool_s[0] + 1
+        Wo = (Wo + 2 * L.pool_p[1] - L.pool_k[1]) // L.pool_s[1] + 1
+    return (N, Ho, Wo)
 
 
 _GRIDS = {}
@@ -708,7 +795,8 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
     use_ibst = wl["ibst"] if ibst is None else ibst
     KG = K if schedule == "frame" else 0
     t_gen = time.perf_counter()
-    frames_np = wl["frames"](frames_needed(chunk, W, K, KP, KG))
+    frames_np = wl["frames"](frames_needed(chunk, W, K, KP, KG,
+                                           align=schedule == "chunk"))
     t_gen = time.perf_counter() - t_gen
     tdt = {"f32": torch.float32, "f16": torch.float16,
            "bf16": torch.bfloat16}[dt]
@@ -743,6 +831,11 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
     dflops = dense_flops(net, [net_conv_grid(net, i) for i in range(L_n)])
 
     run_diffs(feed, W)  # reference frame + warm-up
+    if schedule == "chunk":
+        # the warm-up finishes its chunk, so that the timed frames start at
+        # a chunk boundary (whole chunks, the last one possibly shorter)
+        while not feed.next_is_ref():
+            feed.diff(chunk)
 
     # ---- timed region: K diff frames (reference frames of later chunks
     # are synchronised around and excluded)
@@ -777,7 +870,8 @@ def measure(wl, K, W, KP, thr_val, dense=True, target=0.9, eps=0.025,
         for f in range(len(counts))
         for j, L in enumerate(net.layers)) / KP
     classes = kernel_table(net, recs, counts, es,
-                           chunk_mode=schedule == "chunk")
+                           chunk_mode=schedule == "chunk",
+                           nf=batch if schedule == "chunk" else 1)
     total_ms = sum(c["ms"] for c in classes.values())
     kern = {}
     for name, c in sorted(classes.items(), key=lambda kv: -kv[1]["ms"]):

@@ -397,12 +397,14 @@ st_status st_profile_begin(st_net* net, int32_t max_launches,
                            int32_t max_frames);
 
 /* Stop recording (synchronising).  Writes up to `cap` launch records and,
- * per recorded encode call f and layer j, counts[(f * n_layers + j) * 7 + i]
+ * per recorded encode call f and layer j, counts[(f * n_layers + j) * 8 + i]
  * = {affected conv outputs, rulebook pairs, kept input rows of the layer's
  * source, emitted candidate rows, emitted kept rows, kept rows of the
  * residual source (0 without residual), sites whose state the GEMM epilogue
- * updated over a chunk's frames (st_encode_chunk's fused layers; else 0)},
- * up to `cap_frames` calls; a chunk's counts sum over its frames. */
+ * updated over a chunk's frames (st_encode_chunk's fused layers; else 0),
+ * sites whose state the chunk update kernel updated from the affected list
+ * (st_encode_chunk's deferred layers other than the output layer; else
+ * 0)}, up to `cap_frames` calls; a chunk's counts sum over its frames. */
 st_status st_profile_end(st_net* net, st_launch_record* recs, int32_t cap,
                          int32_t* n, int64_t* counts, int32_t cap_frames,
                          int32_t* n_frames);

@@ -328,7 +328,7 @@ def st_profile_end(net, n_layers, cap=1 << 20, cap_frames=4096):
     recs = (st_launch_record * cap)()
     n = ctypes.c_int32()
     nf = ctypes.c_int32()
-    counts = np.zeros((cap_frames, n_layers, 7), np.int64)
+    counts = np.zeros((cap_frames, n_layers, 8), np.int64)
     _check(_lib.st_profile_end(net, recs, cap, ctypes.byref(n),
                                counts.ctypes.data, cap_frames,
                                ctypes.byref(nf)), net)

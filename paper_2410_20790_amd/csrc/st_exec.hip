@@ -589,6 +589,9 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
     u.P = ws.at<float>(L.off_P);
     u.dP = cdp;
     u.Mo = Mo;
+    u.O = O;
+    u.nO = cO;
+    u.sites = cnt + L.cnt_sites;  // the GEMM epilogue does not count here
     u.dout = ws.at<char>(outT.off_rows);
     u.rowmax = rowmax_out;
     u.aff = ws.at<uint32_t>(net->off_chunk_aff);
@@ -651,9 +654,9 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
       pa.keep_thr_dev = thr_dev;
     }
     launch_chunk_pool_emit(pf, s, net->dtype, pa);
-    launch_chunk_commit(pf, s, ws.at<float>(L.off_P), cdp, Mo,
-                        ws.at<uint32_t>(net->off_chunk_aff), L.conv_grid,
-                        L.cout_p);
+    launch_chunk_commit(pf, s, ws.at<float>(L.off_P), cdp, O, cO,
+                        ws.at<uint32_t>(net->off_chunk_aff), citems,
+                        L.conv_grid, L.cout_p);
   }
   if (L.stateful)
     launch_group_count(pf, s, rowmax_out, cnt + outT.cnt_rows,
@@ -1318,7 +1321,7 @@ extern "C" st_status st_profile_end(st_net* net, st_launch_record* recs,
         const LayerPlan& L = net->layers[j];
         const TensorPlan& in = net->tensors[L.d.src + 1];
         const TensorPlan& out = net->tensors[j + 1];
-        int64_t* q = counts + ((size_t)f * nl + j) * 7;
+        int64_t* q = counts + ((size_t)f * nl + j) * 8;
         q[0] = (int64_t)c[L.cnt_O];
         q[1] = (int64_t)c[L.cnt_pairs];
         q[2] = (int64_t)c[in.cnt_act];
@@ -1327,9 +1330,14 @@ extern "C" st_status st_profile_end(st_net* net, st_launch_record* recs,
         q[5] = L.d.residual_src == -2
                    ? 0
                    : (int64_t)c[net->tensors[L.d.residual_src + 1].cnt_act];
-        q[6] = 0;
+        // sites updated over a chunk: by the fused GEMM epilogue, or by
+        // the chunk update kernel walking the affected list
+        int64_t sites = 0;
         for (int k = 0; k < kSiteSlots; ++k)
-          q[6] += (int64_t)c[L.cnt_sites + k];
+          sites += (int64_t)c[L.cnt_sites + k];
+        const bool fused = net->last_nf > 1 && chunk_fused(net, j);
+        q[6] = fused ? sites : 0;
+        q[7] = fused ? 0 : sites;
       }
     }
   return ST_OK;

@@ -281,6 +281,10 @@ struct ChunkUpdArgs {
   float* P;            // state [npix][cp] (physical sites)
   float* dP;           // deferred update rows [*][cp] (pool mode: P_t)
   const int* Mo;       // conv item -> dP row or -1
+  const int* O;        // affected conv items (site-major), dP row = index
+  const u64* nO;
+  u64* sites;          // partial counts [kSiteSlots] of the sites updated
+                       // (list mode), or NULL
   void* dout;          // emitted rows [*][cp] (not in pool mode)
   uint32_t* rowmax;    // [rows]
   uint32_t* aff;       // [npix] frames that updated each site (pool mode)
@@ -322,10 +326,12 @@ struct ChunkPoolArgs {
 };
 void launch_chunk_pool_emit(const Prof& pf, hipStream_t s, int dtype,
                             const ChunkPoolArgs& a);
-// P[w] = P after the last frame that updated w (pooled layers)
+// P[w] = P after the last frame that updated w, for the sites of the
+// affected list O (site-major items, capacity capO), whose frame bits
+// aff[w] are then cleared (pooled layers)
 void launch_chunk_commit(const Prof& pf, hipStream_t s, float* P,
-                         const float* Pt, const int* Mo, const uint32_t* aff,
-                         int64_t nconv, int cp);
+                         const float* Pt, const int* O, const u64* nO,
+                         uint32_t* aff, int64_t capO, int64_t nconv, int cp);
 
 // ---- dense network output (Accumulation)
 // p16: the state is stored as bf16.  se: the last layer's two gate slots

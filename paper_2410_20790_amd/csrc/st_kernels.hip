@@ -873,16 +873,17 @@ __device__ __forceinline__ int split_count(int64_t ntiles, int nst, int smax) {
 // with device-scope atomics; the last block to finish a row tile (over its
 // column tiles) counts the tile's kept rows for the truncation pass.  Every
 // thread of the block must call it (it synchronises).
+//
+// finish_cols does the per-column work of one thread (16 columns of 64) and
+// returns the largest magnitude it emitted; finish_rows merges the row
+// maxima and counts kept rows.  A wide tile calls finish_cols once per
+// 64-column quarter and finish_rows once.
 template <typename T, bool REF, int ACT, class LoadV, class LoadPo,
           class LoadSk>
-__device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
-                                            LoadPo load_po, LoadSk load_sk,
-                                            const bool (&hv)[2], int64_t eo,
-                                            bool eok, int epix, int64_t m0,
-                                            int n0, int ec, int tiles_n,
-                                            int64_t m_end, int* s_last) {
-  constexpr int BM = kGemmBM;
-  const int tid = threadIdx.x;
+__device__ __forceinline__ float finish_cols(const ConvArgs& a, LoadV load_v,
+                                             LoadPo load_po, LoadSk load_sk,
+                                             const bool (&hv)[2], int64_t eo,
+                                             int epix, int n0, int ec) {
   const int cout_p = a.cout_p;
   T* dout = (T*)a.dout;
   float rm = 0.f;
@@ -936,6 +937,19 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
     }
     rm = fmaxf(rm, Vec8<T>::store(dout + eo * cout_p + n, v));
   }
+  return rm;
+}
+
+// Row maxima of an output tile (rm: this thread's largest emitted
+// magnitude over its columns) and the kept-row count of the last block to
+// finish the row tile.  Every thread of the block must call it (it
+// synchronises).
+__device__ __forceinline__ void finish_rows(const ConvArgs& a, float rm,
+                                            int64_t eo, bool eok, int64_t m0,
+                                            int tiles_n, int64_t m_end,
+                                            int* s_last) {
+  constexpr int BM = kGemmBM;
+  const int tid = threadIdx.x;
   // the four threads of a row are adjacent lanes
   rm = fmaxf(rm, __shfl_xor(rm, 1, 64));
   rm = fmaxf(rm, __shfl_xor(rm, 2, 64));
@@ -975,6 +989,19 @@ __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
       }
     }
   }
+}
+
+template <typename T, bool REF, int ACT, class LoadV, class LoadPo,
+          class LoadSk>
+__device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
+                                            LoadPo load_po, LoadSk load_sk,
+                                            const bool (&hv)[2], int64_t eo,
+                                            bool eok, int epix, int64_t m0,
+                                            int n0, int ec, int tiles_n,
+                                            int64_t m_end, int* s_last) {
+  const float rm = finish_cols<T, REF, ACT>(a, load_v, load_po, load_sk, hv,
+                                            eo, epix, n0, ec);
+  finish_rows(a, rm, eo, eok, m0, tiles_n, m_end, s_last);
 }
 
 // Four channels of a delta row stored in the storage type; returns the
@@ -1062,7 +1089,6 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
       }
     }
   }
-  if (tid < kGemmBM) s_rmax[tid] = 0u;
   __syncthreads();
   const int r0 = run ? s_run[g] : 0, r1 = run ? s_run[g + 1] : 0;
   // the frames of the run, with the activation fixed at compile time
@@ -1109,18 +1135,18 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
                      make_float4(P[4 * q], P[4 * q + 1], P[4 * q + 2],
                                  P[4 * q + 3]));
   }
-  __syncthreads();
-  if (tid < rows && s_rmax[tid])
-    atomicMax(a.rowmax + m0 + tid, s_rmax[tid]);
 }
 
 // Chunk-state epilogue: the tile's rows [m0, m0 + rows) are whole site
-// runs (a site's frames, in frame order), its f32 accumulators in Cs (row
-// stride cld), the rows' sites and residual rows in s_site / s_rsk.  The
-// runs are listed, then each run gets 4, 8 or 16 threads (16, 8 or 4
-// columns each) -- as many as the tile's run count leaves -- so that long
-// runs (sites that changed in most frames) still keep the block busy.
-// Every thread of the block must call it.
+// runs (a site's frames, in frame order), the f32 accumulators of 64 of
+// its columns (from n0) in Cs (row stride cld), the rows' sites and
+// residual rows in s_site / s_rsk.  The runs are listed (first call of a
+// tile), then each run gets 4, 8 or 16 threads (16, 8 or 4 columns each)
+// -- as many as the tile's run count leaves -- so that long runs (sites
+// that changed in most frames) still keep the block busy.  A wide tile
+// calls it once per 64-column quarter; its row maxima gather in s_rmax
+// and the last call merges them into the device row maxima.  Every thread
+// of the block must call it.
 template <typename T>
 __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
                                                   float* Cs, int cld,
@@ -1128,17 +1154,21 @@ __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
                                                   int rows, int n0,
                                                   const int* s_site,
                                                   const int* s_rsk,
-                                                  unsigned* s_rmax) {
+                                                  unsigned* s_rmax,
+                                                  bool first = true,
+                                                  bool last = true) {
   constexpr int BM = kGemmBM;
+  const int tid = threadIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   // run starts: s_run[0..nruns) (wave 0 lists them), s_run[nruns] = rows,
   // s_run[BM + 1] = nruns
-  if (wave == 0) {
-    const bool first =
+  if (first && tid < BM) s_rmax[tid] = 0u;
+  if (first && wave == 0) {
+    const bool opens =
         lane < rows && (lane == 0 || s_site[lane] != s_site[lane - 1]);
-    const u64 starts = __ballot(first);
+    const u64 starts = __ballot(opens);
     const int nr = __popcll(starts);
-    if (first) s_run[lane_prefix(starts)] = lane;
+    if (opens) s_run[lane_prefix(starts)] = lane;
     if (lane == 0) {
       s_run[nr] = rows;
       s_run[BM + 1] = nr;
@@ -1158,26 +1188,67 @@ __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
   else
     chunk_tile_runs<T, 4>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
                           s_rsk, s_rmax);
+  if (last) {
+    __syncthreads();
+    if (tid < rows && s_rmax[tid])
+      atomicMax(a.rowmax + m0 + tid, s_rmax[tid]);
+  }
+}
+
+// Tile shapes of the gather-GEMM.  Both are 64 affected rows by BN output
+// channels with four waves (256 threads):
+//   BN = 64:  waves in a 2x2 arrangement, each a 32x32 sub-tile; reduction
+//             stages of MmaCfg<T>::KC columns.
+//   BN = 256 (wide, f16/bf16 only, for layers whose padded width is a
+//             multiple of 256): waves side by side, each owning 64 columns
+//             of all 64 rows (4x4 MFMA 16x16 blocks), reduction stages of 32
+//             columns.  A wave's 64x64 sub-tile reads half the LDS bytes per
+//             MFMA of a 32x32 one, and the gathered rows are staged once for
+//             256 columns instead of once per 64.  Two blocks per CU.
+template <typename T, bool WIDE> struct GemmTile {
+  static_assert(!WIDE || sizeof(T) == 2, "wide tiles are half-precision");
+  static constexpr int BM = kGemmBM;
+  static constexpr int BN = WIDE ? 4 * kGemmBN : kGemmBN;
+  static constexpr int KC = WIDE ? 32 : MmaCfg<T>::KC;
+  static constexpr int LD = WIDE ? 40 : MmaCfg<T>::LD;
+  static constexpr int WAVES_M = WIDE ? 1 : 2, WAVES_N = WIDE ? 4 : 2;
+  static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+  static constexpr int IM = WM / 16, JN = WN / 16;
+  static constexpr int BLOCKS_PER_CU = WIDE ? 2 : 4;
+};
+
+// Reduction stages of a layer that hold real (not padding) columns, for
+// stages of KC columns.
+template <int KC>
+__device__ __forceinline__ int gemm_stages_kc(const ConvArgs& a) {
+  return min((int)a.ktot_p, (a.K * a.cin_p + KC - 1) / KC * KC) / KC;
 }
 
 // SPLIT: the layer's reduction may be split (split_max > 1); every unit
 // then writes its partial tile (even when this frame needs one split) and
 // the split epilogue finishes the tiles, so no epilogue state is held
-// through the reduction.
-// Four waves per SIMD (the persistent grid holds four blocks per CU):
-// the register budget is fixed at that occupancy.
-template <typename T, bool REF, bool ALIGNED, bool SPLIT, bool CHUNK>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
+// through the reduction.  (64-column tiles only.)
+// The register budget follows the blocks each CU holds: four waves per
+// SIMD for 64-column tiles, two for wide ones.
+template <typename T, bool REF, bool ALIGNED, bool SPLIT, bool CHUNK,
+          bool WIDE>
+__global__ __launch_bounds__(256)
+__attribute__((amdgpu_waves_per_eu(GemmTile<T, WIDE>::BLOCKS_PER_CU)))
 void k_conv_gemm(ConvArgs a) {
-  constexpr int BM = kGemmBM, BN = kGemmBN;
-  constexpr int KC = MmaCfg<T>::KC, LD = MmaCfg<T>::LD;
+  using G = GemmTile<T, WIDE>;
+  static_assert(!(WIDE && SPLIT), "wide tiles are not split");
+  constexpr int BM = G::BM, BN = G::BN;
+  constexpr int KC = G::KC, LD = G::LD;
+  constexpr int IM = G::IM, JN = G::JN;
   constexpr int VEC = 16 / (int)sizeof(T);
   constexpr int VPR = KC / VEC;           // 16-byte vectors per staged row
   constexpr int AV = BM * VPR / 256;      // A vectors per thread per stage
   constexpr int BV = BN * VPR / 256;      // B vectors per thread per stage
-  constexpr int CLD = BN + 4;             // f32 accumulator tile row
+  constexpr int NQ = BN / kGemmBN;        // 64-column quarters per tile
+  constexpr int CLD = kGemmBN + 4;        // f32 accumulator row (a quarter)
   constexpr size_t AB_BYTES = 2ull * (BM + BN) * LD * sizeof(T);
   constexpr size_t C_BYTES = (size_t)BM * CLD * sizeof(float);
+  static_assert(AV >= 1 && BV >= 1, "stage vectors");
   __shared__ __align__(16) char smem[AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES];
   __shared__ u64 s_kmask;
   __shared__ int s_last;
@@ -1185,7 +1256,7 @@ void k_conv_gemm(ConvArgs a) {
   __shared__ unsigned s_rmax[BM];
   extern __shared__ int s_nbr[];          // [K][BM]
   // LDS carve-up: A[2][BM][LD], B[2][BN][LD]; the f32 accumulator tile of
-  // the epilogue reuses the same bytes
+  // the epilogue (one 64-column quarter at a time) reuses the same bytes
   T* const sA = (T*)smem;
   T* const sB = (T*)smem + 2 * BM * LD;
   float* const Cs = (float*)smem;
@@ -1195,7 +1266,7 @@ void k_conv_gemm(ConvArgs a) {
   const T* zvec = (const T*)a.zero;
   const T* dskip = (const T*)a.dskip;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = WIDE ? 0 : wave >> 1, wn = WIDE ? wave : wave & 1;
   const int l16 = lane & 15, lg = lane >> 4;
   const int64_t nO = (int64_t)*a.nO;
   // row tiles: 64 rows each, or (chunk-state mode) aligned to site runs
@@ -1209,7 +1280,7 @@ void k_conv_gemm(ConvArgs a) {
   // reduction stages that hold real (not padding) columns; with ALIGNED
   // (cin_p a multiple of KC) every stage lies within one kernel offset and
   // offset k covers stages [k * spk, (k + 1) * spk)
-  const int nst = gemm_stages<T>(a);
+  const int nst = gemm_stages_kc<KC>(a);
   const int spk = ALIGNED ? cin_p / KC : 1;
   // work units: (split, tile) pairs, split-major, so that neighbouring
   // tiles of one split (which gather the same input rows) stay together
@@ -1224,7 +1295,8 @@ void k_conv_gemm(ConvArgs a) {
   const int xcd = blockIdx.x % kXcd;
   const int u_end = (int)min(nunits, (int64_t)(xcd + 1) * chunk);
   const int per_xcd = gridDim.x / kXcd;
-  // epilogue ownership: thread -> row em, columns [ec, ec + 16) of the tile
+  // epilogue ownership: thread -> row em, columns [ec, ec + 16) of a
+  // 64-column quarter
   const int em = tid >> 2, ec = (tid & 3) * 16;
 
   // run-aligned row tiles (chunk-state mode): a unit's bounds are fetched
@@ -1268,9 +1340,6 @@ void k_conv_gemm(ConvArgs a) {
       if (src >= 0) my |= 1ull << k;
     }
     if (my) atomicOr(&s_kmask, my);
-    bool hv[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) hv[h] = eok && n0 + ec + 8 * h < cout_p;
     __syncthreads();
     const u64 kmask = s_kmask;
     if (CHUNK && u + per_xcd < u_end) {
@@ -1385,48 +1454,46 @@ void k_conv_gemm(ConvArgs a) {
       }
     };
 
-    v4f acc[2][2];
+    v4f acc[IM][JN];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < IM; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < JN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
     auto compute = [&](int buf) {
-      const T* Ab = sA + buf * BM * LD;
-      const T* Bb = sB + buf * BN * LD;
+      const T* Ab = sA + buf * BM * LD + wm * G::WM * LD;
+      const T* Bb = sB + buf * BN * LD + wn * G::WN * LD;
       if constexpr (sizeof(T) == 4) {
 #pragma unroll
         for (int kk = 0; kk < KC; kk += 4) {
-          float af[2], bf[2];
+          float af[IM], bf[JN];
 #pragma unroll
-          for (int i = 0; i < 2; ++i)
-            af[i] = Ab[(wm * 32 + i * 16 + l16) * LD + kk + lg];
+          for (int i = 0; i < IM; ++i)
+            af[i] = Ab[(i * 16 + l16) * LD + kk + lg];
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
-            bf[j] = Bb[(wn * 32 + j * 16 + l16) * LD + kk + lg];
+          for (int j = 0; j < JN; ++j)
+            bf[j] = Bb[(j * 16 + l16) * LD + kk + lg];
 #pragma unroll
-          for (int i = 0; i < 2; ++i)
+          for (int i = 0; i < IM; ++i)
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
+            for (int j = 0; j < JN; ++j)
               acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
                   af[i], bf[j], acc[i][j], 0, 0, 0);
         }
       } else {
 #pragma unroll
         for (int kk = 0; kk < KC; kk += 32) {
-          uint4 av[2], bv[2];
+          uint4 av[IM], bv[JN];
 #pragma unroll
-          for (int i = 0; i < 2; ++i)
-            av[i] = *(const uint4*)(Ab + (wm * 32 + i * 16 + l16) * LD + kk +
-                                    8 * lg);
+          for (int i = 0; i < IM; ++i)
+            av[i] = *(const uint4*)(Ab + (i * 16 + l16) * LD + kk + 8 * lg);
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
-            bv[j] = *(const uint4*)(Bb + (wn * 32 + j * 16 + l16) * LD + kk +
-                                    8 * lg);
+          for (int j = 0; j < JN; ++j)
+            bv[j] = *(const uint4*)(Bb + (j * 16 + l16) * LD + kk + 8 * lg);
 #pragma unroll
-          for (int i = 0; i < 2; ++i) {
+          for (int i = 0; i < IM; ++i) {
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
+            for (int j = 0; j < JN; ++j) {
               if constexpr (__is_same(T, _Float16)) {
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
                     __builtin_bit_cast(v8h, av[i]),
@@ -1473,61 +1540,77 @@ void k_conv_gemm(ConvArgs a) {
       ib = id;
     }
 
-    // ---- fused epilogue.  The accumulator tile goes through LDS so that
-    // each thread finishes 16 contiguous columns of one row: full-width
-    // state loads/stores and 16-byte delta stores.  MFMA 16x16 block
-    // layout: D[row = 4*lg + r][col = l16].
+    // ---- fused epilogue.  The accumulator tile goes through LDS, one
+    // 64-column quarter at a time, so that each thread finishes 16
+    // contiguous columns of one row: full-width state loads/stores and
+    // 16-byte delta stores.  MFMA 16x16 block layout: D[row = 4*lg + r]
+    // [col = l16].  A 64-column tile is its own single quarter (the four
+    // waves' 32x32 sub-tiles); in a wide tile quarter q is wave q's.
     if (CHUNK && (tid & 3) == 0) s_rsk[em] = rsk;
-    __syncthreads();  // every wave is done reading the staged tiles
+    float rm_all = 0.f;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int q = 0; q < NQ; ++q) {
+      __syncthreads();  // staged tiles / the previous quarter are read
+      if (!WIDE || wave == q) {
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+        for (int i = 0; i < IM; ++i)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          Cs[(wm * 32 + i * 16 + 4 * lg + r) * CLD + wn * 32 + j * 16 + l16] =
-              acc[i][j][r];
-    __syncthreads();
-    const float* crow = Cs + em * CLD + ec;
-    if constexpr (SPLIT) {
-      // partial tile of split sp, reduced by the split epilogue
+          for (int j = 0; j < JN; ++j)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        if (!hv[h]) continue;
-        float v[8];
-        load8f(crow + 8 * h, v);
-        store8f(a.part + ((int64_t)sp * a.capO + eo) * cout_p + n0 + ec +
-                    8 * h,
-                v);
+            for (int r = 0; r < 4; ++r)
+              Cs[(wm * G::WM + i * 16 + 4 * lg + r) * CLD +
+                 (WIDE ? 0 : wn * G::WN) + j * 16 + l16] = acc[i][j][r];
       }
-    } else if constexpr (CHUNK) {
-      finish_chunk_tile<T>(a, Cs, CLD, s_run, m0, (int)(m1 - m0), n0,
-                           s_site, s_rsk, s_rmax);
-    } else {
-      auto load_v = [&](int h, float* v) { load8f(crow + 8 * h, v); };
-      auto load_po = [&](int h, float* po) {
-        if (REF) {
+      __syncthreads();
+      const int nq = n0 + q * kGemmBN;
+      const float* crow = Cs + em * CLD + ec;
+      bool hv[2];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) po[e] = 0.f;
-        } else {
-          state_load8(a.P, a.p16, (int64_t)epix * cout_p + n0 + ec + 8 * h,
-                      po);
-        }
-      };
-      auto load_sk = [&](int h, float* sk) {
-        if (rsk >= 0) {
-          Vec8<T>::load(dskip + (int64_t)rsk * cout_p + n0 + ec + 8 * h, sk);
-        } else {
+      for (int h = 0; h < 2; ++h) hv[h] = eok && nq + ec + 8 * h < cout_p;
+      if constexpr (SPLIT) {
+        // partial tile of split sp, reduced by the split epilogue
 #pragma unroll
-          for (int e = 0; e < 8; ++e) sk[e] = 0.f;
+        for (int h = 0; h < 2; ++h) {
+          if (!hv[h]) continue;
+          float v[8];
+          load8f(crow + 8 * h, v);
+          store8f(a.part + ((int64_t)sp * a.capO + eo) * cout_p + nq + ec +
+                      8 * h,
+                  v);
         }
-      };
-      with_act(a.act, [&](auto act_tag) {
-        finish_tile<T, REF, decltype(act_tag)::value>(
-            a, load_v, load_po, load_sk, hv, eo, eok, epix, m0, n0, ec,
-            tiles_n, m1, &s_last);
-      });
+      } else if constexpr (CHUNK) {
+        finish_chunk_tile<T>(a, Cs, CLD, s_run, m0, (int)(m1 - m0), nq,
+                             s_site, s_rsk, s_rmax, q == 0, q == NQ - 1);
+      } else {
+        auto load_v = [&](int h, float* v) { load8f(crow + 8 * h, v); };
+        auto load_po = [&](int h, float* po) {
+          if (REF) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) po[e] = 0.f;
+          } else {
+            state_load8(a.P, a.p16, (int64_t)epix * cout_p + nq + ec + 8 * h,
+                        po);
+          }
+        };
+        auto load_sk = [&](int h, float* sk) {
+          if (rsk >= 0) {
+            Vec8<T>::load(dskip + (int64_t)rsk * cout_p + nq + ec + 8 * h,
+                          sk);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) sk[e] = 0.f;
+          }
+        };
+        with_act(a.act, [&](auto act_tag) {
+          rm_all = fmaxf(rm_all,
+                         finish_cols<T, REF, decltype(act_tag)::value>(
+                             a, load_v, load_po, load_sk, hv, eo, epix, nq,
+                             ec));
+        });
+      }
     }
+    if constexpr (!SPLIT && !CHUNK)
+      finish_rows(a, rm_all, eo, eok, m0, tiles_n, m1, &s_last);
   }
 }
 
@@ -1605,34 +1688,65 @@ static void split_epi_t(hipStream_t s, int grid, const ConvArgs& a) {
     k_split_epi<T, false><<<grid, 256, 0, s>>>(a);
 }
 
-template <typename T, bool SPLIT>
+template <typename T, bool SPLIT, bool WIDE>
 static void gemm_t(hipStream_t s, int grid, size_t lds, const ConvArgs& a) {
-  const bool aligned = a.cin_p % MmaCfg<T>::KC == 0;
-  if (a.ref) {
+  const bool aligned = a.cin_p % GemmTile<T, WIDE>::KC == 0;
+  if constexpr (WIDE) {
+    // wide tiles: aligned chunk-state layers only (use_wide), never split
+    k_conv_gemm<T, false, true, false, true, true><<<grid, 256, lds, s>>>(a);
+  } else if (a.ref) {
     if (aligned)
-      k_conv_gemm<T, true, true, SPLIT, false><<<grid, 256, lds, s>>>(a);
+      k_conv_gemm<T, true, true, SPLIT, false, false><<<grid, 256, lds, s>>>(
+          a);
     else
-      k_conv_gemm<T, true, false, SPLIT, false><<<grid, 256, lds, s>>>(a);
+      k_conv_gemm<T, true, false, SPLIT, false, false><<<grid, 256, lds, s>>>(
+          a);
   } else if (!SPLIT && a.mode == kModeChunkState) {
     // the chunk-state epilogue has a build of its own
     if (aligned)
-      k_conv_gemm<T, false, true, false, true><<<grid, 256, lds, s>>>(a);
+      k_conv_gemm<T, false, true, false, true, false><<<grid, 256, lds, s>>>(
+          a);
     else
-      k_conv_gemm<T, false, false, false, true><<<grid, 256, lds, s>>>(a);
+      k_conv_gemm<T, false, false, false, true, false><<<grid, 256, lds, s>>>(
+          a);
   } else {
     if (aligned)
-      k_conv_gemm<T, false, true, SPLIT, false><<<grid, 256, lds, s>>>(a);
+      k_conv_gemm<T, false, true, SPLIT, false, false><<<grid, 256, lds, s>>>(
+          a);
     else
-      k_conv_gemm<T, false, false, SPLIT, false><<<grid, 256, lds, s>>>(a);
+      k_conv_gemm<T, false, false, SPLIT, false, false>
+          <<<grid, 256, lds, s>>>(a);
   }
 }
 
+// Wide (64 x 256) tiles for half-precision layers with a long reduction
+// over a window (K > 1, at least 512 input channels) whose padded width is
+// a multiple of 256, when the reduction is not split.  There the staged
+// operands dominate and the wide tile's reuse pays; layers whose time goes
+// to the epilogue's state traffic keep four 64-column blocks per CU, which
+// hide its load latency better (measured on ResNet-50: the wide tile
+// lowers the 3x3 512-channel layers by 15-23% and raises 1x1 layers).
+// (In the frame-by-frame and reference passes these layers split their
+// reduction instead, so the wide build is the chunk-state one.)
+static bool use_wide(int dtype, const ConvArgs& a) {
+  return dtype != 0 && a.mode == kModeChunkState && !a.ref &&
+         a.split_max <= 1 && a.cout_p % 256 == 0 && a.K > 1 &&
+         a.cin_p >= 512 && a.cin_p % GemmTile<bf16_t, true>::KC == 0;
+}
+
 template <typename T>
-static void gemm_t(hipStream_t s, int grid, size_t lds, const ConvArgs& a) {
+static void gemm_t(hipStream_t s, int grid, size_t lds, const ConvArgs& a,
+                   bool wide) {
+  if constexpr (sizeof(T) == 2) {
+    if (wide) {
+      gemm_t<T, false, true>(s, grid, lds, a);
+      return;
+    }
+  }
   if (a.split_max > 1)
-    gemm_t<T, true>(s, grid, lds, a);
+    gemm_t<T, true, false>(s, grid, lds, a);
   else
-    gemm_t<T, false>(s, grid, lds, a);
+    gemm_t<T, false, false>(s, grid, lds, a);
 }
 
 bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
@@ -1646,21 +1760,26 @@ bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
   if (a.tstart && (a.split_max > 1 || a.nf < 1 || a.nf > 32 || a.per < 1 ||
                    !a.sites))
     return false;
+  const bool wide = use_wide(dtype, a);
+  const int bn = wide ? GemmTile<bf16_t, true>::BN : kGemmBN;
+  const int per_cu = wide ? GemmTile<bf16_t, true>::BLOCKS_PER_CU
+                          : GemmTile<bf16_t, false>::BLOCKS_PER_CU;
   const int rstep = a.tstart ? chunk_tile_step(a.nf) : kGemmBM;
   const int64_t worst = ((a.capO + rstep - 1) / rstep) *
-                        ((a.cout_p + kGemmBN - 1) / kGemmBN);
+                        ((a.cout_p + bn - 1) / bn);
   // persistent blocks: about what the 256 CUs hold at once
   const int64_t units = worst * (a.split_max > 1 ? a.split_max : 1);
-  int64_t grid = units < 1024 ? units : 1024;
+  const int64_t resident = 256 * per_cu;
+  int64_t grid = units < resident ? units : resident;
   grid = (grid + kXcd - 1) / kXcd * kXcd;
   const size_t lds = sizeof(int) * (size_t)a.K * kGemmBM;
   prof_begin(pf, 7 /*ST_K_CONV_GEMM*/, s);
   if (dtype == 0)
-    gemm_t<float>(s, (int)grid, lds, a);
+    gemm_t<float>(s, (int)grid, lds, a, false);
   else if (dtype == 1)
-    gemm_t<_Float16>(s, (int)grid, lds, a);
+    gemm_t<_Float16>(s, (int)grid, lds, a, wide);
   else
-    gemm_t<bf16_t>(s, (int)grid, lds, a);
+    gemm_t<bf16_t>(s, (int)grid, lds, a, wide);
   prof_end(pf, 7, s);
   if (a.split_max > 1) {
     const int egrid = (int)(worst < 1024 ? worst : 1024);
@@ -2398,20 +2517,27 @@ void launch_chunk_scan(const Prof& pf, hipStream_t s, int dtype,
 // f(P_t) - f(P_{t-1}) and its max |delta|.  Pool mode: the rows get P_t
 // instead (the pool compares window states per frame) and the frames that
 // updated each site are recorded; the state is committed afterwards.
-// With `out` the dense output f(P) after every frame is written too.
 // CARRY (residual carry, not in pool mode): the site's consumers' view
 // stays in registers across the frames; frame t emits f(P_t) - view, and
 // if the row is kept (its largest rounded magnitude, over all the site's
 // channels -- one group of TPS lanes holds them all -- above the
 // threshold) the rounded delta joins the view.
-template <typename T, int TPS, bool GATE, bool CARRY>
+//
+// LIST: the sites are those of the affected list O (item = frame * npix +
+// site, site-major, so a site's frames are adjacent rows in frame order):
+// the group whose row opens a site's run walks the run, the others return;
+// untouched sites are not read.  Otherwise (the output layer, whose dense
+// output f(P) after every frame is written to `out` for every site) every
+// conv site is visited and its rows are found through the map Mo.
+template <typename T, int TPS, bool GATE, bool CARRY, bool LIST>
 __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
   constexpr int R = 256 / TPS, IT = TPS == 64 ? 4 : 1;
   T* dout = (T*)a.dout;
   const int lane = threadIdx.x % TPS;
-  const int64_t p = (int64_t)blockIdx.x * R + threadIdx.x / TPS;
-  if (p >= a.npix) return;
   const int cp = a.cp, V = cp / 8;
+  const uint32_t pu = (uint32_t)a.npix;
+  // site p; LIST: j0 is the first row of its run
+  auto site_work = [&](int64_t p, int64_t j0) {
   float pv[IT][8], yh[IT][8];
 #pragma unroll
   for (int k = 0; k < IT; ++k) {
@@ -2422,91 +2548,103 @@ __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
   const float kthr =
       CARRY ? (a.keep_thr_dev ? *a.keep_thr_dev : a.keep_thr) : 0.f;
   uint32_t bits = 0;
-  for (int t = 0; t < a.nf; ++t) {
-    const int r = a.Mo[(int64_t)t * a.npix + p];
-    if (r >= 0) {
-      bits |= 1u << t;
-      float rm = 0.f;
-      float dr[IT][8];  // the rounded deltas (residual carry)
+  // one frame's row r of this site
+  auto apply = [&](int t, int64_t r) {
+    bits |= 1u << t;
+    float rm = 0.f;
+    float dr[IT][8];  // the rounded deltas (residual carry)
 #pragma unroll
-      for (int k = 0; k < IT; ++k) {
-        const int v = lane + k * TPS;
-        if (v < V) {
-          float dp[8], pn[8];
-          float* row = a.dP + (int64_t)r * cp + v * 8;
-          load8f(row, dp);
+    for (int k = 0; k < IT; ++k) {
+      const int v = lane + k * TPS;
+      if (v < V) {
+        float dp[8], pn[8];
+        float* row = a.dP + r * cp + v * 8;
+        load8f(row, dp);
 #pragma unroll
-          for (int e = 0; e < 8; ++e)
-            pn[e] = state_round(a.p16, pv[k][e] + dp[e]);
-          if (a.pool_mode) {
-            store8f(row, pn);
-          } else {
-            float d[8];
-            if constexpr (GATE) {
-              // frozen squeeze-excitation: both values scaled by the gates
-              float g[8];
-              load8f(gate_slot(a.gate, a.gpar, a.gsz, 0) +
-                         (p / a.gate_hw) * cp + v * 8,
-                     g);
+        for (int e = 0; e < 8; ++e)
+          pn[e] = state_round(a.p16, pv[k][e] + dp[e]);
+        if (a.pool_mode) {
+          store8f(row, pn);
+        } else {
+          float d[8];
+          if constexpr (GATE) {
+            // frozen squeeze-excitation: both values scaled by the gates
+            float g[8];
+            load8f(gate_slot(a.gate, a.gpar, a.gsz, 0) +
+                       (p / a.gate_hw) * cp + v * 8,
+                   g);
 #pragma unroll
-              for (int e = 0; e < 8; ++e)
-                d[e] = act_f(pn[e], a.act) * g[e] -
-                       act_f(pv[k][e], a.act) * g[e];
-            } else if constexpr (CARRY) {
+            for (int e = 0; e < 8; ++e)
+              d[e] = act_f(pn[e], a.act) * g[e] -
+                     act_f(pv[k][e], a.act) * g[e];
+          } else if constexpr (CARRY) {
 #pragma unroll
-              for (int e = 0; e < 8; ++e) {
-                d[e] = act_f(pn[e], a.act) - yh[k][e];
-                dr[k][e] = to_f(from_f<T>(d[e]));
-              }
-            } else {
-#pragma unroll
-              for (int e = 0; e < 8; ++e)
-                d[e] = act_f(pn[e], a.act) - act_f(pv[k][e], a.act);
+            for (int e = 0; e < 8; ++e) {
+              d[e] = act_f(pn[e], a.act) - yh[k][e];
+              dr[k][e] = to_f(from_f<T>(d[e]));
             }
-            rm = fmaxf(rm, Vec8<T>::store(dout + (int64_t)r * cp + v * 8, d));
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              d[e] = act_f(pn[e], a.act) - act_f(pv[k][e], a.act);
           }
-#pragma unroll
-          for (int e = 0; e < 8; ++e) pv[k][e] = pn[e];
+          rm = fmaxf(rm, Vec8<T>::store(dout + r * cp + v * 8, d));
         }
-      }
-      if (!a.pool_mode) {
 #pragma unroll
-        for (int o = 1; o < TPS; o <<= 1)
-          rm = fmaxf(rm, __shfl_xor(rm, o, 64));
-        if (lane == 0) a.rowmax[r] = __float_as_uint(rm);
-        if (CARRY && rm > kthr) {
-          // kept: the consumers receive the rounded delta
-#pragma unroll
-          for (int k = 0; k < IT; ++k)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) yh[k][e] += dr[k][e];
-        }
+        for (int e = 0; e < 8; ++e) pv[k][e] = pn[e];
       }
     }
-    if (a.out) {
-      float* o = a.out + ((int64_t)t * a.npix + p) * a.c;
+    if (!a.pool_mode) {
 #pragma unroll
-      for (int k = 0; k < IT; ++k) {
-        const int v = lane + k * TPS;
-        if (v < V && (a.c & 7) == 0 && ((uintptr_t)a.out & 15) == 0) {
-          // whole 8-channel vectors (rows of c floats, c a multiple of 8,
-          // on a 16-byte aligned output)
-          if (v * 8 < a.c) {
-            float f[8];
+      for (int o = 1; o < TPS; o <<= 1) rm = fmaxf(rm, __shfl_xor(rm, o, 64));
+      if (lane == 0) a.rowmax[r] = __float_as_uint(rm);
+      if (CARRY && rm > kthr) {
+        // kept: the consumers receive the rounded delta
 #pragma unroll
-            for (int e = 0; e < 8; ++e) f[e] = act_f(pv[k][e], a.act);
-            store8f(o + v * 8, f);
+        for (int k = 0; k < IT; ++k)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) yh[k][e] += dr[k][e];
+      }
+    }
+  };
+  if constexpr (LIST) {
+    const int64_t nO = (int64_t)*a.nO;
+    for (int64_t r = j0; r < nO; ++r) {
+      const uint32_t it = (uint32_t)a.O[r];
+      if ((int64_t)(it % pu) != p) break;
+      apply((int)(it / pu), r);
+    }
+  } else {
+    for (int t = 0; t < a.nf; ++t) {
+      const int r = a.Mo[(int64_t)t * a.npix + p];
+      if (r >= 0) apply(t, r);
+      if (a.out) {
+        float* o = a.out + ((int64_t)t * a.npix + p) * a.c;
+#pragma unroll
+        for (int k = 0; k < IT; ++k) {
+          const int v = lane + k * TPS;
+          if (v < V && (a.c & 7) == 0 && ((uintptr_t)a.out & 15) == 0) {
+            // whole 8-channel vectors (rows of c floats, c a multiple of
+            // 8, on a 16-byte aligned output)
+            if (v * 8 < a.c) {
+              float f[8];
+#pragma unroll
+              for (int e = 0; e < 8; ++e) f[e] = act_f(pv[k][e], a.act);
+              store8f(o + v * 8, f);
+            }
+          } else if (v < V) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (v * 8 + e < a.c) o[v * 8 + e] = act_f(pv[k][e], a.act);
           }
-        } else if (v < V) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (v * 8 + e < a.c) o[v * 8 + e] = act_f(pv[k][e], a.act);
         }
       }
     }
   }
   if (a.pool_mode) {
-    if (lane == 0) a.aff[p] = bits;
+    // LIST: only touched sites get bits; the others stay 0 (the commit
+    // clears what it consumed)
+    if (lane == 0 && (!LIST || bits)) a.aff[p] = bits;
   } else if (bits) {
 #pragma unroll
     for (int k = 0; k < IT; ++k) {
@@ -2514,6 +2652,27 @@ __global__ __launch_bounds__(256) void k_chunk_update(ChunkUpdArgs a) {
       if (v < V) state_store8(a.P, a.p16, p * cp + v * 8, pv[k]);
       if (CARRY && v < V) store8f(a.yhat + p * cp + v * 8, yh[k]);
     }
+  }
+  };
+  if constexpr (LIST) {
+    // every group of TPS lanes strides over the rows; a row's group works
+    // only if the row opens its site's run (all lanes of a group agree).
+    // The sites are counted (one atomic per block).
+    const int64_t nO = (int64_t)*a.nO;
+    unsigned nsites = 0;
+    for (int64_t j = (int64_t)blockIdx.x * R + threadIdx.x / TPS; j < nO;
+         j += (int64_t)gridDim.x * R) {
+      const int64_t p = (int64_t)((uint32_t)a.O[j] % pu);
+      if (j > 0 && (int64_t)((uint32_t)a.O[j - 1] % pu) == p) continue;
+      site_work(p, j);
+      nsites += lane == 0 ? 1u : 0u;
+    }
+    nsites = block_sum(nsites);
+    if (threadIdx.x == 0 && nsites && a.sites)
+      atomicAdd(a.sites + blockIdx.x % kSiteSlots, (u64)nsites);
+  } else {
+    const int64_t p = (int64_t)blockIdx.x * R + threadIdx.x / TPS;
+    if (p < a.npix) site_work(p, 0);
   }
 }
 
@@ -2636,35 +2795,55 @@ __global__ __launch_bounds__(256) void k_chunk_pool_emit(ChunkPoolArgs a) {
   }
 }
 
+// P[w] = P after the last frame that updated w, for the sites of the
+// affected list O (run openers; 4 channels per thread of a group of cp / 4
+// threads), and the site's frame bits cleared for the next pooled layer.
 __global__ __launch_bounds__(256) void k_chunk_commit(float* P,
                                                       const float* Pt,
-                                                      const int* Mo,
-                                                      const uint32_t* aff,
+                                                      const int* O,
+                                                      const u64* nOp,
+                                                      uint32_t* aff,
                                                       int64_t nconv, int cp) {
   const int c4 = cp / 4;
-  const int64_t total = nconv * c4;
+  const int64_t nO = (int64_t)*nOp;
+  const int64_t total = nO * c4;
+  const uint32_t pu = (uint32_t)nconv;
   for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
        idx += (int64_t)gridDim.x * 256) {
-    const int64_t w = idx / c4;
-    const uint32_t b = aff[w];
-    if (!b) continue;
-    const int tl = 31 - __clz((int)b);
-    const int r = Mo[(int64_t)tl * nconv + w];
-    const int c = (int)(idx - w * c4) * 4;
-    *(float4*)(P + w * cp + c) = *(const float4*)(Pt + (int64_t)r * cp + c);
+    const int64_t j = idx / c4;
+    const int c = (int)(idx - j * c4) * 4;
+    const uint32_t w = (uint32_t)O[j] % pu;
+    if (j > 0 && (uint32_t)O[j - 1] % pu == w) continue;  // not the opener
+    // the run's last row holds the state after its last frame
+    int64_t r = j;
+    while (r + 1 < nO && (uint32_t)O[r + 1] % pu == w) ++r;
+    *(float4*)(P + (int64_t)w * cp + c) =
+        *(const float4*)(Pt + r * cp + c);
+    if (c == 0) aff[w] = 0u;
   }
 }
 
+template <typename T, int TPS, bool LIST>
+static void chunk_upd_t(hipStream_t s, const ChunkUpdArgs& a, int grid) {
+  if (a.gate)
+    k_chunk_update<T, TPS, true, false, LIST><<<grid, 256, 0, s>>>(a);
+  else if (a.yhat && !a.pool_mode)
+    k_chunk_update<T, TPS, false, true, LIST><<<grid, 256, 0, s>>>(a);
+  else
+    k_chunk_update<T, TPS, false, false, LIST><<<grid, 256, 0, s>>>(a);
+}
+
+// Without a dense output the update walks the affected list (a group per
+// row, its run's opener working); with one, every conv site.
 template <typename T, int TPS>
 static void chunk_upd_t(hipStream_t s, const ChunkUpdArgs& a) {
   constexpr int R = 256 / TPS;
-  const int grid = (int)((a.npix + R - 1) / R);
-  if (a.gate)
-    k_chunk_update<T, TPS, true, false><<<grid, 256, 0, s>>>(a);
-  else if (a.yhat && !a.pool_mode)
-    k_chunk_update<T, TPS, false, true><<<grid, 256, 0, s>>>(a);
-  else
-    k_chunk_update<T, TPS, false, false><<<grid, 256, 0, s>>>(a);
+  if (a.out) {
+    chunk_upd_t<T, TPS, false>(s, a, (int)((a.npix + R - 1) / R));
+  } else {
+    const int64_t cap = a.npix * a.nf;
+    chunk_upd_t<T, TPS, true>(s, a, grid_for(cap * TPS, 8192));
+  }
 }
 
 template <typename T>
@@ -2728,11 +2907,11 @@ void launch_chunk_pool_emit(const Prof& pf, hipStream_t s, int dtype,
 }
 
 void launch_chunk_commit(const Prof& pf, hipStream_t s, float* P,
-                         const float* Pt, const int* Mo, const uint32_t* aff,
-                         int64_t nconv, int cp) {
+                         const float* Pt, const int* O, const u64* nO,
+                         uint32_t* aff, int64_t capO, int64_t nconv, int cp) {
   prof_begin(pf, 13 /*ST_K_COMMIT*/, s);
-  k_chunk_commit<<<grid_for(nconv * (cp / 4), 8192), 256, 0, s>>>(
-      P, Pt, Mo, aff, nconv, cp);
+  k_chunk_commit<<<grid_for(capO * (cp / 4), 8192), 256, 0, s>>>(
+      P, Pt, O, nO, aff, nconv, cp);
   prof_end(pf, 13, s);
 }
 
