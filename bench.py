@@ -679,11 +679,19 @@ def kernel_table(net, recs, counts, es, chunk_mode=False, nf=1):
             seen.add((name, f))
             n0 = int(counts[f, 0, 2]) if net.layers[0].src == -1 else 0
             C, Cp = net.C, (net.C + 7) // 8 * 8
-            # keep bytes read; per kept item its frame and reference value
-            # read, the delta row and list, map entries written; X_hat
-            # committed at the changed sites (bounded by the kept items)
-            c["bytes"] += n_in * nf + n0 * (2 * C * es + Cp * es + 12) + \
-                min(n0, n_in) * 2 * C * es
+            if chunk_mode:
+                # keep bytes read; per kept item its frame and reference
+                # value read, the delta row and list, map entries written;
+                # X_hat committed at the changed sites (bounded by the kept
+                # items)
+                c["bytes"] += n_in * nf + n0 * (2 * C * es + Cp * es + 12) \
+                    + min(n0, n_in) * 2 * C * es
+            else:
+                # frame and X_hat read at every site (the mask); per kept
+                # pixel the delta row and list, map entries written and
+                # X_hat committed
+                c["bytes"] += n_in * 2 * C * es + n0 * (Cp * es + 12 +
+                                                        C * es)
     return classes
 
 

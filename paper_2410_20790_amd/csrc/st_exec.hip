@@ -191,7 +191,6 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
   TensorPlan& out = net->tensors[i + 1];
   u64* cnt = ws.at<u64>(net->off_cnt);
   uint32_t* tiles = ws.at<uint32_t>(net->off_tiles);
-  uint32_t* grp = ws.at<uint32_t>(net->off_grp);
   const Prof pf{net, i};
 
   int* O = ws.at<int>(L.off_O);
@@ -224,7 +223,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
     fa.g = conv_geo(L);
     fa.pairs = cpairs;
     fa.cnt = cO;
-    launch_flag_compact(pf, ST_K_RB_COUNT, ST_K_RB_COMPACT, s, fa);
+    launch_flag_compact(pf, ST_K_RB_COMPACT, s, fa);
   }
 
   // (c) delta convolution with fused (d) update / emission
@@ -254,14 +253,12 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
   a.mode = frozen ? kModeState : L.mode;
   a.act = d.act;
   a.ref = ref ? 1 : 0;
-  a.grp = (L.pool || L.dw || own_rows) ? nullptr : grp;
   if (frozen) {
     a.gate = ws.at<float>(L.off_ses);
     a.gpar = ws.at<int>(net->off_se_par);
     a.gsz = (int64_t)net->N * L.cout_p;
     a.gate_hw = (int64_t)L.Ho * L.Wo;
   }
-  a.mdone = ws.at<uint32_t>(net->off_mdone);
   a.keep_thr = thr;
   a.keep_thr_dev = thr_dev;
   a.yhat = net->carry && !own_rows ? ws.at<float>(L.off_yhat) : nullptr;
@@ -287,7 +284,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
     fp.map = ws.at<int>(out.off_map);
     fp.rowmax = rowmax_out;
     fp.cnt = cnt + out.cnt_rows;
-    launch_flag_compact(pf, ST_K_POOL_COUNT, ST_K_POOL_COMPACT, s, fp);
+    launch_flag_compact(pf, ST_K_POOL_COMPACT, s, fp);
     PoolArgs pa{};
     pa.Q = ws.at<int>(out.off_rowpix);
     pa.nQ = cnt + out.cnt_rows;
@@ -325,11 +322,9 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
     sa.rowmax = rowmax_out;
     sa.rowpix = ws.at<int>(out.off_rowpix);
     sa.map = ws.at<int>(out.off_map);
-    sa.grp = grp;
     sa.cnt_rows = cnt + out.cnt_rows;
     sa.npix = L.conv_grid;
     sa.hw = (int64_t)L.Ho * L.Wo;
-    sa.ngrp = L.conv_grid / 64 + 1;
     sa.tps = L.se_tps;
     sa.N = net->N;
     sa.cp = L.cout_p;
@@ -344,9 +339,6 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
     sa.yhat = net->carry ? ws.at<float>(L.off_yhat) : nullptr;
     launch_se(pf, s, net->dtype, sa);
   }
-  if ((L.pool || L.dw) && !(L.se && !frozen))
-    launch_group_count(pf, s, rowmax_out, cnt + out.cnt_rows, out.grid,
-                       thr, thr_dev, grp);
 
   // truncation of the emitted delta (shared by every consumer), which also
   // prepares the consumers' rulebooks
@@ -359,7 +351,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
   la.rowpix = ws.at<int>(out.off_rowpix);
   la.act = ws.at<int>(out.off_act);
   la.map = ws.at<int>(out.off_map);
-  la.grp = grp;
+  la.tiles = tiles;
   la.cnt_act = cnt + out.cnt_act;
   la.cons = consumers_of(net, i + 1);
   launch_list_compact(pf, s, la);
@@ -406,7 +398,6 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
   sa.thr = thr0;
   sa.thr_dev = thr_dev;
   sa.ref = ref ? 1 : 0;
-  sa.keep = ws.at<uint8_t>(net->off_flags);
   sa.tiles = ws.at<uint32_t>(net->off_tiles);
   sa.rows = ws.at<char>(T0.off_rows);
   sa.rowpix = ws.at<int>(T0.off_rowpix);
@@ -487,7 +478,6 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   TensorPlan& outT = net->tensors[i + 1];
   u64* cnt = ws.at<u64>(net->off_cnt);
   uint32_t* tiles = ws.at<uint32_t>(net->off_tiles);
-  uint32_t* grp = ws.at<uint32_t>(net->off_grp);
   const Prof pf{net, i};
   const int64_t citems = L.conv_grid * nf;
   const int64_t stride = L.conv_grid * net->F;
@@ -527,7 +517,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
       fa.tstart = tstart;
       tiles_cut = true;
     }
-    launch_flag_compact(pf, ST_K_RB_COUNT, ST_K_RB_COMPACT, s, fa);
+    launch_flag_compact(pf, ST_K_RB_COMPACT, s, fa);
   }
   if (fused && !tiles_cut)
     launch_run_tiles(pf, s, O, cO, citems, L.conv_grid, nf, tstart);
@@ -563,7 +553,6 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
     a.mode = kModeLinear;
     a.dout = ws.at<char>(outT.off_rows);
     a.rowmax = rowmax_out;
-    a.grp = grp;
   }
   if (d.residual_src != -2) {
     const TensorPlan& R = net->tensors[d.residual_src + 1];
@@ -572,7 +561,6 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   }
   a.act = d.act;
   a.ref = 0;
-  a.mdone = ws.at<uint32_t>(net->off_mdone);
   a.keep_thr = thr;
   a.keep_thr_dev = thr_dev;
   a.zero = ws.at<char>(net->off_zero);
@@ -631,7 +619,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
     fp.cnt = cnt + outT.cnt_rows;
     fp.nf = nf;
     fp.per = outT.grid;
-    launch_flag_compact(pf, ST_K_POOL_COUNT, ST_K_POOL_COMPACT, s, fp);
+    launch_flag_compact(pf, ST_K_POOL_COMPACT, s, fp);
     ChunkPoolArgs pa{};
     pa.Q = ws.at<int>(outT.off_rowpix);
     pa.nQ = cnt + outT.cnt_rows;
@@ -658,9 +646,6 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
                         ws.at<uint32_t>(net->off_chunk_aff), citems,
                         L.conv_grid, L.cout_p);
   }
-  if (L.stateful)
-    launch_group_count(pf, s, rowmax_out, cnt + outT.cnt_rows,
-                       outT.grid * nf, thr, thr_dev, grp);
 
   ListArgs la{};
   la.rowmax = rowmax_out;
@@ -671,7 +656,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   la.rowpix = ws.at<int>(outT.off_rowpix);
   la.act = ws.at<int>(outT.off_act);
   la.map = ws.at<int>(outT.off_map);
-  la.grp = grp;
+  la.tiles = tiles;
   la.cnt_act = cnt + outT.cnt_act;
   la.cons = consumers_of(net, i + 1, true);
   launch_list_compact(pf, s, la);

@@ -17,7 +17,7 @@ namespace st {
 constexpr int kChanAlign = 8;       // delta rows / weights padded to 8 channels
 constexpr int kMaxChunkFrames = 32; // diff frames per chunk (frame bit masks)
 constexpr int kChunkMaxInC = 16;    // input channels of a chunk's frame scan
-constexpr int kMaxTiles = 4096;     // compaction tiles per pass
+constexpr int kMaxTiles = kCompactMaxTiles;  // compaction tiles per pass
 constexpr int64_t kMaxGrid = (int64_t)kMaxTiles * 8192;  // sites per grid
 constexpr size_t kAlign = 256;      // workspace sub-buffer alignment
 
@@ -114,9 +114,7 @@ struct st_net {
   size_t ws_bytes = 0;
   size_t off_xhat = 0;                     // storage dtype [N*H*W*C]
   size_t off_flags = 0;                    // uint8 [input grid] keep bytes
-  size_t off_tiles = 0;                    // uint32 [kMaxTiles]
-  size_t off_grp = 0;                      // uint32 [max grid / 64 + 1]
-  size_t off_mdone = 0;                    // uint32 [max grid / 64 + 1]
+  size_t off_tiles = 0;                    // uint32 [kMaxTiles + 64]
   size_t off_zero = 0;                     // 256 zero bytes
   size_t off_part = 0;                     // f32 split partials (shared)
   // online threshold adjustment, per produced tensor

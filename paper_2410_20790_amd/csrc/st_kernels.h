@@ -73,8 +73,7 @@ struct ScanArgs {
   float thr;
   const float* thr_dev;  // threshold in device memory (or NULL: thr)
   int ref;
-  uint8_t* keep;
-  uint32_t* tiles;
+  uint32_t* tiles;     // look-back statuses of the compaction
   void* rows;
   int* rowpix;
   int* act;
@@ -110,8 +109,8 @@ struct FlagArgs {
   uint32_t* tstart;
 };
 bool compact_runs_fit(int64_t cap, int run);
-void launch_flag_compact(const Prof& pf, int cls_count, int cls_write,
-                         hipStream_t s, const FlagArgs& a);
+void launch_flag_compact(const Prof& pf, int cls, hipStream_t s,
+                         const FlagArgs& a);
 // flags: site-major (site * nf + frame) over nf frames of nimg images.
 void launch_mark(const Prof& pf, int cls, hipStream_t s, const int* list,
                  const u64* n_list, int64_t max_items, Geo g, uint8_t* flags,
@@ -143,8 +142,6 @@ struct ConvArgs {
   const void* dskip;   // residual delta rows [*, cout_p] or NULL
   const int* mskip;    // residual pixel -> row map
   int mode, act, ref;
-  uint32_t* grp;       // per-64-row kept counts (or NULL)
-  uint32_t* mdone;     // per-row-tile arrival counters (zero between uses)
   float keep_thr;      // threshold of the emitted tensor
   const float* keep_thr_dev;  // in device memory (or NULL: keep_thr)
   const void* zero;    // 16 zero bytes (16-byte aligned)
@@ -208,14 +205,11 @@ struct ListArgs {
   const int* rowpix;
   int* act;
   int* map;
-  const uint32_t* grp;   // per-64-row kept counts
+  uint32_t* tiles;       // look-back statuses of the compaction
   u64* cnt_act;
   ConsList cons;
 };
 void launch_list_compact(const Prof& pf, hipStream_t s, const ListArgs& a);
-void launch_group_count(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
-                        const u64* n_rows, int64_t cap, float thr,
-                        const float* thr_dev, uint32_t* grp);
 
 // ---- squeeze-excitation on a deferred layer
 struct SeArgs {
@@ -237,9 +231,8 @@ struct SeArgs {
   uint32_t* rowmax;
   int* rowpix;
   int* map;
-  uint32_t* grp;       // per-64-site kept counts (zeroed by the squeeze)
   u64* cnt_rows;
-  int64_t npix, hw, ngrp;
+  int64_t npix, hw;
   int N, cp, c, mid, act, ref, chunk, nchunk, tps;
   float keep_thr;
   const float* keep_thr_dev;  // in device memory (or NULL: keep_thr)

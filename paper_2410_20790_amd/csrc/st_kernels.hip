@@ -109,30 +109,34 @@ __device__ __forceinline__ int64_t read_count(const u64* dev, int64_t host) {
 }
 
 // ============================================================ compaction
-// Ascending stream compaction.  Items are split into tiles of `tile`
-// consecutive indices (at most 256 * kMaxItemsPerThread).  The write pass
-// derives each tile's output offset from per-tile or per-64-item-group
-// counts of the items before it -- counted by a separate pass, or by the kernel that
-// produced the items -- and writes the kept items in order, using a wave
-// ballot and mbcnt for the in-wave prefix and LDS for the cross-wave prefix.
-// The block that owns the last item writes the total.
-template <class P>
-__global__ __launch_bounds__(256) void k_compact_count(const u64* n_dev,
-                                                       int64_t n_host,
-                                                       int tile,
-                                                       uint32_t* tile_cnt,
-                                                       P pred) {
-  const int64_t n = read_count(n_dev, n_host);
-  const int64_t base = (int64_t)blockIdx.x * tile;
-  if (base >= n) return;
-  const int64_t end = min(base + (int64_t)tile, n);
-  unsigned c = 0;
-  for (int64_t i = base + threadIdx.x; i < end; i += 256)
-    c += pred.count(i) ? 1u : 0u;
-  c = block_sum(c);
-  if (threadIdx.x == 0) tile_cnt[blockIdx.x] = c;
-}
-
+// Ascending stream compaction in one pass.  Items are split into tiles of
+// `tile` consecutive indices (at most 256 * kMaxItemsPerThread), one block
+// per tile.  Each thread owns ceil(tile / 256) consecutive items and
+// evaluates them; one block scan gives every kept item its position in the
+// tile.  The tile's offset in the output comes from the tiles before it,
+// in the same launch: a tile publishes its own count as soon as it has
+// evaluated its items, then sums the published counts of its predecessors
+// (lookback_offset).  Blocks are dispatched in index order, so every tile a
+// block waits for has been dispatched before it, and it publishes without
+// waiting on anything.  The statuses start at zero; the last live block to
+// finish clears them (and its arrival counter) for the next compaction.
+//
+// The predicate's item data (P::Item, from P::load) is requested together
+// with the item count -- all loads stay within the capacity `cap`, and which
+// items are real is decided once the count has arrived.  With IPT > 0
+// (items per thread known at compile time) the items are kept in registers
+// until the keep decision.  Dropped items are handed to pred.drop by their
+// owner; the kept ones are listed in LDS in position order and emitted by
+// the whole block, consecutive threads taking consecutive positions, so
+// every lane of a wave runs an emit (emits are the expensive part: rows
+// gathered, windows marked, neighbour tables built) and their stores are
+// contiguous.  pred.emit re-loads its item (predicates whose emit ignores
+// the item let the compiler drop that load); it returns a work count that
+// is summed over the block and handed to pred.block_done; pred.finish
+// receives the total.
+constexpr int kMaxItemsPerThread = 32;
+constexpr uint32_t kLbAgg = 1u << 30;  // status: the tile's count is set
+constexpr uint32_t kLbVal = kLbAgg - 1;
 // Exclusive prefix of a per-thread count over a 256-thread block (wave
 // scan with DPP-free shuffles, wave totals through LDS); also returns the
 // block total.
@@ -159,24 +163,10 @@ __device__ __forceinline__ unsigned block_exclusive_scan(unsigned v,
   return wpre + incl - v;
 }
 
-// cnts: `per_tile` counts per tile (1 = per-tile counts, tile/64 = counts of
-// 64-item groups).  Each thread owns ceil(tile / 256) consecutive items of
-// the tile and evaluates them; one block scan gives every kept item its
-// position.  The predicate's item data (P::Item, from P::load) and the
-// first 256 counts before the tile are requested together with the item
-// count -- all loads stay within the capacity `cap` and the count buffer,
-// and which items are real is decided once the count has arrived -- and a
-// live block then sums the rest of the counts before its tile.  With IPT > 0 (items per thread known at compile time) the items
-// are kept in registers until the keep decision.  Dropped items are handed
-// to pred.drop by their owner; the kept ones are listed in LDS in position
-// order and emitted by the whole block, consecutive threads taking
-// consecutive positions, so every lane of a wave runs an emit (emits are
-// the expensive part: rows gathered, windows marked, neighbour tables
-// built) and their stores are contiguous.  pred.emit re-loads its item
-// (predicates whose emit ignores the item let the compiler drop that
-// load); it returns a work count that is summed over the block and handed
-// to pred.block_done; pred.finish receives the total.
-constexpr int kMaxItemsPerThread = 32;
+// Bound on a look-back wait, in sleeps of ~128 cycles (~1 s in all): a
+// wait never runs that long, as the waited-for tile is already dispatched;
+// the bound only guarantees that every wave exits.
+constexpr int kLbSpinLimit = 1 << 23;
 
 // Predicates with P::kRanked cut run-aligned row tiles while they emit: the
 // items form runs of pred.run_len() consecutive indices (a chunk's frames of
@@ -188,19 +178,56 @@ struct IsRanked : std::false_type {};
 template <class P>
 struct IsRanked<P, std::void_t<decltype(P::kRanked)>> : std::true_type {};
 
+// Exclusive output offset of tile t of this block (every thread of the
+// block must call it; all receive it): publishes the tile's count in
+// status[t], then sums the counts of all the tiles before it, which the
+// block's threads read side by side (each thread every 256th tile), waiting
+// only for counts not yet published.  A tile publishes its count as soon
+// as it has evaluated its items, before it waits for anything, so no wait
+// depends on another (a chain of published prefixes would make the last
+// tile wait for every earlier one in turn).
+__device__ __forceinline__ unsigned lookback_offset(uint32_t* status,
+                                                    unsigned t,
+                                                    unsigned count) {
+  if (threadIdx.x == 0)
+    __hip_atomic_store(status + t, kLbAgg | count, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  // all of this thread's statuses are requested at once (one round trip),
+  // then any not yet published is polled again
+  constexpr int Q = kCompactMaxTiles / 256;
+  uint32_t v[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const unsigned j = threadIdx.x + 256u * q;
+    v[q] = j < t ? __hip_atomic_load(status + j, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT)
+                 : kLbAgg;
+  }
+  unsigned sum = 0;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const unsigned j = threadIdx.x + 256u * q;
+    for (int spins = 0; v[q] == 0u && spins < kLbSpinLimit; ++spins) {
+      __builtin_amdgcn_s_sleep(2);
+      v[q] = __hip_atomic_load(status + j, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+    }
+    sum += v[q] & kLbVal;
+  }
+  return block_sum(sum);
+}
+
 template <class P, int IPT>
-__global__ __launch_bounds__(256) void k_compact_write(
-    const u64* n_dev, int64_t n_host, int64_t cap, int tile,
-    const uint32_t* cnts, int per_tile, u64* out_cnt, u64* out_cnt2,
-    P pred) {
+__global__ __launch_bounds__(256) void k_compact(const u64* n_dev,
+                                                 int64_t n_host, int64_t cap,
+                                                 int tile, uint32_t* status,
+                                                 uint32_t* done, u64* out_cnt,
+                                                 u64* out_cnt2, P pred) {
   using Item = typename P::Item;
   // tile offsets of the kept items (tile <= kMaxItemsPerThread * 256)
   __shared__ uint16_t kept[kMaxItemsPerThread * 256];
+  __shared__ int s_clear;
   const int64_t base = (int64_t)blockIdx.x * tile;
-  const int64_t n_req = read_count(n_dev, n_host);
-  // the first 256 counts before the tile are requested with the count
-  const unsigned nprev = blockIdx.x * (unsigned)per_tile;
-  unsigned off = threadIdx.x < nprev ? cnts[threadIdx.x] : 0u;
   const int ipt = IPT > 0 ? IPT : (tile + 255) / 256;
   const int64_t first = base + (int64_t)threadIdx.x * ipt;
   Item it[IPT > 0 ? IPT : 1];
@@ -209,7 +236,7 @@ __global__ __launch_bounds__(256) void k_compact_write(
     for (int j = 0; j < IPT; ++j)
       if (first + j < cap) it[j] = pred.load(first + j);
   }
-  const int64_t n = n_req;
+  const int64_t n = read_count(n_dev, n_host);
   if (base >= n) {
     if (blockIdx.x == 0 && threadIdx.x == 0) {
       *out_cnt = 0;
@@ -218,11 +245,6 @@ __global__ __launch_bounds__(256) void k_compact_write(
     }
     return;
   }
-  // the rest of the counts before the tile, read once the tile is known
-  // to be live (a capacity-sized grid has many blocks past the count, and
-  // summing a whole prefix in each of them would cost a quadratic number
-  // of reads)
-  for (unsigned j = threadIdx.x + 256; j < nprev; j += 256) off += cnts[j];
   const int64_t end = min(base + (int64_t)tile, n);
   uint32_t keepbits = 0;
   unsigned mine = 0;
@@ -240,9 +262,9 @@ __global__ __launch_bounds__(256) void k_compact_write(
       ++mine;
     }
   }
-  off = block_sum(off);
   unsigned tile_total = 0;
   unsigned lp = block_exclusive_scan(mine, &tile_total);
+  const unsigned off = lookback_offset(status, blockIdx.x, tile_total);
   for (int j = 0; j < ipt; ++j) {
     const int64_t i = first + j;
     if (i >= end) break;
@@ -281,29 +303,28 @@ __global__ __launch_bounds__(256) void k_compact_write(
       if (out_cnt2) *out_cnt2 = total;
       pred.finish(total);
     }
+    // every live tile has read the statuses it needed once it arrives
+    const unsigned live = (unsigned)((n + tile - 1) / tile);
+    s_clear = __hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT) == live - 1;
+  }
+  __syncthreads();
+  if (s_clear) {
+    const unsigned live = (unsigned)((n + tile - 1) / tile);
+    for (unsigned j = threadIdx.x; j < live; j += 256)
+      __hip_atomic_store(status + j, 0u, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0)
+      __hip_atomic_store(done, 0u, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
-template <class P>
-static void launch_compact_write(hipStream_t s, int nt, const u64* n_dev,
-                                 int64_t n_host, int64_t cap, int tile,
-                                 const uint32_t* cnts, int per_tile,
-                                 u64* out_cnt, u64* out_cnt2, const P& pred) {
-  if ((tile + 255) / 256 == 2)
-    k_compact_write<P, 2><<<nt, 256, 0, s>>>(n_dev, n_host, cap, tile, cnts,
-                                             per_tile, out_cnt, out_cnt2,
-                                             pred);
-  else
-    k_compact_write<P, 0><<<nt, 256, 0, s>>>(n_dev, n_host, cap, tile, cnts,
-                                             per_tile, out_cnt, out_cnt2,
-                                             pred);
-}
-
 // Tile of a compaction pass: a multiple of 256 items, at least 512, with at
-// most kMaxTiles tiles (the tile-count buffer) and at most 32 items per
-// thread (the keep bitmask of k_compact_write).  run > 1: a multiple of run
-// instead (whole runs per tile), which may take one item per thread more
-// than k_compact_write holds (compact_runs_fit).
+// most kMaxTiles tiles (the status buffer) and at most 32 items per thread
+// (the keep bitmask of k_compact).  run > 1: a multiple of run instead
+// (whole runs per tile), which may take one item per thread more than
+// k_compact holds (compact_runs_fit).
 static int64_t compact_tile(int64_t cap, int run = 0) {
   int64_t t = (cap + 4095) / 4096;
   t = (t + 255) / 256 * 256;
@@ -327,21 +348,24 @@ bool compact_runs_fit(int64_t cap, int run) {
   return compact_tile(cap, run) <= 256 * kMaxItemsPerThread;
 }
 
-// Counting pass + write pass.
+// One compaction launch.  `tiles` holds the kMaxTiles look-back statuses
+// followed by the arrival counter.
 template <class P>
-static void run_compact(const Prof& pf, int cls_count, int cls_write,
-                        hipStream_t s, const u64* n_dev, int64_t n_host,
-                        int64_t cap, uint32_t* tiles, u64* out_cnt,
-                        u64* out_cnt2, P pred, int run = 0) {
+static void run_compact(const Prof& pf, int cls, hipStream_t s,
+                        const u64* n_dev, int64_t n_host, int64_t cap,
+                        uint32_t* tiles, u64* out_cnt, u64* out_cnt2, P pred,
+                        int run = 0) {
   const int tile = (int)compact_tile(cap, run);
   const int nt = compact_tiles(cap, run);
-  prof_begin(pf, cls_count, s);
-  k_compact_count<P><<<nt, 256, 0, s>>>(n_dev, n_host, tile, tiles, pred);
-  prof_end(pf, cls_count, s);
-  prof_begin(pf, cls_write, s);
-  launch_compact_write(s, nt, n_dev, n_host, cap, tile, tiles, 1, out_cnt,
-                       out_cnt2, pred);
-  prof_end(pf, cls_write, s);
+  uint32_t* done = tiles + kCompactMaxTiles;
+  prof_begin(pf, cls, s);
+  if ((tile + 255) / 256 == 2)
+    k_compact<P, 2><<<nt, 256, 0, s>>>(n_dev, n_host, cap, tile, tiles, done,
+                                       out_cnt, out_cnt2, pred);
+  else
+    k_compact<P, 0><<<nt, 256, 0, s>>>(n_dev, n_host, cap, tile, tiles, done,
+                                       out_cnt, out_cnt2, pred);
+  prof_end(pf, cls, s);
 }
 
 // ------------------------------------------- consumer-side rulebook prep
@@ -414,7 +438,6 @@ template <typename T>
 struct ScanPred {
   const T* x;
   T* xhat;
-  uint8_t* keepb;
   T* rows;
   int* rowpix;
   int* act;
@@ -423,24 +446,21 @@ struct ScanPred {
   float thr;
   const float* thr_dev;
   ConsList cons;
-  // pass 1: evaluate the truncation rule and remember it
-  __device__ bool count(int64_t i) const {
+  // the truncation rule on the pixel's largest |X - X_hat| over channels
+  struct Item {
+    uint8_t k;
+  };
+  __device__ Item load(int64_t i) const {
     const float thr = thr_dev ? *thr_dev : this->thr;
     float m = 0.f;
     for (int c = 0; c < C; ++c) {
       float d = to_f(x[i * C + c]) - (ref ? 0.f : to_f(xhat[i * C + c]));
       m = fmaxf(m, fabsf(d));
     }
-    const bool k = m > thr;
-    keepb[i] = k ? 1 : 0;
-    return k;
+    return Item{(uint8_t)(m > thr ? 1 : 0)};
   }
-  struct Item {
-    uint8_t k;
-  };
-  __device__ Item load(int64_t i) const { return Item{keepb[i]}; }
   __device__ bool keep(const Item& it) const { return it.k != 0; }
-  // pass 2: gather the delta row, commit the pixel to X_hat
+  // kept pixels: gather the delta row, commit the pixel to X_hat
   __device__ unsigned emit(int64_t i, unsigned pos, const Item&) const {
     rowpix[pos] = (int)i;
     act[pos] = (int)i;
@@ -456,7 +476,6 @@ struct ScanPred {
         r[c] = zero_v<T>();
       }
     }
-    keepb[i] = 0;
     cons_emit(cons, (int)i, pos, (int)pos);
     return 0u;
   }
@@ -467,10 +486,10 @@ struct ScanPred {
 
 template <typename T>
 static void scan_t(const Prof& pf, hipStream_t s, const ScanArgs& a) {
-  ScanPred<T> p{(const T*)a.x, (T*)a.xhat, a.keep, (T*)a.rows, a.rowpix,
-                a.act, a.map, a.C, a.Cp, a.ref, a.thr, a.thr_dev, a.cons};
-  run_compact(pf, 0 /*ST_K_SCAN_MASK*/, 1 /*ST_K_SCAN_COMPACT*/, s, nullptr,
-              a.npix, a.npix, a.tiles, a.cnt_rows, a.cnt_act, p);
+  ScanPred<T> p{(const T*)a.x, (T*)a.xhat, (T*)a.rows, a.rowpix, a.act,
+                a.map, a.C, a.Cp, a.ref, a.thr, a.thr_dev, a.cons};
+  run_compact(pf, 1 /*ST_K_SCAN_COMPACT*/, s, nullptr, a.npix, a.npix,
+              a.tiles, a.cnt_rows, a.cnt_act, p);
 }
 
 void launch_scan(const Prof& pf, hipStream_t s, int dtype,
@@ -602,7 +621,6 @@ struct FlagPred {
     return emit(j, pos, it);
   }
   // the flags are site-major: item j's flag is flags[j]
-  __device__ bool count(int64_t j) const { return flags[j] != 0; }
   __device__ Item load(int64_t j) const { return Item{flags[j]}; }
   __device__ bool keep(const Item& it) const { return it.f != 0; }
   __device__ unsigned emit(int64_t j, unsigned pos, const Item&) const {
@@ -652,42 +670,12 @@ struct FlagPred {
   }
 };
 
-void launch_flag_compact(const Prof& pf, int cls_count, int cls_write,
-                         hipStream_t s, const FlagArgs& a) {
+void launch_flag_compact(const Prof& pf, int cls, hipStream_t s,
+                         const FlagArgs& a) {
   FlagPred p{a.flags, a.list, a.map, a.rowmax, a.nbr, a.map_in, a.stride,
              a.g, a.pairs, a.nf, a.per, a.tstart};
-  run_compact(pf, cls_count, cls_write, s, nullptr, a.npix, a.npix, a.tiles,
-              a.cnt, nullptr, p, a.tstart ? a.nf : 0);
-}
-
-// Per-64-row kept counts of an emitted tensor (rows whose max |delta|
-// exceeds thr), one wave per group; for the kernels whose epilogue does
-// not count them itself.
-__global__ __launch_bounds__(256) void k_group_count(const uint32_t* rowmax,
-                                                     const u64* n_rows,
-                                                     float thr,
-                                                     const float* thr_dev,
-                                                     uint32_t* grp) {
-  if (thr_dev) thr = *thr_dev;
-  const int64_t n = (int64_t)*n_rows;
-  const int64_t ngrp = (n + 63) / 64;
-  const int lane = threadIdx.x & 63;
-  for (int64_t gi = ((int64_t)blockIdx.x * 256 + threadIdx.x) / 64; gi < ngrp;
-       gi += (int64_t)gridDim.x * 4) {
-    const int64_t r = gi * 64 + lane;
-    const bool k = r < n && __uint_as_float(rowmax[r]) > thr;
-    const u64 b = __ballot(k);
-    if (lane == 0) grp[gi] = (uint32_t)__popcll(b);
-  }
-}
-
-void launch_group_count(const Prof& pf, hipStream_t s, const uint32_t* rowmax,
-                        const u64* n_rows, int64_t cap, float thr,
-                        const float* thr_dev, uint32_t* grp) {
-  prof_begin(pf, 14 /*ST_K_LIST_COUNT*/, s);
-  k_group_count<<<grid_for(cap, 2048), 256, 0, s>>>(rowmax, n_rows, thr,
-                                                    thr_dev, grp);
-  prof_end(pf, 14, s);
+  run_compact(pf, cls, s, nullptr, a.npix, a.npix, a.tiles, a.cnt, nullptr,
+              p, a.tstart ? a.nf : 0);
 }
 
 // ------------------------------------------- (c)+(d) convolution epilogue
@@ -941,54 +929,15 @@ __device__ __forceinline__ float finish_cols(const ConvArgs& a, LoadV load_v,
 }
 
 // Row maxima of an output tile (rm: this thread's largest emitted
-// magnitude over its columns) and the kept-row count of the last block to
-// finish the row tile.  Every thread of the block must call it (it
-// synchronises).
+// magnitude over its columns), merged with device-scope atomics.
 __device__ __forceinline__ void finish_rows(const ConvArgs& a, float rm,
-                                            int64_t eo, bool eok, int64_t m0,
-                                            int tiles_n, int64_t m_end,
-                                            int* s_last) {
-  constexpr int BM = kGemmBM;
+                                            int64_t eo, bool eok) {
   const int tid = threadIdx.x;
   // the four threads of a row are adjacent lanes
   rm = fmaxf(rm, __shfl_xor(rm, 1, 64));
   rm = fmaxf(rm, __shfl_xor(rm, 2, 64));
-  // row maxima: device-scope atomics whose results are waited for, so
-  // they have completed at the coherence point before the barrier below
-  unsigned seen = 0u;
   if (eok && (tid & 3) == 0 && a.mode != 1 && rm > 0.f)
-    seen = __hip_atomic_fetch_max(a.rowmax + eo, __float_as_uint(rm),
-                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-
-  // The last block to finish a row tile (over its column tiles) counts
-  // the tile's kept rows for the truncation pass, reading the row maxima
-  // with device-scope atomic loads; the arrival counter is reset by the
-  // block that reads it.  No cache-maintenance fence is needed: only
-  // atomics carry data between the blocks.
-  if (a.grp) {
-    const int64_t tm = m0 / BM;
-    if (seen == 0xFFFFFFFFu) *s_last = 0;  // consumes the atomic results
-    __syncthreads();
-    if (tid == 0)
-      *s_last = __hip_atomic_fetch_add(a.mdone + tm, 1u, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT) ==
-                (unsigned)(tiles_n - 1);
-    __syncthreads();
-    if (*s_last && tid < 64) {
-      const int64_t o = m0 + tid;
-      bool k = false;
-      if (o < m_end)
-        k = __uint_as_float(__hip_atomic_load(a.rowmax + o, __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT)) >
-            (a.keep_thr_dev ? *a.keep_thr_dev : a.keep_thr);
-      const u64 b = __ballot(k);
-      if (tid == 0) {
-        a.grp[tm] = (uint32_t)__popcll(b);
-        __hip_atomic_store(a.mdone + tm, 0u, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-      }
-    }
-  }
+    atomicMax(a.rowmax + eo, __float_as_uint(rm));
 }
 
 template <typename T, bool REF, int ACT, class LoadV, class LoadPo,
@@ -996,12 +945,11 @@ template <typename T, bool REF, int ACT, class LoadV, class LoadPo,
 __device__ __forceinline__ void finish_tile(const ConvArgs& a, LoadV load_v,
                                             LoadPo load_po, LoadSk load_sk,
                                             const bool (&hv)[2], int64_t eo,
-                                            bool eok, int epix, int64_t m0,
-                                            int n0, int ec, int tiles_n,
-                                            int64_t m_end, int* s_last) {
+                                            bool eok, int epix, int n0,
+                                            int ec) {
   const float rm = finish_cols<T, REF, ACT>(a, load_v, load_po, load_sk, hv,
                                             eo, epix, n0, ec);
-  finish_rows(a, rm, eo, eok, m0, tiles_n, m_end, s_last);
+  finish_rows(a, rm, eo, eok);
 }
 
 // Four channels of a delta row stored in the storage type; returns the
@@ -1251,7 +1199,6 @@ void k_conv_gemm(ConvArgs a) {
   static_assert(AV >= 1 && BV >= 1, "stage vectors");
   __shared__ __align__(16) char smem[AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES];
   __shared__ u64 s_kmask;
-  __shared__ int s_last;
   __shared__ int s_site[BM], s_rsk[BM], s_run[BM + 2];
   __shared__ unsigned s_rmax[BM];
   extern __shared__ int s_nbr[];          // [K][BM]
@@ -1609,8 +1556,7 @@ void k_conv_gemm(ConvArgs a) {
         });
       }
     }
-    if constexpr (!SPLIT && !CHUNK)
-      finish_rows(a, rm_all, eo, eok, m0, tiles_n, m1, &s_last);
+    if constexpr (!SPLIT && !CHUNK) finish_rows(a, rm_all, eo, eok);
   }
 }
 
@@ -1619,7 +1565,6 @@ void k_conv_gemm(ConvArgs a) {
 template <typename T, bool REF>
 __global__ __launch_bounds__(256) void k_split_epi(ConvArgs a) {
   constexpr int BM = kGemmBM, BN = kGemmBN;
-  __shared__ int s_last;
   const int64_t nO = (int64_t)*a.nO;
   const int64_t tiles_m = (nO + BM - 1) / BM;
   const int tiles_n = (a.cout_p + BN - 1) / BN;
@@ -1629,7 +1574,6 @@ __global__ __launch_bounds__(256) void k_split_epi(ConvArgs a) {
   const int em = tid >> 2, ec = (tid & 3) * 16;
   const T* dskip = (const T*)a.dskip;
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    __syncthreads();  // the previous tile's reads of s_last are done
     const int64_t tm_i = t / tiles_n;
     const int64_t m0 = tm_i * BM;
     const int n0 = (int)(t - tm_i * tiles_n) * BN;
@@ -1674,8 +1618,7 @@ __global__ __launch_bounds__(256) void k_split_epi(ConvArgs a) {
     };
     with_act(a.act, [&](auto act_tag) {
       finish_tile<T, REF, decltype(act_tag)::value>(
-          a, load_v, load_po, load_sk, hv, eo, eok, epix, m0, n0, ec, tiles_n,
-          nO, &s_last);
+          a, load_v, load_po, load_sk, hv, eo, eok, epix, n0, ec);
     });
   }
 }
@@ -2005,8 +1948,7 @@ void launch_commit(const Prof& pf, hipStream_t s, const int* O, const u64* nO,
 // ------------------------------------------------ truncation (list mode)
 // Keeps the rows of an emitted tensor whose max |delta| exceeds the
 // threshold (ascending kept list), removes dropped rows from the pixel map
-// and prepares the consumers' rulebooks.  Offsets come from per-64-row
-// kept counts written by the producing kernel (or k_group_count).
+// and prepares the consumers' rulebooks.
 struct ListPred {
   const uint32_t* rowmax;
   const int* rowpix;
@@ -2020,9 +1962,6 @@ struct ListPred {
     int pix;
   };
   __device__ float th() const { return thr_dev ? *thr_dev : thr; }
-  __device__ bool count(int64_t r) const {
-    return __uint_as_float(rowmax[r]) > th();
-  }
   __device__ Item load(int64_t r) const { return Item{rowmax[r], rowpix[r]}; }
   __device__ bool keep(const Item& it) const {
     return __uint_as_float(it.rm) > th();
@@ -2057,12 +1996,8 @@ struct ListPred {
 
 void launch_list_compact(const Prof& pf, hipStream_t s, const ListArgs& a) {
   ListPred p{a.rowmax, a.rowpix, a.act, a.map, a.thr, a.thr_dev, a.cons};
-  const int tile = (int)compact_tile(a.cap);
-  const int nt = compact_tiles(a.cap);
-  prof_begin(pf, 15 /*ST_K_LIST_COMPACT*/, s);
-  launch_compact_write(s, nt, a.n_rows, 0, a.cap, tile, a.grp, tile / 64,
-                       a.cnt_act, nullptr, p);
-  prof_end(pf, 15, s);
+  run_compact(pf, 15 /*ST_K_LIST_COMPACT*/, s, a.n_rows, 0, a.cap, a.tiles,
+              a.cnt_act, nullptr, p);
 }
 
 // ------------------------------------------------- squeeze-excitation
@@ -2090,11 +2025,6 @@ __global__ __launch_bounds__(256) void k_se_squeeze(SeArgs a) {
   const int n = blockIdx.y, g = blockIdx.x;
   const int lane = threadIdx.x % TPS, rl = threadIdx.x / TPS;
   const int cp = a.cp, V = cp / 8;
-  // the emission adds its kept counts into these
-  const int64_t nthr = (int64_t)gridDim.x * gridDim.y * 256;
-  for (int64_t i = ((int64_t)n * gridDim.x + g) * 256 + threadIdx.x;
-       i < a.ngrp; i += nthr)
-    a.grp[i] = 0u;
   float acc[IT][8];
 #pragma unroll
   for (int k = 0; k < IT; ++k)
@@ -2312,13 +2242,6 @@ __global__ __launch_bounds__(256) void k_se_emit(SeArgs a) {
     a.rowpix[row] = (int)row;
     a.map[row] = (int)row;
   }
-  // the sites of one wave lie in one 64-site group
-  const float kthr = a.keep_thr_dev ? *a.keep_thr_dev : a.keep_thr;
-  const u64 b = __ballot(in && lane == 0 && rm > kthr);
-  if ((threadIdx.x & 63) == 0 && b) {
-    const int64_t first = (int64_t)blockIdx.x * R + (threadIdx.x / TPS);
-    atomicAdd(a.grp + first / 64, (unsigned)__popcll(b));
-  }
   if (blockIdx.x == 0 && threadIdx.x == 0) *a.cnt_rows = (u64)a.npix;
 }
 
@@ -2445,7 +2368,6 @@ struct ChunkScanPred {
   };
   // items are visited site-major (a site's kept frames adjacent); the
   // keep bytes are stored in that order
-  __device__ bool count(int64_t j) const { return keepb[j] != 0; }
   __device__ Item load(int64_t j) const { return Item{keepb[j]}; }
   __device__ bool keep(const Item& it) const { return it.k != 0; }
   // delta against the value X_hat held when frame t arrived
@@ -2493,8 +2415,8 @@ static void chunk_scan_t(const Prof& pf, hipStream_t s,
                      (T*)a.rows, a.rowpix, a.act, a.map, a.C, a.Cp, a.nf,
                      a.npix, a.cons};
   const int64_t items = (int64_t)a.nf * a.npix;
-  run_compact(pf, 0 /*ST_K_SCAN_MASK*/, 1 /*ST_K_SCAN_COMPACT*/, s, nullptr,
-              items, items, a.tiles, a.cnt_rows, a.cnt_act, p);
+  run_compact(pf, 1 /*ST_K_SCAN_COMPACT*/, s, nullptr, items, items, a.tiles,
+              a.cnt_rows, a.cnt_act, p);
   prof_begin(pf, 1 /*ST_K_SCAN_COMPACT*/, s);
   k_chunk_xhat_commit<T><<<grid_for(a.npix, 4096), 256, 0, s>>>(a);
   prof_end(pf, 1, s);

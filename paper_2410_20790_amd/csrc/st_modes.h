@@ -16,6 +16,10 @@ enum { kModeState = 0, kModeDefer = 1, kModeLinear = 2, kModeChunkState = 3 };
 // rows (nf <= 32) no tile exceeds 64 rows and none is empty.
 constexpr int chunk_tile_step(int nf) { return 65 - nf; }
 
+// Tiles of one compaction pass at most (its look-back statuses; the
+// arrival counter follows them).
+constexpr int kCompactMaxTiles = 4096;
+
 // Partial counters per layer for the sites a chunk's fused epilogue
 // updated (blocks add to slot blockIdx % kSiteSlots; the host sums them).
 constexpr int kSiteSlots = 8;

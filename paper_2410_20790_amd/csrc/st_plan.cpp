@@ -208,7 +208,8 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
   net->n_counters = 2 * (L_n + 1) + (2 + kSiteSlots) * L_n;
   net->off_cnt = a.take(sizeof(uint64_t) * net->n_counters);
   net->off_dens = a.take(sizeof(uint64_t) * batch * F);
-  net->off_tiles = a.take(sizeof(uint32_t) * kMaxTiles);
+  // compaction look-back statuses, then its arrival counter
+  net->off_tiles = a.take(sizeof(uint32_t) * (kMaxTiles + 64));
   net->off_se_par = a.take(sizeof(int));
   net->off_xhat = a.take((size_t)t0.grid * in_c * net->esize);
   // Per-site buffers of the emitted tensors and rulebooks hold F frames
@@ -308,8 +309,6 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
     net->off_chunk_last = a.take(round_up(t0.grid, 16));
     net->off_chunk_aff = a.take(sizeof(uint32_t) * max_conv_phys);
   }
-  net->off_grp = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
-  net->off_mdone = a.take(sizeof(uint32_t) * (max_grid / 64 + 2));
   net->off_zero = a.take(256);
   const size_t n_t = (size_t)L_n + 1;
   net->off_ibst_theta = a.take(sizeof(double) * n_t);
