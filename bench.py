@@ -337,8 +337,164 @@ KCLASS = {"k_conv_gemm": "conv_gemm", "k_conv_dw": "conv_dw",
           "k_split_epi": "conv_split_epi", "k_pool_emit": "pool_emit",
           "k_commit": "commit", "k_output": "output",
           "k_se_squeeze": "se_squeeze", "k_se_emit": "se_emit",
-          "k_chunk_update": "chunk_update", "k_chunk_pool_emit": "pool_emit",
-          "k_chunk_commit": "commit"}
+          "k_chunk_update": "chunk_update",
+          "k_chunk_pool_emit": "chunk_pool_emit",
+          "k_chunk_commit": "chunk_commit"}
+
+
+# the compactions by predicate (pool-site compactions share FlagPred with
+# the rulebooks)
+PCLASS = {"ScanPred": "scan_compact", "ChunkScanPred": "chunk_scan_compact",
+          "FlagPred": "flag_compact", "ListPred": "list_compact"}
+
+
+def demangle(name):
+    """The readable name of a kernel symbol (the counter files name some
+    kernels by their mangled symbol)."""
+    if not name.startswith("_Z"):
+        return name
+    import subprocess
+    try:
+        r = subprocess.run(["c++filt", name], capture_output=True, text=True)
+        out = r.stdout.strip()
+    except OSError:
+        out = ""
+    if out and out != name:
+        return out
+    return demangle_st(name)
+
+
+def demangle_st(name):
+    """Enough of the Itanium mangling for this library's kernel templates
+    (c++filt does not know _Float16's DF16_): st::<name><args>, the
+    arguments being the storage types, predicate structs and bools/ints."""
+    import re
+    m = re.match(r"_ZN2st(\d+)", name)
+    if not m:
+        return name
+    n = int(m.group(1))
+    i = m.end()
+    fn = name[i:i + n]
+    rest = name[i + n:]
+    if not rest.startswith("I"):
+        return f"st::{fn}"
+    types = {"DF16_": "_Float16", "f": "float", "NS_6bf16_tE": "st::bf16_t"}
+    args, j = [], 1
+    while j < len(rest) and rest[j] != "E":
+        if rest.startswith("Lb", j):
+            args.append("true" if rest[j + 2] == "1" else "false")
+            j = rest.index("E", j) + 1
+            continue
+        if rest.startswith("Li", j):
+            k = rest.index("E", j)
+            args.append(rest[j + 2:k])
+            j = k + 1
+            continue
+        for code, t in types.items():
+            if rest.startswith(code, j):
+                args.append(t)
+                j += len(code)
+                break
+        else:
+            mm = re.match(r"NS_(\d+)", rest[j:])
+            if not mm:
+                break
+            ln = int(mm.group(1))
+            k = j + mm.end()
+            sname = "st::" + rest[k:k + ln]
+            k += ln
+            if rest.startswith("I", k):  # the struct's own type argument
+                for code, t in types.items():
+                    if rest.startswith(code, k + 1):
+                        sname += f"<{t}>"
+                        k += 1 + len(code)
+                        break
+                k = rest.index("E", k) + 1
+            if rest.startswith("E", k):
+                k += 1
+            args.append(sname)
+            j = k
+    return f"st::{fn}<{', '.join(args)}>"
+
+
+def kernel_class(kernel_name):
+    """Kernel class of a traced kernel name, None for kernels outside the
+    diff pass (reference-pass instantiations, library kernels)."""
+    head = demangle(kernel_name).split("(")[0]
+    if head.startswith("void "):
+        head = head[5:]
+    fn = head.split("<")[0].split("::")[-1]
+    targs = (head.split("<", 1)[1].rstrip(">").split(", ")
+             if "<" in head else [])
+    if fn == "k_compact":
+        return PCLASS.get(targs[0].split("<")[0].split("::")[-1])
+    if fn == "k_chunk_scan_prep":
+        return "chunk_scan_mask"
+    if fn == "k_chunk_xhat_commit":
+        return "chunk_xhat_commit"
+    if fn not in KCLASS:
+        return None
+    if fn in ("k_conv_gemm", "k_conv_dw", "k_split_epi") and \
+            targs[1:2] == ["true"]:
+        return None  # reference-pass instantiations
+    return KCLASS[fn]
+
+
+def ingest_mfma(base, workload_name, density, schedule=None):
+    """MFMA utilisation of the diff-pass gather-GEMM from one rocprofv3
+    --pmc run (DIR/pmc_mfma): per dispatch, the cycles the MFMA units were
+    busy summed over every SIMD over (GPU-active cycles x 1024 SIMDs), the
+    MFMA work issued (MOPS x 512 FLOP) and its rate over the dispatch's
+    duration; averaged over the dispatches of each kernel build.  Written to
+    profiles/mfma_util.json with the kernel source hash."""
+    import csv
+    import collections
+    path = os.path.join(base, "pmc_mfma", "run_counter_collection.csv")
+    disp = collections.defaultdict(dict)
+    names = {}
+    for r in csv.DictReader(open(path)):
+        raw = r["Kernel_Name"]
+        if raw not in names:
+            names[raw] = demangle(raw).split("(")[0].replace("void ", "")
+        name = names[raw]
+        if not name.startswith("st::k_conv_gemm"):
+            continue
+        d = disp[r["Dispatch_Id"]]
+        d["name"] = name
+        d["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + \
+            float(r["Counter_Value"])
+    per = collections.defaultdict(list)
+    for d in disp.values():
+        per[d["name"]].append(d)
+    # GRBM_GUI_ACTIVE is summed over the 8 XCDs (each counts the
+    # dispatch's active cycles); the MFMA busy cycles over all 1024 SIMDs
+    simds, xcds = 256 * 4, 8
+    out = {}
+    for name, ds in sorted(per.items()):
+        busy = sum(d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) for d in ds)
+        act = sum(d.get("GRBM_GUI_ACTIVE", 0.0) for d in ds) / xcds
+        mops = sum(d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) +
+                   d.get("SQ_INSTS_VALU_MFMA_MOPS_F16", 0.0) for d in ds)
+        ns = sum(d["ns"] for d in ds)
+        out[name] = {"dispatches": len(ds),
+                     "mfma_busy_frac": busy / max(act * simds, 1.0),
+                     "mfma_gflop_per_dispatch": mops * 512 / len(ds) / 1e9,
+                     "mfma_tflops": mops * 512 / max(ns, 1) / 1e3,
+                     "avg_dispatch_us": ns / len(ds) / 1e3}
+    wl = workload(workload_name, density)
+    out_path = os.path.join(ROOT, "profiles", "mfma_util.json")
+    try:
+        dd = json.load(open(out_path))
+    except (OSError, ValueError):
+        dd = {}
+    dd[f"{wl['desc']}-{default_schedule(wl, schedule)}"] = {
+        "source_hash": kernel_source_hash(), "kernels": out}
+    json.dump(dd, open(out_path, "w"), indent=1, sort_keys=True)
+    for name, v in out.items():
+        print(f"| `{name}` | {v['dispatches']} | {v['avg_dispatch_us']:.1f} "
+              f"| {100 * v['mfma_busy_frac']:.1f}% | "
+              f"{v['mfma_gflop_per_dispatch']:.2f} | {v['mfma_tflops']:.1f} |")
 
 
 def ingest_counters(base, workload_name, density, schedule=None):
@@ -355,22 +511,19 @@ def ingest_counters(base, workload_name, density, schedule=None):
 
     scale = {}
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
-        v = [float(r["Counter_Value"]) for r in rows(f"pmc_copy_{c}")
+        # the copy calibration of this run, else the one beside it
+        cal = f"pmc_copy_{c}"
+        if not os.path.isdir(os.path.join(base, cal)):
+            cal = os.path.join("..", cal)
+        v = [float(r["Counter_Value"]) for r in rows(cal)
              if "copyBuffer" in r["Kernel_Name"]]
         scale[c] = (COPY_BYTES / 1024.0) / (sum(v) / len(v))
     per = collections.defaultdict(lambda: collections.defaultdict(list))
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
         for r in rows(f"pmc_bench_{c}"):
-            head = r["Kernel_Name"].split("(")[0]
-            fn = head.split("<")[0].split("::")[-1]
-            targs = (head.split("<", 1)[1].rstrip(">").split(", ")
-                     if "<" in head else [])
-            if fn not in KCLASS:
-                continue
-            if fn in ("k_conv_gemm", "k_conv_dw", "k_split_epi") and \
-                    targs[1:2] == ["true"]:
-                continue  # reference-pass instantiations
-            per[KCLASS[fn]][c].append(float(r["Counter_Value"]))
+            k = kernel_class(r["Kernel_Name"])
+            if k:
+                per[k][c].append(float(r["Counter_Value"]))
     wl = workload(workload_name, density)
     out_path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     try:
@@ -1288,7 +1441,14 @@ def main():
                     help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs "
                          "(DIR/pmc_{bench,copy}_{FETCH,WRITE}_SIZE) into "
                          "profiles/hbm_traffic.json")
+    ap.add_argument("--ingest-mfma", metavar="DIR",
+                    help="turn a rocprofv3 --pmc run of the MFMA counters "
+                         "(DIR/pmc_mfma) into profiles/mfma_util.json")
     args = ap.parse_args()
+    if args.ingest_mfma:
+        ingest_mfma(args.ingest_mfma, args.workload, args.density,
+                    args.schedule)
+        return
     if args.copy_calibration:
         copy_calibration()
         return
