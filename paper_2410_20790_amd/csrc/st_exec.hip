@@ -364,10 +364,107 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
   return true;
 }
 
+// The reference frame keeps every pixel (threshold -1 everywhere), so the
+// frame-by-frame pass would compact every tensor into its pixels in order.
+// For nets without squeeze-excitation or residual carry it runs dense
+// instead: each tensor's rows are its pixels, the convolutions take their
+// neighbours from the geometry, and no list, map or rulebook is built.  It
+// leaves what the frame-by-frame reference pass leaves for the diff frames
+// and the queries: X_hat, every state, the emitted rows, the kept lists
+// (identities) and the counters (every row kept, the dense pair counts).
+static st_status encode_dense_ref(st_net* net, const void* frame, float* out,
+                                  hipStream_t s) {
+  const WS ws{net->ws};
+  u64* cnt = ws.at<u64>(net->off_cnt);
+  net->last_nf = 1;
+  const Prof pf{net, -1};
+  Recorder* R = net->rec && net->rec->on ? net->rec : nullptr;
+  if (R) ++R->frame;
+  (void)hipGetLastError();  // clear any stale error
+
+  TensorPlan& T0 = net->tensors[0];
+  launch_dense_input(pf, s, net->dtype, frame, ws.at<char>(net->off_xhat),
+                     ws.at<char>(T0.off_rows), net->C, T0.Cp, T0.grid);
+  T0.last_thr = -1.f;
+  const int nl = (int)net->layers.size();
+  for (int i = 0; i < nl; ++i) {
+    const LayerPlan& L = net->layers[i];
+    const st_layer_desc& d = L.d;
+    const TensorPlan& in = net->tensors[d.src + 1];
+    TensorPlan& outT = net->tensors[i + 1];
+    const Prof pfl{net, i};
+    // a pooled layer's rows are its pool's; the output layer's go nowhere
+    const bool no_rows = L.pool || i == nl - 1;
+    ConvArgs a{};
+    a.p16 = net->bf16_state ? 1 : 0;
+    a.din = ws.at<char>(in.off_rows);
+    a.nbr = ws.at<int>(L.off_nbr);
+    a.K = L.K;
+    a.cin_p = L.cin_p;
+    a.cout_p = L.cout_p;
+    a.ktot_p = L.ktot_p;
+    a.w = ws.at<char>(L.off_w);
+    a.bias = ws.at<float>(L.off_bias);
+    a.O = ws.at<int>(L.off_O);
+    a.nO = cnt + L.cnt_O;
+    a.capO = L.conv_grid;
+    a.P = L.stateful ? ws.at<float>(L.off_P) : nullptr;
+    a.dout = no_rows ? nullptr : ws.at<char>(outT.off_rows);
+    a.rowmax = nullptr;
+    if (d.residual_src != -2) {
+      const TensorPlan& Rt = net->tensors[d.residual_src + 1];
+      a.dskip = ws.at<char>(Rt.off_rows);
+      a.mskip = ws.at<int>(Rt.off_map);  // marks the residual; not read
+    }
+    a.mode = no_rows ? kModeStateOnly
+                     : (L.stateful ? kModeState : kModeLinear);
+    a.act = d.act;
+    a.ref = 1;
+    a.keep_thr = -1.f;
+    a.zero = ws.at<char>(net->off_zero);
+    a.part = ws.at<float>(net->off_part);
+    a.split_max = L.split_max;
+    a.dense = 1;
+    a.g = conv_geo(L);
+    if (L.dw)
+      launch_conv_dw(pfl, s, net->dtype, a);
+    else if (!launch_conv_gemm(pfl, s, net->dtype, a))
+      return fail(net, ST_ERR_HIP, "internal: GEMM launch arguments");
+    if (L.pool)
+      launch_pool_dense(pfl, s, net->dtype, ws.at<float>(L.off_P), a.p16,
+                        ws.at<char>(outT.off_rows), pool_geo(L), L.cout_p,
+                        d.act, outT.grid);
+    outT.last_thr = -1.f;
+  }
+  if (out) {
+    const LayerPlan& L = net->layers[nl - 1];
+    const Geo g = L.pool ? pool_geo(L) : Geo{L.Ho, L.Wo, L.Ho, L.Wo, 1, 1,
+                                             1, 1, 0, 0};
+    launch_output(Prof{net, nl - 1}, s, ws.at<float>(L.off_P),
+                  net->bf16_state ? 1 : 0, L.cout_p, L.d.c_out, net->N, g,
+                  L.pool ? 1 : 0, L.d.act, nullptr,
+                  ws.at<int>(net->off_se_par), 1, out);
+  }
+  launch_iota_lists(pf, s, ws.at<IotaEntry>(net->off_iota), net->n_iota,
+                    net->ws, net->max_grid);
+  launch_copy_u64(s, cnt, ws.at<u64>(net->off_refcnt), net->n_counters);
+  if (net->ibst_on && net->ibst_refs++ % net->ibst_cycle_refs == 0)
+    launch_ibst_restart(s, ibst_args(net));
+  if (R && R->n_hist < R->max_frames) {
+    (void)hipMemcpyAsync(R->hist + (size_t)R->n_hist * net->n_counters, cnt,
+                         sizeof(u64) * net->n_counters, hipMemcpyDeviceToHost,
+                         s);
+    ++R->n_hist;
+  }
+  net->last_stream = (void*)s;
+  return hip_check(net, "st_encode_reference");
+}
+
 // thr: host thresholds (ignored for the reference frame), or NULL for the
 // thresholds of the online adjustment in device memory.
 st_status encode(st_net* net, const void* frame, const float* thr, float* out,
                  hipStream_t s, bool ref) {
+  if (ref && net->dense_ref) return encode_dense_ref(net, frame, out, s);
   const float* thr_dev =
       (!ref && !thr) ? WS{net->ws}.at<float>(net->off_ibst_thr) : nullptr;
   const WS ws{net->ws};
@@ -807,12 +904,37 @@ extern "C" st_status st_bind_workspace(st_net* net, void* dev_ptr,
   static_assert(sizeof(CleanEntry) == 32, "cleanup entry layout");
   if ((int)tab.size() != net->n_cleanup)
     return fail(net, ST_ERR_INVALID_ARG, "internal: cleanup table size");
-  // The table must outlive the asynchronous copy: keep it in the net.
+  // The tables must outlive the asynchronous copies: keep them alive.
   static thread_local std::vector<CleanEntry> keep_alive;
   keep_alive = tab;
   hipError_t e = hipMemcpyAsync(ws.at<char>(net->off_cleanup), keep_alive.data(),
                                 sizeof(CleanEntry) * tab.size(),
                                 hipMemcpyHostToDevice, s);
+  // dense reference pass: the counters it leaves (every row of every
+  // tensor kept, every layer's outputs affected, the dense pair counts)
+  // and its identity kept lists
+  static thread_local std::vector<u64> keep_cnt;
+  static thread_local std::vector<IotaEntry> keep_iota;
+  static_assert(sizeof(IotaEntry) == 16, "iota entry layout");
+  if (net->dense_ref && e == hipSuccess) {
+    keep_cnt.assign(net->n_counters, 0);
+    keep_iota.clear();
+    for (const TensorPlan& T : net->tensors) {
+      keep_cnt[T.cnt_rows] = keep_cnt[T.cnt_act] = (u64)T.grid;
+      keep_iota.push_back(IotaEntry{(int64_t)T.off_act, T.grid});
+    }
+    for (const LayerPlan& L : net->layers) {
+      keep_cnt[L.cnt_O] = (u64)L.conv_grid;
+      keep_cnt[L.cnt_pairs] = (u64)L.dense_pairs;
+    }
+    e = hipMemcpyAsync(ws.at<char>(net->off_refcnt), keep_cnt.data(),
+                       sizeof(u64) * keep_cnt.size(), hipMemcpyHostToDevice,
+                       s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(ws.at<char>(net->off_iota), keep_iota.data(),
+                         sizeof(IotaEntry) * keep_iota.size(),
+                         hipMemcpyHostToDevice, s);
+  }
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   if (e != hipSuccess)
     return fail(net, ST_ERR_HIP, std::string("bind: ") + hipGetErrorString(e));

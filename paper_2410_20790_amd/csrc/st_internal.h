@@ -98,6 +98,7 @@ struct LayerPlan {
                                     // GEMM updated (site runs)
   size_t off_tstart = 0;            // chunk mode: uint32 run-aligned GEMM
                                     // row tiles (fused-state layers)
+  int64_t dense_pairs = 0;          // rulebook pairs with every pixel active
 };
 
 struct Recorder;  // executor-side profiling state
@@ -141,9 +142,16 @@ struct st_net {
   size_t off_chunk_aff = 0;
   size_t off_cnt = 0;                      // uint64 [n_counters]
   size_t off_cleanup = 0;                  // cleanup descriptor table
+  // dense reference pass (nets without squeeze-excitation or residual
+  // carry): the counters a reference frame leaves (uint64 [n_counters]),
+  // each layer's dense rulebook pair count, and the {offset, length} table
+  // of the kept lists it writes as identities
+  bool dense_ref = false;
+  size_t off_refcnt = 0, off_iota = 0;
   size_t off_dens = 0;                     // uint64 [batch] per-image counts
   int n_counters = 0;
   int n_cleanup = 0;
+  int n_iota = 0;
   int64_t max_grid = 0;
   // runtime
   char* ws = nullptr;

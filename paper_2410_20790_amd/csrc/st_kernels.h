@@ -35,6 +35,24 @@ void prof_end(const Prof& p, int cls, hipStream_t s);
 
 // ---- per-frame bookkeeping
 void launch_reset(const Prof& pf, hipStream_t s, u64* cnt, int n);
+// dense reference pass: the frame's rows (pixel-ordered, padded to Cp
+// channels) and X_hat = frame; identity kept lists of the tensors (a table
+// of {list offset, length} in the workspace); the frame's counters from a
+// precomputed block
+void launch_dense_input(const Prof& pf, hipStream_t s, int dtype,
+                        const void* x, void* xhat, void* rows, int C, int Cp,
+                        int64_t npix);
+struct IotaEntry {  // list[r] = r for r < n
+  int64_t off, n;
+};
+void launch_iota_lists(const Prof& pf, hipStream_t s, const IotaEntry* tab,
+                       int n_tab, char* ws, int64_t max_n);
+void launch_copy_u64(hipStream_t s, u64* dst, const u64* src, int n);
+// dense max-pool emission of the reference pass: pooled row q (pixel
+// order) = max over the window of f(P) (the state of the conv grid)
+void launch_pool_dense(const Prof& pf, hipStream_t s, int dtype,
+                       const float* P, int p16, void* dout, Geo g, int cp,
+                       int act, int64_t nq);
 void launch_cleanup(const Prof& pf, hipStream_t s, const CleanEntry* tab,
                     int n_tab, char* ws, const u64* cnt, int64_t max_rows);
 
@@ -169,6 +187,13 @@ struct ConvArgs {
   const int* gpar;     // the slot in use (device parity word)
   int64_t gsz;         // floats per slot
   int64_t gate_hw;
+  // dense reference pass: every conv output is a row (row = pixel, nO =
+  // capO), every tensor's rows are pixel-ordered, so the neighbours follow
+  // from the geometry g (input row of output o at offset k, or -1 in the
+  // padding), the residual row of a pixel is the pixel itself, and no row
+  // maximum is kept (rowmax NULL)
+  int dense;
+  Geo g;
 };
 // Returns false (and launches nothing) when a.zero is missing or misaligned.
 bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,

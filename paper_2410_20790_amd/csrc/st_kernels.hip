@@ -398,6 +398,20 @@ static void run_compact(const Prof& pf, int cls, hipStream_t s,
   prof_end(pf, cls, s);
 }
 
+// Input row of output pixel o at kernel offset k in a dense pass, where
+// every tensor's rows are its pixels in order: the input pixel the offset
+// reads, or -1 in the padding.
+__device__ __forceinline__ int dense_src(const Geo& g, int64_t o, int k) {
+  const int64_t hwo = (int64_t)g.Ho * g.Wo;
+  const int n = (int)(o / hwo);
+  const int rem = (int)(o - n * hwo);
+  const int oy = rem / g.Wo, ox = rem - (rem / g.Wo) * g.Wo;
+  const int ky = k / g.kw, kx = k - (k / g.kw) * g.kw;
+  const int iy = oy * g.sh - g.ph + ky, ix = ox * g.sw - g.pw + kx;
+  if (iy < 0 || iy >= g.Hi || ix < 0 || ix >= g.Wi) return -1;
+  return (int)(((int64_t)n * g.Hi + iy) * g.Wi + ix);
+}
+
 // ------------------------------------------- consumer-side rulebook prep
 // When a tensor's kept rows are emitted, the rulebooks of the layers that
 // read it are prepared in the same pass: a 1x1 stride-1 convolution gets its
@@ -921,7 +935,7 @@ __device__ __forceinline__ float finish_cols(const ConvArgs& a, LoadV load_v,
       store8f(a.dP + eo * cout_p + n, v);
       continue;
     }
-    if (a.mode == 0) {
+    if (a.mode == kModeState || a.mode == kModeStateOnly) {
       float po[8], pn[8];
       load_po(h, po);
       if (a.gate) {
@@ -952,6 +966,7 @@ __device__ __forceinline__ float finish_cols(const ConvArgs& a, LoadV load_v,
         }
       }
       state_store8(a.P, a.p16, (int64_t)epix * cout_p + n, pn);
+      if (a.mode == kModeStateOnly) continue;
     }
     rm = fmaxf(rm, Vec8<T>::store(dout + eo * cout_p + n, v));
   }
@@ -966,7 +981,7 @@ __device__ __forceinline__ void finish_rows(const ConvArgs& a, float rm,
   // the four threads of a row are adjacent lanes
   rm = fmaxf(rm, __shfl_xor(rm, 1, 64));
   rm = fmaxf(rm, __shfl_xor(rm, 2, 64));
-  if (eok && (tid & 3) == 0 && a.mode != 1 && rm > 0.f)
+  if (eok && (tid & 3) == 0 && a.mode != 1 && rm > 0.f && a.rowmax)
     atomicMax(a.rowmax + eo, __float_as_uint(rm));
 }
 
@@ -1245,7 +1260,7 @@ void k_conv_gemm(ConvArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = WIDE ? 0 : wave >> 1, wn = WIDE ? wave : wave & 1;
   const int l16 = lane & 15, lg = lane >> 4;
-  const int64_t nO = (int64_t)*a.nO;
+  const int64_t nO = a.dense ? a.capO : (int64_t)*a.nO;
   // row tiles: 64 rows each, or (chunk-state mode) aligned to site runs
   const bool runs = CHUNK;  // the launcher pairs tstart with this mode
   const int rstep = runs ? chunk_tile_step(a.nf) : BM;
@@ -1306,13 +1321,15 @@ void k_conv_gemm(ConvArgs a) {
     // now so that they arrive while the reduction runs
     const int64_t eo = m0 + em;
     const bool eok = eo < m1;
-    const int epix = eok ? a.O[eo] : 0;
+    const int epix = !eok ? 0 : a.dense ? (int)eo : a.O[eo];
     __syncthreads();
     u64 my = 0ull;
     for (int e = tid; e < BM * K; e += 256) {
       const int k = e / BM, m = e - (e / BM) * BM;
       const int64_t o = m0 + m;
-      const int src = o < m1 ? a.nbr[(int64_t)k * a.stride + o] : -1;
+      const int src = o >= m1     ? -1
+                      : a.dense ? dense_src(a.g, o, k)
+                                : a.nbr[(int64_t)k * a.stride + o];
       s_nbr[e] = src;
       if (src >= 0) my |= 1ull << k;
     }
@@ -1488,7 +1505,9 @@ void k_conv_gemm(ConvArgs a) {
 
     // this thread's output row's residual row, requested now so that it
     // arrives during the reduction; (chunk-state mode) the row's site
-    const int rsk = (!SPLIT && a.mskip && eok) ? a.mskip[epix] : -1;
+    const int rsk = (!SPLIT && a.mskip && eok)
+                        ? (a.dense ? epix : a.mskip[epix])
+                        : -1;
     if (CHUNK && (tid & 3) == 0)
       s_site[em] = eok ? (int)((unsigned)epix % (unsigned)a.per) : -1;
 
@@ -1595,7 +1614,7 @@ void k_conv_gemm(ConvArgs a) {
 template <typename T, bool REF>
 __global__ __launch_bounds__(256) void k_split_epi(ConvArgs a) {
   constexpr int BM = kGemmBM, BN = kGemmBN;
-  const int64_t nO = (int64_t)*a.nO;
+  const int64_t nO = a.dense ? a.capO : (int64_t)*a.nO;
   const int64_t tiles_m = (nO + BM - 1) / BM;
   const int tiles_n = (a.cout_p + BN - 1) / BN;
   const int64_t ntiles = tiles_m * tiles_n;
@@ -1609,7 +1628,7 @@ __global__ __launch_bounds__(256) void k_split_epi(ConvArgs a) {
     const int n0 = (int)(t - tm_i * tiles_n) * BN;
     const int64_t eo = m0 + em;
     const bool eok = eo < nO;
-    const int epix = eok ? a.O[eo] : 0;
+    const int epix = !eok ? 0 : a.dense ? (int)eo : a.O[eo];
     bool hv[2];
     float po[2][8], sk[2][8];
 #pragma unroll
@@ -1621,7 +1640,8 @@ __global__ __launch_bounds__(256) void k_split_epi(ConvArgs a) {
       if (hv[h] && a.mode == 0 && !REF)
         state_load8(a.P, a.p16, (int64_t)epix * cout_p + n, po[h]);
     }
-    const int rsk = (a.mskip && eok) ? a.mskip[epix] : -1;
+    const int rsk =
+        (a.mskip && eok) ? (a.dense ? epix : a.mskip[epix]) : -1;
 #pragma unroll
     for (int h = 0; h < 2; ++h)
       if (hv[h] && rsk >= 0)
@@ -1783,14 +1803,14 @@ __device__ __forceinline__ void conv_dw_rows(const ConvArgs& a) {
   const T* dskip = (const T*)a.dskip;
   T* dout = (T*)a.dout;
   const int cout_p = a.cout_p, cin_p = a.cin_p;
-  const int64_t nO = (int64_t)*a.nO;
+  const int64_t nO = a.dense ? a.capO : (int64_t)*a.nO;
   const int cpr = cout_p / 8;
   const int64_t total = nO * cpr;
   for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
        idx += (int64_t)gridDim.x * 256) {
     const int64_t o = idx / cpr;
     const int c0 = (int)(idx - o * cpr) * 8;
-    const int pix = a.O[o];
+    const int pix = a.dense ? (int)o : a.O[o];
     float acc[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[e] = 0.f;
@@ -1798,7 +1818,9 @@ __device__ __forceinline__ void conv_dw_rows(const ConvArgs& a) {
       int src[KB];
 #pragma unroll
       for (int j = 0; j < KB; ++j)
-        src[j] = k0 + j < a.K ? a.nbr[(int64_t)(k0 + j) * a.stride + o] : -1;
+        src[j] = k0 + j >= a.K ? -1
+                 : a.dense     ? dense_src(a.g, o, k0 + j)
+                               : a.nbr[(int64_t)(k0 + j) * a.stride + o];
       uint4 raw[KB][RV];
 #pragma unroll
       for (int j = 0; j < KB; ++j)
@@ -1819,12 +1841,12 @@ __device__ __forceinline__ void conv_dw_rows(const ConvArgs& a) {
       }
     }
     // every load of the epilogue before its stores
-    const int rsk = a.mskip ? a.mskip[pix] : -1;
+    const int rsk = !a.mskip ? -1 : a.dense ? pix : a.mskip[pix];
     float sk[8], po[8], ex[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) sk[e] = po[e] = 0.f;
     if (rsk >= 0) Vec8<T>::load(dskip + (int64_t)rsk * cout_p + c0, sk);
-    const bool state = a.mode == kModeState;
+    const bool state = a.mode == kModeState || a.mode == kModeStateOnly;
     if (state && !REF) state_load8(a.P, a.p16, (int64_t)pix * cout_p + c0, po);
     if (state && a.gate)
       load8f(gate_slot(a.gate, a.gpar, a.gsz, 0) + (pix / a.gate_hw) *
@@ -1848,6 +1870,7 @@ __device__ __forceinline__ void conv_dw_rows(const ConvArgs& a) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) pn[e] = state_round(a.p16, po[e] + v[e]);
       state_store8(a.P, a.p16, (int64_t)pix * cout_p + c0, pn);
+      if (a.mode == kModeStateOnly) continue;
       if (a.gate) {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
@@ -1862,7 +1885,7 @@ __device__ __forceinline__ void conv_dw_rows(const ConvArgs& a) {
       }
     }
     const float rm = Vec8<T>::store(dout + o * cout_p + c0, v);
-    if (rm > 0.f) atomicMax(a.rowmax + o, __float_as_uint(rm));
+    if (rm > 0.f && a.rowmax) atomicMax(a.rowmax + o, __float_as_uint(rm));
   }
 }
 
@@ -2955,6 +2978,133 @@ void launch_cleanup(const Prof& pf, hipStream_t s, const CleanEntry* tab,
   dim3 grid(grid_for(max_rows, 512), n_tab);
   k_cleanup<<<grid, 256, 0, s>>>(tab, ws, cnt);
   prof_end(pf, 17, s);
+}
+
+// ----------------------------------------------- dense reference pass
+// The reference frame encodes every pixel (every delta kept, the state
+// treated as zero), so its rows need no compaction: each tensor's rows are
+// its pixels in order.
+template <typename T>
+__global__ __launch_bounds__(256) void k_dense_input(const T* x, T* xhat,
+                                                     T* rows, int C, int Cp,
+                                                     int64_t npix) {
+  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < npix;
+       p += (int64_t)gridDim.x * 256) {
+    for (int c = 0; c < Cp; ++c) {
+      T v = zero_v<T>();
+      if (c < C) {
+        v = x[p * C + c];
+        xhat[p * C + c] = v;
+      }
+      rows[p * Cp + c] = v;
+    }
+  }
+}
+
+void launch_dense_input(const Prof& pf, hipStream_t s, int dtype,
+                        const void* x, void* xhat, void* rows, int C, int Cp,
+                        int64_t npix) {
+  const int grid = grid_for(npix, 8192);
+  prof_begin(pf, 1 /*ST_K_SCAN_COMPACT*/, s);
+  if (dtype == 0)
+    k_dense_input<float><<<grid, 256, 0, s>>>(
+        (const float*)x, (float*)xhat, (float*)rows, C, Cp, npix);
+  else if (dtype == 1)
+    k_dense_input<_Float16><<<grid, 256, 0, s>>>(
+        (const _Float16*)x, (_Float16*)xhat, (_Float16*)rows, C, Cp, npix);
+  else
+    k_dense_input<bf16_t><<<grid, 256, 0, s>>>(
+        (const bf16_t*)x, (bf16_t*)xhat, (bf16_t*)rows, C, Cp, npix);
+  prof_end(pf, 1, s);
+}
+
+__global__ __launch_bounds__(256) void k_iota_lists(const IotaEntry* tab,
+                                                    char* ws) {
+  const IotaEntry e = tab[blockIdx.y];
+  int* list = (int*)(ws + e.off);
+  for (int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x; r < e.n;
+       r += (int64_t)gridDim.x * 256)
+    list[r] = (int)r;
+}
+
+void launch_iota_lists(const Prof& pf, hipStream_t s, const IotaEntry* tab,
+                       int n_tab, char* ws, int64_t max_n) {
+  if (n_tab < 1) return;
+  const dim3 grid(grid_for(max_n, 1024), n_tab);
+  prof_begin(pf, 17 /*ST_K_CLEANUP*/, s);
+  k_iota_lists<<<grid, 256, 0, s>>>(tab, ws);
+  prof_end(pf, 17, s);
+}
+
+__global__ void k_copy_u64(u64* dst, const u64* src, int n) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) dst[i] = src[i];
+}
+
+void launch_copy_u64(hipStream_t s, u64* dst, const u64* src, int n) {
+  k_copy_u64<<<1, 256, 0, s>>>(dst, src, n);
+}
+
+// One thread per 8 channels of a pooled pixel: the largest f(P) over the
+// window's conv sites (g: Hi/Wi the conv grid, Ho/Wo the pooled grid), as
+// the frame-by-frame pool emission computes it with an all-zero previous
+// state (max f(P) - max f(0), f(0) = 0).
+template <typename T, int ACT>
+__device__ __forceinline__ void pool_dense_rows(const float* P, int p16,
+                                                T* dout, const Geo& g,
+                                                int cp, int64_t nq) {
+  const int cpr = cp / 8;
+  const int64_t hwq = (int64_t)g.Ho * g.Wo;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+       idx < nq * cpr; idx += (int64_t)gridDim.x * 256) {
+    const int64_t q = idx / cpr;
+    const int c0 = (int)(idx - q * cpr) * 8;
+    const int n = (int)(q / hwq);
+    const int rem = (int)(q - n * hwq);
+    const int qy = rem / g.Wo, qx = rem - (rem / g.Wo) * g.Wo;
+    float m[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) m[e] = -INFINITY;
+    for (int ky = 0; ky < g.kh; ++ky) {
+      const int iy = qy * g.sh - g.ph + ky;
+      if (iy < 0 || iy >= g.Hi) continue;
+      for (int kx = 0; kx < g.kw; ++kx) {
+        const int ix = qx * g.sw - g.pw + kx;
+        if (ix < 0 || ix >= g.Wi) continue;
+        const int64_t w = ((int64_t)n * g.Hi + iy) * g.Wi + ix;
+        float v[8];
+        state_load8(P, p16 != 0, w * cp + c0, v);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) m[e] = fmaxf(m[e], act_c<ACT>(v[e]));
+      }
+    }
+    (void)Vec8<T>::store(dout + q * cp + c0, m);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_pool_dense(const float* P, int p16,
+                                                    T* dout, Geo g, int cp,
+                                                    int act, int64_t nq) {
+  with_act(act, [&](auto act_tag) {
+    pool_dense_rows<T, decltype(act_tag)::value>(P, p16, dout, g, cp, nq);
+  });
+}
+
+void launch_pool_dense(const Prof& pf, hipStream_t s, int dtype,
+                       const float* P, int p16, void* dout, Geo g, int cp,
+                       int act, int64_t nq) {
+  const int grid = grid_for(nq * (cp / 8), 8192);
+  prof_begin(pf, 12 /*ST_K_POOL_EMIT*/, s);
+  if (dtype == 0)
+    k_pool_dense<float><<<grid, 256, 0, s>>>(P, p16, (float*)dout, g, cp,
+                                             act, nq);
+  else if (dtype == 1)
+    k_pool_dense<_Float16><<<grid, 256, 0, s>>>(P, p16, (_Float16*)dout, g,
+                                                cp, act, nq);
+  else
+    k_pool_dense<bf16_t><<<grid, 256, 0, s>>>(P, p16, (bf16_t*)dout, g, cp,
+                                              act, nq);
+  prof_end(pf, 12, s);
 }
 
 __global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v) {

@@ -8,8 +8,16 @@ namespace st {
 // update rows (applied later).  Linear: emit dP itself.  ChunkState (chunk
 // mode, rows grouped by site in frame order, tiles aligned to those runs):
 // walk each site's frames in order with the state in registers and emit
-// every frame's f(P_t) - f(P_{t-1}).
-enum { kModeState = 0, kModeDefer = 1, kModeLinear = 2, kModeChunkState = 3 };
+// every frame's f(P_t) - f(P_{t-1}).  StateOnly (dense reference pass of a
+// layer whose emitted rows come from elsewhere -- a pool -- or go nowhere --
+// the net's output): store P, emit nothing.
+enum {
+  kModeState = 0,
+  kModeDefer = 1,
+  kModeLinear = 2,
+  kModeChunkState = 3,
+  kModeStateOnly = 4
+};
 
 // Rows per tile step of the run-aligned tiling: a tile starts at the first
 // row of the site run that holds row j * step, so with runs of at most nf

@@ -320,6 +320,36 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
   net->off_part = a.take(std::max<size_t>(part_bytes, 256));
   net->n_cleanup = n_cleanup;
   net->off_cleanup = a.take(32 * n_cleanup);
+  // the reference frame keeps every pixel; without squeeze-excitation
+  // (whose gates need the per-image sums its own pass keeps) or residual
+  // carry (whose views its list pass rebuilds) it runs dense
+  net->dense_ref = !net->has_se && !carry;
+  if (net->dense_ref) {
+    net->off_refcnt = a.take(sizeof(uint64_t) * net->n_counters);
+    net->n_iota = L_n + 1;
+    net->off_iota = a.take(16 * (size_t)net->n_iota);
+  }
+  for (LayerPlan& L : net->layers) {
+    // (output, offset) pairs whose input site lies inside the input grid
+    const st_layer_desc& d = L.d;
+    int64_t pairs = 0;
+    for (int ky = 0; ky < d.k_h; ++ky) {
+      int64_t ny = 0, nx = 0;
+      for (int oy = 0; oy < L.Ho; ++oy) {
+        const int64_t iy = (int64_t)oy * d.s_h - d.p_h + ky;
+        ny += iy >= 0 && iy < L.Hi;
+      }
+      for (int kx = 0; kx < d.k_w; ++kx) {
+        nx = 0;
+        for (int ox = 0; ox < L.Wo; ++ox) {
+          const int64_t ix = (int64_t)ox * d.s_w - d.p_w + kx;
+          nx += ix >= 0 && ix < L.Wi;
+        }
+        pairs += ny * nx;
+      }
+    }
+    L.dense_pairs = pairs * batch;
+  }
   net->ws_bytes = round_up(a.top, kAlign);
   *out = net;
   return ST_OK;
