@@ -1417,6 +1417,17 @@ void k_conv_gemm(ConvArgs a) {
           k = r / cin_p;
           ci = r - k * cin_p;
         }
+        if (!ALIGNED && VEC == 8 && cin_p == 4) {
+          // a frame of 4 (padded) channels: the vector holds offsets k and
+          // k + 1, four channels each, from two gathered rows
+          const int s0 = (live && k < K) ? s_nbr[k * BM + m] : -1;
+          const int s1 = (live && k + 1 < K) ? s_nbr[(k + 1) * BM + m] : -1;
+          const T* p0 = s0 >= 0 ? din + (int64_t)s0 * 4 : zvec;
+          const T* p1 = s1 >= 0 ? din + (int64_t)s1 * 4 : zvec;
+          const uint2 lo = *(const uint2*)p0, hi = *(const uint2*)p1;
+          ra[q] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+          continue;
+        }
         const int src = (live && k < K) ? s_nbr[k * BM + m] : -1;
         const T* pa = src >= 0 ? din + (int64_t)src * cin_p + ci : zvec;
         ra[q] = *(const uint4*)pa;

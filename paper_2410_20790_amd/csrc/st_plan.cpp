@@ -99,6 +99,18 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
   TensorPlan& t0 = net->tensors[0];
   t0.N = batch; t0.H = in_h; t0.W = in_w; t0.C = in_c;
   t0.Cp = (int)round_up(in_c, kChanAlign);
+  // a frame of at most 4 channels (RGB) is padded to 4 only: the first
+  // convolution's reduction then packs two kernel offsets per 16-byte
+  // half-precision vector instead of one offset and 5 zero channels --
+  // when only dense convolutions read the frame delta as their input (a
+  // depthwise layer or a residual add would read it at the output's
+  // 8-channel padding)
+  bool input_packable = in_c <= 4;
+  for (int i = 0; i < n_layers; ++i)
+    if ((layers[i].src == -1 && layers[i].groups > 1) ||
+        layers[i].residual_src == -1)
+      input_packable = false;
+  if (input_packable) t0.Cp = 4;
   t0.grid = (int64_t)batch * in_h * in_w;
   const int kc = gemm_chunk(dtype);
 
