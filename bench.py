@@ -1359,13 +1359,13 @@ def bf16_state_comparison(name, steps=14, warmup=7):
 
 
 def default_schedule(wl, requested=None):
-    """SparseBatch (one st_encode_chunk call per chunk) where the library
-    offers it -- nets without squeeze-excitation whose input has at most
-    16 channels, and whose thresholds are fixed over a chunk -- else one
-    st_encode_diff call per frame."""
+    """SparseBatch (one st_encode_chunk call per chunk) for nets whose
+    input has at most 16 channels and whose thresholds are fixed over a
+    chunk; with the online threshold search (which steps after every frame
+    of the frame-by-frame entry) one st_encode_diff call per frame."""
     net = wl["net"]
     ok = (wl["chunk"] and wl["chunk"] > 2 and not wl["ibst"] and
-          not any(L.se_mid for L in net.layers) and net.C <= 16)
+          net.C <= 16)
     if requested == "frame" or not ok:
         return "frame"
     return "chunk"
@@ -1391,6 +1391,19 @@ def extra_workload(name, steps, warmup, thr=0.0, cpu_chunk=False):
     if sched == "chunk":
         f = measure(wl, steps, warmup, 7, thr, dense=False, schedule="frame")
         r["frame_by_frame"] = {k: f[k] for k in FRAME_KEYS if k in f}
+    elif wl["ibst"] and wl["chunk"] and net.C <= 16:
+        # SparseBatch chunks (exact squeeze-excitation per frame inside the
+        # chunk) with the threshold search stepping once per chunk: warm-up
+        # over one whole search (chunk - 1 chunks), timed over two more
+        nb = wl["chunk"] - 1
+        log(f"workload {name}: chunk schedule, one search step per chunk")
+        c = measure(wl, 2 * nb, nb * nb, 7, thr, dense=False,
+                    schedule="chunk")
+        c.pop("_thresholds", None)
+        r["chunk_ibst"] = {k: c[k] for k in
+                           ("value", "ms_per_step", "effective_tflops",
+                            "ref_ms", "chunk_amortised_frames_per_s", "ibst",
+                            "roofline") if k in c}
     if cpu_chunk:
         r["cpu_baseline"] = cpu_baseline(wl, net, thr,
                                          n_diff=wl["chunk"] - 1)

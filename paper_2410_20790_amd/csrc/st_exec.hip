@@ -586,7 +586,10 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   u64* cO = cnt + L.cnt_O;
   u64* cpairs = cnt + L.cnt_pairs;
   uint32_t* rowmax_out = ws.at<uint32_t>(outT.off_rowmax);
-  uint32_t* rm_O = L.pool ? nullptr : rowmax_out;
+  // exact squeeze-excitation: every site of every frame emits (per-frame
+  // squeeze and excitation between the update and the emission)
+  const bool exact_se = L.se && !net->frozen_se;
+  uint32_t* rm_O = (L.pool || exact_se) ? nullptr : rowmax_out;
   const bool fused = chunk_fused(net, i);
   // the fused GEMM's run-aligned row tiles: cut by the rulebook
   // compaction, or (identity layers) by the list compaction of the layer
@@ -686,8 +689,10 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
     u.cp = L.cout_p;
     u.c = d.c_out;
     u.act = d.act;
-    u.pool_mode = L.pool ? 1 : 0;
-    if (L.se) {  // frozen gates (the chunk entry takes no exact SE)
+    // pooled and exact squeeze-excitation layers: the states after each
+    // frame go to the update rows, the frames to aff
+    u.pool_mode = (L.pool || exact_se) ? 1 : 0;
+    if (L.se && !exact_se) {  // frozen gates
       u.gate = ws.at<float>(L.off_ses);
       u.gpar = ws.at<int>(net->off_se_par);
       u.gsz = (int64_t)net->N * L.cout_p;
@@ -700,6 +705,52 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
       u.keep_thr_dev = thr_dev;
     }
     launch_chunk_update(pf, s, net->dtype, u);
+  }
+  if (exact_se) {
+    ChunkSeArgs c{};
+    c.p16 = net->bf16_state ? 1 : 0;
+    c.P = ws.at<float>(L.off_P);
+    c.Pt = cdp;
+    c.Mo = Mo;
+    c.aff = ws.at<uint32_t>(net->off_chunk_aff);
+    c.part = ws.at<float>(net->off_chunk_separt);
+    c.gates = ws.at<float>(net->off_chunk_gates);
+    c.slots = ws.at<float>(L.off_ses);
+    c.gpar = ws.at<int>(net->off_se_par);
+    c.gsz = (int64_t)net->N * L.cout_p;
+    c.dout = ws.at<char>(outT.off_rows);
+    c.rowmax = rowmax_out;
+    c.rowpix = ws.at<int>(outT.off_rowpix);
+    c.map = ws.at<int>(outT.off_map);
+    c.cnt_rows = cnt + outT.cnt_rows;
+    c.npix = L.conv_grid;
+    c.hw = (int64_t)L.Ho * L.Wo;
+    c.N = net->N;
+    c.nf = nf;
+    c.cp = L.cout_p;
+    c.act = d.act;
+    c.chunk = L.se_chunk;
+    c.nchunk = L.se_nchunk;
+    c.tps = L.se_tps;
+    SeArgs ex{};
+    ex.S = ws.at<double>(L.off_sesum);
+    ex.w1 = ws.at<float>(L.off_sew1);
+    ex.b1 = ws.at<float>(L.off_seb1);
+    ex.w2t = ws.at<float>(L.off_sew2);
+    ex.b2 = ws.at<float>(L.off_seb2);
+    ex.gates = c.slots;
+    ex.gpar = c.gpar;
+    ex.gsz = c.gsz;
+    ex.hw = c.hw;
+    ex.N = net->N;
+    ex.cp = L.cout_p;
+    ex.c = d.c_out;
+    ex.mid = L.se_mid;
+    ex.nchunk = L.se_nchunk;
+    launch_chunk_se(pf, s, net->dtype, c, ex);
+    launch_chunk_commit(pf, s, c.p16, ws.at<float>(L.off_P), cdp, O, cO,
+                        ws.at<uint32_t>(net->off_chunk_aff), citems,
+                        L.conv_grid, L.cout_p);
   }
   if (L.pool) {
     const Geo gp = pool_geo(L);
@@ -739,7 +790,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
       pa.keep_thr_dev = thr_dev;
     }
     launch_chunk_pool_emit(pf, s, net->dtype, pa);
-    launch_chunk_commit(pf, s, ws.at<float>(L.off_P), cdp, O, cO,
+    launch_chunk_commit(pf, s, 0, ws.at<float>(L.off_P), cdp, O, cO,
                         ws.at<uint32_t>(net->off_chunk_aff), citems,
                         L.conv_grid, L.cout_p);
   }
@@ -806,6 +857,10 @@ st_status encode_chunk(st_net* net, const void* frames, int nf,
       return fail(net, ST_ERR_HIP, "internal: GEMM launch arguments");
   launch_cleanup(pf, s, ws.at<CleanEntry>(net->off_cleanup), net->n_cleanup,
                  net->ws, cnt, net->max_grid);
+  // exact squeeze-excitation: the chunk's last gates (in the new slots)
+  // become the previous ones
+  if (net->has_se && !net->frozen_se)
+    launch_flip_parity(s, ws.at<int>(net->off_se_par));
   if (thr_dev) launch_ibst_step(s, cnt, nf, ibst_args(net));
   if (R && R->n_hist < R->max_frames) {
     (void)hipMemcpyAsync(R->hist + (size_t)R->n_hist * net->n_counters, cnt,
@@ -1021,13 +1076,6 @@ static st_status check_chunk(st_net* net, const void* frames,
   if (net->C > kChunkMaxInC)
     return fail(net, ST_ERR_UNSUPPORTED,
                 "chunks need at most 16 input channels");
-  // exact squeeze-excitation couples every site of a frame; with frozen
-  // gates it is a per-channel scale and batches like any layer
-  for (const LayerPlan& L : net->layers)
-    if (L.se && !net->frozen_se)
-      return fail(net, ST_ERR_UNSUPPORTED,
-                  "squeeze-excitation layers are encoded frame by frame "
-                  "(unless created with ST_NET_FROZEN_SE)");
   if (net->layers[nl - 1].pool || net->layers[nl - 1].se)
     return fail(net, ST_ERR_UNSUPPORTED,
                 "a pooled or squeeze-excitation last layer in a chunk");

@@ -140,6 +140,10 @@ struct st_net {
   // the frames that updated it (bit mask)
   size_t off_chunk_dp = 0, off_chunk_base = 0, off_chunk_last = 0;
   size_t off_chunk_aff = 0;
+  // chunk mode, exact squeeze-excitation: per-frame squeeze partials
+  // [F][N][nchunk][cp] and per-frame gates [F][N][cp] (shared by the
+  // layers, sized for the largest)
+  size_t off_chunk_separt = 0, off_chunk_gates = 0;
   size_t off_cnt = 0;                      // uint64 [n_counters]
   size_t off_cleanup = 0;                  // cleanup descriptor table
   // dense reference pass (nets without squeeze-excitation or residual

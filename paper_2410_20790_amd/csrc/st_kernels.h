@@ -262,8 +262,48 @@ struct SeArgs {
   float keep_thr;
   const float* keep_thr_dev;  // in device memory (or NULL: keep_thr)
   const float* yhat;          // residual carry view or NULL
+  float* gout;                // excitation: gates to [N][cp] here instead
+                              // of the new slot (or NULL)
+  // excitation of a chunk's frames in one launch (nfr frames in order,
+  // frame t's partials at part + t * part_stride, its gates at gout +
+  // t * gout_stride); nfr 0 or 1: one frame
+  int nfr;
+  int64_t part_stride, gout_stride;
 };
 void launch_se(const Prof& pf, hipStream_t s, int dtype, const SeArgs& a);
+
+// ---- exact squeeze-excitation in a chunk (frames t = 0 .. nf - 1): the
+// chunk update has left each updated item's state after its frame in Pt
+// (rows of the layer's affected list, Mo: conv item -> row) and each
+// site's updating frames in aff.  Per frame t the squeeze sums
+// f(P_t) - f(P_{t-1}) over the sites frame t updated into
+// part[t][N][nchunk][cp] (the frame-by-frame squeeze's partials, in its
+// order), the excitation moves S frame by frame and leaves frame t's gates
+// in gates[t][N][cp], and the emission writes, for every site and frame,
+// f(P_t) * s_t - f(P_{t-1}) * s_{t-1} (s_{-1}: the gates before the chunk,
+// slot *gpar of the two-slot gate buffer) as candidate row
+// site * nf + t.  Finally the last frame's gates go to the new gate slot.
+struct ChunkSeArgs {
+  int p16;
+  const float* P;       // state before the chunk [npix][cp]
+  const float* Pt;      // per-item states after their frame's update
+  const int* Mo;        // conv item (frame * npix + site) -> Pt row or -1
+  const uint32_t* aff;  // [npix] frames that updated each site
+  float* part;          // [nf][N][nchunk][cp]
+  float* gates;         // [nf][N][cp]
+  float* slots;         // the layer's two gate slots [2][N][cp]
+  const int* gpar;
+  int64_t gsz;          // floats per slot
+  void* dout;           // candidate rows [npix * nf][cp] (site-major)
+  uint32_t* rowmax;
+  int* rowpix;
+  int* map;
+  u64* cnt_rows;
+  int64_t npix, hw;
+  int N, nf, cp, act, chunk, nchunk, tps;
+};
+void launch_chunk_se(const Prof& pf, hipStream_t s, int dtype,
+                     const ChunkSeArgs& c, const SeArgs& excite);
 // Storage-dtype matrix src [rows][cols] (or, transposed, src [cols][rows])
 // to f32 dst [rows_p][cols_p], zero padded; src may be NULL (zeros).
 void launch_to_f32_pad(hipStream_t s, int dtype, const void* src, float* dst,
@@ -347,7 +387,7 @@ void launch_chunk_pool_emit(const Prof& pf, hipStream_t s, int dtype,
 // P[w] = P after the last frame that updated w, for the sites of the
 // affected list O (site-major items, capacity capO), whose frame bits
 // aff[w] are then cleared (pooled layers)
-void launch_chunk_commit(const Prof& pf, hipStream_t s, float* P,
+void launch_chunk_commit(const Prof& pf, hipStream_t s, int p16, float* P,
                          const float* Pt, const int* O, const u64* nO,
                          uint32_t* aff, int64_t capO, int64_t nconv, int cp);
 

@@ -2154,98 +2154,105 @@ __global__ __launch_bounds__(kSeExciteThreads) void k_se_excite(SeArgs a) {
   float* z = sm + a.cp;
   float4* red = (float4*)(sm + a.cp + round_up8(a.mid));
   const int n = blockIdx.x, cp = a.cp, V4 = cp / 4, t = threadIdx.x;
-  float* s_new = const_cast<float*>(gate_slot(a.gates, a.gpar, a.gsz, 1));
-  const int Lc = V4 <= NT ? NT / V4 : 1;
-  const float4* part = (const float4*)(a.part + (int64_t)n * a.nchunk * cp);
-  for (int v0 = 0; v0 < V4; v0 += NT) {
-    const int v = v0 + (Lc > 1 ? t % V4 : t), l = Lc > 1 ? t / V4 : 0;
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (v < V4 && l < Lc) {
-      for (int g = l; g < a.nchunk; g += Lc) {
-        const float4 q = part[(int64_t)g * V4 + v];
-        acc.x += q.x; acc.y += q.y; acc.z += q.z; acc.w += q.w;
+  const int nfr = a.nfr > 1 ? a.nfr : 1;
+  // frames in order: frame fr + 1 starts from the sums frame fr left
+  for (int fr = 0; fr < nfr; ++fr) {
+    float* s_new = a.gout ? a.gout + fr * a.gout_stride
+                          : const_cast<float*>(gate_slot(a.gates, a.gpar,
+                                                         a.gsz, 1));
+    const int Lc = V4 <= NT ? NT / V4 : 1;
+    const float4* part = (const float4*)(a.part + fr * a.part_stride +
+                                         (int64_t)n * a.nchunk * cp);
+    for (int v0 = 0; v0 < V4; v0 += NT) {
+      const int v = v0 + (Lc > 1 ? t % V4 : t), l = Lc > 1 ? t / V4 : 0;
+      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (v < V4 && l < Lc) {
+        for (int g = l; g < a.nchunk; g += Lc) {
+          const float4 q = part[(int64_t)g * V4 + v];
+          acc.x += q.x; acc.y += q.y; acc.z += q.z; acc.w += q.w;
+        }
       }
-    }
-    red[t] = acc;
-    __syncthreads();
-    if (v < V4 && l == 0) {
-      float4 tot = red[t];
-      for (int j = 1; j < Lc; ++j) {
-        const float4 q = red[t + j * V4];
-        tot.x += q.x; tot.y += q.y; tot.z += q.z; tot.w += q.w;
+      red[t] = acc;
+      __syncthreads();
+      if (v < V4 && l == 0) {
+        float4 tot = red[t];
+        for (int j = 1; j < Lc; ++j) {
+          const float4 q = red[t + j * V4];
+          tot.x += q.x; tot.y += q.y; tot.z += q.z; tot.w += q.w;
+        }
+        const float tv[4] = {tot.x, tot.y, tot.z, tot.w};
+  #pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int c = 4 * v + k;
+          double* S = a.S + (int64_t)n * cp + c;
+          const double sv = (a.ref ? 0.0 : *S) + (double)tv[k];
+          *S = sv;
+          m[c] = (float)(sv / (double)a.hw);
+        }
       }
-      const float tv[4] = {tot.x, tot.y, tot.z, tot.w};
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int c = 4 * v + k;
-        double* S = a.S + (int64_t)n * cp + c;
-        const double sv = (a.ref ? 0.0 : *S) + (double)tv[k];
-        *S = sv;
-        m[c] = (float)(sv / (double)a.hw);
+      __syncthreads();
+    }
+    // hidden units z = silu(w1 . m + b1)
+    const int lane = t & 63, wave = t >> 6, nw = NT / 64;
+    const float4* m4 = (const float4*)m;
+    for (int j0 = wave; j0 < a.mid; j0 += 2 * nw) {
+      const int j1 = j0 + nw;
+      const float4* w0 = (const float4*)(a.w1 + (int64_t)j0 * cp);
+      const float4* w1 = (const float4*)(a.w1 + (int64_t)(j1 < a.mid ? j1 : j0)
+                                         * cp);
+      float d0 = 0.f, d1 = 0.f;
+  #pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int v = lane + 64 * i;
+        if (v < V4) {
+          const float4 x = m4[v], p = w0[v], q = w1[v];
+          d0 += p.x * x.x + p.y * x.y + p.z * x.z + p.w * x.w;
+          d1 += q.x * x.x + q.y * x.y + q.z * x.z + q.w * x.w;
+        }
       }
-    }
-    __syncthreads();
-  }
-  // hidden units z = silu(w1 . m + b1)
-  const int lane = t & 63, wave = t >> 6, nw = NT / 64;
-  const float4* m4 = (const float4*)m;
-  for (int j0 = wave; j0 < a.mid; j0 += 2 * nw) {
-    const int j1 = j0 + nw;
-    const float4* w0 = (const float4*)(a.w1 + (int64_t)j0 * cp);
-    const float4* w1 = (const float4*)(a.w1 + (int64_t)(j1 < a.mid ? j1 : j0)
-                                       * cp);
-    float d0 = 0.f, d1 = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int v = lane + 64 * i;
-      if (v < V4) {
-        const float4 x = m4[v], p = w0[v], q = w1[v];
-        d0 += p.x * x.x + p.y * x.y + p.z * x.z + p.w * x.w;
-        d1 += q.x * x.x + q.y * x.y + q.z * x.z + q.w * x.w;
+  #pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        d0 += __shfl_xor(d0, o, 64);
+        d1 += __shfl_xor(d1, o, 64);
       }
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      d0 += __shfl_xor(d0, o, 64);
-      d1 += __shfl_xor(d1, o, 64);
-    }
-    if (lane == 0) {
-      z[j0] = act_f(d0 + a.b1[j0], 2);
-      if (j1 < a.mid) z[j1] = act_f(d1 + a.b1[j1], 2);
-    }
-  }
-  __syncthreads();
-  // gates: output vector v, hidden units split over Lg groups
-  const int Lg = V4 <= NT ? NT / V4 : 1;
-  for (int v0 = 0; v0 < V4; v0 += NT) {
-    const int v = v0 + (Lg > 1 ? t % V4 : t), l = Lg > 1 ? t / V4 : 0;
-    float4 e = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (v < V4 && l < Lg) {
-      const float4* w = (const float4*)a.w2t + v;
-#pragma unroll 4
-      for (int j = l; j < a.mid; j += Lg) {
-        const float4 q = w[(int64_t)j * V4];
-        const float zj = z[j];
-        e.x += q.x * zj; e.y += q.y * zj; e.z += q.z * zj; e.w += q.w * zj;
-      }
-    }
-    red[t] = e;
-    __syncthreads();
-    if (v < V4 && l == 0) {
-      float4 tot = ((const float4*)a.b2)[v];
-      for (int j = 0; j < Lg; ++j) {
-        const float4 q = red[t + j * V4];
-        tot.x += q.x; tot.y += q.y; tot.z += q.z; tot.w += q.w;
-      }
-      const float ev[4] = {tot.x, tot.y, tot.z, tot.w};
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int c = 4 * v + k;
-        s_new[(int64_t)n * cp + c] =
-            c < a.c ? 1.f / (1.f + expf(-ev[k])) : 0.f;
+      if (lane == 0) {
+        z[j0] = act_f(d0 + a.b1[j0], 2);
+        if (j1 < a.mid) z[j1] = act_f(d1 + a.b1[j1], 2);
       }
     }
     __syncthreads();
+    // gates: output vector v, hidden units split over Lg groups
+    const int Lg = V4 <= NT ? NT / V4 : 1;
+    for (int v0 = 0; v0 < V4; v0 += NT) {
+      const int v = v0 + (Lg > 1 ? t % V4 : t), l = Lg > 1 ? t / V4 : 0;
+      float4 e = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (v < V4 && l < Lg) {
+        const float4* w = (const float4*)a.w2t + v;
+  #pragma unroll 4
+        for (int j = l; j < a.mid; j += Lg) {
+          const float4 q = w[(int64_t)j * V4];
+          const float zj = z[j];
+          e.x += q.x * zj; e.y += q.y * zj; e.z += q.z * zj; e.w += q.w * zj;
+        }
+      }
+      red[t] = e;
+      __syncthreads();
+      if (v < V4 && l == 0) {
+        float4 tot = ((const float4*)a.b2)[v];
+        for (int j = 0; j < Lg; ++j) {
+          const float4 q = red[t + j * V4];
+          tot.x += q.x; tot.y += q.y; tot.z += q.z; tot.w += q.w;
+        }
+        const float ev[4] = {tot.x, tot.y, tot.z, tot.w};
+  #pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int c = 4 * v + k;
+          s_new[(int64_t)n * cp + c] =
+              c < a.c ? 1.f / (1.f + expf(-ev[k])) : 0.f;
+        }
+      }
+      __syncthreads();
+    }
   }
 }
 
@@ -2341,6 +2348,195 @@ void launch_se(const Prof& pf, hipStream_t s, int dtype, const SeArgs& a) {
     case 16: se_t<16>(pf, s, dtype, a); break;
     case 32: se_t<32>(pf, s, dtype, a); break;
     default: se_t<64>(pf, s, dtype, a); break;
+  }
+}
+
+// ---- exact squeeze-excitation in a chunk
+// Row in Pt of site p's state before frame t: the latest frame below t
+// that updated it, or -1 (the chunk's starting state).
+__device__ __forceinline__ int chunk_prev_row(const int* Mo, uint32_t bits,
+                                              int t, int64_t npix,
+                                              int64_t p) {
+  const uint32_t below = t > 0 ? bits & ((1u << t) - 1u) : 0u;
+  if (!below) return -1;
+  const int tp = 31 - __builtin_clz(below);
+  return Mo[(int64_t)tp * npix + p];
+}
+
+// Frame blockIdx.z's squeeze: the partial sums of f(P_t) - f(P_{t-1}) over
+// the sites it updated, with the frame-by-frame squeeze's site chunks,
+// lanes and reduction tree (so its sums, and the gates, come out the same).
+template <int TPS>
+__global__ __launch_bounds__(256) void k_chunk_se_squeeze(ChunkSeArgs a) {
+  constexpr int R = 256 / TPS, IT = TPS == 64 ? 4 : 1;
+  __shared__ float sm[256 * IT * 8];  // [R][cp] per-lane partials
+  const int n = blockIdx.y, g = blockIdx.x, t = blockIdx.z;
+  const int lane = threadIdx.x % TPS, rl = threadIdx.x / TPS;
+  const int cp = a.cp, V = cp / 8;
+  float acc[IT][8];
+#pragma unroll
+  for (int k = 0; k < IT; ++k)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[k][e] = 0.f;
+  const int64_t base = (int64_t)n * a.hw;
+  const int64_t s0 = (int64_t)g * a.chunk;
+  const int64_t s1 = min(s0 + (int64_t)a.chunk, a.hw);
+  for (int64_t si = s0 + rl; si < s1; si += R) {
+    const int64_t p = base + si;
+    const uint32_t bits = a.aff[p];
+    if (!((bits >> t) & 1u)) continue;
+    const int r = a.Mo[(int64_t)t * a.npix + p];
+    const int rp = chunk_prev_row(a.Mo, bits, t, a.npix, p);
+#pragma unroll
+    for (int k = 0; k < IT; ++k) {
+      const int v = lane + k * TPS;
+      if (v >= V) break;
+      float po[8], pn[8];
+      if (rp >= 0)
+        load8f(a.Pt + (int64_t)rp * cp + v * 8, po);
+      else
+        state_load8(a.P, a.p16, p * cp + v * 8, po);
+      load8f(a.Pt + (int64_t)r * cp + v * 8, pn);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        acc[k][e] += act_f(pn[e], a.act) - act_f(po[e], a.act);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < IT; ++k) {
+    const int v = lane + k * TPS;
+    if (v < V) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sm[rl * cp + v * 8 + e] = acc[k][e];
+    }
+  }
+  __syncthreads();
+  for (int h = R / 2; h > 0; h >>= 1) {
+    for (int i = threadIdx.x; i < h * cp; i += 256) {
+      const int j = i / cp, c = i - j * cp;
+      sm[j * cp + c] += sm[(j + h) * cp + c];
+    }
+    __syncthreads();
+  }
+  float* part = a.part + (((int64_t)t * a.N + n) * a.nchunk + g) * cp;
+  for (int c = threadIdx.x; c < cp; c += 256) part[c] = sm[c];
+}
+
+// Every site's frames in order (TPS lanes per site, its state in
+// registers): frame t's candidate row site * nf + t is
+// f(P_t) * s_t - f(P_{t-1}) * s_{t-1}.
+template <typename T, int TPS>
+__global__ __launch_bounds__(256) void k_chunk_se_emit(ChunkSeArgs a) {
+  constexpr int R = 256 / TPS, IT = TPS == 64 ? 4 : 1;
+  T* dout = (T*)a.dout;
+  const int lane = threadIdx.x % TPS;
+  const int64_t p = (int64_t)blockIdx.x * R + threadIdx.x / TPS;
+  const int cp = a.cp, V = cp / 8;
+  if (p < a.npix) {
+    const int n = (int)(p / a.hw);
+    const uint32_t bits = a.aff[p];
+    const float* g_first = gate_slot(a.slots, a.gpar, a.gsz, 0) +
+                           (int64_t)n * cp;
+    float pv[IT][8];
+#pragma unroll
+    for (int k = 0; k < IT; ++k) {
+      const int v = lane + k * TPS;
+      if (v < V) state_load8(a.P, a.p16, p * cp + v * 8, pv[k]);
+    }
+    for (int t = 0; t < a.nf; ++t) {
+      const int r = ((bits >> t) & 1u) ? a.Mo[(int64_t)t * a.npix + p] : -1;
+      const float* gn = a.gates + ((int64_t)t * a.N + n) * cp;
+      const float* go =
+          t ? a.gates + ((int64_t)(t - 1) * a.N + n) * cp : g_first;
+      const int64_t j = p * a.nf + t;
+      float rm = 0.f;
+#pragma unroll
+      for (int k = 0; k < IT; ++k) {
+        const int v = lane + k * TPS;
+        if (v >= V) break;
+        float pn[8], g1[8], g0[8], d[8];
+        if (r >= 0) {
+          load8f(a.Pt + (int64_t)r * cp + v * 8, pn);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) pn[e] = pv[k][e];
+        }
+        load8f(gn + v * 8, g1);
+        load8f(go + v * 8, g0);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          d[e] = act_f(pn[e], a.act) * g1[e] - act_f(pv[k][e], a.act) * g0[e];
+          pv[k][e] = pn[e];
+        }
+        rm = fmaxf(rm, Vec8<T>::store(dout + j * cp + v * 8, d));
+      }
+#pragma unroll
+      for (int o = 1; o < TPS; o <<= 1) rm = fmaxf(rm, __shfl_xor(rm, o, 64));
+      if (lane == 0) {
+        a.rowmax[j] = __float_as_uint(rm);
+        a.rowpix[j] = (int)((int64_t)t * a.npix + p);
+        a.map[(int64_t)t * a.npix + p] = (int)j;
+      }
+    }
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0)
+    *a.cnt_rows = (u64)(a.npix * a.nf);
+}
+
+// The chunk's last gates become the new slot's (the slots flip after the
+// chunk).
+__global__ void k_gate_copy(const float* src, float* slots, const int* gpar,
+                            int64_t gsz, int64_t n) {
+  float* dst = const_cast<float*>(gate_slot(slots, gpar, gsz, 1));
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * 256)
+    dst[i] = src[i];
+}
+
+template <int TPS>
+static void chunk_se_t(const Prof& pf, hipStream_t s, int dtype,
+                       const ChunkSeArgs& c, const SeArgs& ex) {
+  prof_begin(pf, 19 /*ST_K_SE_SQUEEZE*/, s);
+  k_chunk_se_squeeze<TPS><<<dim3(c.nchunk, c.N, c.nf), 256, 0, s>>>(c);
+  prof_end(pf, 19, s);
+  prof_begin(pf, 20 /*ST_K_SE_EXCITE*/, s);
+  SeArgs e = ex;
+  e.part = c.part;
+  e.gout = c.gates;
+  e.nfr = c.nf;
+  e.part_stride = (int64_t)c.N * c.nchunk * c.cp;
+  e.gout_stride = (int64_t)c.N * c.cp;
+  e.ref = 0;
+  k_se_excite<<<c.N, kSeExciteThreads,
+                sizeof(float) * (c.cp + round_up8(e.mid) +
+                                 4 * kSeExciteThreads),
+                s>>>(e);
+  prof_end(pf, 20, s);
+  constexpr int R = 256 / TPS;
+  const int blocks = (int)((c.npix + R - 1) / R);
+  prof_begin(pf, 21 /*ST_K_SE_EMIT*/, s);
+  if (dtype == 0)
+    k_chunk_se_emit<float, TPS><<<blocks, 256, 0, s>>>(c);
+  else if (dtype == 1)
+    k_chunk_se_emit<_Float16, TPS><<<blocks, 256, 0, s>>>(c);
+  else
+    k_chunk_se_emit<bf16_t, TPS><<<blocks, 256, 0, s>>>(c);
+  const int64_t ng = (int64_t)c.N * c.cp;
+  k_gate_copy<<<grid_for(ng, 256), 256, 0, s>>>(
+      c.gates + (int64_t)(c.nf - 1) * ng, c.slots, c.gpar, c.gsz, ng);
+  prof_end(pf, 21, s);
+}
+
+void launch_chunk_se(const Prof& pf, hipStream_t s, int dtype,
+                     const ChunkSeArgs& c, const SeArgs& ex) {
+  switch (c.tps) {
+    case 1: chunk_se_t<1>(pf, s, dtype, c, ex); break;
+    case 2: chunk_se_t<2>(pf, s, dtype, c, ex); break;
+    case 4: chunk_se_t<4>(pf, s, dtype, c, ex); break;
+    case 8: chunk_se_t<8>(pf, s, dtype, c, ex); break;
+    case 16: chunk_se_t<16>(pf, s, dtype, c, ex); break;
+    case 32: chunk_se_t<32>(pf, s, dtype, c, ex); break;
+    default: chunk_se_t<64>(pf, s, dtype, c, ex); break;
   }
 }
 
@@ -2784,7 +2980,7 @@ __global__ __launch_bounds__(256) void k_chunk_pool_emit(ChunkPoolArgs a) {
 // P[w] = P after the last frame that updated w, for the sites of the
 // affected list O (run openers; 4 channels per thread of a group of cp / 4
 // threads), and the site's frame bits cleared for the next pooled layer.
-__global__ __launch_bounds__(256) void k_chunk_commit(float* P,
+__global__ __launch_bounds__(256) void k_chunk_commit(int p16, float* P,
                                                       const float* Pt,
                                                       const int* O,
                                                       const u64* nOp,
@@ -2803,8 +2999,8 @@ __global__ __launch_bounds__(256) void k_chunk_commit(float* P,
     // the run's last row holds the state after its last frame
     int64_t r = j;
     while (r + 1 < nO && (uint32_t)O[r + 1] % pu == w) ++r;
-    *(float4*)(P + (int64_t)w * cp + c) =
-        *(const float4*)(Pt + r * cp + c);
+    state_store4(P, p16 != 0, (int64_t)w * cp + c,
+                 *(const float4*)(Pt + r * cp + c));
     if (c == 0) aff[w] = 0u;
   }
 }
@@ -2892,12 +3088,12 @@ void launch_chunk_pool_emit(const Prof& pf, hipStream_t s, int dtype,
   prof_end(pf, 12, s);
 }
 
-void launch_chunk_commit(const Prof& pf, hipStream_t s, float* P,
+void launch_chunk_commit(const Prof& pf, hipStream_t s, int p16, float* P,
                          const float* Pt, const int* O, const u64* nO,
                          uint32_t* aff, int64_t capO, int64_t nconv, int cp) {
   prof_begin(pf, 13 /*ST_K_COMMIT*/, s);
   k_chunk_commit<<<grid_for(capO * (cp / 4), 8192), 256, 0, s>>>(
-      P, Pt, O, nO, aff, nconv, cp);
+      p16, P, Pt, O, nO, aff, nconv, cp);
   prof_end(pf, 13, s);
 }
 

@@ -242,6 +242,7 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
   }
   int n_cleanup = L_n + 1;
   size_t part_bytes = 0, chunk_dp_bytes = 0;
+  size_t chunk_separt_bytes = 0, chunk_gates_bytes = 0;
   int64_t max_conv_phys = 0;
   for (int i = 0; i < L_n; ++i) {
     LayerPlan& L = net->layers[i];
@@ -311,6 +312,13 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
       net->has_se = true;
       L.off_sesum = a.take(sizeof(double) * batch * L.cout_p);
       L.off_separt = a.take(sizeof(float) * batch * L.se_nchunk * L.cout_p);
+      if (F > 1 && !frozen_se) {
+        chunk_separt_bytes = std::max<size_t>(
+            chunk_separt_bytes,
+            sizeof(float) * F * batch * L.se_nchunk * L.cout_p);
+        chunk_gates_bytes = std::max<size_t>(
+            chunk_gates_bytes, sizeof(float) * F * batch * L.cout_p);
+      }
     }
   }
   net->max_grid = max_grid;
@@ -320,6 +328,10 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
     net->off_chunk_base = a.take(round_up(t0.grid * F, 16));
     net->off_chunk_last = a.take(round_up(t0.grid, 16));
     net->off_chunk_aff = a.take(sizeof(uint32_t) * max_conv_phys);
+    if (chunk_separt_bytes) {
+      net->off_chunk_separt = a.take(chunk_separt_bytes);
+      net->off_chunk_gates = a.take(chunk_gates_bytes);
+    }
   }
   net->off_zero = a.take(256);
   const size_t n_t = (size_t)L_n + 1;

@@ -171,6 +171,33 @@ def test_chunk_frozen_se():
                "frozen se", max_band=2, frozen_se=True)
 
 
+@pytest.mark.parametrize("dtype,thr", [("f32", 0.0), ("f32", 0.05),
+                                       ("f16", 0.0)])
+def test_chunk_exact_se(dtype, thr):
+    """Exact squeeze-excitation inside a chunk: for each frame in turn the
+    squeeze over the sites that frame updated, the excitation from the
+    moved channel sums and the emission at every site, f(P_t) s_t -
+    f(P_{t-1}) s_{t-1} (the mini EfficientNet in chunks of 3, against the
+    oracle and the frame-by-frame path)."""
+    from workloads import efficientnet_mini_net
+    net = efficientnet_mini_net(dtype=dtype)
+    run_chunks(net, random_sparse_video(25, 8, 1, 32, 40, 3, 0.08,
+                                        dtype=dtype),
+               thr, 3, f"exact se {dtype} thr={thr}",
+               max_band=0 if (dtype == "f32" and thr == 0.0) else 8)
+
+
+def test_chunk_b0_exact_se():
+    """All 16 MBConv blocks of EfficientNet-B0 at 64x64 fp16 with exact
+    squeeze-excitation, chunks of 4 and a ragged last chunk, on the
+    detection-like video."""
+    from workloads import efficientnet_net, object_video
+    net = efficientnet_net(H=64, W=64)
+    frames = object_video(seed=1, n_frames=7, H=64, W=64, obj=8)
+    run_chunks(net, frames, 0.02, 4, "effnet-b0 64x64 f16 exact se",
+               max_band=128)
+
+
 def test_chunk_resnet50_full_size():
     """ResNet-50 at 1024x2048 bf16 with 10% clustered change in the launch
     configuration the benchmark times (a reference frame, then the chunk's
