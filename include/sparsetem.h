@@ -145,9 +145,7 @@ enum {
    * the gates computed densely in the reference frame are kept for the
    * chunk's diff frames, so a squeeze-excitation layer emits
    * f(P_new) * s - f(P_old) * s at its affected sites only, with no dense
-   * pass per frame.  Exclusive with ST_NET_RESIDUAL_CARRY; with it the
-   * chunk entry also takes squeeze-excitation nets (last layer without
-   * it). */
+   * pass per frame.  Exclusive with ST_NET_RESIDUAL_CARRY. */
   ST_NET_FROZEN_SE = 2,
   /* Pre-activation state stored in bf16 (half the state memory and its
    * traffic; an approximation): every update rounds the new state to the
@@ -251,9 +249,9 @@ st_status st_encode_diff(st_net* net, const void* frame, const float* thr,
  * Errors: ST_ERR_STATE (no workspace or no reference), ST_ERR_INVALID_ARG
  * (NULL, NaN threshold, n_frames outside [1, max_frames]),
  * ST_ERR_UNSUPPORTED (a net created without chunk capacity, more than 16
- * input channels, squeeze-excitation layers unless the net was created
- * with ST_NET_FROZEN_SE, a pooled or squeeze-excitation last layer),
- * ST_ERR_HIP. */
+ * input channels, a pooled or squeeze-excitation last layer), ST_ERR_HIP.
+ * Exact squeeze-excitation layers take, within the call, each frame's
+ * squeeze, excitation and emission at every site in frame order. */
 st_status st_encode_chunk(st_net* net, const void* frames, int32_t n_frames,
                           const float* thr, float* out, void* stream);
 
