@@ -187,23 +187,32 @@ struct IsRanked<P, std::void_t<decltype(P::kRanked)>> : std::true_type {};
 // as it has evaluated its items, before it waits for anything, so no wait
 // depends on another (a chain of published prefixes would make the last
 // tile wait for every earlier one in turn).
-__device__ __forceinline__ unsigned lookback_offset(uint32_t* status,
-                                                    unsigned t,
-                                                    unsigned count) {
-  if (threadIdx.x == 0)
-    __hip_atomic_store(status + t, kLbAgg | count, __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-  // all of this thread's statuses are requested at once (one round trip),
-  // then any not yet published is polled again
-  constexpr int Q = kCompactMaxTiles / 256;
-  uint32_t v[Q];
+// The look-back is split in two: lookback_request reads this thread's
+// share of the earlier tiles' statuses as soon as the kernel starts (most
+// earlier tiles have published by the time they arrive, so the look-back
+// costs no round trip of its own); lookback_offset publishes the tile's
+// count and polls again only the statuses that were not yet published.
+constexpr int kLbQ = kCompactMaxTiles / 256;
+__device__ __forceinline__ void lookback_request(const uint32_t* status,
+                                                 unsigned t,
+                                                 uint32_t (&v)[kLbQ]) {
 #pragma unroll
-  for (int q = 0; q < Q; ++q) {
+  for (int q = 0; q < kLbQ; ++q) {
     const unsigned j = threadIdx.x + 256u * q;
     v[q] = j < t ? __hip_atomic_load(status + j, __ATOMIC_RELAXED,
                                      __HIP_MEMORY_SCOPE_AGENT)
                  : kLbAgg;
   }
+}
+
+__device__ __forceinline__ unsigned lookback_offset(uint32_t* status,
+                                                    unsigned t,
+                                                    unsigned count,
+                                                    uint32_t (&v)[kLbQ]) {
+  constexpr int Q = kLbQ;
+  if (threadIdx.x == 0)
+    __hip_atomic_store(status + t, kLbAgg | count, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
   unsigned sum = 0;
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
@@ -227,6 +236,9 @@ __global__ __launch_bounds__(256) void k_compact(const u64* n_dev,
   using Item = typename P::Item;
   // tile offsets of the kept items (tile <= kMaxItemsPerThread * 256)
   __shared__ uint16_t kept[kMaxItemsPerThread * 256];
+  // IPT > 0: the kept items themselves, in position order (their emit
+  // reads them here instead of loading them again)
+  __shared__ Item kitem[IPT > 0 ? 256 * IPT : 1];
   __shared__ int s_clear;
   const int64_t base = (int64_t)blockIdx.x * tile;
   const int ipt = IPT > 0 ? IPT : (tile + 255) / 256;
@@ -237,6 +249,8 @@ __global__ __launch_bounds__(256) void k_compact(const u64* n_dev,
     for (int j = 0; j < IPT; ++j)
       if (first + j < cap) it[j] = pred.load(first + j);
   }
+  uint32_t lbv[kLbQ];
+  lookback_request(status, blockIdx.x, lbv);
   const int64_t n = read_count(n_dev, n_host);
   if (base >= n) {
     if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -276,11 +290,13 @@ __global__ __launch_bounds__(256) void k_compact(const u64* n_dev,
   }
   unsigned tile_total = 0;
   unsigned lp = block_exclusive_scan(mine, &tile_total);
-  const unsigned off = lookback_offset(status, blockIdx.x, tile_total);
+  const unsigned off =
+      lookback_offset(status, blockIdx.x, tile_total, lbv);
   for (int j = 0; j < ipt; ++j) {
     const int64_t i = first + j;
     if (i >= end) break;
     if (keepbits & (1u << j)) {
+      if constexpr (IPT > 0) kitem[lp] = it[j < IPT ? j : 0];
       kept[lp++] = (uint16_t)(i - base);
     } else {
       if constexpr (IPT > 0)
@@ -293,6 +309,11 @@ __global__ __launch_bounds__(256) void k_compact(const u64* n_dev,
   unsigned work = 0;
   for (unsigned k = threadIdx.x; k < tile_total; k += 256) {
     const int64_t i = base + kept[k];
+    Item itm;
+    if constexpr (IPT > 0)
+      itm = kitem[k];
+    else
+      itm = pred.load(i);
     if constexpr (IsRanked<P>::value) {
       const unsigned pos = off + k;
       unsigned rank = 0;
@@ -301,9 +322,9 @@ __global__ __launch_bounds__(256) void k_compact(const u64* n_dev,
         const unsigned R = pred.run_len(), g = kept[k] / R;
         while (rank < k && kept[k - 1 - rank] / R == g) ++rank;
       }
-      work += pred.emit_ranked(i, pos, pred.load(i), rank);
+      work += pred.emit_ranked(i, pos, itm, rank);
     } else {
-      work += pred.emit(i, off + k, pred.load(i));
+      work += pred.emit(i, off + k, itm);
     }
   }
   work = block_sum(work);
