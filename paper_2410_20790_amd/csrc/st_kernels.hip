@@ -1705,6 +1705,298 @@ __global__ __launch_bounds__(256) void k_split_epi(ConvArgs a) {
   }
 }
 
+// ---------------------------------------------------------- big tiles
+// 128 rows by 128 output channels per tile, four waves in a 2x2
+// arrangement (64x64 each: 4x4 MFMA 16x16 blocks), reduction stages of 64
+// columns staged through two LDS buffers, two stages of loads in flight in
+// registers.  A staged byte feeds twice the products it feeds in a 64x64
+// tile, but a CU holds two such blocks instead of four; as each wave's
+// gathers are bound by their latency, the two effects nearly cancel, and
+// only the layers with the longest reductions gain (use_big).  LDS rows
+// are unpadded: the eight 16-byte vectors of a staged row are XOR-swizzled
+// (big_swz), so the rows a group of lanes reads at one vector column fall
+// in distinct banks.  Half-precision layers whose input channels are a
+// multiple of 64 only; never split.  The epilogue is the chunk-state one:
+// a tile is two consecutive run-aligned row tiles (at most 64 rows each),
+// finished one after the other.
+constexpr int kBigBM = 128, kBigBN = 128;
+// Vector-column swizzle of staged row r, a function of r's low four bits:
+// distinct for any eight consecutive rows from a multiple of eight, and,
+// among sixteen consecutive rows from a multiple of sixteen, distinct over
+// the even rows and over the odd rows.
+__device__ __forceinline__ int big_swz(int r) {
+  return (r & 7) ^ ((r >> 3) & 1);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+void k_conv_gemm_big(ConvArgs a) {
+  static_assert(sizeof(T) == 2, "big tiles are half-precision");
+  constexpr int BM = kBigBM, BN = kBigBN, KC = 64, VEC = 8;
+  constexpr int VPR = KC / VEC;           // 16-byte vectors per staged row
+  constexpr int AV = BM * VPR / 256;      // A vectors per thread per stage
+  constexpr int BV = BN * VPR / 256;      // B vectors per thread per stage
+  constexpr int IM = 4, JN = 4;           // 16x16 blocks per wave
+  constexpr int CLD = BN + 4;             // f32 accumulator row
+  constexpr int HM = kGemmBM;             // rows of an epilogue half
+  constexpr size_t AB_BYTES = 2ull * (BM + BN) * KC * sizeof(T);
+  constexpr size_t C_BYTES = (size_t)BM * CLD * sizeof(float);
+  __shared__ __align__(16) char smem[AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES];
+  __shared__ u64 s_kmask;
+  __shared__ int s_site[BM], s_rsk[BM], s_run[2][HM + 2];
+  __shared__ unsigned s_rmax[2][HM];
+  extern __shared__ int s_nbr[];          // [K][BM]
+  T* const sA = (T*)smem;
+  T* const sB = (T*)smem + 2 * BM * KC;
+  float* const Cs = (float*)smem;
+
+  const T* din = (const T*)a.din;
+  const T* wt = (const T*)a.w;
+  const T* zvec = (const T*)a.zero;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l16 = lane & 15, lg = lane >> 4;
+  const int64_t nO = (int64_t)*a.nO;
+  // row tiles: run-aligned halves, two per tile
+  const int rstep = chunk_tile_step(a.nf);
+  const int64_t tiles_r = (nO + rstep - 1) / rstep;
+  const int64_t tiles_m = (tiles_r + 1) / 2;
+  const int tiles_n = (a.cout_p + BN - 1) / BN;
+  const int64_t ntiles = tiles_m * tiles_n;
+  const int K = a.K, cin_p = a.cin_p, cout_p = a.cout_p;
+  const int ktot_p = (int)a.ktot_p;
+  const int spk = cin_p / KC;             // stages per kernel offset
+  const int nst = K * spk;
+  // XCD-aware order, as in k_conv_gemm
+  const int chunk = (int)((ntiles + kXcd - 1) / kXcd);
+  const int xcd = blockIdx.x % kXcd;
+  const int u_end = (int)min(ntiles, (int64_t)(xcd + 1) * chunk);
+  const int per_xcd = gridDim.x / kXcd;
+  const int em = tid >> 2, ec = (tid & 3) * 16;
+
+  // a unit's row bounds, fetched during the previous unit
+  unsigned nb0 = 0u, nb1 = 0u, nb2 = 0u;
+  auto fetch_bounds = [&](int u) __attribute__((always_inline)) {
+    const int64_t j = 2 * (int64_t)((unsigned)u / (unsigned)tiles_n);
+    nb0 = a.tstart[j];
+    nb1 = a.tstart[min(j + 1, tiles_r)];
+    nb2 = a.tstart[min(j + 2, tiles_r)];
+  };
+  const int u_first = xcd * chunk + blockIdx.x / kXcd;
+  if (u_first < u_end) fetch_bounds(u_first);
+
+  for (int u = u_first; u < u_end; u += per_xcd) {
+    const int tm = (int)((unsigned)u / (unsigned)tiles_n);
+    const int n0 = (u - tm * tiles_n) * BN;
+    // the tile's rows: halves [m0, mh) and [mh, m1)
+    const int64_t m0 =
+        (int64_t)(unsigned)__builtin_amdgcn_readfirstlane((int)nb0);
+    const int64_t mh =
+        (int64_t)(unsigned)__builtin_amdgcn_readfirstlane((int)nb1);
+    const int64_t m1 =
+        (int64_t)(unsigned)__builtin_amdgcn_readfirstlane((int)nb2);
+
+    __syncthreads();  // the previous unit's LDS reads are complete
+    if (tid == 0) s_kmask = 0ull;
+    // this thread's epilogue row in each half and its pixel
+    const int64_t eo0 = m0 + em, eo1 = mh + em;
+    const bool eok0 = eo0 < mh, eok1 = eo1 < m1;
+    const int epix0 = eok0 ? a.O[eo0] : 0;
+    const int epix1 = eok1 ? a.O[eo1] : 0;
+    __syncthreads();
+    u64 my = 0ull;
+    for (int e = tid; e < BM * K; e += 256) {
+      const int k = e / BM, m = e - (e / BM) * BM;
+      const int64_t o = m0 + m;
+      const int src = o < m1 ? a.nbr[(int64_t)k * a.stride + o] : -1;
+      s_nbr[e] = src;
+      if (src >= 0) my |= 1ull << k;
+    }
+    if (my) atomicOr(&s_kmask, my);
+    __syncthreads();
+    const u64 kmask = s_kmask;
+    if (u + per_xcd < u_end) fetch_bounds(u + per_xcd);
+
+    auto next_k = [&](int k) __attribute__((always_inline)) {
+      if (k >= K) return K;
+      const u64 mk = kmask >> k;
+      return mk ? k + __builtin_ctzll(mk) : K;
+    };
+    // stages walked as (offset kc, sub-stage) pairs, offsets without any
+    // active neighbour in the tile skipped by a bit scan of the offset mask
+    struct It {
+      int kc, sub, st;
+    };
+    auto first_stage = [&]() __attribute__((always_inline)) {
+      It it{next_k(0), 0, 0};
+      it.st = it.kc < K ? it.kc * spk : nst;
+      return it;
+    };
+    auto advance = [&](It it) __attribute__((always_inline)) {
+      if (it.st >= nst) return it;
+      if (++it.sub == spk) {
+        it.kc = next_k(it.kc + 1);
+        it.sub = 0;
+      }
+      it.st = it.kc < K ? it.kc * spk + it.sub : nst;
+      return it;
+    };
+    auto load_stage = [&](const It& it, uint4 (&ra)[AV], uint4 (&rb)[BV]) __attribute__((always_inline)) {
+      const bool live = it.st < nst;
+      const int r0 = it.st * KC;
+#pragma unroll
+      for (int q = 0; q < AV; ++q) {
+        const int v = tid + q * 256;
+        const int m = v / VPR, cv = v - (v / VPR) * VPR;
+        const int src = live ? s_nbr[it.kc * BM + m] : -1;
+        const T* pa = src >= 0 ? din + (int64_t)src * cin_p + it.sub * KC +
+                                     cv * VEC
+                               : zvec;
+        ra[q] = *(const uint4*)pa;
+      }
+#pragma unroll
+      for (int q = 0; q < BV; ++q) {
+        const int v = tid + q * 256;
+        const int nn = v / VPR, cv = v - (v / VPR) * VPR;
+        const int n = n0 + nn;
+        const T* pb = (live && n < cout_p)
+                          ? wt + (int64_t)n * ktot_p + r0 + cv * VEC
+                          : zvec;
+        rb[q] = *(const uint4*)pb;
+      }
+    };
+    auto store_stage = [&](int buf, const uint4 (&ra)[AV],
+                           const uint4 (&rb)[BV]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int q = 0; q < AV; ++q) {
+        const int v = tid + q * 256;
+        const int m = v / VPR, cv = v - (v / VPR) * VPR;
+        lds_store16<T>(sA + buf * BM * KC + m * KC + ((cv ^ big_swz(m)) * VEC),
+                       ra[q]);
+      }
+#pragma unroll
+      for (int q = 0; q < BV; ++q) {
+        const int v = tid + q * 256;
+        const int nn = v / VPR, cv = v - (v / VPR) * VPR;
+        lds_store16<T>(sB + buf * BN * KC + nn * KC +
+                           ((cv ^ big_swz(nn)) * VEC),
+                       rb[q]);
+      }
+    };
+
+    v4f acc[IM][JN];
+#pragma unroll
+    for (int i = 0; i < IM; ++i)
+#pragma unroll
+      for (int j = 0; j < JN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    // a lane reads row (or column) 16 i + l16 of its wave's 64, vector
+    // column kk / 8 + lg; the row's swizzle is that of l16
+    auto compute = [&](int buf) __attribute__((always_inline)) {
+      const T* Ab = sA + buf * BM * KC + wm * 64 * KC;
+      const T* Bb = sB + buf * BN * KC + wn * 64 * KC;
+#pragma unroll
+      for (int kk = 0; kk < KC; kk += 32) {
+        const int vc = ((kk / VEC + lg) ^ big_swz(l16)) * VEC;
+        uint4 av[IM], bv[JN];
+#pragma unroll
+        for (int i = 0; i < IM; ++i)
+          av[i] = *(const uint4*)(Ab + (i * 16 + l16) * KC + vc);
+#pragma unroll
+        for (int j = 0; j < JN; ++j)
+          bv[j] = *(const uint4*)(Bb + (j * 16 + l16) * KC + vc);
+#pragma unroll
+        for (int i = 0; i < IM; ++i) {
+#pragma unroll
+          for (int j = 0; j < JN; ++j) {
+            if constexpr (__is_same(T, _Float16)) {
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                  __builtin_bit_cast(v8h, av[i]),
+                  __builtin_bit_cast(v8h, bv[j]), acc[i][j], 0, 0, 0);
+            } else {
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(v8bf, av[i]),
+                  __builtin_bit_cast(v8bf, bv[j]), acc[i][j], 0, 0, 0);
+            }
+          }
+        }
+      }
+    };
+
+    // residual rows of this thread's epilogue rows, requested now so that
+    // they arrive during the reduction, and the rows' sites
+    const int rsk0 = (a.mskip && eok0) ? a.mskip[epix0] : -1;
+    const int rsk1 = (a.mskip && eok1) ? a.mskip[epix1] : -1;
+    if ((tid & 3) == 0) {
+      if (eok0) s_site[em] = (int)((unsigned)epix0 % (unsigned)a.per);
+      if (eok1)
+        s_site[mh - m0 + em] = (int)((unsigned)epix1 % (unsigned)a.per);
+    }
+
+    // stages go in pairs: a pair's loads are issued together as soon as
+    // the pair before is staged in LDS, and waited for together when the
+    // pair is staged, two reductions later (one wait per pair, whose
+    // count the compiler cannot get wrong)
+    uint4 ra0[AV], rb0[BV], ra1[AV], rb1[BV];
+    It ia = first_stage();
+    It ib = advance(ia);
+    load_stage(ia, ra0, rb0);
+    load_stage(ib, ra1, rb1);
+    while (ia.st < nst) {
+      __syncthreads();  // every wave has read both buffers
+      store_stage(0, ra0, rb0);
+      store_stage(1, ra1, rb1);
+      __syncthreads();
+      const bool two = ib.st < nst;
+      const It ic = advance(ib);
+      const It id = advance(ic);
+      load_stage(ic, ra0, rb0);
+      load_stage(id, ra1, rb1);
+      compute(0);
+      if (two) compute(1);
+      ia = ic;
+      ib = id;
+    }
+
+    // ---- epilogue: the whole accumulator tile to LDS (MFMA 16x16 block
+    // layout: D[row = 4 lg + r][col = l16]), then per half and 64-column
+    // quarter as the 64x64 tile finishes it
+    __syncthreads();  // every wave's last stage is read
+    if ((tid & 3) == 0) {
+      if (eok0) s_rsk[em] = rsk0;
+      if (eok1) s_rsk[mh - m0 + em] = rsk1;
+    }
+#pragma unroll
+    for (int i = 0; i < IM; ++i)
+#pragma unroll
+      for (int j = 0; j < JN; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          Cs[(wm * 64 + i * 16 + 4 * lg + r) * CLD + wn * 64 + j * 16 +
+             l16] = acc[i][j][r];
+    __syncthreads();
+    // one pass per (half, 64-column quarter), kept rolled: a copy of the
+    // epilogue per pass would not fit the instruction cache
+#pragma unroll 1
+    for (int hq = 0; hq < 2 * (BN / kGemmBN); ++hq) {
+      const int h = hq / (BN / kGemmBN), q = hq - h * (BN / kGemmBN);
+      const int64_t hm0 = h ? mh : m0;              // the half's first row
+      const int hb0 = (int)(hm0 - m0);
+      const int rows = (int)((h ? m1 : mh) - hm0);
+      finish_chunk_tile<T>(a, Cs + hb0 * CLD + q * kGemmBN, CLD, s_run[h],
+                           hm0, rows, n0 + q * kGemmBN, s_site + hb0,
+                           s_rsk + hb0, s_rmax[h], q == 0,
+                           q == BN / kGemmBN - 1);
+    }
+  }
+}
+
+template <typename T>
+static void gemm_big_t(hipStream_t s, int grid, size_t lds,
+                       const ConvArgs& a) {
+  k_conv_gemm_big<T><<<grid, 256, lds, s>>>(a);
+}
+
 template <typename T>
 static void split_epi_t(hipStream_t s, int grid, const ConvArgs& a) {
   if (a.ref)
@@ -1774,6 +2066,18 @@ static void gemm_t(hipStream_t s, int grid, size_t lds, const ConvArgs& a,
     gemm_t<T, false, false>(s, grid, lds, a);
 }
 
+// Big tiles for the chunk-state layers where they measured faster than
+// the 64x64 ones (ResNet-50 at 1024x2048, 10% change, chunks of 10): the
+// 3x3 layers with 256 or 512 input channels (-3% to -23%) and the 1x1
+// layers with 2048 input channels (-4% to -15%); a 3x3 layer with 128
+// input channels, or a 1x1 layer with 1024, is 2% to 25% slower with them
+// (half the resident waves, and row tiles of half the count).
+static bool use_big(int dtype, const ConvArgs& a) {
+  return dtype != 0 && a.mode == kModeChunkState && !a.ref &&
+         a.split_max <= 1 && a.cout_p % kBigBN == 0 && a.cin_p % 64 == 0 &&
+         a.K <= 64 && ((a.K > 1 && a.cin_p >= 256) || a.cin_p >= 2048);
+}
+
 bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
                       const ConvArgs& a) {
   // inactive lanes read the zero vector: never launch without it
@@ -1785,6 +2089,21 @@ bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
   if (a.tstart && (a.split_max > 1 || a.nf < 1 || a.nf > 32 || a.per < 1 ||
                    !a.sites))
     return false;
+  if (use_big(dtype, a)) {
+    const int64_t halves =
+        (a.capO + chunk_tile_step(a.nf) - 1) / chunk_tile_step(a.nf);
+    const int64_t units = (halves + 1) / 2 * (a.cout_p / kBigBN);
+    int64_t grid = units < 512 ? units : 512;  // two blocks per CU
+    grid = (grid + kXcd - 1) / kXcd * kXcd;
+    const size_t lds = sizeof(int) * (size_t)a.K * kBigBM;
+    prof_begin(pf, 7 /*ST_K_CONV_GEMM*/, s);
+    if (dtype == 1)
+      gemm_big_t<_Float16>(s, (int)grid, lds, a);
+    else
+      gemm_big_t<bf16_t>(s, (int)grid, lds, a);
+    prof_end(pf, 7, s);
+    return true;
+  }
   const bool wide = use_wide(dtype, a);
   const int bn = wide ? GemmTile<bf16_t, true>::BN : kGemmBN;
   const int per_cu = wide ? GemmTile<bf16_t, true>::BLOCKS_PER_CU

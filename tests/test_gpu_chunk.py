@@ -15,7 +15,8 @@ from paper_2410_20790_amd import SparseTemNet
 from paper_2410_20790_amd import binding as B
 from parity_util import RTOL, band, rel, say, to_dev
 from workloads import (crnn_vgg_net, depthwise_test_net, random_sparse_video,
-                       resnet_mini_net, textline_video, toy_net, toy_video)
+                       resnet_mini_net, textline_video, to_storage, toy_net,
+                       toy_video)
 
 pytestmark = pytest.mark.gpu
 
@@ -239,3 +240,35 @@ def test_chunk_resnet50_full_size():
         g.close()
         s.close()
         d.close()
+
+
+def long_reduction_net(dtype, seed=1733):
+    """Layers on the 128x128-tile gather-GEMM: a 3x3 256->256 layer and a
+    1x1 2048->128 layer (long reductions, output channels a multiple of
+    128) between ordinary ones, all half-precision."""
+    from workloads.nets import ACT_NONE, ACT_RELU, LayerSpec, NetSpec
+    rng = np.random.default_rng(seed)
+
+    def conv(src, cin, cout, k, act, gain=1.0):
+        L = LayerSpec(src=src, c_in=cin, c_out=cout, k=(k, k), s=(1, 1),
+                      p=(k // 2, k // 2), act=act)
+        std = gain * np.sqrt(2.0 / (cin * k * k))
+        L.weight = to_storage(rng.normal(0.0, std, (cout, cin, k, k)), dtype)
+        L.bias = to_storage(rng.normal(0.0, 0.05, (cout,)), dtype)
+        return L
+    layers = [conv(-1, 16, 256, 1, ACT_RELU), conv(0, 256, 256, 3, ACT_RELU),
+              conv(1, 256, 2048, 1, ACT_RELU),
+              conv(2, 2048, 128, 1, ACT_RELU),
+              conv(3, 128, 64, 1, ACT_NONE, gain=0.5)]
+    return NetSpec(f"long_reduction_{dtype}", layers, 1, 40, 56, 16, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_chunk_long_reductions(dtype):
+    """128x128 tiles: two run-aligned row tiles per GEMM tile, each
+    finished by the chunk-state epilogue (ragged last tiles, chunks of 4 and
+    a last chunk of 2), against the oracle frame by frame and the
+    frame-by-frame path."""
+    net = long_reduction_net(dtype)
+    frames = random_sparse_video(31, 7, 1, 40, 56, 16, 0.1, dtype=dtype)
+    run_chunks(net, frames, 0.0, 4, f"long reductions {dtype}", max_band=8)
