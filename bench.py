@@ -333,7 +333,8 @@ def measured_traffic(workload_desc, kernel):
     return e.get("bytes_per_launch")
 
 
-KCLASS = {"k_conv_gemm": "conv_gemm", "k_conv_dw": "conv_dw",
+KCLASS = {"k_conv_gemm": "conv_gemm", "k_conv_gemm_big": "conv_gemm",
+          "k_conv_dw": "conv_dw",
           "k_split_epi": "conv_split_epi", "k_pool_emit": "pool_emit",
           "k_commit": "commit", "k_output": "output",
           "k_se_squeeze": "se_squeeze", "k_se_emit": "se_emit",

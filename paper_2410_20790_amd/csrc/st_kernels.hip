@@ -16,7 +16,9 @@
 // order-independent.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
 #include <type_traits>
+#include <vector>
 
 #include <cstdint>
 
@@ -789,7 +791,7 @@ __device__ __forceinline__ void lds_store16<bf16_t>(bf16_t* dst, uint4 v) {
   *(uint4*)dst = v;
 }
 
-constexpr int kGemmBM = 64, kGemmBN = 64, kXcd = 8;
+constexpr int kGemmBM = 64, kGemmBN = 64, kXcd = 8, kCUs = 256;
 
 // 8 consecutive storage elements <-> 8 floats (16- or 32-byte aligned).
 template <typename T> struct Vec8;
@@ -929,8 +931,7 @@ __device__ __forceinline__ int split_count(int64_t ntiles, int nst, int smax) {
 //
 // finish_cols does the per-column work of one thread (16 columns of 64) and
 // returns the largest magnitude it emitted; finish_rows merges the row
-// maxima and counts kept rows.  A wide tile calls finish_cols once per
-// 64-column quarter and finish_rows once.
+// maxima and counts kept rows.
 template <typename T, bool REF, int ACT, class LoadV, class LoadPo,
           class LoadSk>
 __device__ __forceinline__ float finish_cols(const ConvArgs& a, LoadV load_v,
@@ -1157,10 +1158,10 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
 // residual rows in s_site / s_rsk.  The runs are listed (first call of a
 // tile), then each run gets 4, 8 or 16 threads (16, 8 or 4 columns each)
 // -- as many as the tile's run count leaves -- so that long runs (sites
-// that changed in most frames) still keep the block busy.  A wide tile
-// calls it once per 64-column quarter; its row maxima gather in s_rmax
-// and the last call merges them into the device row maxima.  Every thread
-// of the block must call it.
+// that changed in most frames) still keep the block busy.  A tile of
+// several 64-column quarters calls it once per quarter; its row maxima
+// gather in s_rmax and the last call merges them into the device row
+// maxima.  Every thread of the block must call it.
 template <typename T>
 __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
                                                   float* Cs, int cld,
@@ -1209,26 +1210,16 @@ __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
   }
 }
 
-// Tile shapes of the gather-GEMM.  Both are 64 affected rows by BN output
-// channels with four waves (256 threads):
-//   BN = 64:  waves in a 2x2 arrangement, each a 32x32 sub-tile; reduction
-//             stages of MmaCfg<T>::KC columns.
-//   BN = 256 (wide, f16/bf16 only, for layers whose padded width is a
-//             multiple of 256): waves side by side, each owning 64 columns
-//             of all 64 rows (4x4 MFMA 16x16 blocks), reduction stages of 32
-//             columns.  A wave's 64x64 sub-tile reads half the LDS bytes per
-//             MFMA of a 32x32 one, and the gathered rows are staged once for
-//             256 columns instead of once per 64.  Two blocks per CU.
-template <typename T, bool WIDE> struct GemmTile {
-  static_assert(!WIDE || sizeof(T) == 2, "wide tiles are half-precision");
-  static constexpr int BM = kGemmBM;
-  static constexpr int BN = WIDE ? 4 * kGemmBN : kGemmBN;
-  static constexpr int KC = WIDE ? 32 : MmaCfg<T>::KC;
-  static constexpr int LD = WIDE ? 40 : MmaCfg<T>::LD;
-  static constexpr int WAVES_M = WIDE ? 1 : 2, WAVES_N = WIDE ? 4 : 2;
+// Tile shape of the gather-GEMM: 64 affected rows by 64 output channels,
+// four waves (256 threads) in a 2x2 arrangement, each a 32x32 sub-tile;
+// reduction stages of MmaCfg<T>::KC columns; four blocks per CU.
+template <typename T> struct GemmTile {
+  static constexpr int BM = kGemmBM, BN = kGemmBN;
+  static constexpr int KC = MmaCfg<T>::KC, LD = MmaCfg<T>::LD;
+  static constexpr int WAVES_M = 2, WAVES_N = 2;
   static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   static constexpr int IM = WM / 16, JN = WN / 16;
-  static constexpr int BLOCKS_PER_CU = WIDE ? 2 : 4;
+  static constexpr int BLOCKS_PER_CU = 4;
 };
 
 // Reduction stages of a layer that hold real (not padding) columns, for
@@ -1241,16 +1232,14 @@ __device__ __forceinline__ int gemm_stages_kc(const ConvArgs& a) {
 // SPLIT: the layer's reduction may be split (split_max > 1); every unit
 // then writes its partial tile (even when this frame needs one split) and
 // the split epilogue finishes the tiles, so no epilogue state is held
-// through the reduction.  (64-column tiles only.)
+// through the reduction.
 // The register budget follows the blocks each CU holds: four waves per
-// SIMD for 64-column tiles, two for wide ones.
-template <typename T, bool REF, bool ALIGNED, bool SPLIT, bool CHUNK,
-          bool WIDE>
+// SIMD.
+template <typename T, bool REF, bool ALIGNED, bool SPLIT, bool CHUNK>
 __global__ __launch_bounds__(256)
-__attribute__((amdgpu_waves_per_eu(GemmTile<T, WIDE>::BLOCKS_PER_CU)))
+__attribute__((amdgpu_waves_per_eu(GemmTile<T>::BLOCKS_PER_CU)))
 void k_conv_gemm(ConvArgs a) {
-  using G = GemmTile<T, WIDE>;
-  static_assert(!(WIDE && SPLIT), "wide tiles are not split");
+  using G = GemmTile<T>;
   constexpr int BM = G::BM, BN = G::BN;
   constexpr int KC = G::KC, LD = G::LD;
   constexpr int IM = G::IM, JN = G::JN;
@@ -1267,6 +1256,10 @@ void k_conv_gemm(ConvArgs a) {
   __shared__ u64 s_kmask;
   __shared__ int s_site[BM], s_rsk[BM], s_run[BM + 2];
   __shared__ unsigned s_rmax[BM];
+  // dense pass: window origin of each row of the tile (n * Hi, oy * sh - ph,
+  // ox * sw - pw) and each kernel offset's (ky, kx), so that a neighbour
+  // costs no division
+  __shared__ int s_dorg[REF ? 3 * BM : 1], s_koff[REF ? 64 : 1];
   extern __shared__ int s_nbr[];          // [K][BM]
   // LDS carve-up: A[2][BM][LD], B[2][BN][LD]; the f32 accumulator tile of
   // the epilogue (one 64-column quarter at a time) reuses the same bytes
@@ -1279,7 +1272,7 @@ void k_conv_gemm(ConvArgs a) {
   const T* zvec = (const T*)a.zero;
   const T* dskip = (const T*)a.dskip;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = WIDE ? 0 : wave >> 1, wn = WIDE ? wave : wave & 1;
+  const int wm = wave >> 1, wn = wave & 1;
   const int l16 = lane & 15, lg = lane >> 4;
   const int64_t nO = a.dense ? a.capO : (int64_t)*a.nO;
   // row tiles: 64 rows each, or (chunk-state mode) aligned to site runs
@@ -1311,6 +1304,10 @@ void k_conv_gemm(ConvArgs a) {
   // epilogue ownership: thread -> row em, columns [ec, ec + 16) of a
   // 64-column quarter
   const int em = tid >> 2, ec = (tid & 3) * 16;
+  if (REF && a.dense && tid < K) {
+    const int ky = tid / a.g.kw;
+    s_koff[tid] = (ky << 16) | (tid - ky * a.g.kw);
+  }
 
   // run-aligned row tiles (chunk-state mode): a unit's bounds are fetched
   // during the previous unit, so they have arrived when it starts
@@ -1343,14 +1340,34 @@ void k_conv_gemm(ConvArgs a) {
     const int64_t eo = m0 + em;
     const bool eok = eo < m1;
     const int epix = !eok ? 0 : a.dense ? (int)eo : a.O[eo];
+    if (REF && a.dense && tid < BM) {
+      const int64_t o = m0 + tid;
+      const unsigned op = o < m1 ? (unsigned)o : 0u;
+      const unsigned hwo = (unsigned)a.g.Ho * (unsigned)a.g.Wo;
+      const unsigned n = op / hwo, rem = op - n * hwo;
+      const unsigned oy = rem / (unsigned)a.g.Wo;
+      const unsigned ox = rem - oy * (unsigned)a.g.Wo;
+      s_dorg[tid] = (int)n * a.g.Hi;
+      s_dorg[BM + tid] = (int)oy * a.g.sh - a.g.ph;
+      s_dorg[2 * BM + tid] = (int)ox * a.g.sw - a.g.pw;
+    }
     __syncthreads();
     u64 my = 0ull;
     for (int e = tid; e < BM * K; e += 256) {
       const int k = e / BM, m = e - (e / BM) * BM;
       const int64_t o = m0 + m;
-      const int src = o >= m1     ? -1
-                      : a.dense ? dense_src(a.g, o, k)
-                                : a.nbr[(int64_t)k * a.stride + o];
+      int src = -1;
+      if (o < m1) {
+        if (REF && a.dense) {
+          const int ko = s_koff[k];
+          const int iy = s_dorg[BM + m] + (ko >> 16);
+          const int ix = s_dorg[2 * BM + m] + (ko & 0xffff);
+          if (iy >= 0 && iy < a.g.Hi && ix >= 0 && ix < a.g.Wi)
+            src = (s_dorg[m] + iy) * a.g.Wi + ix;
+        } else {
+          src = a.nbr[(int64_t)k * a.stride + o];
+        }
+      }
       s_nbr[e] = src;
       if (src >= 0) my |= 1ull << k;
     }
@@ -1572,23 +1589,20 @@ void k_conv_gemm(ConvArgs a) {
     // 64-column quarter at a time, so that each thread finishes 16
     // contiguous columns of one row: full-width state loads/stores and
     // 16-byte delta stores.  MFMA 16x16 block layout: D[row = 4*lg + r]
-    // [col = l16].  A 64-column tile is its own single quarter (the four
-    // waves' 32x32 sub-tiles); in a wide tile quarter q is wave q's.
+    // [col = l16]; the four waves' 32x32 sub-tiles make the 64x64 tile.
     if (CHUNK && (tid & 3) == 0) s_rsk[em] = rsk;
     float rm_all = 0.f;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-      __syncthreads();  // staged tiles / the previous quarter are read
-      if (!WIDE || wave == q) {
+      __syncthreads();  // the staged tiles are read
 #pragma unroll
-        for (int i = 0; i < IM; ++i)
+      for (int i = 0; i < IM; ++i)
 #pragma unroll
-          for (int j = 0; j < JN; ++j)
+        for (int j = 0; j < JN; ++j)
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              Cs[(wm * G::WM + i * 16 + 4 * lg + r) * CLD +
-                 (WIDE ? 0 : wn * G::WN) + j * 16 + l16] = acc[i][j][r];
-      }
+          for (int r = 0; r < 4; ++r)
+            Cs[(wm * G::WM + i * 16 + 4 * lg + r) * CLD + wn * G::WN +
+               j * 16 + l16] = acc[i][j][r];
       __syncthreads();
       const int nq = n0 + q * kGemmBN;
       const float* crow = Cs + em * CLD + ec;
@@ -2005,65 +2019,59 @@ static void split_epi_t(hipStream_t s, int grid, const ConvArgs& a) {
     k_split_epi<T, false><<<grid, 256, 0, s>>>(a);
 }
 
-template <typename T, bool SPLIT, bool WIDE>
-static void gemm_t(hipStream_t s, int grid, size_t lds, const ConvArgs& a) {
-  const bool aligned = a.cin_p % GemmTile<T, WIDE>::KC == 0;
-  if constexpr (WIDE) {
-    // wide tiles: aligned chunk-state layers only (use_wide), never split
-    k_conv_gemm<T, false, true, false, true, true><<<grid, 256, lds, s>>>(a);
-  } else if (a.ref) {
-    if (aligned)
-      k_conv_gemm<T, true, true, SPLIT, false, false><<<grid, 256, lds, s>>>(
-          a);
-    else
-      k_conv_gemm<T, true, false, SPLIT, false, false><<<grid, 256, lds, s>>>(
-          a);
-  } else if (!SPLIT && a.mode == kModeChunkState) {
-    // the chunk-state epilogue has a build of its own
-    if (aligned)
-      k_conv_gemm<T, false, true, false, true, false><<<grid, 256, lds, s>>>(
-          a);
-    else
-      k_conv_gemm<T, false, false, false, true, false><<<grid, 256, lds, s>>>(
-          a);
-  } else {
-    if (aligned)
-      k_conv_gemm<T, false, true, SPLIT, false, false><<<grid, 256, lds, s>>>(
-          a);
-    else
-      k_conv_gemm<T, false, false, SPLIT, false, false>
-          <<<grid, 256, lds, s>>>(a);
-  }
-}
+using GemmFn = void (*)(ConvArgs);
 
-// Wide (64 x 256) tiles for half-precision layers with a long reduction
-// over a window (K > 1, at least 512 input channels) whose padded width is
-// a multiple of 256, when the reduction is not split.  There the staged
-// operands dominate and the wide tile's reuse pays; layers whose time goes
-// to the epilogue's state traffic keep four 64-column blocks per CU, which
-// hide its load latency better (measured on ResNet-50: the wide tile
-// lowers the 3x3 512-channel layers by 15-23% and raises 1x1 layers).
-// (In the frame-by-frame and reference passes these layers split their
-// reduction instead, so the wide build is the chunk-state one.)
-static bool use_wide(int dtype, const ConvArgs& a) {
-  return dtype != 0 && a.mode == kModeChunkState && !a.ref &&
-         a.split_max <= 1 && a.cout_p % 256 == 0 && a.K > 1 &&
-         a.cin_p >= 512 && a.cin_p % GemmTile<bf16_t, true>::KC == 0;
+// The gather-GEMM build for a launch.
+template <typename T, bool SPLIT>
+static GemmFn pick_gemm(const ConvArgs& a) {
+  const bool aligned = a.cin_p % GemmTile<T>::KC == 0;
+  if (a.ref)
+    return aligned ? k_conv_gemm<T, true, true, SPLIT, false>
+                   : k_conv_gemm<T, true, false, SPLIT, false>;
+  if (!SPLIT && a.mode == kModeChunkState)  // a build of its own
+    return aligned ? k_conv_gemm<T, false, true, false, true>
+                   : k_conv_gemm<T, false, false, false, true>;
+  return aligned ? k_conv_gemm<T, false, true, SPLIT, false>
+                 : k_conv_gemm<T, false, false, SPLIT, false>;
 }
 
 template <typename T>
-static void gemm_t(hipStream_t s, int grid, size_t lds, const ConvArgs& a,
-                   bool wide) {
-  if constexpr (sizeof(T) == 2) {
-    if (wide) {
-      gemm_t<T, false, true>(s, grid, lds, a);
-      return;
-    }
-  }
-  if (a.split_max > 1)
-    gemm_t<T, true, false>(s, grid, lds, a);
-  else
-    gemm_t<T, false, false>(s, grid, lds, a);
+static GemmFn pick_gemm(const ConvArgs& a) {
+  return a.split_max > 1 ? pick_gemm<T, true>(a) : pick_gemm<T, false>(a);
+}
+
+// Blocks of a persistent kernel that one CU holds at once with `lds`
+// bytes of dynamic LDS (its registers and static LDS decide too; at most
+// `cap`); asked of the runtime once per kernel and size.
+static int blocks_per_cu(const void* fn, size_t lds, int cap) {
+  struct Entry {
+    const void* fn;
+    size_t lds;
+    int n;
+  };
+  static std::mutex mu;
+  static std::vector<Entry> cache;
+  std::lock_guard<std::mutex> lock(mu);
+  for (const Entry& e : cache)
+    if (e.fn == fn && e.lds == lds) return e.n;
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, 256, lds) !=
+          hipSuccess ||
+      n < 1)
+    n = 1;
+  n = n < cap ? n : cap;
+  cache.push_back({fn, lds, n});
+  return n;
+}
+
+// A persistent grid: the units, at most what the CUs hold at once, a
+// multiple of the XCD count.
+static int persistent_grid(int64_t units, const void* fn, size_t lds,
+                           int cap) {
+  const int64_t resident = (int64_t)kCUs * blocks_per_cu(fn, lds, cap);
+  int64_t grid = units < resident ? units : resident;
+  grid = (grid + kXcd - 1) / kXcd * kXcd;
+  return (int)grid;
 }
 
 // Big tiles for the chunk-state layers where they measured faster than
@@ -2093,37 +2101,29 @@ bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
     const int64_t halves =
         (a.capO + chunk_tile_step(a.nf) - 1) / chunk_tile_step(a.nf);
     const int64_t units = (halves + 1) / 2 * (a.cout_p / kBigBN);
-    int64_t grid = units < 512 ? units : 512;  // two blocks per CU
-    grid = (grid + kXcd - 1) / kXcd * kXcd;
     const size_t lds = sizeof(int) * (size_t)a.K * kBigBM;
+    const GemmFn fn = dtype == 1 ? (GemmFn)k_conv_gemm_big<_Float16>
+                                 : (GemmFn)k_conv_gemm_big<bf16_t>;
+    const int grid = persistent_grid(units, (const void*)fn, lds, 2);
     prof_begin(pf, 7 /*ST_K_CONV_GEMM*/, s);
-    if (dtype == 1)
-      gemm_big_t<_Float16>(s, (int)grid, lds, a);
-    else
-      gemm_big_t<bf16_t>(s, (int)grid, lds, a);
+    fn<<<grid, 256, lds, s>>>(a);
     prof_end(pf, 7, s);
     return true;
   }
-  const bool wide = use_wide(dtype, a);
-  const int bn = wide ? GemmTile<bf16_t, true>::BN : kGemmBN;
-  const int per_cu = wide ? GemmTile<bf16_t, true>::BLOCKS_PER_CU
-                          : GemmTile<bf16_t, false>::BLOCKS_PER_CU;
   const int rstep = a.tstart ? chunk_tile_step(a.nf) : kGemmBM;
-  const int64_t worst = ((a.capO + rstep - 1) / rstep) *
-                        ((a.cout_p + bn - 1) / bn);
-  // persistent blocks: about what the 256 CUs hold at once
+  const int64_t worst =
+      ((a.capO + rstep - 1) / rstep) * ((a.cout_p + kGemmBN - 1) / kGemmBN);
   const int64_t units = worst * (a.split_max > 1 ? a.split_max : 1);
-  const int64_t resident = 256 * per_cu;
-  int64_t grid = units < resident ? units : resident;
-  grid = (grid + kXcd - 1) / kXcd * kXcd;
   const size_t lds = sizeof(int) * (size_t)a.K * kGemmBM;
+  const GemmFn fn = dtype == 0   ? pick_gemm<float>(a)
+                    : dtype == 1 ? pick_gemm<_Float16>(a)
+                                 : pick_gemm<bf16_t>(a);
+  // persistent blocks: what the CUs hold at once (a large window's
+  // neighbour table can leave room for fewer than four)
+  const int grid = persistent_grid(units, (const void*)fn, lds,
+                                   GemmTile<bf16_t>::BLOCKS_PER_CU);
   prof_begin(pf, 7 /*ST_K_CONV_GEMM*/, s);
-  if (dtype == 0)
-    gemm_t<float>(s, (int)grid, lds, a, false);
-  else if (dtype == 1)
-    gemm_t<_Float16>(s, (int)grid, lds, a, wide);
-  else
-    gemm_t<bf16_t>(s, (int)grid, lds, a, wide);
+  fn<<<grid, 256, lds, s>>>(a);
   prof_end(pf, 7, s);
   if (a.split_max > 1) {
     const int egrid = (int)(worst < 1024 ? worst : 1024);
