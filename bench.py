@@ -107,7 +107,9 @@ def conv_launch_bytes(L, c, es, mode):
     once, the f32 state read and written and the delta written once per
     affected output row (or the deferred f32 update written, for pooled
     layers; in a chunk's fused epilogue the delta written per row and the
-    state read and written once per site), the residual rows read once."""
+    state read and written once per site; in a pooled layer's chunk
+    epilogue the f32 state after each frame written per row and the state
+    read once per site), the residual rows read once."""
     nO, pairs, n_in, _, _, n_skip = (int(v) for v in c[:6])
     sites = int(c[6]) if len(c) > 6 else 0
     K = L.k[0] * L.k[1]
@@ -117,6 +119,8 @@ def conv_launch_bytes(L, c, es, mode):
         b += nO * L.c_out * (4 + 4 + es)
     elif mode == "fused":
         b += nO * L.c_out * es + sites * L.c_out * (4 + 4)
+    elif mode == "fused_pool":
+        b += nO * L.c_out * 4 + sites * L.c_out * 4
     elif mode == "defer":
         b += nO * L.c_out * 4
     else:
@@ -753,6 +757,8 @@ def kernel_table(net, recs, counts, es, chunk_mode=False, nf=1):
             mode = layer_mode(net, j)
             if chunk_mode and mode == "state":
                 mode = "fused" if counts[f, j, 6] > 0 else "defer"
+            elif chunk_mode and L.pool_k[0] > 0 and counts[f, j, 6] > 0:
+                mode = "fused_pool"
             c["bytes"] += conv_launch_bytes(L, cnt, es, mode)
             c["flops"] += 2.0 * cnt[1] * (L.c_in // L.groups) * L.c_out
         elif name in ("se_squeeze", "se_emit"):
@@ -785,7 +791,7 @@ def kernel_table(net, recs, counts, es, chunk_mode=False, nf=1):
             c["bytes"] += b
         elif name == "commit":
             if chunk_mode:
-                sites = int(cnt[7])
+                sites = int(cnt[6]) + int(cnt[7])
                 c["bytes"] += int(cnt[0]) * 4 + sites * (L.c_out * 8 + 4)
             else:
                 c["bytes"] += int(cnt[0]) * (4 + L.c_out * 12)

@@ -135,6 +135,21 @@ bool chunk_fused(const st_net* net, int i) {
          i != (int)net->layers.size() - 1;
 }
 
+// A max-pooled layer's GEMM epilogue walks each site's frames the same
+// way, but writes the state after each frame to the row's update row (the
+// pool emission compares window states frame by frame) instead of
+// emitting deltas; the commit after the pool emission stores the state.
+bool chunk_fused_pool(const st_net* net, int i) {
+  const LayerPlan& L = net->layers[i];
+  return L.stateful && L.pool && !L.dw && !L.se && !net->carry &&
+         i != (int)net->layers.size() - 1;
+}
+
+// Layers whose GEMM runs on run-aligned row tiles in a chunk.
+bool chunk_tiled_layer(const st_net* net, int i) {
+  return chunk_fused(net, i) || chunk_fused_pool(net, i);
+}
+
 // list_pass: the consumers of a list compaction in a chunk (the pass that
 // cuts the run-aligned tiles of fused identity consumers).
 ConsList consumers_of(st_net* net, int t, bool list_pass = false) {
@@ -156,7 +171,7 @@ ConsList consumers_of(st_net* net, int t, bool list_pass = false) {
                      : ws.at<uint32_t>(net->tensors[j + 1].off_rowmax);
       c.cnt_O = cnt + L.cnt_O;
       c.pairs = cnt + L.cnt_pairs;
-      if (list_pass && net->last_nf > 1 && chunk_fused(net, j)) {
+      if (list_pass && net->last_nf > 1 && chunk_tiled_layer(net, j)) {
         c.tstart = ws.at<uint32_t>(L.off_tstart);
         c.nf = net->last_nf;
         c.per = net->tensors[t].grid;
@@ -591,11 +606,13 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   const bool exact_se = L.se && !net->frozen_se;
   uint32_t* rm_O = (L.pool || exact_se) ? nullptr : rowmax_out;
   const bool fused = chunk_fused(net, i);
+  const bool fpool = chunk_fused_pool(net, i);
   // the fused GEMM's run-aligned row tiles: cut by the rulebook
   // compaction, or (identity layers) by the list compaction of the layer
   // that emitted the input, else by a pass of their own
-  uint32_t* tstart = fused ? ws.at<uint32_t>(L.off_tstart) : nullptr;
-  bool tiles_cut = fused && nf > 1 && L.ident && d.src >= 0;
+  const bool tiled = fused || fpool;
+  uint32_t* tstart = tiled ? ws.at<uint32_t>(L.off_tstart) : nullptr;
+  bool tiles_cut = tiled && nf > 1 && L.ident && d.src >= 0;
 
   if (!L.ident) {
     FlagArgs fa{};
@@ -613,13 +630,13 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
     fa.cnt = cO;
     fa.nf = nf;
     fa.per = L.conv_grid;
-    if (fused && compact_runs_fit(citems, nf)) {
+    if (tiled && compact_runs_fit(citems, nf)) {
       fa.tstart = tstart;
       tiles_cut = true;
     }
     launch_flag_compact(pf, ST_K_RB_COMPACT, s, fa);
   }
-  if (fused && !tiles_cut)
+  if (tiled && !tiles_cut)
     launch_run_tiles(pf, s, O, cO, citems, L.conv_grid, nf, tstart);
 
   ConvArgs a{};
@@ -645,6 +662,15 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
     a.sites = cnt + L.cnt_sites;
     a.nf = nf;
     a.per = L.conv_grid;
+  } else if (fpool) {
+    a.mode = kModeChunkPool;
+    a.P = ws.at<float>(L.off_P);
+    a.dP = cdp;
+    a.aff = ws.at<uint32_t>(net->off_chunk_aff);
+    a.tstart = tstart;
+    a.sites = cnt + L.cnt_sites;
+    a.nf = nf;
+    a.per = L.conv_grid;
   } else if (L.stateful) {
     // every frame's update is deferred; the frame loop applies them
     a.mode = kModeDefer;
@@ -665,13 +691,13 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   a.keep_thr_dev = thr_dev;
   a.zero = ws.at<char>(net->off_zero);
   a.part = ws.at<float>(net->off_part);
-  a.split_max = fused ? 1 : L.split_max;
+  a.split_max = tiled ? 1 : L.split_max;
   if (L.dw)
     launch_conv_dw(pf, s, net->dtype, a);
   else if (!launch_conv_gemm(pf, s, net->dtype, a))
     return false;
 
-  if (L.stateful && !fused) {
+  if (L.stateful && !tiled) {
     ChunkUpdArgs u{};
     u.p16 = net->bf16_state ? 1 : 0;
     u.P = ws.at<float>(L.off_P);
@@ -1490,7 +1516,7 @@ extern "C" st_status st_profile_end(st_net* net, st_launch_record* recs,
         int64_t sites = 0;
         for (int k = 0; k < kSiteSlots; ++k)
           sites += (int64_t)c[L.cnt_sites + k];
-        const bool fused = net->last_nf > 1 && chunk_fused(net, j);
+        const bool fused = net->last_nf > 1 && chunk_tiled_layer(net, j);
         q[6] = fused ? sites : 0;
         q[7] = fused ? 0 : sites;
       }

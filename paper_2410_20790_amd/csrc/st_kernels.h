@@ -180,6 +180,8 @@ struct ConvArgs {
   u64* sites;
   int nf;
   int64_t per;
+  // kModeChunkPool: per conv site, the frames that updated it (bit t)
+  uint32_t* aff;
   // frozen squeeze-excitation: per-image gates [N][cout_p] scaling both
   // emitted values of a state-mode emission (image = site / gate_hw), or
   // NULL

@@ -1048,14 +1048,15 @@ __device__ __forceinline__ float store4(T* p, const float* f) {
 // store the state once.  Row maxima are merged in LDS (s_rmax, one LDS
 // atomic per thread and row, no cross-lane reduction in the frame loop)
 // and then with one device atomic per row and column tile.
-template <typename T, int CPT>
+template <typename T, int CPT, bool POOL>
 __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
                                                 int cld, const int* s_run,
                                                 int nruns, int64_t m0,
                                                 int rows, int n0,
                                                 const int* s_site,
                                                 const int* s_rsk,
-                                                unsigned* s_rmax) {
+                                                unsigned* s_rmax,
+                                                const int* s_frm) {
   constexpr int TPR = 64 / CPT, Q = CPT / 4;
   const int tid = threadIdx.x;
   const int cout_p = a.cout_p;
@@ -1106,6 +1107,28 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
   }
   __syncthreads();
   const int r0 = run ? s_run[g] : 0, r1 = run ? s_run[g + 1] : 0;
+  if constexpr (POOL) {
+    // the states after each frame go to the rows' update rows (f32), the
+    // run's frames to the site's bit mask; the state itself is committed
+    // after the pool emission
+    uint32_t bits = 0u;
+    for (int r = r0; r < r1; ++r) {
+      bits |= 1u << s_frm[r];
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        if (c0 + 4 * q >= cout_p) continue;
+        const float4 u = *(const float4*)(Cs + r * cld + (c0 - n0) + 4 * q);
+        const float uv[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          P[4 * q + e] = state_round(a.p16, P[4 * q + e] + uv[e]);
+        *(float4*)(a.dP + (m0 + r) * cout_p + c0 + 4 * q) =
+            make_float4(P[4 * q], P[4 * q + 1], P[4 * q + 2], P[4 * q + 3]);
+      }
+    }
+    if (run && j == 0) a.aff[site] = bits;
+    return;
+  } else {
   // the frames of the run, with the activation fixed at compile time
   auto frames = [&](auto act_tag) {
     constexpr int ACT = decltype(act_tag)::value;
@@ -1150,6 +1173,7 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
                      make_float4(P[4 * q], P[4 * q + 1], P[4 * q + 2],
                                  P[4 * q + 3]));
   }
+  }
 }
 
 // Chunk-state epilogue: the tile's rows [m0, m0 + rows) are whole site
@@ -1161,8 +1185,10 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
 // that changed in most frames) still keep the block busy.  A tile of
 // several 64-column quarters calls it once per quarter; its row maxima
 // gather in s_rmax and the last call merges them into the device row
-// maxima.  Every thread of the block must call it.
-template <typename T>
+// maxima.  Every thread of the block must call it.  POOL (a max-pooled
+// layer, kModeChunkPool): s_frm holds the rows' frames, and the states
+// after each frame go to the rows' update rows instead of deltas.
+template <typename T, bool POOL = false>
 __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
                                                   float* Cs, int cld,
                                                   int* s_run, int64_t m0,
@@ -1170,6 +1196,7 @@ __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
                                                   const int* s_site,
                                                   const int* s_rsk,
                                                   unsigned* s_rmax,
+                                                  const int* s_frm,
                                                   bool first = true,
                                                   bool last = true) {
   constexpr int BM = kGemmBM;
@@ -1195,14 +1222,14 @@ __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
   __syncthreads();
   const int nruns = s_run[BM + 1];
   if (nruns > 32)
-    chunk_tile_runs<T, 16>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
-                           s_rsk, s_rmax);
+    chunk_tile_runs<T, 16, POOL>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
+                           s_rsk, s_rmax, s_frm);
   else if (nruns > 16)
-    chunk_tile_runs<T, 8>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
-                          s_rsk, s_rmax);
+    chunk_tile_runs<T, 8, POOL>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
+                          s_rsk, s_rmax, s_frm);
   else
-    chunk_tile_runs<T, 4>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
-                          s_rsk, s_rmax);
+    chunk_tile_runs<T, 4, POOL>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
+                          s_rsk, s_rmax, s_frm);
   if (last) {
     __syncthreads();
     if (tid < rows && s_rmax[tid])
@@ -1235,7 +1262,8 @@ __device__ __forceinline__ int gemm_stages_kc(const ConvArgs& a) {
 // through the reduction.
 // The register budget follows the blocks each CU holds: four waves per
 // SIMD.
-template <typename T, bool REF, bool ALIGNED, bool SPLIT, bool CHUNK>
+template <typename T, bool REF, bool ALIGNED, bool SPLIT, bool CHUNK,
+          bool POOL = false>
 __global__ __launch_bounds__(256)
 __attribute__((amdgpu_waves_per_eu(GemmTile<T>::BLOCKS_PER_CU)))
 void k_conv_gemm(ConvArgs a) {
@@ -1254,7 +1282,7 @@ void k_conv_gemm(ConvArgs a) {
   static_assert(AV >= 1 && BV >= 1, "stage vectors");
   __shared__ __align__(16) char smem[AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES];
   __shared__ u64 s_kmask;
-  __shared__ int s_site[BM], s_rsk[BM], s_run[BM + 2];
+  __shared__ int s_site[BM], s_rsk[BM], s_run[BM + 2], s_frm[POOL ? BM : 1];
   __shared__ unsigned s_rmax[BM];
   // dense pass: window origin of each row of the tile (n * Hi, oy * sh - ph,
   // ox * sw - pw) and each kernel offset's (ky, kx), so that a neighbour
@@ -1557,8 +1585,10 @@ void k_conv_gemm(ConvArgs a) {
     const int rsk = (!SPLIT && a.mskip && eok)
                         ? (a.dense ? epix : a.mskip[epix])
                         : -1;
-    if (CHUNK && (tid & 3) == 0)
+    if (CHUNK && (tid & 3) == 0) {
       s_site[em] = eok ? (int)((unsigned)epix % (unsigned)a.per) : -1;
+      if (POOL) s_frm[em] = eok ? (int)((unsigned)epix / (unsigned)a.per) : 0;
+    }
 
     // two stages in flight: slot 0 / slot 1 alternate
     uint4 ra0[AV], rb0[BV], ra1[AV], rb1[BV];
@@ -1621,8 +1651,9 @@ void k_conv_gemm(ConvArgs a) {
                   v);
         }
       } else if constexpr (CHUNK) {
-        finish_chunk_tile<T>(a, Cs, CLD, s_run, m0, (int)(m1 - m0), nq,
-                             s_site, s_rsk, s_rmax, q == 0, q == NQ - 1);
+        finish_chunk_tile<T, POOL>(a, Cs, CLD, s_run, m0, (int)(m1 - m0),
+                                   nq, s_site, s_rsk, s_rmax, s_frm, q == 0,
+                                   q == NQ - 1);
       } else {
         auto load_v = [&](int h, float* v) { load8f(crow + 8 * h, v); };
         auto load_po = [&](int h, float* po) {
@@ -1999,7 +2030,7 @@ void k_conv_gemm_big(ConvArgs a) {
       const int rows = (int)((h ? m1 : mh) - hm0);
       finish_chunk_tile<T>(a, Cs + hb0 * CLD + q * kGemmBN, CLD, s_run[h],
                            hm0, rows, n0 + q * kGemmBN, s_site + hb0,
-                           s_rsk + hb0, s_rmax[h], q == 0,
+                           s_rsk + hb0, s_rmax[h], nullptr, q == 0,
                            q == BN / kGemmBN - 1);
     }
   }
@@ -2028,9 +2059,12 @@ static GemmFn pick_gemm(const ConvArgs& a) {
   if (a.ref)
     return aligned ? k_conv_gemm<T, true, true, SPLIT, false>
                    : k_conv_gemm<T, true, false, SPLIT, false>;
-  if (!SPLIT && a.mode == kModeChunkState)  // a build of its own
+  if (!SPLIT && a.mode == kModeChunkState)  // builds of their own
     return aligned ? k_conv_gemm<T, false, true, false, true>
                    : k_conv_gemm<T, false, false, false, true>;
+  if (!SPLIT && a.mode == kModeChunkPool)
+    return aligned ? k_conv_gemm<T, false, true, false, true, true>
+                   : k_conv_gemm<T, false, false, false, true, true>;
   return aligned ? k_conv_gemm<T, false, true, SPLIT, false>
                  : k_conv_gemm<T, false, false, SPLIT, false>;
 }
@@ -2093,7 +2127,8 @@ bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
   if (a.split_max > 1 && !a.part) return false;
   // run-aligned tiles belong to the chunk-state epilogue, which finishes
   // whole tiles itself (no split)
-  if ((a.tstart != nullptr) != (a.mode == kModeChunkState)) return false;
+  if ((a.tstart != nullptr) != chunk_tiled(a.mode)) return false;
+  if (a.mode == kModeChunkPool && (!a.dP || !a.aff)) return false;
   if (a.tstart && (a.split_max > 1 || a.nf < 1 || a.nf > 32 || a.per < 1 ||
                    !a.sites))
     return false;

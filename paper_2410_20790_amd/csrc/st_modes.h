@@ -10,14 +10,23 @@ namespace st {
 // walk each site's frames in order with the state in registers and emit
 // every frame's f(P_t) - f(P_{t-1}).  StateOnly (dense reference pass of a
 // layer whose emitted rows come from elsewhere -- a pool -- or go nowhere --
-// the net's output): store P, emit nothing.
+// the net's output): store P, emit nothing.  ChunkPool (chunk mode, a
+// max-pooled layer, tiles as for ChunkState): walk each site's frames in
+// order and write every frame's state P_t to the row's update row, and
+// the frames that updated the site to a bit mask; the pool emission reads
+// them and the commit stores the last state.
 enum {
   kModeState = 0,
   kModeDefer = 1,
   kModeLinear = 2,
   kModeChunkState = 3,
-  kModeStateOnly = 4
+  kModeStateOnly = 4,
+  kModeChunkPool = 5
 };
+
+constexpr bool chunk_tiled(int mode) {
+  return mode == kModeChunkState || mode == kModeChunkPool;
+}
 
 // Rows per tile step of the run-aligned tiling: a tile starts at the first
 // row of the site run that holds row j * step, so with runs of at most nf

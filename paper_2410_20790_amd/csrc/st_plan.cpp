@@ -291,7 +291,7 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
                                       : 0);
     }
     if (!L.ident) L.off_flags = a.take(round_up(citems, 16));
-    if (F > 1 && L.stateful && !L.pool && !L.dw && !L.se)
+    if (F > 1 && L.stateful && !L.dw && !L.se)
       L.off_tstart = a.take(sizeof(uint32_t) *
                             (citems / chunk_tile_step(F) + 2));
     if (L.pool) L.off_pflags = a.take(round_up(T.grid * F, 16));

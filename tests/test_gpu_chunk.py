@@ -45,7 +45,7 @@ def run_chunks(net, frames, thr, F, tag, max_band=0, frozen_se=False):
             outs = g.encode_chunk(chunk.contiguous(), thr_l)
             torch.cuda.synchronize()
             _, counts = B.st_profile_end(g.handle, L_n)
-            cand_union = [set() for _ in range(L_n + 1)]
+            aff_union = [set() for _ in range(L_n)]
             acts = [B.st_debug_active(g.handle, k - 1) for k in range(L_n + 1)]
             dens0 = [g.density(-1, j * net.batch) for j in range(nf)]
             for j in range(nf):
@@ -58,10 +58,10 @@ def run_chunks(net, frames, thr, F, tag, max_band=0, frozen_se=False):
                 es = rel(outs[j].cpu().numpy(), out_s.cpu().numpy())
                 assert es <= (1e-5 if dt == "f32" else RTOL[dt]), \
                     f"{tag} frame {t + j}: chunk vs frame-by-frame {es}"
+                for k in range(L_n):
+                    aff_union[k] |= set(o.last["layers"][k]["O"].tolist())
                 for k in range(L_n + 1):
                     T = o.last["tensors"][k]
-                    if "cand" in T:
-                        cand_union[k] |= set(T["cand"].tolist())
                     npix = int(np.prod(T["grid"]))
                     a = acts[k]
                     mine = a[(a >= j * npix) & (a < (j + 1) * npix)] - j * npix
@@ -79,11 +79,12 @@ def run_chunks(net, frames, thr, F, tag, max_band=0, frozen_se=False):
                 N, H, W = o.last["tensors"][0]["grid"]
                 d0 = np.sum(o.last["tensors"][0]["pix"] < H * W) / float(H * W)
                 assert abs(dens0[j] - d0) <= 1e-6 + n_band / (H * W)
-            # sites whose state a fused epilogue updated: the union of the
-            # layer's affected outputs over the chunk's frames
+            # sites whose state a fused epilogue (or a pooled layer's)
+            # updated: the union of the layer's affected outputs over the
+            # chunk's frames
             for j in range(L_n):
                 if counts[0, j, 6] and max_band == 0:
-                    assert counts[0, j, 6] == len(cand_union[j + 1]), (
+                    assert counts[0, j, 6] == len(aff_union[j]), (
                         f"{tag} chunk at {t}: layer {j} sites")
             for i in o.P:
                 Pg = B.st_debug_state(g.handle, i, o.P[i].shape)
