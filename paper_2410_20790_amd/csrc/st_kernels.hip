@@ -448,25 +448,22 @@ __device__ __forceinline__ int dense_src(const Geo& g, int64_t o, int k) {
 // order.
 __device__ __forceinline__ void mark_window(uint8_t* flags, int p,
                                             const Geo& g, int nimg, int nf) {
-  const int64_t hwi = (int64_t)g.Hi * g.Wi;
-  const int nn = (int)(p / hwi);
-  const int t = nn / nimg, n = nn - t * nimg;
-  const int rem = (int)(p - nn * hwi);
-  const int iy = rem / g.Wi, ix = rem - (rem / g.Wi) * g.Wi;
-  for (int ky = 0; ky < g.kh; ++ky) {
-    const int ty = iy + g.ph - ky;
-    if (ty < 0) break;
-    if (ty % g.sh) continue;
-    const int oy = ty / g.sh;
-    if (oy >= g.Ho) continue;
-    for (int kx = 0; kx < g.kw; ++kx) {
-      const int tx = ix + g.pw - kx;
-      if (tx < 0) break;
-      if (tx % g.sw) continue;
-      const int ox = tx / g.sw;
-      if (ox >= g.Wo) continue;
-      flags[(((int64_t)n * g.Ho + oy) * g.Wo + ox) * nf + t] = 1;
-    }
+  const unsigned hwi = (unsigned)g.Hi * (unsigned)g.Wi;
+  const unsigned nn = (unsigned)p / hwi;
+  const unsigned rem = (unsigned)p - nn * hwi;
+  const int t = (int)(nn / (unsigned)nimg), n = (int)nn - t * nimg;
+  const int iy = (int)(rem / (unsigned)g.Wi), ix = (int)rem - iy * g.Wi;
+  // outputs o whose window o * s - pad + [0, k) holds the input: o * s in
+  // [i + pad - k + 1, i + pad], 0 <= o < Ho (the lower bound by ceiling
+  // division, which is 0 or less when the bound is)
+  const int ty = iy + g.ph, tx = ix + g.pw;
+  const int ly = ty - g.kh + 1, lx = tx - g.kw + 1;
+  const int oy0 = ly > 0 ? (ly + g.sh - 1) / g.sh : 0;
+  const int ox0 = lx > 0 ? (lx + g.sw - 1) / g.sw : 0;
+  const int oy1 = min(ty / g.sh, g.Ho - 1), ox1 = min(tx / g.sw, g.Wo - 1);
+  for (int oy = oy0; oy <= oy1; ++oy) {
+    const int64_t rowo = ((int64_t)n * g.Ho + oy) * g.Wo;
+    for (int ox = ox0; ox <= ox1; ++ox) flags[(rowo + ox) * nf + t] = 1;
   }
 }
 
@@ -697,24 +694,31 @@ struct FlagPred {
     flags[j] = 0;
     if (rowmax) rowmax[pos] = 0u;
     if (!nbr) return 0u;
-    const int64_t hwo = (int64_t)g.Ho * g.Wo;
-    const int n = (int)(i / hwo);
-    const int rem = (int)(i - n * hwo);
-    const int oy = rem / g.Wo, ox = rem - (rem / g.Wo) * g.Wo;
+    // items stay below 2^31 (grids times frames are bounded at plan time)
+    const unsigned hwo = (unsigned)g.Ho * (unsigned)g.Wo;
+    const unsigned n = (unsigned)i / hwo;
+    const unsigned rem = (unsigned)i - n * hwo;
+    const int oy = (int)(rem / (unsigned)g.Wo), ox = (int)rem - oy * g.Wo;
     const int K = g.kh * g.kw;
+    const int64_t nrow = (int64_t)n * g.Hi;
     unsigned valid = 0;
     // up to 16 window entries at a time: all their loads are issued before
-    // any neighbour-table store (the two may alias for the compiler)
+    // any neighbour-table store (the two may alias for the compiler); the
+    // offsets' (ky, kx) advance without divisions
+    int ky = 0, kx = 0;
     for (int k0 = 0; k0 < K; k0 += 16) {
       int v[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
         const int k = k0 + u;
-        const int ky = k / g.kw, kx = k - (k / g.kw) * g.kw;
         const int iy = oy * g.sh - g.ph + ky, ix = ox * g.sw - g.pw + kx;
         v[u] = -1;
         if (k < K && iy >= 0 && iy < g.Hi && ix >= 0 && ix < g.Wi)
-          v[u] = map_in[((int64_t)n * g.Hi + iy) * g.Wi + ix];
+          v[u] = map_in[(nrow + iy) * g.Wi + ix];
+        if (++kx == g.kw) {
+          kx = 0;
+          ++ky;
+        }
       }
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
