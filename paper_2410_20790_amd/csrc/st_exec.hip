@@ -86,6 +86,18 @@ struct WS {
   template <typename T> T* at(size_t off) const { return (T*)(base + off); }
 };
 
+// Look-back status sets of the compactions: consecutive compactions (all on
+// the encode's stream) alternate between the two, each clearing the other
+// for the one after it; the reset at the start of an encode clears set 0.
+// Called right before each compaction launch, in launch order.
+uint32_t* status_set(st_net* net, uint32_t** clear) {
+  uint32_t* t = WS{net->ws}.at<uint32_t>(net->off_tiles);
+  const int p = net->cpar;
+  net->cpar ^= 1;
+  *clear = t + (p ^ 1) * kMaxTiles;
+  return t + p * kMaxTiles;
+}
+
 st_status hip_check(st_net* net, const char* what) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess)
@@ -208,7 +220,6 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
   const TensorPlan& in = net->tensors[d.src + 1];
   TensorPlan& out = net->tensors[i + 1];
   u64* cnt = ws.at<u64>(net->off_cnt);
-  uint32_t* tiles = ws.at<uint32_t>(net->off_tiles);
   const Prof pf{net, i};
 
   int* O = ws.at<int>(L.off_O);
@@ -231,7 +242,6 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
     FlagArgs fa{};
     fa.flags = ws.at<uint8_t>(L.off_flags);
     fa.npix = L.conv_grid;
-    fa.tiles = tiles;
     fa.list = O;
     fa.map = Mo;
     fa.rowmax = rm_O;
@@ -241,6 +251,7 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
     fa.g = conv_geo(L);
     fa.pairs = cpairs;
     fa.cnt = cO;
+    fa.tiles = status_set(net, &fa.tiles_clear);
     launch_flag_compact(pf, ST_K_RB_COMPACT, s, fa);
   }
 
@@ -297,11 +308,11 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
     FlagArgs fp{};
     fp.flags = pflags;
     fp.npix = out.grid;
-    fp.tiles = tiles;
     fp.list = ws.at<int>(out.off_rowpix);
     fp.map = ws.at<int>(out.off_map);
     fp.rowmax = rowmax_out;
     fp.cnt = cnt + out.cnt_rows;
+    fp.tiles = status_set(net, &fp.tiles_clear);
     launch_flag_compact(pf, ST_K_POOL_COMPACT, s, fp);
     PoolArgs pa{};
     pa.Q = ws.at<int>(out.off_rowpix);
@@ -369,9 +380,9 @@ bool run_layer(st_net* net, int i, bool ref, float thr, const float* thr_dev,
   la.rowpix = ws.at<int>(out.off_rowpix);
   la.act = ws.at<int>(out.off_act);
   la.map = ws.at<int>(out.off_map);
-  la.tiles = tiles;
   la.cnt_act = cnt + out.cnt_act;
   la.cons = consumers_of(net, i + 1);
+  la.tiles = status_set(net, &la.tiles_clear);
   launch_list_compact(pf, s, la);
   // residual carry: the kept rows join the consumers' view
   if (net->carry)
@@ -493,7 +504,9 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
   if (R) ++R->frame;
   (void)hipGetLastError();  // clear any stale error
 
-  launch_reset(pf, s, cnt, net->n_counters);
+  launch_reset(pf, s, cnt, net->n_counters,
+               ws.at<uint32_t>(net->off_tiles));
+  net->cpar = 0;
   // residual carry: the reference frame's rows (every site) become the
   // consumers' whole view
   if (ref && net->carry)
@@ -513,7 +526,6 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
   sa.thr = thr0;
   sa.thr_dev = thr_dev;
   sa.ref = ref ? 1 : 0;
-  sa.tiles = ws.at<uint32_t>(net->off_tiles);
   sa.rows = ws.at<char>(T0.off_rows);
   sa.rowpix = ws.at<int>(T0.off_rowpix);
   sa.act = ws.at<int>(T0.off_act);
@@ -521,6 +533,7 @@ st_status encode(st_net* net, const void* frame, const float* thr, float* out,
   sa.cnt_rows = cnt + T0.cnt_rows;
   sa.cnt_act = cnt + T0.cnt_act;
   sa.cons = consumers_of(net, 0);
+  sa.tiles = status_set(net, &sa.tiles_clear);
   launch_scan(pf, s, net->dtype, sa);
   T0.last_thr = thr0;
   const int nl = (int)net->layers.size();
@@ -592,7 +605,6 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   const TensorPlan& in = net->tensors[d.src + 1];
   TensorPlan& outT = net->tensors[i + 1];
   u64* cnt = ws.at<u64>(net->off_cnt);
-  uint32_t* tiles = ws.at<uint32_t>(net->off_tiles);
   const Prof pf{net, i};
   const int64_t citems = L.conv_grid * nf;
   const int64_t stride = L.conv_grid * net->F;
@@ -621,7 +633,6 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
     FlagArgs fa{};
     fa.flags = ws.at<uint8_t>(L.off_flags);
     fa.npix = citems;
-    fa.tiles = tiles;
     fa.list = O;
     fa.map = Mo;
     fa.rowmax = rm_O;
@@ -637,6 +648,7 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
       fa.tstart = tstart;
       tiles_cut = true;
     }
+    fa.tiles = status_set(net, &fa.tiles_clear);
     launch_flag_compact(pf, ST_K_RB_COMPACT, s, fa);
   }
   if (tiled && !tiles_cut)
@@ -789,13 +801,13 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
     FlagArgs fp{};
     fp.flags = pflags;
     fp.npix = outT.grid * nf;
-    fp.tiles = tiles;
     fp.list = ws.at<int>(outT.off_rowpix);
     fp.map = ws.at<int>(outT.off_map);
     fp.rowmax = rowmax_out;
     fp.cnt = cnt + outT.cnt_rows;
     fp.nf = nf;
     fp.per = outT.grid;
+    fp.tiles = status_set(net, &fp.tiles_clear);
     launch_flag_compact(pf, ST_K_POOL_COMPACT, s, fp);
     ChunkPoolArgs pa{};
     pa.Q = ws.at<int>(outT.off_rowpix);
@@ -833,9 +845,9 @@ bool run_layer_chunk(st_net* net, int i, int nf, float thr,
   la.rowpix = ws.at<int>(outT.off_rowpix);
   la.act = ws.at<int>(outT.off_act);
   la.map = ws.at<int>(outT.off_map);
-  la.tiles = tiles;
   la.cnt_act = cnt + outT.cnt_act;
   la.cons = consumers_of(net, i + 1, true);
+  la.tiles = status_set(net, &la.tiles_clear);
   launch_list_compact(pf, s, la);
   outT.last_thr = thr;
   return true;
@@ -854,7 +866,9 @@ st_status encode_chunk(st_net* net, const void* frames, int nf,
   (void)hipGetLastError();
   net->last_nf = nf;
 
-  launch_reset(pf, s, cnt, net->n_counters);
+  launch_reset(pf, s, cnt, net->n_counters,
+               ws.at<uint32_t>(net->off_tiles));
+  net->cpar = 0;
   TensorPlan& T0 = net->tensors[0];
   ChunkScanArgs sa{};
   sa.x = frames;
@@ -868,7 +882,6 @@ st_status encode_chunk(st_net* net, const void* frames, int nf,
   sa.keep = ws.at<uint8_t>(net->off_flags);
   sa.base = ws.at<uint8_t>(net->off_chunk_base);
   sa.last = ws.at<uint8_t>(net->off_chunk_last);
-  sa.tiles = ws.at<uint32_t>(net->off_tiles);
   sa.rows = ws.at<char>(T0.off_rows);
   sa.rowpix = ws.at<int>(T0.off_rowpix);
   sa.act = ws.at<int>(T0.off_act);
@@ -876,6 +889,7 @@ st_status encode_chunk(st_net* net, const void* frames, int nf,
   sa.cnt_rows = cnt + T0.cnt_rows;
   sa.cnt_act = cnt + T0.cnt_act;
   sa.cons = consumers_of(net, 0);
+  sa.tiles = status_set(net, &sa.tiles_clear);
   launch_chunk_scan(pf, s, net->dtype, sa);
   T0.last_thr = sa.thr;
   const int nl = (int)net->layers.size();

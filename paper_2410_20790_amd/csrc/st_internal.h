@@ -115,7 +115,8 @@ struct st_net {
   size_t ws_bytes = 0;
   size_t off_xhat = 0;                     // storage dtype [N*H*W*C]
   size_t off_flags = 0;                    // uint8 [input grid] keep bytes
-  size_t off_tiles = 0;                    // uint32 [kMaxTiles + 64]
+  size_t off_tiles = 0;                    // uint32 [2][kMaxTiles] statuses
+  int cpar = 0;                            // status set of the next compaction
   size_t off_zero = 0;                     // 256 zero bytes
   size_t off_part = 0;                     // f32 split partials (shared)
   // online threshold adjustment, per produced tensor

@@ -34,7 +34,9 @@ void prof_begin(const Prof& p, int cls, hipStream_t s);
 void prof_end(const Prof& p, int cls, hipStream_t s);
 
 // ---- per-frame bookkeeping
-void launch_reset(const Prof& pf, hipStream_t s, u64* cnt, int n);
+// counters to zero, and the first look-back status set (kCompactMaxTiles)
+void launch_reset(const Prof& pf, hipStream_t s, u64* cnt, int n,
+                  uint32_t* status);
 // dense reference pass: the frame's rows (pixel-ordered, padded to Cp
 // channels) and X_hat = frame; identity kept lists of the tensors (a table
 // of {list offset, length} in the workspace); the frame's counters from a
@@ -92,6 +94,7 @@ struct ScanArgs {
   const float* thr_dev;  // threshold in device memory (or NULL: thr)
   int ref;
   uint32_t* tiles;     // look-back statuses of the compaction
+  uint32_t* tiles_clear;  // the other status set, cleared for the next one
   void* rows;
   int* rowpix;
   int* act;
@@ -107,6 +110,7 @@ struct FlagArgs {
   uint8_t* flags;
   int64_t npix;       // sites of the output grid
   uint32_t* tiles;
+  uint32_t* tiles_clear;
   int* list;
   int* map;
   uint32_t* rowmax;   // or NULL
@@ -233,6 +237,7 @@ struct ListArgs {
   int* act;
   int* map;
   uint32_t* tiles;       // look-back statuses of the compaction
+  uint32_t* tiles_clear;  // the other status set, cleared for the next one
   u64* cnt_act;
   ConsList cons;
 };
@@ -325,6 +330,7 @@ struct ChunkScanArgs {
   uint8_t* base;       // [nf * npix] frame X_hat held (0xFF: chunk start)
   uint8_t* last;       // [npix] last kept frame (0xFF: none)
   uint32_t* tiles;
+  uint32_t* tiles_clear;
   void* rows;
   int* rowpix;
   int* act;

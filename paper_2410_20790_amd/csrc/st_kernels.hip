@@ -120,8 +120,10 @@ __device__ __forceinline__ int64_t read_count(const u64* dev, int64_t host) {
 // evaluated its items, then sums the published counts of its predecessors
 // (lookback_offset).  Blocks are dispatched in index order, so every tile a
 // block waits for has been dispatched before it, and it publishes without
-// waiting on anything.  The statuses start at zero; the last live block to
-// finish clears them (and its arrival counter) for the next compaction.
+// waiting on anything.  The statuses start at zero: compactions use two
+// status sets in turn, and each one's blocks clear the set it does not use
+// (a slice each), for the next compaction; the per-encode reset clears the
+// first set.  No block waits for the others to finish.
 //
 // The predicate's item data (P::Item, from P::load) is requested together
 // with the item count -- all loads stay within the capacity `cap`, and which
@@ -233,7 +235,7 @@ template <class P, int IPT>
 __global__ __launch_bounds__(256) void k_compact(const u64* n_dev,
                                                  int64_t n_host, int64_t cap,
                                                  int tile, uint32_t* status,
-                                                 uint32_t* done, u64* out_cnt,
+                                                 uint32_t* clear, u64* out_cnt,
                                                  u64* out_cnt2, P pred) {
   using Item = typename P::Item;
   // tile offsets of the kept items (tile <= kMaxItemsPerThread * 256)
@@ -241,8 +243,14 @@ __global__ __launch_bounds__(256) void k_compact(const u64* n_dev,
   // IPT > 0: the kept items themselves, in position order (their emit
   // reads them here instead of loading them again)
   __shared__ Item kitem[IPT > 0 ? 256 * IPT : 1];
-  __shared__ int s_clear;
   const int64_t base = (int64_t)blockIdx.x * tile;
+  {
+    // this block's slice of the other status set, for the next compaction
+    const unsigned per = (kCompactMaxTiles + gridDim.x - 1) / gridDim.x;
+    const unsigned lo = blockIdx.x * per;
+    const unsigned hi = min(lo + per, (unsigned)kCompactMaxTiles);
+    for (unsigned j = lo + threadIdx.x; j < hi; j += 256) clear[j] = 0u;
+  }
   const int ipt = IPT > 0 ? IPT : (tile + 255) / 256;
   const int64_t first = base + (int64_t)threadIdx.x * ipt;
   Item it[IPT > 0 ? IPT : 1];
@@ -338,20 +346,6 @@ __global__ __launch_bounds__(256) void k_compact(const u64* n_dev,
       if (out_cnt2) *out_cnt2 = total;
       pred.finish(total);
     }
-    // every live tile has read the statuses it needed once it arrives
-    const unsigned live = (unsigned)((n + tile - 1) / tile);
-    s_clear = __hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED,
-                                     __HIP_MEMORY_SCOPE_AGENT) == live - 1;
-  }
-  __syncthreads();
-  if (s_clear) {
-    const unsigned live = (unsigned)((n + tile - 1) / tile);
-    for (unsigned j = threadIdx.x; j < live; j += 256)
-      __hip_atomic_store(status + j, 0u, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-    if (threadIdx.x == 0)
-      __hip_atomic_store(done, 0u, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -401,22 +395,22 @@ bool compact_runs_fit(int64_t cap, int run) {
          256 * kMaxItemsPerThread;
 }
 
-// One compaction launch.  `tiles` holds the kMaxTiles look-back statuses
-// followed by the arrival counter.
+// One compaction launch on the kCompactMaxTiles look-back statuses `tiles`;
+// it clears the other set, `clear`, for the next compaction.
 template <class P>
 static void run_compact(const Prof& pf, int cls, hipStream_t s,
                         const u64* n_dev, int64_t n_host, int64_t cap,
-                        uint32_t* tiles, u64* out_cnt, u64* out_cnt2, P pred,
-                        int run = 0, int max_tiles = kCompactMaxTiles) {
+                        uint32_t* tiles, uint32_t* clear, u64* out_cnt,
+                        u64* out_cnt2, P pred, int run = 0,
+                        int max_tiles = kCompactMaxTiles) {
   const int tile = (int)compact_tile(cap, run, max_tiles);
   const int nt = compact_tiles(cap, run, max_tiles);
-  uint32_t* done = tiles + kCompactMaxTiles;
   prof_begin(pf, cls, s);
   if ((tile + 255) / 256 == 2)
-    k_compact<P, 2><<<nt, 256, 0, s>>>(n_dev, n_host, cap, tile, tiles, done,
+    k_compact<P, 2><<<nt, 256, 0, s>>>(n_dev, n_host, cap, tile, tiles, clear,
                                        out_cnt, out_cnt2, pred);
   else
-    k_compact<P, 0><<<nt, 256, 0, s>>>(n_dev, n_host, cap, tile, tiles, done,
+    k_compact<P, 0><<<nt, 256, 0, s>>>(n_dev, n_host, cap, tile, tiles, clear,
                                        out_cnt, out_cnt2, pred);
   prof_end(pf, cls, s);
 }
@@ -553,7 +547,7 @@ static void scan_t(const Prof& pf, hipStream_t s, const ScanArgs& a) {
   ScanPred<T> p{(const T*)a.x, (T*)a.xhat, (T*)a.rows, a.rowpix, a.act,
                 a.map, a.C, a.Cp, a.ref, a.thr, a.thr_dev, a.cons};
   run_compact(pf, 1 /*ST_K_SCAN_COMPACT*/, s, nullptr, a.npix, a.npix,
-              a.tiles, a.cnt_rows, a.cnt_act, p);
+              a.tiles, a.tiles_clear, a.cnt_rows, a.cnt_act, p);
 }
 
 void launch_scan(const Prof& pf, hipStream_t s, int dtype,
@@ -745,7 +739,8 @@ void launch_flag_compact(const Prof& pf, int cls, hipStream_t s,
                          const FlagArgs& a) {
   FlagPred p{a.flags, a.list, a.map, a.rowmax, a.nbr, a.map_in, a.stride,
              a.g, a.pairs, a.nf, a.per, a.tstart};
-  run_compact(pf, cls, s, nullptr, a.npix, a.npix, a.tiles, a.cnt, nullptr,
+  run_compact(pf, cls, s, nullptr, a.npix, a.npix, a.tiles, a.tiles_clear,
+              a.cnt, nullptr,
               p, a.tstart ? a.nf : 0, kSparseCompactTiles);
 }
 
@@ -2440,6 +2435,7 @@ struct ListPred {
 void launch_list_compact(const Prof& pf, hipStream_t s, const ListArgs& a) {
   ListPred p{a.rowmax, a.rowpix, a.act, a.map, a.thr, a.thr_dev, a.cons};
   run_compact(pf, 15 /*ST_K_LIST_COMPACT*/, s, a.n_rows, 0, a.cap, a.tiles,
+              a.tiles_clear,
               a.cnt_act, nullptr, p);
 }
 
@@ -3055,6 +3051,7 @@ static void chunk_scan_t(const Prof& pf, hipStream_t s,
                      a.npix, a.cons};
   const int64_t items = (int64_t)a.nf * a.npix;
   run_compact(pf, 1 /*ST_K_SCAN_COMPACT*/, s, nullptr, items, items, a.tiles,
+              a.tiles_clear,
               a.cnt_rows, a.cnt_act, p);
   prof_begin(pf, 1 /*ST_K_SCAN_COMPACT*/, s);
   k_chunk_xhat_commit<T><<<grid_for(a.npix, 4096), 256, 0, s>>>(a);
@@ -3537,13 +3534,16 @@ void launch_flip_parity(hipStream_t s, int* par) {
 }
 
 // ------------------------------------------------------- bookkeeping
-__global__ void k_reset(u64* cnt, int n) {
+__global__ void k_reset(u64* cnt, int n, uint32_t* status) {
   for (int i = threadIdx.x; i < n; i += blockDim.x) cnt[i] = 0ull;
+  for (int i = threadIdx.x; i < kCompactMaxTiles; i += blockDim.x)
+    status[i] = 0u;
 }
 
-void launch_reset(const Prof& pf, hipStream_t s, u64* cnt, int n) {
+void launch_reset(const Prof& pf, hipStream_t s, u64* cnt, int n,
+                  uint32_t* status) {
   prof_begin(pf, 18 /*ST_K_RESET*/, s);
-  k_reset<<<1, 256, 0, s>>>(cnt, n);
+  k_reset<<<1, 256, 0, s>>>(cnt, n, status);
   prof_end(pf, 18, s);
 }
 

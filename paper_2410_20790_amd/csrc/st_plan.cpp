@@ -221,7 +221,7 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
   net->off_cnt = a.take(sizeof(uint64_t) * net->n_counters);
   net->off_dens = a.take(sizeof(uint64_t) * batch * F);
   // compaction look-back statuses, then its arrival counter
-  net->off_tiles = a.take(sizeof(uint32_t) * (kMaxTiles + 64));
+  net->off_tiles = a.take(sizeof(uint32_t) * 2 * kMaxTiles);
   net->off_se_par = a.take(sizeof(int));
   net->off_xhat = a.take((size_t)t0.grid * in_c * net->esize);
   // Per-site buffers of the emitted tensors and rulebooks hold F frames
