@@ -33,8 +33,8 @@ constexpr bool chunk_tiled(int mode) {
 // rows (nf <= 32) no tile exceeds 64 rows and none is empty.
 constexpr int chunk_tile_step(int nf) { return 65 - nf; }
 
-// Tiles of one compaction pass at most (its look-back statuses; the
-// arrival counter follows them).
+// Tiles of one compaction pass at most (the look-back statuses of a set;
+// compactions alternate between two sets).
 constexpr int kCompactMaxTiles = 4096;
 
 // Partial counters per layer for the sites a chunk's fused epilogue

@@ -220,7 +220,7 @@ static st_status create_impl(const st_layer_desc* layers, int32_t n_layers,
   net->n_counters = 2 * (L_n + 1) + (2 + kSiteSlots) * L_n;
   net->off_cnt = a.take(sizeof(uint64_t) * net->n_counters);
   net->off_dens = a.take(sizeof(uint64_t) * batch * F);
-  // compaction look-back statuses, then its arrival counter
+  // the two sets of compaction look-back statuses
   net->off_tiles = a.take(sizeof(uint32_t) * 2 * kMaxTiles);
   net->off_se_par = a.take(sizeof(int));
   net->off_xhat = a.take((size_t)t0.grid * in_c * net->esize);
