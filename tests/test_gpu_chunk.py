@@ -273,3 +273,99 @@ def test_chunk_long_reductions(dtype):
     net = long_reduction_net(dtype)
     frames = random_sparse_video(31, 7, 1, 40, 56, 16, 0.1, dtype=dtype)
     run_chunks(net, frames, 0.0, 4, f"long reductions {dtype}", max_band=8)
+
+
+def _conv_state_shape(g, net, i):
+    """Shape of layer i's pre-activation state: its convolution's output
+    grid (before any pooling) by its output channels."""
+    L = net.layers[i]
+    N, H, W, _ = g.tensor_shape(L.src)
+    Ho = (H + 2 * L.p[0] - L.k[0]) // L.s[0] + 1
+    Wo = (W + 2 * L.p[1] - L.k[1]) // L.s[1] + 1
+    return (N, Ho, Wo, L.c_out)
+
+
+@pytest.mark.parametrize("which", ["toy", "resnet_mini", "long_reductions"])
+def test_graph_replay_chunk_matches_eager(which):
+    """A chunk encode (st_encode_chunk) captured once as a HIP graph and
+    replayed for consecutive chunks, and again after a reference frame
+    encoded directly, gives bitwise the eager net's results: every frame's
+    output, the kept and candidate lists of every tensor, and every
+    layer's state after each chunk (each replay separated by eager work
+    and a synchronisation).  The replays rerun the same compactions, whose
+    look-back statuses alternate between two sets that each compaction
+    clears for the next."""
+    F = 4
+    if which == "toy":
+        net, frames, thr = toy_net(), toy_video(seed=21, n_frames=14), 0.0
+    elif which == "resnet_mini":
+        net = resnet_mini_net()
+        frames = random_sparse_video(22, 14, 1, 32, 48, 3, 0.08)
+        thr = 0.0
+    else:
+        net = long_reduction_net("bf16")
+        frames = random_sparse_video(23, 14, 1, 40, 56, 16, 0.1,
+                                     dtype="bf16")
+        thr = 0.0
+    dt = net.dtype
+    L_n = len(net.layers)
+    thr_l = [thr] * (L_n + 1)
+    ge = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt,
+                      max_frames=F)
+    gg = SparseTemNet(net.layers, net.batch, net.H, net.W, net.C, dt,
+                      max_frames=F)
+    try:
+        say(f"[gpu] chunk graph replay {which}")
+        dev = [to_dev(f, dt) for f in frames]
+        ge.encode_reference(dev[0])
+        gg.encode_reference(dev[0])
+        torch.cuda.synchronize()
+        slot = torch.zeros((F,) + tuple(gg.in_shape), dtype=gg.tdtype,
+                           device=gg.device)
+        out_g = torch.empty((F,) + tuple(gg.out_shape), dtype=torch.float32,
+                            device=gg.device)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            gg.encode_chunk(slot, thr_l, out=out_g)
+        # chunks at frames 1 and 5 back to back, a reference frame at 9
+        # encoded directly, a chunk at 10
+        for t in (1, 5, 9, 10):
+            if t == 9:
+                ge.encode_reference(dev[t])
+                gg.encode_reference(dev[t])
+                torch.cuda.synchronize()
+                continue
+            chunk = torch.stack(dev[t:t + F]).contiguous()
+            out_e = ge.encode_chunk(chunk, thr_l)
+            torch.cuda.synchronize()
+            slot.copy_(chunk)
+            graph.replay()
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(out_g.cpu().numpy(),
+                                          out_e.cpu().numpy(),
+                                          err_msg=f"{which} chunk at {t}")
+            for k in range(L_n + 1):
+                np.testing.assert_array_equal(
+                    B.st_debug_active(gg.handle, k - 1),
+                    B.st_debug_active(ge.handle, k - 1),
+                    err_msg=f"{which} chunk at {t}: kept list {k}")
+                C = ge.tensor_shape(k - 1)[3]
+                pg, rg = B.st_debug_candidates(gg.handle, k - 1, C)
+                pe, re_ = B.st_debug_candidates(ge.handle, k - 1, C)
+                np.testing.assert_array_equal(pg, pe)
+                np.testing.assert_array_equal(rg, re_)
+            n_state = 0
+            for i in range(L_n):
+                shape = _conv_state_shape(ge, net, i)
+                try:
+                    Pe = B.st_debug_state(ge.handle, i, shape)
+                except B.StError:
+                    continue  # a layer without state
+                Pg = B.st_debug_state(gg.handle, i, shape)
+                np.testing.assert_array_equal(
+                    Pg, Pe, err_msg=f"{which} chunk at {t}: state {i}")
+                n_state += 1
+            assert n_state >= 1, f"{which}: no state compared"
+    finally:
+        ge.close()
+        gg.close()
