@@ -169,15 +169,17 @@ __device__ __forceinline__ unsigned block_exclusive_scan(unsigned v,
 }
 
 // Bound on a look-back wait, in sleeps of ~128 cycles (~1 s in all): a
-// wait never runs that long, as the waited-for tile is already dispatched;
-// the bound only guarantees that every wave exits.
+// wait never runs that long, as the waited-for tile is already dispatched
+// and publishes before it waits for anything; the bound only guarantees
+// that every wave exits (a wait that expired would leave its tile's offset
+// short of the counts it did not see).
 constexpr int kLbSpinLimit = 1 << 23;
 
 // Predicates with P::kRanked cut run-aligned row tiles while they emit: the
 // items form runs of pred.run_len() consecutive indices (a chunk's frames of
 // one site), the pass's tiles hold whole runs, and where pred.rank_needed
-// asks for it the write pass hands pred.emit_ranked the number of kept
-// items of the same run before the item.
+// asks for it the emit hands pred.emit_ranked the number of kept items of
+// the same run before the item.
 template <class P, class = void>
 struct IsRanked : std::false_type {};
 template <class P>
