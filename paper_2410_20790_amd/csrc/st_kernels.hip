@@ -2987,6 +2987,70 @@ __global__ __launch_bounds__(256) void k_chunk_scan_prep(ChunkScanArgs a) {
   }
 }
 
+// The same decisions for three-channel (RGB) half-precision frames, eight
+// sites per thread: a frame's 24 values of the eight sites arrive as three
+// 16-byte loads, and the base bytes of each frame, the sites' keep bytes
+// (8·nf consecutive bytes, site-major) and their last bytes leave as 8-byte
+// words.  Requires npix a multiple of 8 and aligned buffers (the launcher
+// checks).
+template <typename T>
+__global__ __launch_bounds__(256) void k_chunk_scan_prep_rgb8(
+    ChunkScanArgs a) {
+  static_assert(sizeof(T) == 2, "half-precision frames");
+  const T* x = (const T*)a.x;
+  const T* xhat = (const T*)a.xhat;
+  const float thr = a.thr_dev ? *a.thr_dev : a.thr;
+  const int64_t groups = a.npix / 8;
+  for (int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x; g < groups;
+       g += (int64_t)gridDim.x * 256) {
+    const int64_t p0 = g * 8;
+    float xh[24];
+#pragma unroll
+    for (int v = 0; v < 3; ++v)
+      Vec8Half<T>::load(xhat + p0 * 3 + 8 * v, xh + 8 * v);
+    uint32_t kb[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) kb[j] = 0u;
+    uint64_t cur = ~0ull;  // byte j: the frame X_hat of site j holds
+    for (int t = 0; t < a.nf; ++t) {
+      const T* xt = x + ((int64_t)t * a.npix + p0) * 3;
+      float xv[24];
+#pragma unroll
+      for (int v = 0; v < 3; ++v) Vec8Half<T>::load(xt + 8 * v, xv + 8 * v);
+      *(uint64_t*)(a.base + (int64_t)t * a.npix + p0) = cur;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        float m = 0.f;
+#pragma unroll
+        for (int c = 0; c < 3; ++c)
+          m = fmaxf(m, fabsf(xv[3 * j + c] - xh[3 * j + c]));
+        if (m > thr) {
+          kb[j] |= 1u << t;
+#pragma unroll
+          for (int c = 0; c < 3; ++c) xh[3 * j + c] = xv[3 * j + c];
+          cur = (cur & ~(0xFFull << (8 * j))) | ((uint64_t)t << (8 * j));
+        }
+      }
+    }
+    *(uint64_t*)(a.last + p0) = cur;
+    // keep bytes of the eight sites, site-major: 8·nf bytes from p0·nf
+    uint64_t* kp = (uint64_t*)(a.keep + p0 * a.nf);
+    uint64_t w = 0ull;
+    int nb = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      for (int t = 0; t < a.nf; ++t) {
+        w |= (uint64_t)((kb[j] >> t) & 1u) << (8 * nb);
+        if (++nb == 8) {
+          *kp++ = w;
+          w = 0ull;
+          nb = 0;
+        }
+      }
+    }
+  }
+}
+
 template <typename T>
 struct ChunkScanPred {
   const T* x;
@@ -3046,7 +3110,18 @@ template <typename T>
 static void chunk_scan_t(const Prof& pf, hipStream_t s,
                          const ChunkScanArgs& a) {
   prof_begin(pf, 0 /*ST_K_SCAN_MASK*/, s);
-  k_chunk_scan_prep<T><<<grid_for(a.npix, 4096), 256, 0, s>>>(a);
+  bool rgb8 = false;
+  if constexpr (sizeof(T) == 2) {
+    rgb8 = a.C == 3 && a.npix % 8 == 0 &&
+           (((uintptr_t)a.x | (uintptr_t)a.xhat) & 15) == 0 &&
+           (((uintptr_t)a.keep | (uintptr_t)a.base | (uintptr_t)a.last) &
+            7) == 0;
+    if (rgb8)
+      k_chunk_scan_prep_rgb8<T>
+          <<<grid_for(a.npix / 8, 4096), 256, 0, s>>>(a);
+  }
+  if (!rgb8)
+    k_chunk_scan_prep<T><<<grid_for(a.npix, 4096), 256, 0, s>>>(a);
   prof_end(pf, 0, s);
   ChunkScanPred<T> p{(const T*)a.x, (const T*)a.xhat, a.keep, a.base,
                      (T*)a.rows, a.rowpix, a.act, a.map, a.C, a.Cp, a.nf,
