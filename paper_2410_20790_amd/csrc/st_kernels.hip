@@ -2051,6 +2051,158 @@ static void split_epi_t(hipStream_t s, int grid, const ConvArgs& a) {
     k_split_epi<T, false><<<grid, 256, 0, s>>>(a);
 }
 
+// ------------------------------------------------ dense stem (reference)
+// Dense reference pass of a 7x7 stride-2 convolution over rows of at most
+// four channels (a ResNet stem) with at most 64 output channels.  A tile is
+// 64 consecutive output pixels of one output row.  The tile's input window
+// -- 7 rows by 136 pixels of 4 channels, zeros outside the image -- is
+// staged once in LDS, and each 32-wide reduction step is one kernel row:
+// offsets kx = 0..7 of 4 channels, kx = 7 against a zero weight, so a
+// lane's eight values (offsets 2 lg and 2 lg + 1) are two adjacent staged
+// pixels.  The weights are staged once per block in that order.  Tiles are
+// finished as the reference build finishes its tiles.
+constexpr int kStemBM = 64, kStemPW = 136;  // tile pixels, staged row pixels
+
+template <typename T>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
+void k_stem_dense(ConvArgs a) {
+  static_assert(sizeof(T) == 2, "half-precision stem");
+  constexpr int BM = kStemBM, BN = 64, KS = 7, KR = 32;  // 7 steps of 32
+  constexpr int BLD = KS * KR + 8;  // staged weight row
+  constexpr int CLD = BN + 4;       // f32 accumulator row
+  constexpr size_t PATCH_BYTES = (size_t)KS * kStemPW * 4 * sizeof(T);
+  constexpr size_t C_BYTES = (size_t)BM * CLD * sizeof(float);
+  __shared__ __align__(16) T sB[BN * BLD];
+  // the staged window, and (after the products) the accumulator tile
+  __shared__ __align__(16) char smem[PATCH_BYTES > C_BYTES ? PATCH_BYTES
+                                                           : C_BYTES];
+  T* const sP = (T*)smem;          // [KS][kStemPW][4]
+  float* const Cs = (float*)smem;  // [BM][CLD]
+  const T* din = (const T*)a.din;
+  const T* wt = (const T*)a.w;
+  const T* dskip = (const T*)a.dskip;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l16 = lane & 15, lg = lane >> 4;
+  const int cout_p = a.cout_p;
+  const Geo g = a.g;
+  // B[n][ky*32 + kx*4 + c] = w[n][(ky*7 + kx)*4 + c] for kx < 7, else 0
+  for (int e = tid; e < BN * KS * KR; e += 256) {
+    const int n = e / (KS * KR), r = e - n * (KS * KR);
+    const int ky = r / KR, q = r - ky * KR, kx = q >> 2, c = q & 3;
+    T v = zero_v<T>();
+    if (n < cout_p && kx < 7)
+      v = wt[(int64_t)n * a.ktot_p + (ky * 7 + kx) * 4 + c];
+    sB[n * BLD + r] = v;
+  }
+  const int tiles_x = (g.Wo + BM - 1) / BM;
+  const int64_t ntiles = a.capO / g.Wo * tiles_x;  // output rows x tiles
+  // XCD-aware order, as in k_conv_gemm
+  const int chunk = (int)((ntiles + kXcd - 1) / kXcd);
+  const int xcd = blockIdx.x % kXcd;
+  const int u_end = (int)min(ntiles, (int64_t)(xcd + 1) * chunk);
+  const int per_xcd = gridDim.x / kXcd;
+  const int em = tid >> 2, ec = (tid & 3) * 16;
+  for (int u = xcd * chunk + blockIdx.x / kXcd; u < u_end; u += per_xcd) {
+    const int row = u / tiles_x;  // image * Ho + output row
+    const int ox0 = (u - row * tiles_x) * BM;
+    const int img = row / g.Ho, oy = row - img * g.Ho;
+    const int iy0 = oy * 2 - g.ph, ix0 = ox0 * 2 - g.pw;
+    __syncthreads();  // the weights are staged; the last tile's reads done
+    for (int e = tid; e < KS * kStemPW; e += 256) {
+      const int ky = e / kStemPW, px = e - ky * kStemPW;
+      const int iy = iy0 + ky, ix = ix0 + px;
+      uint2 v = make_uint2(0u, 0u);
+      if (iy >= 0 && iy < g.Hi && ix >= 0 && ix < g.Wi)
+        v = *(const uint2*)(din +
+                            ((int64_t)(img * g.Hi + iy) * g.Wi + ix) * 4);
+      *(uint2*)(sP + (ky * kStemPW + px) * 4) = v;
+    }
+    __syncthreads();
+    v4f acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ky = 0; ky < KS; ++ky) {
+      uint4 av[2], bv[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int m = wm * 32 + i * 16 + l16;
+        av[i] = *(const uint4*)(sP + (ky * kStemPW + 2 * m + 2 * lg) * 4);
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int nn = wn * 32 + j * 16 + l16;
+        bv[j] = *(const uint4*)(sB + nn * BLD + ky * KR + 8 * lg);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          if constexpr (__is_same(T, _Float16)) {
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                __builtin_bit_cast(v8h, av[i]), __builtin_bit_cast(v8h, bv[j]),
+                acc[i][j], 0, 0, 0);
+          } else {
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(v8bf, av[i]),
+                __builtin_bit_cast(v8bf, bv[j]), acc[i][j], 0, 0, 0);
+          }
+        }
+      }
+    }
+    __syncthreads();  // every wave has read the window (Cs reuses it)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          Cs[(wm * 32 + i * 16 + 4 * lg + r) * CLD + wn * 32 + j * 16 + l16] =
+              acc[i][j][r];
+    __syncthreads();
+    // thread -> pixel em of the tile, columns [ec, ec + 16)
+    const int ox = ox0 + em;
+    const bool eok = ox < g.Wo;
+    const int64_t eo = (int64_t)row * g.Wo + ox;
+    const int epix = eok ? (int)eo : 0;
+    const int rsk = (a.mskip && eok) ? epix : -1;
+    const float* crow = Cs + em * CLD + ec;
+    bool hv[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) hv[h] = eok && ec + 8 * h < cout_p;
+    auto load_v = [&](int h, float* v) { load8f(crow + 8 * h, v); };
+    auto load_po = [&](int, float* po) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) po[e] = 0.f;
+    };
+    auto load_sk = [&](int h, float* sk) {
+      if (rsk >= 0) {
+        Vec8<T>::load(dskip + (int64_t)rsk * cout_p + ec + 8 * h, sk);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sk[e] = 0.f;
+      }
+    };
+    float rm = 0.f;
+    with_act(a.act, [&](auto act_tag) {
+      rm = finish_cols<T, true, decltype(act_tag)::value>(
+          a, load_v, load_po, load_sk, hv, eo, epix, 0, ec);
+    });
+    finish_rows(a, rm, eo, eok);
+  }
+}
+
+// The dense reference pass's stem takes k_stem_dense: half precision, 7x7
+// stride 2 over rows of 4 (padded) channels, at most 64 output channels.
+static bool stem_dense(int dtype, const ConvArgs& a) {
+  return dtype != 0 && a.ref && a.dense && a.K == 49 && a.cin_p == 4 &&
+         a.cout_p <= 64 && a.g.kh == 7 && a.g.kw == 7 && a.g.sh == 2 &&
+         a.g.sw == 2 && a.split_max <= 1 && a.g.Wo > 0;
+}
+
 using GemmFn = void (*)(ConvArgs);
 
 // The gather-GEMM build for a launch.
@@ -2133,6 +2285,17 @@ bool launch_conv_gemm(const Prof& pf, hipStream_t s, int dtype,
   if (a.tstart && (a.split_max > 1 || a.nf < 1 || a.nf > 32 || a.per < 1 ||
                    !a.sites))
     return false;
+  if (stem_dense(dtype, a)) {
+    const int64_t units =
+        a.capO / a.g.Wo * ((a.g.Wo + kStemBM - 1) / kStemBM);
+    const GemmFn fn = dtype == 1 ? (GemmFn)k_stem_dense<_Float16>
+                                 : (GemmFn)k_stem_dense<bf16_t>;
+    const int grid = persistent_grid(units, (const void*)fn, 0, 3);
+    prof_begin(pf, 7 /*ST_K_CONV_GEMM*/, s);
+    fn<<<grid, 256, 0, s>>>(a);
+    prof_end(pf, 7, s);
+    return true;
+  }
   if (use_big(dtype, a)) {
     const int64_t halves =
         (a.capO + chunk_tile_step(a.nf) - 1) / chunk_tile_step(a.nf);
