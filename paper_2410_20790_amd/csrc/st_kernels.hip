@@ -2059,8 +2059,10 @@ static void split_epi_t(hipStream_t s, int grid, const ConvArgs& a) {
 // staged once in LDS, and each 32-wide reduction step is one kernel row:
 // offsets kx = 0..7 of 4 channels, kx = 7 against a zero weight, so a
 // lane's eight values (offsets 2 lg and 2 lg + 1) are two adjacent staged
-// pixels.  The weights are staged once per block in that order.  Tiles are
-// finished as the reference build finishes its tiles.
+// pixels.  The weights are staged once per block in that order.  A tile's
+// window is requested before the previous tile's epilogue, so that it
+// arrives while that epilogue runs.  Tiles are finished as the reference
+// build finishes its tiles.
 constexpr int kStemBM = 64, kStemPW = 136;  // tile pixels, staged row pixels
 
 template <typename T>
@@ -2103,20 +2105,35 @@ void k_stem_dense(ConvArgs a) {
   const int u_end = (int)min(ntiles, (int64_t)(xcd + 1) * chunk);
   const int per_xcd = gridDim.x / kXcd;
   const int em = tid >> 2, ec = (tid & 3) * 16;
-  for (int u = xcd * chunk + blockIdx.x / kXcd; u < u_end; u += per_xcd) {
-    const int row = u / tiles_x;  // image * Ho + output row
+  // this thread's share of a tile's window: entries tid + 256 q
+  constexpr int WQ = (KS * kStemPW + 255) / 256;
+  auto fetch_window = [&](int u, uint2 (&w)[WQ]) {
+    const int row = u / tiles_x;
     const int ox0 = (u - row * tiles_x) * BM;
     const int img = row / g.Ho, oy = row - img * g.Ho;
     const int iy0 = oy * 2 - g.ph, ix0 = ox0 * 2 - g.pw;
-    __syncthreads();  // the weights are staged; the last tile's reads done
-    for (int e = tid; e < KS * kStemPW; e += 256) {
+#pragma unroll
+    for (int q = 0; q < WQ; ++q) {
+      const int e = tid + 256 * q;
       const int ky = e / kStemPW, px = e - ky * kStemPW;
       const int iy = iy0 + ky, ix = ix0 + px;
-      uint2 v = make_uint2(0u, 0u);
-      if (iy >= 0 && iy < g.Hi && ix >= 0 && ix < g.Wi)
-        v = *(const uint2*)(din +
-                            ((int64_t)(img * g.Hi + iy) * g.Wi + ix) * 4);
-      *(uint2*)(sP + (ky * kStemPW + px) * 4) = v;
+      w[q] = make_uint2(0u, 0u);
+      if (e < KS * kStemPW && iy >= 0 && iy < g.Hi && ix >= 0 && ix < g.Wi)
+        w[q] = *(const uint2*)(din +
+                               ((int64_t)(img * g.Hi + iy) * g.Wi + ix) * 4);
+    }
+  };
+  uint2 win[WQ];
+  const int u0 = xcd * chunk + blockIdx.x / kXcd;
+  if (u0 < u_end) fetch_window(u0, win);
+  for (int u = u0; u < u_end; u += per_xcd) {
+    const int row = u / tiles_x;  // image * Ho + output row
+    const int ox0 = (u - row * tiles_x) * BM;
+    __syncthreads();  // the weights are staged; the last tile's reads done
+#pragma unroll
+    for (int q = 0; q < WQ; ++q) {
+      const int e = tid + 256 * q;
+      if (e < KS * kStemPW) *(uint2*)(sP + e * 4) = win[q];
     }
     __syncthreads();
     v4f acc[2][2];
@@ -2153,6 +2170,7 @@ void k_stem_dense(ConvArgs a) {
         }
       }
     }
+    if (u + per_xcd < u_end) fetch_window(u + per_xcd, win);
     __syncthreads();  // every wave has read the window (Cs reuses it)
 #pragma unroll
     for (int i = 0; i < 2; ++i)
