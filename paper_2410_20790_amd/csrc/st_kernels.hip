@@ -1468,18 +1468,35 @@ void k_conv_gemm(ConvArgs a) {
     // its loads (inactive neighbours, columns past cout_p and stages past
     // the end read a zero vector), so the loads of the next two stages can
     // stay in flight while the current one is staged and multiplied.
+    // ALIGNED: the gathered rows of this thread's A vectors (row pointers,
+    // NULL for an inactive neighbour) are kept for the current kernel
+    // offset, so a stage within it neither reads the neighbour table nor
+    // rebuilds the row addresses.
+    const T* arow[AV];
+    int arow_kc = -1;
     auto load_stage = [&](const It& it, uint4 (&ra)[AV], uint4 (&rb)[BV]) {
       const bool live = it.st < st_hi;
       const int r0 = it.st * KC;
+      if (ALIGNED && live && it.kc != arow_kc) {
+        arow_kc = it.kc;
+#pragma unroll
+        for (int q = 0; q < AV; ++q) {
+          const int m = (tid + q * 256) / VPR;
+          const int src = s_nbr[arow_kc * BM + m];
+          arow[q] = src >= 0 ? din + (int64_t)src * cin_p : nullptr;
+        }
+      }
 #pragma unroll
       for (int q = 0; q < AV; ++q) {
         const int v = tid + q * 256;
         const int m = v / VPR, cv = v - (v / VPR) * VPR;
-        int k, ci;
         if (ALIGNED) {
-          k = it.kc;
-          ci = it.sub * KC + cv * VEC;
-        } else {
+          const T* row = live ? arow[q] : nullptr;
+          ra[q] = *(const uint4*)(row ? row + it.sub * KC + cv * VEC : zvec);
+          continue;
+        }
+        int k, ci;
+        {
           const int r = r0 + cv * VEC;
           k = r / cin_p;
           ci = r - k * cin_p;
