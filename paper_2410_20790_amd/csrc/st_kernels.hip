@@ -1904,18 +1904,28 @@ void k_conv_gemm_big(ConvArgs a) {
       it.st = it.kc < K ? it.kc * spk + it.sub : nst;
       return it;
     };
+    // the gathered rows of this thread's A vectors, kept for the current
+    // kernel offset (NULL: inactive neighbour)
+    const T* arow[AV];
+    int arow_kc = -1;
     auto load_stage = [&](const It& it, uint4 (&ra)[AV], uint4 (&rb)[BV]) __attribute__((always_inline)) {
       const bool live = it.st < nst;
       const int r0 = it.st * KC;
+      if (live && it.kc != arow_kc) {
+        arow_kc = it.kc;
+#pragma unroll
+        for (int q = 0; q < AV; ++q) {
+          const int m = (tid + q * 256) / VPR;
+          const int src = s_nbr[arow_kc * BM + m];
+          arow[q] = src >= 0 ? din + (int64_t)src * cin_p : nullptr;
+        }
+      }
 #pragma unroll
       for (int q = 0; q < AV; ++q) {
         const int v = tid + q * 256;
-        const int m = v / VPR, cv = v - (v / VPR) * VPR;
-        const int src = live ? s_nbr[it.kc * BM + m] : -1;
-        const T* pa = src >= 0 ? din + (int64_t)src * cin_p + it.sub * KC +
-                                     cv * VEC
-                               : zvec;
-        ra[q] = *(const uint4*)pa;
+        const int cv = v - (v / VPR) * VPR;
+        const T* row = live ? arow[q] : nullptr;
+        ra[q] = *(const uint4*)(row ? row + it.sub * KC + cv * VEC : zvec);
       }
 #pragma unroll
       for (int q = 0; q < BV; ++q) {
