@@ -1048,8 +1048,22 @@ __device__ __forceinline__ float store4(T* p, const float* f) {
 // order from LDS -- P_t = P_{t-1} + update, emit f(P_t) - f(P_{t-1}) -- and
 // store the state once.  Row maxima are merged in LDS (s_rmax, one LDS
 // atomic per thread and row, no cross-lane reduction in the frame loop)
-// and then with one device atomic per row and column tile.
-template <typename T, int CPT, bool POOL>
+// and then with one device atomic per row and column tile.  With an
+// active WriteCs, Cs is written by write_cs() once the loads are issued
+// (the accumulators go to LDS while the states and residual rows are on
+// their way), followed by a barrier.
+struct NoCs {
+  static constexpr bool kActive = false;
+  __device__ void operator()() const {}
+};
+template <class F>
+struct ActiveCs {
+  static constexpr bool kActive = true;
+  F& f;
+  __device__ void operator()() const { f(); }
+};
+
+template <typename T, int CPT, bool POOL, class WriteCs>
 __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
                                                 int cld, const int* s_run,
                                                 int nruns, int64_t m0,
@@ -1057,7 +1071,8 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
                                                 const int* s_site,
                                                 const int* s_rsk,
                                                 unsigned* s_rmax,
-                                                const int* s_frm) {
+                                                const int* s_frm,
+                                                WriteCs write_cs) {
   constexpr int TPR = 64 / CPT, Q = CPT / 4;
   const int tid = threadIdx.x;
   const int cout_p = a.cout_p;
@@ -1095,6 +1110,10 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
             (rsk >= 0 && c < cout_p)
                 ? ((const uint4*)(dskip + (int64_t)rsk * cout_p + c))[v]
                 : make_uint4(0u, 0u, 0u, 0u);
+    }
+    if constexpr (WriteCs::kActive) {
+      write_cs();
+      __syncthreads();
     }
     if (rsk >= 0) {
 #pragma unroll
@@ -1189,7 +1208,7 @@ __device__ __forceinline__ void chunk_tile_runs(const ConvArgs& a, float* Cs,
 // maxima.  Every thread of the block must call it.  POOL (a max-pooled
 // layer, kModeChunkPool): s_frm holds the rows' frames, and the states
 // after each frame go to the rows' update rows instead of deltas.
-template <typename T, bool POOL = false>
+template <typename T, bool POOL = false, class WriteCs = NoCs>
 __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
                                                   float* Cs, int cld,
                                                   int* s_run, int64_t m0,
@@ -1199,7 +1218,8 @@ __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
                                                   unsigned* s_rmax,
                                                   const int* s_frm,
                                                   bool first = true,
-                                                  bool last = true) {
+                                                  bool last = true,
+                                                  WriteCs write_cs = {}) {
   constexpr int BM = kGemmBM;
   const int tid = threadIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -1223,14 +1243,14 @@ __device__ __forceinline__ void finish_chunk_tile(const ConvArgs& a,
   __syncthreads();
   const int nruns = s_run[BM + 1];
   if (nruns > 32)
-    chunk_tile_runs<T, 16, POOL>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
-                           s_rsk, s_rmax, s_frm);
+    chunk_tile_runs<T, 16, POOL>(a, Cs, cld, s_run, nruns, m0, rows, n0,
+                                 s_site, s_rsk, s_rmax, s_frm, write_cs);
   else if (nruns > 16)
-    chunk_tile_runs<T, 8, POOL>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
-                          s_rsk, s_rmax, s_frm);
+    chunk_tile_runs<T, 8, POOL>(a, Cs, cld, s_run, nruns, m0, rows, n0,
+                                s_site, s_rsk, s_rmax, s_frm, write_cs);
   else
-    chunk_tile_runs<T, 4, POOL>(a, Cs, cld, s_run, nruns, m0, rows, n0, s_site,
-                          s_rsk, s_rmax, s_frm);
+    chunk_tile_runs<T, 4, POOL>(a, Cs, cld, s_run, nruns, m0, rows, n0,
+                                s_site, s_rsk, s_rmax, s_frm, write_cs);
   if (last) {
     __syncthreads();
     if (tid < rows && s_rmax[tid])
@@ -1639,10 +1659,7 @@ void k_conv_gemm(ConvArgs a) {
     // 16-byte delta stores.  MFMA 16x16 block layout: D[row = 4*lg + r]
     // [col = l16]; the four waves' 32x32 sub-tiles make the 64x64 tile.
     if (CHUNK && (tid & 3) == 0) s_rsk[em] = rsk;
-    float rm_all = 0.f;
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      __syncthreads();  // the staged tiles are read
+    auto write_acc = [&]() {
 #pragma unroll
       for (int i = 0; i < IM; ++i)
 #pragma unroll
@@ -1651,6 +1668,21 @@ void k_conv_gemm(ConvArgs a) {
           for (int r = 0; r < 4; ++r)
             Cs[(wm * G::WM + i * 16 + 4 * lg + r) * CLD + wn * G::WN +
                j * 16 + l16] = acc[i][j][r];
+    };
+    if constexpr (CHUNK && NQ == 1) {
+      // the run listing's barrier also ends the reduction's LDS reads;
+      // the accumulators go to LDS while the states and residual rows
+      // are requested
+      finish_chunk_tile<T, POOL>(a, Cs, CLD, s_run, m0, (int)(m1 - m0), n0,
+                                 s_site, s_rsk, s_rmax, s_frm, true, true,
+                                 ActiveCs<decltype(write_acc)>{write_acc});
+      continue;
+    }
+    float rm_all = 0.f;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      __syncthreads();  // the staged tiles are read
+      write_acc();
       __syncthreads();
       const int nq = n0 + q * kGemmBN;
       const float* crow = Cs + em * CLD + ec;
