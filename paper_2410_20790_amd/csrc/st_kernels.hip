@@ -1302,7 +1302,9 @@ void k_conv_gemm(ConvArgs a) {
   constexpr size_t C_BYTES = (size_t)BM * CLD * sizeof(float);
   static_assert(AV >= 1 && BV >= 1, "stage vectors");
   __shared__ __align__(16) char smem[AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES];
-  __shared__ u64 s_kmask;
+  // the units' kernel-offset masks, two in turn: a unit clears the one
+  // the next unit fills, so no barrier orders the clearing
+  __shared__ u64 s_kmask[2];
   __shared__ int s_site[BM], s_rsk[BM], s_run[BM + 2], s_frm[POOL ? BM : 1];
   __shared__ unsigned s_rmax[BM];
   // dense pass: window origin of each row of the tile (n * Hi, oy * sh - ph,
@@ -1367,7 +1369,9 @@ void k_conv_gemm(ConvArgs a) {
     nb_lo = a.tstart[tm];
     nb_hi = a.tstart[tm + 1];
   }
-  for (int u = u_first; u < u_end; u += per_xcd) {
+  if (tid == 0) s_kmask[0] = 0ull;
+  int kp = 0;  // this unit's offset mask
+  for (int u = u_first; u < u_end; u += per_xcd, kp ^= 1) {
     // this unit's split and tile, and its reduction stages [st_lo, st_hi)
     const int sp = SPLIT ? (int)((unsigned)u / (unsigned)ntiles) : 0;
     const int t = SPLIT ? u - sp * (int)ntiles : u;
@@ -1383,7 +1387,7 @@ void k_conv_gemm(ConvArgs a) {
     const int n0 = (t - tm_i * tiles_n) * BN;
 
     __syncthreads();  // previous tile's LDS reads are complete
-    if (tid == 0) s_kmask = 0ull;
+    if (tid == 0) s_kmask[kp ^ 1] = 0ull;
     // this thread's epilogue row; its old state and residual are fetched
     // now so that they arrive while the reduction runs
     const int64_t eo = m0 + em;
@@ -1400,7 +1404,7 @@ void k_conv_gemm(ConvArgs a) {
       s_dorg[BM + tid] = (int)oy * a.g.sh - a.g.ph;
       s_dorg[2 * BM + tid] = (int)ox * a.g.sw - a.g.pw;
     }
-    __syncthreads();
+    if (REF) __syncthreads();  // the window origins are written
     u64 my = 0ull;
     for (int e = tid; e < BM * K; e += 256) {
       const int k = e / BM, m = e - (e / BM) * BM;
@@ -1420,9 +1424,9 @@ void k_conv_gemm(ConvArgs a) {
       s_nbr[e] = src;
       if (src >= 0) my |= 1ull << k;
     }
-    if (my) atomicOr(&s_kmask, my);
+    if (my) atomicOr(&s_kmask[kp], my);
     __syncthreads();
-    const u64 kmask = s_kmask;
+    const u64 kmask = s_kmask[kp];
     if (CHUNK && u + per_xcd < u_end) {
       const int tm = (int)((unsigned)(u + per_xcd) / (unsigned)tiles_n);
       nb_lo = a.tstart[tm];
@@ -1837,7 +1841,9 @@ void k_conv_gemm_big(ConvArgs a) {
   constexpr size_t AB_BYTES = 2ull * (BM + BN) * KC * sizeof(T);
   constexpr size_t C_BYTES = (size_t)BM * CLD * sizeof(float);
   __shared__ __align__(16) char smem[AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES];
-  __shared__ u64 s_kmask;
+  // the units' kernel-offset masks, two in turn: a unit clears the one
+  // the next unit fills, so no barrier orders the clearing
+  __shared__ u64 s_kmask[2];
   __shared__ int s_site[BM], s_rsk[BM], s_run[2][HM + 2];
   __shared__ unsigned s_rmax[2][HM];
   extern __shared__ int s_nbr[];          // [K][BM]
@@ -1880,7 +1886,9 @@ void k_conv_gemm_big(ConvArgs a) {
   const int u_first = xcd * chunk + blockIdx.x / kXcd;
   if (u_first < u_end) fetch_bounds(u_first);
 
-  for (int u = u_first; u < u_end; u += per_xcd) {
+  if (tid == 0) s_kmask[0] = 0ull;
+  int kp = 0;  // this unit's offset mask
+  for (int u = u_first; u < u_end; u += per_xcd, kp ^= 1) {
     const int tm = (int)((unsigned)u / (unsigned)tiles_n);
     const int n0 = (u - tm * tiles_n) * BN;
     // the tile's rows: halves [m0, mh) and [mh, m1)
@@ -1892,13 +1900,12 @@ void k_conv_gemm_big(ConvArgs a) {
         (int64_t)(unsigned)__builtin_amdgcn_readfirstlane((int)nb2);
 
     __syncthreads();  // the previous unit's LDS reads are complete
-    if (tid == 0) s_kmask = 0ull;
+    if (tid == 0) s_kmask[kp ^ 1] = 0ull;
     // this thread's epilogue row in each half and its pixel
     const int64_t eo0 = m0 + em, eo1 = mh + em;
     const bool eok0 = eo0 < mh, eok1 = eo1 < m1;
     const int epix0 = eok0 ? a.O[eo0] : 0;
     const int epix1 = eok1 ? a.O[eo1] : 0;
-    __syncthreads();
     u64 my = 0ull;
     for (int e = tid; e < BM * K; e += 256) {
       const int k = e / BM, m = e - (e / BM) * BM;
@@ -1907,9 +1914,9 @@ void k_conv_gemm_big(ConvArgs a) {
       s_nbr[e] = src;
       if (src >= 0) my |= 1ull << k;
     }
-    if (my) atomicOr(&s_kmask, my);
+    if (my) atomicOr(&s_kmask[kp], my);
     __syncthreads();
-    const u64 kmask = s_kmask;
+    const u64 kmask = s_kmask[kp];
     if (u + per_xcd < u_end) fetch_bounds(u + per_xcd);
 
     auto next_k = [&](int k) __attribute__((always_inline)) {
