@@ -13,6 +13,9 @@
 #include "st_internal.h"
 #include "st_kernels.h"
 
+static_assert(st::kSplitMax <= st::kEpiSplits,
+              "the split epilogue holds every split");
+
 namespace st {
 
 struct Recorder {

@@ -145,6 +145,9 @@ void launch_run_tiles(const Prof& pf, hipStream_t s, const int* O,
                       uint32_t* tstart);
 
 // ---- (c)+(d) delta convolution with the fused state update / emission
+// Most splits of one reduction (the split epilogue requests them all at
+// once).
+constexpr int kEpiSplits = 8;
 struct ConvArgs {
   int p16;             // state stored as bf16 (P points to bf16 values)
   const void* din;     // input delta rows [*, cin_p]
@@ -169,7 +172,8 @@ struct ConvArgs {
   const void* zero;    // 16 zero bytes (16-byte aligned)
   // split reduction: up to split_max splits of the reduction stages per
   // output tile (chosen per frame from the tile count), their f32 partial
-  // tiles in part [split][capO][cout_p]; split_max = 1: no split
+  // tiles in part [split][capO][cout_p]; split_max = 1: no split;
+  // split_max <= kEpiSplits
   float* part;
   int split_max;
   // residual carry: the consumers' view of the emitted tensor ([grid]

@@ -1663,6 +1663,19 @@ void k_conv_gemm(ConvArgs a) {
     // 16-byte delta stores.  MFMA 16x16 block layout: D[row = 4*lg + r]
     // [col = l16]; the four waves' 32x32 sub-tiles make the 64x64 tile.
     if (CHUNK && (tid & 3) == 0) s_rsk[em] = rsk;
+    // (reference pass, half storage) the residual row's 16 columns of this
+    // thread are requested before the accumulators go through LDS, so that
+    // they arrive meanwhile; a missing row reads as +0, which adds exactly
+    // what the zero residual adds
+    constexpr bool kSkPre = REF && !SPLIT && !CHUNK && sizeof(T) == 2;
+    uint4 skr[kSkPre ? 2 : 1] = {};
+    if constexpr (kSkPre) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        if (rsk >= 0 && n0 + ec + 8 * h < cout_p)
+          skr[h] = *(const uint4*)(dskip + (int64_t)rsk * cout_p + n0 + ec +
+                                   8 * h);
+    }
     auto write_acc = [&]() {
 #pragma unroll
       for (int i = 0; i < IM; ++i)
@@ -1720,7 +1733,11 @@ void k_conv_gemm(ConvArgs a) {
           }
         };
         auto load_sk = [&](int h, float* sk) {
-          if (rsk >= 0) {
+          if constexpr (kSkPre) {
+            const T* hp = (const T*)&skr[h];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) sk[e] = to_f(hp[e]);
+          } else if (rsk >= 0) {
             Vec8<T>::load(dskip + (int64_t)rsk * cout_p + nq + ec + 8 * h,
                           sk);
           } else {
@@ -1779,15 +1796,37 @@ __global__ __launch_bounds__(256) void k_split_epi(ConvArgs a) {
         Vec8<T>::load(dskip + (int64_t)rsk * cout_p + n0 + ec + 8 * h, sk[h]);
     const float* prow = a.part + eo * cout_p + n0 + ec;
     const int64_t pstride = a.capO * cout_p;
+    // every split's partial row is requested before any is summed (one
+    // round trip instead of one per split); the sum is in split order
+    float4 q[kEpiSplits][2][2];
+#pragma unroll
+    for (int sp = 0; sp < kEpiSplits; ++sp) {
+      if (sp >= S) break;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float* pp = prow + sp * pstride + 8 * h;
+        q[sp][h][0] = hv[h] ? *(const float4*)pp : make_float4(0, 0, 0, 0);
+        q[sp][h][1] =
+            hv[h] ? *(const float4*)(pp + 4) : make_float4(0, 0, 0, 0);
+      }
+    }
+    float vs[2][8];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) vs[h][e] = 0.f;
+#pragma unroll
+      for (int sp = 0; sp < kEpiSplits; ++sp) {
+        if (sp >= S) break;
+        const float4 lo = q[sp][h][0], hi = q[sp][h][1];
+        vs[h][0] += lo.x; vs[h][1] += lo.y; vs[h][2] += lo.z;
+        vs[h][3] += lo.w; vs[h][4] += hi.x; vs[h][5] += hi.y;
+        vs[h][6] += hi.z; vs[h][7] += hi.w;
+      }
+    }
     auto load_v = [&](int h, float* v) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = 0.f;
-      for (int sp = 0; sp < S; ++sp) {
-        float q[8];
-        load8f(prow + sp * pstride + 8 * h, q);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] += q[e];
-      }
+      for (int e = 0; e < 8; ++e) v[e] = vs[h][e];
     };
     auto load_po = [&](int h, float* o) {
 #pragma unroll
